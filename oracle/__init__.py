@@ -1,0 +1,11 @@
+"""fp64 CPU oracle for Forgetting Attention.
+
+TEST INFRASTRUCTURE ONLY: imported by the test suite, the smoke check and the
+benchmark's CPU-baseline leg, never by the product path.  It shares no code
+with the HIP library.
+"""
+from .fox_oracle import (  # noqa: F401
+    log_sigmoid, prefix_c, gate_prefix, decay_matrix,
+    forward_head_from_c, backward_head_from_c, reverse_cumsum,
+    forward_from_logf, forward, backward_from_logf, backward, decode,
+)

@@ -1,0 +1,210 @@
+"""Forgetting Attention -- plain fp64 CPU oracle.
+
+TEST INFRASTRUCTURE ONLY.  Nothing on the product path may import, call or
+execute this module: only the test suite, the smoke check and the CPU-baseline
+leg of the benchmark use it.  It shares no code with the HIP library.
+
+Everything is computed in float64 on the host with torch CPU ops, fully
+materialising the L x L decay matrix D, the logit matrix S and the attention
+matrix A for each (batch, head) slice, exactly as the method is defined in the
+paper (Forgetting Transformer, arXiv 2503.02130):
+
+  * forget gate                f_t = sigmoid(logit_t), one scalar per head and
+                               time step                      (Sec. 3, gate def.)
+  * prefix vector              c_i = sum_{l<=i} log f_l       (Sec. 3, "Hardware-
+                                                               aware implementation")
+  * decay matrix               D_ij = sum_{l=j+1}^{i} log f_l = c_i - c_j for
+                               j <= i, -inf above the diagonal (Eq. fot-weight,
+                                                               Eq. fot-matrix, log 0 = -inf)
+  * output                     O = softmax(s * Q K^T + D) V, the 1/sqrt(d)
+                               scale s multiplying q.k only   (Eq. fot-matrix and
+                                                               the footnote of Eq. attn-softmax)
+  * logsumexp                  LSE_i = m_i + log l_i, natural log (Alg. 1, epilogue)
+  * backward                   dV = A^T dO, dA = dO V^T, Delta_i = rowsum(dO o O),
+                               dS = A o (dA - Delta), dQ = s dS K, dK = s dS^T Q,
+                               dc = rowsum(dS) - colsum(dS)    (Alg. 2)
+  * d(log f)                   chain rule through c = cumsum(log f):
+                               d(log f)_l = sum_{i >= l} dc_i  (reverse cumsum)
+  * decode                     the forward's last row for a sequence whose last
+                               key/value is the new token, c_T = c_{T-1} +
+                               log sigmoid(x_new), c_0 = 0    (Eq. fot-weight at i = T)
+
+Readings of the paper this oracle takes (where it is silent or garbled):
+  * the scale multiplies q.k only; D is unscaled; dQ, dK carry s, dc does not;
+  * c is the inclusive prefix sum; O does not depend on log f_1;
+  * Alg. 1's rescale of O by diag(exp(m_old - m_new))^{-1} is read as a
+    multiplication by exp(m_old - m_new) (the FlashAttention-2 rescale); the
+    oracle needs no online softmax, so it simply uses the plain softmax;
+  * Alg. 2's rowsum(dO o O) "in R^d" is one value per row (R^N);
+  * Delta uses the exact O here (the oracle has no rounded O);
+  * decode: the query at position T attends to keys 1..T including itself.
+
+All functions accept any-dtype torch tensors (or numpy arrays) and return fp64
+torch tensors.  Every pin of this module lives in tests/test_oracle_*.py.
+"""
+from __future__ import annotations
+
+import math
+from typing import Optional, Sequence
+
+import torch
+
+F64 = torch.float64
+
+
+def _f64(x) -> torch.Tensor:
+    if not isinstance(x, torch.Tensor):
+        x = torch.as_tensor(x)
+    return x.detach().to(device="cpu", dtype=F64)
+
+
+# ---------------------------------------------------------------------------
+# Gate prelude (Sec. 3: f_t = sigmoid(w_f^T x_t + b_f); c_i = sum_{l<=i} log f_l)
+# ---------------------------------------------------------------------------
+def log_sigmoid(x) -> torch.Tensor:
+    """log sigmoid(x) = -log(1 + exp(-x)), written in the overflow-free form
+    min(x, 0) - log1p(exp(-|x|)).  The forget gate value is f = sigmoid(x)."""
+    x = _f64(x)
+    return torch.minimum(x, torch.zeros_like(x)) - torch.log1p(torch.exp(-x.abs()))
+
+
+def prefix_c(log_f) -> torch.Tensor:
+    """Inclusive prefix sum over the last (time) axis: c_i = sum_{l<=i} log f_l."""
+    return torch.cumsum(_f64(log_f), dim=-1)
+
+
+def gate_prefix(logit):
+    """Returns (log f, c) for gate logits of shape [..., L]."""
+    lf = log_sigmoid(logit)
+    return lf, prefix_c(lf)
+
+
+# ---------------------------------------------------------------------------
+# One (batch, head) slice, materialised
+# ---------------------------------------------------------------------------
+def decay_matrix(c: torch.Tensor, rows: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """D_ij = c_i - c_j for j <= i, -inf for j > i (Eq. fot-weight / fot-matrix).
+
+    `rows` selects query rows (0-based); by default all L rows."""
+    c = _f64(c)
+    L = c.shape[-1]
+    r = torch.arange(L) if rows is None else torch.as_tensor(rows, dtype=torch.long)
+    D = c[r][:, None] - c[None, :]
+    above = torch.arange(L)[None, :] > r[:, None]
+    return D.masked_fill(above, -math.inf)
+
+
+def forward_head_from_c(q, k, v, c, scale: float, rows=None, return_A: bool = False):
+    """O, LSE for one head given c.  q, k, v: [L, d]; c: [L].
+
+    S = s * Q K^T + D;  A = softmax_row(S);  O = A V;  LSE = m + log sum exp(S - m).
+    Rows are independent, so `rows` evaluates only the selected query rows."""
+    q, k, v, c = _f64(q), _f64(k), _f64(v), _f64(c)
+    r = torch.arange(q.shape[0]) if rows is None else torch.as_tensor(rows, dtype=torch.long)
+    S = scale * (q[r] @ k.T) + decay_matrix(c, r)
+    m = S.max(dim=1, keepdim=True).values
+    E = torch.exp(S - m)
+    l = E.sum(dim=1, keepdim=True)
+    A = E / l
+    O = A @ v
+    LSE = (m + torch.log(l)).squeeze(1)
+    if return_A:
+        return O, LSE, A
+    return O, LSE
+
+
+def backward_head_from_c(q, k, v, c, dO, scale: float, return_dS: bool = False):
+    """Gradients of sum(O * dO) for one head, by Alg. 2's formulas on full matrices.
+
+    Returns dQ, dK, dV [L, d] and dc [L] (= dc^q + dc^k, Alg. 2's last steps)."""
+    q, k, v, c, dO = _f64(q), _f64(k), _f64(v), _f64(c), _f64(dO)
+    O, _, A = forward_head_from_c(q, k, v, c, scale, return_A=True)
+    dV = A.T @ dO
+    dA = dO @ v.T
+    delta = (dO * O).sum(dim=1, keepdim=True)          # rowsum(dO o O), one per row
+    dS = A * (dA - delta)                               # masked entries: A = 0 there
+    dQ = scale * (dS @ k)
+    dK = scale * (dS.T @ q)
+    dc_q = dS.sum(dim=1)                                # += rowsum(dS)
+    dc_k = -dS.sum(dim=0)                               # -= colsum(dS)
+    dc = dc_q + dc_k
+    if return_dS:
+        return dQ, dK, dV, dc, dS
+    return dQ, dK, dV, dc
+
+
+def reverse_cumsum(x) -> torch.Tensor:
+    """y_l = sum_{i >= l} x_i over the last axis (chain rule through a cumsum)."""
+    x = _f64(x)
+    return torch.flip(torch.cumsum(torch.flip(x, dims=[-1]), dim=-1), dims=[-1])
+
+
+# ---------------------------------------------------------------------------
+# Batched entry points: q, k, v, dO [B, H, L, d]; logit / log f [B, H, L]
+# ---------------------------------------------------------------------------
+def _heads(B: int, H: int, heads: Optional[Sequence] = None):
+    if heads is None:
+        return [(b, h) for b in range(B) for h in range(H)]
+    return list(heads)
+
+
+def forward_from_logf(q, k, v, log_f, scale: float, heads=None, rows=None):
+    """Forward with log f given directly.  Returns O [B,H,L',d], LSE [B,H,L'] in
+    fp64, with L' = len(rows) when rows are selected; heads not in `heads` are NaN."""
+    B, H, L, d = q.shape
+    c = prefix_c(log_f)
+    nr = L if rows is None else len(rows)
+    O = torch.full((B, H, nr, d), math.nan, dtype=F64)
+    LSE = torch.full((B, H, nr), math.nan, dtype=F64)
+    for b, h in _heads(B, H, heads):
+        O[b, h], LSE[b, h] = forward_head_from_c(q[b, h], k[b, h], v[b, h], c[b, h], scale, rows)
+    return O, LSE
+
+
+def forward(q, k, v, logit, scale: float, heads=None, rows=None):
+    """O, LSE for gate logits (the operator's real input)."""
+    return forward_from_logf(q, k, v, log_sigmoid(logit), scale, heads, rows)
+
+
+def backward_from_logf(q, k, v, log_f, dO, scale: float, heads=None):
+    """dQ, dK, dV [B,H,L,d] and d(log f) [B,H,L], fp64 (NaN outside `heads`)."""
+    B, H, L, d = q.shape
+    c = prefix_c(log_f)
+    dQ = torch.full((B, H, L, d), math.nan, dtype=F64)
+    dK = dQ.clone()
+    dV = dQ.clone()
+    dlogf = torch.full((B, H, L), math.nan, dtype=F64)
+    for b, h in _heads(B, H, heads):
+        gq, gk, gv, dc = backward_head_from_c(q[b, h], k[b, h], v[b, h], c[b, h], dO[b, h], scale)
+        dQ[b, h], dK[b, h], dV[b, h] = gq, gk, gv
+        dlogf[b, h] = reverse_cumsum(dc)
+    return dQ, dK, dV, dlogf
+
+
+def backward(q, k, v, logit, dO, scale: float, heads=None):
+    return backward_from_logf(q, k, v, log_sigmoid(logit), dO, scale, heads)
+
+
+def decode(q, k_cache, v_cache, cached_logit, logit_new, scale: float, heads=None):
+    """One decode step (Eq. fot-weight at i = T).
+
+    q [B,H,d]; k_cache, v_cache [B,H,T,d] whose slot T-1 holds the new token;
+    cached_logit [B,H,T-1] are the gate logits of tokens 1..T-1 (c_1..c_{T-1});
+    logit_new [B,H] is the new token's gate logit, so c_T = c_{T-1} +
+    log sigmoid(logit_new), with c_0 = 0.  Returns o [B,H,d], lse [B,H], and
+    c_T [B,H] (the value the step appends to the prefix cache)."""
+    B, H, d = q.shape
+    T = k_cache.shape[2]
+    lf = torch.cat([log_sigmoid(cached_logit), log_sigmoid(logit_new)[..., None]], dim=-1)
+    assert lf.shape[-1] == T
+    c = prefix_c(lf)
+    o = torch.full((B, H, d), math.nan, dtype=F64)
+    lse = torch.full((B, H), math.nan, dtype=F64)
+    for b, h in _heads(B, H, heads):
+        kc, vc = _f64(k_cache[b, h]), _f64(v_cache[b, h])   # one slice at a time
+        s = scale * (kc @ _f64(q[b, h])) + (c[b, h, T - 1] - c[b, h])
+        m = s.max()
+        e = torch.exp(s - m)
+        o[b, h] = (e @ vc) / e.sum()
+        lse[b, h] = m + torch.log(e.sum())
+    return o, lse, c[..., T - 1]

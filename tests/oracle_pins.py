@@ -1,0 +1,330 @@
+"""Pins of the fp64 oracle against facts the paper and the mathematics fix.
+
+Every function takes the oracle module (`ora`) as an argument and raises
+AssertionError when a pin fails, so that the same pins can be run both on the
+real oracle (tests/test_oracle_pins.py) and on deliberately broken copies of it
+(tests/test_oracle_mutants.py), which shows that a plausible mistake anywhere
+in the oracle is caught by at least one pin.
+
+The pins, with what in the paper fixes them:
+  P1  log f = 0 turns Forgetting Attention into standard causal softmax
+      attention (Eq. attn-softmax vs Eq. fot-weight)  -> torch SDPA (fp64) and
+      its autograd gradients.
+  P2  log f -> -inf (here -1e4): every off-diagonal weight vanishes, so
+      o_i = v_i, LSE_i = s q_i.k_i, dQ = dK = 0, dV = dO.
+  P3  a constant, head-specific gate f = exp(-m) is ALiBi with slope m
+      (Sec. 3, "Connection to ALiBi") -> SDPA with the additive mask -m(i-j).
+  P4  D_ii = 0, D_ij = D_ik + D_kj, D <= 0, D monotone in j; c_i - c_j equals
+      the direct sum of log f over (j, i]  (Eq. fot-weight).
+  P5  attention rows are probability vectors with a zero upper triangle.
+  P6  first row: o_1 = v_1, LSE_1 = s q_1.k_1; L = 1 gives O = V.
+  P7  O is invariant to log f_1 and to c + const; d(log f)_1 = 0; sum dc = 0;
+      rowsum(dS) = 0 (softmax shift invariance).
+  P8  product form prod f_l exp(s q.k) (left side of Eq. fot-weight, gates as
+      sigmoid values) equals the logit-bias form (right side).
+  P9  gradients equal central finite differences and torch autograd of an
+      independently written forward.
+  P10 rectangle identity: d(log f)_l = sum_{r>=l} sum_{j<l} dS_rj, since log f_l
+      sits inside D_rj exactly when j < l <= r.
+  P11 decode equals the last row of the full forward.
+  P12 closed forms with q = 0: LSE_i = log i for log f = 0, and the geometric
+      series log((1 - e^{-m i}) / (1 - e^{-m})) for constant log f = -m.
+  P13 L = 2 written out by hand.
+"""
+from __future__ import annotations
+
+import math
+
+import torch
+import torch.nn.functional as Fnn
+
+F64 = torch.float64
+
+
+def _rand(shape, seed, scale=1.0):
+    g = torch.Generator().manual_seed(seed)
+    return torch.randn(shape, generator=g, dtype=F64) * scale
+
+
+def _close(a, b, tol, what):
+    a, b = torch.as_tensor(a, dtype=F64), torch.as_tensor(b, dtype=F64)
+    err = (a - b).abs().max().item() if a.numel() else 0.0
+    assert err <= tol, f"{what}: max-abs error {err:.3e} > {tol:.1e}"
+
+
+def _sdpa_with_grads(q, k, v, dO, scale, mask=None):
+    q, k, v = (t.clone().requires_grad_(True) for t in (q, k, v))
+    if mask is None:
+        O = Fnn.scaled_dot_product_attention(q, k, v, is_causal=True, scale=scale)
+    else:
+        O = Fnn.scaled_dot_product_attention(q, k, v, attn_mask=mask, scale=scale)
+    gq, gk, gv = torch.autograd.grad((O * dO).sum(), (q, k, v))
+    return O.detach(), gq, gk, gv
+
+
+# --------------------------------------------------------------------------- P1
+def pin_p1_zero_forgetting_is_softmax_attention(ora, B=2, H=3, L=37, d=16, seed=1):
+    q, k, v, dO = (_rand((B, H, L, d), seed + i) for i in range(4))
+    s = 1.0 / math.sqrt(d)
+    lf = torch.zeros(B, H, L, dtype=F64)
+    O, _ = ora.forward_from_logf(q, k, v, lf, s)
+    dQ, dK, dV, _ = ora.backward_from_logf(q, k, v, lf, dO, s)
+    Oref, gq, gk, gv = _sdpa_with_grads(q, k, v, dO, s)
+    _close(O, Oref, 1e-12, "P1 O")
+    _close(dQ, gq, 1e-12, "P1 dQ")
+    _close(dK, gk, 1e-12, "P1 dK")
+    _close(dV, gv, 1e-12, "P1 dV")
+
+
+# --------------------------------------------------------------------------- P2
+def pin_p2_full_forgetting(ora, B=1, H=2, L=19, d=8, seed=2):
+    q, k, v, dO = (_rand((B, H, L, d), seed + i) for i in range(4))
+    s = 0.37
+    lf = torch.full((B, H, L), -1.0e4, dtype=F64)
+    O, LSE = ora.forward_from_logf(q, k, v, lf, s)
+    _close(O, v, 1e-12, "P2 O = V")
+    _close(LSE, s * (q * k).sum(-1), 1e-12, "P2 LSE = s q.k")
+    dQ, dK, dV, dlf = ora.backward_from_logf(q, k, v, lf, dO, s)
+    _close(dQ, torch.zeros_like(dQ), 1e-12, "P2 dQ = 0")
+    _close(dK, torch.zeros_like(dK), 1e-12, "P2 dK = 0")
+    _close(dV, dO, 1e-12, "P2 dV = dO")
+    _close(dlf, torch.zeros_like(dlf), 1e-12, "P2 dlogf = 0")
+
+
+# --------------------------------------------------------------------------- P3
+def pin_p3_constant_gate_is_alibi(ora, B=1, H=4, L=29, d=8, seed=3):
+    q, k, v, dO = (_rand((B, H, L, d), seed + i) for i in range(4))
+    s = 1.0 / math.sqrt(d)
+    m = torch.tensor([0.05, 0.3, 1.0, 2.5], dtype=F64)[:H]
+    lf = (-m)[None, :, None].expand(B, H, L).clone()
+    i = torch.arange(L, dtype=F64)
+    dist = i[:, None] - i[None, :]
+    mask = -m[:, None, None] * dist[None]
+    mask = mask.masked_fill(dist[None] < 0, -math.inf)[None].expand(B, H, L, L)
+    O, _ = ora.forward_from_logf(q, k, v, lf, s)
+    dQ, dK, dV, _ = ora.backward_from_logf(q, k, v, lf, dO, s)
+    Oref, gq, gk, gv = _sdpa_with_grads(q, k, v, dO, s, mask)
+    _close(O, Oref, 1e-12, "P3 O")
+    _close(dQ, gq, 1e-12, "P3 dQ")
+    _close(dK, gk, 1e-12, "P3 dK")
+    _close(dV, gv, 1e-12, "P3 dV")
+
+
+# --------------------------------------------------------------------------- P4
+def pin_p4_decay_matrix(ora, L=23, seed=4):
+    x = _rand((L,), seed) * 2 + 1
+    lf = ora.log_sigmoid(x)
+    c = ora.prefix_c(lf)
+    D = ora.decay_matrix(c)
+    for i in range(L):
+        for j in range(L):
+            if j > i:
+                assert D[i, j] == -math.inf, "P4 upper triangle must be -inf"
+            else:
+                direct = sum(float(lf[l]) for l in range(j + 1, i + 1))
+                assert abs(D[i, j] - direct) <= 1e-12, f"P4 D[{i},{j}] != direct sum"
+    assert torch.all(torch.diagonal(D) == 0), "P4 D_ii = 0"
+    tri = torch.tril(torch.ones(L, L, dtype=torch.bool))
+    assert torch.all(D[tri] <= 0), "P4 D <= 0"
+    for i in range(L):       # monotone non-decreasing in j on the causal part
+        row = D[i, : i + 1]
+        assert torch.all(row[1:] >= row[:-1] - 1e-12), "P4 monotone in j"
+    for (i, kk, j) in [(20, 10, 3), (5, 5, 0), (22, 1, 1)]:
+        assert abs(D[i, j] - (D[i, kk] + D[kk, j])) < 1e-12, "P4 telescoping"
+    # the gate values themselves: log sigmoid(x) = log(1 / (1 + exp(-x)))
+    _close(lf, torch.log(1.0 / (1.0 + torch.exp(-x))), 1e-14, "P4 log sigmoid")
+    _close(ora.log_sigmoid(torch.tensor([0.0, -800.0, 800.0], dtype=F64)),
+           torch.tensor([-math.log(2.0), -800.0, 0.0], dtype=F64), 1e-14, "P4 log sigmoid limits")
+
+
+# --------------------------------------------------------------------------- P5
+def pin_p5_attention_rows(ora, L=31, d=8, seed=5):
+    q, k, v = (_rand((L, d), seed + i) for i in range(3))
+    c = ora.prefix_c(ora.log_sigmoid(_rand((L,), seed + 9)))
+    _, _, A = ora.forward_head_from_c(q, k, v, c, 0.5, return_A=True)
+    assert torch.all(A >= 0), "P5 A >= 0"
+    _close(A.sum(1), torch.ones(L, dtype=F64), 1e-13, "P5 rows sum to 1")
+    assert torch.all(torch.triu(A, 1) == 0), "P5 strict upper triangle is 0"
+
+
+# --------------------------------------------------------------------------- P6
+def pin_p6_first_row(ora, L=17, d=8, seed=6):
+    q, k, v = (_rand((1, 1, L, d), seed + i) for i in range(3))
+    x = _rand((1, 1, L), seed + 7)
+    s = 0.21
+    O, LSE = ora.forward(q, k, v, x, s)
+    _close(O[0, 0, 0], v[0, 0, 0], 1e-14, "P6 o_1 = v_1")
+    _close(LSE[0, 0, 0], s * (q[0, 0, 0] * k[0, 0, 0]).sum(), 1e-14, "P6 LSE_1")
+    O1, _ = ora.forward(q[:, :, :1], k[:, :, :1], v[:, :, :1], x[:, :, :1], s)
+    _close(O1, v[:, :, :1], 1e-14, "P6 L = 1")
+
+
+# --------------------------------------------------------------------------- P7
+def pin_p7_invariances(ora, B=1, H=2, L=27, d=8, seed=7):
+    q, k, v, dO = (_rand((B, H, L, d), seed + i) for i in range(4))
+    lf = ora.log_sigmoid(_rand((B, H, L), seed + 5) + 1)
+    s = 0.33
+    O, LSE = ora.forward_from_logf(q, k, v, lf, s)
+    lf2 = lf.clone()
+    lf2[..., 0] = -7.5
+    O2, LSE2 = ora.forward_from_logf(q, k, v, lf2, s)
+    _close(O, O2, 1e-13, "P7 O invariant to log f_1")
+    _close(LSE, LSE2, 1e-12, "P7 LSE invariant to log f_1")
+    c = ora.prefix_c(lf[0, 0])
+    Oa, La = ora.forward_head_from_c(q[0, 0], k[0, 0], v[0, 0], c, s)
+    Ob, Lb = ora.forward_head_from_c(q[0, 0], k[0, 0], v[0, 0], c + 123.25, s)
+    _close(Oa, Ob, 1e-12, "P7 O invariant to c + const")
+    _close(La, Lb, 1e-10, "P7 LSE invariant to c + const")
+    _, _, _, dlf = ora.backward_from_logf(q, k, v, lf, dO, s)
+    _close(dlf[..., 0], torch.zeros(B, H, dtype=F64), 1e-12, "P7 d(log f)_1 = 0")
+    _, _, _, dc, dS = ora.backward_head_from_c(q[0, 0], k[0, 0], v[0, 0], c, dO[0, 0], s,
+                                              return_dS=True)
+    _close(dc.sum(), 0.0, 1e-12, "P7 sum dc = 0")
+    _close(dS.sum(1), torch.zeros(L, dtype=F64), 1e-12, "P7 rowsum dS = 0")
+
+
+# --------------------------------------------------------------------------- P8
+def pin_p8_product_form(ora, L=12, d=4, seed=8):
+    q, k, v = (_rand((L, d), seed + i) for i in range(3))
+    x = _rand((L,), seed + 3) * 1.5 + 0.5
+    s = 0.6
+    f = [1.0 / (1.0 + math.exp(-float(t))) for t in x]          # sigmoid gate values
+    O_ref = torch.zeros(L, d, dtype=F64)
+    for i in range(L):
+        num = torch.zeros(d, dtype=F64)
+        den = 0.0
+        for j in range(i + 1):
+            F = 1.0
+            for l in range(j + 1, i + 1):
+                F *= f[l]
+            w = F * math.exp(s * float(q[i] @ k[j]))
+            num += w * v[j]
+            den += w
+        O_ref[i] = num / den
+    O, _ = ora.forward(q[None, None], k[None, None], v[None, None], x[None, None], s)
+    _close(O[0, 0], O_ref, 1e-12, "P8 product form = logit-bias form")
+
+
+# --------------------------------------------------------------------------- P9
+def _objective(ora, q, k, v, lf, dO, s):
+    O, _ = ora.forward_from_logf(q, k, v, lf, s)
+    return float((O * dO).sum())
+
+
+def pin_p9_finite_differences(ora, B=1, H=2, L=6, d=3, seed=9):
+    q, k, v, dO = (_rand((B, H, L, d), seed + i) for i in range(4))
+    lf = ora.log_sigmoid(_rand((B, H, L), seed + 5) + 0.5)
+    s = 0.7
+    dQ, dK, dV, dlf = ora.backward_from_logf(q, k, v, lf, dO, s)
+    eps = 1e-6
+    for name, t, g in (("dQ", q, dQ), ("dK", k, dK), ("dV", v, dV), ("dlogf", lf, dlf)):
+        flat = t.view(-1)
+        gflat = g.reshape(-1)
+        for idx in range(flat.numel()):
+            old = float(flat[idx])
+            flat[idx] = old + eps
+            fp = _objective(ora, q, k, v, lf, dO, s)
+            flat[idx] = old - eps
+            fm = _objective(ora, q, k, v, lf, dO, s)
+            flat[idx] = old
+            fd = (fp - fm) / (2 * eps)
+            assert abs(fd - float(gflat[idx])) <= 1e-7 * max(1.0, abs(fd)), \
+                f"P9 {name}[{idx}]: finite difference {fd:.9f} vs oracle {float(gflat[idx]):.9f}"
+
+
+def _autograd_forward(q, k, v, lf, s):
+    """An independent autograd construction of the forward (matrix form)."""
+    L = q.shape[-2]
+    c = torch.cumsum(lf, dim=-1)
+    D = c[..., :, None] - c[..., None, :]
+    upper = torch.ones(L, L, dtype=torch.bool).triu(1)
+    S = s * torch.matmul(q, k.transpose(-1, -2)) + D.masked_fill(upper, -math.inf)
+    return torch.matmul(torch.softmax(S, dim=-1), v)
+
+
+def pin_p9_autograd(ora, B=2, H=2, L=33, d=8, seed=19):
+    q, k, v, dO = (_rand((B, H, L, d), seed + i) for i in range(4))
+    lf = ora.log_sigmoid(_rand((B, H, L), seed + 5) * 2 + 1)
+    s = 0.35
+    leaves = [t.clone().requires_grad_(True) for t in (q, k, v, lf)]
+    O = _autograd_forward(*leaves, s)
+    gq, gk, gv, glf = torch.autograd.grad((O * dO).sum(), leaves)
+    dQ, dK, dV, dlf = ora.backward_from_logf(q, k, v, lf, dO, s)
+    _close(dQ, gq, 1e-12, "P9 autograd dQ")
+    _close(dK, gk, 1e-12, "P9 autograd dK")
+    _close(dV, gv, 1e-12, "P9 autograd dV")
+    _close(dlf, glf, 1e-12, "P9 autograd dlogf")
+
+
+# --------------------------------------------------------------------------- P10
+def pin_p10_rectangle_identity(ora, L=21, d=6, seed=10):
+    q, k, v, dO = (_rand((L, d), seed + i) for i in range(4))
+    lf = ora.log_sigmoid(_rand((L,), seed + 5) + 1)
+    c = ora.prefix_c(lf)
+    _, _, _, dc, dS = ora.backward_head_from_c(q, k, v, c, dO, 0.4, return_dS=True)
+    dlf = ora.reverse_cumsum(dc)
+    rect = torch.tensor([float(dS[l:, :l].sum()) for l in range(L)], dtype=F64)
+    _close(dlf, rect, 1e-12, "P10 rectangle identity")
+
+
+# --------------------------------------------------------------------------- P11
+def pin_p11_decode_is_last_row(ora, B=2, H=2, T=40, d=8, seed=11):
+    q, k, v = (_rand((B, H, T, d), seed + i) for i in range(3))
+    x = _rand((B, H, T), seed + 4) + 2
+    s = 1.0 / math.sqrt(d)
+    O, LSE = ora.forward(q, k, v, x, s)
+    o, lse, cT = ora.decode(q[:, :, T - 1], k, v, x[..., : T - 1], x[..., T - 1], s)
+    _close(o, O[:, :, T - 1], 1e-12, "P11 decode o")
+    _close(lse, LSE[:, :, T - 1], 1e-12, "P11 decode lse")
+    _close(cT, ora.log_sigmoid(x).sum(-1), 1e-12, "P11 c_T")
+
+
+# --------------------------------------------------------------------------- P12
+def pin_p12_zero_query_closed_forms(ora, L=50, d=4, seed=12):
+    k, v = (_rand((1, 1, L, d), seed + i) for i in range(2))
+    q = torch.zeros(1, 1, L, d, dtype=F64)
+    i = torch.arange(1, L + 1, dtype=F64)
+    _, LSE = ora.forward_from_logf(q, k, v, torch.zeros(1, 1, L, dtype=F64), 0.5)
+    _close(LSE[0, 0], torch.log(i), 1e-13, "P12 LSE = log i")
+    m = 0.3
+    O, LSE = ora.forward_from_logf(q, k, v, torch.full((1, 1, L), -m, dtype=F64), 0.5)
+    geo = torch.log((1 - torch.exp(-m * i)) / (1 - math.exp(-m)))
+    _close(LSE[0, 0], geo, 1e-12, "P12 geometric LSE")
+    w = torch.exp(-m * (i[:, None] - i[None, :])).tril()       # F_ij = e^{-m(i-j)}
+    _close(O[0, 0], (w @ v[0, 0]) / w.sum(1, keepdim=True), 1e-12, "P12 O weights")
+
+
+# --------------------------------------------------------------------------- P13
+def pin_p13_two_tokens(ora):
+    q = torch.tensor([[[[0.5, -1.0], [2.0, 0.25]]]], dtype=F64)
+    k = torch.tensor([[[[1.0, 0.5], [-0.5, 1.5]]]], dtype=F64)
+    v = torch.tensor([[[[3.0, -2.0], [1.0, 4.0]]]], dtype=F64)
+    x = torch.tensor([[[0.7, -0.4]]], dtype=F64)
+    s = 0.8
+    O, LSE = ora.forward(q, k, v, x, s)
+    lf2 = -math.log1p(math.exp(0.4))                   # log sigmoid(-0.4)
+    a = s * (2.0 * 1.0 + 0.25 * 0.5) + lf2             # row 2, key 1: s q2.k1 + D_21
+    b = s * (2.0 * -0.5 + 0.25 * 1.5)                  # row 2, key 2: D_22 = 0
+    lse2 = math.log(math.exp(a) + math.exp(b))
+    o2 = (math.exp(a) * v[0, 0, 0] + math.exp(b) * v[0, 0, 1]) / (math.exp(a) + math.exp(b))
+    _close(LSE[0, 0, 0], s * (0.5 * 1.0 - 1.0 * 0.5), 1e-14, "P13 LSE_1")
+    _close(LSE[0, 0, 1], lse2, 1e-14, "P13 LSE_2")
+    _close(O[0, 0, 1], o2, 1e-14, "P13 o_2")
+
+
+ALL_PINS = [
+    pin_p1_zero_forgetting_is_softmax_attention,
+    pin_p2_full_forgetting,
+    pin_p3_constant_gate_is_alibi,
+    pin_p4_decay_matrix,
+    pin_p5_attention_rows,
+    pin_p6_first_row,
+    pin_p7_invariances,
+    pin_p8_product_form,
+    pin_p9_finite_differences,
+    pin_p9_autograd,
+    pin_p10_rectangle_identity,
+    pin_p11_decode_is_last_row,
+    pin_p12_zero_query_closed_forms,
+    pin_p13_two_tokens,
+]

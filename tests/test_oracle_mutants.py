@@ -1,0 +1,146 @@
+"""Plant plausible mistakes in copies of the oracle (on the CPU) and check that
+the pins catch every one of them."""
+import importlib.util
+import math
+import os
+
+import pytest
+import torch
+
+import oracle_pins
+
+ORACLE_FILE = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                           "oracle", "fox_oracle.py")
+
+
+def _fresh_oracle(tag):
+    spec = importlib.util.spec_from_file_location(f"fox_oracle_mutant_{tag}", ORACLE_FILE)
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
+def _m_scale_on_D(m):
+    """The 1/sqrt(d)-like factor applied to D as well as to q.k."""
+    orig = m.decay_matrix
+    m.decay_matrix = lambda c, rows=None: orig(m._f64(c) * 0.5, rows)
+
+
+def _m_exclusive_c(m):
+    m.prefix_c = lambda lf: torch.cumsum(m._f64(lf), -1) - m._f64(lf)
+
+
+def _m_no_mask(m):
+    def dm(c, rows=None):
+        c = m._f64(c)
+        L = c.shape[-1]
+        r = torch.arange(L) if rows is None else torch.as_tensor(rows)
+        return c[r][:, None] - c[None, :]
+    m.decay_matrix = dm
+
+
+def _m_flipped_D(m):
+    orig = m.decay_matrix
+    m.decay_matrix = lambda c, rows=None: orig(-m._f64(c), rows)
+
+
+def _m_logsigmoid_max(m):
+    m.log_sigmoid = lambda x: torch.maximum(m._f64(x), torch.zeros_like(m._f64(x))) - \
+        torch.log1p(torch.exp(-m._f64(x).abs()))
+
+
+def _patch_backward(m, variant):
+    def bwd(q, k, v, c, dO, scale, return_dS=False):
+        q, k, v, c, dO = (m._f64(t) for t in (q, k, v, c, dO))
+        O, _, A = m.forward_head_from_c(q, k, v, c, scale, return_A=True)
+        dV = A @ dO if variant == "dV_untransposed" else A.T @ dO
+        dA = dO @ v.T
+        delta = (dO * O).sum(1, keepdim=True)
+        if variant == "delta_from_dA":
+            delta = dA.sum(1, keepdim=True)
+        dS = A * (dA - delta)
+        dQ = scale * (dS @ k)
+        dK = scale * (dS @ q) if variant == "dK_untransposed" else scale * (dS.T @ q)
+        if variant == "dK_no_scale":
+            dK = dS.T @ q
+        dc = dS.sum(1) - dS.sum(0)
+        if variant == "dc_sign":
+            dc = -dc
+        if return_dS:
+            return dQ, dK, dV, dc, dS
+        return dQ, dK, dV, dc
+    m.backward_head_from_c = bwd
+
+
+def _m_forward_cumsum(m):
+    m.reverse_cumsum = lambda x: torch.cumsum(m._f64(x), -1)
+
+
+def _m_lse_no_max(m):
+    """LSE = log(l), forgetting to add back the row max m."""
+    def fwd(q, k, v, c, scale, rows=None, return_A=False):
+        q, k, v, c = (m._f64(t) for t in (q, k, v, c))
+        r = torch.arange(q.shape[0]) if rows is None else torch.as_tensor(rows)
+        S = scale * (q[r] @ k.T) + m.decay_matrix(c, r)
+        mx = S.max(1, keepdim=True).values
+        E = torch.exp(S - mx)
+        l = E.sum(1, keepdim=True)
+        A = E / l
+        LSE = torch.log(l).squeeze(1)
+        return (A @ v, LSE, A) if return_A else (A @ v, LSE)
+    m.forward_head_from_c = fwd
+
+
+def _m_decode_sign(m):
+    def dec(q, k_cache, v_cache, cached_logit, logit_new, scale, heads=None):
+        B, H, d = q.shape
+        T = k_cache.shape[2]
+        lf = torch.cat([m.log_sigmoid(cached_logit), m.log_sigmoid(logit_new)[..., None]], -1)
+        c = m.prefix_c(lf)
+        o = torch.zeros(B, H, d, dtype=torch.float64)
+        lse = torch.zeros(B, H, dtype=torch.float64)
+        for b in range(B):
+            for h in range(H):
+                s = scale * (m._f64(k_cache[b, h]) @ m._f64(q[b, h])) - (c[b, h, T - 1] - c[b, h])
+                e = torch.exp(s - s.max())
+                o[b, h] = (e @ m._f64(v_cache[b, h])) / e.sum()
+                lse[b, h] = s.max() + torch.log(e.sum())
+        return o, lse, c[..., T - 1]
+    m.decode = dec
+
+
+def _m_scale_twice(m):
+    orig = m.forward_head_from_c
+    m.forward_head_from_c = lambda q, k, v, c, scale, rows=None, return_A=False: \
+        orig(q, k, v, c, scale * scale, rows, return_A)
+
+
+MUTANTS = {
+    "decay_scaled": _m_scale_on_D,
+    "exclusive_prefix": _m_exclusive_c,
+    "no_causal_mask": _m_no_mask,
+    "decay_sign": _m_flipped_D,
+    "logsigmoid_max": _m_logsigmoid_max,
+    "dV_untransposed": lambda m: _patch_backward(m, "dV_untransposed"),
+    "dK_untransposed": lambda m: _patch_backward(m, "dK_untransposed"),
+    "dK_no_scale": lambda m: _patch_backward(m, "dK_no_scale"),
+    "delta_from_dA": lambda m: _patch_backward(m, "delta_from_dA"),
+    "dc_sign": lambda m: _patch_backward(m, "dc_sign"),
+    "forward_cumsum_for_dlogf": _m_forward_cumsum,
+    "lse_without_max": _m_lse_no_max,
+    "decode_bias_sign": _m_decode_sign,
+    "scale_squared": _m_scale_twice,
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name):
+    m = _fresh_oracle(name)
+    MUTANTS[name](m)
+    caught = []
+    for pin in oracle_pins.ALL_PINS:
+        try:
+            pin(m)
+        except (AssertionError, RuntimeError, ValueError, IndexError):
+            caught.append(pin.__name__)
+    assert caught, f"mutant {name} passes every pin"
