@@ -1,0 +1,243 @@
+"""Benchmark of the Forgetting Attention hot path on one MI355X.
+
+One step = the whole training-side path over one batch of the long-context
+workload (B=2, H=16, L=16384, d=128, bf16): gate prefix -> forward (O, LSE) ->
+backward (dQ, dK, dV, d(log f)).  Throughput counts the causal FLOPs of the
+algorithm: 4d per causal (i, j) pair in the forward (QK^T and PV) and 10d in the
+backward (QK^T recompute, dV, dP, dQ, dK), i.e. 14d per pair, the convention of
+the paper's FLOP table (attention costs 2 n_layer d_model L per token and
+direction of each product).  The decode step (B=64, H=16, T=32768, d=128) is
+measured in the same run and reported in HBM GB/s.
+
+Prints ONE JSON line.  Inputs are seeded synthetic tensors already resident in
+HBM when the timed region starts.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import paper_2503_02130_amd as fox  # noqa: E402
+from paper_2503_02130_amd import inputs  # noqa: E402
+
+MFMA_BF16_PEAK_TFLOPS = 2516.6   # MI355X dense bf16 (256 CU x 2.4 GHz x 4096 FLOP/clk)
+HBM_PEAK_GBS = 8000.0            # MI355X HBM3E
+
+
+def causal_pairs(B: int, H: int, L: int) -> int:
+    return B * H * L * (L + 1) // 2
+
+
+def fwd_flops(B, H, L, d) -> float:
+    return 4.0 * d * causal_pairs(B, H, L)
+
+
+def bwd_flops(B, H, L, d) -> float:
+    return 10.0 * d * causal_pairs(B, H, L)
+
+
+def decode_bytes(B, H, T, d, elem=2) -> float:
+    return float(B * H * T * (2 * d * elem + 4))
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+class EventTimer:
+    """Accumulates the duration of bracketed regions with HIP events on the
+    current stream (the stream every library call is enqueued on)."""
+
+    def __init__(self):
+        self.pairs = []
+
+    def __enter__(self):
+        self.a = torch.cuda.Event(enable_timing=True)
+        self.b = torch.cuda.Event(enable_timing=True)
+        self.a.record()
+        return self
+
+    def __exit__(self, *exc):
+        self.b.record()
+        self.pairs.append((self.a, self.b))
+
+    def mean_ms(self):
+        return sum(a.elapsed_time(b) for a, b in self.pairs) / max(1, len(self.pairs))
+
+
+def bench_train(w, steps, warmup):
+    dev = torch.device("cuda:0")
+    x = inputs.workload_inputs(w, device=dev)
+    s = fox.default_scale(w.d)
+    B, H, L, d = w.B, w.H, w.L, w.d
+    c = torch.empty((B, H, L), device=dev)
+    o = torch.empty_like(x["q"])
+    lse = torch.empty((B, H, L), device=dev)
+    dq, dk, dv = torch.empty_like(x["q"]), torch.empty_like(x["k"]), torch.empty_like(x["v"])
+    dlf = torch.empty_like(c)
+    ws = torch.empty(fox.fox_attn_bwd_workspace_bytes(x["q"].dtype, B, H, L, d), device=dev,
+                     dtype=torch.uint8)
+    t_gate, t_fwd, t_bwd = EventTimer(), EventTimer(), EventTimer()
+
+    def step(timed):
+        if timed:
+            with t_gate:
+                fox.fox_gate_prefix(x["logit"], c=c)
+            with t_fwd:
+                fox.fox_attn_fwd(x["q"], x["k"], x["v"], c, s, o=o, lse=lse)
+            with t_bwd:
+                fox.fox_attn_bwd(x["q"], x["k"], x["v"], c, o, lse, x["do"], s, dq=dq, dk=dk,
+                                 dv=dv, d_log_f=dlf, workspace=ws)
+        else:
+            fox.fox_gate_prefix(x["logit"], c=c)
+            fox.fox_attn_fwd(x["q"], x["k"], x["v"], c, s, o=o, lse=lse)
+            fox.fox_attn_bwd(x["q"], x["k"], x["v"], c, o, lse, x["do"], s, dq=dq, dk=dk, dv=dv,
+                             d_log_f=dlf, workspace=ws)
+
+    for _ in range(warmup):
+        step(False)
+    torch.cuda.synchronize()
+    log(f"[bench] {w.name}: warmup done")
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    start.record()
+    for _ in range(steps):
+        step(True)
+    end.record()
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t0) * 1e3 / steps
+    ms = start.elapsed_time(end) / steps
+    if not (torch.isfinite(o.float()).all() and torch.isfinite(dlf).all()):
+        raise RuntimeError("non-finite outputs")
+    return {"ms": ms, "wall_ms": wall_ms, "gate_ms": t_gate.mean_ms(), "fwd_ms": t_fwd.mean_ms(),
+            "bwd_ms": t_bwd.mean_ms()}
+
+
+def bench_decode(w, steps, warmup):
+    dev = torch.device("cuda:0")
+    y = inputs.workload_inputs(w, device=dev)
+    T = w.L
+    cc = torch.empty((w.B, w.H, T), device=dev)
+    cc[..., : T - 1] = fox.fox_gate_prefix(y["cached_logit"])
+    o = torch.empty_like(y["q"])
+    lse = torch.empty((w.B, w.H), device=dev)
+    ws = torch.empty(fox.fox_attn_decode_workspace_bytes(y["q"].dtype, w.B, w.H, T, w.d),
+                     device=dev, dtype=torch.uint8)
+    for _ in range(warmup):
+        fox.fox_attn_decode(y["q"], y["k_cache"], y["v_cache"], cc, y["logit_new"], o=o, lse=lse,
+                            workspace=ws)
+    torch.cuda.synchronize()
+    t = EventTimer()
+    for _ in range(steps):
+        with t:
+            fox.fox_attn_decode(y["q"], y["k_cache"], y["v_cache"], cc, y["logit_new"], o=o,
+                                lse=lse, workspace=ws)
+    torch.cuda.synchronize()
+    return {"ms": t.mean_ms()}
+
+
+def cpu_baseline(w, seconds_hint=20.0):
+    """The fp64 oracle, untouched, on a bounded sample: forward + backward of one
+    (batch, head) slice of the workload (1/(B*H) of the step's work)."""
+    import oracle
+    threads = len(os.sched_getaffinity(0))
+    torch.set_num_threads(threads)
+    x = inputs.attn_inputs(1, 1, w.L, w.d, w.dtype, w.gate, w.seed, device="cpu")
+    s = fox.default_scale(w.d)
+    t0 = time.perf_counter()
+    oracle.forward(x["q"], x["k"], x["v"], x["logit"], s)
+    oracle.backward(x["q"], x["k"], x["v"], x["logit"], x["do"], s)
+    dt = time.perf_counter() - t0
+    flops = fwd_flops(1, 1, w.L, w.d) + bwd_flops(1, 1, w.L, w.d)
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": torch.get_num_threads(),
+            "kind": "oracle",
+            "sample": f"fp64 forward+backward of 1 of {w.B * w.H} (batch, head) slices at "
+                      f"L={w.L}, d={w.d}: {dt:.1f} s; value scales that slice's causal FLOPs"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="fwdbwd_bf16_b2_h16_l16384_d128")
+    ap.add_argument("--decode-workload", default="decode_bf16_b64_h16_t32768_d128")
+    ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(Forgetting Attention shards over (batch, head) with no communication).",
+              file=sys.stderr)
+        sys.exit(2)
+    if not os.path.exists(fox.LIB_PATH):
+        from paper_2503_02130_amd import build
+        build.build()
+    fox.load()
+
+    w = inputs.WORKLOADS[args.workload]
+    r = bench_train(w, args.steps, args.warmup)
+    B, H, L, d = w.B, w.H, w.L, w.d
+    fl_f, fl_b = fwd_flops(B, H, L, d), bwd_flops(B, H, L, d)
+    tflops = (fl_f + fl_b) / (r["ms"] * 1e-3) / 1e12
+    fwd_tf = fl_f / (r["fwd_ms"] * 1e-3) / 1e12
+    bwd_tf = fl_b / (r["bwd_ms"] * 1e-3) / 1e12
+    out = {
+        "metric": "Forgetting-attn fwd+bwd TFLOP/s bf16 L=16k d=128 (% MFMA peak); decode GB/s",
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(r["ms"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": B, "H": H, "L": L, "d": d,
+                   "gate_logits": "per-head mean U[0,6], std 1", "causal": True,
+                   "flops_per_step": fl_f + fl_b, "parallelism": "none (1 GPU)"},
+        "frac_of_peak": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+        "breakdown_ms": {"gate_prefix": round(r["gate_ms"], 4), "fwd": round(r["fwd_ms"], 4),
+                         "bwd": round(r["bwd_ms"], 4), "wall_per_step": round(r["wall_ms"], 4)},
+        "roofline": {"bound": "mfma", "kernel": "fwd_bf16_kernel<128> (fox_attn_fwd)",
+                     "achieved": round(fwd_tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(fwd_tf / MFMA_BF16_PEAK_TFLOPS, 4),
+                     "traffic": None},
+        "roofline_bwd": {"bound": "mfma", "kernels": "fox_attn_bwd (delta, dkdv, dq, scan)",
+                         "achieved": round(bwd_tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
+                         "unit": "TFLOP/s", "frac": round(bwd_tf / MFMA_BF16_PEAK_TFLOPS, 4)},
+    }
+    log(f"[bench] train step {r['ms']:.3f} ms -> {tflops:.1f} TFLOP/s")
+    if not args.no_decode:
+        wd = inputs.WORKLOADS[args.decode_workload]
+        rd = bench_decode(wd, max(args.steps, 10), args.warmup)
+        byt = decode_bytes(wd.B, wd.H, wd.L, wd.d)
+        gbs = byt / (rd["ms"] * 1e-3) / 1e9
+        out["decode"] = {"metric": "decode HBM GB/s", "value": round(gbs, 1), "unit": "GB/s",
+                         "ms_per_step": round(rd["ms"], 4),
+                         "config": {"workload": wd.name, "B": wd.B, "H": wd.H, "T": wd.L,
+                                    "d": wd.d, "bytes_per_step": byt},
+                         "roofline": {"bound": "hbm", "kernel": "fox_attn_decode (split + combine)",
+                                      "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
+                                      "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                                      "traffic": None}}
+        log(f"[bench] decode {rd['ms']:.3f} ms -> {gbs:.0f} GB/s")
+    if not args.no_cpu_baseline:
+        log("[bench] timing the fp64 oracle on the host")
+        out["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

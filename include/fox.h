@@ -1,0 +1,141 @@
+/*
+ * fox.h -- C ABI of the Forgetting Attention library for AMD Instinct MI355X (gfx950).
+ *
+ * Forgetting Attention (Forgetting Transformer, arXiv 2503.02130, Sec. 3,
+ * Eq. fot-weight / fot-matrix) computes, for every (batch, head) slice,
+ *
+ *     o_i = sum_{j<=i} exp(s q_i.k_j + c_i - c_j) v_j / sum_{j<=i} exp(s q_i.k_j + c_i - c_j)
+ *
+ * with the forget gate f_t = sigmoid(logit_t), the prefix vector
+ * c_i = sum_{l<=i} log f_l (inclusive), and the scale s (the paper always
+ * scales q.k by 1/sqrt(d), footnote of Eq. attn-softmax; the scale multiplies
+ * q.k only, never c_i - c_j).
+ *
+ * Conventions shared by every entry point
+ *   - Layout: q, k, v, o, dO, dq, dk, dv are contiguous [B, H, L, d] (d innermost);
+ *     gate logits, log f, c, lse, d(log f) are contiguous [B, H, L] fp32.  The
+ *     decode cache is [B, H, T, d]; its prefix vector [B, H, T] fp32.
+ *   - dtype: FOX_DTYPE_BF16 (bf16 storage, fp32 accumulation, MFMA) or
+ *     FOX_DTYPE_F32 (fp32 storage and arithmetic).  Head dim d is 64 or 128.
+ *   - Pointers are device pointers owned by the caller; every device pointer
+ *     must be 16-byte aligned.  The library allocates no device memory and
+ *     keeps no state between calls; workspaces are caller-provided and their
+ *     contents are undefined on entry and exit.
+ *   - stream is a hipStream_t (NULL = the default stream).  Every call only
+ *     enqueues work on that stream and returns; the library never synchronises.
+ *     Calls on different streams are independent.
+ *   - Errors: arguments are validated on the host before anything is enqueued;
+ *     a failed validation returns a non-zero fox_status_t and launches nothing.
+ *     A failed kernel launch returns FOX_ERR_HIP.  Faults during execution
+ *     surface at the caller's next synchronisation.
+ *   - Causal only (the paper considers causal sequence modelling only, Sec. 2).
+ *   - Gate logits must be finite (then log f is finite and c_i - c_j is defined).
+ */
+#ifndef FOX_H_
+#define FOX_H_
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FOX_DTYPE_F32 = 0,
+  FOX_DTYPE_BF16 = 1
+} fox_dtype_t;
+
+typedef enum {
+  FOX_OK = 0,
+  FOX_ERR_NULL = 1,         /* a required pointer is NULL                         */
+  FOX_ERR_SHAPE = 2,        /* B, H, L (or T) not positive, or sizes overflow      */
+  FOX_ERR_UNSUPPORTED = 3,  /* unsupported dtype or head dim                       */
+  FOX_ERR_ALIGN = 4,        /* a pointer is not 16-byte aligned                    */
+  FOX_ERR_WORKSPACE = 5,    /* workspace missing or smaller than required          */
+  FOX_ERR_HIP = 6           /* the HIP runtime reported an error at launch         */
+} fox_status_t;
+
+/* Human-readable name of a status code.  Never returns NULL. */
+const char* fox_status_string(int status);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int fox_version(void);
+
+/*
+ * Gate prelude (Sec. 3: f_t = sigmoid(w_f^T x_t + b_f); "Hardware-aware
+ * implementation": c_i = sum_{l=1}^{i} log f_l, stored in HBM).
+ *
+ *   gate_logit [B,H,L] fp32 in   the pre-sigmoid gate logits x_t
+ *   log_f      [B,H,L] fp32 out  log f_t = log sigmoid(x_t); may be NULL
+ *   c          [B,H,L] fp32 out  inclusive prefix sum of log f along t
+ */
+int fox_gate_prefix(const float* gate_logit, float* log_f, float* c,
+                    int B, int H, int L, void* stream);
+
+/*
+ * Forward pass (Alg. 1 of the appendix "Hardware-aware implementation of
+ * Forgetting Attention": O = softmax(s Q K^T + D) V with D_ij = c_i - c_j for
+ * j <= i and -inf above the diagonal, plus the row logsumexp).
+ *
+ *   q, k, v [B,H,L,d] dtype in
+ *   c       [B,H,L]   fp32  in   prefix vector from fox_gate_prefix
+ *   o       [B,H,L,d] dtype out
+ *   lse     [B,H,L]   fp32  out  natural-log logsumexp of row i of s Q K^T + D
+ *   scale   the factor s on q.k (1/sqrt(d) in the paper)
+ */
+int fox_attn_fwd(int dtype, const void* q, const void* k, const void* v, const float* c,
+                 void* o, float* lse, int B, int H, int L, int d, float scale, void* stream);
+
+/* Bytes of workspace fox_attn_bwd needs for this shape (0 on invalid arguments). */
+size_t fox_attn_bwd_workspace_bytes(int dtype, int B, int H, int L, int d);
+
+/*
+ * Backward pass (Alg. 2 of the same appendix): the gradients of
+ * sum(O o dO) with respect to q, k, v and log f.  The paper returns
+ * dc = dc^q + dc^k (dc^q += rowsum(dS), dc^k -= colsum(dS)); this entry
+ * point carries the chain rule through c = cumsum(log f) one step further:
+ * d(log f)_l = sum_{i>=l} dc_i.
+ *
+ *   q, k, v, o, d_o  [B,H,L,d] dtype in  (o and lse from fox_attn_fwd)
+ *   c                [B,H,L]   fp32  in
+ *   lse              [B,H,L]   fp32  in
+ *   dq, dk, dv       [B,H,L,d] dtype out (fully overwritten)
+ *   d_log_f          [B,H,L]   fp32  out (fully overwritten)
+ *   workspace        device buffer of at least fox_attn_bwd_workspace_bytes()
+ */
+int fox_attn_bwd(int dtype, const void* q, const void* k, const void* v, const float* c,
+                 const void* o, const float* lse, const void* d_o,
+                 void* dq, void* dk, void* dv, float* d_log_f,
+                 void* workspace, size_t workspace_bytes,
+                 int B, int H, int L, int d, float scale, void* stream);
+
+/* Bytes of workspace fox_attn_decode needs for this shape (0 on invalid arguments). */
+size_t fox_attn_decode_workspace_bytes(int dtype, int B, int H, int T, int d);
+
+/*
+ * One decode step: Eq. fot-weight evaluated for the last position i = T of a
+ * sequence whose keys/values 1..T sit in a cache (the paper's outlook mentions
+ * KV caches, Sec. 6).  The new token attends to every cached key including
+ * itself.
+ *
+ *   q              [B,H,d]   dtype in   query of the new token
+ *   k_cache,v_cache[B,H,T,d] dtype in   slot T-1 already holds the new token's k, v
+ *   c_cache        [B,H,T]   fp32 in/out  entries 0..T-2 are read (c_1..c_{T-1});
+ *                                       entry T-1 is written with
+ *                                       c_T = c_{T-1} + log sigmoid(gate_logit_new)
+ *                                       (c_0 = 0 when T = 1) and never read
+ *   gate_logit_new [B,H]     fp32 in
+ *   o              [B,H,d]   dtype out
+ *   lse            [B,H]     fp32 out  natural-log logsumexp of the new row
+ *   workspace      device buffer of at least fox_attn_decode_workspace_bytes()
+ */
+int fox_attn_decode(int dtype, const void* q, const void* k_cache, const void* v_cache,
+                    float* c_cache, const float* gate_logit_new, void* o, float* lse,
+                    void* workspace, size_t workspace_bytes,
+                    int B, int H, int T, int d, float scale, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FOX_H_ */

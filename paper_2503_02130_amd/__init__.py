@@ -1,0 +1,18 @@
+"""Forgetting Attention (FoX, arXiv 2503.02130) for AMD Instinct MI355X.
+
+The operator runs entirely in hand-written HIP kernels for gfx950, reached
+through the C ABI declared in include/fox.h (libfox.so).  This package holds
+the ctypes binding (same entry-point names as the C ABI), the build script and
+the seeded input generators used by tests and benchmarks.
+"""
+from ._lib import (  # noqa: F401
+    FoxError, default_scale, load, status_string,
+    fox_gate_prefix, fox_attn_fwd, fox_attn_bwd, fox_attn_bwd_workspace_bytes,
+    fox_attn_decode, fox_attn_decode_workspace_bytes, LIB_PATH, EXPORTED,
+)
+
+__all__ = [
+    "FoxError", "default_scale", "load", "status_string",
+    "fox_gate_prefix", "fox_attn_fwd", "fox_attn_bwd", "fox_attn_bwd_workspace_bytes",
+    "fox_attn_decode", "fox_attn_decode_workspace_bytes",
+]

@@ -1,0 +1,223 @@
+"""ctypes binding of libfox.so: argument marshalling only.
+
+Every function here validates torch tensors (device, dtype, shape, contiguity),
+allocates missing outputs and workspaces with torch, and calls the C entry point
+of the same name on the current HIP stream.  All arithmetic runs in the HIP
+kernels; there is no host or PyTorch fallback: if the library is not built or
+cannot be loaded, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional, Tuple
+
+import torch  # imported before libfox.so so that both share torch's HIP runtime
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libfox.so")
+
+FOX_DTYPE_F32 = 0
+FOX_DTYPE_BF16 = 1
+_DT = {torch.float32: FOX_DTYPE_F32, torch.bfloat16: FOX_DTYPE_BF16}
+
+EXPORTED = (
+    "fox_status_string", "fox_version", "fox_gate_prefix", "fox_attn_fwd",
+    "fox_attn_bwd_workspace_bytes", "fox_attn_bwd", "fox_attn_decode_workspace_bytes",
+    "fox_attn_decode",
+)
+
+
+class FoxError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what} failed with status {status}: {status_string(status)}")
+
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load libfox.so (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(
+            f"{LIB_PATH} is missing: build it with `python -m paper_2503_02130_amd.build` "
+            "(the HIP library is required; there is no fallback)")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I, F, Z = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+    lib.fox_status_string.restype = ctypes.c_char_p
+    lib.fox_status_string.argtypes = [I]
+    lib.fox_version.restype = I
+    lib.fox_version.argtypes = []
+    lib.fox_gate_prefix.restype = I
+    lib.fox_gate_prefix.argtypes = [P, P, P, I, I, I, P]
+    lib.fox_attn_fwd.restype = I
+    lib.fox_attn_fwd.argtypes = [I, P, P, P, P, P, P, I, I, I, I, F, P]
+    lib.fox_attn_bwd_workspace_bytes.restype = Z
+    lib.fox_attn_bwd_workspace_bytes.argtypes = [I, I, I, I, I]
+    lib.fox_attn_bwd.restype = I
+    lib.fox_attn_bwd.argtypes = [I, P, P, P, P, P, P, P, P, P, P, P, P, Z, I, I, I, I, F, P]
+    lib.fox_attn_decode_workspace_bytes.restype = Z
+    lib.fox_attn_decode_workspace_bytes.argtypes = [I, I, I, I, I]
+    lib.fox_attn_decode.restype = I
+    lib.fox_attn_decode.argtypes = [I, P, P, P, P, P, P, P, P, Z, I, I, I, I, F, P]
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load().fox_status_string(int(status)).decode()
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(t: torch.Tensor):
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _check(t: torch.Tensor, name: str, shape, dtype, device):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a GPU tensor (got {t.device}); the library has no CPU path")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype} (got {t.dtype})")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)} (got {tuple(t.shape)})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _raise(status: int, what: str):
+    if status != 0:
+        raise FoxError(status, what)
+
+
+def default_scale(d: int) -> float:
+    """The paper's 1/sqrt(d) scale on q.k."""
+    return 1.0 / math.sqrt(d)
+
+
+# ---------------------------------------------------------------------------
+def fox_gate_prefix(gate_logit: torch.Tensor, c: Optional[torch.Tensor] = None,
+                    log_f: Optional[torch.Tensor] = None, want_log_f: bool = False):
+    """c = cumsum(log sigmoid(gate_logit)) over the last axis; [B, H, L] fp32.
+    Returns c, or (c, log_f) when want_log_f or log_f is given."""
+    B, H, L = gate_logit.shape
+    _check(gate_logit, "gate_logit", (B, H, L), torch.float32, None)
+    dev = gate_logit.device
+    if c is None:
+        c = torch.empty_like(gate_logit)
+    _check(c, "c", (B, H, L), torch.float32, dev)
+    if want_log_f and log_f is None:
+        log_f = torch.empty_like(gate_logit)
+    if log_f is not None:
+        _check(log_f, "log_f", (B, H, L), torch.float32, dev)
+    st = load().fox_gate_prefix(_ptr(gate_logit), _ptr(log_f), _ptr(c), B, H, L,
+                                _stream(gate_logit))
+    _raise(st, "fox_gate_prefix")
+    return (c, log_f) if log_f is not None else c
+
+
+def fox_attn_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, c: torch.Tensor,
+                 scale: Optional[float] = None, o: Optional[torch.Tensor] = None,
+                 lse: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """O [B,H,L,d] (q's dtype) and LSE [B,H,L] fp32."""
+    B, H, L, d = q.shape
+    dt = q.dtype
+    if dt not in _DT:
+        raise ValueError(f"unsupported dtype {dt}")
+    dev = q.device
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _check(t, name, (B, H, L, d), dt, dev)
+    _check(c, "c", (B, H, L), torch.float32, dev)
+    if o is None:
+        o = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((B, H, L), device=dev, dtype=torch.float32)
+    _check(o, "o", (B, H, L, d), dt, dev)
+    _check(lse, "lse", (B, H, L), torch.float32, dev)
+    s = default_scale(d) if scale is None else float(scale)
+    st = load().fox_attn_fwd(_DT[dt], _ptr(q), _ptr(k), _ptr(v), _ptr(c), _ptr(o), _ptr(lse),
+                             B, H, L, d, s, _stream(q))
+    _raise(st, "fox_attn_fwd")
+    return o, lse
+
+
+def fox_attn_bwd_workspace_bytes(dtype: torch.dtype, B: int, H: int, L: int, d: int) -> int:
+    return int(load().fox_attn_bwd_workspace_bytes(_DT[dtype], B, H, L, d))
+
+
+def fox_attn_bwd(q, k, v, c, o, lse, d_o, scale: Optional[float] = None,
+                 dq=None, dk=None, dv=None, d_log_f=None, workspace=None):
+    """dq, dk, dv [B,H,L,d] and d(log f) [B,H,L] fp32."""
+    B, H, L, d = q.shape
+    dt = q.dtype
+    if dt not in _DT:
+        raise ValueError(f"unsupported dtype {dt}")
+    dev = q.device
+    for name, t in (("q", q), ("k", k), ("v", v), ("o", o), ("d_o", d_o)):
+        _check(t, name, (B, H, L, d), dt, dev)
+    _check(c, "c", (B, H, L), torch.float32, dev)
+    _check(lse, "lse", (B, H, L), torch.float32, dev)
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(k) if dk is None else dk
+    dv = torch.empty_like(v) if dv is None else dv
+    d_log_f = torch.empty_like(c) if d_log_f is None else d_log_f
+    for name, t in (("dq", dq), ("dk", dk), ("dv", dv)):
+        _check(t, name, (B, H, L, d), dt, dev)
+    _check(d_log_f, "d_log_f", (B, H, L), torch.float32, dev)
+    need = fox_attn_bwd_workspace_bytes(dt, B, H, L, d)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), device=dev, dtype=torch.uint8)
+    s = default_scale(d) if scale is None else float(scale)
+    st = load().fox_attn_bwd(_DT[dt], _ptr(q), _ptr(k), _ptr(v), _ptr(c), _ptr(o), _ptr(lse),
+                             _ptr(d_o), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(d_log_f),
+                             _ptr(workspace), workspace.numel() * workspace.element_size(),
+                             B, H, L, d, s, _stream(q))
+    _raise(st, "fox_attn_bwd")
+    return dq, dk, dv, d_log_f
+
+
+def fox_attn_decode_workspace_bytes(dtype: torch.dtype, B: int, H: int, T: int, d: int) -> int:
+    return int(load().fox_attn_decode_workspace_bytes(_DT[dtype], B, H, T, d))
+
+
+def fox_attn_decode(q, k_cache, v_cache, c_cache, gate_logit_new, scale: Optional[float] = None,
+                    o=None, lse=None, workspace=None):
+    """One decode step.  q [B,H,d]; caches [B,H,T,d] (slot T-1 = new token);
+    c_cache [B,H,T] fp32 (entry T-1 is written); gate_logit_new [B,H] fp32.
+    Returns o [B,H,d] and lse [B,H]."""
+    B, H, d = q.shape
+    T = k_cache.shape[2]
+    dt = q.dtype
+    if dt not in _DT:
+        raise ValueError(f"unsupported dtype {dt}")
+    dev = q.device
+    _check(q, "q", (B, H, d), dt, dev)
+    _check(k_cache, "k_cache", (B, H, T, d), dt, dev)
+    _check(v_cache, "v_cache", (B, H, T, d), dt, dev)
+    _check(c_cache, "c_cache", (B, H, T), torch.float32, dev)
+    _check(gate_logit_new, "gate_logit_new", (B, H), torch.float32, dev)
+    o = torch.empty_like(q) if o is None else o
+    lse = torch.empty((B, H), device=dev, dtype=torch.float32) if lse is None else lse
+    _check(o, "o", (B, H, d), dt, dev)
+    _check(lse, "lse", (B, H), torch.float32, dev)
+    need = fox_attn_decode_workspace_bytes(dt, B, H, T, d)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), device=dev, dtype=torch.uint8)
+    s = default_scale(d) if scale is None else float(scale)
+    st = load().fox_attn_decode(_DT[dt], _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(c_cache),
+                                _ptr(gate_logit_new), _ptr(o), _ptr(lse), _ptr(workspace),
+                                workspace.numel() * workspace.element_size(), B, H, T, d, s,
+                                _stream(q))
+    _raise(st, "fox_attn_decode")
+    return o, lse

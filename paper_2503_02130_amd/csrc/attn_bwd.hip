@@ -1,0 +1,662 @@
+// Forgetting Attention backward pass (appendix, Alg. 2).
+//
+// With P = exp(S - LSE) recomputed from the saved logsumexp,
+//     dV = P^T dO,  dP = dO V^T,  dS = P o (dP - Delta),  Delta_i = rowsum(dO_i o O_i),
+//     dQ = s dS K,  dK = s dS^T Q,  dc^q_i = rowsum_i(dS),  dc^k_j = -colsum_j(dS),
+// and d(log f)_l = sum_{i>=l} (dc^q_i + dc^k_i), the chain rule through
+// c = cumsum(log f).  The paper computes dK, dV, dc^k and dQ, dc^q in two kernels;
+// this file does the same, which keeps every accumulation in one workgroup's
+// registers (no atomics, deterministic results):
+//
+//   delta kernel   Delta_i from the stored O (bf16 or fp32) and dO.
+//   dq kernel      query-stationary: 32 queries per wave; S^T = K Q^T and
+//                  dP^T = V dO^T on MFMA, dS^T in registers, dQ^T += K^T dS^T with
+//                  K also stored transposed in LDS; dc^q from in-register row sums.
+//   dkdv kernel    key-stationary: 32 keys per wave; S = Q K^T and dP = dO V^T,
+//                  then dV^T += dO^T P and dK^T += Q^T dS with Q and dO stored both
+//                  row-major and transposed in LDS; dc^k from in-register sums.
+//   reverse scan   (gate_scan.hip) turns dc^q + dc^k into d(log f).
+//
+// The forget-gate bias is formed relative to c_ref (the first query of the
+// block for dq, the first key of the block for dkdv), exactly as in the forward:
+//     log2 P_ij = s log2(e) q_i.k_j + log2(e) ((c_i - c_ref) - LSE_i) - log2(e) (c_j - c_ref).
+#include "fox_device.h"
+#include "fox_internal.h"
+
+namespace fox {
+
+size_t bwd_workspace_bytes(int BH, int L) { return (size_t)3 * BH * (size_t)L * sizeof(float); }
+
+// ---------------------------------------------------------------------------
+// Delta_i = sum_d dO_id * O_id
+// ---------------------------------------------------------------------------
+template <typename T, int D>
+__global__ __launch_bounds__(256) void bwd_delta_kernel(const T* __restrict__ O,
+                                                        const T* __restrict__ dO,
+                                                        float* __restrict__ delta, size_t rows) {
+  constexpr int VEC = 16 / sizeof(T);
+  constexpr int LPR = D / VEC;  // lanes per row
+  const size_t row = ((size_t)blockIdx.x * 256 + threadIdx.x) / LPR;
+  const int part = threadIdx.x % LPR;
+  float acc = 0.0f;
+  if (row < rows) {
+    const T* o = O + row * D + part * VEC;
+    const T* g = dO + row * D + part * VEC;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) acc += (float)o[e] * (float)g[e];
+  }
+#pragma unroll
+  for (int off = 1; off < LPR; off <<= 1) acc += __shfl_xor(acc, off);
+  if (row < rows && part == 0) delta[row] = acc;
+}
+
+// ---------------------------------------------------------------------------
+// bf16 dq kernel
+// ---------------------------------------------------------------------------
+constexpr int kBwdThreads = 256;
+constexpr int kDqBM = 128;  // queries per workgroup (4 waves x 32)
+constexpr int kDqBN = 64;   // keys per tile
+
+template <int D>
+struct alignas(16) DqTile {
+  static constexpr int RS = D + 8;      // row-major stride
+  static constexpr int TS = kDqBN + 4;  // transposed stride
+  static constexpr int KPT = kDqBN * D / 8 / kBwdThreads;
+  bf16 k[kDqBN * RS];
+  bf16 kt[D * TS];
+  bf16 v[kDqBN * RS];
+  float ck[kDqBN];
+};
+
+template <int D>
+__global__ __launch_bounds__(kBwdThreads) void bwd_dq_bf16_kernel(
+    const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
+    const float* __restrict__ C, const float* __restrict__ LSE, const bf16* __restrict__ dO,
+    const float* __restrict__ delta, bf16* __restrict__ dQ, float* __restrict__ dcq, int BH,
+    int L, int n_mblk, float scale, float scale_log2) {
+  using T = DqTile<D>;
+  __shared__ T sm;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int h = lane >> 5, col = lane & 31;
+  const int bh = blockIdx.x % BH;
+  const int mblk = n_mblk - 1 - (int)(blockIdx.x / BH);
+  const int q0 = mblk * kDqBM;
+  const size_t head = (size_t)bh * (size_t)L;
+  const bf16* Kh = K + head * D;
+  const bf16* Vh = V + head * D;
+  const float* Ch = C + head;
+  const float c_ref = Ch[q0];
+  const int qw0 = q0 + wave * 32;
+  const int qi = qw0 + col;
+  const bool q_valid = qi < L;
+
+  bf16x8 qf[D / 16], dof[D / 16];
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s) {
+    if (q_valid) {
+      qf[s] = *reinterpret_cast<const bf16x8*>(Q + (head + qi) * D + 16 * s + 8 * h);
+      dof[s] = *reinterpret_cast<const bf16x8*>(dO + (head + qi) * D + 16 * s + 8 * h);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        qf[s][e] = to_bf16(0.0f);
+        dof[s][e] = to_bf16(0.0f);
+      }
+    }
+  }
+  const float bias2 = q_valid ? ((Ch[qi] - c_ref) - LSE[head + qi]) * kLog2e : -INFINITY;
+  const float dlt = q_valid ? delta[head + qi] : 0.0f;
+
+  f32x16 dqacc[D / 32];
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) dqacc[db][r] = 0.0f;
+  float dcq_part = 0.0f;
+
+  const int kend = min(L, q0 + kDqBM);
+  const int n_kt = (kend + kDqBN - 1) / kDqBN;
+  const int dg = tid % (D / 8), kg = tid / (D / 8);
+
+  for (int kt = 0; kt < n_kt; ++kt) {
+    const int key0 = kt * kDqBN;
+    bf16x8 kreg[T::KPT], vreg[T::KPT];
+#pragma unroll
+    for (int r = 0; r < T::KPT; ++r) {
+      const int key = key0 + kg * T::KPT + r;
+      if (key < L) {
+        kreg[r] = *reinterpret_cast<const bf16x8*>(Kh + (size_t)key * D + dg * 8);
+        vreg[r] = *reinterpret_cast<const bf16x8*>(Vh + (size_t)key * D + dg * 8);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          kreg[r][e] = to_bf16(0.0f);
+          vreg[r][e] = to_bf16(0.0f);
+        }
+      }
+    }
+    float creg = 0.0f;
+    if (tid < kDqBN) {
+      const int key = key0 + tid;
+      creg = key < L ? (Ch[key] - c_ref) * kLog2e : INFINITY;
+    }
+    __syncthreads();  // previous tile fully consumed
+#pragma unroll
+    for (int r = 0; r < T::KPT; ++r) {
+      const int row = kg * T::KPT + r;
+      *reinterpret_cast<bf16x8*>(&sm.k[row * T::RS + dg * 8]) = kreg[r];
+      *reinterpret_cast<bf16x8*>(&sm.v[row * T::RS + dg * 8]) = vreg[r];
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      bf16* dst = &sm.kt[(dg * 8 + e) * T::TS + kg * T::KPT];
+      if constexpr (T::KPT == 4) {
+        bf16x4 w = {kreg[0][e], kreg[1][e], kreg[2][e], kreg[3][e]};
+        *reinterpret_cast<bf16x4*>(dst) = w;
+      } else {
+        bf16x2 w = {kreg[0][e], kreg[1][e]};
+        *reinterpret_cast<bf16x2*>(dst) = w;
+      }
+    }
+    if (tid < kDqBN) sm.ck[tid] = creg;
+    __syncthreads();
+
+    if (key0 > qw0 + 31) continue;  // the whole tile lies after this wave's queries
+    const bool diag = key0 + kDqBN - 1 > qw0;
+
+    float dsv[32];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      f32x16 sacc, pacc;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        sacc[r] = 0.0f;
+        pacc[r] = 0.0f;
+      }
+#pragma unroll
+      for (int s = 0; s < D / 16; ++s) {
+        const int off = (kb * 32 + col) * T::RS + 16 * s + 8 * h;
+        sacc = mfma32(*reinterpret_cast<const bf16x8*>(&sm.k[off]), qf[s], sacc);
+        pacc = mfma32(*reinterpret_cast<const bf16x8*>(&sm.v[off]), dof[s], pacc);
+      }
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int kl = kb * 32 + 8 * g + 4 * h;
+        const f32x4 ck4 = *reinterpret_cast<const f32x4*>(&sm.ck[kl]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          float p = exp2_fast(sacc[4 * g + j] * scale_log2 - ck4[j] + bias2);
+          if (diag && key0 + kl + j > qi) p = 0.0f;
+          const float ds = p * (pacc[4 * g + j] - dlt);
+          dcq_part += ds;
+          dsv[kb * 16 + 4 * g + j] = ds;
+        }
+      }
+    }
+    bf16x8 dsb[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) dsb[c] = pack8(&dsv[8 * c]);
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const bf16* row = &sm.kt[(db * 32 + col) * T::TS + 16 * c + 4 * h];
+        const bf16x4 lo = *reinterpret_cast<const bf16x4*>(row);
+        const bf16x4 hi = *reinterpret_cast<const bf16x4*>(row + 8);
+        dqacc[db] = mfma32(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7), dsb[c],
+                           dqacc[db]);
+      }
+    }
+  }
+
+  const float dcq_tot = wave_sum_pair(dcq_part);
+  if (q_valid) {
+    bf16* out = dQ + (head + qi) * D;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        bf16x4 w;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) w[j] = to_bf16(dqacc[db][4 * g + j] * scale);
+        *reinterpret_cast<bf16x4*>(out + db * 32 + 8 * g + 4 * h) = w;
+      }
+    }
+    if (h == 0) dcq[head + qi] = dcq_tot;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// bf16 dkdv kernel
+// ---------------------------------------------------------------------------
+constexpr int kKvBN = 128;  // keys per workgroup (4 waves x 32)
+constexpr int kKvBM = 64;   // queries per tile
+
+template <int D>
+struct alignas(16) KvTile {
+  static constexpr int RS = D + 8;
+  static constexpr int TS = kKvBM + 4;
+  static constexpr int QPT = kKvBM * D / 8 / kBwdThreads;  // query rows per thread
+  bf16 q[kKvBM * RS];
+  bf16 qt[D * TS];
+  bf16 g[kKvBM * RS];
+  bf16 gt[D * TS];
+  float bq[kKvBM];
+  float dl[kKvBM];
+};
+
+template <int D>
+__global__ __launch_bounds__(kBwdThreads) void bwd_dkdv_bf16_kernel(
+    const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
+    const float* __restrict__ C, const float* __restrict__ LSE, const bf16* __restrict__ dO,
+    const float* __restrict__ delta, bf16* __restrict__ dK, bf16* __restrict__ dV,
+    float* __restrict__ dck, int BH, int L, float scale, float scale_log2) {
+  using T = KvTile<D>;
+  __shared__ T sm;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int h = lane >> 5, col = lane & 31;
+  const int bh = blockIdx.x % BH;
+  const int nblk = (int)(blockIdx.x / BH);  // key block 0 has the most work: first
+  const int k0 = nblk * kKvBN;
+  const size_t head = (size_t)bh * (size_t)L;
+  const bf16* Qh = Q + head * D;
+  const bf16* Gh = dO + head * D;
+  const float* Ch = C + head;
+  const float c_ref = Ch[k0];
+  const int kw0 = k0 + wave * 32;
+  const int kj = kw0 + col;
+  const bool k_valid = kj < L;
+
+  bf16x8 kf[D / 16], vf[D / 16];
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s) {
+    if (k_valid) {
+      kf[s] = *reinterpret_cast<const bf16x8*>(K + (head + kj) * D + 16 * s + 8 * h);
+      vf[s] = *reinterpret_cast<const bf16x8*>(V + (head + kj) * D + 16 * s + 8 * h);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        kf[s][e] = to_bf16(0.0f);
+        vf[s][e] = to_bf16(0.0f);
+      }
+    }
+  }
+  const float ck2 = k_valid ? (Ch[kj] - c_ref) * kLog2e : INFINITY;
+
+  f32x16 dkacc[D / 32], dvacc[D / 32];
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      dkacc[db][r] = 0.0f;
+      dvacc[db][r] = 0.0f;
+    }
+  float dck_part = 0.0f;
+
+  const int t_begin = k0 / kKvBM;
+  const int n_qt = (L + kKvBM - 1) / kKvBM;
+  const int dg = tid % (D / 8), qg = tid / (D / 8);
+
+  for (int qt = t_begin; qt < n_qt; ++qt) {
+    const int qs0 = qt * kKvBM;
+    bf16x8 qreg[T::QPT], greg[T::QPT];
+#pragma unroll
+    for (int r = 0; r < T::QPT; ++r) {
+      const int qq = qs0 + qg * T::QPT + r;
+      if (qq < L) {
+        qreg[r] = *reinterpret_cast<const bf16x8*>(Qh + (size_t)qq * D + dg * 8);
+        greg[r] = *reinterpret_cast<const bf16x8*>(Gh + (size_t)qq * D + dg * 8);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          qreg[r][e] = to_bf16(0.0f);
+          greg[r][e] = to_bf16(0.0f);
+        }
+      }
+    }
+    float bqreg = -INFINITY, dlreg = 0.0f;
+    if (tid < kKvBM) {
+      const int qq = qs0 + tid;
+      if (qq < L) {
+        bqreg = ((Ch[qq] - c_ref) - LSE[head + qq]) * kLog2e;
+        dlreg = delta[head + qq];
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < T::QPT; ++r) {
+      const int row = qg * T::QPT + r;
+      *reinterpret_cast<bf16x8*>(&sm.q[row * T::RS + dg * 8]) = qreg[r];
+      *reinterpret_cast<bf16x8*>(&sm.g[row * T::RS + dg * 8]) = greg[r];
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      bf16* dq_ = &sm.qt[(dg * 8 + e) * T::TS + qg * T::QPT];
+      bf16* dg_ = &sm.gt[(dg * 8 + e) * T::TS + qg * T::QPT];
+      if constexpr (T::QPT == 4) {
+        bf16x4 a = {qreg[0][e], qreg[1][e], qreg[2][e], qreg[3][e]};
+        bf16x4 b = {greg[0][e], greg[1][e], greg[2][e], greg[3][e]};
+        *reinterpret_cast<bf16x4*>(dq_) = a;
+        *reinterpret_cast<bf16x4*>(dg_) = b;
+      } else {
+        bf16x2 a = {qreg[0][e], qreg[1][e]};
+        bf16x2 b = {greg[0][e], greg[1][e]};
+        *reinterpret_cast<bf16x2*>(dq_) = a;
+        *reinterpret_cast<bf16x2*>(dg_) = b;
+      }
+    }
+    if (tid < kKvBM) {
+      sm.bq[tid] = bqreg;
+      sm.dl[tid] = dlreg;
+    }
+    __syncthreads();
+
+    if (qs0 + kKvBM - 1 < kw0) continue;  // every query of the tile precedes this wave's keys
+    const bool diag = qs0 < kw0 + 31;
+
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      f32x16 sacc, pacc;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        sacc[r] = 0.0f;
+        pacc[r] = 0.0f;
+      }
+#pragma unroll
+      for (int s = 0; s < D / 16; ++s) {
+        const int off = (qb * 32 + col) * T::RS + 16 * s + 8 * h;
+        sacc = mfma32(*reinterpret_cast<const bf16x8*>(&sm.q[off]), kf[s], sacc);
+        pacc = mfma32(*reinterpret_cast<const bf16x8*>(&sm.g[off]), vf[s], pacc);
+      }
+      float pv[16], dsv[16];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int ql = qb * 32 + 8 * g + 4 * h;
+        const f32x4 bq4 = *reinterpret_cast<const f32x4*>(&sm.bq[ql]);
+        const f32x4 dl4 = *reinterpret_cast<const f32x4*>(&sm.dl[ql]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          float p = exp2_fast(sacc[4 * g + j] * scale_log2 + bq4[j] - ck2);
+          if (diag && kj > qs0 + ql + j) p = 0.0f;
+          const float ds = p * (pacc[4 * g + j] - dl4[j]);
+          dck_part -= ds;
+          pv[4 * g + j] = p;
+          dsv[4 * g + j] = ds;
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const bf16x8 pb = pack8(&pv[8 * c]);
+        const bf16x8 dsb = pack8(&dsv[8 * c]);
+        const int qoff = qb * 32 + 16 * c + 4 * h;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) {
+          const int roff = (db * 32 + col) * T::TS + qoff;
+          const bf16x4 glo = *reinterpret_cast<const bf16x4*>(&sm.gt[roff]);
+          const bf16x4 ghi = *reinterpret_cast<const bf16x4*>(&sm.gt[roff + 8]);
+          dvacc[db] = mfma32(__builtin_shufflevector(glo, ghi, 0, 1, 2, 3, 4, 5, 6, 7), pb,
+                             dvacc[db]);
+          const bf16x4 qlo = *reinterpret_cast<const bf16x4*>(&sm.qt[roff]);
+          const bf16x4 qhi = *reinterpret_cast<const bf16x4*>(&sm.qt[roff + 8]);
+          dkacc[db] = mfma32(__builtin_shufflevector(qlo, qhi, 0, 1, 2, 3, 4, 5, 6, 7), dsb,
+                             dkacc[db]);
+        }
+      }
+    }
+  }
+
+  const float dck_tot = wave_sum_pair(dck_part);
+  if (k_valid) {
+    bf16* ok = dK + (head + kj) * D;
+    bf16* ov = dV + (head + kj) * D;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        bf16x4 wk, wv;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          wk[j] = to_bf16(dkacc[db][4 * g + j] * scale);
+          wv[j] = to_bf16(dvacc[db][4 * g + j]);
+        }
+        *reinterpret_cast<bf16x4*>(ok + db * 32 + 8 * g + 4 * h) = wk;
+        *reinterpret_cast<bf16x4*>(ov + db * 32 + 8 * g + 4 * h) = wv;
+      }
+    }
+    if (h == 0) dck[head + kj] = dck_tot;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// fp32 kernels: G = D/32 lanes per row, each lane owning 32 head dims.
+// ---------------------------------------------------------------------------
+constexpr int kF32Threads = 256;
+constexpr int kF32Tile = 32;
+
+template <int D>
+__global__ __launch_bounds__(kF32Threads) void bwd_dq_f32_kernel(
+    const float* __restrict__ Q, const float* __restrict__ K, const float* __restrict__ V,
+    const float* __restrict__ C, const float* __restrict__ LSE, const float* __restrict__ dO,
+    const float* __restrict__ delta, float* __restrict__ dQ, float* __restrict__ dcq, int L,
+    int n_blk, float scale, float scale_log2) {
+  constexpr int G = D / 32;
+  constexpr int RPW = kF32Threads / G;
+  __shared__ float ks[kF32Tile][D + 1];
+  __shared__ float vs[kF32Tile][D + 1];
+  __shared__ float cks[kF32Tile];
+  const int tid = threadIdx.x, sub = tid % G;
+  const size_t head = (size_t)(blockIdx.x / n_blk) * (size_t)L;
+  const int q0 = (int)(blockIdx.x % n_blk) * RPW;
+  const int qi = q0 + tid / G;
+  const bool q_valid = qi < L;
+  const float* Ch = C + head;
+  const float c_ref = Ch[q0];
+  float qv[32], gv[32], acc[32];
+#pragma unroll
+  for (int e = 0; e < 32; ++e) {
+    qv[e] = q_valid ? Q[(head + qi) * D + sub * 32 + e] : 0.0f;
+    gv[e] = q_valid ? dO[(head + qi) * D + sub * 32 + e] : 0.0f;
+    acc[e] = 0.0f;
+  }
+  const float cq = q_valid ? Ch[qi] - c_ref : 0.0f;
+  const float lq = q_valid ? LSE[head + qi] : INFINITY;
+  const float dlt = q_valid ? delta[head + qi] : 0.0f;
+  float dc = 0.0f;
+  const int kend = min(L, q0 + RPW);
+  for (int key0 = 0; key0 < kend; key0 += kF32Tile) {
+    __syncthreads();
+    for (int i = tid; i < kF32Tile * D; i += kF32Threads) {
+      const int r = i / D, e = i % D, key = key0 + r;
+      ks[r][e] = key < L ? K[(head + key) * D + e] : 0.0f;
+      vs[r][e] = key < L ? V[(head + key) * D + e] : 0.0f;
+    }
+    if (tid < kF32Tile) {
+      const int key = key0 + tid;
+      cks[tid] = key < L ? Ch[key] - c_ref : INFINITY;
+    }
+    __syncthreads();
+    for (int j = 0; j < kF32Tile; ++j) {
+      float s = 0.0f, dp = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 32; ++e) {
+        s += qv[e] * ks[j][sub * 32 + e];
+        dp += gv[e] * vs[j][sub * 32 + e];
+      }
+#pragma unroll
+      for (int off = 1; off < G; off <<= 1) {
+        s += __shfl_xor(s, off);
+        dp += __shfl_xor(dp, off);
+      }
+      float p = exp2_fast(s * scale_log2 + ((cq - cks[j]) - lq) * kLog2e);
+      if (key0 + j > qi) p = 0.0f;
+      const float ds = p * (dp - dlt);
+      dc += ds;
+#pragma unroll
+      for (int e = 0; e < 32; ++e) acc[e] += ds * ks[j][sub * 32 + e];
+    }
+  }
+  if (q_valid) {
+#pragma unroll
+    for (int e = 0; e < 32; ++e) dQ[(head + qi) * D + sub * 32 + e] = acc[e] * scale;
+    if (sub == 0) dcq[head + qi] = dc;
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(kF32Threads) void bwd_dkdv_f32_kernel(
+    const float* __restrict__ Q, const float* __restrict__ K, const float* __restrict__ V,
+    const float* __restrict__ C, const float* __restrict__ LSE, const float* __restrict__ dO,
+    const float* __restrict__ delta, float* __restrict__ dK, float* __restrict__ dV,
+    float* __restrict__ dck, int L, int n_blk, float scale, float scale_log2) {
+  constexpr int G = D / 32;
+  constexpr int RPW = kF32Threads / G;
+  __shared__ float qs[kF32Tile][D + 1];
+  __shared__ float gs[kF32Tile][D + 1];
+  __shared__ float cqs[kF32Tile];
+  __shared__ float lqs[kF32Tile];
+  __shared__ float dls[kF32Tile];
+  const int tid = threadIdx.x, sub = tid % G;
+  const size_t head = (size_t)(blockIdx.x / n_blk) * (size_t)L;
+  const int k0 = (int)(blockIdx.x % n_blk) * RPW;
+  const int kj = k0 + tid / G;
+  const bool k_valid = kj < L;
+  const float* Ch = C + head;
+  const float c_ref = Ch[k0];
+  float kv[32], vv[32], ak[32], av[32];
+#pragma unroll
+  for (int e = 0; e < 32; ++e) {
+    kv[e] = k_valid ? K[(head + kj) * D + sub * 32 + e] : 0.0f;
+    vv[e] = k_valid ? V[(head + kj) * D + sub * 32 + e] : 0.0f;
+    ak[e] = 0.0f;
+    av[e] = 0.0f;
+  }
+  const float ck = k_valid ? Ch[kj] - c_ref : -INFINITY;
+  float dc = 0.0f;
+  for (int qs0 = k0; qs0 < L; qs0 += kF32Tile) {
+    __syncthreads();
+    for (int i = tid; i < kF32Tile * D; i += kF32Threads) {
+      const int r = i / D, e = i % D, qq = qs0 + r;
+      qs[r][e] = qq < L ? Q[(head + qq) * D + e] : 0.0f;
+      gs[r][e] = qq < L ? dO[(head + qq) * D + e] : 0.0f;
+    }
+    if (tid < kF32Tile) {
+      const int qq = qs0 + tid;
+      cqs[tid] = qq < L ? Ch[qq] - c_ref : 0.0f;
+      lqs[tid] = qq < L ? LSE[head + qq] : INFINITY;
+      dls[tid] = qq < L ? delta[head + qq] : 0.0f;
+    }
+    __syncthreads();
+    for (int i = 0; i < kF32Tile; ++i) {
+      float s = 0.0f, dp = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 32; ++e) {
+        s += kv[e] * qs[i][sub * 32 + e];
+        dp += vv[e] * gs[i][sub * 32 + e];
+      }
+#pragma unroll
+      for (int off = 1; off < G; off <<= 1) {
+        s += __shfl_xor(s, off);
+        dp += __shfl_xor(dp, off);
+      }
+      float p = exp2_fast(s * scale_log2 + ((cqs[i] - ck) - lqs[i]) * kLog2e);
+      if (kj > qs0 + i || !k_valid) p = 0.0f;
+      const float ds = p * (dp - dls[i]);
+      dc -= ds;
+#pragma unroll
+      for (int e = 0; e < 32; ++e) {
+        av[e] += p * gs[i][sub * 32 + e];
+        ak[e] += ds * qs[i][sub * 32 + e];
+      }
+    }
+  }
+  if (k_valid) {
+#pragma unroll
+    for (int e = 0; e < 32; ++e) {
+      dK[(head + kj) * D + sub * 32 + e] = ak[e] * scale;
+      dV[(head + kj) * D + sub * 32 + e] = av[e];
+    }
+    if (sub == 0) dck[head + kj] = dc;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// launchers
+// ---------------------------------------------------------------------------
+template <typename T>
+static hipError_t launch_delta(const T* o, const T* g, float* delta, int BH, int L, int d,
+                               hipStream_t s) {
+  const size_t rows = (size_t)BH * (size_t)L;
+  const int lpr = d / (16 / (int)sizeof(T));
+  const size_t threads = rows * (size_t)lpr;
+  const dim3 grid((unsigned)((threads + 255) / 256));
+  if (d == 128) {
+    hipLaunchKernelGGL((bwd_delta_kernel<T, 128>), grid, dim3(256), 0, s, o, g, delta, rows);
+  } else {
+    hipLaunchKernelGGL((bwd_delta_kernel<T, 64>), grid, dim3(256), 0, s, o, g, delta, rows);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_bf16(const void* q, const void* k, const void* v, const float* c,
+                           const void* o, const float* lse, const void* d_o, void* dq, void* dk,
+                           void* dv, float* d_log_f, void* ws, int BH, int L, int d, float scale,
+                           hipStream_t s) {
+  float* delta = static_cast<float*>(ws);
+  float* dcq = delta + (size_t)BH * L;
+  float* dck = dcq + (size_t)BH * L;
+  hipError_t e = launch_delta((const bf16*)o, (const bf16*)d_o, delta, BH, L, d, s);
+  if (e != hipSuccess) return e;
+  const float sl2 = scale * kLog2e;
+  const int n_mblk = (L + kDqBM - 1) / kDqBM;
+  const int n_nblk = (L + kKvBN - 1) / kKvBN;
+  const dim3 gq((unsigned)n_mblk * (unsigned)BH), gk((unsigned)n_nblk * (unsigned)BH);
+  if (d == 128) {
+    hipLaunchKernelGGL(bwd_dkdv_bf16_kernel<128>, gk, dim3(kBwdThreads), 0, s, (const bf16*)q,
+                       (const bf16*)k, (const bf16*)v, c, lse, (const bf16*)d_o, delta, (bf16*)dk,
+                       (bf16*)dv, dck, BH, L, scale, sl2);
+    hipLaunchKernelGGL(bwd_dq_bf16_kernel<128>, gq, dim3(kBwdThreads), 0, s, (const bf16*)q,
+                       (const bf16*)k, (const bf16*)v, c, lse, (const bf16*)d_o, delta, (bf16*)dq,
+                       dcq, BH, L, n_mblk, scale, sl2);
+  } else {
+    hipLaunchKernelGGL(bwd_dkdv_bf16_kernel<64>, gk, dim3(kBwdThreads), 0, s, (const bf16*)q,
+                       (const bf16*)k, (const bf16*)v, c, lse, (const bf16*)d_o, delta, (bf16*)dk,
+                       (bf16*)dv, dck, BH, L, scale, sl2);
+    hipLaunchKernelGGL(bwd_dq_bf16_kernel<64>, gq, dim3(kBwdThreads), 0, s, (const bf16*)q,
+                       (const bf16*)k, (const bf16*)v, c, lse, (const bf16*)d_o, delta, (bf16*)dq,
+                       dcq, BH, L, n_mblk, scale, sl2);
+  }
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_reverse_scan_sum(dcq, dck, d_log_f, BH, L, s);
+}
+
+hipError_t launch_bwd_f32(const float* q, const float* k, const float* v, const float* c,
+                          const float* o, const float* lse, const float* d_o, float* dq, float* dk,
+                          float* dv, float* d_log_f, void* ws, int BH, int L, int d, float scale,
+                          hipStream_t s) {
+  float* delta = static_cast<float*>(ws);
+  float* dcq = delta + (size_t)BH * L;
+  float* dck = dcq + (size_t)BH * L;
+  hipError_t e = launch_delta(o, d_o, delta, BH, L, d, s);
+  if (e != hipSuccess) return e;
+  const float sl2 = scale * kLog2e;
+  const int rpw = kF32Threads / (d / 32);
+  const int n_blk = (L + rpw - 1) / rpw;
+  const dim3 grid((unsigned)n_blk * (unsigned)BH);
+  if (d == 128) {
+    hipLaunchKernelGGL(bwd_dkdv_f32_kernel<128>, grid, dim3(kF32Threads), 0, s, q, k, v, c, lse,
+                       d_o, delta, dk, dv, dck, L, n_blk, scale, sl2);
+    hipLaunchKernelGGL(bwd_dq_f32_kernel<128>, grid, dim3(kF32Threads), 0, s, q, k, v, c, lse,
+                       d_o, delta, dq, dcq, L, n_blk, scale, sl2);
+  } else {
+    hipLaunchKernelGGL(bwd_dkdv_f32_kernel<64>, grid, dim3(kF32Threads), 0, s, q, k, v, c, lse,
+                       d_o, delta, dk, dv, dck, L, n_blk, scale, sl2);
+    hipLaunchKernelGGL(bwd_dq_f32_kernel<64>, grid, dim3(kF32Threads), 0, s, q, k, v, c, lse,
+                       d_o, delta, dq, dcq, L, n_blk, scale, sl2);
+  }
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_reverse_scan_sum(dcq, dck, d_log_f, BH, L, s);
+}
+
+}  // namespace fox

@@ -1,0 +1,217 @@
+// One decode step of Forgetting Attention: Eq. fot-weight evaluated for the last
+// position T of a sequence whose keys and values sit in a cache.
+//
+//     c_T   = c_{T-1} + log sigmoid(x_new)           (c_0 = 0)
+//     s_j   = s q.k_j + c_T - c_j,   j = 1..T         (key T is the new token)
+//     o     = sum_j softmax(s)_j v_j,  lse = log sum_j exp(s_j)
+//
+// The step streams K and V once from HBM (the bound), so the kernel is built for
+// bandwidth: the T keys of each (batch, head) are split across workgroups, a
+// group of D/8 (bf16) lanes reads one key's row with 16-byte loads so that a
+// wave reads consecutive rows, several keys per lane group are loaded before
+// any is used, and every lane group keeps its own running (max, sum, output).
+// The lane groups of a workgroup merge through LDS into one partial per split;
+// a small second kernel merges the splits (log-sum-exp merge) and appends c_T
+// to the prefix cache.  Entry T-1 of that cache is never read: every workgroup
+// derives c_T itself, so the write cannot race with the readers.
+#include "fox_device.h"
+#include "fox_internal.h"
+
+namespace fox {
+
+constexpr int kDecThreads = 256;
+constexpr int kDecUnroll = 4;
+
+static int decode_keys_per_split(int BH, int T) {
+  // The largest split (fewer partials) that still gives >= 2048 workgroups.
+  for (int ks = 1024; ks >= 256; ks >>= 1) {
+    const long long wgs = (long long)BH * ((T + ks - 1) / ks);
+    if (wgs >= 2048) return ks;
+  }
+  return 256;
+}
+
+int decode_num_splits(int BH, int T) {
+  const int ks = decode_keys_per_split(BH, T);
+  return (T + ks - 1) / ks;
+}
+
+size_t decode_workspace_bytes(int BH, int T, int d) {
+  return (size_t)BH * (size_t)decode_num_splits(BH, T) * (size_t)(d + 2) * sizeof(float);
+}
+
+template <typename Tt>
+struct Vec16;
+template <>
+struct Vec16<bf16> {
+  typedef bf16x8 type;
+  static constexpr int N = 8;
+};
+template <>
+struct Vec16<float> {
+  typedef f32x4 type;
+  static constexpr int N = 4;
+};
+
+template <typename Tt, int D>
+__global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
+    const Tt* __restrict__ q, const Tt* __restrict__ kc, const Tt* __restrict__ vc,
+    const float* __restrict__ cc, const float* __restrict__ x_new, float* __restrict__ part,
+    int T, int keys_per_split, int n_split, float scale_log2) {
+  typedef typename Vec16<Tt>::type VT;
+  constexpr int VEC = Vec16<Tt>::N;
+  constexpr int LPK = D / VEC;                // lanes per key
+  constexpr int KPI = kDecThreads / LPK;      // keys per workgroup pass
+  __shared__ float s_acc[KPI][D];
+  __shared__ float s_m[KPI], s_l[KPI];
+
+  const int tid = threadIdx.x;
+  const int g = tid / LPK, lp = tid % LPK;
+  const int bh = blockIdx.x / n_split, split = blockIdx.x % n_split;
+  const size_t head = (size_t)bh * (size_t)T;
+  const int kbeg = split * keys_per_split;
+  const int kend = min(T, kbeg + keys_per_split);
+  const float cT = (T >= 2 ? cc[head + T - 2] : 0.0f) + log_sigmoid(x_new[bh]);
+
+  float qv[VEC], acc[VEC];
+  {
+    const VT qq = *reinterpret_cast<const VT*>(q + (size_t)bh * D + lp * VEC);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      qv[e] = (float)qq[e] * scale_log2;
+      acc[e] = 0.0f;
+    }
+  }
+  float m = -INFINITY, l = 0.0f;
+  const Tt* kh = kc + head * D + lp * VEC;
+  const Tt* vh = vc + head * D + lp * VEC;
+
+  for (int base = kbeg; base < kend; base += KPI * kDecUnroll) {
+    VT kr[kDecUnroll], vr[kDecUnroll];
+    float cj[kDecUnroll];
+#pragma unroll
+    for (int u = 0; u < kDecUnroll; ++u) {
+      const int key = base + u * KPI + g;
+      if (key < kend) {
+        kr[u] = __builtin_nontemporal_load(reinterpret_cast<const VT*>(kh + (size_t)key * D));
+        vr[u] = __builtin_nontemporal_load(reinterpret_cast<const VT*>(vh + (size_t)key * D));
+        cj[u] = key == T - 1 ? 0.0f : (cc[head + key] - cT) * kLog2e;
+      } else {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          kr[u][e] = (Tt)0.0f;
+          vr[u][e] = (Tt)0.0f;
+        }
+        cj[u] = INFINITY;
+      }
+    }
+    float sv[kDecUnroll];
+    float mu = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < kDecUnroll; ++u) {
+      float dot = 0.0f;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) dot += qv[e] * (float)kr[u][e];
+#pragma unroll
+      for (int off = 1; off < LPK; off <<= 1) dot += __shfl_xor(dot, off);
+      sv[u] = dot - cj[u];
+      mu = fmaxf(mu, sv[u]);
+    }
+    const float m_new = fmaxf(m, mu);
+    // A lane group with no key yet keeps m = -inf; a finite reference keeps the
+    // exponents below free of (-inf) - (-inf).
+    const float m_ref = m_new == -INFINITY ? 0.0f : m_new;
+    const float alpha = exp2_fast(m - m_ref);
+    l *= alpha;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) acc[e] *= alpha;
+#pragma unroll
+    for (int u = 0; u < kDecUnroll; ++u) {
+      const float p = exp2_fast(sv[u] - m_ref);
+      l += p;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) acc[e] += p * (float)vr[u][e];
+    }
+    m = m_new;
+  }
+
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) s_acc[g][lp * VEC + e] = acc[e];
+  if (lp == 0) {
+    s_m[g] = m;
+    s_l[g] = l;
+  }
+  __syncthreads();
+  float M = -INFINITY;
+  for (int i = 0; i < KPI; ++i) M = fmaxf(M, s_m[i]);
+  float* out = part + ((size_t)bh * n_split + split) * (D + 2);
+  for (int dd = tid; dd < D; dd += kDecThreads) {
+    float o = 0.0f;
+    for (int i = 0; i < KPI; ++i) o += s_acc[i][dd] * exp2_fast(s_m[i] - M);
+    out[2 + dd] = o;
+  }
+  if (tid == 0) {
+    float Ls = 0.0f;
+    for (int i = 0; i < KPI; ++i) Ls += s_l[i] * exp2_fast(s_m[i] - M);
+    out[0] = M;
+    out[1] = Ls;
+  }
+}
+
+template <typename Tt, int D>
+__global__ __launch_bounds__(D) void decode_combine_kernel(
+    const float* __restrict__ part, float* __restrict__ cc, const float* __restrict__ x_new,
+    Tt* __restrict__ o, float* __restrict__ lse, int T, int n_split) {
+  const int bh = blockIdx.x, tid = threadIdx.x;
+  const float* p = part + (size_t)bh * n_split * (D + 2);
+  float M = -INFINITY;
+  for (int s = 0; s < n_split; ++s) M = fmaxf(M, p[(size_t)s * (D + 2)]);
+  float Ls = 0.0f, acc = 0.0f;
+  for (int s = 0; s < n_split; ++s) {
+    const float* ps = p + (size_t)s * (D + 2);
+    const float w = exp2_fast(ps[0] - M);
+    Ls += ps[1] * w;
+    acc += ps[2 + tid] * w;
+  }
+  o[(size_t)bh * D + tid] = (Tt)(acc / Ls);
+  if (tid == 0) {
+    lse[bh] = kLn2 * (M + log2f(Ls));
+    const size_t head = (size_t)bh * (size_t)T;
+    cc[head + T - 1] = (T >= 2 ? cc[head + T - 2] : 0.0f) + log_sigmoid(x_new[bh]);
+  }
+}
+
+template <typename Tt, int D>
+static hipError_t launch_decode_t(const void* q, const void* k_cache, const void* v_cache,
+                                  float* c_cache, const float* logit_new, void* o, float* lse,
+                                  void* ws, int BH, int T, float scale, hipStream_t s) {
+  const int ks = decode_keys_per_split(BH, T);
+  const int n_split = (T + ks - 1) / ks;
+  float* part = static_cast<float*>(ws);
+  hipLaunchKernelGGL((decode_split_kernel<Tt, D>), dim3((unsigned)n_split * (unsigned)BH),
+                     dim3(kDecThreads), 0, s,
+                     (const Tt*)q, (const Tt*)k_cache, (const Tt*)v_cache, c_cache, logit_new,
+                     part, T, ks, n_split, scale * kLog2e);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((decode_combine_kernel<Tt, D>), dim3(BH), dim3(D), 0, s, part, c_cache,
+                     logit_new, (Tt*)o, lse, T, n_split);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode(bool bf16_, const void* q, const void* k_cache, const void* v_cache,
+                         float* c_cache, const float* logit_new, void* o, float* lse, void* ws,
+                         int BH, int T, int d, float scale, hipStream_t s) {
+  if (bf16_) {
+    return d == 128 ? launch_decode_t<bf16, 128>(q, k_cache, v_cache, c_cache, logit_new, o, lse,
+                                                 ws, BH, T, scale, s)
+                    : launch_decode_t<bf16, 64>(q, k_cache, v_cache, c_cache, logit_new, o, lse,
+                                                ws, BH, T, scale, s);
+  }
+  return d == 128 ? launch_decode_t<float, 128>(q, k_cache, v_cache, c_cache, logit_new, o, lse,
+                                                ws, BH, T, scale, s)
+                  : launch_decode_t<float, 64>(q, k_cache, v_cache, c_cache, logit_new, o, lse,
+                                               ws, BH, T, scale, s);
+}
+
+}  // namespace fox

@@ -1,0 +1,348 @@
+// Forgetting Attention forward pass (appendix, Alg. 1): O = softmax(s Q K^T + D) V
+// with D_ij = c_i - c_j (j <= i), plus the natural-log row logsumexp.
+//
+// bf16 kernel (MFMA, gfx950)
+//   * A workgroup owns 128 query rows of one (batch, head): four waves of 32 rows.
+//     Key/value tiles of 64 rows stream through LDS; the next tile is fetched into
+//     registers while the current one is being used.
+//   * Each wave computes S^T = K Q^T (keys on MFMA rows, its 32 queries on
+//     columns), so every lane owns one query: the softmax statistics are per lane
+//     and only the two half-waves holding the same query exchange values.
+//   * The forget-gate bias is applied in registers as it is in the paper (D is
+//     never materialised), but in base 2 and relative to c_ref, the prefix value of
+//     the block's first query: u_ij = s log2(e) q_i.k_j - log2(e) (c_j - c_ref).
+//     The per-row term c_i shifts a whole softmax row and cancels, so it only
+//     enters the logsumexp: LSE_i = (c_i - c_ref) + ln2 (m_i + log2 l_i).  Keeping
+//     the c differences small keeps them exact in fp32 even where |c| is 1e4-1e5.
+//   * P^T (accumulator layout) is reused directly as the B operand of
+//     O^T += V^T P^T; V is written transposed into LDS so that its A-operand
+//     fragments are two 8-byte reads.  Keys are consumed in the order the
+//     accumulator layout holds them, which is a permutation of the contraction
+//     index applied identically to both operands.
+//   * Causal structure: key tiles after a wave's last query are skipped; only
+//     tiles that straddle the diagonal apply the mask.  Query blocks are
+//     dispatched longest-first (workgroup ids map heads fastest).
+//
+// fp32 kernel: a straightforward vector-ALU kernel (D/32 lanes per query row,
+// keys staged through LDS 32 at a time).  It favours accuracy over speed: the
+// bias c_i - c_j is formed in natural-log units before the change to base 2, so
+// the row maximum stays small and the logsumexp carries no cancellation even
+// when c changes by thousands within a block.
+#include "fox_device.h"
+#include "fox_internal.h"
+
+namespace fox {
+
+constexpr int kFwdWaves = 4;
+constexpr int kFwdThreads = 64 * kFwdWaves;
+constexpr int kFwdBM = 32 * kFwdWaves;  // query rows per workgroup
+constexpr int kFwdBN = 64;              // keys per tile
+
+template <int D>
+struct alignas(16) FwdTile {
+  static constexpr int KS = D + 8;       // K row stride in LDS (16-byte pad)
+  static constexpr int VS = kFwdBN + 4;  // V^T row stride in LDS
+  static constexpr int KCH = kFwdBN * D / 8 / kFwdThreads;  // 16-byte K chunks per thread
+  static constexpr int KPT = KCH;                            // keys per thread for V^T
+  bf16 k[kFwdBN * KS];
+  bf16 vt[D * VS];
+  float ck[kFwdBN];
+};
+
+template <int D>
+__global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
+    const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
+    const float* __restrict__ C, bf16* __restrict__ O, float* __restrict__ LSE, int BH, int L,
+    int n_mblk, float scale_log2) {
+  using T = FwdTile<D>;
+  __shared__ T sm;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int h = lane >> 5, col = lane & 31;
+  const int bh = blockIdx.x % BH;
+  const int mblk = n_mblk - 1 - (int)(blockIdx.x / BH);
+  const int q0 = mblk * kFwdBM;
+  const size_t head = (size_t)bh * (size_t)L;
+  const bf16* Qh = Q + head * D;
+  const bf16* Kh = K + head * D;
+  const bf16* Vh = V + head * D;
+  const float* Ch = C + head;
+  const float c_ref = Ch[q0];
+  const int qw0 = q0 + wave * 32;
+  const int qi = qw0 + col;
+  const bool q_valid = qi < L;
+
+  bf16x8 qf[D / 16];
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s) {
+    if (q_valid) {
+      qf[s] = *reinterpret_cast<const bf16x8*>(Qh + (size_t)qi * D + 16 * s + 8 * h);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qf[s][e] = to_bf16(0.0f);
+    }
+  }
+
+  f32x16 oacc[D / 32];
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[db][r] = 0.0f;
+  float m_run = -INFINITY, l_run = 0.0f;
+
+  const int kend = min(L, q0 + kFwdBM);
+  const int n_kt = (kend + kFwdBN - 1) / kFwdBN;
+
+  bf16x8 kreg[T::KCH], vreg[T::KPT];
+  float creg = 0.0f;
+  const int vdg = tid % (D / 8), vkg = tid / (D / 8);
+
+  auto load_tile = [&](int kt) {
+    const int key0 = kt * kFwdBN;
+#pragma unroll
+    for (int i = 0; i < T::KCH; ++i) {
+      const int chunk = tid + kFwdThreads * i;
+      const int row = chunk / (D / 8), c8 = chunk % (D / 8);
+      const int key = key0 + row;
+      if (key < L) {
+        kreg[i] = *reinterpret_cast<const bf16x8*>(Kh + (size_t)key * D + c8 * 8);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) kreg[i][e] = to_bf16(0.0f);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < T::KPT; ++r) {
+      const int key = key0 + vkg * T::KPT + r;
+      if (key < L) {
+        vreg[r] = *reinterpret_cast<const bf16x8*>(Vh + (size_t)key * D + vdg * 8);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) vreg[r][e] = to_bf16(0.0f);
+      }
+    }
+    if (tid < kFwdBN) {
+      const int key = key0 + tid;
+      creg = key < L ? (Ch[key] - c_ref) * kLog2e : INFINITY;
+    }
+  };
+
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int i = 0; i < T::KCH; ++i) {
+      const int chunk = tid + kFwdThreads * i;
+      const int row = chunk / (D / 8), c8 = chunk % (D / 8);
+      *reinterpret_cast<bf16x8*>(&sm.k[row * T::KS + c8 * 8]) = kreg[i];
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      bf16* dst = &sm.vt[(vdg * 8 + e) * T::VS + vkg * T::KPT];
+      if constexpr (T::KPT == 4) {
+        bf16x4 w = {vreg[0][e], vreg[1][e], vreg[2][e], vreg[3][e]};
+        *reinterpret_cast<bf16x4*>(dst) = w;
+      } else {
+        bf16x2 w = {vreg[0][e], vreg[1][e]};
+        *reinterpret_cast<bf16x2*>(dst) = w;
+      }
+    }
+    if (tid < kFwdBN) sm.ck[tid] = creg;
+  };
+
+  load_tile(0);
+  for (int kt = 0; kt < n_kt; ++kt) {
+    __syncthreads();
+    store_tile();
+    __syncthreads();
+    if (kt + 1 < n_kt) load_tile(kt + 1);
+    const int key0 = kt * kFwdBN;
+    if (key0 > qw0 + 31) continue;  // the whole tile lies after this wave's queries
+    const bool diag = key0 + kFwdBN - 1 > qw0;
+
+    float u[32];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      f32x16 acc;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
+#pragma unroll
+      for (int s = 0; s < D / 16; ++s) {
+        const bf16x8 a =
+            *reinterpret_cast<const bf16x8*>(&sm.k[(kb * 32 + col) * T::KS + 16 * s + 8 * h]);
+        acc = mfma32(a, qf[s], acc);
+      }
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int kl = kb * 32 + 8 * g + 4 * h;
+        const f32x4 ck4 = *reinterpret_cast<const f32x4*>(&sm.ck[kl]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          float x = acc[4 * g + j] * scale_log2 - ck4[j];
+          if (diag && key0 + kl + j > qi) x = -INFINITY;
+          u[kb * 16 + 4 * g + j] = x;
+        }
+      }
+    }
+    float mt = u[0];
+#pragma unroll
+    for (int r = 1; r < 32; ++r) mt = fmaxf(mt, u[r]);
+    mt = wave_max_pair(mt);
+    const float m_new = fmaxf(m_run, mt);
+    const float alpha = exp2_fast(m_run - m_new);
+    float psum = 0.0f;
+#pragma unroll
+    for (int r = 0; r < 32; ++r) {
+      u[r] = exp2_fast(u[r] - m_new);
+      psum += u[r];
+    }
+    l_run = l_run * alpha + psum;
+    m_run = m_new;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) oacc[db] *= alpha;
+
+    bf16x8 pb[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) pb[c] = pack8(&u[8 * c]);
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const bf16* vrow = &sm.vt[(db * 32 + col) * T::VS + 16 * c + 4 * h];
+        const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow);
+        const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 8);
+        const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        oacc[db] = mfma32(a, pb[c], oacc[db]);
+      }
+    }
+  }
+
+  const float l_tot = wave_sum_pair(l_run);
+  if (q_valid) {
+    const float inv = 1.0f / l_tot;
+    bf16* orow = O + (head + (size_t)qi) * D;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        bf16x4 w;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) w[j] = to_bf16(oacc[db][4 * g + j] * inv);
+        *reinterpret_cast<bf16x4*>(orow + db * 32 + 8 * g + 4 * h) = w;
+      }
+    }
+    if (h == 0) LSE[head + qi] = (Ch[qi] - c_ref) + kLn2 * (m_run + log2f(l_tot));
+  }
+}
+
+// ---------------------------------------------------------------------------
+// fp32 forward: G = D/32 lanes per query row, each lane owning 32 head dims.
+// ---------------------------------------------------------------------------
+constexpr int kF32Threads = 256;
+constexpr int kF32BN = 32;
+
+template <int D>
+__global__ __launch_bounds__(kF32Threads) void fwd_f32_kernel(
+    const float* __restrict__ Q, const float* __restrict__ K, const float* __restrict__ V,
+    const float* __restrict__ C, float* __restrict__ O, float* __restrict__ LSE, int L,
+    int n_blk, float scale_log2) {
+  constexpr int G = D / 32;
+  constexpr int RPW = kF32Threads / G;  // query rows per workgroup
+  __shared__ float ks[kF32BN][D + 1];
+  __shared__ float vs[kF32BN][D + 1];
+  __shared__ float cks[kF32BN];
+  const int tid = threadIdx.x;
+  const int sub = tid % G;
+  const size_t head = (size_t)(blockIdx.x / n_blk) * (size_t)L;
+  const int q0 = (int)(blockIdx.x % n_blk) * RPW;
+  const int qi = q0 + tid / G;
+  const bool q_valid = qi < L;
+  const float* Ch = C + head;
+  const float c_ref = Ch[q0];
+  const float cq = q_valid ? Ch[qi] - c_ref : 0.0f;
+  float qv[32], ov[32];
+#pragma unroll
+  for (int e = 0; e < 32; ++e) {
+    qv[e] = q_valid ? Q[(head + qi) * D + sub * 32 + e] : 0.0f;
+    ov[e] = 0.0f;
+  }
+  float m_run = -INFINITY, l_run = 0.0f;
+  const int kend = min(L, q0 + RPW);
+  for (int key0 = 0; key0 < kend; key0 += kF32BN) {
+    __syncthreads();
+    for (int i = tid; i < kF32BN * D; i += kF32Threads) {
+      const int r = i / D, e = i % D, key = key0 + r;
+      ks[r][e] = key < L ? K[(head + key) * D + e] : 0.0f;
+      vs[r][e] = key < L ? V[(head + key) * D + e] : 0.0f;
+    }
+    if (tid < kF32BN) {
+      const int key = key0 + tid;
+      cks[tid] = key < L ? Ch[key] - c_ref : INFINITY;
+    }
+    __syncthreads();
+    float sc[kF32BN];
+    float mt = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < kF32BN; ++j) {
+      float part = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 32; ++e) part += qv[e] * ks[j][sub * 32 + e];
+#pragma unroll
+      for (int off = 1; off < G; off <<= 1) part += __shfl_xor(part, off);
+      float x = part * scale_log2 + (cq - cks[j]) * kLog2e;
+      if (key0 + j > qi) x = -INFINITY;
+      sc[j] = x;
+      mt = fmaxf(mt, x);
+    }
+    // Key 0 lies in the first tile and is never masked, so m_new is finite.
+    const float m_new = fmaxf(m_run, mt);
+    const float alpha = exp2_fast(m_run - m_new);
+    l_run *= alpha;
+#pragma unroll
+    for (int e = 0; e < 32; ++e) ov[e] *= alpha;
+#pragma unroll
+    for (int j = 0; j < kF32BN; ++j) {
+      const float p = exp2_fast(sc[j] - m_new);
+      l_run += p;
+#pragma unroll
+      for (int e = 0; e < 32; ++e) ov[e] += p * vs[j][sub * 32 + e];
+    }
+    m_run = m_new;
+  }
+  if (q_valid) {
+    const float inv = 1.0f / l_run;
+#pragma unroll
+    for (int e = 0; e < 32; ++e) O[(head + qi) * D + sub * 32 + e] = ov[e] * inv;
+    if (sub == 0) LSE[head + qi] = kLn2 * (m_run + log2f(l_run));
+  }
+}
+
+hipError_t launch_fwd_bf16(const void* q, const void* k, const void* v, const float* c, void* o,
+                           float* lse, int BH, int L, int d, float scale, hipStream_t s) {
+  const int n_mblk = (L + kFwdBM - 1) / kFwdBM;
+  const dim3 grid((unsigned)n_mblk * (unsigned)BH);
+  const float sl2 = scale * kLog2e;
+  if (d == 128) {
+    hipLaunchKernelGGL(fwd_bf16_kernel<128>, grid, dim3(kFwdThreads), 0, s, (const bf16*)q,
+                       (const bf16*)k, (const bf16*)v, c, (bf16*)o, lse, BH, L, n_mblk, sl2);
+  } else {
+    hipLaunchKernelGGL(fwd_bf16_kernel<64>, grid, dim3(kFwdThreads), 0, s, (const bf16*)q,
+                       (const bf16*)k, (const bf16*)v, c, (bf16*)o, lse, BH, L, n_mblk, sl2);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_fwd_f32(const float* q, const float* k, const float* v, const float* c, float* o,
+                          float* lse, int BH, int L, int d, float scale, hipStream_t s) {
+  const float sl2 = scale * kLog2e;
+  const int rpw = kF32Threads / (d / 32);
+  const int n_blk = (L + rpw - 1) / rpw;
+  const dim3 grid((unsigned)n_blk * (unsigned)BH);
+  if (d == 128) {
+    hipLaunchKernelGGL(fwd_f32_kernel<128>, grid, dim3(kF32Threads), 0, s, q, k, v, c, o, lse, L,
+                       n_blk, sl2);
+  } else {
+    hipLaunchKernelGGL(fwd_f32_kernel<64>, grid, dim3(kF32Threads), 0, s, q, k, v, c, o, lse, L,
+                       n_blk, sl2);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace fox

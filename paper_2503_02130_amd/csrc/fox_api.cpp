@@ -1,0 +1,138 @@
+// C ABI of the Forgetting Attention library: argument validation on the host,
+// then kernel launches on the caller's stream.  Nothing here allocates device
+// memory or synchronises.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "fox.h"
+#include "fox_internal.h"
+
+namespace {
+
+constexpr long long kMaxElems = 1LL << 40;        // per tensor
+constexpr long long kMaxWorkgroups = 1LL << 22;   // 256-thread workgroups per launch
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int check_dims(int B, int H, int L, int d) {
+  if (B <= 0 || H <= 0 || L <= 0 || d <= 0) return FOX_ERR_SHAPE;
+  const long long bh = (long long)B * H;
+  if (bh > (1LL << 30)) return FOX_ERR_SHAPE;
+  if (bh * L > (1LL << 31) - 1) return FOX_ERR_SHAPE;          // row index fits in int
+  if (bh * L * d > kMaxElems) return FOX_ERR_SHAPE;
+  if (bh * ((L + 63) / 64) > kMaxWorkgroups) return FOX_ERR_SHAPE;
+  return FOX_OK;
+}
+
+int check_dtype_d(int dtype, int d) {
+  if (dtype != FOX_DTYPE_F32 && dtype != FOX_DTYPE_BF16) return FOX_ERR_UNSUPPORTED;
+  if (d != 64 && d != 128) return FOX_ERR_UNSUPPORTED;
+  return FOX_OK;
+}
+
+int launch_status(hipError_t e) { return e == hipSuccess ? FOX_OK : FOX_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+const char* fox_status_string(int status) {
+  switch (status) {
+    case FOX_OK: return "FOX_OK";
+    case FOX_ERR_NULL: return "FOX_ERR_NULL: a required pointer is NULL";
+    case FOX_ERR_SHAPE: return "FOX_ERR_SHAPE: sizes must be positive and within limits";
+    case FOX_ERR_UNSUPPORTED: return "FOX_ERR_UNSUPPORTED: dtype must be f32/bf16, head dim 64/128";
+    case FOX_ERR_ALIGN: return "FOX_ERR_ALIGN: device pointers must be 16-byte aligned";
+    case FOX_ERR_WORKSPACE: return "FOX_ERR_WORKSPACE: workspace missing or too small";
+    case FOX_ERR_HIP: return "FOX_ERR_HIP: the HIP runtime reported a launch error";
+    default: return "unknown fox status";
+  }
+}
+
+int fox_version(void) { return 100; }
+
+int fox_gate_prefix(const float* gate_logit, float* log_f, float* c, int B, int H, int L,
+                    void* stream) {
+  if (!gate_logit || !c) return FOX_ERR_NULL;
+  int st = check_dims(B, H, L, 1);
+  if (st) return st;
+  if (!aligned16(gate_logit) || !aligned16(c) || (log_f && !aligned16(log_f))) return FOX_ERR_ALIGN;
+  return launch_status(fox::launch_gate_prefix(gate_logit, log_f, c, B * H, L,
+                                               static_cast<hipStream_t>(stream)));
+}
+
+int fox_attn_fwd(int dtype, const void* q, const void* k, const void* v, const float* c, void* o,
+                 float* lse, int B, int H, int L, int d, float scale, void* stream) {
+  if (!q || !k || !v || !c || !o || !lse) return FOX_ERR_NULL;
+  int st = check_dims(B, H, L, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(c) || !aligned16(o) ||
+      !aligned16(lse))
+    return FOX_ERR_ALIGN;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (dtype == FOX_DTYPE_BF16)
+    return launch_status(fox::launch_fwd_bf16(q, k, v, c, o, lse, B * H, L, d, scale, s));
+  return launch_status(fox::launch_fwd_f32((const float*)q, (const float*)k, (const float*)v, c,
+                                           (float*)o, lse, B * H, L, d, scale, s));
+}
+
+size_t fox_attn_bwd_workspace_bytes(int dtype, int B, int H, int L, int d) {
+  if (check_dims(B, H, L, d) || check_dtype_d(dtype, d)) return 0;
+  return fox::bwd_workspace_bytes(B * H, L);
+}
+
+int fox_attn_bwd(int dtype, const void* q, const void* k, const void* v, const float* c,
+                 const void* o, const float* lse, const void* d_o, void* dq, void* dk, void* dv,
+                 float* d_log_f, void* workspace, size_t workspace_bytes, int B, int H, int L,
+                 int d, float scale, void* stream) {
+  if (!q || !k || !v || !c || !o || !lse || !d_o || !dq || !dk || !dv || !d_log_f)
+    return FOX_ERR_NULL;
+  int st = check_dims(B, H, L, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(c) || !aligned16(o) ||
+      !aligned16(lse) || !aligned16(d_o) || !aligned16(dq) || !aligned16(dk) || !aligned16(dv) ||
+      !aligned16(d_log_f))
+    return FOX_ERR_ALIGN;
+  if (!workspace || workspace_bytes < fox::bwd_workspace_bytes(B * H, L)) return FOX_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return FOX_ERR_ALIGN;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (dtype == FOX_DTYPE_BF16)
+    return launch_status(fox::launch_bwd_bf16(q, k, v, c, o, lse, d_o, dq, dk, dv, d_log_f,
+                                              workspace, B * H, L, d, scale, s));
+  return launch_status(fox::launch_bwd_f32(
+      (const float*)q, (const float*)k, (const float*)v, c, (const float*)o, lse,
+      (const float*)d_o, (float*)dq, (float*)dk, (float*)dv, d_log_f, workspace, B * H, L, d,
+      scale, s));
+}
+
+size_t fox_attn_decode_workspace_bytes(int dtype, int B, int H, int T, int d) {
+  if (check_dims(B, H, T, d) || check_dtype_d(dtype, d)) return 0;
+  return fox::decode_workspace_bytes(B * H, T, d);
+}
+
+int fox_attn_decode(int dtype, const void* q, const void* k_cache, const void* v_cache,
+                    float* c_cache, const float* gate_logit_new, void* o, float* lse,
+                    void* workspace, size_t workspace_bytes, int B, int H, int T, int d,
+                    float scale, void* stream) {
+  if (!q || !k_cache || !v_cache || !c_cache || !gate_logit_new || !o || !lse)
+    return FOX_ERR_NULL;
+  int st = check_dims(B, H, T, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(c_cache) ||
+      !aligned16(gate_logit_new) || !aligned16(o) || !aligned16(lse))
+    return FOX_ERR_ALIGN;
+  if (!workspace || workspace_bytes < fox::decode_workspace_bytes(B * H, T, d))
+    return FOX_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return FOX_ERR_ALIGN;
+  return launch_status(fox::launch_decode(dtype == FOX_DTYPE_BF16, q, k_cache, v_cache, c_cache,
+                                          gate_logit_new, o, lse, workspace, B * H, T, d, scale,
+                                          static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,61 @@
+// Device-side helpers shared by the Forgetting Attention kernels (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+namespace fox {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// 2^x on the transcendental unit (v_exp_f32); exp2(-inf) = 0.
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// One 32x32x16 bf16 MFMA: C[32x32] += A[32x16] * B[16x32], fp32 accumulation.
+//
+// Operand layout (wave64, lane l, h = l / 32): lane l supplies row (l % 32) of A
+// and column (l % 32) of B, eight contraction elements each; lanes h = 0 and
+// h = 1 supply complementary halves of the 16-element contraction.  Both
+// operands use the same element-to-k assignment, so any consistent permutation
+// of the contraction index gives the same product.
+//
+// Result layout: lane l holds column (l % 32) of C; its register r holds row
+//     row(r, h) = 8 * (r / 4) + 4 * h + (r % 4),   r = 0..15.
+__device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ int mfma_row(int r, int h) { return 8 * (r >> 2) + 4 * h + (r & 3); }
+
+// Round-to-nearest-even fp32 -> bf16 (the hardware conversion on gfx950).
+__device__ __forceinline__ bf16 to_bf16(float x) { return (bf16)x; }
+__device__ __forceinline__ float to_f32(bf16 x) { return (float)x; }
+
+// Eight consecutive accumulator registers (starting at r0) packed to bf16 as one
+// MFMA operand: register r0+i becomes element i.
+__device__ __forceinline__ bf16x8 pack8(const float* p) {
+  bf16x8 r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) r[i] = to_bf16(p[i]);
+  return r;
+}
+
+__device__ __forceinline__ float wave_max_pair(float x) {  // lanes l and l ^ 32
+  return fmaxf(x, __shfl_xor(x, 32));
+}
+__device__ __forceinline__ float wave_sum_pair(float x) { return x + __shfl_xor(x, 32); }
+
+// log sigmoid(x) = min(x, 0) - log1p(exp(-|x|)), overflow-free for any finite x.
+__device__ __forceinline__ float log_sigmoid(float x) {
+  return fminf(x, 0.0f) - log1pf(expf(-fabsf(x)));
+}
+
+}  // namespace fox

@@ -1,0 +1,38 @@
+// Host-side launchers shared between the C ABI and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+
+namespace fox {
+
+// Inclusive prefix sums over rows of length L (one workgroup per row).
+hipError_t launch_gate_prefix(const float* logit, float* log_f, float* c, int rows, int L,
+                              hipStream_t s);
+// out_l = sum_{i>=l} (a_i + b_i) per row: the chain rule through c = cumsum(log f).
+hipError_t launch_reverse_scan_sum(const float* a, const float* b, float* out, int rows, int L,
+                                   hipStream_t s);
+
+hipError_t launch_fwd_bf16(const void* q, const void* k, const void* v, const float* c, void* o,
+                           float* lse, int BH, int L, int d, float scale, hipStream_t s);
+hipError_t launch_fwd_f32(const float* q, const float* k, const float* v, const float* c, float* o,
+                          float* lse, int BH, int L, int d, float scale, hipStream_t s);
+
+// Workspace layout of the backward: delta, dc_q, dc_k, each [BH, L] fp32.
+size_t bwd_workspace_bytes(int BH, int L);
+hipError_t launch_bwd_bf16(const void* q, const void* k, const void* v, const float* c,
+                           const void* o, const float* lse, const void* d_o, void* dq, void* dk,
+                           void* dv, float* d_log_f, void* ws, int BH, int L, int d, float scale,
+                           hipStream_t s);
+hipError_t launch_bwd_f32(const float* q, const float* k, const float* v, const float* c,
+                          const float* o, const float* lse, const float* d_o, float* dq, float* dk,
+                          float* dv, float* d_log_f, void* ws, int BH, int L, int d, float scale,
+                          hipStream_t s);
+
+int decode_num_splits(int BH, int T);
+size_t decode_workspace_bytes(int BH, int T, int d);
+hipError_t launch_decode(bool bf16, const void* q, const void* k_cache, const void* v_cache,
+                         float* c_cache, const float* logit_new, void* o, float* lse, void* ws,
+                         int BH, int T, int d, float scale, hipStream_t s);
+
+}  // namespace fox

@@ -1,0 +1,112 @@
+"""The C ABI on the host: the library loads, exports every declared entry point,
+and rejects bad arguments before touching the GPU (no device needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+import torch
+
+import paper_2503_02130_amd as fox
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fox.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(fox.LIB_PATH):
+        from paper_2503_02130_amd import build
+        build.build()
+    return fox.load()
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fox_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_symbols()
+    for n in ("fox_gate_prefix", "fox_attn_fwd", "fox_attn_bwd", "fox_attn_decode",
+              "fox_attn_bwd_workspace_bytes", "fox_attn_decode_workspace_bytes",
+              "fox_status_string", "fox_version"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for n in declared_symbols():
+        assert hasattr(lib, n), f"{n} is declared in fox.h but not exported"
+    assert set(fox.EXPORTED) == set(declared_symbols())
+
+
+def test_status_strings(lib):
+    for code in range(7):
+        assert lib.fox_status_string(code)
+    assert b"unknown" in lib.fox_status_string(99)
+    assert lib.fox_version() >= 100
+
+
+P16 = 0x10000  # a 16-byte aligned fake address: never dereferenced by these calls
+
+
+def _fwd(lib, dtype=1, ptrs=(P16,) * 6, B=1, H=1, L=8, d=64):
+    return lib.fox_attn_fwd(dtype, *[ctypes.c_void_p(p) if p else None for p in ptrs],
+                            B, H, L, d, ctypes.c_float(0.125), None)
+
+
+def test_fwd_validation(lib):
+    assert _fwd(lib, ptrs=(0,) + (P16,) * 5) == 1                      # NULL
+    assert _fwd(lib, B=0) == 2 and _fwd(lib, L=-3) == 2                # shape
+    assert _fwd(lib, B=1 << 20, H=1 << 12, L=1 << 16) == 2             # overflow
+    assert _fwd(lib, d=96) == 3 and _fwd(lib, dtype=5) == 3            # unsupported
+    assert _fwd(lib, ptrs=(P16 + 2,) + (P16,) * 5) == 4                # alignment
+
+
+def test_gate_prefix_validation(lib):
+    c = ctypes.c_void_p
+    assert lib.fox_gate_prefix(None, None, c(P16), 1, 1, 4, None) == 1
+    assert lib.fox_gate_prefix(c(P16), None, c(P16), 1, 0, 4, None) == 2
+    assert lib.fox_gate_prefix(c(P16), c(P16 + 4), c(P16), 1, 1, 4, None) == 4
+
+
+def test_bwd_validation_and_workspace(lib):
+    c = ctypes.c_void_p
+    B, H, L, d = 2, 3, 100, 128
+    need = lib.fox_attn_bwd_workspace_bytes(1, B, H, L, d)
+    assert need == 3 * 4 * B * H * L
+    assert lib.fox_attn_bwd_workspace_bytes(1, B, H, L, 80) == 0
+    args = [c(P16)] * 11
+    assert lib.fox_attn_bwd(1, *args, c(P16), need - 1, B, H, L, d, ctypes.c_float(0.1), None) == 5
+    assert lib.fox_attn_bwd(1, *args, None, need, B, H, L, d, ctypes.c_float(0.1), None) == 5
+    assert lib.fox_attn_bwd(1, *args[:-1], None, c(P16), need, B, H, L, d,
+                            ctypes.c_float(0.1), None) == 1
+
+
+def test_decode_validation_and_workspace(lib):
+    c = ctypes.c_void_p
+    need = lib.fox_attn_decode_workspace_bytes(1, 64, 16, 32768, 128)
+    assert need > 0 and need % (4 * 130) == 0
+    assert lib.fox_attn_decode_workspace_bytes(1, 64, 16, 32768, 32) == 0
+    args = [c(P16)] * 7
+    assert lib.fox_attn_decode(1, *args, c(P16), need - 4, 64, 16, 32768, 128,
+                               ctypes.c_float(0.1), None) == 5
+    assert lib.fox_attn_decode(1, *args, c(P16), need, 64, 16, 0, 128,
+                               ctypes.c_float(0.1), None) == 2
+
+
+def test_binding_refuses_host_tensors(lib):
+    """There is no CPU path: host tensors are rejected before any call."""
+    x = torch.zeros(1, 1, 8)
+    with pytest.raises(ValueError):
+        fox.fox_gate_prefix(x)
+    q = torch.zeros(1, 1, 8, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        fox.fox_attn_fwd(q, q, q, x)
+
+
+def test_single_hip_runtime(lib):
+    """libfox.so binds to the HIP runtime torch already loaded (one copy)."""
+    maps = [l.split()[-1] for l in open("/proc/self/maps") if "libamdhip64" in l]
+    assert len(set(maps)) == 1, set(maps)

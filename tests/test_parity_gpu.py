@@ -1,0 +1,319 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 oracle.
+
+Tolerances (from the operator's specification):
+  * fp32: max-abs <= 1e-4 on O (and on LSE);
+  * bf16: relative L2 <= 1e-2 on O, <= 2e-2 on dQ, dK, dV and d(log f);
+    LSE max-abs <= 1e-2 (bf16 inputs and fp32 accumulation);
+  * gate prefix (fp32): log f within 2e-6 absolute, c within a few fp32 ulps of
+    the largest |c| of its row times log2(L).
+Small shapes cover ragged tails (lengths that are not multiples of any tile),
+L = 1, both head dims and both dtypes; the full-size workloads run in the same
+launch configuration as the benchmark and are compared on sampled heads / rows
+that the oracle computes exactly.
+"""
+import math
+import os
+
+import pytest
+import torch
+
+import oracle
+import paper_2503_02130_amd as fox
+from paper_2503_02130_amd import inputs
+
+pytestmark = pytest.mark.gpu
+torch.set_num_threads(max(1, min(16, len(os.sched_getaffinity(0)))))
+DEV = "cuda:0"
+
+
+def rel_l2(a, b) -> float:
+    a = a.detach().double().cpu()
+    b = b.detach().double().cpu()
+    den = float(torch.linalg.vector_norm(b))
+    return float(torch.linalg.vector_norm(a - b)) / max(den, 1e-300)
+
+
+def max_abs(a, b) -> float:
+    return float((a.detach().double().cpu() - b.detach().double().cpu()).abs().max())
+
+
+def gpu_forward(x, s):
+    c = fox.fox_gate_prefix(x["logit"])
+    o, lse = fox.fox_attn_fwd(x["q"], x["k"], x["v"], c, s)
+    return c, o, lse
+
+
+def cpu(x):
+    return {k: v.cpu() for k, v in x.items()}
+
+
+def check_fwd(dtype, o, lse, O, LSE, what=""):
+    if dtype == "f32":
+        assert max_abs(o, O) <= 1e-4, f"{what} O max-abs {max_abs(o, O):.3e}"
+        assert max_abs(lse, LSE) <= 1e-4, f"{what} LSE max-abs {max_abs(lse, LSE):.3e}"
+    else:
+        assert rel_l2(o, O) <= 1e-2, f"{what} O rel-L2 {rel_l2(o, O):.3e}"
+        assert max_abs(lse, LSE) <= 1e-2, f"{what} LSE max-abs {max_abs(lse, LSE):.3e}"
+
+
+def check_bwd(dtype, got, ref, what=""):
+    """Relative L2 per gradient.  Where the exact gradient vanishes identically
+    (dQ = dK = d(log f) = 0 at L = 1) a relative error is undefined, and the
+    rounding residue is bounded absolutely instead."""
+    lim = 1e-4 if dtype == "f32" else 2e-2
+    lim_abs = 1e-5 if dtype == "f32" else 1e-3
+    for name, g, r in zip(("dQ", "dK", "dV", "dlogf"), got, ref):
+        r64 = r.detach().double().cpu()
+        if float(torch.linalg.vector_norm(r64)) <= 1e-9 * math.sqrt(r64.numel()):
+            e = max_abs(g, r64)
+            assert e <= lim_abs, f"{what} {name} (exactly zero) max-abs {e:.3e} > {lim_abs}"
+            continue
+        e = rel_l2(g, r)
+        assert e <= lim, f"{what} {name} rel-L2 {e:.3e} > {lim}"
+
+
+@pytest.fixture(autouse=True)
+def _free_memory():
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+# --------------------------------------------------------------------- prelude
+@pytest.mark.parametrize("L", [1, 2, 3, 17, 2047, 2048, 2049, 65536])
+def test_gate_prefix(L):
+    print(f"gate_prefix L={L}", flush=True)
+    g = torch.Generator(device=DEV).manual_seed(L)
+    x = torch.randn(3, 2, L, generator=g, device=DEV) * 2.0 + torch.tensor(
+        [-2.0, 1.0, 6.0], device=DEV)[:, None, None]
+    c, lf = fox.fox_gate_prefix(x, want_log_f=True)
+    torch.cuda.synchronize()
+    lf_ref, c_ref = oracle.gate_prefix(x.cpu())
+    assert max_abs(lf, lf_ref) <= 2e-6
+    tol = 4 * 2.0 ** -23 * float(c_ref.abs().max()) * max(1.0, math.log2(L)) + 1e-5
+    assert max_abs(c, c_ref) <= tol, (max_abs(c, c_ref), tol)
+
+
+# ------------------------------------------------------------ small forward
+FWD_CASES = ([("f32", 64, L) for L in (1, 3, 64, 65, 200)] +
+             [("f32", 128, L) for L in (17, 130)] +
+             [("bf16", 64, L) for L in (1, 2, 17, 63, 64, 65, 127, 128, 129, 1000)] +
+             [("bf16", 128, L) for L in (1, 31, 129, 333, 1000)])
+
+
+@pytest.mark.parametrize("dtype,d,L", FWD_CASES)
+def test_forward_small(dtype, d, L):
+    print(f"forward dtype={dtype} d={d} L={L}", flush=True)
+    x = inputs.attn_inputs(2, 3, L, d, dtype, ("normal", 2.0, 1.0), 100 + L, device=DEV, grad=False)
+    s = fox.default_scale(d)
+    _, o, lse = gpu_forward(x, s)
+    torch.cuda.synchronize()
+    xc = cpu(x)
+    O, LSE = oracle.forward(xc["q"], xc["k"], xc["v"], xc["logit"], s)
+    check_fwd(dtype, o, lse, O, LSE, f"L={L}")
+
+
+GATES = {
+    "strong": ("normal", -2.0, 1.0),      # log f ~ -2: very local attention
+    "none": ("constant", 30.0),           # log f ~ -1e-13: plain causal softmax attention
+    "full": ("constant", -30.0),          # log f ~ -30: every row copies its own value
+    "mixed": ("split_heads", (6.0, 1.0), (0.0, 1.4142135623730951)),
+}
+
+
+@pytest.mark.parametrize("gate", sorted(GATES))
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_forward_gate_regimes(gate, dtype):
+    print(f"forward gate={gate} dtype={dtype}", flush=True)
+    x = inputs.attn_inputs(1, 4, 300, 128, dtype, GATES[gate], 7, device=DEV, grad=False)
+    s = fox.default_scale(128)
+    _, o, lse = gpu_forward(x, s)
+    torch.cuda.synchronize()
+    xc = cpu(x)
+    O, LSE = oracle.forward(xc["q"], xc["k"], xc["v"], xc["logit"], s)
+    check_fwd(dtype, o, lse, O, LSE, gate)
+    if gate == "full":
+        assert rel_l2(o, xc["v"]) <= (1e-6 if dtype == "f32" else 1e-2)
+
+
+# ----------------------------------------------------------- small backward
+BWD_CASES = ([("f32", 64, L) for L in (1, 5, 64, 100)] +
+             [("f32", 128, L) for L in (33, 130)] +
+             [("bf16", 64, L) for L in (1, 2, 17, 63, 64, 65, 127, 128, 129, 700)] +
+             [("bf16", 128, L) for L in (1, 31, 129, 333, 700)])
+
+
+@pytest.mark.parametrize("dtype,d,L", BWD_CASES)
+def test_backward_small(dtype, d, L):
+    print(f"backward dtype={dtype} d={d} L={L}", flush=True)
+    x = inputs.attn_inputs(2, 2, L, d, dtype, ("normal", 2.0, 1.0), 200 + L, device=DEV)
+    s = fox.default_scale(d)
+    c, o, lse = gpu_forward(x, s)
+    got = fox.fox_attn_bwd(x["q"], x["k"], x["v"], c, o, lse, x["do"], s)
+    torch.cuda.synchronize()
+    xc = cpu(x)
+    ref = oracle.backward(xc["q"], xc["k"], xc["v"], xc["logit"], xc["do"], s)
+    check_bwd(dtype, got, ref, f"L={L}")
+    assert float(got[3][..., 0].abs().max()) <= 1e-3 * max(1.0, float(ref[3].abs().max()))
+
+
+@pytest.mark.parametrize("gate", sorted(GATES))
+def test_backward_gate_regimes(gate):
+    print(f"backward gate={gate}", flush=True)
+    x = inputs.attn_inputs(1, 4, 260, 64, "bf16", GATES[gate], 11, device=DEV)
+    s = fox.default_scale(64)
+    c, o, lse = gpu_forward(x, s)
+    got = fox.fox_attn_bwd(x["q"], x["k"], x["v"], c, o, lse, x["do"], s)
+    torch.cuda.synchronize()
+    xc = cpu(x)
+    ref = oracle.backward(xc["q"], xc["k"], xc["v"], xc["logit"], xc["do"], s)
+    if gate == "full":
+        # dQ = dK = 0 and d(log f) ~ 0 exactly in the limit; compare absolutely
+        assert max_abs(got[0], ref[0]) <= 1e-3 and max_abs(got[1], ref[1]) <= 1e-3
+        assert rel_l2(got[2], ref[2]) <= 2e-2
+        assert max_abs(got[3], ref[3]) <= 1e-3
+    else:
+        check_bwd("bf16", got, ref, gate)
+
+
+def test_backward_is_deterministic():
+    x = inputs.attn_inputs(2, 2, 777, 128, "bf16", ("normal", 1.0, 1.0), 5, device=DEV)
+    s = fox.default_scale(128)
+    c, o, lse = gpu_forward(x, s)
+    a = fox.fox_attn_bwd(x["q"], x["k"], x["v"], c, o, lse, x["do"], s)
+    b = fox.fox_attn_bwd(x["q"], x["k"], x["v"], c, o, lse, x["do"], s)
+    torch.cuda.synchronize()
+    for u, w in zip(a, b):
+        assert torch.equal(u, w)
+
+
+# ------------------------------------------------------------------- decode
+@pytest.mark.parametrize("dtype,d,T", [("bf16", 128, 1), ("bf16", 128, 2), ("bf16", 128, 100),
+                                       ("bf16", 64, 1000), ("bf16", 128, 5000),
+                                       ("f32", 64, 77), ("f32", 128, 3000)])
+def test_decode_small(dtype, d, T):
+    print(f"decode dtype={dtype} d={d} T={T}", flush=True)
+    B, H = 3, 2
+    y = inputs.decode_inputs(B, H, T, d, dtype, ("normal", 3.0, 1.0), 300 + T, device=DEV)
+    cc = torch.full((B, H, T), float("nan"), device=DEV)
+    if T > 1:
+        cc[..., : T - 1] = fox.fox_gate_prefix(y["cached_logit"])
+    o, lse = fox.fox_attn_decode(y["q"], y["k_cache"], y["v_cache"], cc, y["logit_new"])
+    torch.cuda.synchronize()
+    yc = cpu(y)
+    o_ref, lse_ref, cT_ref = oracle.decode(yc["q"], yc["k_cache"], yc["v_cache"],
+                                           yc["cached_logit"], yc["logit_new"], fox.default_scale(d))
+    if dtype == "f32":
+        assert max_abs(o, o_ref) <= 1e-4 and max_abs(lse, lse_ref) <= 1e-4
+    else:
+        assert rel_l2(o, o_ref) <= 1e-2 and max_abs(lse, lse_ref) <= 1e-2
+    assert max_abs(cc[..., T - 1], cT_ref) <= 1e-5 * max(1.0, float(cT_ref.abs().max())) * 8
+
+
+def test_decode_equals_last_forward_row():
+    T, d = 1500, 128
+    x = inputs.attn_inputs(2, 2, T, d, "bf16", ("normal", 3.0, 1.0), 9, device=DEV, grad=False)
+    s = fox.default_scale(d)
+    c, o, lse = gpu_forward(x, s)
+    cc = c.clone()
+    cc[..., T - 1] = float("nan")
+    od, lsed = fox.fox_attn_decode(x["q"][:, :, T - 1].contiguous(), x["k"], x["v"], cc,
+                                   x["logit"][..., T - 1].contiguous(), s)
+    torch.cuda.synchronize()
+    assert rel_l2(od, o[:, :, T - 1]) <= 1e-2
+    assert max_abs(lsed, lse[..., T - 1]) <= 1e-3
+    assert max_abs(cc[..., T - 1], c[..., T - 1]) <= 1e-3
+
+
+# ------------------------------------------------------- full-size workloads
+W = inputs.WORKLOADS
+
+
+def test_workload_fwd_f32_b1_h2_l256_d64():
+    w = W["fwd_f32_b1_h2_l256_d64"]
+    x = inputs.workload_inputs(w, device=DEV)
+    s = fox.default_scale(w.d)
+    _, o, lse = gpu_forward(x, s)
+    torch.cuda.synchronize()
+    xc = cpu(x)
+    O, LSE = oracle.forward(xc["q"], xc["k"], xc["v"], xc["logit"], s)
+    check_fwd("f32", o, lse, O, LSE, w.name)
+
+
+def test_workload_fwdbwd_bf16_b8_h12_l2048_d64():
+    w = W["fwdbwd_bf16_b8_h12_l2048_d64"]
+    x = inputs.workload_inputs(w, device=DEV)
+    s = fox.default_scale(w.d)
+    c, o, lse = gpu_forward(x, s)
+    got = fox.fox_attn_bwd(x["q"], x["k"], x["v"], c, o, lse, x["do"], s)
+    torch.cuda.synchronize()
+    xc = cpu(x)
+    O, LSE = oracle.forward(xc["q"], xc["k"], xc["v"], xc["logit"], s)
+    check_fwd("bf16", o, lse, O, LSE, w.name)
+    ref = oracle.backward(xc["q"], xc["k"], xc["v"], xc["logit"], xc["do"], s)
+    check_bwd("bf16", [t.cpu() for t in got], ref, w.name)
+
+
+def _sampled_heads_by_gate(logit, n_each):
+    """Heads with the strongest and the weakest mean forgetting."""
+    mean_lf = oracle.log_sigmoid(logit.cpu()).mean(-1)          # [B, H]
+    order = torch.argsort(mean_lf.flatten())
+    H = logit.shape[1]
+    picks = list(order[:n_each]) + list(order[-n_each:])
+    return [(int(i) // H, int(i) % H) for i in picks]
+
+
+def test_workload_fwdbwd_bf16_b2_h16_l16384_d128():
+    w = W["fwdbwd_bf16_b2_h16_l16384_d128"]
+    x = inputs.workload_inputs(w, device=DEV)
+    s = fox.default_scale(w.d)
+    c, o, lse = gpu_forward(x, s)
+    dq, dk, dv, dlf = fox.fox_attn_bwd(x["q"], x["k"], x["v"], c, o, lse, x["do"], s)
+    torch.cuda.synchronize()
+    heads = _sampled_heads_by_gate(x["logit"], 1)
+    print(f"{w.name}: oracle on heads {heads}", flush=True)
+    for (b, h) in heads:
+        sl = {k: v[b:b + 1, h:h + 1].cpu() for k, v in x.items()}
+        O, LSE = oracle.forward(sl["q"], sl["k"], sl["v"], sl["logit"], s)
+        check_fwd("bf16", o[b:b + 1, h:h + 1], lse[b:b + 1, h:h + 1], O, LSE, f"head {(b, h)}")
+        ref = oracle.backward(sl["q"], sl["k"], sl["v"], sl["logit"], sl["do"], s)
+        got = [t[b:b + 1, h:h + 1] for t in (dq, dk, dv, dlf)]
+        check_bwd("bf16", got, ref, f"head {(b, h)}")
+        del O, LSE, ref
+
+
+def test_workload_fwd_bf16_b1_h16_l65536_d128():
+    w = W["fwd_bf16_b1_h16_l65536_d128"]
+    x = inputs.workload_inputs(w, device=DEV)
+    s = fox.default_scale(w.d)
+    c, o, lse = gpu_forward(x, s)
+    torch.cuda.synchronize()
+    L = w.L
+    g = torch.Generator().manual_seed(1)
+    rows = sorted(set([0, 1, 63, 64, 127, 128, L - 129, L - 2, L - 1] +
+                      torch.randint(0, L, (23,), generator=g).tolist()))
+    for h in (0, 5, 8, 15):                       # both gate groups
+        sl = {k: v[:, h:h + 1].cpu() for k, v in x.items()}
+        O, LSE = oracle.forward(sl["q"], sl["k"], sl["v"], sl["logit"], s, rows=rows)
+        check_fwd("bf16", o[:, h:h + 1, rows], lse[:, h:h + 1, rows], O, LSE, f"head {h}")
+
+
+def test_workload_decode_bf16_b64_h16_t32768_d128():
+    w = W["decode_bf16_b64_h16_t32768_d128"]
+    y = inputs.workload_inputs(w, device=DEV)
+    T = w.L
+    cc = torch.empty((w.B, w.H, T), device=DEV)
+    cc[..., : T - 1] = fox.fox_gate_prefix(y["cached_logit"])
+    o, lse = fox.fox_attn_decode(y["q"], y["k_cache"], y["v_cache"], cc, y["logit_new"])
+    torch.cuda.synchronize()
+    g = torch.Generator().manual_seed(2)
+    picks = [(0, 0), (w.B - 1, w.H - 1)] + [(int(torch.randint(0, w.B, (1,), generator=g)),
+                                             int(torch.randint(0, w.H, (1,), generator=g)))
+                                            for _ in range(6)]
+    for (b, h) in picks:
+        sl = {k: v[b:b + 1, h:h + 1].cpu() for k, v in y.items()}
+        o_ref, lse_ref, _ = oracle.decode(sl["q"], sl["k_cache"], sl["v_cache"],
+                                          sl["cached_logit"], sl["logit_new"],
+                                          fox.default_scale(w.d))
+        assert rel_l2(o[b:b + 1, h:h + 1], o_ref) <= 1e-2, (b, h)
+        assert max_abs(lse[b:b + 1, h:h + 1], lse_ref) <= 1e-2, (b, h)
