@@ -2,26 +2,34 @@
 // with D_ij = c_i - c_j (j <= i), plus the natural-log row logsumexp.
 //
 // bf16 kernel (MFMA, gfx950)
-//   * A workgroup owns 128 query rows of one (batch, head): four waves of 32 rows.
-//     Key/value tiles of 64 rows stream through LDS; the next tile is fetched into
-//     registers while the current one is being used.
+//   * A workgroup owns 128 query rows of one (batch, head): four waves of 32 rows,
+//     two workgroups per CU.  Key/value tiles of 64 rows are double-buffered in
+//     LDS and move there with buffer loads that write LDS directly (no registers,
+//     no VALU); out-of-range rows of a ragged last tile read as zero.  The next
+//     tile's loads are in flight while the current tile is used.
+//   * LDS rows are stored with an XOR swizzle of their 16-byte chunks so that the
+//     32 rows touched by one MFMA operand read fall in different banks.
 //   * Each wave computes S^T = K Q^T (keys on MFMA rows, its 32 queries on
 //     columns), so every lane owns one query: the softmax statistics are per lane
 //     and only the two half-waves holding the same query exchange values.
-//   * The forget-gate bias is applied in registers as it is in the paper (D is
-//     never materialised), but in base 2 and relative to c_ref, the prefix value of
-//     the block's first query: u_ij = s log2(e) q_i.k_j - log2(e) (c_j - c_ref).
-//     The per-row term c_i shifts a whole softmax row and cancels, so it only
-//     enters the logsumexp: LSE_i = (c_i - c_ref) + ln2 (m_i + log2 l_i).  Keeping
-//     the c differences small keeps them exact in fp32 even where |c| is 1e4-1e5.
-//   * P^T (accumulator layout) is reused directly as the B operand of
-//     O^T += V^T P^T; V is written transposed into LDS so that its A-operand
-//     fragments are two 8-byte reads.  Keys are consumed in the order the
-//     accumulator layout holds them, which is a permutation of the contraction
-//     index applied identically to both operands.
-//   * Causal structure: key tiles after a wave's last query are skipped; only
-//     tiles that straddle the diagonal apply the mask.  Query blocks are
-//     dispatched longest-first (workgroup ids map heads fastest).
+//   * The forget-gate bias is applied in registers, as in the paper (D is never
+//     materialised), in base 2 and relative to c_ref, the prefix value of the
+//     block's first query: u_ij = s log2(e) q_i.k_j - log2(e) (c_j - c_ref).  The
+//     row term c_i shifts a whole softmax row and cancels; it only enters the
+//     logsumexp: LSE_i = (c_i - c_ref) + ln2 (m_i + log2 l_i).  Keeping the c
+//     differences small keeps them exact in fp32 even where |c| is 1e4-1e5.
+//   * P^T (accumulator layout) is the B operand of O^T += V^T P^T.  The V^T
+//     A operand comes straight from the row-major V tile through transposing LDS
+//     reads; keys are consumed in the order the accumulator layout holds them, a
+//     permutation of the contraction index applied identically to both operands.
+//   * Key tiles are visited from the diagonal backwards.  The running maximum is
+//     therefore found early, and O and l are only rescaled when a new maximum
+//     exceeds the one in use by more than 2^8 (the exponents stay <= 8, which
+//     bf16 P and fp32 sums absorb), which makes rescaling rare.
+//   * Causal structure: tiles after a wave's last query are skipped and only the
+//     tile holding its diagonal applies the mask.  Query blocks are dispatched
+//     longest-first with heads fastest, so a head's blocks share an XCD's L2
+//     whenever the head count is a multiple of 8.
 //
 // fp32 kernel: a straightforward vector-ALU kernel (D/32 lanes per query row,
 // keys staged through LDS 32 at a time).  It favours accuracy over speed: the
@@ -37,25 +45,27 @@ constexpr int kFwdWaves = 4;
 constexpr int kFwdThreads = 64 * kFwdWaves;
 constexpr int kFwdBM = 32 * kFwdWaves;  // query rows per workgroup
 constexpr int kFwdBN = 64;              // keys per tile
+constexpr float kRescaleSlack = 8.0f;   // log2 headroom before O and l are rescaled
+
+// Swizzled position of 16-byte chunk c of LDS row r in a [rows][D] bf16 tile.
+template <int D>
+__device__ __forceinline__ int swz_chunk(int r, int c) {
+  return D == 128 ? (c ^ (r & 15)) : (c ^ ((r >> 1) & 7));
+}
 
 template <int D>
-struct alignas(16) FwdTile {
-  static constexpr int KS = D + 8;       // K row stride in LDS (16-byte pad)
-  static constexpr int VS = kFwdBN + 4;  // V^T row stride in LDS
-  static constexpr int KCH = kFwdBN * D / 8 / kFwdThreads;  // 16-byte K chunks per thread
-  static constexpr int KPT = KCH;                            // keys per thread for V^T
-  bf16 k[kFwdBN * KS];
-  bf16 vt[D * VS];
-  float ck[kFwdBN];
-};
+__global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(2)))
+void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
+                     const bf16* __restrict__ V, const float* __restrict__ C,
+                     bf16* __restrict__ O, float* __restrict__ LSE, int BH, int L, int n_mblk,
+                     float scale_log2) {
+  constexpr int CPR = D / 8;                               // 16-byte chunks per row
+  constexpr int TILE = kFwdBN * D;                         // bf16 elements per tile
+  constexpr int NDMA = TILE * 2 / 1024 / kFwdWaves;        // 1 KB DMA loads per wave per tile
+  __shared__ __attribute__((aligned(16))) bf16 ks[2][TILE];
+  __shared__ __attribute__((aligned(16))) bf16 vs[2][TILE];
+  __shared__ __attribute__((aligned(16))) float cks[2][kFwdBN];
 
-template <int D>
-__global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
-    const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
-    const float* __restrict__ C, bf16* __restrict__ O, float* __restrict__ LSE, int BH, int L,
-    int n_mblk, float scale_log2) {
-  using T = FwdTile<D>;
-  __shared__ T sm;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = lane >> 5, col = lane & 31;
   const int bh = blockIdx.x % BH;
@@ -63,13 +73,41 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
   const int q0 = mblk * kFwdBM;
   const size_t head = (size_t)bh * (size_t)L;
   const bf16* Qh = Q + head * D;
-  const bf16* Kh = K + head * D;
-  const bf16* Vh = V + head * D;
   const float* Ch = C + head;
   const float c_ref = Ch[q0];
   const int qw0 = q0 + wave * 32;
   const int qi = qw0 + col;
   const bool q_valid = qi < L;
+  const uint32_t head_bytes = (uint32_t)L * D * 2;
+  const __amdgpu_buffer_rsrc_t rk = make_rsrc(K + head * D, head_bytes);
+  const __amdgpu_buffer_rsrc_t rv = make_rsrc(V + head * D, head_bytes);
+
+  // per-lane source offsets of the DMA loads (slot -> swizzled logical chunk)
+  uint32_t dma_off[NDMA];
+#pragma unroll
+  for (int i = 0; i < NDMA; ++i) {
+    const int slot = (i * kFwdWaves + wave) * 64 + lane;
+    const int r = slot / CPR;
+    const int c = swz_chunk<D>(r, slot % CPR);
+    dma_off[i] = (uint32_t)(r * D * 2 + c * 16);
+  }
+  // per-lane LDS element offsets of the K operand reads (row = key col, chunk 2s+h)
+  int koff[D / 16];
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s) koff[s] = col * D + swz_chunk<D>(col, 2 * s + h) * 8;
+  // per-lane LDS element offsets of the transposing V reads, for the two 4-key
+  // halves (k2) and each 32-wide block of head dims (db)
+  const int g16 = lane >> 4, j16 = lane & 15;
+  int voff[2][D / 32];
+#pragma unroll
+  for (int k2 = 0; k2 < 2; ++k2) {
+    const int r = 8 * k2 + 4 * (g16 >> 1) + (j16 >> 2);
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+      const int e = db * 32 + 16 * (g16 & 1) + 4 * (j16 & 3);
+      voff[k2][db] = r * D + swz_chunk<D>(r, e >> 3) * 8 + (e & 7);
+    }
+  }
 
   bf16x8 qf[D / 16];
 #pragma unroll
@@ -81,137 +119,112 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
       for (int e = 0; e < 8; ++e) qf[s][e] = to_bf16(0.0f);
     }
   }
-
   f32x16 oacc[D / 32];
 #pragma unroll
   for (int db = 0; db < D / 32; ++db)
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[db][r] = 0.0f;
-  float m_run = -INFINITY, l_run = 0.0f;
+  float m_used = -INFINITY, l_run = 0.0f;
 
   const int kend = min(L, q0 + kFwdBM);
-  const int n_kt = (kend + kFwdBN - 1) / kFwdBN;
+  const int t_last = (kend + kFwdBN - 1) / kFwdBN - 1;
+  const int t_diag = qw0 / kFwdBN;  // tile holding this wave's diagonal
 
-  bf16x8 kreg[T::KCH], vreg[T::KPT];
+  auto issue_tile = [&](int kt) {
+    const int buf = kt & 1;
+    const uint32_t base = (uint32_t)kt * kFwdBN * D * 2;
+#pragma unroll
+    for (int i = 0; i < NDMA; ++i) {
+      const int wslot = (i * kFwdWaves + wave) * 512;  // bf16 elements of this wave's 1 KB
+      dma16(rk, &ks[buf][wslot], base + dma_off[i]);
+      dma16(rv, &vs[buf][wslot], base + dma_off[i]);
+    }
+  };
   float creg = 0.0f;
-  const int vdg = tid % (D / 8), vkg = tid / (D / 8);
-
-  auto load_tile = [&](int kt) {
-    const int key0 = kt * kFwdBN;
-#pragma unroll
-    for (int i = 0; i < T::KCH; ++i) {
-      const int chunk = tid + kFwdThreads * i;
-      const int row = chunk / (D / 8), c8 = chunk % (D / 8);
-      const int key = key0 + row;
-      if (key < L) {
-        kreg[i] = *reinterpret_cast<const bf16x8*>(Kh + (size_t)key * D + c8 * 8);
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) kreg[i][e] = to_bf16(0.0f);
-      }
-    }
-#pragma unroll
-    for (int r = 0; r < T::KPT; ++r) {
-      const int key = key0 + vkg * T::KPT + r;
-      if (key < L) {
-        vreg[r] = *reinterpret_cast<const bf16x8*>(Vh + (size_t)key * D + vdg * 8);
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) vreg[r][e] = to_bf16(0.0f);
-      }
-    }
-    if (tid < kFwdBN) {
-      const int key = key0 + tid;
-      creg = key < L ? (Ch[key] - c_ref) * kLog2e : INFINITY;
-    }
+  auto load_c = [&](int kt) {
+    const int key = kt * kFwdBN + lane;
+    creg = key < L ? (Ch[key] - c_ref) * kLog2e : INFINITY;
   };
 
-  auto store_tile = [&]() {
-#pragma unroll
-    for (int i = 0; i < T::KCH; ++i) {
-      const int chunk = tid + kFwdThreads * i;
-      const int row = chunk / (D / 8), c8 = chunk % (D / 8);
-      *reinterpret_cast<bf16x8*>(&sm.k[row * T::KS + c8 * 8]) = kreg[i];
-    }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      bf16* dst = &sm.vt[(vdg * 8 + e) * T::VS + vkg * T::KPT];
-      if constexpr (T::KPT == 4) {
-        bf16x4 w = {vreg[0][e], vreg[1][e], vreg[2][e], vreg[3][e]};
-        *reinterpret_cast<bf16x4*>(dst) = w;
-      } else {
-        bf16x2 w = {vreg[0][e], vreg[1][e]};
-        *reinterpret_cast<bf16x2*>(dst) = w;
-      }
-    }
-    if (tid < kFwdBN) sm.ck[tid] = creg;
-  };
+  issue_tile(t_last);
+  if (wave == 0) {
+    load_c(t_last);
+    cks[t_last & 1][lane] = creg;
+  }
 
-  load_tile(0);
-  for (int kt = 0; kt < n_kt; ++kt) {
-    __syncthreads();
-    store_tile();
-    __syncthreads();
-    if (kt + 1 < n_kt) load_tile(kt + 1);
-    const int key0 = kt * kFwdBN;
-    if (key0 > qw0 + 31) continue;  // the whole tile lies after this wave's queries
-    const bool diag = key0 + kFwdBN - 1 > qw0;
-
-    float u[32];
+  for (int j = t_last; j >= 0; --j) {
+    wait_all_memory();
+    __syncthreads();  // tile j is in LDS; every wave is done with tile j + 1
+    if (j > 0) {
+      issue_tile(j - 1);
+      if (wave == 0) load_c(j - 1);
+    }
+    if (j <= t_diag) {
+      const int buf = j & 1;
+      const bf16* kt_ = ks[buf];
+      const bf16* vt_ = vs[buf];
+      const float* ct_ = cks[buf];
+      const int key0 = j * kFwdBN;
+      float u[32];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      f32x16 acc;
+      for (int kb = 0; kb < 2; ++kb) {
+        f32x16 acc;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
+        for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
 #pragma unroll
-      for (int s = 0; s < D / 16; ++s) {
-        const bf16x8 a =
-            *reinterpret_cast<const bf16x8*>(&sm.k[(kb * 32 + col) * T::KS + 16 * s + 8 * h]);
-        acc = mfma32(a, qf[s], acc);
+        for (int s = 0; s < D / 16; ++s) {
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(kt_ + kb * 32 * D + koff[s]);
+          acc = mfma32(a, qf[s], acc);
+        }
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x4 ck4 = *reinterpret_cast<const f32x4*>(ct_ + kb * 32 + 8 * g + 4 * h);
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj) u[kb * 16 + 4 * g + jj] = acc[4 * g + jj] * scale_log2 - ck4[jj];
+        }
       }
+      if (j == t_diag) {
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int kl = kb * 32 + 8 * g + 4 * h;
-        const f32x4 ck4 = *reinterpret_cast<const f32x4*>(&sm.ck[kl]);
+        for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          float x = acc[4 * g + j] * scale_log2 - ck4[j];
-          if (diag && key0 + kl + j > qi) x = -INFINITY;
-          u[kb * 16 + 4 * g + j] = x;
+          for (int r = 0; r < 16; ++r)
+            if (key0 + kb * 32 + mfma_row(r, h) > qi) u[kb * 16 + r] = -INFINITY;
+      }
+      float mt = u[0];
+#pragma unroll
+      for (int r = 1; r < 32; ++r) mt = fmaxf(mt, u[r]);
+      mt = wave_max_pair(mt);
+      if (__any(mt > m_used + kRescaleSlack)) {
+        const float m_new = fmaxf(m_used, mt);
+        const float alpha = exp2_fast(m_used - m_new);
+        l_run *= alpha;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) oacc[db] *= alpha;
+        m_used = m_new;
+      }
+      const float m_ref = m_used == -INFINITY ? 0.0f : m_used;  // rows past the end only
+      float psum = 0.0f;
+#pragma unroll
+      for (int r = 0; r < 32; ++r) {
+        u[r] = exp2_fast(u[r] - m_ref);
+        psum += u[r];
+      }
+      l_run += psum;
+      bf16x8 pb[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) pb[c] = pack8(&u[8 * c]);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) {
+          const bf16x4 lo = lds_read_tr16(vt_ + c * 16 * D + voff[0][db]);
+          const bf16x4 hi = lds_read_tr16(vt_ + c * 16 * D + voff[1][db]);
+          oacc[db] = mfma32(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7), pb[c],
+                            oacc[db]);
         }
       }
     }
-    float mt = u[0];
-#pragma unroll
-    for (int r = 1; r < 32; ++r) mt = fmaxf(mt, u[r]);
-    mt = wave_max_pair(mt);
-    const float m_new = fmaxf(m_run, mt);
-    const float alpha = exp2_fast(m_run - m_new);
-    float psum = 0.0f;
-#pragma unroll
-    for (int r = 0; r < 32; ++r) {
-      u[r] = exp2_fast(u[r] - m_new);
-      psum += u[r];
-    }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db) oacc[db] *= alpha;
-
-    bf16x8 pb[4];
-#pragma unroll
-    for (int c = 0; c < 4; ++c) pb[c] = pack8(&u[8 * c]);
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db) {
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const bf16* vrow = &sm.vt[(db * 32 + col) * T::VS + 16 * c + 4 * h];
-        const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow);
-        const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 8);
-        const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-        oacc[db] = mfma32(a, pb[c], oacc[db]);
-      }
-    }
+    if (j > 0 && wave == 0) cks[(j - 1) & 1][lane] = creg;
   }
 
   const float l_tot = wave_sum_pair(l_run);
@@ -224,11 +237,11 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
       for (int g = 0; g < 4; ++g) {
         bf16x4 w;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) w[j] = to_bf16(oacc[db][4 * g + j] * inv);
+        for (int jj = 0; jj < 4; ++jj) w[jj] = to_bf16(oacc[db][4 * g + jj] * inv);
         *reinterpret_cast<bf16x4*>(orow + db * 32 + 8 * g + 4 * h) = w;
       }
     }
-    if (h == 0) LSE[head + qi] = (Ch[qi] - c_ref) + kLn2 * (m_run + log2f(l_tot));
+    if (h == 0) LSE[head + qi] = (Ch[qi] - c_ref) + kLn2 * (m_used + log2f(l_tot));
   }
 }
 

@@ -20,6 +20,7 @@ int check_dims(int B, int H, int L, int d) {
   if (bh > (1LL << 30)) return FOX_ERR_SHAPE;
   if (bh * L > (1LL << 31) - 1) return FOX_ERR_SHAPE;          // row index fits in int
   if (bh * L * d > kMaxElems) return FOX_ERR_SHAPE;
+  if ((long long)L * d * 4 >= (1LL << 31)) return FOX_ERR_SHAPE;  // one head addressed in 32 bits
   if (bh * ((L + 63) / 64) > kMaxWorkgroups) return FOX_ERR_SHAPE;
   return FOX_OK;
 }

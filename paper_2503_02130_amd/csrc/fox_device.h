@@ -10,6 +10,8 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4_t;
 
 namespace fox {
 
@@ -56,6 +58,35 @@ __device__ __forceinline__ float wave_sum_pair(float x) { return x + __shfl_xor(
 // log sigmoid(x) = min(x, 0) - log1p(exp(-|x|)), overflow-free for any finite x.
 __device__ __forceinline__ float log_sigmoid(float x) {
   return fminf(x, 0.0f) - log1pf(expf(-fabsf(x)));
+}
+
+// ---------------------------------------------------------------------------
+// Global -> LDS without registers (buffer_load ... lds).  One instruction moves
+// 16 bytes per lane: lane l's bytes land at lds_wave_base + 16 * l, whatever
+// global offset the lane asked for, and offsets at or beyond the resource's
+// byte count read as zero (the hardware range check), which pads ragged tiles.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  // word 3 = 0x00020000: 32-bit data format, the raw-buffer setting for gfx9-family parts
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                           0x00020000);
+}
+
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rsrc, void* lds_wave_base,
+                                      uint32_t voffset) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t*)lds_wave_base, 16, voffset, 0, 0, 0);
+}
+
+// Wait until every outstanding memory operation of this wave (including the
+// LDS-bound buffer loads above) has completed.
+__device__ __forceinline__ void wait_all_memory() { __builtin_amdgcn_s_waitcnt(0); }
+
+// Transposing LDS read (ds_read_b64_tr_b16).  Within each group of 16 lanes,
+// lane j supplies the address of 4 consecutive bf16 in row (j / 4) of a 4 x 16
+// block, columns 4 * (j % 4) .. +3; lane i of the group receives column i of the
+// block, i.e. the 4 values of rows 0..3 in that column.
+__device__ __forceinline__ bf16x4 lds_read_tr16(const bf16* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)p);
 }
 
 }  // namespace fox
