@@ -51,44 +51,48 @@ __global__ __launch_bounds__(256) void bwd_delta_kernel(const T* __restrict__ O,
 }
 
 // ---------------------------------------------------------------------------
-// bf16 dq kernel
+// bf16 dq kernel: 128 queries per workgroup (4 waves x 32), 64-key tiles
+// double-buffered in LDS through DMA loads, diagonal tile first.
 // ---------------------------------------------------------------------------
 constexpr int kBwdThreads = 256;
-constexpr int kDqBM = 128;  // queries per workgroup (4 waves x 32)
-constexpr int kDqBN = 64;   // keys per tile
+constexpr int kDqWaves = 4;
+constexpr int kDqBM = 32 * kDqWaves;
+constexpr int kDqBN = 64;
 
 template <int D>
-struct alignas(16) DqTile {
-  static constexpr int RS = D + 8;      // row-major stride
-  static constexpr int TS = kDqBN + 4;  // transposed stride
-  static constexpr int KPT = kDqBN * D / 8 / kBwdThreads;
-  bf16 k[kDqBN * RS];
-  bf16 kt[D * TS];
-  bf16 v[kDqBN * RS];
-  float ck[kDqBN];
-};
+__global__ __launch_bounds__(kBwdThreads) __attribute__((amdgpu_waves_per_eu(2)))
+void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
+                        const bf16* __restrict__ V, const float* __restrict__ C,
+                        const float* __restrict__ LSE, const bf16* __restrict__ dO,
+                        const float* __restrict__ delta, bf16* __restrict__ dQ,
+                        float* __restrict__ dcq, int BH, int L, int n_mblk, float scale,
+                        float scale_log2) {
+  constexpr int TILE = kDqBN * D;
+  constexpr int NDMA = TILE * 2 / 1024 / kDqWaves;
+  __shared__ __attribute__((aligned(16))) bf16 ks[2][TILE];
+  __shared__ __attribute__((aligned(16))) bf16 vs[2][TILE];
+  __shared__ __attribute__((aligned(16))) float cks[2][kDqBN];
 
-template <int D>
-__global__ __launch_bounds__(kBwdThreads) void bwd_dq_bf16_kernel(
-    const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
-    const float* __restrict__ C, const float* __restrict__ LSE, const bf16* __restrict__ dO,
-    const float* __restrict__ delta, bf16* __restrict__ dQ, float* __restrict__ dcq, int BH,
-    int L, int n_mblk, float scale, float scale_log2) {
-  using T = DqTile<D>;
-  __shared__ T sm;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = lane >> 5, col = lane & 31;
   const int bh = blockIdx.x % BH;
   const int mblk = n_mblk - 1 - (int)(blockIdx.x / BH);
   const int q0 = mblk * kDqBM;
   const size_t head = (size_t)bh * (size_t)L;
-  const bf16* Kh = K + head * D;
-  const bf16* Vh = V + head * D;
   const float* Ch = C + head;
   const float c_ref = Ch[q0];
   const int qw0 = q0 + wave * 32;
   const int qi = qw0 + col;
   const bool q_valid = qi < L;
+  const uint32_t head_bytes = (uint32_t)L * D * 2;
+  const __amdgpu_buffer_rsrc_t rk = make_rsrc(K + head * D, head_bytes);
+  const __amdgpu_buffer_rsrc_t rv = make_rsrc(V + head * D, head_bytes);
+  uint32_t dma_off[NDMA];
+  tile_dma_offsets<D, NDMA>(dma_off, wave, kDqWaves, lane);
+  int roff[D / 16];
+  tile_row_offsets<D>(roff, col, h);
+  int toff[2][D / 32];
+  tile_tr_offsets<D>(toff, lane);
 
   bf16x8 qf[D / 16], dof[D / 16];
 #pragma unroll
@@ -115,98 +119,80 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dq_bf16_kernel(
   float dcq_part = 0.0f;
 
   const int kend = min(L, q0 + kDqBM);
-  const int n_kt = (kend + kDqBN - 1) / kDqBN;
-  const int dg = tid % (D / 8), kg = tid / (D / 8);
+  const int t_last = (kend + kDqBN - 1) / kDqBN - 1;
+  const int t_diag = qw0 / kDqBN;
 
-  for (int kt = 0; kt < n_kt; ++kt) {
-    const int key0 = kt * kDqBN;
-    bf16x8 kreg[T::KPT], vreg[T::KPT];
+  auto issue_tile = [&](int kt) {
+    const int buf = kt & 1;
+    const uint32_t base = (uint32_t)kt * kDqBN * D * 2;
 #pragma unroll
-    for (int r = 0; r < T::KPT; ++r) {
-      const int key = key0 + kg * T::KPT + r;
-      if (key < L) {
-        kreg[r] = *reinterpret_cast<const bf16x8*>(Kh + (size_t)key * D + dg * 8);
-        vreg[r] = *reinterpret_cast<const bf16x8*>(Vh + (size_t)key * D + dg * 8);
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          kreg[r][e] = to_bf16(0.0f);
-          vreg[r][e] = to_bf16(0.0f);
-        }
-      }
+    for (int i = 0; i < NDMA; ++i) {
+      const int wslot = (i * kDqWaves + wave) * 512;
+      dma16(rk, &ks[buf][wslot], base + dma_off[i]);
+      dma16(rv, &vs[buf][wslot], base + dma_off[i]);
     }
-    float creg = 0.0f;
-    if (tid < kDqBN) {
-      const int key = key0 + tid;
-      creg = key < L ? (Ch[key] - c_ref) * kLog2e : INFINITY;
-    }
-    __syncthreads();  // previous tile fully consumed
-#pragma unroll
-    for (int r = 0; r < T::KPT; ++r) {
-      const int row = kg * T::KPT + r;
-      *reinterpret_cast<bf16x8*>(&sm.k[row * T::RS + dg * 8]) = kreg[r];
-      *reinterpret_cast<bf16x8*>(&sm.v[row * T::RS + dg * 8]) = vreg[r];
-    }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      bf16* dst = &sm.kt[(dg * 8 + e) * T::TS + kg * T::KPT];
-      if constexpr (T::KPT == 4) {
-        bf16x4 w = {kreg[0][e], kreg[1][e], kreg[2][e], kreg[3][e]};
-        *reinterpret_cast<bf16x4*>(dst) = w;
-      } else {
-        bf16x2 w = {kreg[0][e], kreg[1][e]};
-        *reinterpret_cast<bf16x2*>(dst) = w;
-      }
-    }
-    if (tid < kDqBN) sm.ck[tid] = creg;
+  };
+  float creg = 0.0f;
+  auto load_c = [&](int kt) {
+    const int key = kt * kDqBN + lane;
+    creg = key < L ? (Ch[key] - c_ref) * kLog2e : INFINITY;
+  };
+
+  issue_tile(t_last);
+  if (wave == 0) {
+    load_c(t_last);
+    cks[t_last & 1][lane] = creg;
+  }
+  for (int j = t_last; j >= 0; --j) {
+    wait_all_memory();
     __syncthreads();
-
-    if (key0 > qw0 + 31) continue;  // the whole tile lies after this wave's queries
-    const bool diag = key0 + kDqBN - 1 > qw0;
-
-    float dsv[32];
+    if (j > 0) {
+      issue_tile(j - 1);
+      if (wave == 0) load_c(j - 1);
+    }
+    if (j <= t_diag) {
+      const int buf = j & 1;
+      const bf16* kt_ = ks[buf];
+      const bf16* vt_ = vs[buf];
+      const float* ct_ = cks[buf];
+      const int key0 = j * kDqBN;
+      bf16x8 dsb[4];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      f32x16 sacc, pacc;
+      for (int kb = 0; kb < 2; ++kb) {
+        f32x16 sacc, pacc;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        sacc[r] = 0.0f;
-        pacc[r] = 0.0f;
-      }
-#pragma unroll
-      for (int s = 0; s < D / 16; ++s) {
-        const int off = (kb * 32 + col) * T::RS + 16 * s + 8 * h;
-        sacc = mfma32(*reinterpret_cast<const bf16x8*>(&sm.k[off]), qf[s], sacc);
-        pacc = mfma32(*reinterpret_cast<const bf16x8*>(&sm.v[off]), dof[s], pacc);
-      }
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int kl = kb * 32 + 8 * g + 4 * h;
-        const f32x4 ck4 = *reinterpret_cast<const f32x4*>(&sm.ck[kl]);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          float p = exp2_fast(sacc[4 * g + j] * scale_log2 - ck4[j] + bias2);
-          if (diag && key0 + kl + j > qi) p = 0.0f;
-          const float ds = p * (pacc[4 * g + j] - dlt);
-          dcq_part += ds;
-          dsv[kb * 16 + 4 * g + j] = ds;
+        for (int r = 0; r < 16; ++r) {
+          sacc[r] = 0.0f;
+          pacc[r] = 0.0f;
         }
+#pragma unroll
+        for (int s = 0; s < D / 16; ++s) {
+          sacc = mfma32(*reinterpret_cast<const bf16x8*>(kt_ + kb * 32 * D + roff[s]), qf[s], sacc);
+          pacc = mfma32(*reinterpret_cast<const bf16x8*>(vt_ + kb * 32 * D + roff[s]), dof[s], pacc);
+        }
+        float dsv[16];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x4 ck4 = *reinterpret_cast<const f32x4*>(ct_ + kb * 32 + 8 * g + 4 * h);
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj) {
+            float p = exp2_fast(sacc[4 * g + jj] * scale_log2 - ck4[jj] + bias2);
+            if (j == t_diag && key0 + kb * 32 + 8 * g + 4 * h + jj > qi) p = 0.0f;
+            const float ds = p * (pacc[4 * g + jj] - dlt);
+            dcq_part += ds;
+            dsv[4 * g + jj] = ds;
+          }
+        }
+        dsb[2 * kb] = pack8(&dsv[0]);
+        dsb[2 * kb + 1] = pack8(&dsv[8]);
       }
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+          dqacc[db] = mfma32(tile_tr_operand<D>(kt_, toff, c, db), dsb[c], dqacc[db]);
     }
-    bf16x8 dsb[4];
-#pragma unroll
-    for (int c = 0; c < 4; ++c) dsb[c] = pack8(&dsv[8 * c]);
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db) {
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const bf16* row = &sm.kt[(db * 32 + col) * T::TS + 16 * c + 4 * h];
-        const bf16x4 lo = *reinterpret_cast<const bf16x4*>(row);
-        const bf16x4 hi = *reinterpret_cast<const bf16x4*>(row + 8);
-        dqacc[db] = mfma32(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7), dsb[c],
-                           dqacc[db]);
-      }
-    }
+    if (j > 0 && wave == 0) cks[(j - 1) & 1][lane] = creg;
   }
 
   const float dcq_tot = wave_sum_pair(dcq_part);
@@ -218,7 +204,7 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dq_bf16_kernel(
       for (int g = 0; g < 4; ++g) {
         bf16x4 w;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) w[j] = to_bf16(dqacc[db][4 * g + j] * scale);
+        for (int jj = 0; jj < 4; ++jj) w[jj] = to_bf16(dqacc[db][4 * g + jj] * scale);
         *reinterpret_cast<bf16x4*>(out + db * 32 + 8 * g + 4 * h) = w;
       }
     }
@@ -227,45 +213,49 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dq_bf16_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// bf16 dkdv kernel
+// bf16 dkdv kernel: 32 keys per wave, KV_WAVES waves per workgroup; 64-query tiles
+// of Q and dO double-buffered in LDS through DMA loads.
 // ---------------------------------------------------------------------------
-constexpr int kKvBN = 128;  // keys per workgroup (4 waves x 32)
-constexpr int kKvBM = 64;   // queries per tile
+constexpr int kKvWaves = 4;
+constexpr int kKvThreads = 64 * kKvWaves;
+constexpr int kKvBN = 32 * kKvWaves;  // keys per workgroup
+constexpr int kKvBM = 64;             // queries per tile
 
 template <int D>
-struct alignas(16) KvTile {
-  static constexpr int RS = D + 8;
-  static constexpr int TS = kKvBM + 4;
-  static constexpr int QPT = kKvBM * D / 8 / kBwdThreads;  // query rows per thread
-  bf16 q[kKvBM * RS];
-  bf16 qt[D * TS];
-  bf16 g[kKvBM * RS];
-  bf16 gt[D * TS];
-  float bq[kKvBM];
-  float dl[kKvBM];
-};
-
-template <int D>
-__global__ __launch_bounds__(kBwdThreads) void bwd_dkdv_bf16_kernel(
+__global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
     const float* __restrict__ C, const float* __restrict__ LSE, const bf16* __restrict__ dO,
     const float* __restrict__ delta, bf16* __restrict__ dK, bf16* __restrict__ dV,
     float* __restrict__ dck, int BH, int L, float scale, float scale_log2) {
-  using T = KvTile<D>;
-  __shared__ T sm;
+  constexpr int TILE = kKvBM * D;
+  constexpr int NDMA = TILE * 2 / 1024 / kKvWaves;
+  __shared__ __attribute__((aligned(16))) bf16 qs[2][TILE];
+  __shared__ __attribute__((aligned(16))) bf16 gs[2][TILE];
+  __shared__ __attribute__((aligned(16))) float bqs[2][kKvBM];
+  __shared__ __attribute__((aligned(16))) float dls[2][kKvBM];
+
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = lane >> 5, col = lane & 31;
   const int bh = blockIdx.x % BH;
   const int nblk = (int)(blockIdx.x / BH);  // key block 0 has the most work: first
   const int k0 = nblk * kKvBN;
   const size_t head = (size_t)bh * (size_t)L;
-  const bf16* Qh = Q + head * D;
-  const bf16* Gh = dO + head * D;
   const float* Ch = C + head;
+  const float* Lh = LSE + head;
+  const float* Dh = delta + head;
   const float c_ref = Ch[k0];
   const int kw0 = k0 + wave * 32;
   const int kj = kw0 + col;
   const bool k_valid = kj < L;
+  const uint32_t head_bytes = (uint32_t)L * D * 2;
+  const __amdgpu_buffer_rsrc_t rq = make_rsrc(Q + head * D, head_bytes);
+  const __amdgpu_buffer_rsrc_t rg = make_rsrc(dO + head * D, head_bytes);
+  uint32_t dma_off[NDMA];
+  tile_dma_offsets<D, NDMA>(dma_off, wave, kKvWaves, lane);
+  int roff[D / 16];
+  tile_row_offsets<D>(roff, col, h);
+  int toff[2][D / 32];
+  tile_tr_offsets<D>(toff, lane);
 
   bf16x8 kf[D / 16], vf[D / 16];
 #pragma unroll
@@ -293,116 +283,96 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dkdv_bf16_kernel(
     }
   float dck_part = 0.0f;
 
-  const int t_begin = k0 / kKvBM;
-  const int n_qt = (L + kKvBM - 1) / kKvBM;
-  const int dg = tid % (D / 8), qg = tid / (D / 8);
+  const int t_first = k0 / kKvBM;
+  const int t_end = (L + kKvBM - 1) / kKvBM;
+  const int t_diag = kw0 / kKvBM;  // tile holding this wave's diagonal
 
-  for (int qt = t_begin; qt < n_qt; ++qt) {
-    const int qs0 = qt * kKvBM;
-    bf16x8 qreg[T::QPT], greg[T::QPT];
+  auto issue_tile = [&](int qt) {
+    const int buf = qt & 1;
+    const uint32_t base = (uint32_t)qt * kKvBM * D * 2;
 #pragma unroll
-    for (int r = 0; r < T::QPT; ++r) {
-      const int qq = qs0 + qg * T::QPT + r;
-      if (qq < L) {
-        qreg[r] = *reinterpret_cast<const bf16x8*>(Qh + (size_t)qq * D + dg * 8);
-        greg[r] = *reinterpret_cast<const bf16x8*>(Gh + (size_t)qq * D + dg * 8);
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          qreg[r][e] = to_bf16(0.0f);
-          greg[r][e] = to_bf16(0.0f);
-        }
-      }
+    for (int i = 0; i < NDMA; ++i) {
+      const int wslot = (i * kKvWaves + wave) * 512;
+      dma16(rq, &qs[buf][wslot], base + dma_off[i]);
+      dma16(rg, &gs[buf][wslot], base + dma_off[i]);
     }
-    float bqreg = -INFINITY, dlreg = 0.0f;
-    if (tid < kKvBM) {
-      const int qq = qs0 + tid;
-      if (qq < L) {
-        bqreg = ((Ch[qq] - c_ref) - LSE[head + qq]) * kLog2e;
-        dlreg = delta[head + qq];
-      }
+  };
+  float breg = 0.0f, dreg = 0.0f;
+  auto load_rows = [&](int qt) {
+    const int qq = qt * kKvBM + lane;
+    breg = -INFINITY;
+    dreg = 0.0f;
+    if (qq < L) {
+      breg = ((Ch[qq] - c_ref) - Lh[qq]) * kLog2e;
+      dreg = Dh[qq];
     }
+  };
+  auto store_rows = [&](int buf) {
+    bqs[buf][lane] = breg;
+    dls[buf][lane] = dreg;
+  };
+
+  issue_tile(t_first);
+  if (wave == 0) {
+    load_rows(t_first);
+    store_rows(t_first & 1);
+  }
+  for (int qt = t_first; qt < t_end; ++qt) {
+    wait_all_memory();
     __syncthreads();
-#pragma unroll
-    for (int r = 0; r < T::QPT; ++r) {
-      const int row = qg * T::QPT + r;
-      *reinterpret_cast<bf16x8*>(&sm.q[row * T::RS + dg * 8]) = qreg[r];
-      *reinterpret_cast<bf16x8*>(&sm.g[row * T::RS + dg * 8]) = greg[r];
+    if (qt + 1 < t_end) {
+      issue_tile(qt + 1);
+      if (wave == 0) load_rows(qt + 1);
     }
+    if (qt >= t_diag) {
+      const int buf = qt & 1;
+      const bf16* qt_ = qs[buf];
+      const bf16* gt_ = gs[buf];
+      const float* bq_ = bqs[buf];
+      const float* dl_ = dls[buf];
+      const int qs0 = qt * kKvBM;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      bf16* dq_ = &sm.qt[(dg * 8 + e) * T::TS + qg * T::QPT];
-      bf16* dg_ = &sm.gt[(dg * 8 + e) * T::TS + qg * T::QPT];
-      if constexpr (T::QPT == 4) {
-        bf16x4 a = {qreg[0][e], qreg[1][e], qreg[2][e], qreg[3][e]};
-        bf16x4 b = {greg[0][e], greg[1][e], greg[2][e], greg[3][e]};
-        *reinterpret_cast<bf16x4*>(dq_) = a;
-        *reinterpret_cast<bf16x4*>(dg_) = b;
-      } else {
-        bf16x2 a = {qreg[0][e], qreg[1][e]};
-        bf16x2 b = {greg[0][e], greg[1][e]};
-        *reinterpret_cast<bf16x2*>(dq_) = a;
-        *reinterpret_cast<bf16x2*>(dg_) = b;
-      }
-    }
-    if (tid < kKvBM) {
-      sm.bq[tid] = bqreg;
-      sm.dl[tid] = dlreg;
-    }
-    __syncthreads();
-
-    if (qs0 + kKvBM - 1 < kw0) continue;  // every query of the tile precedes this wave's keys
-    const bool diag = qs0 < kw0 + 31;
-
+      for (int qb = 0; qb < 2; ++qb) {
+        f32x16 sacc, pacc;
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-      f32x16 sacc, pacc;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        sacc[r] = 0.0f;
-        pacc[r] = 0.0f;
-      }
-#pragma unroll
-      for (int s = 0; s < D / 16; ++s) {
-        const int off = (qb * 32 + col) * T::RS + 16 * s + 8 * h;
-        sacc = mfma32(*reinterpret_cast<const bf16x8*>(&sm.q[off]), kf[s], sacc);
-        pacc = mfma32(*reinterpret_cast<const bf16x8*>(&sm.g[off]), vf[s], pacc);
-      }
-      float pv[16], dsv[16];
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int ql = qb * 32 + 8 * g + 4 * h;
-        const f32x4 bq4 = *reinterpret_cast<const f32x4*>(&sm.bq[ql]);
-        const f32x4 dl4 = *reinterpret_cast<const f32x4*>(&sm.dl[ql]);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          float p = exp2_fast(sacc[4 * g + j] * scale_log2 + bq4[j] - ck2);
-          if (diag && kj > qs0 + ql + j) p = 0.0f;
-          const float ds = p * (pacc[4 * g + j] - dl4[j]);
-          dck_part -= ds;
-          pv[4 * g + j] = p;
-          dsv[4 * g + j] = ds;
+        for (int r = 0; r < 16; ++r) {
+          sacc[r] = 0.0f;
+          pacc[r] = 0.0f;
         }
-      }
 #pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        const bf16x8 pb = pack8(&pv[8 * c]);
-        const bf16x8 dsb = pack8(&dsv[8 * c]);
-        const int qoff = qb * 32 + 16 * c + 4 * h;
+        for (int s = 0; s < D / 16; ++s) {
+          sacc = mfma32(*reinterpret_cast<const bf16x8*>(qt_ + qb * 32 * D + roff[s]), kf[s], sacc);
+          pacc = mfma32(*reinterpret_cast<const bf16x8*>(gt_ + qb * 32 * D + roff[s]), vf[s], pacc);
+        }
+        float pv[16], dsv[16];
 #pragma unroll
-        for (int db = 0; db < D / 32; ++db) {
-          const int roff = (db * 32 + col) * T::TS + qoff;
-          const bf16x4 glo = *reinterpret_cast<const bf16x4*>(&sm.gt[roff]);
-          const bf16x4 ghi = *reinterpret_cast<const bf16x4*>(&sm.gt[roff + 8]);
-          dvacc[db] = mfma32(__builtin_shufflevector(glo, ghi, 0, 1, 2, 3, 4, 5, 6, 7), pb,
-                             dvacc[db]);
-          const bf16x4 qlo = *reinterpret_cast<const bf16x4*>(&sm.qt[roff]);
-          const bf16x4 qhi = *reinterpret_cast<const bf16x4*>(&sm.qt[roff + 8]);
-          dkacc[db] = mfma32(__builtin_shufflevector(qlo, qhi, 0, 1, 2, 3, 4, 5, 6, 7), dsb,
-                             dkacc[db]);
+        for (int g = 0; g < 4; ++g) {
+          const int ql = qb * 32 + 8 * g + 4 * h;
+          const f32x4 bq4 = *reinterpret_cast<const f32x4*>(bq_ + ql);
+          const f32x4 dl4 = *reinterpret_cast<const f32x4*>(dl_ + ql);
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj) {
+            float p = exp2_fast(sacc[4 * g + jj] * scale_log2 + bq4[jj] - ck2);
+            if (qt == t_diag && kj > qs0 + ql + jj) p = 0.0f;
+            const float ds = p * (pacc[4 * g + jj] - dl4[jj]);
+            dck_part -= ds;
+            pv[4 * g + jj] = p;
+            dsv[4 * g + jj] = ds;
+          }
+        }
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          const bf16x8 pb = pack8(&pv[8 * c]);
+          const bf16x8 dsb = pack8(&dsv[8 * c]);
+#pragma unroll
+          for (int db = 0; db < D / 32; ++db) {
+            dvacc[db] = mfma32(tile_tr_operand<D>(gt_, toff, 2 * qb + c, db), pb, dvacc[db]);
+            dkacc[db] = mfma32(tile_tr_operand<D>(qt_, toff, 2 * qb + c, db), dsb, dkacc[db]);
+          }
         }
       }
     }
+    if (qt + 1 < t_end && wave == 0) store_rows((qt + 1) & 1);
   }
 
   const float dck_tot = wave_sum_pair(dck_part);
@@ -415,9 +385,9 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dkdv_bf16_kernel(
       for (int g = 0; g < 4; ++g) {
         bf16x4 wk, wv;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          wk[j] = to_bf16(dkacc[db][4 * g + j] * scale);
-          wv[j] = to_bf16(dvacc[db][4 * g + j]);
+        for (int jj = 0; jj < 4; ++jj) {
+          wk[jj] = to_bf16(dkacc[db][4 * g + jj] * scale);
+          wv[jj] = to_bf16(dvacc[db][4 * g + jj]);
         }
         *reinterpret_cast<bf16x4*>(ok + db * 32 + 8 * g + 4 * h) = wk;
         *reinterpret_cast<bf16x4*>(ov + db * 32 + 8 * g + 4 * h) = wv;
@@ -611,14 +581,14 @@ hipError_t launch_bwd_bf16(const void* q, const void* k, const void* v, const fl
   const int n_nblk = (L + kKvBN - 1) / kKvBN;
   const dim3 gq((unsigned)n_mblk * (unsigned)BH), gk((unsigned)n_nblk * (unsigned)BH);
   if (d == 128) {
-    hipLaunchKernelGGL(bwd_dkdv_bf16_kernel<128>, gk, dim3(kBwdThreads), 0, s, (const bf16*)q,
+    hipLaunchKernelGGL(bwd_dkdv_bf16_kernel<128>, gk, dim3(kKvThreads), 0, s, (const bf16*)q,
                        (const bf16*)k, (const bf16*)v, c, lse, (const bf16*)d_o, delta, (bf16*)dk,
                        (bf16*)dv, dck, BH, L, scale, sl2);
     hipLaunchKernelGGL(bwd_dq_bf16_kernel<128>, gq, dim3(kBwdThreads), 0, s, (const bf16*)q,
                        (const bf16*)k, (const bf16*)v, c, lse, (const bf16*)d_o, delta, (bf16*)dq,
                        dcq, BH, L, n_mblk, scale, sl2);
   } else {
-    hipLaunchKernelGGL(bwd_dkdv_bf16_kernel<64>, gk, dim3(kBwdThreads), 0, s, (const bf16*)q,
+    hipLaunchKernelGGL(bwd_dkdv_bf16_kernel<64>, gk, dim3(kKvThreads), 0, s, (const bf16*)q,
                        (const bf16*)k, (const bf16*)v, c, lse, (const bf16*)d_o, delta, (bf16*)dk,
                        (bf16*)dv, dck, BH, L, scale, sl2);
     hipLaunchKernelGGL(bwd_dq_bf16_kernel<64>, gq, dim3(kBwdThreads), 0, s, (const bf16*)q,

@@ -47,19 +47,12 @@ constexpr int kFwdBM = 32 * kFwdWaves;  // query rows per workgroup
 constexpr int kFwdBN = 64;              // keys per tile
 constexpr float kRescaleSlack = 8.0f;   // log2 headroom before O and l are rescaled
 
-// Swizzled position of 16-byte chunk c of LDS row r in a [rows][D] bf16 tile.
-template <int D>
-__device__ __forceinline__ int swz_chunk(int r, int c) {
-  return D == 128 ? (c ^ (r & 15)) : (c ^ ((r >> 1) & 7));
-}
-
 template <int D>
 __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
                      const bf16* __restrict__ V, const float* __restrict__ C,
                      bf16* __restrict__ O, float* __restrict__ LSE, int BH, int L, int n_mblk,
                      float scale_log2) {
-  constexpr int CPR = D / 8;                               // 16-byte chunks per row
   constexpr int TILE = kFwdBN * D;                         // bf16 elements per tile
   constexpr int NDMA = TILE * 2 / 1024 / kFwdWaves;        // 1 KB DMA loads per wave per tile
   __shared__ __attribute__((aligned(16))) bf16 ks[2][TILE];
@@ -82,32 +75,12 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
   const __amdgpu_buffer_rsrc_t rk = make_rsrc(K + head * D, head_bytes);
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(V + head * D, head_bytes);
 
-  // per-lane source offsets of the DMA loads (slot -> swizzled logical chunk)
   uint32_t dma_off[NDMA];
-#pragma unroll
-  for (int i = 0; i < NDMA; ++i) {
-    const int slot = (i * kFwdWaves + wave) * 64 + lane;
-    const int r = slot / CPR;
-    const int c = swz_chunk<D>(r, slot % CPR);
-    dma_off[i] = (uint32_t)(r * D * 2 + c * 16);
-  }
-  // per-lane LDS element offsets of the K operand reads (row = key col, chunk 2s+h)
+  tile_dma_offsets<D, NDMA>(dma_off, wave, kFwdWaves, lane);
   int koff[D / 16];
-#pragma unroll
-  for (int s = 0; s < D / 16; ++s) koff[s] = col * D + swz_chunk<D>(col, 2 * s + h) * 8;
-  // per-lane LDS element offsets of the transposing V reads, for the two 4-key
-  // halves (k2) and each 32-wide block of head dims (db)
-  const int g16 = lane >> 4, j16 = lane & 15;
+  tile_row_offsets<D>(koff, col, h);
   int voff[2][D / 32];
-#pragma unroll
-  for (int k2 = 0; k2 < 2; ++k2) {
-    const int r = 8 * k2 + 4 * (g16 >> 1) + (j16 >> 2);
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db) {
-      const int e = db * 32 + 16 * (g16 & 1) + 4 * (j16 & 3);
-      voff[k2][db] = r * D + swz_chunk<D>(r, e >> 3) * 8 + (e & 7);
-    }
-  }
+  tile_tr_offsets<D>(voff, lane);
 
   bf16x8 qf[D / 16];
 #pragma unroll
@@ -214,15 +187,10 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
 #pragma unroll
       for (int c = 0; c < 4; ++c) pb[c] = pack8(&u[8 * c]);
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
+      for (int c = 0; c < 4; ++c)
 #pragma unroll
-        for (int db = 0; db < D / 32; ++db) {
-          const bf16x4 lo = lds_read_tr16(vt_ + c * 16 * D + voff[0][db]);
-          const bf16x4 hi = lds_read_tr16(vt_ + c * 16 * D + voff[1][db]);
-          oacc[db] = mfma32(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7), pb[c],
-                            oacc[db]);
-        }
-      }
+        for (int db = 0; db < D / 32; ++db)
+          oacc[db] = mfma32(tile_tr_operand<D>(vt_, voff, c, db), pb[c], oacc[db]);
     }
     if (j > 0 && wave == 0) cks[(j - 1) & 1][lane] = creg;
   }

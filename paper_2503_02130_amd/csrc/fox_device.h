@@ -89,4 +89,64 @@ __device__ __forceinline__ bf16x4 lds_read_tr16(const bf16* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)p);
 }
 
+// ---------------------------------------------------------------------------
+// Swizzled LDS tiles: a [rows][D] bf16 tile stores the 16-byte chunk c of row r
+// at chunk position c ^ f(r), so that the 32 (or 16) rows touched by one MFMA
+// operand read land in distinct LDS banks.
+// ---------------------------------------------------------------------------
+template <int D>
+__device__ __forceinline__ int swz_chunk(int r, int c) {
+  return D == 128 ? (c ^ (r & 15)) : (c ^ ((r >> 1) & 7));
+}
+
+// Global byte offsets (relative to the tile's first row) of the 16-byte chunks a
+// wave moves with its DMA loads: load i of wave w fills LDS slots
+// [(i * nwaves + w) * 64, +64), and slot s holds logical chunk swz(r, s % CPR) of
+// row r = s / CPR.
+template <int D, int NDMA>
+__device__ __forceinline__ void tile_dma_offsets(uint32_t (&off)[NDMA], int wave, int nwaves,
+                                                 int lane) {
+#pragma unroll
+  for (int i = 0; i < NDMA; ++i) {
+    const int slot = (i * nwaves + wave) * 64 + lane;
+    const int r = slot / (D / 8);
+    off[i] = (uint32_t)(r * D * 2 + swz_chunk<D>(r, slot % (D / 8)) * 16);
+  }
+}
+
+// Element offsets of a lane's plain MFMA-operand reads from a swizzled tile:
+// row `row` (the lane's M or N index), contraction chunk 2s+h (elements 16s+8h..+7).
+template <int D>
+__device__ __forceinline__ void tile_row_offsets(int (&off)[D / 16], int row, int h) {
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s) off[s] = row * D + swz_chunk<D>(row, 2 * s + h) * 8;
+}
+
+// Element offsets of a lane's transposing reads from a swizzled tile, giving the
+// A operand X^T (rows = head dims, contraction = tile rows) of a 32x32x16 MFMA:
+// for 16-row chunk 0, half k2 (rows 8*k2 + 4*h + 0..3) and 32-dim block db.  Add
+// 16 * D * chunk for later chunks (the swizzle repeats every 16 rows).
+template <int D>
+__device__ __forceinline__ void tile_tr_offsets(int (&off)[2][D / 32], int lane) {
+  const int g16 = lane >> 4, j16 = lane & 15;
+#pragma unroll
+  for (int k2 = 0; k2 < 2; ++k2) {
+    const int r = 8 * k2 + 4 * (g16 >> 1) + (j16 >> 2);
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+      const int e = db * 32 + 16 * (g16 & 1) + 4 * (j16 & 3);
+      off[k2][db] = r * D + swz_chunk<D>(r, e >> 3) * 8 + (e & 7);
+    }
+  }
+}
+
+// The A operand X^T[db block][16-row chunk c] from a swizzled tile.
+template <int D>
+__device__ __forceinline__ bf16x8 tile_tr_operand(const bf16* tile, const int (&off)[2][D / 32],
+                                                  int c, int db) {
+  const bf16x4 lo = lds_read_tr16(tile + c * 16 * D + off[0][db]);
+  const bf16x4 hi = lds_read_tr16(tile + c * 16 * D + off[1][db]);
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
 }  // namespace fox
