@@ -20,6 +20,8 @@
 // The forget-gate bias is formed relative to c_ref (the first query of the
 // block for dq, the first key of the block for dkdv), exactly as in the forward:
 //     log2 P_ij = s log2(e) q_i.k_j + log2(e) ((c_i - c_ref) - LSE_i) - log2(e) (c_j - c_ref).
+#include <type_traits>
+
 #include "fox_device.h"
 #include "fox_internal.h"
 
@@ -213,13 +215,23 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
 }
 
 // ---------------------------------------------------------------------------
-// bf16 dkdv kernel: 32 keys per wave, KV_WAVES waves per workgroup; 64-query tiles
-// of Q and dO double-buffered in LDS through DMA loads.
+// bf16 dkdv kernel: 32 keys per wave (K, V rows of the wave in registers),
+// 4 waves per workgroup; 64-query tiles of Q and dO double-buffered in LDS
+// through DMA loads.  The query-tile loop is unrolled by two so that every LDS
+// address is a per-lane base plus an immediate offset.
 // ---------------------------------------------------------------------------
 constexpr int kKvWaves = 4;
 constexpr int kKvThreads = 64 * kKvWaves;
 constexpr int kKvBN = 32 * kKvWaves;  // keys per workgroup
 constexpr int kKvBM = 64;             // queries per tile
+
+template <int D>
+struct KvSmem {
+  bf16 q[2][kKvBM * D];
+  bf16 g[2][kKvBM * D];
+  float bq[2][kKvBM];
+  float dl[2][kKvBM];
+};
 
 template <int D>
 __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
@@ -229,10 +241,7 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
     float* __restrict__ dck, int BH, int L, float scale, float scale_log2) {
   constexpr int TILE = kKvBM * D;
   constexpr int NDMA = TILE * 2 / 1024 / kKvWaves;
-  __shared__ __attribute__((aligned(16))) bf16 qs[2][TILE];
-  __shared__ __attribute__((aligned(16))) bf16 gs[2][TILE];
-  __shared__ __attribute__((aligned(16))) float bqs[2][kKvBM];
-  __shared__ __attribute__((aligned(16))) float dls[2][kKvBM];
+  __shared__ __attribute__((aligned(16))) KvSmem<D> sm;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = lane >> 5, col = lane & 31;
@@ -287,92 +296,104 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
   const int t_end = (L + kKvBM - 1) / kKvBM;
   const int t_diag = kw0 / kKvBM;  // tile holding this wave's diagonal
 
-  auto issue_tile = [&](int qt) {
-    const int buf = qt & 1;
+  float breg = 0.0f, dreg = 0.0f;
+  auto issue_tile = [&](int qt, auto bufc) {
+    constexpr int B = decltype(bufc)::value;
     const uint32_t base = (uint32_t)qt * kKvBM * D * 2;
 #pragma unroll
     for (int i = 0; i < NDMA; ++i) {
       const int wslot = (i * kKvWaves + wave) * 512;
-      dma16(rq, &qs[buf][wslot], base + dma_off[i]);
-      dma16(rg, &gs[buf][wslot], base + dma_off[i]);
+      dma16(rq, &sm.q[B][wslot], base + dma_off[i]);
+      dma16(rg, &sm.g[B][wslot], base + dma_off[i]);
+    }
+    if (wave == 0) {
+      const int qq = qt * kKvBM + lane;
+      breg = -INFINITY;
+      dreg = 0.0f;
+      if (qq < L) {
+        breg = ((Ch[qq] - c_ref) - Lh[qq]) * kLog2e;
+        dreg = Dh[qq];
+      }
     }
   };
-  float breg = 0.0f, dreg = 0.0f;
-  auto load_rows = [&](int qt) {
-    const int qq = qt * kKvBM + lane;
-    breg = -INFINITY;
-    dreg = 0.0f;
-    if (qq < L) {
-      breg = ((Ch[qq] - c_ref) - Lh[qq]) * kLog2e;
-      dreg = Dh[qq];
+  auto store_rows = [&](auto bufc) {
+    constexpr int B = decltype(bufc)::value;
+    if (wave == 0) {
+      sm.bq[B][lane] = breg;
+      sm.dl[B][lane] = dreg;
     }
-  };
-  auto store_rows = [&](int buf) {
-    bqs[buf][lane] = breg;
-    dls[buf][lane] = dreg;
   };
 
-  issue_tile(t_first);
-  if (wave == 0) {
-    load_rows(t_first);
-    store_rows(t_first & 1);
-  }
-  for (int qt = t_first; qt < t_end; ++qt) {
-    wait_all_memory();
-    __syncthreads();
-    if (qt + 1 < t_end) {
-      issue_tile(qt + 1);
-      if (wave == 0) load_rows(qt + 1);
-    }
-    if (qt >= t_diag) {
-      const int buf = qt & 1;
-      const bf16* qt_ = qs[buf];
-      const bf16* gt_ = gs[buf];
-      const float* bq_ = bqs[buf];
-      const float* dl_ = dls[buf];
-      const int qs0 = qt * kKvBM;
+  auto tile_body = [&](int qt, auto bufc, auto masked) {
+    constexpr int B = decltype(bufc)::value;
+    constexpr bool MASK = decltype(masked)::value;
+    const bf16* qt_ = sm.q[B];
+    const bf16* gt_ = sm.g[B];
+    const float* bq_ = sm.bq[B];
+    const float* dl_ = sm.dl[B];
+    const int qs0 = qt * kKvBM;
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        f32x16 sacc, pacc;
+    for (int qb = 0; qb < 2; ++qb) {
+      f32x16 sacc, pacc;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          sacc[r] = 0.0f;
-          pacc[r] = 0.0f;
+      for (int r = 0; r < 16; ++r) {
+        sacc[r] = 0.0f;
+        pacc[r] = 0.0f;
+      }
+#pragma unroll
+      for (int s = 0; s < D / 16; ++s) {
+        sacc = mfma32(*reinterpret_cast<const bf16x8*>(qt_ + qb * 32 * D + roff[s]), kf[s], sacc);
+        pacc = mfma32(*reinterpret_cast<const bf16x8*>(gt_ + qb * 32 * D + roff[s]), vf[s], pacc);
+      }
+      float pv[16], dsv[16];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int ql = qb * 32 + 8 * g + 4 * h;
+        const f32x4 bq4 = *reinterpret_cast<const f32x4*>(bq_ + ql);
+        const f32x4 dl4 = *reinterpret_cast<const f32x4*>(dl_ + ql);
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          float p = exp2_fast(sacc[4 * g + jj] * scale_log2 + (bq4[jj] - ck2));
+          if (MASK && kj > qs0 + ql + jj) p = 0.0f;
+          const float ds = p * (pacc[4 * g + jj] - dl4[jj]);
+          dck_part -= ds;
+          pv[4 * g + jj] = p;
+          dsv[4 * g + jj] = ds;
         }
+      }
 #pragma unroll
-        for (int s = 0; s < D / 16; ++s) {
-          sacc = mfma32(*reinterpret_cast<const bf16x8*>(qt_ + qb * 32 * D + roff[s]), kf[s], sacc);
-          pacc = mfma32(*reinterpret_cast<const bf16x8*>(gt_ + qb * 32 * D + roff[s]), vf[s], pacc);
-        }
-        float pv[16], dsv[16];
+      for (int c = 0; c < 2; ++c) {
+        const bf16x8 pb = pack8(&pv[8 * c]);
+        const bf16x8 dsb = pack8(&dsv[8 * c]);
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int ql = qb * 32 + 8 * g + 4 * h;
-          const f32x4 bq4 = *reinterpret_cast<const f32x4*>(bq_ + ql);
-          const f32x4 dl4 = *reinterpret_cast<const f32x4*>(dl_ + ql);
-#pragma unroll
-          for (int jj = 0; jj < 4; ++jj) {
-            float p = exp2_fast(sacc[4 * g + jj] * scale_log2 + bq4[jj] - ck2);
-            if (qt == t_diag && kj > qs0 + ql + jj) p = 0.0f;
-            const float ds = p * (pacc[4 * g + jj] - dl4[jj]);
-            dck_part -= ds;
-            pv[4 * g + jj] = p;
-            dsv[4 * g + jj] = ds;
-          }
-        }
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-          const bf16x8 pb = pack8(&pv[8 * c]);
-          const bf16x8 dsb = pack8(&dsv[8 * c]);
-#pragma unroll
-          for (int db = 0; db < D / 32; ++db) {
-            dvacc[db] = mfma32(tile_tr_operand<D>(gt_, toff, 2 * qb + c, db), pb, dvacc[db]);
-            dkacc[db] = mfma32(tile_tr_operand<D>(qt_, toff, 2 * qb + c, db), dsb, dkacc[db]);
-          }
+        for (int db = 0; db < D / 32; ++db) {
+          dvacc[db] = mfma32(tile_tr_operand<D>(gt_, toff, 2 * qb + c, db), pb, dvacc[db]);
+          dkacc[db] = mfma32(tile_tr_operand<D>(qt_, toff, 2 * qb + c, db), dsb, dkacc[db]);
         }
       }
     }
-    if (qt + 1 < t_end && wave == 0) store_rows((qt + 1) & 1);
+  };
+
+  // one query tile held in buffer B; the next tile goes to buffer 1 - B
+  auto step = [&](int qt, auto bufc) {
+    constexpr int B = decltype(bufc)::value;
+    wait_all_memory();
+    __syncthreads();  // tile qt is in LDS; every wave is done with tile qt - 1
+    const bool more = qt + 1 < t_end;
+    if (more) issue_tile(qt + 1, std::integral_constant<int, 1 - B>());
+    if (qt == t_diag) {
+      tile_body(qt, bufc, std::true_type());
+    } else if (qt > t_diag) {
+      tile_body(qt, bufc, std::false_type());
+    }
+    if (more) store_rows(std::integral_constant<int, 1 - B>());
+  };
+
+  issue_tile(t_first, std::integral_constant<int, 0>());
+  store_rows(std::integral_constant<int, 0>());
+  for (int qt = t_first; qt < t_end; qt += 2) {
+    step(qt, std::integral_constant<int, 0>());
+    if (qt + 1 < t_end) step(qt + 1, std::integral_constant<int, 1>());
   }
 
   const float dck_tot = wave_sum_pair(dck_part);
