@@ -234,7 +234,7 @@ struct KvSmem {
 };
 
 template <int D>
-__global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
+__global__ __launch_bounds__(kKvThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) void bwd_dkdv_bf16_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
     const float* __restrict__ C, const float* __restrict__ LSE, const bf16* __restrict__ dO,
     const float* __restrict__ delta, bf16* __restrict__ dK, bf16* __restrict__ dV,
@@ -340,10 +340,17 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
         sacc[r] = 0.0f;
         pacc[r] = 0.0f;
       }
+      // all operand fragments of this sub-block first, so the reads overlap
+      bf16x8 qa[D / 16], ga[D / 16];
 #pragma unroll
       for (int s = 0; s < D / 16; ++s) {
-        sacc = mfma32(*reinterpret_cast<const bf16x8*>(qt_ + qb * 32 * D + roff[s]), kf[s], sacc);
-        pacc = mfma32(*reinterpret_cast<const bf16x8*>(gt_ + qb * 32 * D + roff[s]), vf[s], pacc);
+        qa[s] = *reinterpret_cast<const bf16x8*>(qt_ + qb * 32 * D + roff[s]);
+        ga[s] = *reinterpret_cast<const bf16x8*>(gt_ + qb * 32 * D + roff[s]);
+      }
+#pragma unroll
+      for (int s = 0; s < D / 16; ++s) {
+        sacc = mfma32(qa[s], kf[s], sacc);
+        pacc = mfma32(ga[s], vf[s], pacc);
       }
       float pv[16], dsv[16];
 #pragma unroll
@@ -365,10 +372,16 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
       for (int c = 0; c < 2; ++c) {
         const bf16x8 pb = pack8(&pv[8 * c]);
         const bf16x8 dsb = pack8(&dsv[8 * c]);
+        bf16x8 ta[D / 32], tb[D / 32];
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) {
-          dvacc[db] = mfma32(tile_tr_operand<D>(gt_, toff, 2 * qb + c, db), pb, dvacc[db]);
-          dkacc[db] = mfma32(tile_tr_operand<D>(qt_, toff, 2 * qb + c, db), dsb, dkacc[db]);
+          ta[db] = tile_tr_operand<D>(gt_, toff, 2 * qb + c, db);
+          tb[db] = tile_tr_operand<D>(qt_, toff, 2 * qb + c, db);
+        }
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) {
+          dvacc[db] = mfma32(ta[db], pb, dvacc[db]);
+          dkacc[db] = mfma32(tb[db], dsb, dkacc[db]);
         }
       }
     }
