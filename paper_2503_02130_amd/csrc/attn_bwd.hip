@@ -54,12 +54,20 @@ __global__ __launch_bounds__(256) void bwd_delta_kernel(const T* __restrict__ O,
 
 // ---------------------------------------------------------------------------
 // bf16 dq kernel: 128 queries per workgroup (4 waves x 32), 64-key tiles
-// double-buffered in LDS through DMA loads, diagonal tile first.
+// double-buffered in LDS through DMA loads, diagonal tile first.  The tile loop
+// is unrolled by two so every LDS address is a per-lane base plus an immediate.
 // ---------------------------------------------------------------------------
 constexpr int kBwdThreads = 256;
 constexpr int kDqWaves = 4;
 constexpr int kDqBM = 32 * kDqWaves;
 constexpr int kDqBN = 64;
+
+template <int D>
+struct DqSmem {
+  bf16 k[2][kDqBN * D];
+  bf16 v[2][kDqBN * D];
+  float c[2][kDqBN];
+};
 
 template <int D>
 __global__ __launch_bounds__(kBwdThreads) __attribute__((amdgpu_waves_per_eu(2)))
@@ -71,9 +79,7 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
                         float scale_log2) {
   constexpr int TILE = kDqBN * D;
   constexpr int NDMA = TILE * 2 / 1024 / kDqWaves;
-  __shared__ __attribute__((aligned(16))) bf16 ks[2][TILE];
-  __shared__ __attribute__((aligned(16))) bf16 vs[2][TILE];
-  __shared__ __attribute__((aligned(16))) float cks[2][kDqBN];
+  __shared__ __attribute__((aligned(16))) DqSmem<D> sm;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = lane >> 5, col = lane & 31;
@@ -124,77 +130,100 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
   const int t_last = (kend + kDqBN - 1) / kDqBN - 1;
   const int t_diag = qw0 / kDqBN;
 
-  auto issue_tile = [&](int kt) {
-    const int buf = kt & 1;
+  float creg = 0.0f;
+  auto issue_tile = [&](int kt, auto bufc) {
+    constexpr int B = decltype(bufc)::value;
     const uint32_t base = (uint32_t)kt * kDqBN * D * 2;
 #pragma unroll
     for (int i = 0; i < NDMA; ++i) {
       const int wslot = (i * kDqWaves + wave) * 512;
-      dma16(rk, &ks[buf][wslot], base + dma_off[i]);
-      dma16(rv, &vs[buf][wslot], base + dma_off[i]);
+      dma16(rk, &sm.k[B][wslot], base + dma_off[i]);
+      dma16(rv, &sm.v[B][wslot], base + dma_off[i]);
+    }
+    if (wave == 0) {
+      const int key = kt * kDqBN + lane;
+      creg = key < L ? (Ch[key] - c_ref) * kLog2e : INFINITY;
     }
   };
-  float creg = 0.0f;
-  auto load_c = [&](int kt) {
-    const int key = kt * kDqBN + lane;
-    creg = key < L ? (Ch[key] - c_ref) * kLog2e : INFINITY;
+  auto store_c = [&](auto bufc) {
+    constexpr int B = decltype(bufc)::value;
+    if (wave == 0) sm.c[B][lane] = creg;
   };
 
-  issue_tile(t_last);
-  if (wave == 0) {
-    load_c(t_last);
-    cks[t_last & 1][lane] = creg;
-  }
-  for (int j = t_last; j >= 0; --j) {
-    wait_all_memory();
-    __syncthreads();
-    if (j > 0) {
-      issue_tile(j - 1);
-      if (wave == 0) load_c(j - 1);
-    }
-    if (j <= t_diag) {
-      const int buf = j & 1;
-      const bf16* kt_ = ks[buf];
-      const bf16* vt_ = vs[buf];
-      const float* ct_ = cks[buf];
-      const int key0 = j * kDqBN;
-      bf16x8 dsb[4];
+  auto tile_body = [&](int j, auto bufc, auto masked) {
+    constexpr int B = decltype(bufc)::value;
+    constexpr bool MASK = decltype(masked)::value;
+    const bf16* kt_ = sm.k[B];
+    const bf16* vt_ = sm.v[B];
+    const float* ct_ = sm.c[B];
+    const int key0 = j * kDqBN;
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        f32x16 sacc, pacc;
+    for (int kb = 0; kb < 2; ++kb) {
+      f32x16 sacc, pacc;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          sacc[r] = 0.0f;
-          pacc[r] = 0.0f;
+      for (int r = 0; r < 16; ++r) {
+        sacc[r] = 0.0f;
+        pacc[r] = 0.0f;
+      }
+      {
+        bf16x8 ka[D / 16];
+#pragma unroll
+        for (int s = 0; s < D / 16; ++s)
+          ka[s] = *reinterpret_cast<const bf16x8*>(kt_ + kb * 32 * D + roff[s]);
+#pragma unroll
+        for (int s = 0; s < D / 16; ++s) sacc = mfma32(ka[s], qf[s], sacc);
+      }
+      {
+        bf16x8 va[D / 16];
+#pragma unroll
+        for (int s = 0; s < D / 16; ++s)
+          va[s] = *reinterpret_cast<const bf16x8*>(vt_ + kb * 32 * D + roff[s]);
+#pragma unroll
+        for (int s = 0; s < D / 16; ++s) pacc = mfma32(va[s], dof[s], pacc);
+      }
+      float dsv[16];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 ck4 = *reinterpret_cast<const f32x4*>(ct_ + kb * 32 + 8 * g + 4 * h);
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          float p = exp2_fast(sacc[4 * g + jj] * scale_log2 + (bias2 - ck4[jj]));
+          if (MASK && key0 + kb * 32 + 8 * g + 4 * h + jj > qi) p = 0.0f;
+          const float ds = p * (pacc[4 * g + jj] - dlt);
+          dcq_part += ds;
+          dsv[4 * g + jj] = ds;
         }
-#pragma unroll
-        for (int s = 0; s < D / 16; ++s) {
-          sacc = mfma32(*reinterpret_cast<const bf16x8*>(kt_ + kb * 32 * D + roff[s]), qf[s], sacc);
-          pacc = mfma32(*reinterpret_cast<const bf16x8*>(vt_ + kb * 32 * D + roff[s]), dof[s], pacc);
-        }
-        float dsv[16];
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const f32x4 ck4 = *reinterpret_cast<const f32x4*>(ct_ + kb * 32 + 8 * g + 4 * h);
-#pragma unroll
-          for (int jj = 0; jj < 4; ++jj) {
-            float p = exp2_fast(sacc[4 * g + jj] * scale_log2 - ck4[jj] + bias2);
-            if (j == t_diag && key0 + kb * 32 + 8 * g + 4 * h + jj > qi) p = 0.0f;
-            const float ds = p * (pacc[4 * g + jj] - dlt);
-            dcq_part += ds;
-            dsv[4 * g + jj] = ds;
-          }
-        }
-        dsb[2 * kb] = pack8(&dsv[0]);
-        dsb[2 * kb + 1] = pack8(&dsv[8]);
       }
 #pragma unroll
-      for (int c = 0; c < 4; ++c)
+      for (int c = 0; c < 2; ++c) {
+        const bf16x8 dsb = pack8(&dsv[8 * c]);
+        bf16x8 ta[D / 32];
 #pragma unroll
-        for (int db = 0; db < D / 32; ++db)
-          dqacc[db] = mfma32(tile_tr_operand<D>(kt_, toff, c, db), dsb[c], dqacc[db]);
+        for (int db = 0; db < D / 32; ++db) ta[db] = tile_tr_operand<D>(kt_, toff, 2 * kb + c, db);
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) dqacc[db] = mfma32(ta[db], dsb, dqacc[db]);
+      }
     }
-    if (j > 0 && wave == 0) cks[(j - 1) & 1][lane] = creg;
+  };
+
+  auto step = [&](int j, auto bufc) {
+    constexpr int B = decltype(bufc)::value;
+    wait_all_memory();
+    __syncthreads();  // tile j is in LDS; every wave is done with tile j + 1
+    if (j > 0) issue_tile(j - 1, std::integral_constant<int, 1 - B>());
+    if (j == t_diag) {
+      tile_body(j, bufc, std::true_type());
+    } else if (j < t_diag) {
+      tile_body(j, bufc, std::false_type());
+    }
+    if (j > 0) store_c(std::integral_constant<int, 1 - B>());
+  };
+
+  issue_tile(t_last, std::integral_constant<int, 0>());
+  store_c(std::integral_constant<int, 0>());
+  for (int j = t_last; j >= 0; j -= 2) {
+    step(j, std::integral_constant<int, 0>());
+    if (j > 0) step(j - 1, std::integral_constant<int, 1>());
   }
 
   const float dcq_tot = wave_sum_pair(dcq_part);
@@ -234,7 +263,7 @@ struct KvSmem {
 };
 
 template <int D>
-__global__ __launch_bounds__(kKvThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) void bwd_dkdv_bf16_kernel(
+__global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
     const float* __restrict__ C, const float* __restrict__ LSE, const bf16* __restrict__ dO,
     const float* __restrict__ delta, bf16* __restrict__ dK, bf16* __restrict__ dV,

@@ -36,6 +36,8 @@
 // bias c_i - c_j is formed in natural-log units before the change to base 2, so
 // the row maximum stays small and the logsumexp carries no cancellation even
 // when c changes by thousands within a block.
+#include <type_traits>
+
 #include "fox_device.h"
 #include "fox_internal.h"
 
@@ -48,6 +50,13 @@ constexpr int kFwdBN = 64;              // keys per tile
 constexpr float kRescaleSlack = 8.0f;   // log2 headroom before O and l are rescaled
 
 template <int D>
+struct FwdSmem {
+  bf16 k[2][kFwdBN * D];
+  bf16 v[2][kFwdBN * D];
+  float c[2][kFwdBN];
+};
+
+template <int D>
 __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
                      const bf16* __restrict__ V, const float* __restrict__ C,
@@ -55,9 +64,7 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
                      float scale_log2) {
   constexpr int TILE = kFwdBN * D;                         // bf16 elements per tile
   constexpr int NDMA = TILE * 2 / 1024 / kFwdWaves;        // 1 KB DMA loads per wave per tile
-  __shared__ __attribute__((aligned(16))) bf16 ks[2][TILE];
-  __shared__ __attribute__((aligned(16))) bf16 vs[2][TILE];
-  __shared__ __attribute__((aligned(16))) float cks[2][kFwdBN];
+  __shared__ __attribute__((aligned(16))) FwdSmem<D> sm;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = lane >> 5, col = lane & 31;
@@ -103,96 +110,105 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
   const int t_last = (kend + kFwdBN - 1) / kFwdBN - 1;
   const int t_diag = qw0 / kFwdBN;  // tile holding this wave's diagonal
 
-  auto issue_tile = [&](int kt) {
-    const int buf = kt & 1;
+  float creg = 0.0f;
+  auto issue_tile = [&](int kt, auto bufc) {
+    constexpr int B = decltype(bufc)::value;
     const uint32_t base = (uint32_t)kt * kFwdBN * D * 2;
 #pragma unroll
     for (int i = 0; i < NDMA; ++i) {
       const int wslot = (i * kFwdWaves + wave) * 512;  // bf16 elements of this wave's 1 KB
-      dma16(rk, &ks[buf][wslot], base + dma_off[i]);
-      dma16(rv, &vs[buf][wslot], base + dma_off[i]);
+      dma16(rk, &sm.k[B][wslot], base + dma_off[i]);
+      dma16(rv, &sm.v[B][wslot], base + dma_off[i]);
+    }
+    if (wave == 0) {
+      const int key = kt * kFwdBN + lane;
+      creg = key < L ? (Ch[key] - c_ref) * kLog2e : INFINITY;
     }
   };
-  float creg = 0.0f;
-  auto load_c = [&](int kt) {
-    const int key = kt * kFwdBN + lane;
-    creg = key < L ? (Ch[key] - c_ref) * kLog2e : INFINITY;
+  auto store_c = [&](auto bufc) {
+    constexpr int B = decltype(bufc)::value;
+    if (wave == 0) sm.c[B][lane] = creg;
   };
 
-  issue_tile(t_last);
-  if (wave == 0) {
-    load_c(t_last);
-    cks[t_last & 1][lane] = creg;
-  }
+  auto tile_body = [&](int j, auto bufc, auto masked) {
+    constexpr int B = decltype(bufc)::value;
+    constexpr bool MASK = decltype(masked)::value;
+    const bf16* kt_ = sm.k[B];
+    const bf16* vt_ = sm.v[B];
+    const float* ct_ = sm.c[B];
+    const int key0 = j * kFwdBN;
+    float u[32];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      bf16x8 ka[D / 16];
+#pragma unroll
+      for (int s = 0; s < D / 16; ++s)
+        ka[s] = *reinterpret_cast<const bf16x8*>(kt_ + kb * 32 * D + koff[s]);
+      f32x16 acc;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
+#pragma unroll
+      for (int s = 0; s < D / 16; ++s) acc = mfma32(ka[s], qf[s], acc);
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 ck4 = *reinterpret_cast<const f32x4*>(ct_ + kb * 32 + 8 * g + 4 * h);
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          float x = acc[4 * g + jj] * scale_log2 - ck4[jj];
+          if (MASK && key0 + kb * 32 + 8 * g + 4 * h + jj > qi) x = -INFINITY;
+          u[kb * 16 + 4 * g + jj] = x;
+        }
+      }
+    }
+    float mt = u[0];
+#pragma unroll
+    for (int r = 1; r < 32; ++r) mt = fmaxf(mt, u[r]);
+    mt = wave_max_pair(mt);
+    if (__any(mt > m_used + kRescaleSlack)) {
+      const float m_new = fmaxf(m_used, mt);
+      const float alpha = exp2_fast(m_used - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) oacc[db] *= alpha;
+      m_used = m_new;
+    }
+    const float m_ref = m_used == -INFINITY ? 0.0f : m_used;  // rows past the end only
+    float psum = 0.0f;
+#pragma unroll
+    for (int r = 0; r < 32; ++r) {
+      u[r] = exp2_fast(u[r] - m_ref);
+      psum += u[r];
+    }
+    l_run += psum;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const bf16x8 pb = pack8(&u[8 * c]);
+      bf16x8 va[D / 32];
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) va[db] = tile_tr_operand<D>(vt_, voff, c, db);
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) oacc[db] = mfma32(va[db], pb, oacc[db]);
+    }
+  };
 
-  for (int j = t_last; j >= 0; --j) {
+  auto step = [&](int j, auto bufc) {
+    constexpr int B = decltype(bufc)::value;
     wait_all_memory();
     __syncthreads();  // tile j is in LDS; every wave is done with tile j + 1
-    if (j > 0) {
-      issue_tile(j - 1);
-      if (wave == 0) load_c(j - 1);
+    if (j > 0) issue_tile(j - 1, std::integral_constant<int, 1 - B>());
+    if (j == t_diag) {
+      tile_body(j, bufc, std::true_type());
+    } else if (j < t_diag) {
+      tile_body(j, bufc, std::false_type());
     }
-    if (j <= t_diag) {
-      const int buf = j & 1;
-      const bf16* kt_ = ks[buf];
-      const bf16* vt_ = vs[buf];
-      const float* ct_ = cks[buf];
-      const int key0 = j * kFwdBN;
-      float u[32];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        f32x16 acc;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
-#pragma unroll
-        for (int s = 0; s < D / 16; ++s) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(kt_ + kb * 32 * D + koff[s]);
-          acc = mfma32(a, qf[s], acc);
-        }
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const f32x4 ck4 = *reinterpret_cast<const f32x4*>(ct_ + kb * 32 + 8 * g + 4 * h);
-#pragma unroll
-          for (int jj = 0; jj < 4; ++jj) u[kb * 16 + 4 * g + jj] = acc[4 * g + jj] * scale_log2 - ck4[jj];
-        }
-      }
-      if (j == t_diag) {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            if (key0 + kb * 32 + mfma_row(r, h) > qi) u[kb * 16 + r] = -INFINITY;
-      }
-      float mt = u[0];
-#pragma unroll
-      for (int r = 1; r < 32; ++r) mt = fmaxf(mt, u[r]);
-      mt = wave_max_pair(mt);
-      if (__any(mt > m_used + kRescaleSlack)) {
-        const float m_new = fmaxf(m_used, mt);
-        const float alpha = exp2_fast(m_used - m_new);
-        l_run *= alpha;
-#pragma unroll
-        for (int db = 0; db < D / 32; ++db) oacc[db] *= alpha;
-        m_used = m_new;
-      }
-      const float m_ref = m_used == -INFINITY ? 0.0f : m_used;  // rows past the end only
-      float psum = 0.0f;
-#pragma unroll
-      for (int r = 0; r < 32; ++r) {
-        u[r] = exp2_fast(u[r] - m_ref);
-        psum += u[r];
-      }
-      l_run += psum;
-      bf16x8 pb[4];
-#pragma unroll
-      for (int c = 0; c < 4; ++c) pb[c] = pack8(&u[8 * c]);
-#pragma unroll
-      for (int c = 0; c < 4; ++c)
-#pragma unroll
-        for (int db = 0; db < D / 32; ++db)
-          oacc[db] = mfma32(tile_tr_operand<D>(vt_, voff, c, db), pb[c], oacc[db]);
-    }
-    if (j > 0 && wave == 0) cks[(j - 1) & 1][lane] = creg;
+    if (j > 0) store_c(std::integral_constant<int, 1 - B>());
+  };
+
+  issue_tile(t_last, std::integral_constant<int, 0>());
+  store_c(std::integral_constant<int, 0>());
+  for (int j = t_last; j >= 0; j -= 2) {
+    step(j, std::integral_constant<int, 0>());
+    if (j > 0) step(j - 1, std::integral_constant<int, 1>());
   }
 
   const float l_tot = wave_sum_pair(l_run);
