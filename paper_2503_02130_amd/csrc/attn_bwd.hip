@@ -189,6 +189,9 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
         for (int jj = 0; jj < 4; ++jj) {
           float p = exp2_fast(sacc[4 * g + jj] * scale_log2 + (bias2 - ck4[jj]));
           if (MASK && key0 + kb * 32 + 8 * g + 4 * h + jj > qi) p = 0.0f;
+          // P rounded to bf16 exactly as the dkdv kernel sees it, so that the row
+          // sums (dc^q) and column sums (dc^k) of dS come from the same matrix
+          p = to_f32(to_bf16(p));
           const float ds = p * (pacc[4 * g + jj] - dlt);
           dcq_part += ds;
           dsv[4 * g + jj] = ds;
@@ -244,22 +247,37 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
 }
 
 // ---------------------------------------------------------------------------
-// bf16 dkdv kernel: 32 keys per wave (K, V rows of the wave in registers),
-// 4 waves per workgroup; 64-query tiles of Q and dO double-buffered in LDS
-// through DMA loads.  The query-tile loop is unrolled by two so that every LDS
-// address is a per-lane base plus an immediate offset.
+// bf16 dkdv kernel, split into two wave roles.  Eight waves per workgroup own
+// 128 keys as four pairs of 32; both waves of a pair run on the same SIMD.
+//   P wave (waves 0-3): K rows in registers; for query tile t computes
+//          S = Q K^T, P = exp(S - LSE) with the gate bias and the mask, stores P
+//          (bf16) in LDS, and accumulates dV^T += dO^T P.
+//   G wave (waves 4-7): V rows in registers; one tile behind, for tile t - 1
+//          computes dP = dO V^T, reads P back, dS = P o (dP - Delta),
+//          dc^k -= colsum(dS) and accumulates dK^T += Q^T dS.
+// Each wave holds one D x 32 accumulator, so two waves fit on a SIMD, and the
+// two roles never wait for each other inside a tile: Q / dO tiles, their row
+// statistics and P are triple-buffered (tile t + 1 loads by DMA while P works
+// on t and G on t - 1), with one barrier per tile.  The loop is unrolled by
+// three so every LDS address is a per-lane base plus an immediate.
 // ---------------------------------------------------------------------------
-constexpr int kKvWaves = 4;
+constexpr int kKvWaves = 8;
 constexpr int kKvThreads = 64 * kKvWaves;
-constexpr int kKvBN = 32 * kKvWaves;  // keys per workgroup
-constexpr int kKvBM = 64;             // queries per tile
+constexpr int kKvPairs = kKvWaves / 2;
+constexpr int kKvBN = 32 * kKvPairs;  // keys per workgroup
+// queries per tile: 32 at D = 128 keeps all six tiles within the 64 KB reach of
+// an LDS instruction's immediate offset
+template <int D>
+constexpr int kv_bm() { return D == 128 ? 32 : 64; }
 
 template <int D>
 struct KvSmem {
-  bf16 q[2][kKvBM * D];
-  bf16 g[2][kKvBM * D];
-  float bq[2][kKvBM];
-  float dl[2][kKvBM];
+  static constexpr int BM = kv_bm<D>();
+  bf16 q[3][BM * D];
+  bf16 g[3][BM * D];
+  bf16x8 p[3][kKvPairs][BM / 16][64];  // P of each pair: [16-query chunk][lane], bf16 x 8
+  float bq[3][BM];
+  float dl[3][BM];
 };
 
 template <int D>
@@ -268,12 +286,17 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
     const float* __restrict__ C, const float* __restrict__ LSE, const bf16* __restrict__ dO,
     const float* __restrict__ delta, bf16* __restrict__ dK, bf16* __restrict__ dV,
     float* __restrict__ dck, int BH, int L, float scale, float scale_log2) {
+  constexpr int kKvBM = kv_bm<D>();
+  constexpr int NQB = kKvBM / 32;  // 32-query sub-blocks per tile
   constexpr int TILE = kKvBM * D;
   constexpr int NDMA = TILE * 2 / 1024 / kKvWaves;
+  static_assert(NDMA >= 1, "every wave issues at least one DMA load per tile");
   __shared__ __attribute__((aligned(16))) KvSmem<D> sm;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = lane >> 5, col = lane & 31;
+  const bool pwave = wave < kKvPairs;  // role
+  const int pair = wave % kKvPairs;
   const int bh = blockIdx.x % BH;
   const int nblk = (int)(blockIdx.x / BH);  // key block 0 has the most work: first
   const int k0 = nblk * kKvBN;
@@ -282,7 +305,7 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
   const float* Lh = LSE + head;
   const float* Dh = delta + head;
   const float c_ref = Ch[k0];
-  const int kw0 = k0 + wave * 32;
+  const int kw0 = k0 + pair * 32;
   const int kj = kw0 + col;
   const bool k_valid = kj < L;
   const uint32_t head_bytes = (uint32_t)L * D * 2;
@@ -295,35 +318,32 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
   int toff[2][D / 32];
   tile_tr_offsets<D>(toff, lane);
 
-  bf16x8 kf[D / 16], vf[D / 16];
+  // P waves hold K rows, G waves hold V rows
+  bf16x8 kvf[D / 16];
+  {
+    const bf16* src = (pwave ? K : V) + (head + kj) * D;
 #pragma unroll
-  for (int s = 0; s < D / 16; ++s) {
-    if (k_valid) {
-      kf[s] = *reinterpret_cast<const bf16x8*>(K + (head + kj) * D + 16 * s + 8 * h);
-      vf[s] = *reinterpret_cast<const bf16x8*>(V + (head + kj) * D + 16 * s + 8 * h);
-    } else {
+    for (int s = 0; s < D / 16; ++s) {
+      if (k_valid) {
+        kvf[s] = *reinterpret_cast<const bf16x8*>(src + 16 * s + 8 * h);
+      } else {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        kf[s][e] = to_bf16(0.0f);
-        vf[s][e] = to_bf16(0.0f);
+        for (int e = 0; e < 8; ++e) kvf[s][e] = to_bf16(0.0f);
       }
     }
   }
   const float ck2 = k_valid ? (Ch[kj] - c_ref) * kLog2e : INFINITY;
 
-  f32x16 dkacc[D / 32], dvacc[D / 32];
+  f32x16 acc[D / 32];  // dV^T (P waves) or dK^T (G waves)
 #pragma unroll
   for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      dkacc[db][r] = 0.0f;
-      dvacc[db][r] = 0.0f;
-    }
+    for (int r = 0; r < 16; ++r) acc[db][r] = 0.0f;
   float dck_part = 0.0f;
 
   const int t_first = k0 / kKvBM;
-  const int t_end = (L + kKvBM - 1) / kKvBM;
-  const int t_diag = kw0 / kKvBM;  // tile holding this wave's diagonal
+  const int n_tiles = (L + kKvBM - 1) / kKvBM - t_first;
+  const int t_diag = kw0 / kKvBM;  // tile holding this pair's diagonal
 
   float breg = 0.0f, dreg = 0.0f;
   auto issue_tile = [&](int qt, auto bufc) {
@@ -335,7 +355,7 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
       dma16(rq, &sm.q[B][wslot], base + dma_off[i]);
       dma16(rg, &sm.g[B][wslot], base + dma_off[i]);
     }
-    if (wave == 0) {
+    if (wave == 0 && lane < kKvBM) {
       const int qq = qt * kKvBM + lane;
       breg = -INFINITY;
       dreg = 0.0f;
@@ -347,116 +367,139 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
   };
   auto store_rows = [&](auto bufc) {
     constexpr int B = decltype(bufc)::value;
-    if (wave == 0) {
+    if (wave == 0 && lane < kKvBM) {
       sm.bq[B][lane] = breg;
       sm.dl[B][lane] = dreg;
     }
   };
 
-  auto tile_body = [&](int qt, auto bufc, auto masked) {
+  // P wave on tile qt held in buffer B
+  auto p_tile = [&](int qt, auto bufc, auto masked) {
     constexpr int B = decltype(bufc)::value;
     constexpr bool MASK = decltype(masked)::value;
-    const bf16* qt_ = sm.q[B];
-    const bf16* gt_ = sm.g[B];
-    const float* bq_ = sm.bq[B];
-    const float* dl_ = sm.dl[B];
     const int qs0 = qt * kKvBM;
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-      f32x16 sacc, pacc;
+    for (int qb = 0; qb < NQB; ++qb) {
+      bf16x8 qa[D / 16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        sacc[r] = 0.0f;
-        pacc[r] = 0.0f;
-      }
-      // all operand fragments of this sub-block first, so the reads overlap
-      bf16x8 qa[D / 16], ga[D / 16];
+      for (int s = 0; s < D / 16; ++s)
+        qa[s] = *reinterpret_cast<const bf16x8*>(sm.q[B] + qb * 32 * D + roff[s]);
+      f32x16 sacc;
 #pragma unroll
-      for (int s = 0; s < D / 16; ++s) {
-        qa[s] = *reinterpret_cast<const bf16x8*>(qt_ + qb * 32 * D + roff[s]);
-        ga[s] = *reinterpret_cast<const bf16x8*>(gt_ + qb * 32 * D + roff[s]);
-      }
+      for (int r = 0; r < 16; ++r) sacc[r] = 0.0f;
 #pragma unroll
-      for (int s = 0; s < D / 16; ++s) {
-        sacc = mfma32(qa[s], kf[s], sacc);
-        pacc = mfma32(ga[s], vf[s], pacc);
-      }
-      float pv[16], dsv[16];
+      for (int s = 0; s < D / 16; ++s) sacc = mfma32(qa[s], kvf[s], sacc);
+      float pv[16];
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int ql = qb * 32 + 8 * g + 4 * h;
-        const f32x4 bq4 = *reinterpret_cast<const f32x4*>(bq_ + ql);
-        const f32x4 dl4 = *reinterpret_cast<const f32x4*>(dl_ + ql);
+        const f32x4 bq4 = *reinterpret_cast<const f32x4*>(sm.bq[B] + ql);
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj) {
           float p = exp2_fast(sacc[4 * g + jj] * scale_log2 + (bq4[jj] - ck2));
           if (MASK && kj > qs0 + ql + jj) p = 0.0f;
-          const float ds = p * (pacc[4 * g + jj] - dl4[jj]);
-          dck_part -= ds;
           pv[4 * g + jj] = p;
-          dsv[4 * g + jj] = ds;
         }
       }
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
         const bf16x8 pb = pack8(&pv[8 * c]);
-        const bf16x8 dsb = pack8(&dsv[8 * c]);
-        bf16x8 ta[D / 32], tb[D / 32];
+        sm.p[B][pair][2 * qb + c][lane] = pb;
+        bf16x8 ta[D / 32];
 #pragma unroll
-        for (int db = 0; db < D / 32; ++db) {
-          ta[db] = tile_tr_operand<D>(gt_, toff, 2 * qb + c, db);
-          tb[db] = tile_tr_operand<D>(qt_, toff, 2 * qb + c, db);
-        }
+        for (int db = 0; db < D / 32; ++db)
+          ta[db] = tile_tr_operand<D>(sm.g[B], toff, 2 * qb + c, db);
 #pragma unroll
-        for (int db = 0; db < D / 32; ++db) {
-          dvacc[db] = mfma32(ta[db], pb, dvacc[db]);
-          dkacc[db] = mfma32(tb[db], dsb, dkacc[db]);
+        for (int db = 0; db < D / 32; ++db) acc[db] = mfma32(ta[db], pb, acc[db]);
+      }
+    }
+  };
+  // G wave on tile qt held in buffer B (its P was stored in the same buffer slot)
+  auto g_tile = [&](auto bufc) {
+    constexpr int B = decltype(bufc)::value;
+#pragma unroll
+    for (int qb = 0; qb < NQB; ++qb) {
+      bf16x8 ga[D / 16];
+#pragma unroll
+      for (int s = 0; s < D / 16; ++s)
+        ga[s] = *reinterpret_cast<const bf16x8*>(sm.g[B] + qb * 32 * D + roff[s]);
+      f32x16 pacc;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) pacc[r] = 0.0f;
+#pragma unroll
+      for (int s = 0; s < D / 16; ++s) pacc = mfma32(ga[s], kvf[s], pacc);
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const bf16x8 pb = sm.p[B][pair][2 * qb + c][lane];
+        float dsv[8];
+#pragma unroll
+        for (int g2 = 0; g2 < 2; ++g2) {
+          const int ql = qb * 32 + 8 * (2 * c + g2) + 4 * h;
+          const f32x4 dl4 = *reinterpret_cast<const f32x4*>(sm.dl[B] + ql);
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj) {
+            const float ds = to_f32(pb[4 * g2 + jj]) * (pacc[8 * c + 4 * g2 + jj] - dl4[jj]);
+            dck_part -= ds;
+            dsv[4 * g2 + jj] = ds;
+          }
         }
+        const bf16x8 dsb = pack8(dsv);
+        bf16x8 ta[D / 32];
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+          ta[db] = tile_tr_operand<D>(sm.q[B], toff, 2 * qb + c, db);
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) acc[db] = mfma32(ta[db], dsb, acc[db]);
       }
     }
   };
 
-  // one query tile held in buffer B; the next tile goes to buffer 1 - B
-  auto step = [&](int qt, auto bufc) {
+  // iteration it: the P wave works on tile it (buffer it % 3), the G wave on tile
+  // it - 1 (buffer (it - 1) % 3), and tile it + 1 loads into buffer (it + 1) % 3
+  auto step = [&](int it, auto bufc) {
     constexpr int B = decltype(bufc)::value;
+    constexpr int BN = (B + 1) % 3, BP = (B + 2) % 3;
     wait_all_memory();
-    __syncthreads();  // tile qt is in LDS; every wave is done with tile qt - 1
-    const bool more = qt + 1 < t_end;
-    if (more) issue_tile(qt + 1, std::integral_constant<int, 1 - B>());
-    if (qt == t_diag) {
-      tile_body(qt, bufc, std::true_type());
-    } else if (qt > t_diag) {
-      tile_body(qt, bufc, std::false_type());
+    __syncthreads();  // tile it and P of tile it - 1 are in LDS
+    if (it + 1 < n_tiles) issue_tile(t_first + it + 1, std::integral_constant<int, BN>());
+    if (pwave) {
+      const int qt = t_first + it;
+      if (it < n_tiles) {
+        if (qt == t_diag) p_tile(qt, bufc, std::true_type());
+        else if (qt > t_diag) p_tile(qt, bufc, std::false_type());
+      }
+    } else {
+      const int qt = t_first + it - 1;
+      if (it >= 1 && qt >= t_diag) g_tile(std::integral_constant<int, BP>());
     }
-    if (more) store_rows(std::integral_constant<int, 1 - B>());
+    if (it + 1 < n_tiles) store_rows(std::integral_constant<int, BN>());
   };
 
   issue_tile(t_first, std::integral_constant<int, 0>());
   store_rows(std::integral_constant<int, 0>());
-  for (int qt = t_first; qt < t_end; qt += 2) {
-    step(qt, std::integral_constant<int, 0>());
-    if (qt + 1 < t_end) step(qt + 1, std::integral_constant<int, 1>());
+  for (int it = 0; it <= n_tiles; it += 3) {
+    step(it, std::integral_constant<int, 0>());
+    if (it + 1 <= n_tiles) step(it + 1, std::integral_constant<int, 1>());
+    if (it + 2 <= n_tiles) step(it + 2, std::integral_constant<int, 2>());
   }
 
-  const float dck_tot = wave_sum_pair(dck_part);
   if (k_valid) {
-    bf16* ok = dK + (head + kj) * D;
-    bf16* ov = dV + (head + kj) * D;
+    bf16* out = (pwave ? dV : dK) + (head + kj) * D;
+    const float f = pwave ? 1.0f : scale;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        bf16x4 wk, wv;
+        bf16x4 w;
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-          wk[jj] = to_bf16(dkacc[db][4 * g + jj] * scale);
-          wv[jj] = to_bf16(dvacc[db][4 * g + jj]);
-        }
-        *reinterpret_cast<bf16x4*>(ok + db * 32 + 8 * g + 4 * h) = wk;
-        *reinterpret_cast<bf16x4*>(ov + db * 32 + 8 * g + 4 * h) = wv;
+        for (int jj = 0; jj < 4; ++jj) w[jj] = to_bf16(acc[db][4 * g + jj] * f);
+        *reinterpret_cast<bf16x4*>(out + db * 32 + 8 * g + 4 * h) = w;
       }
     }
-    if (h == 0) dck[head + kj] = dck_tot;
+  }
+  if (!pwave) {
+    const float dck_tot = wave_sum_pair(dck_part);
+    if (k_valid && h == 0) dck[head + kj] = dck_tot;
   }
 }
 

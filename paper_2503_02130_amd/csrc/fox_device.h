@@ -91,12 +91,22 @@ __device__ __forceinline__ bf16x4 lds_read_tr16(const bf16* p) {
 
 // ---------------------------------------------------------------------------
 // Swizzled LDS tiles: a [rows][D] bf16 tile stores the 16-byte chunk c of row r
-// at chunk position c ^ f(r), so that the 32 (or 16) rows touched by one MFMA
-// operand read land in distinct LDS banks.
+// at chunk position c ^ f(r).  Two access patterns must be free of bank
+// conflicts, whether the LDS serves 128 or 256 bytes per cycle:
+//   * plain 16-byte operand reads: 8 (or 16) consecutive rows, same chunk;
+//   * transposing reads: 4 consecutive rows (aligned to 4), 2 (or 4)
+//     consecutive chunks (aligned).
+// With r = (r3 r2 r1 r0) the masks below are linear maps chosen so that both
+// sets of rows/chunks land on distinct chunk positions modulo 8 and 16:
+//   D = 128 (16 chunks per row): f = r2 | r1 << 1 | r0 << 2 | (r3^r1^r0) << 3
+//   D = 64  ( 8 chunks per row): f = r2 | (r0^r3) << 1 | r1 << 2
 // ---------------------------------------------------------------------------
 template <int D>
 __device__ __forceinline__ int swz_chunk(int r, int c) {
-  return D == 128 ? (c ^ (r & 15)) : (c ^ ((r >> 1) & 7));
+  const int r0 = r & 1, r1 = (r >> 1) & 1, r2 = (r >> 2) & 1, r3 = (r >> 3) & 1;
+  const int f = D == 128 ? (r2 | (r1 << 1) | (r0 << 2) | ((r3 ^ r1 ^ r0) << 3))
+                         : (r2 | ((r0 ^ r3) << 1) | (r1 << 2));
+  return c ^ f;
 }
 
 // Global byte offsets (relative to the tile's first row) of the 16-byte chunks a
@@ -125,7 +135,7 @@ __device__ __forceinline__ void tile_row_offsets(int (&off)[D / 16], int row, in
 // Element offsets of a lane's transposing reads from a swizzled tile, giving the
 // A operand X^T (rows = head dims, contraction = tile rows) of a 32x32x16 MFMA:
 // for 16-row chunk 0, half k2 (rows 8*k2 + 4*h + 0..3) and 32-dim block db.  Add
-// 16 * D * chunk for later chunks (the swizzle repeats every 16 rows).
+// 16 * D * chunk for later chunks (the swizzle depends on the row modulo 16).
 template <int D>
 __device__ __forceinline__ void tile_tr_offsets(int (&off)[2][D / 32], int lane) {
   const int g16 = lane >> 4, j16 = lane & 15;
