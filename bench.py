@@ -15,6 +15,7 @@ HBM when the timed region starts.
 from __future__ import annotations
 
 import argparse
+import contextlib
 import json
 import os
 import sys
@@ -70,11 +71,17 @@ class EventTimer:
         self.b.record()
         self.pairs.append((self.a, self.b))
 
+    def maybe(self, on):
+        return self if on else contextlib.nullcontext()
+
     def mean_ms(self):
         return sum(a.elapsed_time(b) for a, b in self.pairs) / max(1, len(self.pairs))
 
 
 def bench_train(w, steps, warmup):
+    """One step = gate prefix -> forward -> backward, the backward through its
+    stage entry points (exactly what fox_attn_bwd runs) so that the dominant
+    kernel, dK/dV, can be bracketed by events on the call stream."""
     dev = torch.device("cuda:0")
     x = inputs.workload_inputs(w, device=dev)
     s = fox.default_scale(w.d)
@@ -83,25 +90,23 @@ def bench_train(w, steps, warmup):
     o = torch.empty_like(x["q"])
     lse = torch.empty((B, H, L), device=dev)
     dq, dk, dv = torch.empty_like(x["q"]), torch.empty_like(x["k"]), torch.empty_like(x["v"])
-    dlf = torch.empty_like(c)
-    ws = torch.empty(fox.fox_attn_bwd_workspace_bytes(x["q"].dtype, B, H, L, d), device=dev,
-                     dtype=torch.uint8)
-    t_gate, t_fwd, t_bwd = EventTimer(), EventTimer(), EventTimer()
+    dlf, delta, dcq, dck = (torch.empty((B, H, L), device=dev) for _ in range(4))
+    t_gate, t_fwd, t_dkdv, t_dq, t_bwd = (EventTimer() for _ in range(5))
 
     def step(timed):
-        if timed:
-            with t_gate:
-                fox.fox_gate_prefix(x["logit"], c=c)
-            with t_fwd:
-                fox.fox_attn_fwd(x["q"], x["k"], x["v"], c, s, o=o, lse=lse)
-            with t_bwd:
-                fox.fox_attn_bwd(x["q"], x["k"], x["v"], c, o, lse, x["do"], s, dq=dq, dk=dk,
-                                 dv=dv, d_log_f=dlf, workspace=ws)
-        else:
+        with t_gate.maybe(timed):
             fox.fox_gate_prefix(x["logit"], c=c)
+        with t_fwd.maybe(timed):
             fox.fox_attn_fwd(x["q"], x["k"], x["v"], c, s, o=o, lse=lse)
-            fox.fox_attn_bwd(x["q"], x["k"], x["v"], c, o, lse, x["do"], s, dq=dq, dk=dk, dv=dv,
-                             d_log_f=dlf, workspace=ws)
+        with t_bwd.maybe(timed):
+            fox.fox_attn_bwd_delta(o, x["do"], delta=delta)
+            with t_dkdv.maybe(timed):
+                fox.fox_attn_bwd_dkdv(x["q"], x["k"], x["v"], c, lse, x["do"], delta, s, dk=dk,
+                                      dv=dv, dc_k=dck)
+            with t_dq.maybe(timed):
+                fox.fox_attn_bwd_dq(x["q"], x["k"], x["v"], c, lse, x["do"], delta, s, dq=dq,
+                                    dc_q=dcq)
+            fox.fox_dlogf_from_dc(dcq, dck, d_log_f=dlf)
 
     for _ in range(warmup):
         step(False)
@@ -119,7 +124,7 @@ def bench_train(w, steps, warmup):
     if not (torch.isfinite(o.float()).all() and torch.isfinite(dlf).all()):
         raise RuntimeError("non-finite outputs")
     return {"ms": ms, "wall_ms": wall_ms, "gate_ms": t_gate.mean_ms(), "fwd_ms": t_fwd.mean_ms(),
-            "bwd_ms": t_bwd.mean_ms()}
+            "bwd_ms": t_bwd.mean_ms(), "dkdv_ms": t_dkdv.mean_ms(), "dq_ms": t_dq.mean_ms()}
 
 
 def bench_decode(w, steps, warmup):
@@ -145,23 +150,23 @@ def bench_decode(w, steps, warmup):
     return {"ms": t.mean_ms()}
 
 
-def cpu_baseline(w, seconds_hint=20.0):
-    """The fp64 oracle, untouched, on a bounded sample: forward + backward of one
-    (batch, head) slice of the workload (1/(B*H) of the step's work)."""
+def cpu_baseline(w, n_heads=4):
+    """The fp64 oracle, untouched, on a bounded sample: forward + backward of
+    n_heads (batch, head) slices of the workload (n_heads / (B*H) of the step)."""
     import oracle
     threads = len(os.sched_getaffinity(0))
     torch.set_num_threads(threads)
-    x = inputs.attn_inputs(1, 1, w.L, w.d, w.dtype, w.gate, w.seed, device="cpu")
+    x = inputs.attn_inputs(1, n_heads, w.L, w.d, w.dtype, w.gate, w.seed, device="cpu")
     s = fox.default_scale(w.d)
     t0 = time.perf_counter()
     oracle.forward(x["q"], x["k"], x["v"], x["logit"], s)
     oracle.backward(x["q"], x["k"], x["v"], x["logit"], x["do"], s)
     dt = time.perf_counter() - t0
-    flops = fwd_flops(1, 1, w.L, w.d) + bwd_flops(1, 1, w.L, w.d)
+    flops = fwd_flops(1, n_heads, w.L, w.d) + bwd_flops(1, n_heads, w.L, w.d)
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": torch.get_num_threads(),
             "kind": "oracle",
-            "sample": f"fp64 forward+backward of 1 of {w.B * w.H} (batch, head) slices at "
-                      f"L={w.L}, d={w.d}: {dt:.1f} s; value scales that slice's causal FLOPs"}
+            "sample": f"fp64 forward+backward of {n_heads} of {w.B * w.H} (batch, head) slices "
+                      f"at L={w.L}, d={w.d}: {dt:.1f} s; value = those slices' causal FLOPs / time"}
 
 
 def main():
@@ -191,6 +196,9 @@ def main():
     tflops = (fl_f + fl_b) / (r["ms"] * 1e-3) / 1e12
     fwd_tf = fl_f / (r["fwd_ms"] * 1e-3) / 1e12
     bwd_tf = fl_b / (r["bwd_ms"] * 1e-3) / 1e12
+    # dK/dV kernel: its 4 GEMMs (S recomputed, dV, dP, dK) are 8d FLOPs per causal pair
+    fl_kv = 8.0 * d * causal_pairs(B, H, L)
+    kv_tf = fl_kv / (r["dkdv_ms"] * 1e-3) / 1e12
     out = {
         "metric": "Forgetting-attn fwd+bwd TFLOP/s bf16 L=16k d=128 (% MFMA peak); decode GB/s",
         "value": round(tflops, 2),
@@ -209,12 +217,16 @@ def main():
                    "flops_per_step": fl_f + fl_b, "parallelism": "none (1 GPU)"},
         "frac_of_peak": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
         "breakdown_ms": {"gate_prefix": round(r["gate_ms"], 4), "fwd": round(r["fwd_ms"], 4),
-                         "bwd": round(r["bwd_ms"], 4), "wall_per_step": round(r["wall_ms"], 4)},
-        "roofline": {"bound": "mfma", "kernel": "fwd_bf16_kernel<128> (fox_attn_fwd)",
-                     "achieved": round(fwd_tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(fwd_tf / MFMA_BF16_PEAK_TFLOPS, 4),
-                     "traffic": None},
-        "roofline_bwd": {"bound": "mfma", "kernels": "fox_attn_bwd (delta, dkdv, dq, scan)",
+                         "bwd": round(r["bwd_ms"], 4), "bwd_dkdv": round(r["dkdv_ms"], 4),
+                         "bwd_dq": round(r["dq_ms"], 4), "wall_per_step": round(r["wall_ms"], 4)},
+        "roofline": {"bound": "mfma", "kernel": "bwd_dkdv_bf16_kernel<128> (fox_attn_bwd_dkdv)",
+                     "achieved": round(kv_tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(kv_tf / MFMA_BF16_PEAK_TFLOPS, 4),
+                     "traffic": None, "algorithmic_flops_per_launch": fl_kv},
+        "roofline_fwd": {"bound": "mfma", "kernel": "fwd_bf16_kernel<128> (fox_attn_fwd)",
+                         "achieved": round(fwd_tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
+                         "unit": "TFLOP/s", "frac": round(fwd_tf / MFMA_BF16_PEAK_TFLOPS, 4)},
+        "roofline_bwd": {"bound": "mfma", "kernels": "fox_attn_bwd stages (delta, dkdv, dq, scan)",
                          "achieved": round(bwd_tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
                          "unit": "TFLOP/s", "frac": round(bwd_tf / MFMA_BF16_PEAK_TFLOPS, 4)},
     }

@@ -109,6 +109,36 @@ int fox_attn_bwd(int dtype, const void* q, const void* k, const void* v, const f
                  void* workspace, size_t workspace_bytes,
                  int B, int H, int L, int d, float scale, void* stream);
 
+/*
+ * The backward pass in stages, for callers that schedule them themselves (for
+ * instance dK/dV and dQ on two streams).  fox_attn_bwd is exactly
+ *     fox_attn_bwd_delta -> fox_attn_bwd_dkdv -> fox_attn_bwd_dq -> fox_dlogf_from_dc
+ * with delta, dc_q and dc_k carved from its workspace.
+ *
+ * fox_attn_bwd_delta: delta_i = sum_d dO_id O_id (Alg. 2, the preprocessing
+ *   rowsum(dO o O), one value per row).  o, d_o [B,H,L,d] dtype; delta [B,H,L] fp32 out.
+ * fox_attn_bwd_dkdv: dK, dV (dtype, overwritten) and dc_k = -colsum(dS) [B,H,L]
+ *   fp32 (overwritten), the key-side half of Alg. 2.
+ * fox_attn_bwd_dq: dQ (dtype, overwritten) and dc_q = rowsum(dS) [B,H,L] fp32
+ *   (overwritten), the query-side half of Alg. 2.
+ * fox_dlogf_from_dc: d(log f)_l = sum_{i>=l} (dc_q_i + dc_k_i), the chain rule
+ *   through c = cumsum(log f) (Alg. 2 returns dc = dc^q + dc^k); [B,H,L] fp32.
+ * Both halves form dS from P rounded to bf16 (bf16 dtype), so that dc_q and dc_k
+ * are the row and column sums of one matrix.  Inputs as for fox_attn_bwd.
+ */
+int fox_attn_bwd_delta(int dtype, const void* o, const void* d_o, float* delta,
+                       int B, int H, int L, int d, void* stream);
+int fox_attn_bwd_dkdv(int dtype, const void* q, const void* k, const void* v, const float* c,
+                      const float* lse, const void* d_o, const float* delta,
+                      void* dk, void* dv, float* dc_k,
+                      int B, int H, int L, int d, float scale, void* stream);
+int fox_attn_bwd_dq(int dtype, const void* q, const void* k, const void* v, const float* c,
+                    const float* lse, const void* d_o, const float* delta,
+                    void* dq, float* dc_q,
+                    int B, int H, int L, int d, float scale, void* stream);
+int fox_dlogf_from_dc(const float* dc_q, const float* dc_k, float* d_log_f,
+                      int B, int H, int L, void* stream);
+
 /* Bytes of workspace fox_attn_decode needs for this shape (0 on invalid arguments). */
 size_t fox_attn_decode_workspace_bytes(int dtype, int B, int H, int T, int d);
 

@@ -24,8 +24,8 @@ _DT = {torch.float32: FOX_DTYPE_F32, torch.bfloat16: FOX_DTYPE_BF16}
 
 EXPORTED = (
     "fox_status_string", "fox_version", "fox_gate_prefix", "fox_attn_fwd",
-    "fox_attn_bwd_workspace_bytes", "fox_attn_bwd", "fox_attn_decode_workspace_bytes",
-    "fox_attn_decode",
+    "fox_attn_bwd_workspace_bytes", "fox_attn_bwd", "fox_attn_bwd_delta", "fox_attn_bwd_dkdv",
+    "fox_attn_bwd_dq", "fox_dlogf_from_dc", "fox_attn_decode_workspace_bytes", "fox_attn_decode",
 )
 
 
@@ -61,6 +61,14 @@ def load() -> ctypes.CDLL:
     lib.fox_attn_bwd_workspace_bytes.argtypes = [I, I, I, I, I]
     lib.fox_attn_bwd.restype = I
     lib.fox_attn_bwd.argtypes = [I, P, P, P, P, P, P, P, P, P, P, P, P, Z, I, I, I, I, F, P]
+    lib.fox_attn_bwd_delta.restype = I
+    lib.fox_attn_bwd_delta.argtypes = [I, P, P, P, I, I, I, I, P]
+    lib.fox_attn_bwd_dkdv.restype = I
+    lib.fox_attn_bwd_dkdv.argtypes = [I, P, P, P, P, P, P, P, P, P, P, I, I, I, I, F, P]
+    lib.fox_attn_bwd_dq.restype = I
+    lib.fox_attn_bwd_dq.argtypes = [I, P, P, P, P, P, P, P, P, P, I, I, I, I, F, P]
+    lib.fox_dlogf_from_dc.restype = I
+    lib.fox_dlogf_from_dc.argtypes = [P, P, P, I, I, I, P]
     lib.fox_attn_decode_workspace_bytes.restype = Z
     lib.fox_attn_decode_workspace_bytes.argtypes = [I, I, I, I, I]
     lib.fox_attn_decode.restype = I
@@ -185,6 +193,82 @@ def fox_attn_bwd(q, k, v, c, o, lse, d_o, scale: Optional[float] = None,
                              B, H, L, d, s, _stream(q))
     _raise(st, "fox_attn_bwd")
     return dq, dk, dv, d_log_f
+
+
+def _check_bwd_inputs(q, k, v, c, lse, d_o):
+    B, H, L, d = q.shape
+    dt = q.dtype
+    if dt not in _DT:
+        raise ValueError(f"unsupported dtype {dt}")
+    dev = q.device
+    for name, t in (("q", q), ("k", k), ("v", v), ("d_o", d_o)):
+        _check(t, name, (B, H, L, d), dt, dev)
+    _check(c, "c", (B, H, L), torch.float32, dev)
+    _check(lse, "lse", (B, H, L), torch.float32, dev)
+    return B, H, L, d, dt, dev
+
+
+def fox_attn_bwd_delta(o, d_o, delta=None):
+    """delta_i = rowsum(dO o O), [B,H,L] fp32."""
+    B, H, L, d = o.shape
+    dt = o.dtype
+    if dt not in _DT:
+        raise ValueError(f"unsupported dtype {dt}")
+    _check(o, "o", (B, H, L, d), dt, None)
+    _check(d_o, "d_o", (B, H, L, d), dt, o.device)
+    delta = torch.empty((B, H, L), device=o.device, dtype=torch.float32) if delta is None else delta
+    _check(delta, "delta", (B, H, L), torch.float32, o.device)
+    st = load().fox_attn_bwd_delta(_DT[dt], _ptr(o), _ptr(d_o), _ptr(delta), B, H, L, d, _stream(o))
+    _raise(st, "fox_attn_bwd_delta")
+    return delta
+
+
+def fox_attn_bwd_dkdv(q, k, v, c, lse, d_o, delta, scale: Optional[float] = None,
+                      dk=None, dv=None, dc_k=None):
+    """dK, dV (q's dtype) and dc_k = -colsum(dS) [B,H,L] fp32."""
+    B, H, L, d, dt, dev = _check_bwd_inputs(q, k, v, c, lse, d_o)
+    _check(delta, "delta", (B, H, L), torch.float32, dev)
+    dk = torch.empty_like(k) if dk is None else dk
+    dv = torch.empty_like(v) if dv is None else dv
+    dc_k = torch.empty_like(c) if dc_k is None else dc_k
+    _check(dk, "dk", (B, H, L, d), dt, dev)
+    _check(dv, "dv", (B, H, L, d), dt, dev)
+    _check(dc_k, "dc_k", (B, H, L), torch.float32, dev)
+    s = default_scale(d) if scale is None else float(scale)
+    st = load().fox_attn_bwd_dkdv(_DT[dt], _ptr(q), _ptr(k), _ptr(v), _ptr(c), _ptr(lse),
+                                  _ptr(d_o), _ptr(delta), _ptr(dk), _ptr(dv), _ptr(dc_k),
+                                  B, H, L, d, s, _stream(q))
+    _raise(st, "fox_attn_bwd_dkdv")
+    return dk, dv, dc_k
+
+
+def fox_attn_bwd_dq(q, k, v, c, lse, d_o, delta, scale: Optional[float] = None,
+                    dq=None, dc_q=None):
+    """dQ (q's dtype) and dc_q = rowsum(dS) [B,H,L] fp32."""
+    B, H, L, d, dt, dev = _check_bwd_inputs(q, k, v, c, lse, d_o)
+    _check(delta, "delta", (B, H, L), torch.float32, dev)
+    dq = torch.empty_like(q) if dq is None else dq
+    dc_q = torch.empty_like(c) if dc_q is None else dc_q
+    _check(dq, "dq", (B, H, L, d), dt, dev)
+    _check(dc_q, "dc_q", (B, H, L), torch.float32, dev)
+    s = default_scale(d) if scale is None else float(scale)
+    st = load().fox_attn_bwd_dq(_DT[dt], _ptr(q), _ptr(k), _ptr(v), _ptr(c), _ptr(lse),
+                                _ptr(d_o), _ptr(delta), _ptr(dq), _ptr(dc_q), B, H, L, d, s,
+                                _stream(q))
+    _raise(st, "fox_attn_bwd_dq")
+    return dq, dc_q
+
+
+def fox_dlogf_from_dc(dc_q, dc_k, d_log_f=None):
+    """d(log f)_l = sum_{i>=l} (dc_q + dc_k)_i, [B,H,L] fp32."""
+    B, H, L = dc_q.shape
+    _check(dc_q, "dc_q", (B, H, L), torch.float32, None)
+    _check(dc_k, "dc_k", (B, H, L), torch.float32, dc_q.device)
+    d_log_f = torch.empty_like(dc_q) if d_log_f is None else d_log_f
+    _check(d_log_f, "d_log_f", (B, H, L), torch.float32, dc_q.device)
+    st = load().fox_dlogf_from_dc(_ptr(dc_q), _ptr(dc_k), _ptr(d_log_f), B, H, L, _stream(dc_q))
+    _raise(st, "fox_dlogf_from_dc")
+    return d_log_f
 
 
 def fox_attn_decode_workspace_bytes(dtype: torch.dtype, B: int, H: int, T: int, d: int) -> int:

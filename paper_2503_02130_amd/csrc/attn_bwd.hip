@@ -673,66 +673,92 @@ static hipError_t launch_delta(const T* o, const T* g, float* delta, int BH, int
   return hipGetLastError();
 }
 
-hipError_t launch_bwd_bf16(const void* q, const void* k, const void* v, const float* c,
-                           const void* o, const float* lse, const void* d_o, void* dq, void* dk,
-                           void* dv, float* d_log_f, void* ws, int BH, int L, int d, float scale,
-                           hipStream_t s) {
-  float* delta = static_cast<float*>(ws);
-  float* dcq = delta + (size_t)BH * L;
-  float* dck = dcq + (size_t)BH * L;
-  hipError_t e = launch_delta((const bf16*)o, (const bf16*)d_o, delta, BH, L, d, s);
-  if (e != hipSuccess) return e;
-  const float sl2 = scale * kLog2e;
-  const int n_mblk = (L + kDqBM - 1) / kDqBM;
-  const int n_nblk = (L + kKvBN - 1) / kKvBN;
-  const dim3 gq((unsigned)n_mblk * (unsigned)BH), gk((unsigned)n_nblk * (unsigned)BH);
-  if (d == 128) {
-    hipLaunchKernelGGL(bwd_dkdv_bf16_kernel<128>, gk, dim3(kKvThreads), 0, s, (const bf16*)q,
-                       (const bf16*)k, (const bf16*)v, c, lse, (const bf16*)d_o, delta, (bf16*)dk,
-                       (bf16*)dv, dck, BH, L, scale, sl2);
-    hipLaunchKernelGGL(bwd_dq_bf16_kernel<128>, gq, dim3(kBwdThreads), 0, s, (const bf16*)q,
-                       (const bf16*)k, (const bf16*)v, c, lse, (const bf16*)d_o, delta, (bf16*)dq,
-                       dcq, BH, L, n_mblk, scale, sl2);
-  } else {
-    hipLaunchKernelGGL(bwd_dkdv_bf16_kernel<64>, gk, dim3(kKvThreads), 0, s, (const bf16*)q,
-                       (const bf16*)k, (const bf16*)v, c, lse, (const bf16*)d_o, delta, (bf16*)dk,
-                       (bf16*)dv, dck, BH, L, scale, sl2);
-    hipLaunchKernelGGL(bwd_dq_bf16_kernel<64>, gq, dim3(kBwdThreads), 0, s, (const bf16*)q,
-                       (const bf16*)k, (const bf16*)v, c, lse, (const bf16*)d_o, delta, (bf16*)dq,
-                       dcq, BH, L, n_mblk, scale, sl2);
-  }
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  return launch_reverse_scan_sum(dcq, dck, d_log_f, BH, L, s);
+hipError_t launch_bwd_delta(bool bf16_, const void* o, const void* d_o, float* delta, int BH,
+                            int L, int d, hipStream_t s) {
+  return bf16_ ? launch_delta((const bf16*)o, (const bf16*)d_o, delta, BH, L, d, s)
+               : launch_delta((const float*)o, (const float*)d_o, delta, BH, L, d, s);
 }
 
-hipError_t launch_bwd_f32(const float* q, const float* k, const float* v, const float* c,
-                          const float* o, const float* lse, const float* d_o, float* dq, float* dk,
-                          float* dv, float* d_log_f, void* ws, int BH, int L, int d, float scale,
-                          hipStream_t s) {
+hipError_t launch_bwd_dkdv(bool bf16_, const void* q, const void* k, const void* v,
+                           const float* c, const float* lse, const void* d_o, const float* delta,
+                           void* dk, void* dv, float* dck, int BH, int L, int d, float scale,
+                           hipStream_t s) {
+  const float sl2 = scale * kLog2e;
+  if (bf16_) {
+    const dim3 grid((unsigned)((L + kKvBN - 1) / kKvBN) * (unsigned)BH);
+    if (d == 128) {
+      hipLaunchKernelGGL(bwd_dkdv_bf16_kernel<128>, grid, dim3(kKvThreads), 0, s, (const bf16*)q,
+                         (const bf16*)k, (const bf16*)v, c, lse, (const bf16*)d_o, delta,
+                         (bf16*)dk, (bf16*)dv, dck, BH, L, scale, sl2);
+    } else {
+      hipLaunchKernelGGL(bwd_dkdv_bf16_kernel<64>, grid, dim3(kKvThreads), 0, s, (const bf16*)q,
+                         (const bf16*)k, (const bf16*)v, c, lse, (const bf16*)d_o, delta,
+                         (bf16*)dk, (bf16*)dv, dck, BH, L, scale, sl2);
+    }
+  } else {
+    const int rpw = kF32Threads / (d / 32);
+    const int n_blk = (L + rpw - 1) / rpw;
+    const dim3 grid((unsigned)n_blk * (unsigned)BH);
+    if (d == 128) {
+      hipLaunchKernelGGL(bwd_dkdv_f32_kernel<128>, grid, dim3(kF32Threads), 0, s, (const float*)q,
+                         (const float*)k, (const float*)v, c, lse, (const float*)d_o, delta,
+                         (float*)dk, (float*)dv, dck, L, n_blk, scale, sl2);
+    } else {
+      hipLaunchKernelGGL(bwd_dkdv_f32_kernel<64>, grid, dim3(kF32Threads), 0, s, (const float*)q,
+                         (const float*)k, (const float*)v, c, lse, (const float*)d_o, delta,
+                         (float*)dk, (float*)dv, dck, L, n_blk, scale, sl2);
+    }
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_dq(bool bf16_, const void* q, const void* k, const void* v, const float* c,
+                         const float* lse, const void* d_o, const float* delta, void* dq,
+                         float* dcq, int BH, int L, int d, float scale, hipStream_t s) {
+  const float sl2 = scale * kLog2e;
+  if (bf16_) {
+    const int n_mblk = (L + kDqBM - 1) / kDqBM;
+    const dim3 grid((unsigned)n_mblk * (unsigned)BH);
+    if (d == 128) {
+      hipLaunchKernelGGL(bwd_dq_bf16_kernel<128>, grid, dim3(kBwdThreads), 0, s, (const bf16*)q,
+                         (const bf16*)k, (const bf16*)v, c, lse, (const bf16*)d_o, delta,
+                         (bf16*)dq, dcq, BH, L, n_mblk, scale, sl2);
+    } else {
+      hipLaunchKernelGGL(bwd_dq_bf16_kernel<64>, grid, dim3(kBwdThreads), 0, s, (const bf16*)q,
+                         (const bf16*)k, (const bf16*)v, c, lse, (const bf16*)d_o, delta,
+                         (bf16*)dq, dcq, BH, L, n_mblk, scale, sl2);
+    }
+  } else {
+    const int rpw = kF32Threads / (d / 32);
+    const int n_blk = (L + rpw - 1) / rpw;
+    const dim3 grid((unsigned)n_blk * (unsigned)BH);
+    if (d == 128) {
+      hipLaunchKernelGGL(bwd_dq_f32_kernel<128>, grid, dim3(kF32Threads), 0, s, (const float*)q,
+                         (const float*)k, (const float*)v, c, lse, (const float*)d_o, delta,
+                         (float*)dq, dcq, L, n_blk, scale, sl2);
+    } else {
+      hipLaunchKernelGGL(bwd_dq_f32_kernel<64>, grid, dim3(kF32Threads), 0, s, (const float*)q,
+                         (const float*)k, (const float*)v, c, lse, (const float*)d_o, delta,
+                         (float*)dq, dcq, L, n_blk, scale, sl2);
+    }
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd(bool bf16_, const void* q, const void* k, const void* v, const float* c,
+                      const void* o, const float* lse, const void* d_o, void* dq, void* dk,
+                      void* dv, float* d_log_f, void* ws, int BH, int L, int d, float scale,
+                      hipStream_t s) {
   float* delta = static_cast<float*>(ws);
   float* dcq = delta + (size_t)BH * L;
   float* dck = dcq + (size_t)BH * L;
-  hipError_t e = launch_delta(o, d_o, delta, BH, L, d, s);
-  if (e != hipSuccess) return e;
-  const float sl2 = scale * kLog2e;
-  const int rpw = kF32Threads / (d / 32);
-  const int n_blk = (L + rpw - 1) / rpw;
-  const dim3 grid((unsigned)n_blk * (unsigned)BH);
-  if (d == 128) {
-    hipLaunchKernelGGL(bwd_dkdv_f32_kernel<128>, grid, dim3(kF32Threads), 0, s, q, k, v, c, lse,
-                       d_o, delta, dk, dv, dck, L, n_blk, scale, sl2);
-    hipLaunchKernelGGL(bwd_dq_f32_kernel<128>, grid, dim3(kF32Threads), 0, s, q, k, v, c, lse,
-                       d_o, delta, dq, dcq, L, n_blk, scale, sl2);
-  } else {
-    hipLaunchKernelGGL(bwd_dkdv_f32_kernel<64>, grid, dim3(kF32Threads), 0, s, q, k, v, c, lse,
-                       d_o, delta, dk, dv, dck, L, n_blk, scale, sl2);
-    hipLaunchKernelGGL(bwd_dq_f32_kernel<64>, grid, dim3(kF32Threads), 0, s, q, k, v, c, lse,
-                       d_o, delta, dq, dcq, L, n_blk, scale, sl2);
-  }
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  return launch_reverse_scan_sum(dcq, dck, d_log_f, BH, L, s);
+  hipError_t e = launch_bwd_delta(bf16_, o, d_o, delta, BH, L, d, s);
+  if (e == hipSuccess)
+    e = launch_bwd_dkdv(bf16_, q, k, v, c, lse, d_o, delta, dk, dv, dck, BH, L, d, scale, s);
+  if (e == hipSuccess)
+    e = launch_bwd_dq(bf16_, q, k, v, c, lse, d_o, delta, dq, dcq, BH, L, d, scale, s);
+  if (e == hipSuccess) e = launch_reverse_scan_sum(dcq, dck, d_log_f, BH, L, s);
+  return e;
 }
 
 }  // namespace fox

@@ -100,14 +100,64 @@ int fox_attn_bwd(int dtype, const void* q, const void* k, const void* v, const f
     return FOX_ERR_ALIGN;
   if (!workspace || workspace_bytes < fox::bwd_workspace_bytes(B * H, L)) return FOX_ERR_WORKSPACE;
   if (!aligned16(workspace)) return FOX_ERR_ALIGN;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  if (dtype == FOX_DTYPE_BF16)
-    return launch_status(fox::launch_bwd_bf16(q, k, v, c, o, lse, d_o, dq, dk, dv, d_log_f,
-                                              workspace, B * H, L, d, scale, s));
-  return launch_status(fox::launch_bwd_f32(
-      (const float*)q, (const float*)k, (const float*)v, c, (const float*)o, lse,
-      (const float*)d_o, (float*)dq, (float*)dk, (float*)dv, d_log_f, workspace, B * H, L, d,
-      scale, s));
+  return launch_status(fox::launch_bwd(dtype == FOX_DTYPE_BF16, q, k, v, c, o, lse, d_o, dq, dk,
+                                       dv, d_log_f, workspace, B * H, L, d, scale,
+                                       static_cast<hipStream_t>(stream)));
+}
+
+int fox_attn_bwd_delta(int dtype, const void* o, const void* d_o, float* delta, int B, int H,
+                       int L, int d, void* stream) {
+  if (!o || !d_o || !delta) return FOX_ERR_NULL;
+  int st = check_dims(B, H, L, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (!aligned16(o) || !aligned16(d_o) || !aligned16(delta)) return FOX_ERR_ALIGN;
+  return launch_status(fox::launch_bwd_delta(dtype == FOX_DTYPE_BF16, o, d_o, delta, B * H, L, d,
+                                             static_cast<hipStream_t>(stream)));
+}
+
+int fox_attn_bwd_dkdv(int dtype, const void* q, const void* k, const void* v, const float* c,
+                      const float* lse, const void* d_o, const float* delta, void* dk, void* dv,
+                      float* dc_k, int B, int H, int L, int d, float scale, void* stream) {
+  if (!q || !k || !v || !c || !lse || !d_o || !delta || !dk || !dv || !dc_k) return FOX_ERR_NULL;
+  int st = check_dims(B, H, L, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(c) || !aligned16(lse) ||
+      !aligned16(d_o) || !aligned16(delta) || !aligned16(dk) || !aligned16(dv) ||
+      !aligned16(dc_k))
+    return FOX_ERR_ALIGN;
+  return launch_status(fox::launch_bwd_dkdv(dtype == FOX_DTYPE_BF16, q, k, v, c, lse, d_o, delta,
+                                            dk, dv, dc_k, B * H, L, d, scale,
+                                            static_cast<hipStream_t>(stream)));
+}
+
+int fox_attn_bwd_dq(int dtype, const void* q, const void* k, const void* v, const float* c,
+                    const float* lse, const void* d_o, const float* delta, void* dq, float* dc_q,
+                    int B, int H, int L, int d, float scale, void* stream) {
+  if (!q || !k || !v || !c || !lse || !d_o || !delta || !dq || !dc_q) return FOX_ERR_NULL;
+  int st = check_dims(B, H, L, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(c) || !aligned16(lse) ||
+      !aligned16(d_o) || !aligned16(delta) || !aligned16(dq) || !aligned16(dc_q))
+    return FOX_ERR_ALIGN;
+  return launch_status(fox::launch_bwd_dq(dtype == FOX_DTYPE_BF16, q, k, v, c, lse, d_o, delta,
+                                          dq, dc_q, B * H, L, d, scale,
+                                          static_cast<hipStream_t>(stream)));
+}
+
+int fox_dlogf_from_dc(const float* dc_q, const float* dc_k, float* d_log_f, int B, int H, int L,
+                      void* stream) {
+  if (!dc_q || !dc_k || !d_log_f) return FOX_ERR_NULL;
+  int st = check_dims(B, H, L, 1);
+  if (st) return st;
+  if (!aligned16(dc_q) || !aligned16(dc_k) || !aligned16(d_log_f)) return FOX_ERR_ALIGN;
+  return launch_status(fox::launch_reverse_scan_sum(dc_q, dc_k, d_log_f, B * H, L,
+                                                    static_cast<hipStream_t>(stream)));
 }
 
 size_t fox_attn_decode_workspace_bytes(int dtype, int B, int H, int T, int d) {

@@ -20,14 +20,18 @@ hipError_t launch_fwd_f32(const float* q, const float* k, const float* v, const 
 
 // Workspace layout of the backward: delta, dc_q, dc_k, each [BH, L] fp32.
 size_t bwd_workspace_bytes(int BH, int L);
-hipError_t launch_bwd_bf16(const void* q, const void* k, const void* v, const float* c,
-                           const void* o, const float* lse, const void* d_o, void* dq, void* dk,
-                           void* dv, float* d_log_f, void* ws, int BH, int L, int d, float scale,
-                           hipStream_t s);
-hipError_t launch_bwd_f32(const float* q, const float* k, const float* v, const float* c,
-                          const float* o, const float* lse, const float* d_o, float* dq, float* dk,
-                          float* dv, float* d_log_f, void* ws, int BH, int L, int d, float scale,
-                          hipStream_t s);
+hipError_t launch_bwd_delta(bool bf16, const void* o, const void* d_o, float* delta, int BH,
+                            int L, int d, hipStream_t s);
+hipError_t launch_bwd_dkdv(bool bf16, const void* q, const void* k, const void* v, const float* c,
+                           const float* lse, const void* d_o, const float* delta, void* dk,
+                           void* dv, float* dck, int BH, int L, int d, float scale, hipStream_t s);
+hipError_t launch_bwd_dq(bool bf16, const void* q, const void* k, const void* v, const float* c,
+                         const float* lse, const void* d_o, const float* delta, void* dq,
+                         float* dcq, int BH, int L, int d, float scale, hipStream_t s);
+hipError_t launch_bwd(bool bf16, const void* q, const void* k, const void* v, const float* c,
+                      const void* o, const float* lse, const void* d_o, void* dq, void* dk,
+                      void* dv, float* d_log_f, void* ws, int BH, int L, int d, float scale,
+                      hipStream_t s);
 
 int decode_num_splits(int BH, int T);
 size_t decode_workspace_bytes(int BH, int T, int d);

@@ -317,3 +317,19 @@ def test_workload_decode_bf16_b64_h16_t32768_d128():
                                           fox.default_scale(w.d))
         assert rel_l2(o[b:b + 1, h:h + 1], o_ref) <= 1e-2, (b, h)
         assert max_abs(lse[b:b + 1, h:h + 1], lse_ref) <= 1e-2, (b, h)
+
+
+def test_backward_stages_equal_fused_entry_point():
+    """fox_attn_bwd == delta -> dkdv -> dq -> d(log f) stages, bit for bit."""
+    for dtype, d in (("bf16", 128), ("bf16", 64), ("f32", 64)):
+        x = inputs.attn_inputs(2, 3, 333, d, dtype, ("normal", 1.0, 1.0), 77, device=DEV)
+        s = fox.default_scale(d)
+        c, o, lse = gpu_forward(x, s)
+        ref = fox.fox_attn_bwd(x["q"], x["k"], x["v"], c, o, lse, x["do"], s)
+        delta = fox.fox_attn_bwd_delta(o, x["do"])
+        dk, dv, dck = fox.fox_attn_bwd_dkdv(x["q"], x["k"], x["v"], c, lse, x["do"], delta, s)
+        dq, dcq = fox.fox_attn_bwd_dq(x["q"], x["k"], x["v"], c, lse, x["do"], delta, s)
+        dlf = fox.fox_dlogf_from_dc(dcq, dck)
+        torch.cuda.synchronize()
+        for a, b in zip(ref, (dq, dk, dv, dlf)):
+            assert torch.equal(a, b), dtype
