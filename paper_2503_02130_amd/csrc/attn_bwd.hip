@@ -170,6 +170,7 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
 #pragma unroll
         for (int s = 0; s < D / 16; ++s)
           ka[s] = *reinterpret_cast<const bf16x8*>(kt_ + kb * 32 * D + roff[s]);
+        sched_fence();
 #pragma unroll
         for (int s = 0; s < D / 16; ++s) sacc = mfma32(ka[s], qf[s], sacc);
       }
@@ -178,6 +179,7 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
 #pragma unroll
         for (int s = 0; s < D / 16; ++s)
           va[s] = *reinterpret_cast<const bf16x8*>(vt_ + kb * 32 * D + roff[s]);
+        sched_fence();
 #pragma unroll
         for (int s = 0; s < D / 16; ++s) pacc = mfma32(va[s], dof[s], pacc);
       }
@@ -203,6 +205,7 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
         bf16x8 ta[D / 32];
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) ta[db] = tile_tr_operand<D>(kt_, toff, 2 * kb + c, db);
+        sched_fence();
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) dqacc[db] = mfma32(ta[db], dsb, dqacc[db]);
       }

@@ -144,6 +144,7 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
 #pragma unroll
       for (int s = 0; s < D / 16; ++s)
         ka[s] = *reinterpret_cast<const bf16x8*>(kt_ + kb * 32 * D + koff[s]);
+      sched_fence();
       f32x16 acc;
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
@@ -186,6 +187,7 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
       bf16x8 va[D / 32];
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) va[db] = tile_tr_operand<D>(vt_, voff, c, db);
+      sched_fence();
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) oacc[db] = mfma32(va[db], pb, oacc[db]);
     }

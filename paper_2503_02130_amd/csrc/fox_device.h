@@ -50,10 +50,22 @@ __device__ __forceinline__ bf16x8 pack8(const float* p) {
   return r;
 }
 
-__device__ __forceinline__ float wave_max_pair(float x) {  // lanes l and l ^ 32
-  return fmaxf(x, __shfl_xor(x, 32));
+// Combine a value with the one held by lane l ^ 32 (v_permlane32_swap on gfx950:
+// the swap of the two half-waves leaves lane l holding both x_l and x_{l^32}).
+__device__ __forceinline__ float wave_max_pair(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
-__device__ __forceinline__ float wave_sum_pair(float x) { return x + __shfl_xor(x, 32); }
+__device__ __forceinline__ float wave_sum_pair(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Keep the compiler from moving instructions across this point (used to issue
+// a batch of operand loads before the MFMAs that consume them).
+__device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 
 // log sigmoid(x) = min(x, 0) - log1p(exp(-|x|)), overflow-free for any finite x.
 __device__ __forceinline__ float log_sigmoid(float x) {
