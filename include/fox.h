@@ -123,8 +123,10 @@ int fox_attn_bwd(int dtype, const void* q, const void* k, const void* v, const f
  *   (overwritten), the query-side half of Alg. 2.
  * fox_dlogf_from_dc: d(log f)_l = sum_{i>=l} (dc_q_i + dc_k_i), the chain rule
  *   through c = cumsum(log f) (Alg. 2 returns dc = dc^q + dc^k); [B,H,L] fp32.
- * Both halves form dS from P rounded to bf16 (bf16 dtype), so that dc_q and dc_k
- * are the row and column sums of one matrix.  Inputs as for fox_attn_bwd.
+ * Both halves form P and dS from the same expression (bf16 dtype: P rounded to
+ * bf16 before dS = P o (dP - delta)), so that dc_q and dc_k are the row and column
+ * sums of one matrix and sum(dc) = d(log f)_1 = 0 holds to fp32 rounding.  Inputs
+ * as for fox_attn_bwd.
  */
 int fox_attn_bwd_delta(int dtype, const void* o, const void* d_o, float* delta,
                        int B, int H, int L, int d, void* stream);

@@ -61,12 +61,21 @@ constexpr int kBwdThreads = 256;
 constexpr int kDqWaves = 4;
 constexpr int kDqBM = 32 * kDqWaves;
 constexpr int kDqBN = 64;
+// Both backward kernels form P from the same expression, so that their bf16
+// roundings of P agree bit for bit and dc^q, dc^k are the row and column sums of
+// one matrix: the bias is taken relative to the prefix value at the start of the
+// key's aligned block of kRefBlock keys, the query's part
+// ((c_i - c_ref) - LSE_i) / s seeds the S accumulator, the key's part
+// (c_j - c_ref) log2(e) is subtracted in the exponent.
+constexpr int kRefBlock = 128;
+static_assert(kRefBlock % kDqBN == 0, "a dq key tile lies in one reference block");
 
 template <int D>
 struct DqSmem {
   bf16 k[2][kDqBN * D];
   bf16 v[2][kDqBN * D];
   float c[2][kDqBN];
+  float cref[2];  // the tile's reference prefix value
 };
 
 template <int D>
@@ -88,7 +97,6 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
   const int q0 = mblk * kDqBM;
   const size_t head = (size_t)bh * (size_t)L;
   const float* Ch = C + head;
-  const float c_ref = Ch[q0];
   const int qw0 = q0 + wave * 32;
   const int qi = qw0 + col;
   const bool q_valid = qi < L;
@@ -116,7 +124,8 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
       }
     }
   }
-  const float bias2 = q_valid ? ((Ch[qi] - c_ref) - LSE[head + qi]) * kLog2e : -INFINITY;
+  const float cq = q_valid ? Ch[qi] : 0.0f;
+  const float lse_q = q_valid ? LSE[head + qi] : 0.0f;
   const float dlt = q_valid ? delta[head + qi] : 0.0f;
 
   f32x16 dqacc[D / 32];
@@ -130,7 +139,8 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
   const int t_last = (kend + kDqBN - 1) / kDqBN - 1;
   const int t_diag = qw0 / kDqBN;
 
-  float creg = 0.0f;
+  const float inv_scale = 1.0f / scale;
+  float creg = 0.0f, crefreg = 0.0f;
   auto issue_tile = [&](int kt, auto bufc) {
     constexpr int B = decltype(bufc)::value;
     const uint32_t base = (uint32_t)kt * kDqBN * D * 2;
@@ -142,12 +152,16 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
     }
     if (wave == 0) {
       const int key = kt * kDqBN + lane;
-      creg = key < L ? (Ch[key] - c_ref) * kLog2e : INFINITY;
+      crefreg = Ch[kt * kDqBN / kRefBlock * kRefBlock];
+      creg = key < L ? (Ch[key] - crefreg) * kLog2e : INFINITY;
     }
   };
   auto store_c = [&](auto bufc) {
     constexpr int B = decltype(bufc)::value;
-    if (wave == 0) sm.c[B][lane] = creg;
+    if (wave == 0) {
+      sm.c[B][lane] = creg;
+      if (lane == 0) sm.cref[B] = crefreg;
+    }
   };
 
   auto tile_body = [&](int j, auto bufc, auto masked) {
@@ -157,12 +171,13 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
     const bf16* vt_ = sm.v[B];
     const float* ct_ = sm.c[B];
     const int key0 = j * kDqBN;
+    const float bq = q_valid ? ((cq - sm.cref[B]) - lse_q) * inv_scale : -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       f32x16 sacc, pacc;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        sacc[r] = 0.0f;
+        sacc[r] = bq;
         pacc[r] = 0.0f;
       }
       {
@@ -189,13 +204,12 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
         const f32x4 ck4 = *reinterpret_cast<const f32x4*>(ct_ + kb * 32 + 8 * g + 4 * h);
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj) {
-          float p = exp2_fast(sacc[4 * g + jj] * scale_log2 + (bias2 - ck4[jj]));
+          float p = exp2_fast(sacc[4 * g + jj] * scale_log2 - ck4[jj]);
           if (MASK && key0 + kb * 32 + 8 * g + 4 * h + jj > qi) p = 0.0f;
-          // P rounded to bf16 exactly as the dkdv kernel sees it, so that the row
-          // sums (dc^q) and column sums (dc^k) of dS come from the same matrix
+          // P rounded to bf16 exactly as the dkdv kernel sees it
           p = to_f32(to_bf16(p));
           const float ds = p * (pacc[4 * g + jj] - dlt);
-          dcq_part += ds;
+          dcq_part += ds;  // dc^q and dc^k sum fp32 dS, the row and column sums of one matrix
           dsv[4 * g + jj] = ds;
         }
       }
@@ -268,6 +282,7 @@ constexpr int kKvWaves = 8;
 constexpr int kKvThreads = 64 * kKvWaves;
 constexpr int kKvPairs = kKvWaves / 2;
 constexpr int kKvBN = 32 * kKvPairs;  // keys per workgroup
+static_assert(kKvBN == kRefBlock, "a dkdv workgroup's keys form one reference block");
 // queries per tile: 32 at D = 128 keeps all six tiles within the 64 KB reach of
 // an LDS instruction's immediate offset
 template <int D>
@@ -279,8 +294,8 @@ struct KvSmem {
   bf16 q[3][BM * D];
   bf16 g[3][BM * D];
   bf16x8 p[3][kKvPairs][BM / 16][64];  // P of each pair: [16-query chunk][lane], bf16 x 8
-  float bq[3][BM];
-  float dl[3][BM];
+  float bq[3][BM];  // ((c_i - c_ref) - LSE_i) / s of each query row
+  float dl[3][BM];  // Delta_i
 };
 
 template <int D>
@@ -348,6 +363,8 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
   const int n_tiles = (L + kKvBM - 1) / kKvBM - t_first;
   const int t_diag = kw0 / kKvBM;  // tile holding this pair's diagonal
 
+  // per query row of a tile: ((c_i - c_ref) - LSE_i) / s and Delta_i
+  const float inv_scale = 1.0f / scale;
   float breg = 0.0f, dreg = 0.0f;
   auto issue_tile = [&](int qt, auto bufc) {
     constexpr int B = decltype(bufc)::value;
@@ -363,7 +380,7 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
       breg = -INFINITY;
       dreg = 0.0f;
       if (qq < L) {
-        breg = ((Ch[qq] - c_ref) - Lh[qq]) * kLog2e;
+        breg = ((Ch[qq] - c_ref) - Lh[qq]) * inv_scale;
         dreg = Dh[qq];
       }
     }
@@ -387,19 +404,23 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
 #pragma unroll
       for (int s = 0; s < D / 16; ++s)
         qa[s] = *reinterpret_cast<const bf16x8*>(sm.q[B] + qb * 32 * D + roff[s]);
+      // the accumulator starts at the query's row term divided by s
       f32x16 sacc;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[r] = 0.0f;
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 bq4 = *reinterpret_cast<const f32x4*>(sm.bq[B] + qb * 32 + 8 * g + 4 * h);
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) sacc[4 * g + jj] = bq4[jj];
+      }
 #pragma unroll
       for (int s = 0; s < D / 16; ++s) sacc = mfma32(qa[s], kvf[s], sacc);
       float pv[16];
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int ql = qb * 32 + 8 * g + 4 * h;
-        const f32x4 bq4 = *reinterpret_cast<const f32x4*>(sm.bq[B] + ql);
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj) {
-          float p = exp2_fast(sacc[4 * g + jj] * scale_log2 + (bq4[jj] - ck2));
+          float p = exp2_fast(sacc[4 * g + jj] * scale_log2 - ck2);
           if (MASK && kj > qs0 + ql + jj) p = 0.0f;
           pv[4 * g + jj] = p;
         }
@@ -442,7 +463,7 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
 #pragma unroll
           for (int jj = 0; jj < 4; ++jj) {
             const float ds = to_f32(pb[4 * g2 + jj]) * (pacc[8 * c + 4 * g2 + jj] - dl4[jj]);
-            dck_part -= ds;
+            dck_part += ds;
             dsv[4 * g2 + jj] = ds;
           }
         }
@@ -502,7 +523,7 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
   }
   if (!pwave) {
     const float dck_tot = wave_sum_pair(dck_part);
-    if (k_valid && h == 0) dck[head + kj] = dck_tot;
+    if (k_valid && h == 0) dck[head + kj] = -dck_tot;
   }
 }
 

@@ -18,14 +18,21 @@
 //     row term c_i shifts a whole softmax row and cancels; it only enters the
 //     logsumexp: LSE_i = (c_i - c_ref) + ln2 (m_i + log2 l_i).  Keeping the c
 //     differences small keeps them exact in fp32 even where |c| is 1e4-1e5.
+//     The key term enters through the accumulator: each S tile starts from
+//     (c_ref - c_j) / s, so the MFMA chain adds it and one fma per score gives
+//     u_ij - m_i.
 //   * P^T (accumulator layout) is the B operand of O^T += V^T P^T.  The V^T
 //     A operand comes straight from the row-major V tile through transposing LDS
 //     reads; keys are consumed in the order the accumulator layout holds them, a
 //     permutation of the contraction index applied identically to both operands.
-//   * Key tiles are visited from the diagonal backwards.  The running maximum is
-//     therefore found early, and O and l are only rescaled when a new maximum
-//     exceeds the one in use by more than 2^8 (the exponents stay <= 8, which
-//     bf16 P and fp32 sums absorb), which makes rescaling rare.
+//   * Key tiles are visited from the diagonal backwards, so the row maximum of
+//     the diagonal tile (the first one visited) is a good reference for all
+//     later tiles: they are exponentiated against it without a maximum search.
+//     Only when some score exceeds the reference by more than the slack (then a
+//     lane's tile sum of P exceeds 2^8) is the tile maximum taken and O and l
+//     rescaled.  Exponents up to 8 are absorbed by bf16 P and the fp32 sums.
+//   * l sums P after its rounding to bf16 (v_dot2_f32_bf16 against ones), the
+//     same values the P V product uses.
 //   * Causal structure: tiles after a wave's last query are skipped and only the
 //     tile holding its diagonal applies the mask.  Query blocks are dispatched
 //     longest-first with heads fastest, so a head's blocks share an XCD's L2
@@ -48,6 +55,7 @@ constexpr int kFwdThreads = 64 * kFwdWaves;
 constexpr int kFwdBM = 32 * kFwdWaves;  // query rows per workgroup
 constexpr int kFwdBN = 64;              // keys per tile
 constexpr float kRescaleSlack = 8.0f;   // log2 headroom before O and l are rescaled
+constexpr float kRescaleSum = 256.0f;  // 2^slack: a lane's tile sum above it triggers a rescale
 
 template <int D>
 struct FwdSmem {
@@ -105,6 +113,7 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[db][r] = 0.0f;
   float m_used = -INFINITY, l_run = 0.0f;
+  const float inv_scale = kLog2e / scale_log2;  // 1 / s
 
   const int kend = min(L, q0 + kFwdBM);
   const int t_last = (kend + kFwdBN - 1) / kFwdBN - 1;
@@ -122,7 +131,7 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
     }
     if (wave == 0) {
       const int key = kt * kFwdBN + lane;
-      creg = key < L ? (Ch[key] - c_ref) * kLog2e : INFINITY;
+      creg = key < L ? (c_ref - Ch[key]) * inv_scale : -INFINITY;
     }
   };
   auto store_c = [&](auto bufc) {
@@ -137,6 +146,9 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
     const bf16* vt_ = sm.v[B];
     const float* ct_ = sm.c[B];
     const int key0 = j * kFwdBN;
+    // u = log2(e) (s q.k - (c_j - c_ref)) - m: the accumulator starts at the key's
+    // bias divided by s, so the MFMA chain adds it and one fma per score remains
+    const float m_sub = MASK ? 0.0f : m_used;
     float u[32];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
@@ -144,52 +156,84 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
 #pragma unroll
       for (int s = 0; s < D / 16; ++s)
         ka[s] = *reinterpret_cast<const bf16x8*>(kt_ + kb * 32 * D + koff[s]);
-      sched_fence();
       f32x16 acc;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
-#pragma unroll
-      for (int s = 0; s < D / 16; ++s) acc = mfma32(ka[s], qf[s], acc);
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const f32x4 ck4 = *reinterpret_cast<const f32x4*>(ct_ + kb * 32 + 8 * g + 4 * h);
 #pragma unroll
+        for (int jj = 0; jj < 4; ++jj) acc[4 * g + jj] = ck4[jj];
+      }
+      sched_fence();
+#pragma unroll
+      for (int s = 0; s < D / 16; ++s) acc = mfma32(ka[s], qf[s], acc);
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+#pragma unroll
         for (int jj = 0; jj < 4; ++jj) {
-          float x = acc[4 * g + jj] * scale_log2 - ck4[jj];
+          float x = acc[4 * g + jj] * scale_log2 - m_sub;
           if (MASK && key0 + kb * 32 + 8 * g + 4 * h + jj > qi) x = -INFINITY;
           u[kb * 16 + 4 * g + jj] = x;
         }
       }
     }
-    float mt = u[0];
-#pragma unroll
-    for (int r = 1; r < 32; ++r) mt = fmaxf(mt, u[r]);
-    mt = wave_max_pair(mt);
-    if (__any(mt > m_used + kRescaleSlack)) {
-      const float m_new = fmaxf(m_used, mt);
-      const float alpha = exp2_fast(m_used - m_new);
+    // rescale O and l by 2^-shift and take u relative to the new maximum
+    auto rescale = [&](float shift) {
+      const float alpha = exp2_fast(-shift);
       l_run *= alpha;
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) oacc[db] *= alpha;
-      m_used = m_new;
-    }
-    const float m_ref = m_used == -INFINITY ? 0.0f : m_used;  // rows past the end only
-    float psum = 0.0f;
 #pragma unroll
-    for (int r = 0; r < 32; ++r) {
-      u[r] = exp2_fast(u[r] - m_ref);
-      psum += u[r];
+      for (int r = 0; r < 32; ++r) u[r] -= shift;
+    };
+    auto tile_max = [&]() {
+      float mt = u[0];
+#pragma unroll
+      for (int r = 1; r < 32; ++r) mt = fmaxf(mt, u[r]);
+      return wave_max_pair(mt);
+    };
+    bf16x8 pb[4];
+    auto exponentiate = [&]() {
+      float psum = 0.0f;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        float pv[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) pv[i] = exp2_fast(u[8 * c + i]);
+        pb[c] = pack8(pv);
+        psum = sum8_bf16(pb[c], psum);
+      }
+      return psum;
+    };
+    float psum;
+    if (MASK) {
+      // the diagonal tile is the first one a wave visits (O and l are still zero):
+      // its row maximum becomes the reference
+      const float mt = tile_max();
+#pragma unroll
+      for (int r = 0; r < 32; ++r) u[r] -= mt;
+      m_used = mt;
+      psum = exponentiate();
+    } else {
+      // no maximum: exponentiate against the running one, and only if some score
+      // exceeds it by more than the slack (the lane's sum then exceeds 2^slack)
+      // find the tile maximum, rescale and exponentiate again
+      psum = exponentiate();
+      if (__any(q_valid && psum > kRescaleSum)) {
+        const float shift = fmaxf(tile_max(), 0.0f);
+        rescale(shift);
+        m_used += shift;
+        psum = exponentiate();
+      }
     }
     l_run += psum;
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      const bf16x8 pb = pack8(&u[8 * c]);
       bf16x8 va[D / 32];
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) va[db] = tile_tr_operand<D>(vt_, voff, c, db);
       sched_fence();
 #pragma unroll
-      for (int db = 0; db < D / 32; ++db) oacc[db] = mfma32(va[db], pb, oacc[db]);
+      for (int db = 0; db < D / 32; ++db) oacc[db] = mfma32(va[db], pb[c], oacc[db]);
     }
   };
 

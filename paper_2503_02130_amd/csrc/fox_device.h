@@ -50,6 +50,18 @@ __device__ __forceinline__ bf16x8 pack8(const float* p) {
   return r;
 }
 
+// acc + the sum of eight bf16 values (v_dot2_f32_bf16 against (1, 1): two
+// elements per instruction, fp32 accumulation).
+__device__ __forceinline__ float sum8_bf16(const bf16x8& v, float acc) {
+  const bf16x2 one = {(bf16)1.0f, (bf16)1.0f};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const bf16x2 pair = {v[2 * i], v[2 * i + 1]};
+    acc = __builtin_amdgcn_fdot2_f32_bf16(pair, one, acc, false);
+  }
+  return acc;
+}
+
 // Combine a value with the one held by lane l ^ 32 (v_permlane32_swap on gfx950:
 // the swap of the two half-waves leaves lane l holding both x_l and x_{l^32}).
 __device__ __forceinline__ float wave_max_pair(float x) {
