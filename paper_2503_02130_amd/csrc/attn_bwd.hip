@@ -275,18 +275,20 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
 // Each wave holds one D x 32 accumulator, so two waves fit on a SIMD, and the
 // two roles never wait for each other inside a tile: Q / dO tiles, their row
 // statistics and P are triple-buffered (tile t + 1 loads by DMA while P works
-// on t and G on t - 1), with one barrier per tile.  The loop is unrolled by
-// three so every LDS address is a per-lane base plus an immediate.
+// on t and G on t - 1), with one barrier per tile of 64 queries.  Every LDS
+// operand address is one of a few opaque per-lane registers plus an immediate:
+// plain reads come from the tile the role multiplies from the left (Q for P,
+// dO for G) and transposing reads from the other one, so both roles share the
+// same sixteen address registers, and the loop is unrolled by three so the
+// buffer index is part of the immediate.
 // ---------------------------------------------------------------------------
 constexpr int kKvWaves = 8;
 constexpr int kKvThreads = 64 * kKvWaves;
 constexpr int kKvPairs = kKvWaves / 2;
 constexpr int kKvBN = 32 * kKvPairs;  // keys per workgroup
 static_assert(kKvBN == kRefBlock, "a dkdv workgroup's keys form one reference block");
-// queries per tile: 32 at D = 128 keeps all six tiles within the 64 KB reach of
-// an LDS instruction's immediate offset
 template <int D>
-constexpr int kv_bm() { return D == 128 ? 32 : 64; }
+constexpr int kv_bm() { return 64; }  // queries per tile
 
 template <int D>
 struct KvSmem {
@@ -335,6 +337,28 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
   tile_row_offsets<D>(roff, col, h);
   int toff[2][D / 32];
   tile_tr_offsets<D>(toff, lane);
+  const lds_byte* plain_base = pwave ? lds_ptr(&sm.q[0][0]) : lds_ptr(&sm.g[0][0]);
+  const lds_byte* tr_base = pwave ? lds_ptr(&sm.g[0][0]) : lds_ptr(&sm.q[0][0]);
+  const lds_byte* pa[D / 16];
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s) pa[s] = lds_opaque(plain_base + 2 * roff[s]);
+  const lds_byte* ta_[2][D / 32];
+#pragma unroll
+  for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) ta_[k2][db] = lds_opaque(tr_base + 2 * toff[k2][db]);
+  const lds_byte* p_at = lds_opaque(lds_ptr(&sm.p[0][pair][0][lane]));
+  const lds_byte* row_at = lds_opaque(lds_ptr(&sm.bq[0][4 * h]));
+  constexpr int kPBuf = kKvPairs * (kKvBM / 16) * 64 * 16;  // bytes of one P buffer
+  constexpr int kDlOff = 3 * kKvBM * 4;                      // bytes from bq to dl
+  // plain operand s of 32-row block qb of buffer B; transposing operand of
+  // 16-row chunk ch, head-dim block db
+  auto plain_op = [&](int s, int boff) { return *(const lds_bf16x8_t*)(pa[s] + boff); };
+  auto tr_op = [&](int db, int boff) {
+    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(ta_[0][db] + boff));
+    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(ta_[1][db] + boff));
+    return (bf16x8)__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  };
 
   // P waves hold K rows, G waves hold V rows
   bf16x8 kvf[D / 16];
@@ -403,12 +427,12 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
       bf16x8 qa[D / 16];
 #pragma unroll
       for (int s = 0; s < D / 16; ++s)
-        qa[s] = *reinterpret_cast<const bf16x8*>(sm.q[B] + qb * 32 * D + roff[s]);
+        qa[s] = plain_op(s, 2 * (B * TILE + qb * 32 * D));
       // the accumulator starts at the query's row term divided by s
       f32x16 sacc;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const f32x4 bq4 = *reinterpret_cast<const f32x4*>(sm.bq[B] + qb * 32 + 8 * g + 4 * h);
+        const f32x4 bq4 = *(const lds_f32x4_t*)(row_at + 4 * (B * kKvBM + qb * 32 + 8 * g));
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj) sacc[4 * g + jj] = bq4[jj];
       }
@@ -428,11 +452,11 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
         const bf16x8 pb = pack8(&pv[8 * c]);
-        sm.p[B][pair][2 * qb + c][lane] = pb;
+        *(lds_bf16x8_t*)(p_at + B * kPBuf + (2 * qb + c) * 1024) = pb;
         bf16x8 ta[D / 32];
 #pragma unroll
         for (int db = 0; db < D / 32; ++db)
-          ta[db] = tile_tr_operand<D>(sm.g[B], toff, 2 * qb + c, db);
+          ta[db] = tr_op(db, 2 * (B * TILE + (2 * qb + c) * 16 * D));
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) acc[db] = mfma32(ta[db], pb, acc[db]);
       }
@@ -446,7 +470,7 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
       bf16x8 ga[D / 16];
 #pragma unroll
       for (int s = 0; s < D / 16; ++s)
-        ga[s] = *reinterpret_cast<const bf16x8*>(sm.g[B] + qb * 32 * D + roff[s]);
+        ga[s] = plain_op(s, 2 * (B * TILE + qb * 32 * D));
       f32x16 pacc;
 #pragma unroll
       for (int r = 0; r < 16; ++r) pacc[r] = 0.0f;
@@ -454,12 +478,11 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
       for (int s = 0; s < D / 16; ++s) pacc = mfma32(ga[s], kvf[s], pacc);
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
-        const bf16x8 pb = sm.p[B][pair][2 * qb + c][lane];
+        const bf16x8 pb = *(const lds_bf16x8_t*)(p_at + B * kPBuf + (2 * qb + c) * 1024);
         float dsv[8];
 #pragma unroll
         for (int g2 = 0; g2 < 2; ++g2) {
-          const int ql = qb * 32 + 8 * (2 * c + g2) + 4 * h;
-          const f32x4 dl4 = *reinterpret_cast<const f32x4*>(sm.dl[B] + ql);
+          const f32x4 dl4 = *(const lds_f32x4_t*)(row_at + kDlOff + 4 * (B * kKvBM + qb * 32 + 8 * (2 * c + g2)));
 #pragma unroll
           for (int jj = 0; jj < 4; ++jj) {
             const float ds = to_f32(pb[4 * g2 + jj]) * (pacc[8 * c + 4 * g2 + jj] - dl4[jj]);
@@ -471,7 +494,7 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
         bf16x8 ta[D / 32];
 #pragma unroll
         for (int db = 0; db < D / 32; ++db)
-          ta[db] = tile_tr_operand<D>(sm.q[B], toff, 2 * qb + c, db);
+          ta[db] = tr_op(db, 2 * (B * TILE + (2 * qb + c) * 16 * D));
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) acc[db] = mfma32(ta[db], dsb, acc[db]);
       }

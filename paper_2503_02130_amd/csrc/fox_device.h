@@ -113,6 +113,24 @@ __device__ __forceinline__ bf16x4 lds_read_tr16(const bf16* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)p);
 }
 
+// LDS pointers with explicit address space (32-bit), for kernels whose LDS use
+// exceeds the 64 KB reach of an instruction's immediate offset.
+typedef __attribute__((address_space(3))) char lds_byte;
+typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8_t;
+typedef __attribute__((address_space(3))) f32x4 lds_f32x4_t;
+
+template <typename T>
+__device__ __forceinline__ const lds_byte* lds_ptr(const T* generic) {
+  return (const lds_byte*)generic;
+}
+// The same address, opaque to the compiler: accesses through it compile to this
+// register plus an immediate offset instead of a precomputed register per
+// access (which spills once the constant offsets pass 64 KB).
+__device__ __forceinline__ const lds_byte* lds_opaque(const lds_byte* p) {
+  asm volatile("" : "+v"(p));
+  return p;
+}
+
 // ---------------------------------------------------------------------------
 // Swizzled LDS tiles: a [rows][D] bf16 tile stores the 16-byte chunk c of row r
 // at chunk position c ^ f(r).  Two access patterns must be free of bank
