@@ -8,4 +8,5 @@ from .fox_oracle import (  # noqa: F401
     log_sigmoid, prefix_c, gate_prefix, decay_matrix,
     forward_head_from_c, backward_head_from_c, reverse_cumsum,
     forward_from_logf, forward, backward_from_logf, backward, decode,
+    gate_backward, backward_logit,
 )

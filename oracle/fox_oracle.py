@@ -25,6 +25,8 @@ paper (Forgetting Transformer, arXiv 2503.02130):
                                dc = rowsum(dS) - colsum(dS)    (Alg. 2)
   * d(log f)                   chain rule through c = cumsum(log f):
                                d(log f)_l = sum_{i >= l} dc_i  (reverse cumsum)
+  * d(logit)                   through f = sigmoid(logit): d(logit) =
+                               d(log f) * sigmoid(-logit)      (Sec. 3, gate def.)
   * decode                     the forward's last row for a sequence whose last
                                key/value is the new token, c_T = c_{T-1} +
                                log sigmoid(x_new), c_0 = 0    (Eq. fot-weight at i = T)
@@ -183,6 +185,18 @@ def backward_from_logf(q, k, v, log_f, dO, scale: float, heads=None):
 
 def backward(q, k, v, logit, dO, scale: float, heads=None):
     return backward_from_logf(q, k, v, log_sigmoid(logit), dO, scale, heads)
+
+
+def gate_backward(logit, d_log_f) -> torch.Tensor:
+    """d(logit) from d(log f) through the forget gate f = sigmoid(logit) (Sec. 3):
+    d log sigmoid(x) / dx = 1 - sigmoid(x) = sigmoid(-x), elementwise."""
+    return _f64(d_log_f) * torch.sigmoid(-_f64(logit))
+
+
+def backward_logit(q, k, v, logit, dO, scale: float, heads=None):
+    """dQ, dK, dV and the gradient with respect to the gate logits."""
+    dQ, dK, dV, dlf = backward(q, k, v, logit, dO, scale, heads)
+    return dQ, dK, dV, gate_backward(logit, dlf)
 
 
 def decode(q, k_cache, v_cache, cached_logit, logit_new, scale: float, heads=None):

@@ -198,7 +198,7 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
 #pragma unroll
         for (int s = 0; s < D / 16; ++s) pacc = mfma32(va[s], dof[s], pacc);
       }
-      float dsv[16];
+      float pv[16];
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const f32x4 ck4 = *reinterpret_cast<const f32x4*>(ct_ + kb * 32 + 8 * g + 4 * h);
@@ -206,12 +206,18 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
         for (int jj = 0; jj < 4; ++jj) {
           float p = exp2_fast(sacc[4 * g + jj] * scale_log2 - ck4[jj]);
           if (MASK && key0 + kb * 32 + 8 * g + 4 * h + jj > qi) p = 0.0f;
-          // P rounded to bf16 exactly as the dkdv kernel sees it
-          p = to_f32(to_bf16(p));
-          const float ds = p * (pacc[4 * g + jj] - dlt);
-          dcq_part += ds;  // dc^q and dc^k sum fp32 dS, the row and column sums of one matrix
-          dsv[4 * g + jj] = ds;
+          pv[4 * g + jj] = p;
         }
+      }
+      // P rounded to bf16 exactly as the dkdv kernel sees it
+#pragma unroll
+      for (int r = 0; r < 16; r += 2) round_bf16_pair(pv[r], pv[r + 1]);
+      float dsv[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float ds = pv[r] * (pacc[r] - dlt);
+        dcq_part += ds;  // dc^q and dc^k sum fp32 dS, the row and column sums of one matrix
+        dsv[r] = ds;
       }
 #pragma unroll
       for (int c = 0; c < 2; ++c) {

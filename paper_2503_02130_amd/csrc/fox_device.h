@@ -41,6 +41,16 @@ __device__ __forceinline__ int mfma_row(int r, int h) { return 8 * (r >> 2) + 4 
 __device__ __forceinline__ bf16 to_bf16(float x) { return (bf16)x; }
 __device__ __forceinline__ float to_f32(bf16 x) { return (float)x; }
 
+// Round two floats to bf16 (round to nearest even) and back, converting them as
+// one packed pair (one v_cvt_pk_bf16_f32 instead of one per value).
+__device__ __forceinline__ void round_bf16_pair(float& a, float& b) {
+  const bf16x2 v = {to_bf16(a), to_bf16(b)};
+  uint32_t w = __builtin_bit_cast(uint32_t, v);
+  asm volatile("" : "+v"(w));  // keep the pair packed in one register
+  a = __uint_as_float(w << 16);
+  b = __uint_as_float(w & 0xffff0000u);
+}
+
 // Eight consecutive accumulator registers (starting at r0) packed to bf16 as one
 // MFMA operand: register r0+i becomes element i.
 __device__ __forceinline__ bf16x8 pack8(const float* p) {

@@ -30,6 +30,8 @@ The pins, with what in the paper fixes them:
   P12 closed forms with q = 0: LSE_i = log i for log f = 0, and the geometric
       series log((1 - e^{-m i}) / (1 - e^{-m})) for constant log f = -m.
   P13 L = 2 written out by hand.
+  P14 gate-logit gradient: central finite differences through the logits, the
+      zero gradient of the first gate, and the sigmoid-derivative closed form.
 """
 from __future__ import annotations
 
@@ -312,6 +314,42 @@ def pin_p13_two_tokens(ora):
     _close(O[0, 0, 1], o2, 1e-14, "P13 o_2")
 
 
+# --------------------------------------------------------------------------- P14
+def _objective_logit(ora, q, k, v, x, dO, s):
+    O, _ = ora.forward(q, k, v, x, s)
+    return float((O * dO).sum())
+
+
+def pin_p14_gate_logit_gradient(ora, B=1, H=2, L=7, d=3, seed=14):
+    """d(logit) equals central finite differences of sum(O o dO) taken through
+    the gate logits themselves (f = sigmoid(x), Sec. 3), and the gate factor
+    d log f / dx is 1 - f (closed form of the sigmoid's derivative)."""
+    q, k, v, dO = (_rand((B, H, L, d), seed + i) for i in range(4))
+    x = _rand((B, H, L), seed + 5) * 2 + 1
+    s = 0.6
+    _, _, _, dx = ora.backward_logit(q, k, v, x, dO, s)
+    eps = 1e-6
+    flat = x.view(-1)
+    for idx in range(flat.numel()):
+        old = float(flat[idx])
+        flat[idx] = old + eps
+        fp = _objective_logit(ora, q, k, v, x, dO, s)
+        flat[idx] = old - eps
+        fm = _objective_logit(ora, q, k, v, x, dO, s)
+        flat[idx] = old
+        fd = (fp - fm) / (2 * eps)
+        got = float(dx.reshape(-1)[idx])
+        assert abs(fd - got) <= 1e-7 * max(1.0, abs(fd)), \
+            f"P14 dlogit[{idx}]: finite difference {fd:.9f} vs oracle {got:.9f}"
+    # the first gate never enters O: its logit gradient is zero
+    assert float(dx[..., 0].abs().max()) <= 1e-12
+    # gate factor: 1 - f with f = exp(log sigmoid(x)); 1/2 at x = 0
+    xs = torch.tensor([-30.0, -3.0, -0.5, 0.0, 0.5, 3.0, 30.0], dtype=torch.float64)
+    factor = ora.gate_backward(xs, torch.ones_like(xs))
+    _close(factor, 1.0 - torch.exp(ora.log_sigmoid(xs)), 1e-15, "P14 gate factor 1 - f")
+    assert abs(float(factor[3]) - 0.5) <= 1e-15
+
+
 ALL_PINS = [
     pin_p1_zero_forgetting_is_softmax_attention,
     pin_p2_full_forgetting,
@@ -327,4 +365,5 @@ ALL_PINS = [
     pin_p11_decode_is_last_row,
     pin_p12_zero_query_closed_forms,
     pin_p13_two_tokens,
+    pin_p14_gate_logit_gradient,
 ]

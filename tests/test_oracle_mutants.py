@@ -115,6 +115,11 @@ def _m_scale_twice(m):
         orig(q, k, v, c, scale * scale, rows, return_A)
 
 
+def _m_gate_factor_sign(m):
+    """sigmoid(x) instead of sigmoid(-x) as the gate's derivative factor."""
+    m.gate_backward = lambda logit, dlf: m._f64(dlf) * torch.sigmoid(m._f64(logit))
+
+
 MUTANTS = {
     "decay_scaled": _m_scale_on_D,
     "exclusive_prefix": _m_exclusive_c,
@@ -130,6 +135,7 @@ MUTANTS = {
     "lse_without_max": _m_lse_no_max,
     "decode_bias_sign": _m_decode_sign,
     "scale_squared": _m_scale_twice,
+    "gate_factor_sign": _m_gate_factor_sign,
 }
 
 
