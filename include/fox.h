@@ -141,6 +141,19 @@ int fox_attn_bwd_dq(int dtype, const void* q, const void* k, const void* v, cons
 int fox_dlogf_from_dc(const float* dc_q, const float* dc_k, float* d_log_f,
                       int B, int H, int L, void* stream);
 
+/*
+ * Gate backward (Sec. 3: f_t = sigmoid(x_t), so d log f_t / d x_t = 1 - f_t =
+ * sigmoid(-x_t)), fused into the reverse scan of fox_dlogf_from_dc:
+ *     d(log f)_l = sum_{i>=l} (dc_q_i + dc_k_i),   d x_l = d(log f)_l * sigmoid(-x_l).
+ *
+ *   dc_q, dc_k  [B,H,L] fp32 in   from fox_attn_bwd_dq / fox_attn_bwd_dkdv
+ *   gate_logit  [B,H,L] fp32 in   the logits x_t given to fox_gate_prefix
+ *   d_log_f     [B,H,L] fp32 out  may be NULL
+ *   d_logit     [B,H,L] fp32 out  the gradient with respect to the gate logits
+ */
+int fox_dlogit_from_dc(const float* dc_q, const float* dc_k, const float* gate_logit,
+                       float* d_log_f, float* d_logit, int B, int H, int L, void* stream);
+
 /* Bytes of workspace fox_attn_decode needs for this shape (0 on invalid arguments). */
 size_t fox_attn_decode_workspace_bytes(int dtype, int B, int H, int T, int d);
 

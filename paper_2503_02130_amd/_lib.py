@@ -25,7 +25,8 @@ _DT = {torch.float32: FOX_DTYPE_F32, torch.bfloat16: FOX_DTYPE_BF16}
 EXPORTED = (
     "fox_status_string", "fox_version", "fox_gate_prefix", "fox_attn_fwd",
     "fox_attn_bwd_workspace_bytes", "fox_attn_bwd", "fox_attn_bwd_delta", "fox_attn_bwd_dkdv",
-    "fox_attn_bwd_dq", "fox_dlogf_from_dc", "fox_attn_decode_workspace_bytes", "fox_attn_decode",
+    "fox_attn_bwd_dq", "fox_dlogf_from_dc", "fox_dlogit_from_dc",
+    "fox_attn_decode_workspace_bytes", "fox_attn_decode",
 )
 
 
@@ -69,6 +70,8 @@ def load() -> ctypes.CDLL:
     lib.fox_attn_bwd_dq.argtypes = [I, P, P, P, P, P, P, P, P, P, I, I, I, I, F, P]
     lib.fox_dlogf_from_dc.restype = I
     lib.fox_dlogf_from_dc.argtypes = [P, P, P, I, I, I, P]
+    lib.fox_dlogit_from_dc.restype = I
+    lib.fox_dlogit_from_dc.argtypes = [P, P, P, P, P, I, I, I, P]
     lib.fox_attn_decode_workspace_bytes.restype = Z
     lib.fox_attn_decode_workspace_bytes.argtypes = [I, I, I, I, I]
     lib.fox_attn_decode.restype = I
@@ -269,6 +272,25 @@ def fox_dlogf_from_dc(dc_q, dc_k, d_log_f=None):
     st = load().fox_dlogf_from_dc(_ptr(dc_q), _ptr(dc_k), _ptr(d_log_f), B, H, L, _stream(dc_q))
     _raise(st, "fox_dlogf_from_dc")
     return d_log_f
+
+
+def fox_dlogit_from_dc(dc_q, dc_k, gate_logit, d_logit=None, d_log_f=None):
+    """d(logit) = d(log f) * sigmoid(-logit) with d(log f) the reverse cumsum of
+    dc_q + dc_k, [B,H,L] fp32.  Returns d_logit, or (d_logit, d_log_f) when
+    d_log_f is given."""
+    B, H, L = dc_q.shape
+    _check(dc_q, "dc_q", (B, H, L), torch.float32, None)
+    _check(dc_k, "dc_k", (B, H, L), torch.float32, dc_q.device)
+    _check(gate_logit, "gate_logit", (B, H, L), torch.float32, dc_q.device)
+    d_logit = torch.empty_like(dc_q) if d_logit is None else d_logit
+    _check(d_logit, "d_logit", (B, H, L), torch.float32, dc_q.device)
+    if d_log_f is not None:
+        _check(d_log_f, "d_log_f", (B, H, L), torch.float32, dc_q.device)
+    st = load().fox_dlogit_from_dc(_ptr(dc_q), _ptr(dc_k), _ptr(gate_logit),
+                                   _ptr(d_log_f) if d_log_f is not None else None, _ptr(d_logit),
+                                   B, H, L, _stream(dc_q))
+    _raise(st, "fox_dlogit_from_dc")
+    return d_logit if d_log_f is None else (d_logit, d_log_f)
 
 
 def fox_attn_decode_workspace_bytes(dtype: torch.dtype, B: int, H: int, T: int, d: int) -> int:

@@ -160,6 +160,18 @@ int fox_dlogf_from_dc(const float* dc_q, const float* dc_k, float* d_log_f, int 
                                                     static_cast<hipStream_t>(stream)));
 }
 
+int fox_dlogit_from_dc(const float* dc_q, const float* dc_k, const float* gate_logit,
+                       float* d_log_f, float* d_logit, int B, int H, int L, void* stream) {
+  if (!dc_q || !dc_k || !gate_logit || !d_logit) return FOX_ERR_NULL;
+  int st = check_dims(B, H, L, 1);
+  if (st) return st;
+  if (!aligned16(dc_q) || !aligned16(dc_k) || !aligned16(gate_logit) || !aligned16(d_logit) ||
+      (d_log_f && !aligned16(d_log_f)))
+    return FOX_ERR_ALIGN;
+  return launch_status(fox::launch_reverse_scan_gate(dc_q, dc_k, gate_logit, d_log_f, d_logit,
+                                                     B * H, L, static_cast<hipStream_t>(stream)));
+}
+
 size_t fox_attn_decode_workspace_bytes(int dtype, int B, int H, int T, int d) {
   if (check_dims(B, H, T, d) || check_dtype_d(dtype, d)) return 0;
   return fox::decode_workspace_bytes(B * H, T, d);

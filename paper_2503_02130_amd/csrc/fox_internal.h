@@ -12,6 +12,10 @@ hipError_t launch_gate_prefix(const float* logit, float* log_f, float* c, int ro
 // out_l = sum_{i>=l} (a_i + b_i) per row: the chain rule through c = cumsum(log f).
 hipError_t launch_reverse_scan_sum(const float* a, const float* b, float* out, int rows, int L,
                                    hipStream_t s);
+// d(log f) (optional) and d(logit) = d(log f) * sigmoid(-logit) in one reverse scan.
+hipError_t launch_reverse_scan_gate(const float* a, const float* b, const float* logit,
+                                    float* d_log_f, float* d_logit, int rows, int L,
+                                    hipStream_t s);
 
 hipError_t launch_fwd_bf16(const void* q, const void* k, const void* v, const float* c, void* o,
                            float* lse, int BH, int L, int d, float scale, hipStream_t s);

@@ -3,7 +3,9 @@
 //  * gate prefix: log f_t = log sigmoid(x_t), c_i = sum_{l<=i} log f_l, one
 //    workgroup per (batch, head) row (Sec. 3, "Hardware-aware implementation").
 //  * reverse scan: d(log f)_l = sum_{i>=l} (dc^q_i + dc^k_i), the chain rule
-//    through c = cumsum(log f) applied to Alg. 2's dc = dc^q + dc^k.
+//    through c = cumsum(log f) applied to Alg. 2's dc = dc^q + dc^k, optionally
+//    carried on through the gate f = sigmoid(x) (Sec. 3) in the same pass:
+//    d x_l = d(log f)_l * sigmoid(-x_l).
 //
 // Each workgroup walks its row in segments of 2048 elements: every thread scans
 // eight consecutive elements sequentially, the 256 thread totals are scanned
@@ -19,11 +21,14 @@ constexpr int kScanThreads = 256;
 constexpr int kScanPerThread = 8;
 constexpr int kScanSegment = kScanThreads * kScanPerThread;
 
-// MODE 0: x = log sigmoid(a) (forward order, also stores x to aux if non-null).
-// MODE 1: x = a + b, scanned from the end of the row (reverse order).
+// MODE 0: x = log sigmoid(a) (forward order, also stores x to aux if non-null);
+//         out = the inclusive scan.
+// MODE 1: x = a + b, scanned from the end of the row (reverse order); out = scan.
+// MODE 2: as MODE 1, aux (if non-null) = scan, out = scan * sigmoid(-g).
 template <int MODE>
 __global__ __launch_bounds__(kScanThreads) void scan_rows_kernel(const float* __restrict__ a,
                                                                  const float* __restrict__ b,
+                                                                 const float* __restrict__ g,
                                                                  float* __restrict__ aux,
                                                                  float* __restrict__ out, int L) {
   const size_t base = (size_t)blockIdx.x * (size_t)L;
@@ -68,7 +73,16 @@ __global__ __launch_bounds__(kScanThreads) void scan_rows_kernel(const float* __
 #pragma unroll
     for (int e = 0; e < kScanPerThread; ++e) {
       const int p = seg + threadIdx.x * kScanPerThread + e;
-      if (p < L) out[base + (size_t)(MODE == 0 ? p : L - 1 - p)] = excl + incl_local[e];
+      if (p < L) {
+        const size_t idx = base + (size_t)(MODE == 0 ? p : L - 1 - p);
+        const float y = excl + incl_local[e];
+        if (MODE == 2) {
+          if (aux) aux[idx] = y;
+          out[idx] = y / (1.0f + expf(g[idx]));  // d log sigmoid(x) / dx = sigmoid(-x)
+        } else {
+          out[idx] = y;
+        }
+      }
     }
     carry += total;
     __syncthreads();
@@ -78,14 +92,22 @@ __global__ __launch_bounds__(kScanThreads) void scan_rows_kernel(const float* __
 hipError_t launch_gate_prefix(const float* logit, float* log_f, float* c, int rows, int L,
                               hipStream_t s) {
   hipLaunchKernelGGL(scan_rows_kernel<0>, dim3(rows), dim3(kScanThreads), 0, s, logit, nullptr,
-                     log_f, c, L);
+                     nullptr, log_f, c, L);
   return hipGetLastError();
 }
 
 hipError_t launch_reverse_scan_sum(const float* a, const float* b, float* out, int rows, int L,
                                    hipStream_t s) {
-  hipLaunchKernelGGL(scan_rows_kernel<1>, dim3(rows), dim3(kScanThreads), 0, s, a, b, nullptr, out,
-                     L);
+  hipLaunchKernelGGL(scan_rows_kernel<1>, dim3(rows), dim3(kScanThreads), 0, s, a, b, nullptr,
+                     nullptr, out, L);
+  return hipGetLastError();
+}
+
+hipError_t launch_reverse_scan_gate(const float* a, const float* b, const float* logit,
+                                    float* d_log_f, float* d_logit, int rows, int L,
+                                    hipStream_t s) {
+  hipLaunchKernelGGL(scan_rows_kernel<2>, dim3(rows), dim3(kScanThreads), 0, s, a, b, logit,
+                     d_log_f, d_logit, L);
   return hipGetLastError();
 }
 

@@ -71,6 +71,16 @@ def test_gate_prefix_validation(lib):
     assert lib.fox_gate_prefix(c(P16), c(P16 + 4), c(P16), 1, 1, 4, None) == 4
 
 
+def test_dlogit_validation(lib):
+    c = ctypes.c_void_p
+    ok = [c(P16), c(P16), c(P16), None, c(P16)]
+    assert lib.fox_dlogit_from_dc(c(P16), c(P16), None, None, c(P16), 1, 1, 4, None) == 1
+    assert lib.fox_dlogit_from_dc(c(P16), c(P16), c(P16), c(P16), None, 1, 1, 4, None) == 1
+    assert lib.fox_dlogit_from_dc(*ok, 1, 1, 0, None) == 2
+    assert lib.fox_dlogit_from_dc(c(P16), c(P16), c(P16), c(P16 + 8), c(P16), 1, 1, 4, None) == 4
+    assert lib.fox_dlogit_from_dc(c(P16), c(P16), c(P16 + 4), None, c(P16), 1, 1, 4, None) == 4
+
+
 def test_bwd_validation_and_workspace(lib):
     c = ctypes.c_void_p
     B, H, L, d = 2, 3, 100, 128

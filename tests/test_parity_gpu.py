@@ -56,20 +56,24 @@ def check_fwd(dtype, o, lse, O, LSE, what=""):
         assert max_abs(lse, LSE) <= 1e-2, f"{what} LSE max-abs {max_abs(lse, LSE):.3e}"
 
 
-def check_bwd(dtype, got, ref, what=""):
-    """Relative L2 per gradient.  Where the exact gradient vanishes identically
-    (dQ = dK = d(log f) = 0 at L = 1) a relative error is undefined, and the
-    rounding residue is bounded absolutely instead."""
+def check_grad(dtype, name, g, r, what=""):
+    """Relative L2 of one gradient.  Where the exact gradient vanishes
+    identically (dQ = dK = d(log f) = 0 at L = 1) a relative error is undefined,
+    and the rounding residue is bounded absolutely instead."""
     lim = 1e-4 if dtype == "f32" else 2e-2
     lim_abs = 1e-5 if dtype == "f32" else 1e-3
+    r64 = r.detach().double().cpu()
+    if float(torch.linalg.vector_norm(r64)) <= 1e-9 * math.sqrt(r64.numel()):
+        e = max_abs(g, r64)
+        assert e <= lim_abs, f"{what} {name} (exactly zero) max-abs {e:.3e} > {lim_abs}"
+        return
+    e = rel_l2(g, r)
+    assert e <= lim, f"{what} {name} rel-L2 {e:.3e} > {lim}"
+
+
+def check_bwd(dtype, got, ref, what=""):
     for name, g, r in zip(("dQ", "dK", "dV", "dlogf"), got, ref):
-        r64 = r.detach().double().cpu()
-        if float(torch.linalg.vector_norm(r64)) <= 1e-9 * math.sqrt(r64.numel()):
-            e = max_abs(g, r64)
-            assert e <= lim_abs, f"{what} {name} (exactly zero) max-abs {e:.3e} > {lim_abs}"
-            continue
-        e = rel_l2(g, r)
-        assert e <= lim, f"{what} {name} rel-L2 {e:.3e} > {lim}"
+        check_grad(dtype, name, g, r, what)
 
 
 @pytest.fixture(autouse=True)
@@ -333,3 +337,28 @@ def test_backward_stages_equal_fused_entry_point():
         torch.cuda.synchronize()
         for a, b in zip(ref, (dq, dk, dv, dlf)):
             assert torch.equal(a, b), dtype
+
+
+# ------------------------------------------------------------ gate backward
+@pytest.mark.parametrize("dtype,d,L", [("f32", 64, 100), ("bf16", 64, 1), ("bf16", 64, 129),
+                                       ("bf16", 128, 700), ("bf16", 128, 4100)])
+def test_gate_logit_gradient(dtype, d, L):
+    """d(logit) = d(log f) * sigmoid(-logit), fused into the reverse scan, against
+    the oracle; its d(log f) output equals fox_dlogf_from_dc bit for bit."""
+    print(f"gate logit gradient dtype={dtype} d={d} L={L}", flush=True)
+    x = inputs.attn_inputs(2, 2, L, d, dtype, ("normal", 2.0, 1.5), 300 + L, device=DEV)
+    s = fox.default_scale(d)
+    c, o, lse = gpu_forward(x, s)
+    delta = fox.fox_attn_bwd_delta(o, x["do"])
+    _, _, dck = fox.fox_attn_bwd_dkdv(x["q"], x["k"], x["v"], c, lse, x["do"], delta, s)
+    _, dcq = fox.fox_attn_bwd_dq(x["q"], x["k"], x["v"], c, lse, x["do"], delta, s)
+    dlf_ref_gpu = fox.fox_dlogf_from_dc(dcq, dck)
+    dx, dlf = fox.fox_dlogit_from_dc(dcq, dck, x["logit"], d_log_f=torch.empty_like(dcq))
+    dx_only = fox.fox_dlogit_from_dc(dcq, dck, x["logit"])
+    torch.cuda.synchronize()
+    assert torch.equal(dlf, dlf_ref_gpu)
+    assert torch.equal(dx, dx_only)
+    xc = cpu(x)
+    ref = oracle.backward_logit(xc["q"], xc["k"], xc["v"], xc["logit"], xc["do"], s)[3]
+    check_grad(dtype, "dlogit", dx, ref, f"L={L}")
+    assert float(dx[..., 0].abs().max()) <= 1e-3 * max(1.0, float(ref.abs().max()))
