@@ -16,8 +16,12 @@ from __future__ import annotations
 
 import argparse
 import contextlib
+import csv
+import glob
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -32,6 +36,26 @@ from paper_2503_02130_amd import inputs  # noqa: E402
 
 MFMA_BF16_PEAK_TFLOPS = 2516.6   # MI355X dense bf16 (256 CU x 2.4 GHz x 4096 FLOP/clk)
 HBM_PEAK_GBS = 8000.0            # MI355X HBM3E
+
+CSRC = os.path.join(ROOT, "paper_2503_02130_amd", "csrc")
+PROFILES = os.path.join(ROOT, "profiles")
+TRAFFIC_FILE = os.path.join(PROFILES, "hbm_traffic_bench_fwdbwd_l16384_decode_t32768.txt")
+# kernel -> the sources its machine code is built from (the traffic measured for
+# a kernel is reported only while these are unchanged)
+KERNEL_SOURCES = {
+    "bwd_dkdv_bf16_kernel": ("attn_bwd.hip", "fox_device.h"),
+    "bwd_dq_bf16_kernel": ("attn_bwd.hip", "fox_device.h"),
+    "fwd_bf16_kernel": ("attn_fwd.hip", "fox_device.h"),
+    "decode_split_kernel": ("attn_decode.hip", "fox_device.h"),
+}
+
+
+def sources_hash(kernel: str) -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
 
 
 def causal_pairs(B: int, H: int, L: int) -> int:
@@ -80,8 +104,9 @@ class EventTimer:
 
 def bench_train(w, steps, warmup):
     """One step = gate prefix -> forward -> backward, the backward through its
-    stage entry points (exactly what fox_attn_bwd runs) so that the dominant
-    kernel, dK/dV, can be bracketed by events on the call stream."""
+    stage entry points (what fox_attn_bwd runs, its last stage also producing the
+    gate-logit gradient) so that the dominant kernel, dK/dV, can be bracketed by
+    events on the call stream."""
     dev = torch.device("cuda:0")
     x = inputs.workload_inputs(w, device=dev)
     s = fox.default_scale(w.d)
@@ -90,7 +115,7 @@ def bench_train(w, steps, warmup):
     o = torch.empty_like(x["q"])
     lse = torch.empty((B, H, L), device=dev)
     dq, dk, dv = torch.empty_like(x["q"]), torch.empty_like(x["k"]), torch.empty_like(x["v"])
-    dlf, delta, dcq, dck = (torch.empty((B, H, L), device=dev) for _ in range(4))
+    dlf, dlogit, delta, dcq, dck = (torch.empty((B, H, L), device=dev) for _ in range(5))
     t_gate, t_fwd, t_dkdv, t_dq, t_bwd = (EventTimer() for _ in range(5))
 
     def step(timed):
@@ -106,7 +131,7 @@ def bench_train(w, steps, warmup):
             with t_dq.maybe(timed):
                 fox.fox_attn_bwd_dq(x["q"], x["k"], x["v"], c, lse, x["do"], delta, s, dq=dq,
                                     dc_q=dcq)
-            fox.fox_dlogf_from_dc(dcq, dck, d_log_f=dlf)
+            fox.fox_dlogit_from_dc(dcq, dck, x["logit"], d_logit=dlogit, d_log_f=dlf)
 
     for _ in range(warmup):
         step(False)
@@ -169,6 +194,94 @@ def cpu_baseline(w, n_heads=4):
                       f"at L={w.L}, d={w.d}: {dt:.1f} s; value = those slices' causal FLOPs / time"}
 
 
+def calibration_copy(mib: int):
+    """A plain device copy of `mib` MiB (reads and writes mib MiB): the reference
+    that scales the FETCH_SIZE / WRITE_SIZE counters to bytes."""
+    n = mib * 2**20 // 4
+    src = torch.rand(n, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"[bench] calibration copy of {mib} MiB done")
+
+
+def _counter_rows(d):
+    rows = []
+    for path in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        with open(path) as f:
+            rows += list(csv.DictReader(f))
+    if not rows:
+        raise SystemExit(f"no counter_collection.csv under {d}")
+    return rows
+
+
+def _kernel_family(name):
+    """fox::<family><...> (demangled or Itanium-mangled), or "copy" for the
+    runtime's device-to-device copy kernel; None for anything else."""
+    m = re.search(r"fox::(\w+)<", name)
+    if m:
+        return m.group(1)
+    m = re.match(r"_ZN3fox(\d+)", name)
+    if m:
+        n = int(m.group(1))
+        return name[m.end():m.end() + n]
+    return "copy" if "copyBuffer" in name else None
+
+
+def _per_kernel_kib(rows, counter):
+    """Mean counter value (KiB) per dispatch, per kernel family."""
+    per = {}
+    for r in rows:
+        if r["Counter_Name"] != counter:
+            continue
+        key = _kernel_family(r["Kernel_Name"])
+        if key is None:
+            continue
+        per.setdefault(key, {}).setdefault(r["Dispatch_Id"], 0.0)
+        per[key][r["Dispatch_Id"]] += float(r["Counter_Value"])
+    return per
+
+
+def pmc_summary(fetch_dir, write_dir, copy_mib, command):
+    """Text summary of two rocprofv3 --pmc passes (FETCH_SIZE, WRITE_SIZE) of this
+    benchmark run with --calibrate-copy-mib: per-launch HBM bytes of each kernel,
+    scaled by what the counters read for the plain copy of known size."""
+    fetch = _per_kernel_kib(_counter_rows(fetch_dir), "FETCH_SIZE")
+    write = _per_kernel_kib(_counter_rows(write_dir), "WRITE_SIZE")
+    # the calibration copy is by far the largest device-to-device copy of the run
+    cf = max(fetch["copy"].values())
+    cw = max(write["copy"].values())
+    f_fac = copy_mib * 1024.0 / cf
+    w_fac = copy_mib * 1024.0 / cw
+    lines = ["# HBM traffic per launch from rocprofv3 FETCH_SIZE / WRITE_SIZE",
+             f"# command (one pass per counter): {command}",
+             f"# calibration: plain copy of {copy_mib} MiB read {cf:.0f} KiB and wrote {cw:.0f} KiB;",
+             f"#   scale factors fetch {f_fac:.4f}, write {w_fac:.4f}",
+             "# kernel  dispatches  fetch_KiB  write_KiB  traffic_bytes_per_launch  sources_sha256"]
+    for k in sorted(KERNEL_SOURCES):
+        if k not in fetch or k not in write:
+            continue
+        fk = sum(fetch[k].values()) / len(fetch[k])
+        wk = sum(write[k].values()) / len(write[k])
+        tb = (fk * f_fac + wk * w_fac) * 1024.0
+        lines.append(f"{k} {len(fetch[k])} {fk:.1f} {wk:.1f} {tb:.0f} {sources_hash(k)}")
+    return "\n".join(lines) + "\n"
+
+
+def measured_traffic(kernel: str):
+    """Bytes per launch recorded for `kernel`, or None when there is no record or
+    the kernel's sources changed since the counters were taken."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    for line in open(TRAFFIC_FILE):
+        f = line.split()
+        if line.startswith("#") or len(f) != 6 or f[0] != kernel:
+            continue
+        return float(f[4]) if f[5] == sources_hash(kernel) else None
+    return None
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -178,7 +291,16 @@ def main():
     ap.add_argument("--decode-workload", default="decode_bf16_b64_h16_t32768_d128")
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="run a plain device copy of this size first (counter calibration)")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="summarise two rocprofv3 --pmc passes of this benchmark and exit")
+    ap.add_argument("--pmc-command", default="", help="the profiled command, for the summary")
     args = ap.parse_args()
+    if args.pmc_summary:
+        print(pmc_summary(*args.pmc_summary, args.calibrate_copy_mib or 1024, args.pmc_command),
+              end="")
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(Forgetting Attention shards over (batch, head) with no communication).",
@@ -189,6 +311,8 @@ def main():
         build.build()
     fox.load()
 
+    if args.calibrate_copy_mib:
+        calibration_copy(args.calibrate_copy_mib)
     w = inputs.WORKLOADS[args.workload]
     r = bench_train(w, args.steps, args.warmup)
     B, H, L, d = w.B, w.H, w.L, w.d
@@ -199,6 +323,10 @@ def main():
     # dK/dV kernel: its 4 GEMMs (S recomputed, dV, dP, dK) are 8d FLOPs per causal pair
     fl_kv = 8.0 * d * causal_pairs(B, H, L)
     kv_tf = fl_kv / (r["dkdv_ms"] * 1e-3) / 1e12
+    # compulsory HBM bytes of one dK/dV launch: read q, k, v, dO (bf16), c, LSE,
+    # delta (fp32); write dK, dV (bf16), dc_k (fp32)
+    kv_bytes = B * H * L * (6 * d * 2 + 4 * 4)
+    kv_traffic = measured_traffic("bwd_dkdv_bf16_kernel")
     out = {
         "metric": "Forgetting-attn fwd+bwd TFLOP/s bf16 L=16k d=128 (% MFMA peak); decode GB/s",
         "value": round(tflops, 2),
@@ -222,7 +350,8 @@ def main():
         "roofline": {"bound": "mfma", "kernel": "bwd_dkdv_bf16_kernel<128> (fox_attn_bwd_dkdv)",
                      "achieved": round(kv_tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(kv_tf / MFMA_BF16_PEAK_TFLOPS, 4),
-                     "traffic": None, "algorithmic_flops_per_launch": fl_kv},
+                     "traffic": kv_traffic, "algorithmic_flops_per_launch": fl_kv,
+                     "compulsory_bytes_per_launch": kv_bytes},
         "roofline_fwd": {"bound": "mfma", "kernel": "fwd_bf16_kernel<128> (fox_attn_fwd)",
                          "achieved": round(fwd_tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
                          "unit": "TFLOP/s", "frac": round(fwd_tf / MFMA_BF16_PEAK_TFLOPS, 4)},
@@ -243,7 +372,7 @@ def main():
                          "roofline": {"bound": "hbm", "kernel": "fox_attn_decode (split + combine)",
                                       "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
                                       "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
-                                      "traffic": None}}
+                                      "traffic": measured_traffic("decode_split_kernel")}}
         log(f"[bench] decode {rd['ms']:.3f} ms -> {gbs:.0f} GB/s")
     if not args.no_cpu_baseline:
         log("[bench] timing the fp64 oracle on the host")
