@@ -9,4 +9,6 @@ from .fox_oracle import (  # noqa: F401
     forward_head_from_c, backward_head_from_c, reverse_cumsum,
     forward_from_logf, forward, backward_from_logf, backward, decode,
     gate_backward, backward_logit,
+    time_constant, fixed_gate_bias_init, fixed_gate_log_f, forward_fixed_gate,
+    backward_fixed_gate,
 )

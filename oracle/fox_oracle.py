@@ -27,6 +27,10 @@ paper (Forgetting Transformer, arXiv 2503.02130):
                                d(log f)_l = sum_{i >= l} dc_i  (reverse cumsum)
   * d(logit)                   through f = sigmoid(logit): d(logit) =
                                d(log f) * sigmoid(-logit)      (Sec. 3, gate def.)
+  * fixed gates                f_t^(h) = sigmoid(b^(h)) for all t (ALiBi with slope
+                               -log sigmoid(b^(h)), Sec. 3); b^(h) initialised so that
+                               T(b) = -1/log sigmoid(b) is log-spaced in [T_min, T_max]
+                                                              (appendix, gate init.)
   * decode                     the forward's last row for a sequence whose last
                                key/value is the new token, c_T = c_{T-1} +
                                log sigmoid(x_new), c_0 = 0    (Eq. fot-weight at i = T)
@@ -197,6 +201,45 @@ def backward_logit(q, k, v, logit, dO, scale: float, heads=None):
     """dQ, dK, dV and the gradient with respect to the gate logits."""
     dQ, dK, dV, dlf = backward(q, k, v, logit, dO, scale, heads)
     return dQ, dK, dV, gate_backward(logit, dlf)
+
+
+# ---------------------------------------------------------------------------
+# Data-independent / fixed forget gates (Sec. 3 "Connection to ALiBi"; Sec. 5
+# ablations; appendix "Data-independent forget gate initialization")
+# ---------------------------------------------------------------------------
+def time_constant(b) -> torch.Tensor:
+    """T(b) = 1 / (-log sigmoid(b)): the steps a gate sigmoid(b) needs to decay by 1/e."""
+    return -1.0 / log_sigmoid(b)
+
+
+def fixed_gate_bias_init(H: int, t_min: float, t_max: float) -> torch.Tensor:
+    """b^(h), h = 1..H, with T(b^(h)) log-spaced from T_min to T_max.  Inverting
+    T: sigmoid(b) = exp(-1/T), so b = log(e^{-1/T} / (1 - e^{-1/T})).  For H = 1
+    the spacing is undefined; the single head takes T_min."""
+    h = torch.arange(H, dtype=F64)
+    frac = h / (H - 1) if H > 1 else torch.zeros(1, dtype=F64)
+    T = torch.exp(math.log(t_min) + (math.log(t_max) - math.log(t_min)) * frac)
+    return -1.0 / T - torch.log(-torch.expm1(-1.0 / T))
+
+
+def fixed_gate_log_f(bias, B: int, L: int) -> torch.Tensor:
+    """log f_t^(h) = log sigmoid(b^(h)) for every batch row and time step: [B,H,L]."""
+    lf = log_sigmoid(bias)
+    return lf[None, :, None].expand(B, lf.shape[0], L).clone()
+
+
+def forward_fixed_gate(q, k, v, bias, scale: float, heads=None, rows=None):
+    B, H, L, _ = q.shape
+    return forward_from_logf(q, k, v, fixed_gate_log_f(bias, B, L), scale, heads, rows)
+
+
+def backward_fixed_gate(q, k, v, bias, dO, scale: float):
+    """dQ, dK, dV and d b^(h) [H]: every log f_t^(h) is log sigmoid(b^(h)), so
+    d b^(h) = sigmoid(-b^(h)) * sum over batch and time of d(log f)."""
+    B, H, L, _ = q.shape
+    dQ, dK, dV, dlf = backward_from_logf(q, k, v, fixed_gate_log_f(bias, B, L), dO, scale)
+    db = torch.sigmoid(-_f64(bias)) * dlf.sum(dim=(0, 2))
+    return dQ, dK, dV, db
 
 
 def decode(q, k_cache, v_cache, cached_logit, logit_new, scale: float, heads=None):

@@ -32,10 +32,13 @@ The pins, with what in the paper fixes them:
   P13 L = 2 written out by hand.
   P14 gate-logit gradient: central finite differences through the logits, the
       zero gradient of the first gate, and the sigmoid-derivative closed form.
+  P15 fixed gates: the appendix's initialisation example (golden file), the
+      equivalence with ALiBi at slopes 1/T_h, and d b by finite differences.
 """
 from __future__ import annotations
 
 import math
+import os
 
 import torch
 import torch.nn.functional as Fnn
@@ -350,6 +353,70 @@ def pin_p14_gate_logit_gradient(ora, B=1, H=2, L=7, d=3, seed=14):
     assert abs(float(factor[3]) - 0.5) <= 1e-15
 
 
+# --------------------------------------------------------------------------- P15
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _read_golden(name):
+    vals = {}
+    for line in open(os.path.join(GOLDEN, name)):
+        line = line.split("#", 1)[0].split()
+        if line:
+            vals[line[0]] = [float(x) for x in line[1:]]
+    return vals
+
+
+def pin_p15_fixed_gate_init_worked_example(ora):
+    """The appendix's worked example: H = 4, (T_min, T_max) = (2, 128) gives time
+    constants (2, 8, 32, 128); and sigmoid(b)^T(b) = 1/e by definition of T."""
+    g = _read_golden("fixed_gate_init.txt")
+    b = ora.fixed_gate_bias_init(int(g["H"][0]), g["T_min"][0], g["T_max"][0])
+    _close(ora.time_constant(b), torch.tensor(g["T"], dtype=F64), 1e-11, "P15 T(b_init)")
+    _close(torch.sigmoid(b) ** ora.time_constant(b), torch.full_like(b, math.exp(-1.0)), 1e-14,
+           "P15 sigmoid(b)^T(b) = 1/e")
+    assert torch.all(b[1:] > b[:-1]), "P15 longer time constants need larger biases"
+
+
+def pin_p15_fixed_gate_is_alibi_with_init_slopes(ora, B=1, H=4, L=26, d=8, seed=15):
+    """A fixed gate initialised with (T_min, T_max) is ALiBi with slopes 1/T_h,
+    ranging from 1/T_max to 1/T_min (Sec. 3 and the appendix)."""
+    q, k, v, dO = (_rand((B, H, L, d), seed + i) for i in range(4))
+    s = 1.0 / math.sqrt(d)
+    b = ora.fixed_gate_bias_init(H, 2.0, 128.0)
+    slopes = torch.tensor([1 / 2, 1 / 8, 1 / 32, 1 / 128], dtype=F64)
+    i = torch.arange(L, dtype=F64)
+    dist = i[:, None] - i[None, :]
+    mask = -slopes[:, None, None] * dist[None]
+    mask = mask.masked_fill(dist[None] < 0, -math.inf)[None].expand(B, H, L, L)
+    O, _ = ora.forward_fixed_gate(q, k, v, b, s)
+    Oref, _, _, _ = _sdpa_with_grads(q, k, v, dO, s, mask)
+    _close(O, Oref, 1e-11, "P15 fixed gate = ALiBi(1/T_h)")
+
+
+def _objective_bias(ora, q, k, v, b, dO, s):
+    O, _ = ora.forward_fixed_gate(q, k, v, b, s)
+    return float((O * dO).sum())
+
+
+def pin_p15_fixed_gate_bias_gradient(ora, B=2, H=3, L=9, d=3, seed=25):
+    """d b^(h) equals central finite differences of sum(O o dO) in b^(h)."""
+    q, k, v, dO = (_rand((B, H, L, d), seed + i) for i in range(4))
+    b = _rand((H,), seed + 5) + 1.0
+    s = 0.5
+    _, _, _, db = ora.backward_fixed_gate(q, k, v, b, dO, s)
+    eps = 1e-6
+    for h in range(H):
+        old = float(b[h])
+        b[h] = old + eps
+        fp = _objective_bias(ora, q, k, v, b, dO, s)
+        b[h] = old - eps
+        fm = _objective_bias(ora, q, k, v, b, dO, s)
+        b[h] = old
+        fd = (fp - fm) / (2 * eps)
+        assert abs(fd - float(db[h])) <= 1e-7 * max(1.0, abs(fd)), \
+            f"P15 db[{h}]: finite difference {fd:.9f} vs oracle {float(db[h]):.9f}"
+
+
 ALL_PINS = [
     pin_p1_zero_forgetting_is_softmax_attention,
     pin_p2_full_forgetting,
@@ -366,4 +433,7 @@ ALL_PINS = [
     pin_p12_zero_query_closed_forms,
     pin_p13_two_tokens,
     pin_p14_gate_logit_gradient,
+    pin_p15_fixed_gate_init_worked_example,
+    pin_p15_fixed_gate_is_alibi_with_init_slopes,
+    pin_p15_fixed_gate_bias_gradient,
 ]

@@ -120,6 +120,23 @@ def _m_gate_factor_sign(m):
     m.gate_backward = lambda logit, dlf: m._f64(dlf) * torch.sigmoid(m._f64(logit))
 
 
+def _m_init_linear_spacing(m):
+    """Time constants spaced linearly instead of logarithmically."""
+    def init(H, t_min, t_max):
+        T = torch.linspace(t_min, t_max, H, dtype=torch.float64)
+        return -1.0 / T - torch.log(-torch.expm1(-1.0 / T))
+    m.fixed_gate_bias_init = init
+
+
+def _m_fixed_db_no_gate_factor(m):
+    """d b summed without the sigmoid(-b) factor."""
+    def bwd(q, k, v, bias, dO, scale):
+        B, H, L, _ = q.shape
+        dQ, dK, dV, dlf = m.backward_from_logf(q, k, v, m.fixed_gate_log_f(bias, B, L), dO, scale)
+        return dQ, dK, dV, dlf.sum(dim=(0, 2))
+    m.backward_fixed_gate = bwd
+
+
 MUTANTS = {
     "decay_scaled": _m_scale_on_D,
     "exclusive_prefix": _m_exclusive_c,
@@ -136,6 +153,8 @@ MUTANTS = {
     "decode_bias_sign": _m_decode_sign,
     "scale_squared": _m_scale_twice,
     "gate_factor_sign": _m_gate_factor_sign,
+    "init_linear_spacing": _m_init_linear_spacing,
+    "fixed_db_no_gate_factor": _m_fixed_db_no_gate_factor,
 }
 
 
