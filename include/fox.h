@@ -179,6 +179,40 @@ int fox_attn_decode(int dtype, const void* q, const void* k_cache, const void* v
                     void* workspace, size_t workspace_bytes,
                     int B, int H, int T, int d, float scale, void* stream);
 
+/*
+ * Fixed (data-independent) forget gates: f_t^(h) = sigmoid(b^(h)) for every t
+ * (Sec. 3, "Connection to ALiBi": ALiBi with slope -log sigmoid(b^(h))).  The
+ * kernels form c_i - c_j = (i - j) log sigmoid(b^(h)) from the positions, so no
+ * prefix array exists; everything else is as in the entry points above.
+ *
+ * fox_fixed_gate_init: the appendix "Data-independent forget gate
+ *   initialization": with T(b) = 1 / (-log sigmoid(b)), head h = 0..H-1 gets
+ *   T(b^(h)) = exp(log T_min + (log T_max - log T_min) h / (H - 1)) (H = 1: T_min).
+ *   gate_bias is HOST memory [H] fp32 (out).  Requires 0 < t_min <= t_max.
+ *   No device work.
+ * fox_attn_fwd_fixed_gate: O, LSE as fox_attn_fwd; gate_bias [H] fp32 device.
+ * fox_attn_bwd_fixed_gate: dq, dk, dv as fox_attn_bwd, and the gradient of the
+ *   biases d_gate_bias [H] fp32 (may be NULL for a gate that is not trained):
+ *   d b^(h) = sigmoid(-b^(h)) * sum over batch and t of d(log f)_t^(h).
+ *   workspace: at least fox_attn_bwd_fixed_gate_workspace_bytes().
+ * fox_attn_decode_fixed_gate: one decode step as fox_attn_decode, without a
+ *   prefix cache; workspace: fox_attn_decode_workspace_bytes().
+ */
+int fox_fixed_gate_init(float* gate_bias, int H, float t_min, float t_max);
+int fox_attn_fwd_fixed_gate(int dtype, const void* q, const void* k, const void* v,
+                            const float* gate_bias, void* o, float* lse, int B, int H, int L, int d,
+                            float scale, void* stream);
+size_t fox_attn_bwd_fixed_gate_workspace_bytes(int dtype, int B, int H, int L, int d);
+int fox_attn_bwd_fixed_gate(int dtype, const void* q, const void* k, const void* v,
+                            const float* gate_bias, const void* o, const float* lse,
+                            const void* d_o, void* dq, void* dk, void* dv, float* d_gate_bias,
+                            void* workspace, size_t workspace_bytes, int B, int H, int L, int d,
+                            float scale, void* stream);
+int fox_attn_decode_fixed_gate(int dtype, const void* q, const void* k_cache,
+                               const void* v_cache, const float* gate_bias, void* o, float* lse,
+                               void* workspace, size_t workspace_bytes, int B, int H, int T, int d,
+                               float scale, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

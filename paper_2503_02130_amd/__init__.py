@@ -9,13 +9,18 @@ from ._lib import (  # noqa: F401
     FoxError, default_scale, load, status_string,
     fox_gate_prefix, fox_attn_fwd, fox_attn_bwd, fox_attn_bwd_workspace_bytes,
     fox_attn_bwd_delta, fox_attn_bwd_dkdv, fox_attn_bwd_dq, fox_dlogf_from_dc,
-    fox_dlogit_from_dc, fox_attn_decode, fox_attn_decode_workspace_bytes, LIB_PATH, EXPORTED,
+    fox_dlogit_from_dc, fox_attn_decode,
+    fox_fixed_gate_init, fox_attn_fwd_fixed_gate, fox_attn_bwd_fixed_gate,
+    fox_attn_bwd_fixed_gate_workspace_bytes, fox_attn_decode_fixed_gate,
+    fox_attn_decode_workspace_bytes, LIB_PATH, EXPORTED,
 )
 
 __all__ = [
     "FoxError", "default_scale", "load", "status_string",
     "fox_gate_prefix", "fox_attn_fwd", "fox_attn_bwd", "fox_attn_bwd_workspace_bytes",
     "fox_attn_bwd_delta", "fox_attn_bwd_dkdv", "fox_attn_bwd_dq", "fox_dlogf_from_dc",
-    "fox_dlogit_from_dc",
+    "fox_dlogit_from_dc", "fox_fixed_gate_init", "fox_attn_fwd_fixed_gate",
+    "fox_attn_bwd_fixed_gate", "fox_attn_bwd_fixed_gate_workspace_bytes",
+    "fox_attn_decode_fixed_gate",
     "fox_attn_decode", "fox_attn_decode_workspace_bytes",
 ]

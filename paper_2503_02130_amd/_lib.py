@@ -27,6 +27,8 @@ EXPORTED = (
     "fox_attn_bwd_workspace_bytes", "fox_attn_bwd", "fox_attn_bwd_delta", "fox_attn_bwd_dkdv",
     "fox_attn_bwd_dq", "fox_dlogf_from_dc", "fox_dlogit_from_dc",
     "fox_attn_decode_workspace_bytes", "fox_attn_decode",
+    "fox_fixed_gate_init", "fox_attn_fwd_fixed_gate", "fox_attn_bwd_fixed_gate_workspace_bytes",
+    "fox_attn_bwd_fixed_gate", "fox_attn_decode_fixed_gate",
 )
 
 
@@ -76,6 +78,17 @@ def load() -> ctypes.CDLL:
     lib.fox_attn_decode_workspace_bytes.argtypes = [I, I, I, I, I]
     lib.fox_attn_decode.restype = I
     lib.fox_attn_decode.argtypes = [I, P, P, P, P, P, P, P, P, Z, I, I, I, I, F, P]
+    lib.fox_fixed_gate_init.restype = I
+    lib.fox_fixed_gate_init.argtypes = [P, I, F, F]
+    lib.fox_attn_fwd_fixed_gate.restype = I
+    lib.fox_attn_fwd_fixed_gate.argtypes = [I, P, P, P, P, P, P, I, I, I, I, F, P]
+    lib.fox_attn_bwd_fixed_gate_workspace_bytes.restype = Z
+    lib.fox_attn_bwd_fixed_gate_workspace_bytes.argtypes = [I, I, I, I, I]
+    lib.fox_attn_bwd_fixed_gate.restype = I
+    lib.fox_attn_bwd_fixed_gate.argtypes = [I, P, P, P, P, P, P, P, P, P, P, P, P, Z, I, I, I, I,
+                                            F, P]
+    lib.fox_attn_decode_fixed_gate.restype = I
+    lib.fox_attn_decode_fixed_gate.argtypes = [I, P, P, P, P, P, P, P, Z, I, I, I, I, F, P]
     _lib = lib
     return lib
 
@@ -326,4 +339,105 @@ def fox_attn_decode(q, k_cache, v_cache, c_cache, gate_logit_new, scale: Optiona
                                 workspace.numel() * workspace.element_size(), B, H, T, d, s,
                                 _stream(q))
     _raise(st, "fox_attn_decode")
+    return o, lse
+
+
+# ---------------------------------------------------------------- fixed gates
+def fox_fixed_gate_init(H: int, t_min: float, t_max: float) -> torch.Tensor:
+    """Biases b [H] (host fp32) whose time constants T(b) = -1/log sigmoid(b)
+    are log-spaced from t_min to t_max (the paper's fixed-gate initialisation)."""
+    out = torch.empty(H, dtype=torch.float32)
+    st = load().fox_fixed_gate_init(ctypes.c_void_p(out.data_ptr()), H, float(t_min), float(t_max))
+    _raise(st, "fox_fixed_gate_init")
+    return out
+
+
+def fox_attn_fwd_fixed_gate(q, k, v, gate_bias, scale: Optional[float] = None, o=None, lse=None):
+    """O, LSE with the fixed gate f_t^(h) = sigmoid(gate_bias[h]) (ALiBi form)."""
+    B, H, L, d = q.shape
+    dt = q.dtype
+    if dt not in _DT:
+        raise ValueError(f"unsupported dtype {dt}")
+    dev = q.device
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _check(t, name, (B, H, L, d), dt, dev)
+    _check(gate_bias, "gate_bias", (H,), torch.float32, dev)
+    o = torch.empty_like(q) if o is None else o
+    lse = torch.empty((B, H, L), device=dev, dtype=torch.float32) if lse is None else lse
+    _check(o, "o", (B, H, L, d), dt, dev)
+    _check(lse, "lse", (B, H, L), torch.float32, dev)
+    s = default_scale(d) if scale is None else float(scale)
+    st = load().fox_attn_fwd_fixed_gate(_DT[dt], _ptr(q), _ptr(k), _ptr(v), _ptr(gate_bias),
+                                        _ptr(o), _ptr(lse), B, H, L, d, s, _stream(q))
+    _raise(st, "fox_attn_fwd_fixed_gate")
+    return o, lse
+
+
+def fox_attn_bwd_fixed_gate_workspace_bytes(dtype: torch.dtype, B: int, H: int, L: int,
+                                            d: int) -> int:
+    return int(load().fox_attn_bwd_fixed_gate_workspace_bytes(_DT[dtype], B, H, L, d))
+
+
+def fox_attn_bwd_fixed_gate(q, k, v, gate_bias, o, lse, d_o, scale: Optional[float] = None,
+                            dq=None, dk=None, dv=None, d_gate_bias=None, want_bias_grad=True,
+                            workspace=None):
+    """dq, dk, dv and d gate_bias [H] (None when want_bias_grad is False)."""
+    B, H, L, d = q.shape
+    dt = q.dtype
+    if dt not in _DT:
+        raise ValueError(f"unsupported dtype {dt}")
+    dev = q.device
+    for name, t in (("q", q), ("k", k), ("v", v), ("o", o), ("d_o", d_o)):
+        _check(t, name, (B, H, L, d), dt, dev)
+    _check(gate_bias, "gate_bias", (H,), torch.float32, dev)
+    _check(lse, "lse", (B, H, L), torch.float32, dev)
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(k) if dk is None else dk
+    dv = torch.empty_like(v) if dv is None else dv
+    for name, t in (("dq", dq), ("dk", dk), ("dv", dv)):
+        _check(t, name, (B, H, L, d), dt, dev)
+    if want_bias_grad:
+        d_gate_bias = torch.empty_like(gate_bias) if d_gate_bias is None else d_gate_bias
+        _check(d_gate_bias, "d_gate_bias", (H,), torch.float32, dev)
+    else:
+        d_gate_bias = None
+    need = fox_attn_bwd_fixed_gate_workspace_bytes(dt, B, H, L, d)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), device=dev, dtype=torch.uint8)
+    s = default_scale(d) if scale is None else float(scale)
+    st = load().fox_attn_bwd_fixed_gate(_DT[dt], _ptr(q), _ptr(k), _ptr(v), _ptr(gate_bias),
+                                        _ptr(o), _ptr(lse), _ptr(d_o), _ptr(dq), _ptr(dk),
+                                        _ptr(dv), _ptr(d_gate_bias), _ptr(workspace),
+                                        workspace.numel() * workspace.element_size(),
+                                        B, H, L, d, s, _stream(q))
+    _raise(st, "fox_attn_bwd_fixed_gate")
+    return dq, dk, dv, d_gate_bias
+
+
+def fox_attn_decode_fixed_gate(q, k_cache, v_cache, gate_bias, scale: Optional[float] = None,
+                               o=None, lse=None, workspace=None):
+    """One decode step with fixed gates (no prefix cache).  Returns o, lse."""
+    B, H, d = q.shape
+    T = k_cache.shape[2]
+    dt = q.dtype
+    if dt not in _DT:
+        raise ValueError(f"unsupported dtype {dt}")
+    dev = q.device
+    _check(q, "q", (B, H, d), dt, dev)
+    _check(k_cache, "k_cache", (B, H, T, d), dt, dev)
+    _check(v_cache, "v_cache", (B, H, T, d), dt, dev)
+    _check(gate_bias, "gate_bias", (H,), torch.float32, dev)
+    o = torch.empty_like(q) if o is None else o
+    lse = torch.empty((B, H), device=dev, dtype=torch.float32) if lse is None else lse
+    _check(o, "o", (B, H, d), dt, dev)
+    _check(lse, "lse", (B, H), torch.float32, dev)
+    need = fox_attn_decode_workspace_bytes(dt, B, H, T, d)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), device=dev, dtype=torch.uint8)
+    s = default_scale(d) if scale is None else float(scale)
+    st = load().fox_attn_decode_fixed_gate(_DT[dt], _ptr(q), _ptr(k_cache), _ptr(v_cache),
+                                           _ptr(gate_bias), _ptr(o), _ptr(lse), _ptr(workspace),
+                                           workspace.numel() * workspace.element_size(),
+                                           B, H, T, d, s, _stream(q))
+    _raise(st, "fox_attn_decode_fixed_gate")
     return o, lse

@@ -78,13 +78,13 @@ struct DqSmem {
   float cref[2];  // the tile's reference prefix value
 };
 
-template <int D>
+template <int D, bool FIXED>
 __global__ __launch_bounds__(kBwdThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
-                        const bf16* __restrict__ V, const float* __restrict__ C,
+                        const bf16* __restrict__ V, const float* __restrict__ gate,
                         const float* __restrict__ LSE, const bf16* __restrict__ dO,
                         const float* __restrict__ delta, bf16* __restrict__ dQ,
-                        float* __restrict__ dcq, int BH, int L, int n_mblk, float scale,
+                        float* __restrict__ dcq, int BH, int H, int L, int n_mblk, float scale,
                         float scale_log2) {
   constexpr int TILE = kDqBN * D;
   constexpr int NDMA = TILE * 2 / 1024 / kDqWaves;
@@ -96,7 +96,7 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
   const int mblk = n_mblk - 1 - (int)(blockIdx.x / BH);
   const int q0 = mblk * kDqBM;
   const size_t head = (size_t)bh * (size_t)L;
-  const float* Ch = C + head;
+  const GateRow<FIXED> gr(gate, bh, H, head);
   const int qw0 = q0 + wave * 32;
   const int qi = qw0 + col;
   const bool q_valid = qi < L;
@@ -124,7 +124,8 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
       }
     }
   }
-  const float cq = q_valid ? Ch[qi] : 0.0f;
+  float cq = 0.0f;  // c_i itself (prefix array only)
+  if constexpr (!FIXED) cq = q_valid ? gr.c[qi] : 0.0f;
   const float lse_q = q_valid ? LSE[head + qi] : 0.0f;
   const float dlt = q_valid ? delta[head + qi] : 0.0f;
 
@@ -152,8 +153,9 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
     }
     if (wave == 0) {
       const int key = kt * kDqBN + lane;
-      crefreg = Ch[kt * kDqBN / kRefBlock * kRefBlock];
-      creg = key < L ? (Ch[key] - crefreg) * kLog2e : INFINITY;
+      const int kref = kt * kDqBN / kRefBlock * kRefBlock;
+      if constexpr (!FIXED) crefreg = gr.c[kref];
+      creg = key < L ? gr.diff(key, kref) * kLog2e : INFINITY;
     }
   };
   auto store_c = [&](auto bufc) {
@@ -171,7 +173,8 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
     const bf16* vt_ = sm.v[B];
     const float* ct_ = sm.c[B];
     const int key0 = j * kDqBN;
-    const float bq = q_valid ? ((cq - sm.cref[B]) - lse_q) * inv_scale : -INFINITY;
+    const float dref = FIXED ? gr.diff(qi, key0 / kRefBlock * kRefBlock) : cq - sm.cref[B];
+    const float bq = q_valid ? (dref - lse_q) * inv_scale : -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       f32x16 sacc, pacc;
@@ -306,12 +309,12 @@ struct KvSmem {
   float dl[3][BM];  // Delta_i
 };
 
-template <int D>
+template <int D, bool FIXED>
 __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
-    const float* __restrict__ C, const float* __restrict__ LSE, const bf16* __restrict__ dO,
+    const float* __restrict__ gate, const float* __restrict__ LSE, const bf16* __restrict__ dO,
     const float* __restrict__ delta, bf16* __restrict__ dK, bf16* __restrict__ dV,
-    float* __restrict__ dck, int BH, int L, float scale, float scale_log2) {
+    float* __restrict__ dck, int BH, int H, int L, float scale, float scale_log2) {
   constexpr int kKvBM = kv_bm<D>();
   constexpr int NQB = kKvBM / 32;  // 32-query sub-blocks per tile
   constexpr int TILE = kKvBM * D;
@@ -327,10 +330,9 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
   const int nblk = (int)(blockIdx.x / BH);  // key block 0 has the most work: first
   const int k0 = nblk * kKvBN;
   const size_t head = (size_t)bh * (size_t)L;
-  const float* Ch = C + head;
+  const GateRow<FIXED> gr(gate, bh, H, head);  // reference: c at k0
   const float* Lh = LSE + head;
   const float* Dh = delta + head;
-  const float c_ref = Ch[k0];
   const int kw0 = k0 + pair * 32;
   const int kj = kw0 + col;
   const bool k_valid = kj < L;
@@ -380,7 +382,7 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
       }
     }
   }
-  const float ck2 = k_valid ? (Ch[kj] - c_ref) * kLog2e : INFINITY;
+  const float ck2 = k_valid ? gr.diff(kj, k0) * kLog2e : INFINITY;
 
   f32x16 acc[D / 32];  // dV^T (P waves) or dK^T (G waves)
 #pragma unroll
@@ -410,7 +412,7 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
       breg = -INFINITY;
       dreg = 0.0f;
       if (qq < L) {
-        breg = ((Ch[qq] - c_ref) - Lh[qq]) * inv_scale;
+        breg = (gr.diff(qq, k0) - Lh[qq]) * inv_scale;
         dreg = Dh[qq];
       }
     }
@@ -562,24 +564,24 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
 constexpr int kF32Threads = 256;
 constexpr int kF32Tile = 32;
 
-template <int D>
+template <int D, bool FIXED>
 __global__ __launch_bounds__(kF32Threads) void bwd_dq_f32_kernel(
     const float* __restrict__ Q, const float* __restrict__ K, const float* __restrict__ V,
-    const float* __restrict__ C, const float* __restrict__ LSE, const float* __restrict__ dO,
-    const float* __restrict__ delta, float* __restrict__ dQ, float* __restrict__ dcq, int L,
-    int n_blk, float scale, float scale_log2) {
+    const float* __restrict__ gate, const float* __restrict__ LSE, const float* __restrict__ dO,
+    const float* __restrict__ delta, float* __restrict__ dQ, float* __restrict__ dcq, int H,
+    int L, int n_blk, float scale, float scale_log2) {
   constexpr int G = D / 32;
   constexpr int RPW = kF32Threads / G;
   __shared__ float ks[kF32Tile][D + 1];
   __shared__ float vs[kF32Tile][D + 1];
   __shared__ float cks[kF32Tile];
   const int tid = threadIdx.x, sub = tid % G;
-  const size_t head = (size_t)(blockIdx.x / n_blk) * (size_t)L;
+  const int bh = (int)(blockIdx.x / n_blk);
+  const size_t head = (size_t)bh * (size_t)L;
   const int q0 = (int)(blockIdx.x % n_blk) * RPW;
   const int qi = q0 + tid / G;
   const bool q_valid = qi < L;
-  const float* Ch = C + head;
-  const float c_ref = Ch[q0];
+  const GateRow<FIXED> gr(gate, bh, H, head);
   float qv[32], gv[32], acc[32];
 #pragma unroll
   for (int e = 0; e < 32; ++e) {
@@ -587,7 +589,7 @@ __global__ __launch_bounds__(kF32Threads) void bwd_dq_f32_kernel(
     gv[e] = q_valid ? dO[(head + qi) * D + sub * 32 + e] : 0.0f;
     acc[e] = 0.0f;
   }
-  const float cq = q_valid ? Ch[qi] - c_ref : 0.0f;
+  const float cq = q_valid ? gr.diff(qi, q0) : 0.0f;
   const float lq = q_valid ? LSE[head + qi] : INFINITY;
   const float dlt = q_valid ? delta[head + qi] : 0.0f;
   float dc = 0.0f;
@@ -601,7 +603,7 @@ __global__ __launch_bounds__(kF32Threads) void bwd_dq_f32_kernel(
     }
     if (tid < kF32Tile) {
       const int key = key0 + tid;
-      cks[tid] = key < L ? Ch[key] - c_ref : INFINITY;
+      cks[tid] = key < L ? gr.diff(key, q0) : INFINITY;
     }
     __syncthreads();
     for (int j = 0; j < kF32Tile; ++j) {
@@ -631,12 +633,12 @@ __global__ __launch_bounds__(kF32Threads) void bwd_dq_f32_kernel(
   }
 }
 
-template <int D>
+template <int D, bool FIXED>
 __global__ __launch_bounds__(kF32Threads) void bwd_dkdv_f32_kernel(
     const float* __restrict__ Q, const float* __restrict__ K, const float* __restrict__ V,
-    const float* __restrict__ C, const float* __restrict__ LSE, const float* __restrict__ dO,
+    const float* __restrict__ gate, const float* __restrict__ LSE, const float* __restrict__ dO,
     const float* __restrict__ delta, float* __restrict__ dK, float* __restrict__ dV,
-    float* __restrict__ dck, int L, int n_blk, float scale, float scale_log2) {
+    float* __restrict__ dck, int H, int L, int n_blk, float scale, float scale_log2) {
   constexpr int G = D / 32;
   constexpr int RPW = kF32Threads / G;
   __shared__ float qs[kF32Tile][D + 1];
@@ -645,12 +647,12 @@ __global__ __launch_bounds__(kF32Threads) void bwd_dkdv_f32_kernel(
   __shared__ float lqs[kF32Tile];
   __shared__ float dls[kF32Tile];
   const int tid = threadIdx.x, sub = tid % G;
-  const size_t head = (size_t)(blockIdx.x / n_blk) * (size_t)L;
+  const int bh = (int)(blockIdx.x / n_blk);
+  const size_t head = (size_t)bh * (size_t)L;
   const int k0 = (int)(blockIdx.x % n_blk) * RPW;
   const int kj = k0 + tid / G;
   const bool k_valid = kj < L;
-  const float* Ch = C + head;
-  const float c_ref = Ch[k0];
+  const GateRow<FIXED> gr(gate, bh, H, head);
   float kv[32], vv[32], ak[32], av[32];
 #pragma unroll
   for (int e = 0; e < 32; ++e) {
@@ -659,7 +661,7 @@ __global__ __launch_bounds__(kF32Threads) void bwd_dkdv_f32_kernel(
     ak[e] = 0.0f;
     av[e] = 0.0f;
   }
-  const float ck = k_valid ? Ch[kj] - c_ref : -INFINITY;
+  const float ck = k_valid ? gr.diff(kj, k0) : -INFINITY;
   float dc = 0.0f;
   for (int qs0 = k0; qs0 < L; qs0 += kF32Tile) {
     __syncthreads();
@@ -670,7 +672,7 @@ __global__ __launch_bounds__(kF32Threads) void bwd_dkdv_f32_kernel(
     }
     if (tid < kF32Tile) {
       const int qq = qs0 + tid;
-      cqs[tid] = qq < L ? Ch[qq] - c_ref : 0.0f;
+      cqs[tid] = qq < L ? gr.diff(qq, k0) : 0.0f;
       lqs[tid] = qq < L ? LSE[head + qq] : INFINITY;
       dls[tid] = qq < L ? delta[head + qq] : 0.0f;
     }
@@ -732,85 +734,138 @@ hipError_t launch_bwd_delta(bool bf16_, const void* o, const void* d_o, float* d
                : launch_delta((const float*)o, (const float*)d_o, delta, BH, L, d, s);
 }
 
-hipError_t launch_bwd_dkdv(bool bf16_, const void* q, const void* k, const void* v,
-                           const float* c, const float* lse, const void* d_o, const float* delta,
-                           void* dk, void* dv, float* dck, int BH, int L, int d, float scale,
-                           hipStream_t s) {
+template <int D, bool FIXED>
+static void dkdv_t(bool bf16_, const void* q, const void* k, const void* v, GateSpec g,
+                   const float* lse, const void* d_o, const float* delta, void* dk, void* dv,
+                   float* dck, int BH, int L, float scale, hipStream_t s) {
   const float sl2 = scale * kLog2e;
   if (bf16_) {
     const dim3 grid((unsigned)((L + kKvBN - 1) / kKvBN) * (unsigned)BH);
-    if (d == 128) {
-      hipLaunchKernelGGL(bwd_dkdv_bf16_kernel<128>, grid, dim3(kKvThreads), 0, s, (const bf16*)q,
-                         (const bf16*)k, (const bf16*)v, c, lse, (const bf16*)d_o, delta,
-                         (bf16*)dk, (bf16*)dv, dck, BH, L, scale, sl2);
-    } else {
-      hipLaunchKernelGGL(bwd_dkdv_bf16_kernel<64>, grid, dim3(kKvThreads), 0, s, (const bf16*)q,
-                         (const bf16*)k, (const bf16*)v, c, lse, (const bf16*)d_o, delta,
-                         (bf16*)dk, (bf16*)dv, dck, BH, L, scale, sl2);
-    }
+    hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, FIXED>), grid, dim3(kKvThreads), 0, s,
+                       (const bf16*)q, (const bf16*)k, (const bf16*)v, g.ptr, lse,
+                       (const bf16*)d_o, delta, (bf16*)dk, (bf16*)dv, dck, BH, g.H, L, scale,
+                       sl2);
   } else {
-    const int rpw = kF32Threads / (d / 32);
+    const int rpw = kF32Threads / (D / 32);
     const int n_blk = (L + rpw - 1) / rpw;
     const dim3 grid((unsigned)n_blk * (unsigned)BH);
-    if (d == 128) {
-      hipLaunchKernelGGL(bwd_dkdv_f32_kernel<128>, grid, dim3(kF32Threads), 0, s, (const float*)q,
-                         (const float*)k, (const float*)v, c, lse, (const float*)d_o, delta,
-                         (float*)dk, (float*)dv, dck, L, n_blk, scale, sl2);
-    } else {
-      hipLaunchKernelGGL(bwd_dkdv_f32_kernel<64>, grid, dim3(kF32Threads), 0, s, (const float*)q,
-                         (const float*)k, (const float*)v, c, lse, (const float*)d_o, delta,
-                         (float*)dk, (float*)dv, dck, L, n_blk, scale, sl2);
-    }
+    hipLaunchKernelGGL((bwd_dkdv_f32_kernel<D, FIXED>), grid, dim3(kF32Threads), 0, s,
+                       (const float*)q, (const float*)k, (const float*)v, g.ptr, lse,
+                       (const float*)d_o, delta, (float*)dk, (float*)dv, dck, g.H, L, n_blk,
+                       scale, sl2);
+  }
+}
+
+hipError_t launch_bwd_dkdv(bool bf16_, const void* q, const void* k, const void* v, GateSpec g,
+                           const float* lse, const void* d_o, const float* delta, void* dk,
+                           void* dv, float* dck, int BH, int L, int d, float scale,
+                           hipStream_t s) {
+  if (d == 128) {
+    if (g.fixed) dkdv_t<128, true>(bf16_, q, k, v, g, lse, d_o, delta, dk, dv, dck, BH, L, scale, s);
+    else dkdv_t<128, false>(bf16_, q, k, v, g, lse, d_o, delta, dk, dv, dck, BH, L, scale, s);
+  } else {
+    if (g.fixed) dkdv_t<64, true>(bf16_, q, k, v, g, lse, d_o, delta, dk, dv, dck, BH, L, scale, s);
+    else dkdv_t<64, false>(bf16_, q, k, v, g, lse, d_o, delta, dk, dv, dck, BH, L, scale, s);
   }
   return hipGetLastError();
 }
 
-hipError_t launch_bwd_dq(bool bf16_, const void* q, const void* k, const void* v, const float* c,
-                         const float* lse, const void* d_o, const float* delta, void* dq,
-                         float* dcq, int BH, int L, int d, float scale, hipStream_t s) {
+template <int D, bool FIXED>
+static void dq_t(bool bf16_, const void* q, const void* k, const void* v, GateSpec g,
+                 const float* lse, const void* d_o, const float* delta, void* dq, float* dcq,
+                 int BH, int L, float scale, hipStream_t s) {
   const float sl2 = scale * kLog2e;
   if (bf16_) {
     const int n_mblk = (L + kDqBM - 1) / kDqBM;
     const dim3 grid((unsigned)n_mblk * (unsigned)BH);
-    if (d == 128) {
-      hipLaunchKernelGGL(bwd_dq_bf16_kernel<128>, grid, dim3(kBwdThreads), 0, s, (const bf16*)q,
-                         (const bf16*)k, (const bf16*)v, c, lse, (const bf16*)d_o, delta,
-                         (bf16*)dq, dcq, BH, L, n_mblk, scale, sl2);
-    } else {
-      hipLaunchKernelGGL(bwd_dq_bf16_kernel<64>, grid, dim3(kBwdThreads), 0, s, (const bf16*)q,
-                         (const bf16*)k, (const bf16*)v, c, lse, (const bf16*)d_o, delta,
-                         (bf16*)dq, dcq, BH, L, n_mblk, scale, sl2);
-    }
+    hipLaunchKernelGGL((bwd_dq_bf16_kernel<D, FIXED>), grid, dim3(kBwdThreads), 0, s,
+                       (const bf16*)q, (const bf16*)k, (const bf16*)v, g.ptr, lse,
+                       (const bf16*)d_o, delta, (bf16*)dq, dcq, BH, g.H, L, n_mblk, scale, sl2);
   } else {
-    const int rpw = kF32Threads / (d / 32);
+    const int rpw = kF32Threads / (D / 32);
     const int n_blk = (L + rpw - 1) / rpw;
     const dim3 grid((unsigned)n_blk * (unsigned)BH);
-    if (d == 128) {
-      hipLaunchKernelGGL(bwd_dq_f32_kernel<128>, grid, dim3(kF32Threads), 0, s, (const float*)q,
-                         (const float*)k, (const float*)v, c, lse, (const float*)d_o, delta,
-                         (float*)dq, dcq, L, n_blk, scale, sl2);
-    } else {
-      hipLaunchKernelGGL(bwd_dq_f32_kernel<64>, grid, dim3(kF32Threads), 0, s, (const float*)q,
-                         (const float*)k, (const float*)v, c, lse, (const float*)d_o, delta,
-                         (float*)dq, dcq, L, n_blk, scale, sl2);
-    }
+    hipLaunchKernelGGL((bwd_dq_f32_kernel<D, FIXED>), grid, dim3(kF32Threads), 0, s,
+                       (const float*)q, (const float*)k, (const float*)v, g.ptr, lse,
+                       (const float*)d_o, delta, (float*)dq, dcq, g.H, L, n_blk, scale, sl2);
+  }
+}
+
+hipError_t launch_bwd_dq(bool bf16_, const void* q, const void* k, const void* v, GateSpec g,
+                         const float* lse, const void* d_o, const float* delta, void* dq,
+                         float* dcq, int BH, int L, int d, float scale, hipStream_t s) {
+  if (d == 128) {
+    if (g.fixed) dq_t<128, true>(bf16_, q, k, v, g, lse, d_o, delta, dq, dcq, BH, L, scale, s);
+    else dq_t<128, false>(bf16_, q, k, v, g, lse, d_o, delta, dq, dcq, BH, L, scale, s);
+  } else {
+    if (g.fixed) dq_t<64, true>(bf16_, q, k, v, g, lse, d_o, delta, dq, dcq, BH, L, scale, s);
+    else dq_t<64, false>(bf16_, q, k, v, g, lse, d_o, delta, dq, dcq, BH, L, scale, s);
   }
   return hipGetLastError();
+}
+
+static hipError_t launch_bwd_stages(bool bf16_, const void* q, const void* k, const void* v,
+                                    GateSpec g, const void* o, const float* lse, const void* d_o,
+                                    void* dq, void* dk, void* dv, float* d_log_f, float* ws,
+                                    int BH, int L, int d, float scale, hipStream_t s) {
+  float* delta = ws;
+  float* dcq = delta + (size_t)BH * L;
+  float* dck = dcq + (size_t)BH * L;
+  hipError_t e = launch_bwd_delta(bf16_, o, d_o, delta, BH, L, d, s);
+  if (e == hipSuccess)
+    e = launch_bwd_dkdv(bf16_, q, k, v, g, lse, d_o, delta, dk, dv, dck, BH, L, d, scale, s);
+  if (e == hipSuccess)
+    e = launch_bwd_dq(bf16_, q, k, v, g, lse, d_o, delta, dq, dcq, BH, L, d, scale, s);
+  if (e == hipSuccess) e = launch_reverse_scan_sum(dcq, dck, d_log_f, BH, L, s);
+  return e;
 }
 
 hipError_t launch_bwd(bool bf16_, const void* q, const void* k, const void* v, const float* c,
                       const void* o, const float* lse, const void* d_o, void* dq, void* dk,
                       void* dv, float* d_log_f, void* ws, int BH, int L, int d, float scale,
                       hipStream_t s) {
-  float* delta = static_cast<float*>(ws);
-  float* dcq = delta + (size_t)BH * L;
-  float* dck = dcq + (size_t)BH * L;
-  hipError_t e = launch_bwd_delta(bf16_, o, d_o, delta, BH, L, d, s);
-  if (e == hipSuccess)
-    e = launch_bwd_dkdv(bf16_, q, k, v, c, lse, d_o, delta, dk, dv, dck, BH, L, d, scale, s);
-  if (e == hipSuccess)
-    e = launch_bwd_dq(bf16_, q, k, v, c, lse, d_o, delta, dq, dcq, BH, L, d, scale, s);
-  if (e == hipSuccess) e = launch_reverse_scan_sum(dcq, dck, d_log_f, BH, L, s);
+  return launch_bwd_stages(bf16_, q, k, v, gate_array(c), o, lse, d_o, dq, dk, dv, d_log_f,
+                           static_cast<float*>(ws), BH, L, d, scale, s);
+}
+
+// d b^(h) = sigmoid(-b^(h)) * sum over the rows of head h and all t of d(log f):
+// one workgroup per head, a tree sum over its B rows of length L.
+constexpr int kBiasThreads = 256;
+__global__ __launch_bounds__(kBiasThreads) void fixed_bias_grad_kernel(
+    const float* __restrict__ dlf, const float* __restrict__ bias, float* __restrict__ dbias,
+    int B, int H, int L) {
+  const int h = blockIdx.x;
+  float acc = 0.0f;
+  for (int b = 0; b < B; ++b) {
+    const float* row = dlf + ((size_t)b * H + h) * (size_t)L;
+    for (int t = threadIdx.x; t < L; t += kBiasThreads) acc += row[t];
+  }
+  __shared__ float part[kBiasThreads / 64];
+  for (int off = 32; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float tot = 0.0f;
+    for (int w = 0; w < kBiasThreads / 64; ++w) tot += part[w];
+    dbias[h] = tot / (1.0f + expf(bias[h]));  // times sigmoid(-b)
+  }
+}
+
+size_t bwd_fixed_workspace_bytes(int BH, int L) { return 16 * (size_t)BH * (size_t)L; }
+
+hipError_t launch_bwd_fixed(bool bf16_, const void* q, const void* k, const void* v,
+                            const float* bias, int H, const void* o, const float* lse,
+                            const void* d_o, void* dq, void* dk, void* dv, float* d_bias, void* ws,
+                            int BH, int L, int d, float scale, hipStream_t s) {
+  float* w = static_cast<float*>(ws);
+  float* dlf = w + 3 * (size_t)BH * L;
+  hipError_t e = launch_bwd_stages(bf16_, q, k, v, gate_fixed(bias, H), o, lse, d_o, dq, dk, dv,
+                                   dlf, w, BH, L, d, scale, s);
+  if (e == hipSuccess && d_bias) {
+    hipLaunchKernelGGL(fixed_bias_grad_kernel, dim3(H), dim3(kBiasThreads), 0, s, dlf, bias,
+                       d_bias, BH / H, H, L);
+    e = hipGetLastError();
+  }
   return e;
 }
 

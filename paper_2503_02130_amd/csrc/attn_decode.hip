@@ -53,11 +53,13 @@ struct Vec16<float> {
   static constexpr int N = 4;
 };
 
-template <typename Tt, int D>
+// FIXED: gate = b [H] (fixed gates, c_T - c_j = (T - 1 - j) log sigmoid(b));
+// otherwise gate = the prefix cache [BH, T] and x_new the new token's gate logit.
+template <typename Tt, int D, bool FIXED>
 __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
     const Tt* __restrict__ q, const Tt* __restrict__ kc, const Tt* __restrict__ vc,
-    const float* __restrict__ cc, const float* __restrict__ x_new, float* __restrict__ part,
-    int T, int keys_per_split, int n_split, float scale_log2) {
+    const float* __restrict__ gate, const float* __restrict__ x_new, float* __restrict__ part,
+    int H, int T, int keys_per_split, int n_split, float scale_log2) {
   typedef typename Vec16<Tt>::type VT;
   constexpr int VEC = Vec16<Tt>::N;
   constexpr int LPK = D / VEC;                // lanes per key
@@ -71,7 +73,12 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
   const size_t head = (size_t)bh * (size_t)T;
   const int kbeg = split * keys_per_split;
   const int kend = min(T, kbeg + keys_per_split);
-  const float cT = (T >= 2 ? cc[head + T - 2] : 0.0f) + log_sigmoid(x_new[bh]);
+  float cT = 0.0f, lf = 0.0f;
+  if constexpr (FIXED) {
+    lf = log_sigmoid(gate[bh % H]);
+  } else {
+    cT = (T >= 2 ? gate[head + T - 2] : 0.0f) + log_sigmoid(x_new[bh]);
+  }
 
   float qv[VEC], acc[VEC];
   {
@@ -95,7 +102,8 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
       if (key < kend) {
         kr[u] = __builtin_nontemporal_load(reinterpret_cast<const VT*>(kh + (size_t)key * D));
         vr[u] = __builtin_nontemporal_load(reinterpret_cast<const VT*>(vh + (size_t)key * D));
-        cj[u] = key == T - 1 ? 0.0f : (cc[head + key] - cT) * kLog2e;
+        if constexpr (FIXED) cj[u] = (float)(key - (T - 1)) * lf * kLog2e;
+        else cj[u] = key == T - 1 ? 0.0f : (gate[head + key] - cT) * kLog2e;
       } else {
 #pragma unroll
         for (int e = 0; e < VEC; ++e) {
@@ -176,22 +184,25 @@ __global__ __launch_bounds__(D) void decode_combine_kernel(
   o[(size_t)bh * D + tid] = (Tt)(acc / Ls);
   if (tid == 0) {
     lse[bh] = kLn2 * (M + log2f(Ls));
-    const size_t head = (size_t)bh * (size_t)T;
-    cc[head + T - 1] = (T >= 2 ? cc[head + T - 2] : 0.0f) + log_sigmoid(x_new[bh]);
+    if (cc) {  // append c_T to the prefix cache (data-dependent gates)
+      const size_t head = (size_t)bh * (size_t)T;
+      cc[head + T - 1] = (T >= 2 ? cc[head + T - 2] : 0.0f) + log_sigmoid(x_new[bh]);
+    }
   }
 }
 
-template <typename Tt, int D>
+template <typename Tt, int D, bool FIXED>
 static hipError_t launch_decode_t(const void* q, const void* k_cache, const void* v_cache,
-                                  float* c_cache, const float* logit_new, void* o, float* lse,
-                                  void* ws, int BH, int T, float scale, hipStream_t s) {
+                                  const float* gate, int H, float* c_cache, const float* logit_new,
+                                  void* o, float* lse, void* ws, int BH, int T, float scale,
+                                  hipStream_t s) {
   const int ks = decode_keys_per_split(BH, T);
   const int n_split = (T + ks - 1) / ks;
   float* part = static_cast<float*>(ws);
-  hipLaunchKernelGGL((decode_split_kernel<Tt, D>), dim3((unsigned)n_split * (unsigned)BH),
+  hipLaunchKernelGGL((decode_split_kernel<Tt, D, FIXED>), dim3((unsigned)n_split * (unsigned)BH),
                      dim3(kDecThreads), 0, s,
-                     (const Tt*)q, (const Tt*)k_cache, (const Tt*)v_cache, c_cache, logit_new,
-                     part, T, ks, n_split, scale * kLog2e);
+                     (const Tt*)q, (const Tt*)k_cache, (const Tt*)v_cache, gate, logit_new,
+                     part, H, T, ks, n_split, scale * kLog2e);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((decode_combine_kernel<Tt, D>), dim3(BH), dim3(D), 0, s, part, c_cache,
@@ -199,19 +210,35 @@ static hipError_t launch_decode_t(const void* q, const void* k_cache, const void
   return hipGetLastError();
 }
 
+template <bool FIXED>
+static hipError_t decode_dispatch(bool bf16_, const void* q, const void* k_cache,
+                                  const void* v_cache, const float* gate, int H, float* c_cache,
+                                  const float* logit_new, void* o, float* lse, void* ws, int BH,
+                                  int T, int d, float scale, hipStream_t s) {
+  if (bf16_) {
+    return d == 128 ? launch_decode_t<bf16, 128, FIXED>(q, k_cache, v_cache, gate, H, c_cache,
+                                                        logit_new, o, lse, ws, BH, T, scale, s)
+                    : launch_decode_t<bf16, 64, FIXED>(q, k_cache, v_cache, gate, H, c_cache,
+                                                       logit_new, o, lse, ws, BH, T, scale, s);
+  }
+  return d == 128 ? launch_decode_t<float, 128, FIXED>(q, k_cache, v_cache, gate, H, c_cache,
+                                                       logit_new, o, lse, ws, BH, T, scale, s)
+                  : launch_decode_t<float, 64, FIXED>(q, k_cache, v_cache, gate, H, c_cache,
+                                                      logit_new, o, lse, ws, BH, T, scale, s);
+}
+
 hipError_t launch_decode(bool bf16_, const void* q, const void* k_cache, const void* v_cache,
                          float* c_cache, const float* logit_new, void* o, float* lse, void* ws,
                          int BH, int T, int d, float scale, hipStream_t s) {
-  if (bf16_) {
-    return d == 128 ? launch_decode_t<bf16, 128>(q, k_cache, v_cache, c_cache, logit_new, o, lse,
-                                                 ws, BH, T, scale, s)
-                    : launch_decode_t<bf16, 64>(q, k_cache, v_cache, c_cache, logit_new, o, lse,
-                                                ws, BH, T, scale, s);
-  }
-  return d == 128 ? launch_decode_t<float, 128>(q, k_cache, v_cache, c_cache, logit_new, o, lse,
-                                                ws, BH, T, scale, s)
-                  : launch_decode_t<float, 64>(q, k_cache, v_cache, c_cache, logit_new, o, lse,
-                                               ws, BH, T, scale, s);
+  return decode_dispatch<false>(bf16_, q, k_cache, v_cache, c_cache, 1, c_cache, logit_new, o,
+                                lse, ws, BH, T, d, scale, s);
+}
+
+hipError_t launch_decode_fixed(bool bf16_, const void* q, const void* k_cache, const void* v_cache,
+                               const float* bias, int H, void* o, float* lse, void* ws, int BH,
+                               int T, int d, float scale, hipStream_t s) {
+  return decode_dispatch<true>(bf16_, q, k_cache, v_cache, bias, H, nullptr, nullptr, o, lse, ws,
+                               BH, T, d, scale, s);
 }
 
 }  // namespace fox

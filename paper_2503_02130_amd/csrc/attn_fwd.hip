@@ -64,12 +64,12 @@ struct FwdSmem {
   float c[2][kFwdBN];
 };
 
-template <int D>
+template <int D, bool FIXED>
 __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
-                     const bf16* __restrict__ V, const float* __restrict__ C,
-                     bf16* __restrict__ O, float* __restrict__ LSE, int BH, int L, int n_mblk,
-                     float scale_log2) {
+                     const bf16* __restrict__ V, const float* __restrict__ gate,
+                     bf16* __restrict__ O, float* __restrict__ LSE, int BH, int H, int L,
+                     int n_mblk, float scale_log2) {
   constexpr int TILE = kFwdBN * D;                         // bf16 elements per tile
   constexpr int NDMA = TILE * 2 / 1024 / kFwdWaves;        // 1 KB DMA loads per wave per tile
   __shared__ __attribute__((aligned(16))) FwdSmem<D> sm;
@@ -81,8 +81,7 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
   const int q0 = mblk * kFwdBM;
   const size_t head = (size_t)bh * (size_t)L;
   const bf16* Qh = Q + head * D;
-  const float* Ch = C + head;
-  const float c_ref = Ch[q0];
+  const GateRow<FIXED> gr(gate, bh, H, head);  // c_i - c_j; the reference is c at q0
   const int qw0 = q0 + wave * 32;
   const int qi = qw0 + col;
   const bool q_valid = qi < L;
@@ -131,7 +130,7 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
     }
     if (wave == 0) {
       const int key = kt * kFwdBN + lane;
-      creg = key < L ? (c_ref - Ch[key]) * inv_scale : -INFINITY;
+      creg = key < L ? gr.diff(q0, key) * inv_scale : -INFINITY;
     }
   };
   auto store_c = [&](auto bufc) {
@@ -271,7 +270,7 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
         *reinterpret_cast<bf16x4*>(orow + db * 32 + 8 * g + 4 * h) = w;
       }
     }
-    if (h == 0) LSE[head + qi] = (Ch[qi] - c_ref) + kLn2 * (m_used + log2f(l_tot));
+    if (h == 0) LSE[head + qi] = gr.diff(qi, q0) + kLn2 * (m_used + log2f(l_tot));
   }
 }
 
@@ -281,10 +280,10 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
 constexpr int kF32Threads = 256;
 constexpr int kF32BN = 32;
 
-template <int D>
+template <int D, bool FIXED>
 __global__ __launch_bounds__(kF32Threads) void fwd_f32_kernel(
     const float* __restrict__ Q, const float* __restrict__ K, const float* __restrict__ V,
-    const float* __restrict__ C, float* __restrict__ O, float* __restrict__ LSE, int L,
+    const float* __restrict__ gate, float* __restrict__ O, float* __restrict__ LSE, int H, int L,
     int n_blk, float scale_log2) {
   constexpr int G = D / 32;
   constexpr int RPW = kF32Threads / G;  // query rows per workgroup
@@ -293,13 +292,13 @@ __global__ __launch_bounds__(kF32Threads) void fwd_f32_kernel(
   __shared__ float cks[kF32BN];
   const int tid = threadIdx.x;
   const int sub = tid % G;
-  const size_t head = (size_t)(blockIdx.x / n_blk) * (size_t)L;
+  const int bh = (int)(blockIdx.x / n_blk);
+  const size_t head = (size_t)bh * (size_t)L;
   const int q0 = (int)(blockIdx.x % n_blk) * RPW;
   const int qi = q0 + tid / G;
   const bool q_valid = qi < L;
-  const float* Ch = C + head;
-  const float c_ref = Ch[q0];
-  const float cq = q_valid ? Ch[qi] - c_ref : 0.0f;
+  const GateRow<FIXED> gr(gate, bh, H, head);
+  const float cq = q_valid ? gr.diff(qi, q0) : 0.0f;
   float qv[32], ov[32];
 #pragma unroll
   for (int e = 0; e < 32; ++e) {
@@ -317,7 +316,7 @@ __global__ __launch_bounds__(kF32Threads) void fwd_f32_kernel(
     }
     if (tid < kF32BN) {
       const int key = key0 + tid;
-      cks[tid] = key < L ? Ch[key] - c_ref : INFINITY;
+      cks[tid] = key < L ? gr.diff(key, q0) : INFINITY;
     }
     __syncthreads();
     float sc[kF32BN];
@@ -357,33 +356,48 @@ __global__ __launch_bounds__(kF32Threads) void fwd_f32_kernel(
   }
 }
 
-hipError_t launch_fwd_bf16(const void* q, const void* k, const void* v, const float* c, void* o,
-                           float* lse, int BH, int L, int d, float scale, hipStream_t s) {
+template <int D, bool FIXED>
+static void fwd_bf16_t(const void* q, const void* k, const void* v, GateSpec g, void* o,
+                       float* lse, int BH, int L, float sl2, hipStream_t s) {
   const int n_mblk = (L + kFwdBM - 1) / kFwdBM;
   const dim3 grid((unsigned)n_mblk * (unsigned)BH);
+  hipLaunchKernelGGL((fwd_bf16_kernel<D, FIXED>), grid, dim3(kFwdThreads), 0, s, (const bf16*)q,
+                     (const bf16*)k, (const bf16*)v, g.ptr, (bf16*)o, lse, BH, g.H, L, n_mblk,
+                     sl2);
+}
+
+hipError_t launch_fwd_bf16(const void* q, const void* k, const void* v, GateSpec g, void* o,
+                           float* lse, int BH, int L, int d, float scale, hipStream_t s) {
   const float sl2 = scale * kLog2e;
   if (d == 128) {
-    hipLaunchKernelGGL(fwd_bf16_kernel<128>, grid, dim3(kFwdThreads), 0, s, (const bf16*)q,
-                       (const bf16*)k, (const bf16*)v, c, (bf16*)o, lse, BH, L, n_mblk, sl2);
+    if (g.fixed) fwd_bf16_t<128, true>(q, k, v, g, o, lse, BH, L, sl2, s);
+    else fwd_bf16_t<128, false>(q, k, v, g, o, lse, BH, L, sl2, s);
   } else {
-    hipLaunchKernelGGL(fwd_bf16_kernel<64>, grid, dim3(kFwdThreads), 0, s, (const bf16*)q,
-                       (const bf16*)k, (const bf16*)v, c, (bf16*)o, lse, BH, L, n_mblk, sl2);
+    if (g.fixed) fwd_bf16_t<64, true>(q, k, v, g, o, lse, BH, L, sl2, s);
+    else fwd_bf16_t<64, false>(q, k, v, g, o, lse, BH, L, sl2, s);
   }
   return hipGetLastError();
 }
 
-hipError_t launch_fwd_f32(const float* q, const float* k, const float* v, const float* c, float* o,
-                          float* lse, int BH, int L, int d, float scale, hipStream_t s) {
-  const float sl2 = scale * kLog2e;
-  const int rpw = kF32Threads / (d / 32);
+template <int D, bool FIXED>
+static void fwd_f32_t(const float* q, const float* k, const float* v, GateSpec g, float* o,
+                      float* lse, int BH, int L, float sl2, hipStream_t s) {
+  const int rpw = kF32Threads / (D / 32);
   const int n_blk = (L + rpw - 1) / rpw;
   const dim3 grid((unsigned)n_blk * (unsigned)BH);
+  hipLaunchKernelGGL((fwd_f32_kernel<D, FIXED>), grid, dim3(kF32Threads), 0, s, q, k, v, g.ptr,
+                     o, lse, g.H, L, n_blk, sl2);
+}
+
+hipError_t launch_fwd_f32(const float* q, const float* k, const float* v, GateSpec g, float* o,
+                          float* lse, int BH, int L, int d, float scale, hipStream_t s) {
+  const float sl2 = scale * kLog2e;
   if (d == 128) {
-    hipLaunchKernelGGL(fwd_f32_kernel<128>, grid, dim3(kF32Threads), 0, s, q, k, v, c, o, lse, L,
-                       n_blk, sl2);
+    if (g.fixed) fwd_f32_t<128, true>(q, k, v, g, o, lse, BH, L, sl2, s);
+    else fwd_f32_t<128, false>(q, k, v, g, o, lse, BH, L, sl2, s);
   } else {
-    hipLaunchKernelGGL(fwd_f32_kernel<64>, grid, dim3(kF32Threads), 0, s, q, k, v, c, o, lse, L,
-                       n_blk, sl2);
+    if (g.fixed) fwd_f32_t<64, true>(q, k, v, g, o, lse, BH, L, sl2, s);
+    else fwd_f32_t<64, false>(q, k, v, g, o, lse, BH, L, sl2, s);
   }
   return hipGetLastError();
 }

@@ -2,6 +2,7 @@
 // then kernel launches on the caller's stream.  Nothing here allocates device
 // memory or synchronises.
 #include <hip/hip_runtime.h>
+#include <math.h>
 #include <stdint.h>
 
 #include "fox.h"
@@ -74,9 +75,10 @@ int fox_attn_fwd(int dtype, const void* q, const void* k, const void* v, const f
     return FOX_ERR_ALIGN;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (dtype == FOX_DTYPE_BF16)
-    return launch_status(fox::launch_fwd_bf16(q, k, v, c, o, lse, B * H, L, d, scale, s));
-  return launch_status(fox::launch_fwd_f32((const float*)q, (const float*)k, (const float*)v, c,
-                                           (float*)o, lse, B * H, L, d, scale, s));
+    return launch_status(fox::launch_fwd_bf16(q, k, v, fox::gate_array(c), o, lse, B * H, L, d, scale, s));
+  return launch_status(fox::launch_fwd_f32((const float*)q, (const float*)k, (const float*)v,
+                                           fox::gate_array(c), (float*)o, lse, B * H, L, d, scale,
+                                           s));
 }
 
 size_t fox_attn_bwd_workspace_bytes(int dtype, int B, int H, int L, int d) {
@@ -129,7 +131,7 @@ int fox_attn_bwd_dkdv(int dtype, const void* q, const void* k, const void* v, co
       !aligned16(d_o) || !aligned16(delta) || !aligned16(dk) || !aligned16(dv) ||
       !aligned16(dc_k))
     return FOX_ERR_ALIGN;
-  return launch_status(fox::launch_bwd_dkdv(dtype == FOX_DTYPE_BF16, q, k, v, c, lse, d_o, delta,
+  return launch_status(fox::launch_bwd_dkdv(dtype == FOX_DTYPE_BF16, q, k, v, fox::gate_array(c), lse, d_o, delta,
                                             dk, dv, dc_k, B * H, L, d, scale,
                                             static_cast<hipStream_t>(stream)));
 }
@@ -145,7 +147,7 @@ int fox_attn_bwd_dq(int dtype, const void* q, const void* k, const void* v, cons
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(c) || !aligned16(lse) ||
       !aligned16(d_o) || !aligned16(delta) || !aligned16(dq) || !aligned16(dc_q))
     return FOX_ERR_ALIGN;
-  return launch_status(fox::launch_bwd_dq(dtype == FOX_DTYPE_BF16, q, k, v, c, lse, d_o, delta,
+  return launch_status(fox::launch_bwd_dq(dtype == FOX_DTYPE_BF16, q, k, v, fox::gate_array(c), lse, d_o, delta,
                                           dq, dc_q, B * H, L, d, scale,
                                           static_cast<hipStream_t>(stream)));
 }
@@ -196,6 +198,86 @@ int fox_attn_decode(int dtype, const void* q, const void* k_cache, const void* v
   return launch_status(fox::launch_decode(dtype == FOX_DTYPE_BF16, q, k_cache, v_cache, c_cache,
                                           gate_logit_new, o, lse, workspace, B * H, T, d, scale,
                                           static_cast<hipStream_t>(stream)));
+}
+
+// ---------------------------------------------------------------- fixed gates
+int fox_fixed_gate_init(float* gate_bias, int H, float t_min, float t_max) {
+  if (!gate_bias) return FOX_ERR_NULL;
+  if (H <= 0 || !(t_min > 0.0f) || !(t_max >= t_min) || !isfinite(t_max)) return FOX_ERR_SHAPE;
+  for (int h = 0; h < H; ++h) {
+    const double frac = H > 1 ? (double)h / (double)(H - 1) : 0.0;
+    const double T = exp(log((double)t_min) + (log((double)t_max) - log((double)t_min)) * frac);
+    // sigmoid(b) = exp(-1/T)  <=>  b = log(e^{-1/T} / (1 - e^{-1/T}))
+    gate_bias[h] = (float)(-1.0 / T - log(-expm1(-1.0 / T)));
+  }
+  return FOX_OK;
+}
+
+int fox_attn_fwd_fixed_gate(int dtype, const void* q, const void* k, const void* v,
+                            const float* gate_bias, void* o, float* lse, int B, int H, int L, int d,
+                            float scale, void* stream) {
+  if (!q || !k || !v || !gate_bias || !o || !lse) return FOX_ERR_NULL;
+  int st = check_dims(B, H, L, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(gate_bias) || !aligned16(o) ||
+      !aligned16(lse))
+    return FOX_ERR_ALIGN;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const fox::GateSpec g = fox::gate_fixed(gate_bias, H);
+  if (dtype == FOX_DTYPE_BF16)
+    return launch_status(fox::launch_fwd_bf16(q, k, v, g, o, lse, B * H, L, d, scale, s));
+  return launch_status(fox::launch_fwd_f32((const float*)q, (const float*)k, (const float*)v, g,
+                                           (float*)o, lse, B * H, L, d, scale, s));
+}
+
+size_t fox_attn_bwd_fixed_gate_workspace_bytes(int dtype, int B, int H, int L, int d) {
+  if (check_dims(B, H, L, d) || check_dtype_d(dtype, d)) return 0;
+  return fox::bwd_fixed_workspace_bytes(B * H, L);
+}
+
+int fox_attn_bwd_fixed_gate(int dtype, const void* q, const void* k, const void* v,
+                            const float* gate_bias, const void* o, const float* lse,
+                            const void* d_o, void* dq, void* dk, void* dv, float* d_gate_bias,
+                            void* workspace, size_t workspace_bytes, int B, int H, int L, int d,
+                            float scale, void* stream) {
+  if (!q || !k || !v || !gate_bias || !o || !lse || !d_o || !dq || !dk || !dv)
+    return FOX_ERR_NULL;
+  int st = check_dims(B, H, L, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(gate_bias) || !aligned16(o) ||
+      !aligned16(lse) || !aligned16(d_o) || !aligned16(dq) || !aligned16(dk) || !aligned16(dv) ||
+      (d_gate_bias && !aligned16(d_gate_bias)))
+    return FOX_ERR_ALIGN;
+  if (!workspace || workspace_bytes < fox::bwd_fixed_workspace_bytes(B * H, L))
+    return FOX_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return FOX_ERR_ALIGN;
+  return launch_status(fox::launch_bwd_fixed(dtype == FOX_DTYPE_BF16, q, k, v, gate_bias, H, o,
+                                             lse, d_o, dq, dk, dv, d_gate_bias, workspace, B * H,
+                                             L, d, scale, static_cast<hipStream_t>(stream)));
+}
+
+int fox_attn_decode_fixed_gate(int dtype, const void* q, const void* k_cache,
+                               const void* v_cache, const float* gate_bias, void* o, float* lse,
+                               void* workspace, size_t workspace_bytes, int B, int H, int T, int d,
+                               float scale, void* stream) {
+  if (!q || !k_cache || !v_cache || !gate_bias || !o || !lse) return FOX_ERR_NULL;
+  int st = check_dims(B, H, T, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(gate_bias) ||
+      !aligned16(o) || !aligned16(lse))
+    return FOX_ERR_ALIGN;
+  if (!workspace || workspace_bytes < fox::decode_workspace_bytes(B * H, T, d))
+    return FOX_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return FOX_ERR_ALIGN;
+  return launch_status(fox::launch_decode_fixed(dtype == FOX_DTYPE_BF16, q, k_cache, v_cache,
+                                                gate_bias, H, o, lse, workspace, B * H, T, d, scale,
+                                                static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

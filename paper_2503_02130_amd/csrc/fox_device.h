@@ -95,6 +95,30 @@ __device__ __forceinline__ float log_sigmoid(float x) {
 }
 
 // ---------------------------------------------------------------------------
+// The forget gates of one (batch, head) row, used only through differences of
+// the prefix values, c_i - c_j (0-based positions).  Data-dependent gates pass
+// the array c of fox_gate_prefix; a gate fixed per head, f_t = sigmoid(b)
+// (the ALiBi form of Sec. 3), passes the biases b [H] and gets
+// c_i - c_j = (i - j) log sigmoid(b) straight from the indices.
+// ---------------------------------------------------------------------------
+template <bool FIXED>
+struct GateRow;
+template <>
+struct GateRow<false> {
+  const float* c;
+  __device__ GateRow(const float* gate, int /*bh*/, int /*H*/, size_t row)
+      : c(gate + row) {}
+  __device__ float diff(int i, int j) const { return c[i] - c[j]; }
+};
+template <>
+struct GateRow<true> {
+  float lf;
+  __device__ GateRow(const float* gate, int bh, int H, size_t /*row*/)
+      : lf(log_sigmoid(gate[bh % H])) {}
+  __device__ float diff(int i, int j) const { return (float)(i - j) * lf; }
+};
+
+// ---------------------------------------------------------------------------
 // Global -> LDS without registers (buffer_load ... lds).  One instruction moves
 // 16 bytes per lane: lane l's bytes land at lds_wave_base + 16 * l, whatever
 // global offset the lane asked for, and offsets at or beyond the resource's

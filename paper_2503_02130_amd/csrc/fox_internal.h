@@ -6,6 +6,17 @@
 
 namespace fox {
 
+// The forget gates as the attention kernels see them: the prefix array c
+// [BH, L] (data-dependent gates) or one bias per head, b [H] (fixed gates,
+// f_t = sigmoid(b)); bh % H selects a row's head.
+struct GateSpec {
+  const float* ptr;
+  bool fixed;
+  int H;
+};
+inline GateSpec gate_array(const float* c) { return GateSpec{c, false, 1}; }
+inline GateSpec gate_fixed(const float* bias, int H) { return GateSpec{bias, true, H}; }
+
 // Inclusive prefix sums over rows of length L (one workgroup per row).
 hipError_t launch_gate_prefix(const float* logit, float* log_f, float* c, int rows, int L,
                               hipStream_t s);
@@ -17,30 +28,41 @@ hipError_t launch_reverse_scan_gate(const float* a, const float* b, const float*
                                     float* d_log_f, float* d_logit, int rows, int L,
                                     hipStream_t s);
 
-hipError_t launch_fwd_bf16(const void* q, const void* k, const void* v, const float* c, void* o,
+hipError_t launch_fwd_bf16(const void* q, const void* k, const void* v, GateSpec g, void* o,
                            float* lse, int BH, int L, int d, float scale, hipStream_t s);
-hipError_t launch_fwd_f32(const float* q, const float* k, const float* v, const float* c, float* o,
+hipError_t launch_fwd_f32(const float* q, const float* k, const float* v, GateSpec g, float* o,
                           float* lse, int BH, int L, int d, float scale, hipStream_t s);
 
 // Workspace layout of the backward: delta, dc_q, dc_k, each [BH, L] fp32.
 size_t bwd_workspace_bytes(int BH, int L);
 hipError_t launch_bwd_delta(bool bf16, const void* o, const void* d_o, float* delta, int BH,
                             int L, int d, hipStream_t s);
-hipError_t launch_bwd_dkdv(bool bf16, const void* q, const void* k, const void* v, const float* c,
+hipError_t launch_bwd_dkdv(bool bf16, const void* q, const void* k, const void* v, GateSpec g,
                            const float* lse, const void* d_o, const float* delta, void* dk,
                            void* dv, float* dck, int BH, int L, int d, float scale, hipStream_t s);
-hipError_t launch_bwd_dq(bool bf16, const void* q, const void* k, const void* v, const float* c,
+hipError_t launch_bwd_dq(bool bf16, const void* q, const void* k, const void* v, GateSpec g,
                          const float* lse, const void* d_o, const float* delta, void* dq,
                          float* dcq, int BH, int L, int d, float scale, hipStream_t s);
 hipError_t launch_bwd(bool bf16, const void* q, const void* k, const void* v, const float* c,
                       const void* o, const float* lse, const void* d_o, void* dq, void* dk,
                       void* dv, float* d_log_f, void* ws, int BH, int L, int d, float scale,
                       hipStream_t s);
+// Fixed gates: workspace delta, dc_q, dc_k, d(log f), each [BH, L] fp32; the bias
+// gradient d_bias [H] (may be NULL) = sigmoid(-b) * sum over rows and t of d(log f).
+size_t bwd_fixed_workspace_bytes(int BH, int L);
+hipError_t launch_bwd_fixed(bool bf16, const void* q, const void* k, const void* v,
+                            const float* bias, int H, const void* o, const float* lse,
+                            const void* d_o, void* dq, void* dk, void* dv, float* d_bias, void* ws,
+                            int BH, int L, int d, float scale, hipStream_t s);
 
 int decode_num_splits(int BH, int T);
 size_t decode_workspace_bytes(int BH, int T, int d);
 hipError_t launch_decode(bool bf16, const void* q, const void* k_cache, const void* v_cache,
                          float* c_cache, const float* logit_new, void* o, float* lse, void* ws,
                          int BH, int T, int d, float scale, hipStream_t s);
+// Fixed gates: no prefix cache; bias [H].
+hipError_t launch_decode_fixed(bool bf16, const void* q, const void* k_cache, const void* v_cache,
+                               const float* bias, int H, void* o, float* lse, void* ws, int BH,
+                               int T, int d, float scale, hipStream_t s);
 
 }  // namespace fox

@@ -81,6 +81,38 @@ def test_dlogit_validation(lib):
     assert lib.fox_dlogit_from_dc(c(P16), c(P16), c(P16 + 4), None, c(P16), 1, 1, 4, None) == 4
 
 
+def test_fixed_gate_init_host(lib):
+    """The host-side initialisation: the paper's worked example and argument checks."""
+    import oracle
+    b = fox.fox_fixed_gate_init(4, 2.0, 128.0)
+    assert torch.allclose(b.double(), oracle.fixed_gate_bias_init(4, 2.0, 128.0), atol=1e-6)
+    assert torch.allclose(oracle.time_constant(b.double()),
+                          torch.tensor([2.0, 8.0, 32.0, 128.0], dtype=torch.float64), rtol=1e-5)
+    buf = (ctypes.c_float * 4)()
+    assert lib.fox_fixed_gate_init(None, 4, ctypes.c_float(2), ctypes.c_float(128)) == 1
+    assert lib.fox_fixed_gate_init(buf, 0, ctypes.c_float(2), ctypes.c_float(128)) == 2
+    assert lib.fox_fixed_gate_init(buf, 4, ctypes.c_float(0), ctypes.c_float(128)) == 2
+    assert lib.fox_fixed_gate_init(buf, 4, ctypes.c_float(8), ctypes.c_float(2)) == 2
+
+
+def test_fixed_gate_validation(lib):
+    c = ctypes.c_void_p
+    f = ctypes.c_float(0.1)
+    assert lib.fox_attn_fwd_fixed_gate(1, c(P16), c(P16), c(P16), None, c(P16), c(P16),
+                                       1, 2, 8, 64, f, None) == 1
+    assert lib.fox_attn_fwd_fixed_gate(1, c(P16), c(P16), c(P16), c(P16 + 4), c(P16), c(P16),
+                                       1, 2, 8, 64, f, None) == 4
+    assert lib.fox_attn_fwd_fixed_gate(1, *[c(P16)] * 6, 1, 2, 8, 96, f, None) == 3
+    need = lib.fox_attn_bwd_fixed_gate_workspace_bytes(1, 2, 3, 100, 64)
+    assert need == 4 * 4 * 2 * 3 * 100
+    args = [c(P16)] * 10
+    assert lib.fox_attn_bwd_fixed_gate(1, *args, None, c(P16), need - 1, 2, 3, 100, 64, f,
+                                       None) == 5
+    dneed = lib.fox_attn_decode_workspace_bytes(1, 2, 3, 100, 64)
+    assert lib.fox_attn_decode_fixed_gate(1, *[c(P16)] * 6, c(P16), dneed - 1, 2, 3, 100, 64, f,
+                                          None) == 5
+
+
 def test_bwd_validation_and_workspace(lib):
     c = ctypes.c_void_p
     B, H, L, d = 2, 3, 100, 128

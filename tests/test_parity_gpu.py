@@ -362,3 +362,55 @@ def test_gate_logit_gradient(dtype, d, L):
     ref = oracle.backward_logit(xc["q"], xc["k"], xc["v"], xc["logit"], xc["do"], s)[3]
     check_grad(dtype, "dlogit", dx, ref, f"L={L}")
     assert float(dx[..., 0].abs().max()) <= 1e-3 * max(1.0, float(ref.abs().max()))
+
+
+# ------------------------------------------------------------- fixed gates
+FIXED_CASES = [("f32", 64, 100, 2.0, 128.0), ("bf16", 64, 129, 2.0, 128.0),
+               ("bf16", 128, 700, 2.0, 64.0), ("bf16", 128, 3000, 8.0, 4096.0)]
+
+
+@pytest.mark.parametrize("dtype,d,L,tmin,tmax", FIXED_CASES)
+def test_fixed_gate_forward_backward(dtype, d, L, tmin, tmax):
+    """Fixed gates f = sigmoid(b) (ALiBi form) with the paper's initialisation:
+    O, LSE, dQ, dK, dV and d b against the oracle."""
+    print(f"fixed gate dtype={dtype} d={d} L={L} T=({tmin},{tmax})", flush=True)
+    B, H = 2, 4
+    x = inputs.attn_inputs(B, H, L, d, dtype, ("normal", 2.0, 1.0), 400 + L, device=DEV)
+    b = fox.fox_fixed_gate_init(H, tmin, tmax).to(DEV)
+    s = fox.default_scale(d)
+    o, lse = fox.fox_attn_fwd_fixed_gate(x["q"], x["k"], x["v"], b, s)
+    dq, dk, dv, db = fox.fox_attn_bwd_fixed_gate(x["q"], x["k"], x["v"], b, o, lse, x["do"], s)
+    torch.cuda.synchronize()
+    xc = cpu(x)
+    bc = b.cpu()
+    O, LSE = oracle.forward_fixed_gate(xc["q"], xc["k"], xc["v"], bc, s)
+    check_fwd(dtype, o, lse, O, LSE, f"fixed L={L}")
+    ref = oracle.backward_fixed_gate(xc["q"], xc["k"], xc["v"], bc, xc["do"], s)
+    for name, g, r in zip(("dQ", "dK", "dV"), (dq, dk, dv), ref[:3]):
+        check_grad(dtype, name, g, r, f"fixed L={L}")
+    # d b sums d(log f) over B * L positions: compare against its own scale
+    tol = 1e-4 if dtype == "f32" else 2e-2
+    err = max_abs(db, ref[3]) / max(1e-6, float(ref[3].abs().max()))
+    assert err <= tol, f"fixed L={L} d_bias rel error {err:.3e}"
+    # the same gates through the data-dependent path (constant logits = b)
+    logit = b[None, :, None].expand(B, H, L).contiguous()
+    c = fox.fox_gate_prefix(logit)
+    o2, _ = fox.fox_attn_fwd(x["q"], x["k"], x["v"], c, s)
+    torch.cuda.synchronize()
+    assert rel_l2(o2, o.double()) <= (1e-5 if dtype == "f32" else 1e-2)
+
+
+@pytest.mark.parametrize("dtype,d,T", [("f32", 64, 77), ("bf16", 128, 1), ("bf16", 128, 5000)])
+def test_fixed_gate_decode(dtype, d, T):
+    """Fixed-gate decode equals the last row of the fixed-gate oracle forward."""
+    print(f"fixed gate decode dtype={dtype} d={d} T={T}", flush=True)
+    B, H = 3, 4
+    x = inputs.attn_inputs(B, H, T, d, dtype, ("normal", 2.0, 1.0), 500 + T, device=DEV)
+    b = fox.fox_fixed_gate_init(H, 2.0, 256.0).to(DEV)
+    s = fox.default_scale(d)
+    q_last = x["q"][:, :, T - 1].contiguous()
+    o, lse = fox.fox_attn_decode_fixed_gate(q_last, x["k"], x["v"], b, s)
+    torch.cuda.synchronize()
+    xc = cpu(x)
+    O, LSE = oracle.forward_fixed_gate(xc["q"], xc["k"], xc["v"], b.cpu(), s, rows=[T - 1])
+    check_fwd(dtype, o, lse, O[:, :, 0], LSE[:, :, 0], f"fixed decode T={T}")
