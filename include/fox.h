@@ -180,6 +180,28 @@ int fox_attn_decode(int dtype, const void* q, const void* k_cache, const void* v
                     int B, int H, int T, int d, float scale, void* stream);
 
 /*
+ * Gate-aware exact skipping (the paper's outlook, Sec. 6: forget gates could
+ * prune computation).  D_ij = c_i - c_j <= 0 falls monotonically with the
+ * distance i - j, and s q.k <= s ||q|| ||k||, so a whole block of keys can be
+ * shown to contribute an exact fp32 zero.  Such blocks are not read; the
+ * results are bit for bit those of the entry points without skipping.
+ *
+ * fox_row_norm_max: out[b,h] = max_t ||x[b,h,t,:]||_2 (fp32 [B,H]), enlarged by
+ *   2^-10 relative so that it bounds the exact norm.  x [B,H,L,d] dtype.
+ * fox_attn_decode_skip: fox_attn_decode with k_norm_max [B,H] fp32, an upper
+ *   bound of ||k_j|| over the whole cache (fox_row_norm_max over k_cache, or
+ *   maintained as keys are appended: max(old, ||k_new||)).  A split of keys is
+ *   skipped when all its scores lie more than 160 (base 2) below the new
+ *   token's own score, which makes its merge weight an exact zero.
+ */
+int fox_row_norm_max(int dtype, const void* x, float* out, int B, int H, int L, int d,
+                     void* stream);
+int fox_attn_decode_skip(int dtype, const void* q, const void* k_cache, const void* v_cache,
+                         float* c_cache, const float* gate_logit_new, const float* k_norm_max,
+                         void* o, float* lse, void* workspace, size_t workspace_bytes, int B,
+                         int H, int T, int d, float scale, void* stream);
+
+/*
  * Fixed (data-independent) forget gates: f_t^(h) = sigmoid(b^(h)) for every t
  * (Sec. 3, "Connection to ALiBi": ALiBi with slope -log sigmoid(b^(h))).  The
  * kernels form c_i - c_j = (i - j) log sigmoid(b^(h)) from the positions, so no

@@ -29,6 +29,7 @@ EXPORTED = (
     "fox_attn_decode_workspace_bytes", "fox_attn_decode",
     "fox_fixed_gate_init", "fox_attn_fwd_fixed_gate", "fox_attn_bwd_fixed_gate_workspace_bytes",
     "fox_attn_bwd_fixed_gate", "fox_attn_decode_fixed_gate",
+    "fox_row_norm_max", "fox_attn_decode_skip",
 )
 
 
@@ -89,6 +90,10 @@ def load() -> ctypes.CDLL:
                                             F, P]
     lib.fox_attn_decode_fixed_gate.restype = I
     lib.fox_attn_decode_fixed_gate.argtypes = [I, P, P, P, P, P, P, P, Z, I, I, I, I, F, P]
+    lib.fox_row_norm_max.restype = I
+    lib.fox_row_norm_max.argtypes = [I, P, P, I, I, I, I, P]
+    lib.fox_attn_decode_skip.restype = I
+    lib.fox_attn_decode_skip.argtypes = [I, P, P, P, P, P, P, P, P, P, Z, I, I, I, I, F, P]
     _lib = lib
     return lib
 
@@ -440,4 +445,50 @@ def fox_attn_decode_fixed_gate(q, k_cache, v_cache, gate_bias, scale: Optional[f
                                            workspace.numel() * workspace.element_size(),
                                            B, H, T, d, s, _stream(q))
     _raise(st, "fox_attn_decode_fixed_gate")
+    return o, lse
+
+
+# ------------------------------------------------------- gate-aware skipping
+def fox_row_norm_max(x, out=None):
+    """max_t ||x[b,h,t,:]||_2 per (b, h) as fp32 [B,H] (an upper bound)."""
+    B, H, L, d = x.shape
+    if x.dtype not in _DT:
+        raise ValueError(f"unsupported dtype {x.dtype}")
+    _check(x, "x", (B, H, L, d), x.dtype, None)
+    out = torch.empty((B, H), device=x.device, dtype=torch.float32) if out is None else out
+    _check(out, "out", (B, H), torch.float32, x.device)
+    st = load().fox_row_norm_max(_DT[x.dtype], _ptr(x), _ptr(out), B, H, L, d, _stream(x))
+    _raise(st, "fox_row_norm_max")
+    return out
+
+
+def fox_attn_decode_skip(q, k_cache, v_cache, c_cache, gate_logit_new, k_norm_max,
+                         scale: Optional[float] = None, o=None, lse=None, workspace=None):
+    """fox_attn_decode with exact gate-aware skipping of key splits."""
+    B, H, d = q.shape
+    T = k_cache.shape[2]
+    dt = q.dtype
+    if dt not in _DT:
+        raise ValueError(f"unsupported dtype {dt}")
+    dev = q.device
+    _check(q, "q", (B, H, d), dt, dev)
+    _check(k_cache, "k_cache", (B, H, T, d), dt, dev)
+    _check(v_cache, "v_cache", (B, H, T, d), dt, dev)
+    _check(c_cache, "c_cache", (B, H, T), torch.float32, dev)
+    _check(gate_logit_new, "gate_logit_new", (B, H), torch.float32, dev)
+    _check(k_norm_max, "k_norm_max", (B, H), torch.float32, dev)
+    o = torch.empty_like(q) if o is None else o
+    lse = torch.empty((B, H), device=dev, dtype=torch.float32) if lse is None else lse
+    _check(o, "o", (B, H, d), dt, dev)
+    _check(lse, "lse", (B, H), torch.float32, dev)
+    need = fox_attn_decode_workspace_bytes(dt, B, H, T, d)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), device=dev, dtype=torch.uint8)
+    s = default_scale(d) if scale is None else float(scale)
+    st = load().fox_attn_decode_skip(_DT[dt], _ptr(q), _ptr(k_cache), _ptr(v_cache),
+                                     _ptr(c_cache), _ptr(gate_logit_new), _ptr(k_norm_max),
+                                     _ptr(o), _ptr(lse), _ptr(workspace),
+                                     workspace.numel() * workspace.element_size(),
+                                     B, H, T, d, s, _stream(q))
+    _raise(st, "fox_attn_decode_skip")
     return o, lse

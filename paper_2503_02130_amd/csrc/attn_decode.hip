@@ -10,6 +10,9 @@
 // group of D/8 (bf16) lanes reads one key's row with 16-byte loads so that a
 // wave reads consecutive rows, several keys per lane group are loaded before
 // any is used, and every lane group keeps its own running (max, sum, output).
+// Workgroups are ordered split-major, most recent keys first, so that work is
+// spread over all XCDs also when gate-aware skipping (below) keeps only the
+// recent splits of every sequence.
 // The lane groups of a workgroup merge through LDS into one partial per split;
 // a small second kernel merges the splits (log-sum-exp merge) and appends c_T
 // to the prefix cache.  Entry T-1 of that cache is never read: every workgroup
@@ -21,6 +24,10 @@ namespace fox {
 
 constexpr int kDecThreads = 256;
 constexpr int kDecUnroll = 4;
+// A split is skipped when its scores provably lie this far (base 2) below the
+// new token's own score: 150 makes its merge weight exp2(m_split - M) an exact
+// fp32 zero, and 10 more absorb the rounding of the bound itself.
+constexpr float kSkipMargin = 160.0f;
 
 static int decode_keys_per_split(int BH, int T) {
   // The largest split (fewer partials) that still gives >= 2048 workgroups.
@@ -55,11 +62,15 @@ struct Vec16<float> {
 
 // FIXED: gate = b [H] (fixed gates, c_T - c_j = (T - 1 - j) log sigmoid(b));
 // otherwise gate = the prefix cache [BH, T] and x_new the new token's gate logit.
-template <typename Tt, int D, bool FIXED>
+// SKIP: knorm [BH] bounds the key norms; a split that cannot contribute (its
+// merge weight would be an exact zero) writes an empty partial without reading
+// its keys, which leaves the result bit for bit as without skipping.
+template <typename Tt, int D, bool FIXED, bool SKIP>
 __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
     const Tt* __restrict__ q, const Tt* __restrict__ kc, const Tt* __restrict__ vc,
-    const float* __restrict__ gate, const float* __restrict__ x_new, float* __restrict__ part,
-    int H, int T, int keys_per_split, int n_split, float scale_log2) {
+    const float* __restrict__ gate, const float* __restrict__ x_new,
+    const float* __restrict__ knorm, float* __restrict__ part, int H, int T, int keys_per_split,
+    int n_split, float scale_log2) {
   typedef typename Vec16<Tt>::type VT;
   constexpr int VEC = Vec16<Tt>::N;
   constexpr int LPK = D / VEC;                // lanes per key
@@ -69,7 +80,10 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
 
   const int tid = threadIdx.x;
   const int g = tid / LPK, lp = tid % LPK;
-  const int bh = blockIdx.x / n_split, split = blockIdx.x % n_split;
+  // split-major, most recent split first: the splits that gate-aware skipping
+  // keeps (the recent ones) are spread over all XCDs and dispatched first
+  const int n_bh = (int)(gridDim.x / n_split);
+  const int bh = blockIdx.x % n_bh, split = n_split - 1 - (int)(blockIdx.x / n_bh);
   const size_t head = (size_t)bh * (size_t)T;
   const int kbeg = split * keys_per_split;
   const int kend = min(T, kbeg + keys_per_split);
@@ -92,6 +106,42 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
   float m = -INFINITY, l = 0.0f;
   const Tt* kh = kc + head * D + lp * VEC;
   const Tt* vh = vc + head * D + lp * VEC;
+
+  if constexpr (SKIP) {
+    // Every score of the split is at most ||s log2(e) q|| max||k|| minus the
+    // decay to the split's last key (c decreases along the sequence), while the
+    // merged maximum is at least the new token's own score.  The butterfly sums
+    // below give bitwise the same value in every lane, so the decision is
+    // uniform across the workgroup.
+    float qq = 0.0f, dot = 0.0f;
+    const VT kl = *reinterpret_cast<const VT*>(kh + (size_t)(T - 1) * D);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      qq += qv[e] * qv[e];
+      dot += qv[e] * (float)kl[e];
+    }
+#pragma unroll
+    for (int off = 1; off < LPK; off <<= 1) {
+      qq += __shfl_xor(qq, off);
+      dot += __shfl_xor(dot, off);
+    }
+    const int jl = kend - 1;  // the split's last (least decayed) key
+    float decay = 0.0f;       // (c_jl - c_T) log2(e) >= 0
+    if (jl != T - 1) {
+      if constexpr (FIXED) decay = (float)(jl - (T - 1)) * lf * kLog2e;
+      else decay = (gate[head + jl] - cT) * kLog2e;
+    }
+    const float bound = sqrtf(qq) * knorm[bh] - decay;
+    if (bound < dot - kSkipMargin) {
+      float* out = part + ((size_t)bh * n_split + split) * (D + 2);
+      for (int dd = tid; dd < D; dd += kDecThreads) out[2 + dd] = 0.0f;
+      if (tid == 0) {
+        out[0] = -INFINITY;
+        out[1] = 0.0f;
+      }
+      return;
+    }
+  }
 
   for (int base = kbeg; base < kend; base += KPI * kDecUnroll) {
     VT kr[kDecUnroll], vr[kDecUnroll];
@@ -191,17 +241,17 @@ __global__ __launch_bounds__(D) void decode_combine_kernel(
   }
 }
 
-template <typename Tt, int D, bool FIXED>
+template <typename Tt, int D, bool FIXED, bool SKIP>
 static hipError_t launch_decode_t(const void* q, const void* k_cache, const void* v_cache,
                                   const float* gate, int H, float* c_cache, const float* logit_new,
-                                  void* o, float* lse, void* ws, int BH, int T, float scale,
-                                  hipStream_t s) {
+                                  const float* knorm, void* o, float* lse, void* ws, int BH, int T,
+                                  float scale, hipStream_t s) {
   const int ks = decode_keys_per_split(BH, T);
   const int n_split = (T + ks - 1) / ks;
   float* part = static_cast<float*>(ws);
-  hipLaunchKernelGGL((decode_split_kernel<Tt, D, FIXED>), dim3((unsigned)n_split * (unsigned)BH),
-                     dim3(kDecThreads), 0, s,
-                     (const Tt*)q, (const Tt*)k_cache, (const Tt*)v_cache, gate, logit_new,
+  hipLaunchKernelGGL((decode_split_kernel<Tt, D, FIXED, SKIP>),
+                     dim3((unsigned)n_split * (unsigned)BH), dim3(kDecThreads), 0, s,
+                     (const Tt*)q, (const Tt*)k_cache, (const Tt*)v_cache, gate, logit_new, knorm,
                      part, H, T, ks, n_split, scale * kLog2e);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -210,35 +260,47 @@ static hipError_t launch_decode_t(const void* q, const void* k_cache, const void
   return hipGetLastError();
 }
 
-template <bool FIXED>
+template <bool FIXED, bool SKIP>
 static hipError_t decode_dispatch(bool bf16_, const void* q, const void* k_cache,
                                   const void* v_cache, const float* gate, int H, float* c_cache,
-                                  const float* logit_new, void* o, float* lse, void* ws, int BH,
-                                  int T, int d, float scale, hipStream_t s) {
+                                  const float* logit_new, const float* knorm, void* o, float* lse,
+                                  void* ws, int BH, int T, int d, float scale, hipStream_t s) {
   if (bf16_) {
-    return d == 128 ? launch_decode_t<bf16, 128, FIXED>(q, k_cache, v_cache, gate, H, c_cache,
-                                                        logit_new, o, lse, ws, BH, T, scale, s)
-                    : launch_decode_t<bf16, 64, FIXED>(q, k_cache, v_cache, gate, H, c_cache,
-                                                       logit_new, o, lse, ws, BH, T, scale, s);
+    return d == 128 ? launch_decode_t<bf16, 128, FIXED, SKIP>(q, k_cache, v_cache, gate, H,
+                                                              c_cache, logit_new, knorm, o, lse,
+                                                              ws, BH, T, scale, s)
+                    : launch_decode_t<bf16, 64, FIXED, SKIP>(q, k_cache, v_cache, gate, H,
+                                                             c_cache, logit_new, knorm, o, lse,
+                                                             ws, BH, T, scale, s);
   }
-  return d == 128 ? launch_decode_t<float, 128, FIXED>(q, k_cache, v_cache, gate, H, c_cache,
-                                                       logit_new, o, lse, ws, BH, T, scale, s)
-                  : launch_decode_t<float, 64, FIXED>(q, k_cache, v_cache, gate, H, c_cache,
-                                                      logit_new, o, lse, ws, BH, T, scale, s);
+  return d == 128 ? launch_decode_t<float, 128, FIXED, SKIP>(q, k_cache, v_cache, gate, H,
+                                                             c_cache, logit_new, knorm, o, lse,
+                                                             ws, BH, T, scale, s)
+                  : launch_decode_t<float, 64, FIXED, SKIP>(q, k_cache, v_cache, gate, H,
+                                                            c_cache, logit_new, knorm, o, lse,
+                                                            ws, BH, T, scale, s);
 }
 
 hipError_t launch_decode(bool bf16_, const void* q, const void* k_cache, const void* v_cache,
                          float* c_cache, const float* logit_new, void* o, float* lse, void* ws,
                          int BH, int T, int d, float scale, hipStream_t s) {
-  return decode_dispatch<false>(bf16_, q, k_cache, v_cache, c_cache, 1, c_cache, logit_new, o,
-                                lse, ws, BH, T, d, scale, s);
+  return decode_dispatch<false, false>(bf16_, q, k_cache, v_cache, c_cache, 1, c_cache, logit_new,
+                                       nullptr, o, lse, ws, BH, T, d, scale, s);
+}
+
+hipError_t launch_decode_skip(bool bf16_, const void* q, const void* k_cache, const void* v_cache,
+                              float* c_cache, const float* logit_new, const float* k_norm_max,
+                              void* o, float* lse, void* ws, int BH, int T, int d, float scale,
+                              hipStream_t s) {
+  return decode_dispatch<false, true>(bf16_, q, k_cache, v_cache, c_cache, 1, c_cache, logit_new,
+                                      k_norm_max, o, lse, ws, BH, T, d, scale, s);
 }
 
 hipError_t launch_decode_fixed(bool bf16_, const void* q, const void* k_cache, const void* v_cache,
                                const float* bias, int H, void* o, float* lse, void* ws, int BH,
                                int T, int d, float scale, hipStream_t s) {
-  return decode_dispatch<true>(bf16_, q, k_cache, v_cache, bias, H, nullptr, nullptr, o, lse, ws,
-                               BH, T, d, scale, s);
+  return decode_dispatch<true, false>(bf16_, q, k_cache, v_cache, bias, H, nullptr, nullptr,
+                                      nullptr, o, lse, ws, BH, T, d, scale, s);
 }
 
 }  // namespace fox

@@ -200,6 +200,41 @@ int fox_attn_decode(int dtype, const void* q, const void* k_cache, const void* v
                                           static_cast<hipStream_t>(stream)));
 }
 
+// ------------------------------------------------------- gate-aware skipping
+int fox_row_norm_max(int dtype, const void* x, float* out, int B, int H, int L, int d,
+                     void* stream) {
+  if (!x || !out) return FOX_ERR_NULL;
+  int st = check_dims(B, H, L, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (!aligned16(x) || !aligned16(out)) return FOX_ERR_ALIGN;
+  return launch_status(fox::launch_row_norm_max(dtype == FOX_DTYPE_BF16, x, out, B * H, L, d,
+                                                static_cast<hipStream_t>(stream)));
+}
+
+int fox_attn_decode_skip(int dtype, const void* q, const void* k_cache, const void* v_cache,
+                         float* c_cache, const float* gate_logit_new, const float* k_norm_max,
+                         void* o, float* lse, void* workspace, size_t workspace_bytes, int B,
+                         int H, int T, int d, float scale, void* stream) {
+  if (!q || !k_cache || !v_cache || !c_cache || !gate_logit_new || !k_norm_max || !o || !lse)
+    return FOX_ERR_NULL;
+  int st = check_dims(B, H, T, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(c_cache) ||
+      !aligned16(gate_logit_new) || !aligned16(k_norm_max) || !aligned16(o) || !aligned16(lse))
+    return FOX_ERR_ALIGN;
+  if (!workspace || workspace_bytes < fox::decode_workspace_bytes(B * H, T, d))
+    return FOX_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return FOX_ERR_ALIGN;
+  return launch_status(fox::launch_decode_skip(dtype == FOX_DTYPE_BF16, q, k_cache, v_cache,
+                                               c_cache, gate_logit_new, k_norm_max, o, lse,
+                                               workspace, B * H, T, d, scale,
+                                               static_cast<hipStream_t>(stream)));
+}
+
 // ---------------------------------------------------------------- fixed gates
 int fox_fixed_gate_init(float* gate_bias, int H, float t_min, float t_max) {
   if (!gate_bias) return FOX_ERR_NULL;

@@ -55,11 +55,22 @@ hipError_t launch_bwd_fixed(bool bf16, const void* q, const void* k, const void*
                             const void* d_o, void* dq, void* dk, void* dv, float* d_bias, void* ws,
                             int BH, int L, int d, float scale, hipStream_t s);
 
+// out[bh] = max_t ||x[bh, t, :]||_2, enlarged by 2^-10 relative (an upper bound).
+hipError_t launch_row_norm_max(bool bf16, const void* x, float* out, int BH, int L, int d,
+                               hipStream_t s);
+
 int decode_num_splits(int BH, int T);
 size_t decode_workspace_bytes(int BH, int T, int d);
 hipError_t launch_decode(bool bf16, const void* q, const void* k_cache, const void* v_cache,
                          float* c_cache, const float* logit_new, void* o, float* lse, void* ws,
                          int BH, int T, int d, float scale, hipStream_t s);
+// Exact gate-aware skipping (k_norm_max [BH] from launch_row_norm_max over the
+// whole cache): a split whose every score lies more than 160 (base 2) below the
+// new token's own score is not read; its merge weight would underflow to 0.
+hipError_t launch_decode_skip(bool bf16, const void* q, const void* k_cache, const void* v_cache,
+                              float* c_cache, const float* logit_new, const float* k_norm_max,
+                              void* o, float* lse, void* ws, int BH, int T, int d, float scale,
+                              hipStream_t s);
 // Fixed gates: no prefix cache; bias [H].
 hipError_t launch_decode_fixed(bool bf16, const void* q, const void* k_cache, const void* v_cache,
                                const float* bias, int H, void* o, float* lse, void* ws, int BH,

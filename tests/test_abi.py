@@ -113,6 +113,20 @@ def test_fixed_gate_validation(lib):
                                           None) == 5
 
 
+def test_skip_validation(lib):
+    c = ctypes.c_void_p
+    f = ctypes.c_float(0.1)
+    assert lib.fox_row_norm_max(1, None, c(P16), 1, 2, 8, 64, None) == 1
+    assert lib.fox_row_norm_max(1, c(P16), c(P16 + 4), 1, 2, 8, 64, None) == 4
+    assert lib.fox_row_norm_max(1, c(P16), c(P16), 1, 2, 8, 80, None) == 3
+    need = lib.fox_attn_decode_workspace_bytes(1, 2, 3, 100, 64)
+    args = [c(P16)] * 9
+    assert lib.fox_attn_decode_skip(1, *args[:6], None, c(P16), c(P16), need, 2, 3, 100, 64, f,
+                                    None) == 1
+    assert lib.fox_attn_decode_skip(1, *args, need - 1, 2, 3, 100, 64, f, None) == 5
+    assert lib.fox_attn_decode_skip(1, *args, need, 2, 3, 0, 64, f, None) == 2
+
+
 def test_bwd_validation_and_workspace(lib):
     c = ctypes.c_void_p
     B, H, L, d = 2, 3, 100, 128

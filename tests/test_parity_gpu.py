@@ -414,3 +414,42 @@ def test_fixed_gate_decode(dtype, d, T):
     xc = cpu(x)
     O, LSE = oracle.forward_fixed_gate(xc["q"], xc["k"], xc["v"], b.cpu(), s, rows=[T - 1])
     check_fwd(dtype, o, lse, O[:, :, 0], LSE[:, :, 0], f"fixed decode T={T}")
+
+
+# ------------------------------------------------------ gate-aware skipping
+@pytest.mark.parametrize("dtype,d,L", [("bf16", 128, 1), ("bf16", 64, 3000), ("f32", 128, 1000)])
+def test_row_norm_max(dtype, d, L):
+    x = inputs.attn_inputs(2, 3, L, d, dtype, ("normal", 0.0, 1.0), 600 + L, device=DEV)["k"]
+    got = fox.fox_row_norm_max(x)
+    torch.cuda.synchronize()
+    ref = torch.linalg.vector_norm(x.double().cpu(), dim=-1).amax(dim=-1)
+    g = got.double().cpu()
+    assert torch.all(g >= ref) and torch.all(g <= ref * (1 + 2e-3))
+
+
+DECODE_SKIP_CASES = [
+    # (dtype, d, B, H, T, gate (kind, mean, std)): strong gates skip almost all
+    # splits, weak gates none, the workload's N(3, 1) the distant past only
+    ("bf16", 128, 2, 4, 20000, ("normal", 3.0, 1.0)),
+    ("bf16", 128, 2, 2, 9000, ("normal", -2.0, 1.0)),
+    ("bf16", 64, 3, 2, 5000, ("normal", 12.0, 1.0)),
+    ("f32", 64, 2, 2, 7777, ("normal", 1.0, 1.0)),
+    ("bf16", 128, 1, 1, 1, ("normal", 3.0, 1.0)),
+]
+
+
+@pytest.mark.parametrize("dtype,d,B,H,T,gate", DECODE_SKIP_CASES)
+def test_decode_skip_is_bitwise_dense(dtype, d, B, H, T, gate):
+    """Skipping only drops splits whose merge weight is an exact zero, so o, lse
+    and the appended c_T equal the dense decode's bit for bit."""
+    print(f"decode skip dtype={dtype} d={d} B={B} H={H} T={T} gate={gate}", flush=True)
+    y = inputs.decode_inputs(B, H, T, d, dtype, gate, 700 + T, device=DEV)
+    cc = torch.zeros((B, H, T), device=DEV)
+    if T > 1:
+        cc[..., : T - 1] = fox.fox_gate_prefix(y["cached_logit"])
+    cc2 = cc.clone()
+    kn = fox.fox_row_norm_max(y["k_cache"])
+    o1, l1 = fox.fox_attn_decode(y["q"], y["k_cache"], y["v_cache"], cc, y["logit_new"])
+    o2, l2 = fox.fox_attn_decode_skip(y["q"], y["k_cache"], y["v_cache"], cc2, y["logit_new"], kn)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2) and torch.equal(cc, cc2)
