@@ -148,8 +148,36 @@ def bench_train(w, steps, warmup):
     ms = start.elapsed_time(end) / steps
     if not (torch.isfinite(o.float()).all() and torch.isfinite(dlf).all()):
         raise RuntimeError("non-finite outputs")
+
+    # The same step with exact gate-aware skipping (row-norm bounds computed
+    # inside the timed step); its outputs must equal the dense step's bit for bit.
+    ref = [t.clone() for t in (o, lse, dq, dk, dv, dlf)]
+    qn = torch.empty((B, H), device=dev)
+    kn = torch.empty((B, H), device=dev)
+    ws = torch.empty(fox.fox_attn_bwd_workspace_bytes(x["q"].dtype, B, H, L, d), device=dev,
+                     dtype=torch.uint8)
+
+    def step_skip():
+        fox.fox_gate_prefix(x["logit"], c=c)
+        fox.fox_row_norm_max(x["q"], out=qn)
+        fox.fox_row_norm_max(x["k"], out=kn)
+        fox.fox_attn_fwd_skip(x["q"], x["k"], x["v"], c, qn, kn, s, o=o, lse=lse)
+        fox.fox_attn_bwd_skip(x["q"], x["k"], x["v"], c, o, lse, x["do"], qn, kn, s, dq=dq, dk=dk,
+                              dv=dv, d_log_f=dlf, workspace=ws)
+
+    for _ in range(warmup):
+        step_skip()
+    torch.cuda.synchronize()
+    t_skip = EventTimer()
+    for _ in range(steps):
+        with t_skip:
+            step_skip()
+    torch.cuda.synchronize()
+    if not all(torch.equal(a, b) for a, b in zip(ref, (o, lse, dq, dk, dv, dlf))):
+        raise RuntimeError("the skipping step differs from the dense step")
     return {"ms": ms, "wall_ms": wall_ms, "gate_ms": t_gate.mean_ms(), "fwd_ms": t_fwd.mean_ms(),
-            "bwd_ms": t_bwd.mean_ms(), "dkdv_ms": t_dkdv.mean_ms(), "dq_ms": t_dq.mean_ms()}
+            "bwd_ms": t_bwd.mean_ms(), "dkdv_ms": t_dkdv.mean_ms(), "dq_ms": t_dq.mean_ms(),
+            "skip_ms": t_skip.mean_ms()}
 
 
 def bench_decode(w, steps, warmup):
@@ -368,6 +396,13 @@ def main():
                      "unit": "TFLOP/s", "frac": round(kv_tf / MFMA_BF16_PEAK_TFLOPS, 4),
                      "traffic": kv_traffic, "algorithmic_flops_per_launch": fl_kv,
                      "compulsory_bytes_per_launch": kv_bytes},
+        "skip": {"what": "the same step through fox_attn_fwd_skip / fox_attn_bwd_skip (exact "
+                         "gate-aware tile skipping, bound kernels included); outputs bitwise "
+                         "equal to the dense step",
+                 "ms_per_step": round(r["skip_ms"], 4),
+                 "speedup_vs_dense": round(r["ms"] / r["skip_ms"], 3),
+                 "dense_equivalent_TFLOP/s": round((fl_f + fl_b) / (r["skip_ms"] * 1e-3) / 1e12,
+                                                   2)},
         "roofline_fwd": {"bound": "mfma", "kernel": "fwd_bf16_kernel<128> (fox_attn_fwd)",
                          "achieved": round(fwd_tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
                          "unit": "TFLOP/s", "frac": round(fwd_tf / MFMA_BF16_PEAK_TFLOPS, 4)},
@@ -375,7 +410,8 @@ def main():
                          "achieved": round(bwd_tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
                          "unit": "TFLOP/s", "frac": round(bwd_tf / MFMA_BF16_PEAK_TFLOPS, 4)},
     }
-    log(f"[bench] train step {r['ms']:.3f} ms -> {tflops:.1f} TFLOP/s")
+    log(f"[bench] train step {r['ms']:.3f} ms -> {tflops:.1f} TFLOP/s; with skipping "
+        f"{r['skip_ms']:.3f} ms")
     if not args.no_decode:
         wd = inputs.WORKLOADS[args.decode_workload]
         rd = bench_decode(wd, max(args.steps, 10), args.warmup)

@@ -194,8 +194,24 @@ int fox_attn_decode(int dtype, const void* q, const void* k_cache, const void* v
  *   skipped when all its scores lie more than 160 (base 2) below the new
  *   token's own score, which makes its merge weight an exact zero.
  */
+/*
+ * fox_attn_fwd_skip / fox_attn_bwd_skip: fox_attn_fwd / fox_attn_bwd with
+ *   q_norm_max, k_norm_max [B,H] fp32 (fox_row_norm_max of q and k).  With
+ *   Qmax, Kmax the bounds, P_ij < exp(2 s Qmax Kmax + c_i - c_j) relative to the
+ *   row maximum (forward) or exp(-LSE_i) (backward), so a tile pair whose
+ *   closest query/key pair puts this below 2^-160 is skipped.  bf16 only; the
+ *   fp32 path runs dense.  Workspace as fox_attn_bwd.
+ */
 int fox_row_norm_max(int dtype, const void* x, float* out, int B, int H, int L, int d,
                      void* stream);
+int fox_attn_fwd_skip(int dtype, const void* q, const void* k, const void* v, const float* c,
+                      const float* q_norm_max, const float* k_norm_max, void* o, float* lse,
+                      int B, int H, int L, int d, float scale, void* stream);
+int fox_attn_bwd_skip(int dtype, const void* q, const void* k, const void* v, const float* c,
+                      const void* o, const float* lse, const void* d_o, const float* q_norm_max,
+                      const float* k_norm_max, void* dq, void* dk, void* dv, float* d_log_f,
+                      void* workspace, size_t workspace_bytes, int B, int H, int L, int d,
+                      float scale, void* stream);
 int fox_attn_decode_skip(int dtype, const void* q, const void* k_cache, const void* v_cache,
                          float* c_cache, const float* gate_logit_new, const float* k_norm_max,
                          void* o, float* lse, void* workspace, size_t workspace_bytes, int B,

@@ -12,7 +12,8 @@ from ._lib import (  # noqa: F401
     fox_dlogit_from_dc, fox_attn_decode,
     fox_fixed_gate_init, fox_attn_fwd_fixed_gate, fox_attn_bwd_fixed_gate,
     fox_attn_bwd_fixed_gate_workspace_bytes, fox_attn_decode_fixed_gate,
-    fox_attn_decode_workspace_bytes, fox_row_norm_max, fox_attn_decode_skip, LIB_PATH,
+    fox_attn_decode_workspace_bytes, fox_row_norm_max, fox_attn_decode_skip,
+    fox_attn_fwd_skip, fox_attn_bwd_skip, LIB_PATH,
     EXPORTED,
 )
 
@@ -24,5 +25,5 @@ __all__ = [
     "fox_attn_bwd_fixed_gate", "fox_attn_bwd_fixed_gate_workspace_bytes",
     "fox_attn_decode_fixed_gate",
     "fox_attn_decode", "fox_attn_decode_workspace_bytes", "fox_row_norm_max",
-    "fox_attn_decode_skip",
+    "fox_attn_decode_skip", "fox_attn_fwd_skip", "fox_attn_bwd_skip",
 ]

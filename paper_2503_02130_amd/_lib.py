@@ -29,7 +29,7 @@ EXPORTED = (
     "fox_attn_decode_workspace_bytes", "fox_attn_decode",
     "fox_fixed_gate_init", "fox_attn_fwd_fixed_gate", "fox_attn_bwd_fixed_gate_workspace_bytes",
     "fox_attn_bwd_fixed_gate", "fox_attn_decode_fixed_gate",
-    "fox_row_norm_max", "fox_attn_decode_skip",
+    "fox_row_norm_max", "fox_attn_decode_skip", "fox_attn_fwd_skip", "fox_attn_bwd_skip",
 )
 
 
@@ -92,6 +92,11 @@ def load() -> ctypes.CDLL:
     lib.fox_attn_decode_fixed_gate.argtypes = [I, P, P, P, P, P, P, P, Z, I, I, I, I, F, P]
     lib.fox_row_norm_max.restype = I
     lib.fox_row_norm_max.argtypes = [I, P, P, I, I, I, I, P]
+    lib.fox_attn_fwd_skip.restype = I
+    lib.fox_attn_fwd_skip.argtypes = [I, P, P, P, P, P, P, P, P, I, I, I, I, F, P]
+    lib.fox_attn_bwd_skip.restype = I
+    lib.fox_attn_bwd_skip.argtypes = [I, P, P, P, P, P, P, P, P, P, P, P, P, P, P, Z, I, I, I, I,
+                                      F, P]
     lib.fox_attn_decode_skip.restype = I
     lib.fox_attn_decode_skip.argtypes = [I, P, P, P, P, P, P, P, P, P, Z, I, I, I, I, F, P]
     _lib = lib
@@ -492,3 +497,62 @@ def fox_attn_decode_skip(q, k_cache, v_cache, c_cache, gate_logit_new, k_norm_ma
                                      B, H, T, d, s, _stream(q))
     _raise(st, "fox_attn_decode_skip")
     return o, lse
+
+
+def fox_attn_fwd_skip(q, k, v, c, q_norm_max, k_norm_max, scale: Optional[float] = None,
+                      o=None, lse=None):
+    """fox_attn_fwd with exact gate-aware skipping of key tiles (bitwise equal)."""
+    B, H, L, d = q.shape
+    dt = q.dtype
+    if dt not in _DT:
+        raise ValueError(f"unsupported dtype {dt}")
+    dev = q.device
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _check(t, name, (B, H, L, d), dt, dev)
+    _check(c, "c", (B, H, L), torch.float32, dev)
+    _check(q_norm_max, "q_norm_max", (B, H), torch.float32, dev)
+    _check(k_norm_max, "k_norm_max", (B, H), torch.float32, dev)
+    o = torch.empty_like(q) if o is None else o
+    lse = torch.empty((B, H, L), device=dev, dtype=torch.float32) if lse is None else lse
+    _check(o, "o", (B, H, L, d), dt, dev)
+    _check(lse, "lse", (B, H, L), torch.float32, dev)
+    s = default_scale(d) if scale is None else float(scale)
+    st = load().fox_attn_fwd_skip(_DT[dt], _ptr(q), _ptr(k), _ptr(v), _ptr(c), _ptr(q_norm_max),
+                                  _ptr(k_norm_max), _ptr(o), _ptr(lse), B, H, L, d, s, _stream(q))
+    _raise(st, "fox_attn_fwd_skip")
+    return o, lse
+
+
+def fox_attn_bwd_skip(q, k, v, c, o, lse, d_o, q_norm_max, k_norm_max,
+                      scale: Optional[float] = None, dq=None, dk=None, dv=None, d_log_f=None,
+                      workspace=None):
+    """fox_attn_bwd with exact gate-aware skipping of tile pairs (bitwise equal)."""
+    B, H, L, d = q.shape
+    dt = q.dtype
+    if dt not in _DT:
+        raise ValueError(f"unsupported dtype {dt}")
+    dev = q.device
+    for name, t in (("q", q), ("k", k), ("v", v), ("o", o), ("d_o", d_o)):
+        _check(t, name, (B, H, L, d), dt, dev)
+    _check(c, "c", (B, H, L), torch.float32, dev)
+    _check(lse, "lse", (B, H, L), torch.float32, dev)
+    _check(q_norm_max, "q_norm_max", (B, H), torch.float32, dev)
+    _check(k_norm_max, "k_norm_max", (B, H), torch.float32, dev)
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(k) if dk is None else dk
+    dv = torch.empty_like(v) if dv is None else dv
+    d_log_f = torch.empty_like(c) if d_log_f is None else d_log_f
+    for name, t in (("dq", dq), ("dk", dk), ("dv", dv)):
+        _check(t, name, (B, H, L, d), dt, dev)
+    _check(d_log_f, "d_log_f", (B, H, L), torch.float32, dev)
+    need = fox_attn_bwd_workspace_bytes(dt, B, H, L, d)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), device=dev, dtype=torch.uint8)
+    s = default_scale(d) if scale is None else float(scale)
+    st = load().fox_attn_bwd_skip(_DT[dt], _ptr(q), _ptr(k), _ptr(v), _ptr(c), _ptr(o), _ptr(lse),
+                                  _ptr(d_o), _ptr(q_norm_max), _ptr(k_norm_max), _ptr(dq),
+                                  _ptr(dk), _ptr(dv), _ptr(d_log_f), _ptr(workspace),
+                                  workspace.numel() * workspace.element_size(),
+                                  B, H, L, d, s, _stream(q))
+    _raise(st, "fox_attn_bwd_skip")
+    return dq, dk, dv, d_log_f

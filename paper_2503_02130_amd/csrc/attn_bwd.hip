@@ -68,6 +68,14 @@ constexpr int kDqBN = 64;
 // ((c_i - c_ref) - LSE_i) / s seeds the S accumulator, the key's part
 // (c_j - c_ref) log2(e) is subtracted in the exponent.
 constexpr int kRefBlock = 128;
+// Gate-aware skipping: with Qmax, Kmax bounding the row norms, every
+// P_ij = exp(s q_i.k_j + c_i - c_j - LSE_i) is below exp(2 s Qmax Kmax + c_i - c_j)
+// (LSE_i >= s q_i.k_i >= -s Qmax Kmax).  A (query tile, key tile) pair whose
+// closest query and key give log2 of that bound below -kSkipMargin produces an
+// exact fp32 zero everywhere (150 for the underflow, 10 for the rounding of the
+// bound), and since c falls along the sequence so do all pairs further apart:
+// the tile loops stop there, bit for bit as without skipping.
+constexpr float kSkipMargin = 160.0f;
 static_assert(kRefBlock % kDqBN == 0, "a dq key tile lies in one reference block");
 
 template <int D>
@@ -76,12 +84,14 @@ struct DqSmem {
   bf16 v[2][kDqBN * D];
   float c[2][kDqBN];
   float cref[2];  // the tile's reference prefix value
+  int skip[2];    // the tile and every earlier one contribute exact zeros
 };
 
-template <int D, bool FIXED>
+template <int D, bool FIXED, bool SKIP>
 __global__ __launch_bounds__(kBwdThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
                         const bf16* __restrict__ V, const float* __restrict__ gate,
+                        const float* __restrict__ qnorm, const float* __restrict__ knorm,
                         const float* __restrict__ LSE, const bf16* __restrict__ dO,
                         const float* __restrict__ delta, bf16* __restrict__ dQ,
                         float* __restrict__ dcq, int BH, int H, int L, int n_mblk, float scale,
@@ -92,8 +102,10 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = lane >> 5, col = lane & 31;
-  const int bh = blockIdx.x % BH;
-  const int mblk = n_mblk - 1 - (int)(blockIdx.x / BH);
+  // heads fastest; rotated over the XCDs when skipping (see the forward kernel)
+  const int row = (int)(blockIdx.x / BH);
+  const int bh = SKIP ? (int)((blockIdx.x + row) % BH) : (int)(blockIdx.x % BH);
+  const int mblk = n_mblk - 1 - row;
   const int q0 = mblk * kDqBM;
   const size_t head = (size_t)bh * (size_t)L;
   const GateRow<FIXED> gr(gate, bh, H, head);
@@ -141,7 +153,9 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
   const int t_diag = qw0 / kDqBN;
 
   const float inv_scale = 1.0f / scale;
+  const float skip_norm = SKIP ? 2.0f * scale * qnorm[bh] * knorm[bh] : 0.0f;
   float creg = 0.0f, crefreg = 0.0f;
+  bool skipreg = false;
   auto issue_tile = [&](int kt, auto bufc) {
     constexpr int B = decltype(bufc)::value;
     const uint32_t base = (uint32_t)kt * kDqBN * D * 2;
@@ -156,6 +170,11 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
       const int kref = kt * kDqBN / kRefBlock * kRefBlock;
       if constexpr (!FIXED) crefreg = gr.c[kref];
       creg = key < L ? gr.diff(key, kref) * kLog2e : INFINITY;
+      if constexpr (SKIP) {
+        // the tile's last key against the block's first query
+        if (lane == kDqBN - 1)
+          skipreg = key < L && kLog2e * (skip_norm + gr.diff(q0, key)) < -kSkipMargin;
+      }
     }
   };
   auto store_c = [&](auto bufc) {
@@ -163,6 +182,7 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
     if (wave == 0) {
       sm.c[B][lane] = creg;
       if (lane == 0) sm.cref[B] = crefreg;
+      if (SKIP && lane == kDqBN - 1) sm.skip[B] = skipreg;
     }
   };
 
@@ -235,10 +255,12 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
     }
   };
 
+  // returns true when tile j and all earlier tiles can be skipped
   auto step = [&](int j, auto bufc) {
     constexpr int B = decltype(bufc)::value;
     wait_all_memory();
     __syncthreads();  // tile j is in LDS; every wave is done with tile j + 1
+    if (SKIP && sm.skip[B]) return true;
     if (j > 0) issue_tile(j - 1, std::integral_constant<int, 1 - B>());
     if (j == t_diag) {
       tile_body(j, bufc, std::true_type());
@@ -246,13 +268,14 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
       tile_body(j, bufc, std::false_type());
     }
     if (j > 0) store_c(std::integral_constant<int, 1 - B>());
+    return false;
   };
 
   issue_tile(t_last, std::integral_constant<int, 0>());
   store_c(std::integral_constant<int, 0>());
   for (int j = t_last; j >= 0; j -= 2) {
-    step(j, std::integral_constant<int, 0>());
-    if (j > 0) step(j - 1, std::integral_constant<int, 1>());
+    if (step(j, std::integral_constant<int, 0>())) break;
+    if (j > 0 && step(j - 1, std::integral_constant<int, 1>())) break;
   }
 
   const float dcq_tot = wave_sum_pair(dcq_part);
@@ -307,12 +330,14 @@ struct KvSmem {
   bf16x8 p[3][kKvPairs][BM / 16][64];  // P of each pair: [16-query chunk][lane], bf16 x 8
   float bq[3][BM];  // ((c_i - c_ref) - LSE_i) / s of each query row
   float dl[3][BM];  // Delta_i
+  int skip[3];      // the query tile and every later one contribute exact zeros
 };
 
-template <int D, bool FIXED>
+template <int D, bool FIXED, bool SKIP>
 __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
-    const float* __restrict__ gate, const float* __restrict__ LSE, const bf16* __restrict__ dO,
+    const float* __restrict__ gate, const float* __restrict__ qnorm,
+    const float* __restrict__ knorm, const float* __restrict__ LSE, const bf16* __restrict__ dO,
     const float* __restrict__ delta, bf16* __restrict__ dK, bf16* __restrict__ dV,
     float* __restrict__ dck, int BH, int H, int L, float scale, float scale_log2) {
   constexpr int kKvBM = kv_bm<D>();
@@ -326,8 +351,9 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
   const int h = lane >> 5, col = lane & 31;
   const bool pwave = wave < kKvPairs;  // role
   const int pair = wave % kKvPairs;
-  const int bh = blockIdx.x % BH;
   const int nblk = (int)(blockIdx.x / BH);  // key block 0 has the most work: first
+  // heads fastest; rotated over the XCDs when skipping (see the forward kernel)
+  const int bh = SKIP ? (int)((blockIdx.x + nblk) % BH) : (int)(blockIdx.x % BH);
   const int k0 = nblk * kKvBN;
   const size_t head = (size_t)bh * (size_t)L;
   const GateRow<FIXED> gr(gate, bh, H, head);  // reference: c at k0
@@ -392,7 +418,10 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
   float dck_part = 0.0f;
 
   const int t_first = k0 / kKvBM;
-  const int n_tiles = (L + kKvBM - 1) / kKvBM - t_first;
+  int n_tiles = (L + kKvBM - 1) / kKvBM - t_first;  // lowered by gate-aware skipping
+  const float skip_norm = SKIP ? 2.0f * scale * qnorm[bh] * knorm[bh] : 0.0f;
+  const int k_last = min(L, k0 + kKvBN) - 1;  // the block's least decayed key
+  bool skipreg = false;
   const int t_diag = kw0 / kKvBM;  // tile holding this pair's diagonal
 
   // per query row of a tile: ((c_i - c_ref) - LSE_i) / s and Delta_i
@@ -407,6 +436,8 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
       dma16(rq, &sm.q[B][wslot], base + dma_off[i]);
       dma16(rg, &sm.g[B][wslot], base + dma_off[i]);
     }
+    if (SKIP && wave == 0 && lane == 0)  // the tile's first query against the block's last key
+      skipreg = kLog2e * (skip_norm + gr.diff(qt * kKvBM, k_last)) < -kSkipMargin;
     if (wave == 0 && lane < kKvBM) {
       const int qq = qt * kKvBM + lane;
       breg = -INFINITY;
@@ -423,6 +454,7 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
       sm.bq[B][lane] = breg;
       sm.dl[B][lane] = dreg;
     }
+    if (SKIP && wave == 0 && lane == 0) sm.skip[B] = skipreg;
   };
 
   // P wave on tile qt held in buffer B
@@ -516,6 +548,8 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
     constexpr int BN = (B + 1) % 3, BP = (B + 2) % 3;
     wait_all_memory();
     __syncthreads();  // tile it and P of tile it - 1 are in LDS
+    // tile it and all later ones add exact zeros: the G waves finish tile it - 1
+    if (SKIP && it < n_tiles && sm.skip[B]) n_tiles = it;
     if (it + 1 < n_tiles) issue_tile(t_first + it + 1, std::integral_constant<int, BN>());
     if (pwave) {
       const int qt = t_first + it;
@@ -737,12 +771,19 @@ hipError_t launch_bwd_delta(bool bf16_, const void* o, const void* d_o, float* d
 template <int D, bool FIXED>
 static void dkdv_t(bool bf16_, const void* q, const void* k, const void* v, GateSpec g,
                    const float* lse, const void* d_o, const float* delta, void* dk, void* dv,
-                   float* dck, int BH, int L, float scale, hipStream_t s) {
+                   float* dck, int BH, int L, float scale, hipStream_t s, const float* qn,
+                   const float* kn) {
   const float sl2 = scale * kLog2e;
   if (bf16_) {
     const dim3 grid((unsigned)((L + kKvBN - 1) / kKvBN) * (unsigned)BH);
-    hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, FIXED>), grid, dim3(kKvThreads), 0, s,
-                       (const bf16*)q, (const bf16*)k, (const bf16*)v, g.ptr, lse,
+    if (qn)
+      hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, FIXED, true>), grid, dim3(kKvThreads), 0, s,
+                         (const bf16*)q, (const bf16*)k, (const bf16*)v, g.ptr, qn, kn, lse,
+                         (const bf16*)d_o, delta, (bf16*)dk, (bf16*)dv, dck, BH, g.H, L, scale,
+                         sl2);
+    else
+    hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, FIXED, false>), grid, dim3(kKvThreads), 0, s,
+                       (const bf16*)q, (const bf16*)k, (const bf16*)v, g.ptr, qn, kn, lse,
                        (const bf16*)d_o, delta, (bf16*)dk, (bf16*)dv, dck, BH, g.H, L, scale,
                        sl2);
   } else {
@@ -759,13 +800,17 @@ static void dkdv_t(bool bf16_, const void* q, const void* k, const void* v, Gate
 hipError_t launch_bwd_dkdv(bool bf16_, const void* q, const void* k, const void* v, GateSpec g,
                            const float* lse, const void* d_o, const float* delta, void* dk,
                            void* dv, float* dck, int BH, int L, int d, float scale,
-                           hipStream_t s) {
+                           hipStream_t s, const float* qn, const float* kn) {
   if (d == 128) {
-    if (g.fixed) dkdv_t<128, true>(bf16_, q, k, v, g, lse, d_o, delta, dk, dv, dck, BH, L, scale, s);
-    else dkdv_t<128, false>(bf16_, q, k, v, g, lse, d_o, delta, dk, dv, dck, BH, L, scale, s);
+    if (g.fixed)
+      dkdv_t<128, true>(bf16_, q, k, v, g, lse, d_o, delta, dk, dv, dck, BH, L, scale, s, qn, kn);
+    else
+      dkdv_t<128, false>(bf16_, q, k, v, g, lse, d_o, delta, dk, dv, dck, BH, L, scale, s, qn, kn);
   } else {
-    if (g.fixed) dkdv_t<64, true>(bf16_, q, k, v, g, lse, d_o, delta, dk, dv, dck, BH, L, scale, s);
-    else dkdv_t<64, false>(bf16_, q, k, v, g, lse, d_o, delta, dk, dv, dck, BH, L, scale, s);
+    if (g.fixed)
+      dkdv_t<64, true>(bf16_, q, k, v, g, lse, d_o, delta, dk, dv, dck, BH, L, scale, s, qn, kn);
+    else
+      dkdv_t<64, false>(bf16_, q, k, v, g, lse, d_o, delta, dk, dv, dck, BH, L, scale, s, qn, kn);
   }
   return hipGetLastError();
 }
@@ -773,13 +818,18 @@ hipError_t launch_bwd_dkdv(bool bf16_, const void* q, const void* k, const void*
 template <int D, bool FIXED>
 static void dq_t(bool bf16_, const void* q, const void* k, const void* v, GateSpec g,
                  const float* lse, const void* d_o, const float* delta, void* dq, float* dcq,
-                 int BH, int L, float scale, hipStream_t s) {
+                 int BH, int L, float scale, hipStream_t s, const float* qn, const float* kn) {
   const float sl2 = scale * kLog2e;
   if (bf16_) {
     const int n_mblk = (L + kDqBM - 1) / kDqBM;
     const dim3 grid((unsigned)n_mblk * (unsigned)BH);
-    hipLaunchKernelGGL((bwd_dq_bf16_kernel<D, FIXED>), grid, dim3(kBwdThreads), 0, s,
-                       (const bf16*)q, (const bf16*)k, (const bf16*)v, g.ptr, lse,
+    if (qn)
+      hipLaunchKernelGGL((bwd_dq_bf16_kernel<D, FIXED, true>), grid, dim3(kBwdThreads), 0, s,
+                         (const bf16*)q, (const bf16*)k, (const bf16*)v, g.ptr, qn, kn, lse,
+                         (const bf16*)d_o, delta, (bf16*)dq, dcq, BH, g.H, L, n_mblk, scale, sl2);
+    else
+    hipLaunchKernelGGL((bwd_dq_bf16_kernel<D, FIXED, false>), grid, dim3(kBwdThreads), 0, s,
+                       (const bf16*)q, (const bf16*)k, (const bf16*)v, g.ptr, qn, kn, lse,
                        (const bf16*)d_o, delta, (bf16*)dq, dcq, BH, g.H, L, n_mblk, scale, sl2);
   } else {
     const int rpw = kF32Threads / (D / 32);
@@ -793,13 +843,18 @@ static void dq_t(bool bf16_, const void* q, const void* k, const void* v, GateSp
 
 hipError_t launch_bwd_dq(bool bf16_, const void* q, const void* k, const void* v, GateSpec g,
                          const float* lse, const void* d_o, const float* delta, void* dq,
-                         float* dcq, int BH, int L, int d, float scale, hipStream_t s) {
+                         float* dcq, int BH, int L, int d, float scale, hipStream_t s,
+                         const float* qn, const float* kn) {
   if (d == 128) {
-    if (g.fixed) dq_t<128, true>(bf16_, q, k, v, g, lse, d_o, delta, dq, dcq, BH, L, scale, s);
-    else dq_t<128, false>(bf16_, q, k, v, g, lse, d_o, delta, dq, dcq, BH, L, scale, s);
+    if (g.fixed)
+      dq_t<128, true>(bf16_, q, k, v, g, lse, d_o, delta, dq, dcq, BH, L, scale, s, qn, kn);
+    else
+      dq_t<128, false>(bf16_, q, k, v, g, lse, d_o, delta, dq, dcq, BH, L, scale, s, qn, kn);
   } else {
-    if (g.fixed) dq_t<64, true>(bf16_, q, k, v, g, lse, d_o, delta, dq, dcq, BH, L, scale, s);
-    else dq_t<64, false>(bf16_, q, k, v, g, lse, d_o, delta, dq, dcq, BH, L, scale, s);
+    if (g.fixed)
+      dq_t<64, true>(bf16_, q, k, v, g, lse, d_o, delta, dq, dcq, BH, L, scale, s, qn, kn);
+    else
+      dq_t<64, false>(bf16_, q, k, v, g, lse, d_o, delta, dq, dcq, BH, L, scale, s, qn, kn);
   }
   return hipGetLastError();
 }
@@ -807,15 +862,17 @@ hipError_t launch_bwd_dq(bool bf16_, const void* q, const void* k, const void* v
 static hipError_t launch_bwd_stages(bool bf16_, const void* q, const void* k, const void* v,
                                     GateSpec g, const void* o, const float* lse, const void* d_o,
                                     void* dq, void* dk, void* dv, float* d_log_f, float* ws,
-                                    int BH, int L, int d, float scale, hipStream_t s) {
+                                    int BH, int L, int d, float scale, hipStream_t s,
+                                    const float* qn = nullptr, const float* kn = nullptr) {
   float* delta = ws;
   float* dcq = delta + (size_t)BH * L;
   float* dck = dcq + (size_t)BH * L;
   hipError_t e = launch_bwd_delta(bf16_, o, d_o, delta, BH, L, d, s);
   if (e == hipSuccess)
-    e = launch_bwd_dkdv(bf16_, q, k, v, g, lse, d_o, delta, dk, dv, dck, BH, L, d, scale, s);
+    e = launch_bwd_dkdv(bf16_, q, k, v, g, lse, d_o, delta, dk, dv, dck, BH, L, d, scale, s, qn,
+                        kn);
   if (e == hipSuccess)
-    e = launch_bwd_dq(bf16_, q, k, v, g, lse, d_o, delta, dq, dcq, BH, L, d, scale, s);
+    e = launch_bwd_dq(bf16_, q, k, v, g, lse, d_o, delta, dq, dcq, BH, L, d, scale, s, qn, kn);
   if (e == hipSuccess) e = launch_reverse_scan_sum(dcq, dck, d_log_f, BH, L, s);
   return e;
 }
@@ -823,9 +880,9 @@ static hipError_t launch_bwd_stages(bool bf16_, const void* q, const void* k, co
 hipError_t launch_bwd(bool bf16_, const void* q, const void* k, const void* v, const float* c,
                       const void* o, const float* lse, const void* d_o, void* dq, void* dk,
                       void* dv, float* d_log_f, void* ws, int BH, int L, int d, float scale,
-                      hipStream_t s) {
+                      hipStream_t s, const float* q_norm_max, const float* k_norm_max) {
   return launch_bwd_stages(bf16_, q, k, v, gate_array(c), o, lse, d_o, dq, dk, dv, d_log_f,
-                           static_cast<float*>(ws), BH, L, d, scale, s);
+                           static_cast<float*>(ws), BH, L, d, scale, s, q_norm_max, k_norm_max);
 }
 
 // d b^(h) = sigmoid(-b^(h)) * sum over the rows of head h and all t of d(log f):

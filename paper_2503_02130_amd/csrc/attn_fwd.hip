@@ -56,6 +56,10 @@ constexpr int kFwdBM = 32 * kFwdWaves;  // query rows per workgroup
 constexpr int kFwdBN = 64;              // keys per tile
 constexpr float kRescaleSlack = 8.0f;   // log2 headroom before O and l are rescaled
 constexpr float kRescaleSum = 256.0f;  // 2^slack: a lane's tile sum above it triggers a rescale
+// Gate-aware skipping: a key tile is dropped when every P it could produce lies
+// below 2^-160 relative to the row maximum (150 for an exact fp32 zero, 10 more
+// for the rounding of the bound).
+constexpr float kSkipMargin = 160.0f;
 
 template <int D>
 struct FwdSmem {
@@ -64,10 +68,18 @@ struct FwdSmem {
   float c[2][kFwdBN];
 };
 
-template <int D, bool FIXED>
+// SKIP: qnorm, knorm [BH] bound the row norms of Q and K.  For a query block
+// starting at q0 and a key tile ending at jl, every score is at most
+// s Qmax Kmax + (c_i - c_j) <= s Qmax Kmax + (c_q0 - c_jl), and every row
+// maximum is at least the diagonal score s q_i.k_i >= -s Qmax Kmax, so once
+// log2(e) (2 s Qmax Kmax + c_q0 - c_jl) < -kSkipMargin the tile (and, as c
+// falls along the sequence, every earlier tile) adds exact zeros: the loop
+// stops there and the results equal the dense kernel's bit for bit.
+template <int D, bool FIXED, bool SKIP>
 __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
                      const bf16* __restrict__ V, const float* __restrict__ gate,
+                     const float* __restrict__ qnorm, const float* __restrict__ knorm,
                      bf16* __restrict__ O, float* __restrict__ LSE, int BH, int H, int L,
                      int n_mblk, float scale_log2) {
   constexpr int TILE = kFwdBN * D;                         // bf16 elements per tile
@@ -76,8 +88,11 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = lane >> 5, col = lane & 31;
-  const int bh = blockIdx.x % BH;
-  const int mblk = n_mblk - 1 - (int)(blockIdx.x / BH);
+  // heads fastest (a head's blocks on one XCD, sharing its L2); with skipping the
+  // work per head depends on its gates, so the heads rotate over the XCDs
+  const int row = (int)(blockIdx.x / BH);
+  const int bh = SKIP ? (int)((blockIdx.x + row) % BH) : (int)(blockIdx.x % BH);
+  const int mblk = n_mblk - 1 - row;
   const int q0 = mblk * kFwdBM;
   const size_t head = (size_t)bh * (size_t)L;
   const bf16* Qh = Q + head * D;
@@ -117,6 +132,8 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
   const int kend = min(L, q0 + kFwdBM);
   const int t_last = (kend + kFwdBN - 1) / kFwdBN - 1;
   const int t_diag = qw0 / kFwdBN;  // tile holding this wave's diagonal
+  // skip test in the units of the stored key terms ((c_q0 - c_j) / s)
+  const float skip_norm = SKIP ? 2.0f * qnorm[bh] * knorm[bh] : 0.0f;
 
   float creg = 0.0f;
   auto issue_tile = [&](int kt, auto bufc) {
@@ -236,10 +253,17 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
     }
   };
 
+  // returns true when tile j and all earlier tiles can be skipped
   auto step = [&](int j, auto bufc) {
     constexpr int B = decltype(bufc)::value;
     wait_all_memory();
     __syncthreads();  // tile j is in LDS; every wave is done with tile j + 1
+    if constexpr (SKIP) {
+      // the tile's last key is the least decayed one (full tiles only: the
+      // diagonal region never passes the test)
+      if (j < t_last && scale_log2 * (skip_norm + sm.c[B][kFwdBN - 1]) < -kSkipMargin)
+        return true;
+    }
     if (j > 0) issue_tile(j - 1, std::integral_constant<int, 1 - B>());
     if (j == t_diag) {
       tile_body(j, bufc, std::true_type());
@@ -247,13 +271,14 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
       tile_body(j, bufc, std::false_type());
     }
     if (j > 0) store_c(std::integral_constant<int, 1 - B>());
+    return false;
   };
 
   issue_tile(t_last, std::integral_constant<int, 0>());
   store_c(std::integral_constant<int, 0>());
   for (int j = t_last; j >= 0; j -= 2) {
-    step(j, std::integral_constant<int, 0>());
-    if (j > 0) step(j - 1, std::integral_constant<int, 1>());
+    if (step(j, std::integral_constant<int, 0>())) break;
+    if (j > 0 && step(j - 1, std::integral_constant<int, 1>())) break;
   }
 
   const float l_tot = wave_sum_pair(l_run);
@@ -356,25 +381,37 @@ __global__ __launch_bounds__(kF32Threads) void fwd_f32_kernel(
   }
 }
 
-template <int D, bool FIXED>
-static void fwd_bf16_t(const void* q, const void* k, const void* v, GateSpec g, void* o,
-                       float* lse, int BH, int L, float sl2, hipStream_t s) {
+template <int D, bool FIXED, bool SKIP>
+static void fwd_bf16_t(const void* q, const void* k, const void* v, GateSpec g,
+                       const float* qn, const float* kn, void* o, float* lse, int BH, int L,
+                       float sl2, hipStream_t s) {
   const int n_mblk = (L + kFwdBM - 1) / kFwdBM;
   const dim3 grid((unsigned)n_mblk * (unsigned)BH);
-  hipLaunchKernelGGL((fwd_bf16_kernel<D, FIXED>), grid, dim3(kFwdThreads), 0, s, (const bf16*)q,
-                     (const bf16*)k, (const bf16*)v, g.ptr, (bf16*)o, lse, BH, g.H, L, n_mblk,
-                     sl2);
+  hipLaunchKernelGGL((fwd_bf16_kernel<D, FIXED, SKIP>), grid, dim3(kFwdThreads), 0, s,
+                     (const bf16*)q, (const bf16*)k, (const bf16*)v, g.ptr, qn, kn, (bf16*)o, lse,
+                     BH, g.H, L, n_mblk, sl2);
+}
+
+template <int D, bool FIXED>
+static void fwd_bf16_s(const void* q, const void* k, const void* v, GateSpec g,
+                       const float* qn, const float* kn, void* o, float* lse, int BH, int L,
+                       float sl2, hipStream_t s) {
+  if (qn) fwd_bf16_t<D, FIXED, true>(q, k, v, g, qn, kn, o, lse, BH, L, sl2, s);
+  else fwd_bf16_t<D, FIXED, false>(q, k, v, g, qn, kn, o, lse, BH, L, sl2, s);
 }
 
 hipError_t launch_fwd_bf16(const void* q, const void* k, const void* v, GateSpec g, void* o,
-                           float* lse, int BH, int L, int d, float scale, hipStream_t s) {
+                           float* lse, int BH, int L, int d, float scale, hipStream_t s,
+                           const float* q_norm_max, const float* k_norm_max) {
   const float sl2 = scale * kLog2e;
+  const float* qn = q_norm_max;
+  const float* kn = k_norm_max;
   if (d == 128) {
-    if (g.fixed) fwd_bf16_t<128, true>(q, k, v, g, o, lse, BH, L, sl2, s);
-    else fwd_bf16_t<128, false>(q, k, v, g, o, lse, BH, L, sl2, s);
+    if (g.fixed) fwd_bf16_s<128, true>(q, k, v, g, qn, kn, o, lse, BH, L, sl2, s);
+    else fwd_bf16_s<128, false>(q, k, v, g, qn, kn, o, lse, BH, L, sl2, s);
   } else {
-    if (g.fixed) fwd_bf16_t<64, true>(q, k, v, g, o, lse, BH, L, sl2, s);
-    else fwd_bf16_t<64, false>(q, k, v, g, o, lse, BH, L, sl2, s);
+    if (g.fixed) fwd_bf16_s<64, true>(q, k, v, g, qn, kn, o, lse, BH, L, sl2, s);
+    else fwd_bf16_s<64, false>(q, k, v, g, qn, kn, o, lse, BH, L, sl2, s);
   }
   return hipGetLastError();
 }

@@ -213,6 +213,51 @@ int fox_row_norm_max(int dtype, const void* x, float* out, int B, int H, int L, 
                                                 static_cast<hipStream_t>(stream)));
 }
 
+int fox_attn_fwd_skip(int dtype, const void* q, const void* k, const void* v, const float* c,
+                      const float* q_norm_max, const float* k_norm_max, void* o, float* lse,
+                      int B, int H, int L, int d, float scale, void* stream) {
+  if (!q || !k || !v || !c || !q_norm_max || !k_norm_max || !o || !lse) return FOX_ERR_NULL;
+  int st = check_dims(B, H, L, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(c) ||
+      !aligned16(q_norm_max) || !aligned16(k_norm_max) || !aligned16(o) || !aligned16(lse))
+    return FOX_ERR_ALIGN;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (dtype == FOX_DTYPE_BF16)
+    return launch_status(fox::launch_fwd_bf16(q, k, v, fox::gate_array(c), o, lse, B * H, L, d,
+                                              scale, s, q_norm_max, k_norm_max));
+  return launch_status(fox::launch_fwd_f32((const float*)q, (const float*)k, (const float*)v,
+                                           fox::gate_array(c), (float*)o, lse, B * H, L, d, scale,
+                                           s));
+}
+
+int fox_attn_bwd_skip(int dtype, const void* q, const void* k, const void* v, const float* c,
+                      const void* o, const float* lse, const void* d_o, const float* q_norm_max,
+                      const float* k_norm_max, void* dq, void* dk, void* dv, float* d_log_f,
+                      void* workspace, size_t workspace_bytes, int B, int H, int L, int d,
+                      float scale, void* stream) {
+  if (!q || !k || !v || !c || !o || !lse || !d_o || !q_norm_max || !k_norm_max || !dq || !dk ||
+      !dv || !d_log_f)
+    return FOX_ERR_NULL;
+  int st = check_dims(B, H, L, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(c) || !aligned16(o) ||
+      !aligned16(lse) || !aligned16(d_o) || !aligned16(q_norm_max) || !aligned16(k_norm_max) ||
+      !aligned16(dq) || !aligned16(dk) || !aligned16(dv) || !aligned16(d_log_f))
+    return FOX_ERR_ALIGN;
+  if (!workspace || workspace_bytes < fox::bwd_workspace_bytes(B * H, L)) return FOX_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return FOX_ERR_ALIGN;
+  const bool bf = dtype == FOX_DTYPE_BF16;
+  return launch_status(fox::launch_bwd(bf, q, k, v, c, o, lse, d_o, dq, dk, dv, d_log_f,
+                                       workspace, B * H, L, d, scale,
+                                       static_cast<hipStream_t>(stream), bf ? q_norm_max : nullptr,
+                                       bf ? k_norm_max : nullptr));
+}
+
 int fox_attn_decode_skip(int dtype, const void* q, const void* k_cache, const void* v_cache,
                          float* c_cache, const float* gate_logit_new, const float* k_norm_max,
                          void* o, float* lse, void* workspace, size_t workspace_bytes, int B,

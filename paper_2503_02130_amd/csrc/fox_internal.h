@@ -28,8 +28,11 @@ hipError_t launch_reverse_scan_gate(const float* a, const float* b, const float*
                                     float* d_log_f, float* d_logit, int rows, int L,
                                     hipStream_t s);
 
+// q_norm_max / k_norm_max [BH] (both or neither): exact gate-aware skipping of
+// key tiles whose contribution is an fp32 zero.
 hipError_t launch_fwd_bf16(const void* q, const void* k, const void* v, GateSpec g, void* o,
-                           float* lse, int BH, int L, int d, float scale, hipStream_t s);
+                           float* lse, int BH, int L, int d, float scale, hipStream_t s,
+                           const float* q_norm_max = nullptr, const float* k_norm_max = nullptr);
 hipError_t launch_fwd_f32(const float* q, const float* k, const float* v, GateSpec g, float* o,
                           float* lse, int BH, int L, int d, float scale, hipStream_t s);
 
@@ -39,14 +42,17 @@ hipError_t launch_bwd_delta(bool bf16, const void* o, const void* d_o, float* de
                             int L, int d, hipStream_t s);
 hipError_t launch_bwd_dkdv(bool bf16, const void* q, const void* k, const void* v, GateSpec g,
                            const float* lse, const void* d_o, const float* delta, void* dk,
-                           void* dv, float* dck, int BH, int L, int d, float scale, hipStream_t s);
+                           void* dv, float* dck, int BH, int L, int d, float scale, hipStream_t s,
+                           const float* q_norm_max = nullptr, const float* k_norm_max = nullptr);
 hipError_t launch_bwd_dq(bool bf16, const void* q, const void* k, const void* v, GateSpec g,
                          const float* lse, const void* d_o, const float* delta, void* dq,
-                         float* dcq, int BH, int L, int d, float scale, hipStream_t s);
+                         float* dcq, int BH, int L, int d, float scale, hipStream_t s,
+                         const float* q_norm_max = nullptr, const float* k_norm_max = nullptr);
 hipError_t launch_bwd(bool bf16, const void* q, const void* k, const void* v, const float* c,
                       const void* o, const float* lse, const void* d_o, void* dq, void* dk,
                       void* dv, float* d_log_f, void* ws, int BH, int L, int d, float scale,
-                      hipStream_t s);
+                      hipStream_t s, const float* q_norm_max = nullptr,
+                      const float* k_norm_max = nullptr);
 // Fixed gates: workspace delta, dc_q, dc_k, d(log f), each [BH, L] fp32; the bias
 // gradient d_bias [H] (may be NULL) = sigmoid(-b) * sum over rows and t of d(log f).
 size_t bwd_fixed_workspace_bytes(int BH, int L);

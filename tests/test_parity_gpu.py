@@ -453,3 +453,32 @@ def test_decode_skip_is_bitwise_dense(dtype, d, B, H, T, gate):
     o2, l2 = fox.fox_attn_decode_skip(y["q"], y["k_cache"], y["v_cache"], cc2, y["logit_new"], kn)
     torch.cuda.synchronize()
     assert torch.equal(o1, o2) and torch.equal(l1, l2) and torch.equal(cc, cc2)
+
+
+SKIP_CASES = [
+    ("bf16", 128, 2, 3, 3000, ("normal", 1.0, 1.0)),
+    ("bf16", 64, 2, 2, 4100, ("normal", -3.0, 1.0)),
+    ("bf16", 128, 1, 4, 2500, ("head_mean_uniform", 0.0, 6.0, 1.0)),
+    ("bf16", 64, 1, 2, 1000, ("normal", 8.0, 1.0)),
+    ("bf16", 128, 1, 1, 1, ("normal", 1.0, 1.0)),
+    ("f32", 64, 1, 2, 300, ("normal", -2.0, 1.0)),
+]
+
+
+@pytest.mark.parametrize("dtype,d,B,H,L,gate", SKIP_CASES)
+def test_fwd_bwd_skip_is_bitwise_dense(dtype, d, B, H, L, gate):
+    """Exact gate-aware skipping drops only tile pairs whose contributions are
+    fp32 zeros: O, LSE, dQ, dK, dV, d(log f) equal the dense results bit for bit."""
+    print(f"fwd/bwd skip dtype={dtype} d={d} B={B} H={H} L={L} gate={gate}", flush=True)
+    x = inputs.attn_inputs(B, H, L, d, dtype, gate, 800 + L, device=DEV)
+    s = fox.default_scale(d)
+    c = fox.fox_gate_prefix(x["logit"])
+    qn, kn = fox.fox_row_norm_max(x["q"]), fox.fox_row_norm_max(x["k"])
+    o1, l1 = fox.fox_attn_fwd(x["q"], x["k"], x["v"], c, s)
+    o2, l2 = fox.fox_attn_fwd_skip(x["q"], x["k"], x["v"], c, qn, kn, s)
+    g1 = fox.fox_attn_bwd(x["q"], x["k"], x["v"], c, o1, l1, x["do"], s)
+    g2 = fox.fox_attn_bwd_skip(x["q"], x["k"], x["v"], c, o1, l1, x["do"], qn, kn, s)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+    for name, a, b in zip(("dq", "dk", "dv", "dlogf"), g1, g2):
+        assert torch.equal(a, b), name
