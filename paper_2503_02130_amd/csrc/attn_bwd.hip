@@ -388,10 +388,20 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
   // plain operand s of 32-row block qb of buffer B; transposing operand of
   // 16-row chunk ch, head-dim block db
   auto plain_op = [&](int s, int boff) { return *(const lds_bf16x8_t*)(pa[s] + boff); };
-  auto tr_op = [&](int db, int boff) {
-    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(ta_[0][db] + boff));
-    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(ta_[1][db] + boff));
-    return (bf16x8)__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  uint32_t taddr[2][D / 32];  // the same as 32-bit addresses for the assembly reads
+#pragma unroll
+  for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) taddr[k2][db] = (uint32_t)(uintptr_t)ta_[k2][db];
+  constexpr int NR = 2 * (D / 32);  // transposing reads per 16-query chunk
+  // transposing operands of 16-query chunk CH of buffer B, read by inline assembly
+  auto read_tr = [&](auto bufc, auto chc, bf16x4 (&t)[NR]) {
+    constexpr int OFF = 2 * (decltype(bufc)::value * TILE + decltype(chc)::value * 16 * D);
+    static_for<D / 32>([&](auto dbc) {
+      constexpr int DB = decltype(dbc)::value;
+      t[2 * DB] = ds_read_tr_asm<OFF>(taddr[0][DB]);
+      t[2 * DB + 1] = ds_read_tr_asm<OFF>(taddr[1][DB]);
+    });
   };
 
   // P waves hold K rows, G waves hold V rows
@@ -421,11 +431,11 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
   int n_tiles = (L + kKvBM - 1) / kKvBM - t_first;  // lowered by gate-aware skipping
   const float skip_norm = SKIP ? 2.0f * scale * qnorm[bh] * knorm[bh] : 0.0f;
   const int k_last = min(L, k0 + kKvBN) - 1;  // the block's least decayed key
-  bool skipreg = false;
   const int t_diag = kw0 / kKvBM;  // tile holding this pair's diagonal
 
   // per query row of a tile: ((c_i - c_ref) - LSE_i) / s and Delta_i
   const float inv_scale = 1.0f / scale;
+  bool skipreg = false;
   float breg = 0.0f, dreg = 0.0f;
   auto issue_tile = [&](int qt, auto bufc) {
     constexpr int B = decltype(bufc)::value;
@@ -462,8 +472,8 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
     constexpr int B = decltype(bufc)::value;
     constexpr bool MASK = decltype(masked)::value;
     const int qs0 = qt * kKvBM;
-#pragma unroll
-    for (int qb = 0; qb < NQB; ++qb) {
+    static_for<NQB>([&](auto qbc) {
+      constexpr int qb = decltype(qbc)::value;
       bf16x8 qa[D / 16];
 #pragma unroll
       for (int s = 0; s < D / 16; ++s)
@@ -478,6 +488,10 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
       }
 #pragma unroll
       for (int s = 0; s < D / 16; ++s) sacc = mfma32(qa[s], kvf[s], sacc);
+      // the dO^T operands of the first chunk load while P is formed (the
+      // skipping kernel, short of registers, reads them just before use)
+      bf16x4 tr[NR];
+      if constexpr (!SKIP) read_tr(bufc, std::integral_constant<int, 2 * qb>(), tr);
       float pv[16];
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
@@ -489,24 +503,24 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
           pv[4 * g + jj] = p;
         }
       }
-#pragma unroll
-      for (int c = 0; c < 2; ++c) {
+      static_for<2>([&](auto cc) {
+        constexpr int c = decltype(cc)::value;
         const bf16x8 pb = pack8(&pv[8 * c]);
         *(lds_bf16x8_t*)(p_at + B * kPBuf + (2 * qb + c) * 1024) = pb;
-        bf16x8 ta[D / 32];
+        if constexpr (SKIP) read_tr(bufc, std::integral_constant<int, 2 * qb + c>(), tr);
+        lds_wait<SKIP ? 0 : 1>(tr);  // the store may stay in flight
 #pragma unroll
         for (int db = 0; db < D / 32; ++db)
-          ta[db] = tr_op(db, 2 * (B * TILE + (2 * qb + c) * 16 * D));
-#pragma unroll
-        for (int db = 0; db < D / 32; ++db) acc[db] = mfma32(ta[db], pb, acc[db]);
-      }
-    }
+          acc[db] = mfma32(cat4(tr[2 * db], tr[2 * db + 1]), pb, acc[db]);
+        if constexpr (!SKIP && c == 0) read_tr(bufc, std::integral_constant<int, 2 * qb + 1>(), tr);
+      });
+    });
   };
   // G wave on tile qt held in buffer B (its P was stored in the same buffer slot)
   auto g_tile = [&](auto bufc) {
     constexpr int B = decltype(bufc)::value;
-#pragma unroll
-    for (int qb = 0; qb < NQB; ++qb) {
+    static_for<NQB>([&](auto qbc) {
+      constexpr int qb = decltype(qbc)::value;
       bf16x8 ga[D / 16];
 #pragma unroll
       for (int s = 0; s < D / 16; ++s)
@@ -516,8 +530,11 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
       for (int r = 0; r < 16; ++r) pacc[r] = 0.0f;
 #pragma unroll
       for (int s = 0; s < D / 16; ++s) pacc = mfma32(ga[s], kvf[s], pacc);
-#pragma unroll
-      for (int c = 0; c < 2; ++c) {
+      // the Q^T operands of the first chunk load while dS is formed
+      bf16x4 tr[NR];
+      if constexpr (!SKIP) read_tr(bufc, std::integral_constant<int, 2 * qb>(), tr);
+      static_for<2>([&](auto cc) {
+        constexpr int c = decltype(cc)::value;
         const bf16x8 pb = *(const lds_bf16x8_t*)(p_at + B * kPBuf + (2 * qb + c) * 1024);
         float dsv[8];
 #pragma unroll
@@ -531,14 +548,14 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
           }
         }
         const bf16x8 dsb = pack8(dsv);
-        bf16x8 ta[D / 32];
+        if constexpr (SKIP) read_tr(bufc, std::integral_constant<int, 2 * qb + c>(), tr);
+        lds_wait<0>(tr);
 #pragma unroll
         for (int db = 0; db < D / 32; ++db)
-          ta[db] = tr_op(db, 2 * (B * TILE + (2 * qb + c) * 16 * D));
-#pragma unroll
-        for (int db = 0; db < D / 32; ++db) acc[db] = mfma32(ta[db], dsb, acc[db]);
-      }
-    }
+          acc[db] = mfma32(cat4(tr[2 * db], tr[2 * db + 1]), dsb, acc[db]);
+        if constexpr (!SKIP && c == 0) read_tr(bufc, std::integral_constant<int, 2 * qb + 1>(), tr);
+      });
+    });
   };
 
   // iteration it: the P wave works on tile it (buffer it % 3), the G wave on tile

@@ -110,6 +110,11 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
   tile_row_offsets<D>(koff, col, h);
   int voff[2][D / 32];
   tile_tr_offsets<D>(voff, lane);
+  uint32_t vaddr[2][D / 32];  // byte addresses of the transposing reads in V buffer 0
+#pragma unroll
+  for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) vaddr[k2][db] = lds_addr(&sm.v[0][0]) + 2 * voff[k2][db];
 
   bf16x8 qf[D / 16];
 #pragma unroll
@@ -135,7 +140,12 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
   // skip test in the units of the stored key terms ((c_q0 - c_j) / s)
   const float skip_norm = SKIP ? 2.0f * qnorm[bh] * knorm[bh] : 0.0f;
 
-  float creg = 0.0f;
+  // wave 0 stages the key terms of the next tile: the prefix values are loaded
+  // with the tile's DMA and converted after the tile body, so that waiting for
+  // them never waits for the DMA (memory operations complete in order)
+  const float c_q0 = gr.raw(q0);
+  float craw = 0.0f;
+  int ckey = 0;
   auto issue_tile = [&](int kt, auto bufc) {
     constexpr int B = decltype(bufc)::value;
     const uint32_t base = (uint32_t)kt * kFwdBN * D * 2;
@@ -146,13 +156,14 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
       dma16(rv, &sm.v[B][wslot], base + dma_off[i]);
     }
     if (wave == 0) {
-      const int key = kt * kFwdBN + lane;
-      creg = key < L ? gr.diff(q0, key) * inv_scale : -INFINITY;
+      ckey = kt * kFwdBN + lane;
+      if (ckey < L) craw = gr.raw(ckey);
     }
   };
   auto store_c = [&](auto bufc) {
     constexpr int B = decltype(bufc)::value;
-    if (wave == 0) sm.c[B][lane] = creg;
+    if (wave == 0)
+      sm.c[B][lane] = ckey < L ? gr.diff_raw(q0, c_q0, ckey, craw) * inv_scale : -INFINITY;
   };
 
   auto tile_body = [&](int j, auto bufc, auto masked) {
@@ -242,15 +253,31 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
       }
     }
     l_run += psum;
+    // O^T += V^T P^T over the four 16-key chunks; the V^T operands of chunk c + 1
+    // are read while chunk c is multiplied
+    constexpr int NR = 2 * (D / 32);  // transposing reads per chunk
+    bf16x4 tv[2][NR];
+    auto read_v = [&](auto cc, bf16x4 (&t)[NR]) {
+      constexpr int C = decltype(cc)::value;
+      static_for<D / 32>([&](auto dbc) {
+        constexpr int DB = decltype(dbc)::value;
+        t[2 * DB] = ds_read_tr_asm<(B * TILE + C * 16 * D) * 2>(vaddr[0][DB]);
+        t[2 * DB + 1] = ds_read_tr_asm<(B * TILE + C * 16 * D) * 2>(vaddr[1][DB]);
+      });
+    };
+    read_v(std::integral_constant<int, 0>(), tv[0]);
+    static_for<4>([&](auto cc) {
+      constexpr int C = decltype(cc)::value;
+      if constexpr (C + 1 < 4) {
+        read_v(std::integral_constant<int, C + 1>(), tv[(C + 1) % 2]);
+        lds_wait<NR>(tv[C % 2]);
+      } else {
+        lds_wait<0>(tv[C % 2]);
+      }
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      bf16x8 va[D / 32];
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db) va[db] = tile_tr_operand<D>(vt_, voff, c, db);
-      sched_fence();
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db) oacc[db] = mfma32(va[db], pb[c], oacc[db]);
-    }
+      for (int db = 0; db < D / 32; ++db)
+        oacc[db] = mfma32(cat4(tv[C % 2][2 * db], tv[C % 2][2 * db + 1]), pb[C], oacc[db]);
+    });
   };
 
   // returns true when tile j and all earlier tiles can be skipped

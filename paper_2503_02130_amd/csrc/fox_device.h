@@ -4,6 +4,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+#include <utility>
+
 typedef __bf16 bf16;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
@@ -109,6 +112,9 @@ struct GateRow<false> {
   __device__ GateRow(const float* gate, int /*bh*/, int /*H*/, size_t row)
       : c(gate + row) {}
   __device__ float diff(int i, int j) const { return c[i] - c[j]; }
+  // the same difference split into loads (issued early) and arithmetic (later)
+  __device__ float raw(int j) const { return c[j]; }
+  __device__ float diff_raw(int, float ci, int, float cj) const { return ci - cj; }
 };
 template <>
 struct GateRow<true> {
@@ -116,6 +122,8 @@ struct GateRow<true> {
   __device__ GateRow(const float* gate, int bh, int H, size_t /*row*/)
       : lf(log_sigmoid(gate[bh % H])) {}
   __device__ float diff(int i, int j) const { return (float)(i - j) * lf; }
+  __device__ float raw(int) const { return 0.0f; }
+  __device__ float diff_raw(int i, float, int j, float) const { return (float)(i - j) * lf; }
 };
 
 // ---------------------------------------------------------------------------
@@ -163,6 +171,53 @@ __device__ __forceinline__ const lds_byte* lds_ptr(const T* generic) {
 __device__ __forceinline__ const lds_byte* lds_opaque(const lds_byte* p) {
   asm volatile("" : "+v"(p));
   return p;
+}
+
+// Compile-time loop: f(std::integral_constant<int, I>()) for I = 0 .. N-1.
+template <typename F, int... Is>
+__device__ __forceinline__ void static_for_seq(F&& f, std::integer_sequence<int, Is...>) {
+  (f(std::integral_constant<int, Is>()), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_seq(f, std::make_integer_sequence<int, N>());
+}
+
+// 32-bit LDS address of a shared-memory object.
+template <typename T>
+__device__ __forceinline__ uint32_t lds_addr(const T* p) {
+  return (uint32_t)(uintptr_t)(const lds_byte*)p;
+}
+
+// The transposing read (ds_read_b64_tr_b16, see lds_read_tr16) at byte address
+// base + OFF, issued as inline assembly.  Through the compiler builtin every such
+// read first waits for all of the wave's outstanding LDS DMA (the compiler cannot
+// tell the buffers apart), which would stall each tile on the next tile's loads;
+// the tiles read here are never a DMA target while they are read.  The results
+// are valid only after lds_wait() (LDS operations complete in order).
+template <int OFF>
+__device__ __forceinline__ bf16x4 ds_read_tr_asm(uint32_t base) {
+  bf16x4 r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(base), "i"(OFF));
+  return r;
+}
+// Wait until at most N LDS operations of the wave are outstanding; the values
+// are tied to the wait so that their users come after it.
+template <int N>
+__device__ __forceinline__ void lds_wait(bf16x4 (&r)[4]) {
+  asm volatile("s_waitcnt lgkmcnt(%4)"
+               : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3])
+               : "i"(N));
+}
+template <int N>
+__device__ __forceinline__ void lds_wait(bf16x4 (&r)[8]) {
+  asm volatile("s_waitcnt lgkmcnt(%8)"
+               : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]), "+v"(r[4]), "+v"(r[5]),
+                 "+v"(r[6]), "+v"(r[7])
+               : "i"(N));
+}
+__device__ __forceinline__ bf16x8 cat4(const bf16x4& lo, const bf16x4& hi) {
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
 }
 
 // ---------------------------------------------------------------------------
