@@ -11,4 +11,7 @@ from .fox_oracle import (  # noqa: F401
     gate_backward, backward_logit,
     time_constant, fixed_gate_bias_init, fixed_gate_log_f, forward_fixed_gate,
     backward_fixed_gate,
+    rms_norm, rms_norm_backward, token_shift, token_shift_backward,
+    pro_prologue, pro_prologue_backward, output_gate, output_gate_backward,
+    pro_forward, pro_backward,
 )

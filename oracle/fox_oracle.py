@@ -34,6 +34,11 @@ paper (Forgetting Transformer, arXiv 2503.02130):
   * decode                     the forward's last row for a sequence whose last
                                key/value is the new token, c_T = c_{T-1} +
                                log sigmoid(x_new), c_0 = 0    (Eq. fot-weight at i = T)
+  * FoX (Pro) prologue         q = RMSNorm(q~), k = RMSNorm(a k~_{t-1} + (1-a) k~_t),
+                               v = b v~_{t-1} + (1-b) v~_t with a, b sigmoids of
+                               the shift logits      (Eq. shift-linear; appendix,
+                                                      FoX (Pro) layer computation)
+  * FoX (Pro) epilogue         y = RMSNorm(o) o sigmoid(g)   (same appendix)
 
 Readings of the paper this oracle takes (where it is silent or garbled):
   * the scale multiplies q.k only; D is unscaled; dQ, dK carry s, dc does not;
@@ -44,6 +49,8 @@ Readings of the paper this oracle takes (where it is silent or garbled):
   * Alg. 2's rowsum(dO o O) "in R^d" is one value per row (R^N);
   * Delta uses the exact O here (the oracle has no rounded O);
   * decode: the query at position T attends to keys 1..T including itself.
+  * Pro layer: RMSNorm(x) = x / sqrt(mean(x^2) + eps) * w with per-head
+    weights and eps an argument; the token shift of t = 1 mixes with zero.
 
 All functions accept any-dtype torch tensors (or numpy arrays) and return fp64
 torch tensors.  Every pin of this module lives in tests/test_oracle_*.py.
@@ -265,3 +272,128 @@ def decode(q, k_cache, v_cache, cached_logit, logit_new, scale: float, heads=Non
         o[b, h] = (e @ vc) / e.sum()
         lse[b, h] = m + torch.log(e.sum())
     return o, lse, c[..., T - 1]
+
+
+# ---------------------------------------------------------------------------
+# FoX (Pro) prologue and epilogue (Sec. 3 "Architecture design", Eq. shift-linear;
+# appendix "Detailed FoX (Pro) layer computation").  Per head h and time t, from
+# the raw projections q~ = W_q x, k~ = W_k x, v~ = W_v x (already split into heads):
+#   q_t = RMSNorm_q(q~_t)
+#   k_t = RMSNorm_k(a_t k~_{t-1} + (1 - a_t) k~_t),   a_t = sigmoid(w_k^T x_t)
+#   v_t = b_t v~_{t-1} + (1 - b_t) v~_t,              b_t = sigmoid(w_v^T x_t)
+# then, after the attention, y_t = RMSNorm_o(o_t) o sigmoid(W_g x_t).  The
+# output projection W_o and the sum over heads are plain matrix products and
+# not part of this module.
+# Readings: RMSNorm(x) = x / sqrt(mean(x^2) + eps) * w with a per-head weight
+# w^(h) in R^d (the paper gives no eps; it is an argument); the shift of the
+# first token mixes with a zero vector (k~_0 = v~_0 = 0); the shift logits
+# w_k^T x_t, w_v^T x_t and the gate logits W_g x_t are the inputs, and their
+# gradients are returned.
+# ---------------------------------------------------------------------------
+def _head_weight(weight, ndim):
+    """[H, d] per-head weights broadcast against [B, H, L, d] (or [H, L, d])."""
+    w = _f64(weight)
+    return w.reshape((1,) * (ndim - 3) + (w.shape[0], 1, w.shape[1]))
+
+
+def rms_norm(x, weight, eps: float):
+    """RMSNorm over the head dimension with per-head weights: x [.., H, L, d],
+    weight [H, d].  Returns (y, r) with r = 1 / sqrt(mean(x^2) + eps) [.., H, L]."""
+    x = _f64(x)
+    r = 1.0 / torch.sqrt((x * x).mean(dim=-1) + eps)
+    return x * r[..., None] * _head_weight(weight, x.dim()), r
+
+
+def rms_norm_backward(x, weight, eps: float, dy):
+    """Gradients of sum(RMSNorm(x) o dy): with n = x r and dn = dy o w,
+    dx = r (dn - n mean(dn o n)) (the mean over the head dimension), and
+    dw^(h) = sum over batch and time of dy o n."""
+    x, dy = _f64(x), _f64(dy)
+    _, r = rms_norm(x, weight, eps)
+    n = x * r[..., None]
+    dn = dy * _head_weight(weight, x.dim())
+    dx = r[..., None] * (dn - n * (dn * n).mean(dim=-1, keepdim=True))
+    dw = (dy * n).sum(dim=-2)                    # over time
+    if dw.dim() == 3:
+        dw = dw.sum(dim=0)                       # over batch
+    return dx, dw
+
+
+def token_shift(x, shift_logit):
+    """Eq. shift-linear's mix: a_t x_{t-1} + (1 - a_t) x_t with a_t = sigmoid(logit_t)
+    and x_0 = 0.  x [.., L, d], shift_logit [.., L]."""
+    x = _f64(x)
+    a = torch.sigmoid(_f64(shift_logit))[..., None]
+    prev = torch.zeros_like(x)
+    prev[..., 1:, :] = x[..., :-1, :]
+    return a * prev + (1.0 - a) * x
+
+
+def token_shift_backward(x, shift_logit, dy):
+    """Gradients of sum(token_shift(x) o dy): x_t enters output t with weight
+    (1 - a_t) and output t + 1 with weight a_{t+1}; d logit_t = a_t (1 - a_t)
+    (x_{t-1} - x_t) . dy_t."""
+    x, dy = _f64(x), _f64(dy)
+    a = torch.sigmoid(_f64(shift_logit))
+    dx = (1.0 - a)[..., None] * dy
+    dx[..., :-1, :] += a[..., 1:, None] * dy[..., 1:, :]
+    prev = torch.zeros_like(x)
+    prev[..., 1:, :] = x[..., :-1, :]
+    dlogit = a * (1.0 - a) * ((prev - x) * dy).sum(dim=-1)
+    return dx, dlogit
+
+
+def pro_prologue(q_raw, k_raw, v_raw, k_shift_logit, v_shift_logit, q_norm_weight,
+                 k_norm_weight, eps: float):
+    """q, k, v of a FoX (Pro) layer from the raw projections [B,H,L,d], the shift
+    logits [B,H,L] and the QK-norm weights [H,d]."""
+    q, _ = rms_norm(q_raw, q_norm_weight, eps)
+    k, _ = rms_norm(token_shift(k_raw, k_shift_logit), k_norm_weight, eps)
+    v = token_shift(v_raw, v_shift_logit)
+    return q, k, v
+
+
+def pro_prologue_backward(q_raw, k_raw, v_raw, k_shift_logit, v_shift_logit, q_norm_weight,
+                          k_norm_weight, eps: float, dq, dk, dv):
+    """Gradients of sum(q o dq + k o dk + v o dv) with respect to the raw
+    projections, the shift logits and the QK-norm weights:
+    (dq_raw, dk_raw, dv_raw, dk_shift_logit, dv_shift_logit, dq_norm_weight,
+    dk_norm_weight)."""
+    dq_raw, dwq = rms_norm_backward(q_raw, q_norm_weight, eps, dq)
+    k_mix = token_shift(k_raw, k_shift_logit)
+    dk_mix, dwk = rms_norm_backward(k_mix, k_norm_weight, eps, dk)
+    dk_raw, dka = token_shift_backward(k_raw, k_shift_logit, dk_mix)
+    dv_raw, dva = token_shift_backward(v_raw, v_shift_logit, dv)
+    return dq_raw, dk_raw, dv_raw, dka, dva, dwq, dwk
+
+
+def output_gate(o, g_logit, o_norm_weight, eps: float):
+    """y = RMSNorm_o(o) o sigmoid(g): o, g_logit [B,H,L,d]; o_norm_weight [H,d]."""
+    n, _ = rms_norm(o, o_norm_weight, eps)
+    return n * torch.sigmoid(_f64(g_logit))
+
+
+def output_gate_backward(o, g_logit, o_norm_weight, eps: float, dy):
+    """Gradients of sum(y o dy): (do, dg_logit, do_norm_weight).  With
+    u = RMSNorm_o(o) and sg = sigmoid(g): du = dy o sg, dg = dy o u o sg (1 - sg)."""
+    dy = _f64(dy)
+    sg = torch.sigmoid(_f64(g_logit))
+    u, _ = rms_norm(o, o_norm_weight, eps)
+    do, dw = rms_norm_backward(o, o_norm_weight, eps, dy * sg)
+    dg = dy * u * sg * (1.0 - sg)
+    return do, dg, dw
+
+
+def pro_forward(q, k, v, logit, g_logit, o_norm_weight, eps: float, scale: float):
+    """Attention followed by the output norm and gate: (y, O, LSE)."""
+    O, LSE = forward(q, k, v, logit, scale)
+    return output_gate(O, g_logit, o_norm_weight, eps), O, LSE
+
+
+def pro_backward(q, k, v, logit, g_logit, o_norm_weight, eps: float, scale: float, dy):
+    """Gradients of sum(y o dy) for pro_forward:
+    (dQ, dK, dV, d(log f), dg_logit, do_norm_weight)."""
+    O, _ = forward(q, k, v, logit, scale)
+    dO, dg, dw = output_gate_backward(O, g_logit, o_norm_weight, eps, dy)
+    dQ, dK, dV, dlf = backward(q, k, v, logit, dO, scale)
+    return dQ, dK, dV, dlf, dg, dw

@@ -34,6 +34,17 @@ The pins, with what in the paper fixes them:
       zero gradient of the first gate, and the sigmoid-derivative closed form.
   P15 fixed gates: the appendix's initialisation example (golden file), the
       equivalence with ALiBi at slopes 1/T_h, and d b by finite differences.
+  P16 RMSNorm (Pro layer): unit weight and eps = 0 give rows of mean square
+      exactly 1 and invariance to scaling each row; eps > 0 gives mean square
+      ms / (ms + eps); each head uses its own weight row.
+  P17 token shift (Eq. shift-linear): logit -> -inf is the identity, +inf the
+      shift by one step with a zero first row, 0 the average of neighbours; the
+      Pro prologue reduces to these with QK-norm applied.
+  P18 Pro gradients: central finite differences of the prologue and of the
+      output norm and gate, and torch autograd of an independently written
+      Pro layer (prologue, attention, epilogue) against the oracle's chain.
+  P19 output gate: g -> +inf leaves RMSNorm(o); g = 0 halves it; d g vanishes
+      where the gate saturates.
 """
 from __future__ import annotations
 
@@ -417,6 +428,150 @@ def pin_p15_fixed_gate_bias_gradient(ora, B=2, H=3, L=9, d=3, seed=25):
             f"P15 db[{h}]: finite difference {fd:.9f} vs oracle {float(db[h]):.9f}"
 
 
+# --------------------------------------------------------------------------- P16
+def pin_p16_rms_norm(ora, H=3, L=11, d=7, seed=16):
+    """Unit weight, eps = 0: every row has mean square 1 and is scale invariant;
+    with eps the mean square is ms / (ms + eps); per-head weights scale per head."""
+    x = _rand((2, H, L, d), seed)
+    ones = torch.ones(H, d, dtype=F64)
+    y, r = ora.rms_norm(x, ones, 0.0)
+    _close((y * y).mean(-1), torch.ones(2, H, L, dtype=F64), 1e-12, "P16 unit mean square")
+    lam = torch.rand(2, H, L, 1, generator=torch.Generator().manual_seed(seed), dtype=F64) * 5 + 0.1
+    y2, _ = ora.rms_norm(x * lam, ones, 0.0)
+    _close(y2, y, 1e-12, "P16 scale invariance")
+    ms = (x * x).mean(-1)
+    eps = 0.37
+    y3, _ = ora.rms_norm(x, ones, eps)
+    _close((y3 * y3).mean(-1), ms / (ms + eps), 1e-12, "P16 mean square with eps")
+    w = _rand((H, d), seed + 1)
+    y4, _ = ora.rms_norm(x, w, 0.0)
+    for h in range(H):
+        _close(y4[:, h], y[:, h] * w[h], 1e-12, f"P16 head {h} weight")
+
+
+# --------------------------------------------------------------------------- P17
+def pin_p17_token_shift_limits(ora, B=2, H=2, L=9, d=5, seed=17):
+    """Shift logits at -inf, +inf and 0 give the identity, the one-step shift with
+    a zero first row, and the average with the previous row (zero before t = 1)."""
+    x = _rand((B, H, L, d), seed)
+    big = torch.full((B, H, L), 1e4, dtype=F64)
+    _close(ora.token_shift(x, -big), x, 0.0, "P17 identity")
+    sh = ora.token_shift(x, big)
+    _close(sh[..., 0, :], torch.zeros(B, H, d, dtype=F64), 0.0, "P17 first row")
+    _close(sh[..., 1:, :], x[..., :-1, :], 0.0, "P17 shift")
+    av = ora.token_shift(x, torch.zeros(B, H, L, dtype=F64))
+    _close(av[..., 1:, :], 0.5 * (x[..., 1:, :] + x[..., :-1, :]), 1e-15, "P17 average")
+    _close(av[..., 0, :], 0.5 * x[..., 0, :], 1e-15, "P17 average, first row")
+    # the prologue with saturated shifts: plain QK-norm, and keys taken from t - 1
+    qr, kr, vr = x, _rand((B, H, L, d), seed + 1), _rand((B, H, L, d), seed + 2)
+    wq, wk = _rand((H, d), seed + 3), _rand((H, d), seed + 4)
+    q, k, v = ora.pro_prologue(qr, kr, vr, -big, big, wq, wk, 1e-6)
+    n = lambda t, w: t / torch.sqrt((t * t).mean(-1, keepdim=True) + 1e-6) * w[None, :, None, :]
+    _close(q, n(qr, wq), 1e-12, "P17 prologue q")
+    _close(k, n(kr, wk), 1e-12, "P17 prologue k without shift")
+    _close(v[..., 1:, :], vr[..., :-1, :], 0.0, "P17 prologue v shifted")
+
+
+# --------------------------------------------------------------------------- P18
+def _fd_check(f, x, grad, eps, tol, what, n_probe=12, seed=0):
+    """Central finite differences of the scalar f at n_probe entries of x."""
+    g = torch.Generator().manual_seed(seed)
+    flat = x.view(-1)
+    idx = torch.randperm(flat.numel(), generator=g)[:n_probe]
+    for i in idx.tolist():
+        old = float(flat[i])
+        flat[i] = old + eps
+        fp = f()
+        flat[i] = old - eps
+        fm = f()
+        flat[i] = old
+        fd = (fp - fm) / (2 * eps)
+        an = float(grad.reshape(-1)[i])
+        assert abs(fd - an) <= tol * max(1.0, abs(fd)), f"{what}[{i}]: fd {fd:.9f} vs oracle {an:.9f}"
+
+
+def pin_p18_pro_finite_differences(ora, B=1, H=2, L=5, d=3, seed=18):
+    """Prologue and output-gate gradients against central finite differences."""
+    t = [_rand((B, H, L, d), seed + i) for i in range(3)]
+    ka, va = _rand((B, H, L), seed + 3), _rand((B, H, L), seed + 4)
+    wq, wk = _rand((H, d), seed + 5), _rand((H, d), seed + 6)
+    dq, dk, dv = (_rand((B, H, L, d), seed + 7 + i) for i in range(3))
+    eps = 0.05
+    grads = ora.pro_prologue_backward(t[0], t[1], t[2], ka, va, wq, wk, eps, dq, dk, dv)
+
+    def obj():
+        q, k, v = ora.pro_prologue(t[0], t[1], t[2], ka, va, wq, wk, eps)
+        return float((q * dq).sum() + (k * dk).sum() + (v * dv).sum())
+    for x, g, name in zip((t[0], t[1], t[2], ka, va, wq, wk), grads,
+                          ("dq_raw", "dk_raw", "dv_raw", "dk_shift", "dv_shift", "dwq", "dwk")):
+        _fd_check(obj, x, g, 1e-6, 1e-6, f"P18 {name}")
+    o, gl = _rand((B, H, L, d), seed + 10), _rand((B, H, L, d), seed + 11)
+    wo, dy = _rand((H, d), seed + 12), _rand((B, H, L, d), seed + 13)
+    do, dg, dw = ora.output_gate_backward(o, gl, wo, eps, dy)
+    obj2 = lambda: float((ora.output_gate(o, gl, wo, eps) * dy).sum())
+    for x, g, name in ((o, do, "do"), (gl, dg, "dg"), (wo, dw, "dwo")):
+        _fd_check(obj2, x, g, 1e-6, 1e-6, f"P18 {name}")
+
+
+def _autograd_pro_layer(qr, kr, vr, ka, va, wq, wk, lf, gl, wo, eps, s):
+    """The Pro layer written directly with differentiable torch ops."""
+    def norm(x, w):
+        return x * torch.rsqrt(x.pow(2).mean(-1, keepdim=True) + eps) * w[None, :, None, :]
+
+    def shift(x, logit):
+        a = torch.sigmoid(logit)[..., None]
+        prev = Fnn.pad(x, (0, 0, 1, 0))[..., :-1, :]
+        return a * prev + (1 - a) * x
+    q, k, v = norm(qr, wq), norm(shift(kr, ka), wk), shift(vr, va)
+    L = q.shape[-2]
+    c = torch.cumsum(lf, -1)
+    Dm = (c[..., :, None] - c[..., None, :]).masked_fill(
+        torch.ones(L, L, dtype=torch.bool).triu(1), -math.inf)
+    O = torch.softmax(s * q @ k.transpose(-1, -2) + Dm, -1) @ v
+    return norm(O, wo) * torch.sigmoid(gl)
+
+
+def pin_p18_pro_autograd(ora, B=2, H=2, L=13, d=6, seed=28):
+    """torch autograd of an independently written Pro layer equals the oracle's
+    prologue -> attention -> epilogue forward and hand-derived backward chain."""
+    leaves = [_rand((B, H, L, d), seed), _rand((B, H, L, d), seed + 1), _rand((B, H, L, d), seed + 2),
+              _rand((B, H, L), seed + 3), _rand((B, H, L), seed + 4), _rand((H, d), seed + 5),
+              _rand((H, d), seed + 6), -torch.rand(B, H, L, generator=torch.Generator().manual_seed(seed),
+                                                   dtype=F64), _rand((B, H, L, d), seed + 7),
+              _rand((H, d), seed + 8)]
+    eps, s = 1e-3, 0.4
+    dy = _rand((B, H, L, d), seed + 9)
+    lv = [x.clone().requires_grad_(True) for x in leaves]
+    y = _autograd_pro_layer(*lv, eps, s)
+    ag = torch.autograd.grad((y * dy).sum(), lv)
+    qr, kr, vr, ka, va, wq, wk, lf, gl, wo = leaves
+    q, k, v = ora.pro_prologue(qr, kr, vr, ka, va, wq, wk, eps)
+    O, _ = ora.forward_from_logf(q, k, v, lf, s)
+    _close(ora.output_gate(O, gl, wo, eps), y.detach(), 1e-12, "P18 Pro forward")
+    dO, dg, dwo = ora.output_gate_backward(O, gl, wo, eps, dy)
+    dq, dk, dv, dlf = ora.backward_from_logf(q, k, v, lf, dO, s)
+    pg = ora.pro_prologue_backward(qr, kr, vr, ka, va, wq, wk, eps, dq, dk, dv)
+    mine = list(pg[:5]) + [pg[5], pg[6], dlf, dg, dwo]
+    names = ("dq_raw", "dk_raw", "dv_raw", "dk_shift", "dv_shift", "dwq", "dwk", "dlogf", "dg", "dwo")
+    for a, b, name in zip(ag, mine, names):
+        _close(b, a, 1e-10, f"P18 autograd {name}")
+
+
+# --------------------------------------------------------------------------- P19
+def pin_p19_output_gate_limits(ora, B=1, H=3, L=6, d=5, seed=29):
+    """Saturated gate: y = RMSNorm(o) and d g = 0; zero logit: y = RMSNorm(o) / 2."""
+    o, dy = _rand((B, H, L, d), seed), _rand((B, H, L, d), seed + 1)
+    wo = _rand((H, d), seed + 2)
+    n, _ = ora.rms_norm(o, wo, 1e-6)
+    big = torch.full((B, H, L, d), 1e4, dtype=F64)
+    _close(ora.output_gate(o, big, wo, 1e-6), n, 1e-12, "P19 open gate")
+    _close(ora.output_gate(o, 0 * big, wo, 1e-6), 0.5 * n, 1e-12, "P19 half gate")
+    _, dg, _ = ora.output_gate_backward(o, big, wo, 1e-6, dy)
+    _close(dg, torch.zeros_like(dg), 0.0, "P19 saturated gate gradient")
+    do, _, _ = ora.output_gate_backward(o, -big, wo, 1e-6, dy)
+    _close(do, torch.zeros_like(do), 0.0, "P19 closed gate passes no gradient to o")
+
+
 ALL_PINS = [
     pin_p1_zero_forgetting_is_softmax_attention,
     pin_p2_full_forgetting,
@@ -436,4 +591,9 @@ ALL_PINS = [
     pin_p15_fixed_gate_init_worked_example,
     pin_p15_fixed_gate_is_alibi_with_init_slopes,
     pin_p15_fixed_gate_bias_gradient,
+    pin_p16_rms_norm,
+    pin_p17_token_shift_limits,
+    pin_p18_pro_finite_differences,
+    pin_p18_pro_autograd,
+    pin_p19_output_gate_limits,
 ]

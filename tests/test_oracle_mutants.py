@@ -137,6 +137,76 @@ def _m_fixed_db_no_gate_factor(m):
     m.backward_fixed_gate = bwd
 
 
+def _m_rms_sum_not_mean(m):
+    """RMSNorm divides by the root of the sum of squares instead of the mean."""
+    def rn(x, weight, eps):
+        x = m._f64(x)
+        r = 1.0 / torch.sqrt((x * x).sum(dim=-1) + eps)
+        return x * r[..., None] * m._head_weight(weight, x.dim()), r
+    m.rms_norm = rn
+
+
+def _m_rms_bwd_no_projection(m):
+    """RMSNorm backward without the component along n."""
+    def rb(x, weight, eps, dy):
+        x, dy = m._f64(x), m._f64(dy)
+        _, r = m.rms_norm(x, weight, eps)
+        n = x * r[..., None]
+        dx = r[..., None] * dy * m._head_weight(weight, x.dim())
+        dw = (dy * n).sum(dim=-2)
+        return dx, (dw.sum(dim=0) if dw.dim() == 3 else dw)
+    m.rms_norm_backward = rb
+
+
+def _m_shift_from_next(m):
+    """The token shift mixes with the next token instead of the previous one."""
+    def ts(x, logit):
+        x = m._f64(x)
+        a = torch.sigmoid(m._f64(logit))[..., None]
+        nxt = torch.zeros_like(x)
+        nxt[..., :-1, :] = x[..., 1:, :]
+        return a * nxt + (1.0 - a) * x
+    m.token_shift = ts
+
+
+def _m_shift_bwd_no_next_term(m):
+    """Token-shift backward forgetting that x_t also feeds output t + 1."""
+    orig = m.token_shift_backward
+    def tb(x, logit, dy):
+        dx, dl = orig(x, logit, dy)
+        a = torch.sigmoid(m._f64(logit))
+        return (1.0 - a)[..., None] * m._f64(dy), dl
+    m.token_shift_backward = tb
+
+
+def _m_shift_logit_sign(m):
+    orig = m.token_shift_backward
+    def tb(x, logit, dy):
+        dx, dl = orig(x, logit, dy)
+        return dx, -dl
+    m.token_shift_backward = tb
+
+
+def _m_gate_bwd_no_derivative(m):
+    """Output-gate backward using sigmoid(g) in place of its derivative."""
+    def ob(o, g, w, eps, dy):
+        dy = m._f64(dy)
+        sg = torch.sigmoid(m._f64(g))
+        u, _ = m.rms_norm(o, w, eps)
+        do, dw = m.rms_norm_backward(o, w, eps, dy * sg)
+        return do, dy * u * sg, dw
+    m.output_gate_backward = ob
+
+
+def _m_head_weight_first_row(m):
+    """Every head normalised with head 0's weight row."""
+    def hw(weight, ndim):
+        w = m._f64(weight)
+        w = w[:1].expand_as(w)
+        return w.reshape((1,) * (ndim - 3) + (w.shape[0], 1, w.shape[1]))
+    m._head_weight = hw
+
+
 MUTANTS = {
     "decay_scaled": _m_scale_on_D,
     "exclusive_prefix": _m_exclusive_c,
@@ -155,6 +225,13 @@ MUTANTS = {
     "gate_factor_sign": _m_gate_factor_sign,
     "init_linear_spacing": _m_init_linear_spacing,
     "fixed_db_no_gate_factor": _m_fixed_db_no_gate_factor,
+    "rms_sum_not_mean": _m_rms_sum_not_mean,
+    "rms_bwd_no_projection": _m_rms_bwd_no_projection,
+    "shift_from_next": _m_shift_from_next,
+    "shift_bwd_no_next_term": _m_shift_bwd_no_next_term,
+    "shift_logit_sign": _m_shift_logit_sign,
+    "gate_bwd_no_derivative": _m_gate_bwd_no_derivative,
+    "head_weight_first_row": _m_head_weight_first_row,
 }
 
 
