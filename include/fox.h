@@ -52,7 +52,8 @@ typedef enum {
   FOX_ERR_UNSUPPORTED = 3,  /* unsupported dtype or head dim                       */
   FOX_ERR_ALIGN = 4,        /* a pointer is not 16-byte aligned                    */
   FOX_ERR_WORKSPACE = 5,    /* workspace missing or smaller than required          */
-  FOX_ERR_HIP = 6           /* the HIP runtime reported an error at launch         */
+  FOX_ERR_HIP = 6,          /* the HIP runtime reported an error at launch         */
+  FOX_ERR_VALUE = 7         /* a scalar argument out of range (eps: finite, >= 0)  */
 } fox_status_t;
 
 /* Human-readable name of a status code.  Never returns NULL. */
@@ -250,6 +251,67 @@ int fox_attn_decode_fixed_gate(int dtype, const void* q, const void* k_cache,
                                const void* v_cache, const float* gate_bias, void* o, float* lse,
                                void* workspace, size_t workspace_bytes, int B, int H, int T, int d,
                                float scale, void* stream);
+
+/*
+ * FoX (Pro) prologue and epilogue (Sec. 3 "Architecture design", Eq. shift-linear;
+ * appendix "Detailed FoX (Pro) layer computation").  Per head h and time t, from
+ * the raw projections q~ = W_q x, k~ = W_k x, v~ = W_v x (already split into
+ * heads, [B,H,L,d] in dtype) and the shift logits w_k^T x_t, w_v^T x_t ([B,H,L]
+ * fp32, one per head and token):
+ *     q_t = RMSNorm_q(q~_t)
+ *     k_t = RMSNorm_k(a_t k~_{t-1} + (1 - a_t) k~_t),   a_t = sigmoid(k_shift_logit_t)
+ *     v_t = b_t v~_{t-1} + (1 - b_t) v~_t,              b_t = sigmoid(v_shift_logit_t)
+ * with k~_0 = v~_0 = 0 (the first token mixes with zeros), and after the attention
+ *     y_t = RMSNorm_o(o_t) o sigmoid(g_t),   g = W_g x ([B,H,L,d] in dtype).
+ * RMSNorm(x) = x / sqrt(mean over d of x^2 + eps) * w^(h), with per-head weights
+ * [H,d] fp32 (a weight shared by all heads, as in the paper's runs, is H equal
+ * rows).  eps must be finite and >= 0 (else FOX_ERR_VALUE).  The projections
+ * and W_o are ordinary matrix products and not part of this library.  Outputs
+ * must not alias inputs (rows t - 1 and t + 1 are read while row t is written).
+ *
+ * fox_pro_prologue: q, k, v for the attention entry points.
+ * fox_pro_prologue_bwd: from dq, dk, dv (of the attention backward) the
+ *   gradients of the raw projections (dtype), of the shift logits ([B,H,L]
+ *   fp32) and of the QK-norm weights ([H,d] fp32, summed over batch and time).
+ *   workspace: at least fox_pro_prologue_bwd_workspace_bytes().
+ * fox_pro_output_gate: y from an attention output o (standalone epilogue).
+ * fox_attn_fwd_pro: fox_attn_fwd followed by the output norm and gate: writes
+ *   o and lse (the backward needs them) and y.  bf16 applies the norm and gate
+ *   in the attention kernel's epilogue, to o as rounded to bf16; fp32 runs the
+ *   standalone epilogue kernel after the attention.
+ * fox_attn_bwd_pro: gradients of sum(y o dy): dq, dk, dv, d_log_f as
+ *   fox_attn_bwd, the gate-logit gradient dg_logit (dtype, [B,H,L,d]) and the
+ *   output-norm weight gradient do_norm_weight ([H,d] fp32).  The norm/gate
+ *   backward also forms dO (rounded to dtype) and Delta_i = rowsum(dO o O) for
+ *   the attention backward, in the workspace: at least
+ *   fox_attn_bwd_pro_workspace_bytes().
+ */
+int fox_pro_prologue(int dtype, const void* q_raw, const void* k_raw, const void* v_raw,
+                     const float* k_shift_logit, const float* v_shift_logit,
+                     const float* q_norm_weight, const float* k_norm_weight, float eps, void* q,
+                     void* k, void* v, int B, int H, int L, int d, void* stream);
+size_t fox_pro_prologue_bwd_workspace_bytes(int dtype, int B, int H, int L, int d);
+int fox_pro_prologue_bwd(int dtype, const void* q_raw, const void* k_raw, const void* v_raw,
+                         const float* k_shift_logit, const float* v_shift_logit,
+                         const float* q_norm_weight, const float* k_norm_weight, float eps,
+                         const void* dq, const void* dk, const void* dv, void* dq_raw,
+                         void* dk_raw, void* dv_raw, float* dk_shift_logit,
+                         float* dv_shift_logit, float* dq_norm_weight, float* dk_norm_weight,
+                         void* workspace, size_t workspace_bytes, int B, int H, int L, int d,
+                         void* stream);
+int fox_pro_output_gate(int dtype, const void* o, const void* g_logit,
+                        const float* o_norm_weight, float eps, void* y, int B, int H, int L,
+                        int d, void* stream);
+int fox_attn_fwd_pro(int dtype, const void* q, const void* k, const void* v, const float* c,
+                     const void* g_logit, const float* o_norm_weight, float eps, void* o,
+                     float* lse, void* y, int B, int H, int L, int d, float scale, void* stream);
+size_t fox_attn_bwd_pro_workspace_bytes(int dtype, int B, int H, int L, int d);
+int fox_attn_bwd_pro(int dtype, const void* q, const void* k, const void* v, const float* c,
+                     const void* o, const float* lse, const void* g_logit,
+                     const float* o_norm_weight, float eps, const void* dy, void* dq, void* dk,
+                     void* dv, float* d_log_f, void* dg_logit, float* do_norm_weight,
+                     void* workspace, size_t workspace_bytes, int B, int H, int L, int d,
+                     float scale, void* stream);
 
 #ifdef __cplusplus
 }

@@ -30,6 +30,9 @@ EXPORTED = (
     "fox_fixed_gate_init", "fox_attn_fwd_fixed_gate", "fox_attn_bwd_fixed_gate_workspace_bytes",
     "fox_attn_bwd_fixed_gate", "fox_attn_decode_fixed_gate",
     "fox_row_norm_max", "fox_attn_decode_skip", "fox_attn_fwd_skip", "fox_attn_bwd_skip",
+    "fox_pro_prologue", "fox_pro_prologue_bwd_workspace_bytes", "fox_pro_prologue_bwd",
+    "fox_pro_output_gate", "fox_attn_fwd_pro", "fox_attn_bwd_pro_workspace_bytes",
+    "fox_attn_bwd_pro",
 )
 
 
@@ -99,6 +102,22 @@ def load() -> ctypes.CDLL:
                                       F, P]
     lib.fox_attn_decode_skip.restype = I
     lib.fox_attn_decode_skip.argtypes = [I, P, P, P, P, P, P, P, P, P, Z, I, I, I, I, F, P]
+    lib.fox_pro_prologue.restype = I
+    lib.fox_pro_prologue.argtypes = [I, P, P, P, P, P, P, P, F, P, P, P, I, I, I, I, P]
+    lib.fox_pro_prologue_bwd_workspace_bytes.restype = Z
+    lib.fox_pro_prologue_bwd_workspace_bytes.argtypes = [I, I, I, I, I]
+    lib.fox_pro_prologue_bwd.restype = I
+    lib.fox_pro_prologue_bwd.argtypes = [I, P, P, P, P, P, P, P, F, P, P, P, P, P, P, P, P, P, P,
+                                         P, Z, I, I, I, I, P]
+    lib.fox_pro_output_gate.restype = I
+    lib.fox_pro_output_gate.argtypes = [I, P, P, P, F, P, I, I, I, I, P]
+    lib.fox_attn_fwd_pro.restype = I
+    lib.fox_attn_fwd_pro.argtypes = [I, P, P, P, P, P, P, F, P, P, P, I, I, I, I, F, P]
+    lib.fox_attn_bwd_pro_workspace_bytes.restype = Z
+    lib.fox_attn_bwd_pro_workspace_bytes.argtypes = [I, I, I, I, I]
+    lib.fox_attn_bwd_pro.restype = I
+    lib.fox_attn_bwd_pro.argtypes = [I, P, P, P, P, P, P, P, P, F, P, P, P, P, P, P, P, P, Z, I, I,
+                                     I, I, F, P]
     _lib = lib
     return lib
 
@@ -556,3 +575,135 @@ def fox_attn_bwd_skip(q, k, v, c, o, lse, d_o, q_norm_max, k_norm_max,
                                   B, H, L, d, s, _stream(q))
     _raise(st, "fox_attn_bwd_skip")
     return dq, dk, dv, d_log_f
+
+
+# ---------------------------------------------------------------------------
+# FoX (Pro) prologue and epilogue
+# ---------------------------------------------------------------------------
+def _pro_shapes(x, name="q_raw"):
+    B, H, L, d = x.shape
+    dt = x.dtype
+    if dt not in _DT:
+        raise ValueError(f"unsupported dtype {dt}")
+    return B, H, L, d, dt, x.device
+
+
+def fox_pro_prologue(q_raw, k_raw, v_raw, k_shift_logit, v_shift_logit, q_norm_weight,
+                     k_norm_weight, eps: float = 1e-6, q=None, k=None, v=None):
+    """q = RMSNorm(q_raw), k = RMSNorm(shift(k_raw)), v = shift(v_raw) (FoX Pro)."""
+    B, H, L, d, dt, dev = _pro_shapes(q_raw)
+    for name, t in (("q_raw", q_raw), ("k_raw", k_raw), ("v_raw", v_raw)):
+        _check(t, name, (B, H, L, d), dt, dev)
+    for name, t in (("k_shift_logit", k_shift_logit), ("v_shift_logit", v_shift_logit)):
+        _check(t, name, (B, H, L), torch.float32, dev)
+    for name, t in (("q_norm_weight", q_norm_weight), ("k_norm_weight", k_norm_weight)):
+        _check(t, name, (H, d), torch.float32, dev)
+    q = torch.empty_like(q_raw) if q is None else q
+    k = torch.empty_like(k_raw) if k is None else k
+    v = torch.empty_like(v_raw) if v is None else v
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _check(t, name, (B, H, L, d), dt, dev)
+    st = load().fox_pro_prologue(_DT[dt], _ptr(q_raw), _ptr(k_raw), _ptr(v_raw),
+                                 _ptr(k_shift_logit), _ptr(v_shift_logit), _ptr(q_norm_weight),
+                                 _ptr(k_norm_weight), float(eps), _ptr(q), _ptr(k), _ptr(v),
+                                 B, H, L, d, _stream(q_raw))
+    _raise(st, "fox_pro_prologue")
+    return q, k, v
+
+
+def fox_pro_prologue_bwd_workspace_bytes(dtype: torch.dtype, B: int, H: int, L: int,
+                                         d: int) -> int:
+    return int(load().fox_pro_prologue_bwd_workspace_bytes(_DT[dtype], B, H, L, d))
+
+
+def fox_pro_prologue_bwd(q_raw, k_raw, v_raw, k_shift_logit, v_shift_logit, q_norm_weight,
+                         k_norm_weight, dq, dk, dv, eps: float = 1e-6, workspace=None):
+    """Gradients (dq_raw, dk_raw, dv_raw, dk_shift_logit, dv_shift_logit,
+    dq_norm_weight, dk_norm_weight) of the prologue from dq, dk, dv."""
+    B, H, L, d, dt, dev = _pro_shapes(q_raw)
+    for name, t in (("q_raw", q_raw), ("k_raw", k_raw), ("v_raw", v_raw), ("dq", dq),
+                    ("dk", dk), ("dv", dv)):
+        _check(t, name, (B, H, L, d), dt, dev)
+    for name, t in (("k_shift_logit", k_shift_logit), ("v_shift_logit", v_shift_logit)):
+        _check(t, name, (B, H, L), torch.float32, dev)
+    for name, t in (("q_norm_weight", q_norm_weight), ("k_norm_weight", k_norm_weight)):
+        _check(t, name, (H, d), torch.float32, dev)
+    dqr, dkr, dvr = (torch.empty_like(q_raw) for _ in range(3))
+    dka, dva = torch.empty_like(k_shift_logit), torch.empty_like(v_shift_logit)
+    dwq, dwk = torch.empty_like(q_norm_weight), torch.empty_like(k_norm_weight)
+    need = fox_pro_prologue_bwd_workspace_bytes(dt, B, H, L, d)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), device=dev, dtype=torch.uint8)
+    st = load().fox_pro_prologue_bwd(_DT[dt], _ptr(q_raw), _ptr(k_raw), _ptr(v_raw),
+                                     _ptr(k_shift_logit), _ptr(v_shift_logit),
+                                     _ptr(q_norm_weight), _ptr(k_norm_weight), float(eps),
+                                     _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dqr), _ptr(dkr),
+                                     _ptr(dvr), _ptr(dka), _ptr(dva), _ptr(dwq), _ptr(dwk),
+                                     _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                     B, H, L, d, _stream(q_raw))
+    _raise(st, "fox_pro_prologue_bwd")
+    return dqr, dkr, dvr, dka, dva, dwq, dwk
+
+
+def fox_pro_output_gate(o, g_logit, o_norm_weight, eps: float = 1e-6, y=None):
+    """y = RMSNorm(o) * sigmoid(g_logit)."""
+    B, H, L, d, dt, dev = _pro_shapes(o)
+    _check(g_logit, "g_logit", (B, H, L, d), dt, dev)
+    _check(o_norm_weight, "o_norm_weight", (H, d), torch.float32, dev)
+    y = torch.empty_like(o) if y is None else y
+    _check(y, "y", (B, H, L, d), dt, dev)
+    st = load().fox_pro_output_gate(_DT[dt], _ptr(o), _ptr(g_logit), _ptr(o_norm_weight),
+                                    float(eps), _ptr(y), B, H, L, d, _stream(o))
+    _raise(st, "fox_pro_output_gate")
+    return y
+
+
+def fox_attn_fwd_pro(q, k, v, c, g_logit, o_norm_weight, scale: Optional[float] = None,
+                     eps: float = 1e-6, o=None, lse=None, y=None):
+    """Attention with the output norm and gate: returns (y, o, lse)."""
+    B, H, L, d, dt, dev = _pro_shapes(q)
+    for name, t in (("q", q), ("k", k), ("v", v), ("g_logit", g_logit)):
+        _check(t, name, (B, H, L, d), dt, dev)
+    _check(c, "c", (B, H, L), torch.float32, dev)
+    _check(o_norm_weight, "o_norm_weight", (H, d), torch.float32, dev)
+    o = torch.empty_like(q) if o is None else o
+    y = torch.empty_like(q) if y is None else y
+    lse = torch.empty((B, H, L), device=dev, dtype=torch.float32) if lse is None else lse
+    _check(o, "o", (B, H, L, d), dt, dev)
+    _check(y, "y", (B, H, L, d), dt, dev)
+    _check(lse, "lse", (B, H, L), torch.float32, dev)
+    s = default_scale(d) if scale is None else float(scale)
+    st = load().fox_attn_fwd_pro(_DT[dt], _ptr(q), _ptr(k), _ptr(v), _ptr(c), _ptr(g_logit),
+                                 _ptr(o_norm_weight), float(eps), _ptr(o), _ptr(lse), _ptr(y),
+                                 B, H, L, d, s, _stream(q))
+    _raise(st, "fox_attn_fwd_pro")
+    return y, o, lse
+
+
+def fox_attn_bwd_pro_workspace_bytes(dtype: torch.dtype, B: int, H: int, L: int, d: int) -> int:
+    return int(load().fox_attn_bwd_pro_workspace_bytes(_DT[dtype], B, H, L, d))
+
+
+def fox_attn_bwd_pro(q, k, v, c, o, lse, g_logit, o_norm_weight, dy,
+                     scale: Optional[float] = None, eps: float = 1e-6, workspace=None):
+    """Gradients of sum(y * dy): (dq, dk, dv, d_log_f, dg_logit, do_norm_weight)."""
+    B, H, L, d, dt, dev = _pro_shapes(q)
+    for name, t in (("q", q), ("k", k), ("v", v), ("o", o), ("g_logit", g_logit), ("dy", dy)):
+        _check(t, name, (B, H, L, d), dt, dev)
+    _check(c, "c", (B, H, L), torch.float32, dev)
+    _check(lse, "lse", (B, H, L), torch.float32, dev)
+    _check(o_norm_weight, "o_norm_weight", (H, d), torch.float32, dev)
+    dq, dk, dv, dg = (torch.empty_like(q) for _ in range(4))
+    dlf = torch.empty_like(c)
+    dw = torch.empty_like(o_norm_weight)
+    need = fox_attn_bwd_pro_workspace_bytes(dt, B, H, L, d)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), device=dev, dtype=torch.uint8)
+    s = default_scale(d) if scale is None else float(scale)
+    st = load().fox_attn_bwd_pro(_DT[dt], _ptr(q), _ptr(k), _ptr(v), _ptr(c), _ptr(o), _ptr(lse),
+                                 _ptr(g_logit), _ptr(o_norm_weight), float(eps), _ptr(dy),
+                                 _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dlf), _ptr(dg), _ptr(dw),
+                                 _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                 B, H, L, d, s, _stream(q))
+    _raise(st, "fox_attn_bwd_pro")
+    return dq, dk, dv, dlf, dg, dw

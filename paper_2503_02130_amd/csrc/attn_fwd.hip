@@ -75,13 +75,18 @@ struct FwdSmem {
 // log2(e) (2 s Qmax Kmax + c_q0 - c_jl) < -kSkipMargin the tile (and, as c
 // falls along the sequence, every earlier tile) adds exact zeros: the loop
 // stops there and the results equal the dense kernel's bit for bit.
-template <int D, bool FIXED, bool SKIP>
+//
+// OUTG: the FoX (Pro) output norm and gate in the epilogue (appendix, FoX (Pro)
+// layer computation): y = RMSNorm(o) o sigmoid(g) per query row, from the row
+// as rounded to bf16 for O (the backward normalises the stored O the same way).
+// A lane holds half of its row; the other half is in lane l ^ 32.
+template <int D, bool FIXED, bool SKIP, bool OUTG = false>
 __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
                      const bf16* __restrict__ V, const float* __restrict__ gate,
                      const float* __restrict__ qnorm, const float* __restrict__ knorm,
                      bf16* __restrict__ O, float* __restrict__ LSE, int BH, int H, int L,
-                     int n_mblk, float scale_log2) {
+                     int n_mblk, float scale_log2, OutGateArgs og) {
   constexpr int TILE = kFwdBN * D;                         // bf16 elements per tile
   constexpr int NDMA = TILE * 2 / 1024 / kFwdWaves;        // 1 KB DMA loads per wave per tile
   __shared__ __attribute__((aligned(16))) FwdSmem<D> sm;
@@ -309,7 +314,44 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
   }
 
   const float l_tot = wave_sum_pair(l_run);
-  if (q_valid) {
+  if constexpr (OUTG) {
+    const float inv = 1.0f / l_tot;
+    bf16x4 ob[D / 32][4];
+    float ss = 0.0f;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          ob[db][g][jj] = to_bf16(oacc[db][4 * g + jj] * inv);
+          const float x = to_f32(ob[db][g][jj]);
+          ss += x * x;
+        }
+    ss += __shfl_xor(ss, 32);
+    if (q_valid) {
+      const float r = 1.0f / sqrtf(ss * (1.0f / D) + og.eps);
+      const size_t roff = (head + (size_t)qi) * D;
+      const float* w = og.w + (size_t)(bh % og.heads) * D;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int e = db * 32 + 8 * g + 4 * h;
+          *reinterpret_cast<bf16x4*>(O + roff + e) = ob[db][g];
+          const bf16x4 gv = *reinterpret_cast<const bf16x4*>(og.g + roff + e);
+          const f32x4 wv = *reinterpret_cast<const f32x4*>(w + e);
+          bf16x4 y;
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj)
+            y[jj] = to_bf16(to_f32(ob[db][g][jj]) * r * wv[jj] /
+                            (1.0f + expf(-to_f32(gv[jj]))));
+          *reinterpret_cast<bf16x4*>(og.y + roff + e) = y;
+        }
+      }
+      if (h == 0) LSE[head + qi] = gr.diff(qi, q0) + kLn2 * (m_used + log2f(l_tot));
+    }
+  } else if (q_valid) {
     const float inv = 1.0f / l_tot;
     bf16* orow = O + (head + (size_t)qi) * D;
 #pragma unroll
@@ -416,7 +458,7 @@ static void fwd_bf16_t(const void* q, const void* k, const void* v, GateSpec g,
   const dim3 grid((unsigned)n_mblk * (unsigned)BH);
   hipLaunchKernelGGL((fwd_bf16_kernel<D, FIXED, SKIP>), grid, dim3(kFwdThreads), 0, s,
                      (const bf16*)q, (const bf16*)k, (const bf16*)v, g.ptr, qn, kn, (bf16*)o, lse,
-                     BH, g.H, L, n_mblk, sl2);
+                     BH, g.H, L, n_mblk, sl2, OutGateArgs{});
 }
 
 template <int D, bool FIXED>
@@ -440,6 +482,26 @@ hipError_t launch_fwd_bf16(const void* q, const void* k, const void* v, GateSpec
     if (g.fixed) fwd_bf16_s<64, true>(q, k, v, g, qn, kn, o, lse, BH, L, sl2, s);
     else fwd_bf16_s<64, false>(q, k, v, g, qn, kn, o, lse, BH, L, sl2, s);
   }
+  return hipGetLastError();
+}
+
+template <int D>
+static void fwd_bf16_outg_t(const void* q, const void* k, const void* v, const float* c, void* o,
+                            float* lse, OutGateArgs og, int BH, int L, float sl2, hipStream_t s) {
+  const int n_mblk = (L + kFwdBM - 1) / kFwdBM;
+  const dim3 grid((unsigned)n_mblk * (unsigned)BH);
+  hipLaunchKernelGGL((fwd_bf16_kernel<D, false, false, true>), grid, dim3(kFwdThreads), 0, s,
+                     (const bf16*)q, (const bf16*)k, (const bf16*)v, c, nullptr, nullptr,
+                     (bf16*)o, lse, BH, 1, L, n_mblk, sl2, og);
+}
+
+hipError_t launch_fwd_bf16_out_gate(const void* q, const void* k, const void* v, const float* c,
+                                    void* o, float* lse, const void* g, const float* wo,
+                                    float eps, void* y, int H, int BH, int L, int d, float scale,
+                                    hipStream_t s) {
+  const OutGateArgs og{static_cast<const bf16*>(g), wo, eps, static_cast<bf16*>(y), H};
+  if (d == 128) fwd_bf16_outg_t<128>(q, k, v, c, o, lse, og, BH, L, scale * kLog2e, s);
+  else fwd_bf16_outg_t<64>(q, k, v, c, o, lse, og, BH, L, scale * kLog2e, s);
   return hipGetLastError();
 }
 

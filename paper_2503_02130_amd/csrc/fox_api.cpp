@@ -5,6 +5,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <initializer_list>
+
 #include "fox.h"
 #include "fox_internal.h"
 
@@ -34,6 +36,20 @@ int check_dtype_d(int dtype, int d) {
 
 int launch_status(hipError_t e) { return e == hipSuccess ? FOX_OK : FOX_ERR_HIP; }
 
+bool valid_eps(float eps) { return isfinite(eps) && eps >= 0.0f; }
+
+bool all_aligned16(std::initializer_list<const void*> ps) {
+  for (const void* p : ps)
+    if (!aligned16(p)) return false;
+  return true;
+}
+
+bool all_set(std::initializer_list<const void*> ps) {
+  for (const void* p : ps)
+    if (!p) return false;
+  return true;
+}
+
 }  // namespace
 
 extern "C" {
@@ -47,6 +63,7 @@ const char* fox_status_string(int status) {
     case FOX_ERR_ALIGN: return "FOX_ERR_ALIGN: device pointers must be 16-byte aligned";
     case FOX_ERR_WORKSPACE: return "FOX_ERR_WORKSPACE: workspace missing or too small";
     case FOX_ERR_HIP: return "FOX_ERR_HIP: the HIP runtime reported a launch error";
+    case FOX_ERR_VALUE: return "FOX_ERR_VALUE: a scalar argument is out of range (eps: finite, >= 0)";
     default: return "unknown fox status";
   }
 }
@@ -358,6 +375,134 @@ int fox_attn_decode_fixed_gate(int dtype, const void* q, const void* k_cache,
   return launch_status(fox::launch_decode_fixed(dtype == FOX_DTYPE_BF16, q, k_cache, v_cache,
                                                 gate_bias, H, o, lse, workspace, B * H, T, d, scale,
                                                 static_cast<hipStream_t>(stream)));
+}
+
+// ---------------------------------------------------------------------------
+// FoX (Pro) prologue and epilogue
+// ---------------------------------------------------------------------------
+int fox_pro_prologue(int dtype, const void* q_raw, const void* k_raw, const void* v_raw,
+                     const float* k_shift_logit, const float* v_shift_logit,
+                     const float* q_norm_weight, const float* k_norm_weight, float eps, void* q,
+                     void* k, void* v, int B, int H, int L, int d, void* stream) {
+  if (!all_set({q_raw, k_raw, v_raw, k_shift_logit, v_shift_logit, q_norm_weight, k_norm_weight,
+                q, k, v}))
+    return FOX_ERR_NULL;
+  int st = check_dims(B, H, L, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (!valid_eps(eps)) return FOX_ERR_VALUE;
+  if (!all_aligned16({q_raw, k_raw, v_raw, k_shift_logit, v_shift_logit, q_norm_weight,
+                      k_norm_weight, q, k, v}))
+    return FOX_ERR_ALIGN;
+  return launch_status(fox::launch_pro_prologue(
+      dtype == FOX_DTYPE_BF16, q_raw, k_raw, v_raw, k_shift_logit, v_shift_logit, q_norm_weight,
+      k_norm_weight, eps, q, k, v, H, B * H, L, d, static_cast<hipStream_t>(stream)));
+}
+
+size_t fox_pro_prologue_bwd_workspace_bytes(int dtype, int B, int H, int L, int d) {
+  if (check_dims(B, H, L, d) || check_dtype_d(dtype, d)) return 0;
+  return fox::pro_prologue_bwd_workspace_bytes(B * H, L, d);
+}
+
+int fox_pro_prologue_bwd(int dtype, const void* q_raw, const void* k_raw, const void* v_raw,
+                         const float* k_shift_logit, const float* v_shift_logit,
+                         const float* q_norm_weight, const float* k_norm_weight, float eps,
+                         const void* dq, const void* dk, const void* dv, void* dq_raw,
+                         void* dk_raw, void* dv_raw, float* dk_shift_logit,
+                         float* dv_shift_logit, float* dq_norm_weight, float* dk_norm_weight,
+                         void* workspace, size_t workspace_bytes, int B, int H, int L, int d,
+                         void* stream) {
+  if (!all_set({q_raw, k_raw, v_raw, k_shift_logit, v_shift_logit, q_norm_weight, k_norm_weight,
+                dq, dk, dv, dq_raw, dk_raw, dv_raw, dk_shift_logit, dv_shift_logit,
+                dq_norm_weight, dk_norm_weight}))
+    return FOX_ERR_NULL;
+  int st = check_dims(B, H, L, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (!valid_eps(eps)) return FOX_ERR_VALUE;
+  if (!all_aligned16({q_raw, k_raw, v_raw, k_shift_logit, v_shift_logit, q_norm_weight,
+                      k_norm_weight, dq, dk, dv, dq_raw, dk_raw, dv_raw, dk_shift_logit,
+                      dv_shift_logit, dq_norm_weight, dk_norm_weight}))
+    return FOX_ERR_ALIGN;
+  if (!workspace || workspace_bytes < fox::pro_prologue_bwd_workspace_bytes(B * H, L, d))
+    return FOX_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return FOX_ERR_ALIGN;
+  return launch_status(fox::launch_pro_prologue_bwd(
+      dtype == FOX_DTYPE_BF16, q_raw, k_raw, v_raw, k_shift_logit, v_shift_logit, q_norm_weight,
+      k_norm_weight, eps, dq, dk, dv, dq_raw, dk_raw, dv_raw, dk_shift_logit, dv_shift_logit,
+      dq_norm_weight, dk_norm_weight, workspace, H, B * H, L, d,
+      static_cast<hipStream_t>(stream)));
+}
+
+int fox_pro_output_gate(int dtype, const void* o, const void* g_logit,
+                        const float* o_norm_weight, float eps, void* y, int B, int H, int L,
+                        int d, void* stream) {
+  if (!all_set({o, g_logit, o_norm_weight, y})) return FOX_ERR_NULL;
+  int st = check_dims(B, H, L, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (!valid_eps(eps)) return FOX_ERR_VALUE;
+  if (!all_aligned16({o, g_logit, o_norm_weight, y})) return FOX_ERR_ALIGN;
+  return launch_status(fox::launch_out_gate(dtype == FOX_DTYPE_BF16, o, g_logit, o_norm_weight,
+                                            eps, y, H, B * H, L, d,
+                                            static_cast<hipStream_t>(stream)));
+}
+
+int fox_attn_fwd_pro(int dtype, const void* q, const void* k, const void* v, const float* c,
+                     const void* g_logit, const float* o_norm_weight, float eps, void* o,
+                     float* lse, void* y, int B, int H, int L, int d, float scale, void* stream) {
+  if (!all_set({q, k, v, c, g_logit, o_norm_weight, o, lse, y})) return FOX_ERR_NULL;
+  int st = check_dims(B, H, L, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (!valid_eps(eps)) return FOX_ERR_VALUE;
+  if (!all_aligned16({q, k, v, c, g_logit, o_norm_weight, o, lse, y})) return FOX_ERR_ALIGN;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (dtype == FOX_DTYPE_BF16)
+    return launch_status(fox::launch_fwd_bf16_out_gate(q, k, v, c, o, lse, g_logit,
+                                                       o_norm_weight, eps, y, H, B * H, L, d,
+                                                       scale, s));
+  hipError_t e = fox::launch_fwd_f32((const float*)q, (const float*)k, (const float*)v,
+                                     fox::gate_array(c), (float*)o, lse, B * H, L, d, scale, s);
+  if (e == hipSuccess)
+    e = fox::launch_out_gate(false, o, g_logit, o_norm_weight, eps, y, H, B * H, L, d, s);
+  return launch_status(e);
+}
+
+size_t fox_attn_bwd_pro_workspace_bytes(int dtype, int B, int H, int L, int d) {
+  if (check_dims(B, H, L, d) || check_dtype_d(dtype, d)) return 0;
+  return fox::bwd_pro_workspace_bytes(dtype == FOX_DTYPE_BF16, B * H, L, d);
+}
+
+int fox_attn_bwd_pro(int dtype, const void* q, const void* k, const void* v, const float* c,
+                     const void* o, const float* lse, const void* g_logit,
+                     const float* o_norm_weight, float eps, const void* dy, void* dq, void* dk,
+                     void* dv, float* d_log_f, void* dg_logit, float* do_norm_weight,
+                     void* workspace, size_t workspace_bytes, int B, int H, int L, int d,
+                     float scale, void* stream) {
+  if (!all_set({q, k, v, c, o, lse, g_logit, o_norm_weight, dy, dq, dk, dv, d_log_f, dg_logit,
+                do_norm_weight}))
+    return FOX_ERR_NULL;
+  int st = check_dims(B, H, L, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (!valid_eps(eps)) return FOX_ERR_VALUE;
+  if (!all_aligned16({q, k, v, c, o, lse, g_logit, o_norm_weight, dy, dq, dk, dv, d_log_f,
+                      dg_logit, do_norm_weight}))
+    return FOX_ERR_ALIGN;
+  const bool bf = dtype == FOX_DTYPE_BF16;
+  if (!workspace || workspace_bytes < fox::bwd_pro_workspace_bytes(bf, B * H, L, d))
+    return FOX_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return FOX_ERR_ALIGN;
+  return launch_status(fox::launch_bwd_pro(bf, q, k, v, c, o, lse, g_logit, o_norm_weight, eps,
+                                           dy, dq, dk, dv, d_log_f, dg_logit, do_norm_weight,
+                                           workspace, H, B * H, L, d, scale,
+                                           static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

@@ -18,6 +18,17 @@ typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4_t;
 
 namespace fox {
 
+// Arguments of the FoX (Pro) output norm and gate fused into a forward epilogue:
+// gate logits g [BH, L, D] bf16, per-head weights w [heads, D] fp32, RMSNorm eps,
+// output y [BH, L, D] bf16.
+struct OutGateArgs {
+  const bf16* g;
+  const float* w;
+  float eps;
+  bf16* y;
+  int heads;
+};
+
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 

@@ -82,4 +82,34 @@ hipError_t launch_decode_fixed(bool bf16, const void* q, const void* k_cache, co
                                const float* bias, int H, void* o, float* lse, void* ws, int BH,
                                int T, int d, float scale, hipStream_t s);
 
+// FoX (Pro) prologue and epilogue (pro_fusions.hip).  Weights [H, d] fp32; shift
+// logits [BH, L] fp32; everything else [BH, L, d] in the storage type.
+int pro_chunks(int L);
+size_t pro_prologue_bwd_workspace_bytes(int BH, int L, int d);
+size_t bwd_pro_workspace_bytes(bool bf16, int BH, int L, int d);
+hipError_t launch_pro_prologue(bool bf16, const void* qr, const void* kr, const void* vr,
+                               const float* ka, const float* va, const float* wq,
+                               const float* wk, float eps, void* q, void* k, void* v, int H,
+                               int BH, int L, int d, hipStream_t s);
+hipError_t launch_pro_prologue_bwd(bool bf16, const void* qr, const void* kr, const void* vr,
+                                   const float* ka, const float* va, const float* wq,
+                                   const float* wk, float eps, const void* dq, const void* dk,
+                                   const void* dv, void* dqr, void* dkr, void* dvr, float* dka,
+                                   float* dva, float* dwq, float* dwk, void* ws, int H, int BH,
+                                   int L, int d, hipStream_t s);
+hipError_t launch_out_gate(bool bf16, const void* o, const void* g, const float* wo, float eps,
+                           void* y, int H, int BH, int L, int d, hipStream_t s);
+// bf16 forward with the output norm and gate in its epilogue (writes O, LSE and y)
+hipError_t launch_fwd_bf16_out_gate(const void* q, const void* k, const void* v, const float* c,
+                                    void* o, float* lse, const void* g, const float* wo,
+                                    float eps, void* y, int H, int BH, int L, int d, float scale,
+                                    hipStream_t s);
+// backward of attention + output norm and gate: the norm/gate backward writes dO
+// and Delta into the workspace, then the attention backward stages run
+hipError_t launch_bwd_pro(bool bf16, const void* q, const void* k, const void* v, const float* c,
+                          const void* o, const float* lse, const void* g, const float* wo,
+                          float eps, const void* dy, void* dq, void* dk, void* dv, float* d_log_f,
+                          void* dg, float* dwo, void* ws, int H, int BH, int L, int d, float scale,
+                          hipStream_t s);
+
 }  // namespace fox

@@ -124,6 +124,27 @@ def attn_inputs(B: int, H: int, L: int, d: int, dtype: str, gate: Tuple, seed: i
     return out
 
 
+def pro_inputs(B: int, H: int, L: int, d: int, dtype: str, gate: Tuple, seed: int,
+               device="cpu") -> Dict[str, torch.Tensor]:
+    """Inputs of a FoX (Pro) layer around the attention: raw projections q_raw,
+    k_raw, v_raw and the output-gate logits g [B,H,L,d] N(0,1) (dtype); the token
+    shift logits k_shift, v_shift [B,H,L] fp32 N(0, 2) (mix weights spread over
+    (0, 1)); per-head norm weights wq, wk, wo [H,d] fp32 1 + N(0, 0.1^2); the
+    forget-gate logits [B,H,L] by `gate`; upstream gradients dq, dk, dv, dy
+    [B,H,L,d] N(0,1) (dtype)."""
+    g = _gen(seed, device)
+    f32 = dict(generator=g, device=device, dtype=torch.float32)
+    out = {name: randn((B, H, L, d), dtype, g, device) for name in ("q_raw", "k_raw", "v_raw")}
+    out["k_shift"] = torch.randn((B, H, L), **f32) * 2.0
+    out["v_shift"] = torch.randn((B, H, L), **f32) * 2.0
+    for name in ("wq", "wk", "wo"):
+        out[name] = 1.0 + 0.1 * torch.randn((H, d), **f32)
+    out["logit"] = gate_logits(gate, B, H, L, g, device)
+    for name in ("g", "dq", "dk", "dv", "dy"):
+        out[name] = randn((B, H, L, d), dtype, g, device)
+    return out
+
+
 def decode_inputs(B: int, H: int, T: int, d: int, dtype: str, gate: Tuple, seed: int,
                   device="cpu") -> Dict[str, torch.Tensor]:
     """One decode step: q [B,H,d]; k_cache, v_cache [B,H,T,d] whose slot T-1 is

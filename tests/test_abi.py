@@ -42,8 +42,8 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_status_strings(lib):
-    for code in range(7):
-        assert lib.fox_status_string(code)
+    for code in range(8):
+        assert lib.fox_status_string(code) and b"unknown" not in lib.fox_status_string(code)
     assert b"unknown" in lib.fox_status_string(99)
     assert lib.fox_version() >= 100
 
@@ -125,6 +125,48 @@ def test_skip_validation(lib):
                                     None) == 1
     assert lib.fox_attn_decode_skip(1, *args, need - 1, 2, 3, 100, 64, f, None) == 5
     assert lib.fox_attn_decode_skip(1, *args, need, 2, 3, 0, 64, f, None) == 2
+
+
+def test_pro_validation_and_workspace(lib):
+    """FoX (Pro) entry points: NULLs, eps range, alignment, head dim, workspace."""
+    c = ctypes.c_void_p
+    f = ctypes.c_float
+    B, H, L, d = 2, 3, 600, 128
+    ok = [c(P16)] * 7
+    out = [c(P16)] * 3
+    assert lib.fox_pro_prologue(1, None, *ok[1:], f(1e-6), *out, B, H, L, d, None) == 1
+    assert lib.fox_pro_prologue(1, *ok, f(-1.0), *out, B, H, L, d, None) == 7
+    assert lib.fox_pro_prologue(1, *ok, f(float("inf")), *out, B, H, L, d, None) == 7
+    assert lib.fox_pro_prologue(1, *ok, f(float("nan")), *out, B, H, L, d, None) == 7
+    assert lib.fox_pro_prologue(1, *ok[:5], c(P16 + 4), ok[6], f(0.0), *out, B, H, L, d, None) == 4
+    assert lib.fox_pro_prologue(1, *ok, f(0.0), *out, B, H, L, 96, None) == 3
+    need = lib.fox_pro_prologue_bwd_workspace_bytes(1, B, H, L, d)
+    assert need == 2 * B * H * 3 * d * 4          # 3 chunks of 256 rows
+    assert lib.fox_pro_prologue_bwd_workspace_bytes(1, B, H, L, 80) == 0
+    grads = [c(P16)] * 10
+    assert lib.fox_pro_prologue_bwd(1, *ok, f(1e-6), *grads, c(P16), need - 1, B, H, L, d,
+                                    None) == 5
+    assert lib.fox_pro_prologue_bwd(1, *ok, f(1e-6), *grads, None, need, B, H, L, d, None) == 5
+    assert lib.fox_pro_prologue_bwd(1, *ok, f(-2.0), *grads, c(P16), need, B, H, L, d, None) == 7
+    assert lib.fox_pro_output_gate(1, c(P16), None, c(P16), f(1e-6), c(P16), B, H, L, d,
+                                   None) == 1
+    assert lib.fox_pro_output_gate(1, c(P16), c(P16), c(P16), f(-1e-3), c(P16), B, H, L, d,
+                                   None) == 7
+    assert lib.fox_attn_fwd_pro(1, *[c(P16)] * 6, f(float("nan")), c(P16), c(P16), c(P16),
+                                B, H, L, d, f(0.1), None) == 7
+    assert lib.fox_attn_fwd_pro(1, *[c(P16)] * 6, f(1e-6), c(P16), c(P16 + 8), c(P16),
+                                B, H, L, d, f(0.1), None) == 4
+    bneed = lib.fox_attn_bwd_pro_workspace_bytes(1, B, H, L, d)
+    base = lambda x: (x + 255) // 256 * 256
+    assert bneed == base(3 * 4 * B * H * L) + base(B * H * L * d * 2) + B * H * 3 * d * 4
+    assert lib.fox_attn_bwd_pro_workspace_bytes(0, B, H, L, d) == \
+        base(3 * 4 * B * H * L) + base(B * H * L * d * 4) + B * H * 3 * d * 4
+    args = [c(P16)] * 8
+    grads = [c(P16)] * 7
+    assert lib.fox_attn_bwd_pro(1, *args, f(1e-6), *grads, c(P16), bneed - 1, B, H, L, d, f(0.1),
+                                None) == 5
+    assert lib.fox_attn_bwd_pro(1, *args, f(-1.0), *grads, c(P16), bneed, B, H, L, d, f(0.1),
+                                None) == 7
 
 
 def test_bwd_validation_and_workspace(lib):

@@ -482,3 +482,106 @@ def test_fwd_bwd_skip_is_bitwise_dense(dtype, d, B, H, L, gate):
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
     for name, a, b in zip(("dq", "dk", "dv", "dlogf"), g1, g2):
         assert torch.equal(a, b), name
+
+
+# ------------------------------------------------------------ FoX (Pro) layer
+PRO_EPS = 1e-6
+PRO_GATE = ("normal", 2.0, 1.0)
+
+
+def check_out(dtype, name, g, r, what=""):
+    """Forward outputs: fp32 max-abs <= 1e-4, bf16 relative L2 <= 1e-2."""
+    if dtype == "f32":
+        e = max_abs(g, r)
+        assert e <= 1e-4, f"{what} {name} max-abs {e:.3e}"
+    else:
+        e = rel_l2(g, r)
+        assert e <= 1e-2, f"{what} {name} rel-L2 {e:.3e}"
+
+
+PRO_CASES = [("f32", 64, 1), ("f32", 128, 300), ("bf16", 64, 2), ("bf16", 128, 257),
+             ("bf16", 64, 1000), ("bf16", 128, 513)]
+
+
+@pytest.mark.parametrize("dtype,d,L", PRO_CASES)
+def test_pro_prologue_forward_backward(dtype, d, L):
+    print(f"pro prologue dtype={dtype} d={d} L={L}", flush=True)
+    x = inputs.pro_inputs(2, 3, L, d, dtype, PRO_GATE, 700 + L, device=DEV)
+    args = (x["q_raw"], x["k_raw"], x["v_raw"], x["k_shift"], x["v_shift"], x["wq"], x["wk"])
+    q, k, v = fox.fox_pro_prologue(*args, eps=PRO_EPS)
+    grads = fox.fox_pro_prologue_bwd(*args, x["dq"], x["dk"], x["dv"], eps=PRO_EPS)
+    torch.cuda.synchronize()
+    xc = cpu(x)
+    cargs = (xc["q_raw"], xc["k_raw"], xc["v_raw"], xc["k_shift"], xc["v_shift"], xc["wq"],
+             xc["wk"], PRO_EPS)
+    for name, g, r in zip("qkv", (q, k, v), oracle.pro_prologue(*cargs)):
+        check_out(dtype, name, g, r, f"L={L}")
+    ref = oracle.pro_prologue_backward(*cargs, xc["dq"], xc["dk"], xc["dv"])
+    names = ("dq_raw", "dk_raw", "dv_raw", "dk_shift", "dv_shift", "dwq", "dwk")
+    for name, g, r in zip(names, grads, ref):
+        if L == 1 and name == "dk_shift":
+            # one token: k = RMSNorm((1 - a) k~_1) depends on a only through
+            # eps, so the exact gradient is a small difference of large terms
+            # (eps / mean square); bound the fp32 cancellation absolutely
+            assert max_abs(g, r) <= (2e-5 if dtype == "f32" else 1e-4), max_abs(g, r)
+            continue
+        check_grad(dtype, name, g, r, f"L={L}")
+
+
+@pytest.mark.parametrize("dtype,d,L", [("f32", 64, 100), ("f32", 128, 257), ("bf16", 64, 1),
+                                       ("bf16", 128, 333), ("bf16", 64, 1000)])
+def test_pro_attention_forward_backward(dtype, d, L):
+    """Attention with the output norm and gate (fused into the bf16 forward's
+    epilogue; its backward fused with Delta) against the oracle's chain."""
+    print(f"pro attention dtype={dtype} d={d} L={L}", flush=True)
+    x = inputs.pro_inputs(2, 3, L, d, dtype, PRO_GATE, 800 + L, device=DEV)
+    q, k, v = x["q_raw"], x["k_raw"], x["v_raw"]  # any q, k, v will do here
+    s = fox.default_scale(d)
+    c = fox.fox_gate_prefix(x["logit"])
+    y, o, lse = fox.fox_attn_fwd_pro(q, k, v, c, x["g"], x["wo"], s, eps=PRO_EPS)
+    grads = fox.fox_attn_bwd_pro(q, k, v, c, o, lse, x["g"], x["wo"], x["dy"], s, eps=PRO_EPS)
+    y_sep = fox.fox_pro_output_gate(o, x["g"], x["wo"], eps=PRO_EPS)
+    torch.cuda.synchronize()
+    xc = cpu(x)
+    Y, O, LSE = oracle.pro_forward(xc["q_raw"], xc["k_raw"], xc["v_raw"], xc["logit"], xc["g"],
+                                   xc["wo"], PRO_EPS, s)
+    check_fwd(dtype, o, lse, O, LSE, f"L={L}")
+    check_out(dtype, "y", y, Y, f"L={L}")
+    # the fused epilogue and the standalone kernel normalise the same stored O
+    assert rel_l2(y, y_sep) <= (1e-6 if dtype == "f32" else 4e-3), rel_l2(y, y_sep)
+    ref = oracle.pro_backward(xc["q_raw"], xc["k_raw"], xc["v_raw"], xc["logit"], xc["g"],
+                              xc["wo"], PRO_EPS, s, xc["dy"])
+    for name, g, r in zip(("dQ", "dK", "dV", "dlogf", "dg", "dwo"), grads, ref):
+        check_grad(dtype, name, g, r, f"L={L}")
+
+
+def test_pro_layer_chain_bf16():
+    """Prologue -> attention with output norm and gate -> backward -> prologue
+    backward, against the oracle's chain (every gradient of the Pro layer)."""
+    B, H, L, d = 2, 4, 700, 128
+    x = inputs.pro_inputs(B, H, L, d, "bf16", ("head_mean_uniform", 0.0, 6.0, 1.0), 901,
+                          device=DEV)
+    s = fox.default_scale(d)
+    pargs = (x["q_raw"], x["k_raw"], x["v_raw"], x["k_shift"], x["v_shift"], x["wq"], x["wk"])
+    q, k, v = fox.fox_pro_prologue(*pargs, eps=PRO_EPS)
+    c = fox.fox_gate_prefix(x["logit"])
+    y, o, lse = fox.fox_attn_fwd_pro(q, k, v, c, x["g"], x["wo"], s, eps=PRO_EPS)
+    dq, dk, dv, dlf, dg, dwo = fox.fox_attn_bwd_pro(q, k, v, c, o, lse, x["g"], x["wo"], x["dy"],
+                                                    s, eps=PRO_EPS)
+    pg = fox.fox_pro_prologue_bwd(*pargs, dq, dk, dv, eps=PRO_EPS)
+    torch.cuda.synchronize()
+    xc = cpu(x)
+    cq, ck, cv = oracle.pro_prologue(xc["q_raw"], xc["k_raw"], xc["v_raw"], xc["k_shift"],
+                                     xc["v_shift"], xc["wq"], xc["wk"], PRO_EPS)
+    Y, _, _ = oracle.pro_forward(cq, ck, cv, xc["logit"], xc["g"], xc["wo"], PRO_EPS, s)
+    check_out("bf16", "y", y, Y)
+    rq, rk, rv, rlf, rg, rwo = oracle.pro_backward(cq, ck, cv, xc["logit"], xc["g"], xc["wo"],
+                                                   PRO_EPS, s, xc["dy"])
+    rp = oracle.pro_prologue_backward(xc["q_raw"], xc["k_raw"], xc["v_raw"], xc["k_shift"],
+                                      xc["v_shift"], xc["wq"], xc["wk"], PRO_EPS, rq, rk, rv)
+    got = (dlf, dg, dwo) + tuple(pg)
+    ref = (rlf, rg, rwo) + tuple(rp)
+    names = ("dlogf", "dg", "dwo", "dq_raw", "dk_raw", "dv_raw", "dk_shift", "dv_shift", "dwq",
+             "dwk")
+    for name, g, r in zip(names, got, ref):
+        check_grad("bf16", name, g, r, "chain")
