@@ -180,6 +180,53 @@ def bench_train(w, steps, warmup):
             "skip_ms": t_skip.mean_ms()}
 
 
+def bench_pro(w, steps, warmup):
+    """The FoX (Pro) layer's hot path at the training workload's shape: prologue
+    (QK-norm, KV-shift), attention with the output norm and gate fused into the
+    forward's epilogue, its backward (norm/gate backward fused with Delta), and
+    the prologue's backward.  Each part is timed on its own."""
+    dev = torch.device("cuda:0")
+    B, H, L, d = w.B, w.H, w.L, w.d
+    x = inputs.pro_inputs(B, H, L, d, w.dtype, w.gate, w.seed + 1, device=dev)
+    s = fox.default_scale(d)
+    q, k, v = (torch.empty_like(x["q_raw"]) for _ in range(3))
+    c = fox.fox_gate_prefix(x["logit"])
+    o, y = torch.empty_like(q), torch.empty_like(q)
+    lse = torch.empty((B, H, L), device=dev)
+    pws = torch.empty(fox.fox_pro_prologue_bwd_workspace_bytes(q.dtype, B, H, L, d), device=dev,
+                      dtype=torch.uint8)
+    bws = torch.empty(fox.fox_attn_bwd_pro_workspace_bytes(q.dtype, B, H, L, d), device=dev,
+                      dtype=torch.uint8)
+    pargs = (x["q_raw"], x["k_raw"], x["v_raw"], x["k_shift"], x["v_shift"], x["wq"], x["wk"])
+    timers = {n: EventTimer() for n in ("prologue", "fwd_pro", "bwd_pro", "prologue_bwd",
+                                         "out_gate")}
+    grads = {}
+
+    def step(timed):
+        with timers["prologue"].maybe(timed):
+            fox.fox_pro_prologue(*pargs, q=q, k=k, v=v)
+        with timers["fwd_pro"].maybe(timed):
+            fox.fox_attn_fwd_pro(q, k, v, c, x["g"], x["wo"], s, o=o, lse=lse, y=y)
+        with timers["bwd_pro"].maybe(timed):
+            grads["attn"] = fox.fox_attn_bwd_pro(q, k, v, c, o, lse, x["g"], x["wo"], x["dy"], s,
+                                                 workspace=bws)
+        dq, dk, dv = grads["attn"][:3]
+        with timers["prologue_bwd"].maybe(timed):
+            grads["pro"] = fox.fox_pro_prologue_bwd(*pargs, dq, dk, dv, workspace=pws)
+        with timers["out_gate"].maybe(timed):  # the standalone epilogue, for its bandwidth
+            fox.fox_pro_output_gate(o, x["g"], x["wo"], y=y)
+
+    for _ in range(warmup):
+        step(False)
+    torch.cuda.synchronize()
+    for _ in range(steps):
+        step(True)
+    torch.cuda.synchronize()
+    if not all(torch.isfinite(t.float()).all() for t in grads["attn"] + grads["pro"]):
+        raise RuntimeError("non-finite Pro gradients")
+    return {n: t.mean_ms() for n, t in timers.items()}
+
+
 def bench_decode(w, steps, warmup):
     dev = torch.device("cuda:0")
     y = inputs.workload_inputs(w, device=dev)
@@ -334,6 +381,7 @@ def main():
     ap.add_argument("--workload", default="fwdbwd_bf16_b2_h16_l16384_d128")
     ap.add_argument("--decode-workload", default="decode_bf16_b64_h16_t32768_d128")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-pro", action="store_true", help="skip the FoX (Pro) layer timings")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="run a plain device copy of this size first (counter calibration)")
@@ -412,6 +460,43 @@ def main():
     }
     log(f"[bench] train step {r['ms']:.3f} ms -> {tflops:.1f} TFLOP/s; with skipping "
         f"{r['skip_ms']:.3f} ms")
+    if not args.no_pro:
+        rp = bench_pro(w, args.steps, args.warmup)
+        rows = B * H * L
+        e = 2  # bf16
+        # compulsory bytes per row: prologue reads q~, k~, v~ and two shift logits,
+        # writes q, k, v; its backward reads q~, k~, v~, dq, dk, dv and the shift
+        # logits, writes dq~, dk~, dv~ and two logit gradients; the standalone
+        # output gate reads o, g and writes y
+        pb = {"prologue": rows * (6 * d * e + 8), "prologue_bwd": rows * (9 * d * e + 16),
+              "out_gate": rows * 3 * d * e}
+        hbm = {n: {"ms": round(rp[n], 4), "GB/s": round(b / (rp[n] * 1e-3) / 1e9, 1),
+                   "frac_of_hbm_peak": round(b / (rp[n] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                   "compulsory_bytes": b} for n, b in pb.items()}
+        pro_ms = rp["prologue"] + rp["fwd_pro"] + rp["bwd_pro"] + rp["prologue_bwd"]
+        # practical ceiling for kernels that read and write HBM: a plain device copy
+        # of about the prologue's traffic (half read, half written)
+        src = torch.empty(pb["prologue"] // 2 // 4, device="cuda:0", dtype=torch.float32)
+        dst = torch.empty_like(src)
+        tc = EventTimer()
+        for i in range(6):
+            with tc.maybe(i > 0):
+                dst.copy_(src)
+        torch.cuda.synchronize()
+        copy_gbs = 2 * src.numel() * 4 / (tc.mean_ms() * 1e-3) / 1e9
+        del src, dst
+        out["pro"] = {
+            "what": "FoX (Pro) layer hot path at the same shape: prologue (QK-norm, KV-shift) -> "
+                    "attention with the output RMSNorm and sigmoid gate in the forward epilogue "
+                    "-> its backward (norm/gate backward fused with Delta) -> prologue backward",
+            "ms_per_step": round(pro_ms, 4),
+            "overhead_vs_plain_step": round(pro_ms / (r["fwd_ms"] + r["bwd_ms"]) - 1.0, 4),
+            "fwd_pro_ms": round(rp["fwd_pro"], 4), "bwd_pro_ms": round(rp["bwd_pro"], 4),
+            "hbm_kernels": hbm,
+            "device_copy_GB/s": round(copy_gbs, 1)}
+        log(f"[bench] Pro layer {pro_ms:.3f} ms (fwd_pro {rp['fwd_pro']:.3f}, bwd_pro "
+            f"{rp['bwd_pro']:.3f}, prologue {rp['prologue']:.3f}, prologue_bwd "
+            f"{rp['prologue_bwd']:.3f}, out_gate {rp['out_gate']:.3f})")
     if not args.no_decode:
         wd = inputs.WORKLOADS[args.decode_workload]
         rd = bench_decode(wd, max(args.steps, 10), args.warmup)

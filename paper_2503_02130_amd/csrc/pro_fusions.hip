@@ -9,7 +9,7 @@
 // with RMSNorm(x) = x / sqrt(mean(x^2) + eps) * w^(h) and k~_0 = v~_0 = 0.  Every
 // kernel here is row-parallel and bound by HBM: LPR lanes hold one row of d
 // values as 16-byte vectors, reductions over the head dimension are shuffles
-// within those lanes, and a workgroup walks kProRows consecutive rows of one
+// within those lanes (DPP), and a workgroup walks kProRows consecutive rows of one
 // (batch, head) slice, so the neighbour rows the token shift reads come from
 // the cache.  Weight gradients are summed per workgroup (through LDS) and then
 // over the workgroups of a head by a second kernel: no atomics, deterministic.
@@ -61,11 +61,23 @@ __device__ __forceinline__ void load_w(const float* p, float (&w)[N]) {
   }
 }
 
-// sum over the LPR lanes of a row (aligned groups of LPR lanes)
+// x from another lane of the same DPP row (16 lanes), selected by a DPP control
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over the LPR lanes of a row (aligned groups of LPR lanes), every lane
+// receiving the sum: lane ^ 1 and lane ^ 2 (quad permutes), then the mirrored
+// lane within 8 (the other quad) and within 16 (the other half), then lane ^ 16.
 template <int LPR>
 __device__ __forceinline__ float row_sum(float x) {
-#pragma unroll
-  for (int off = 1; off < LPR; off <<= 1) x += __shfl_xor(x, off);
+  static_assert(LPR == 8 || LPR == 16 || LPR == 32, "rows span 8, 16 or 32 lanes");
+  x += dpp<0xB1>(x);   // quad_perm [1,0,3,2]
+  x += dpp<0x4E>(x);   // quad_perm [2,3,0,1]
+  x += dpp<0x141>(x);  // row_half_mirror
+  if constexpr (LPR >= 16) x += dpp<0x140>(x);  // row_mirror
+  if constexpr (LPR == 32) x += __shfl_xor(x, 16);
   return x;
 }
 
@@ -111,44 +123,46 @@ __global__ __launch_bounds__(kProThreads) void pro_prologue_kernel(
   load_w<VEC>(wk + (size_t)(bh % H) * D + part * VEC, wkv);
   const size_t base = (size_t)bh * L;
   const int t_end = min(L, (chunk + 1) * kProRows);
+#pragma unroll 2
   for (int t = chunk * kProRows + slot; t < t_end; t += RPP) {
     const size_t row = base + t;
     const size_t off = row * D + part * VEC;
-    float x[VEC], p[VEC];
+    // every load first; row t - 1 is clamped to row t at t = 0 and weighted 0
+    const size_t offp = t > 0 ? off - D : off;
+    float xq[VEC], xk[VEC], pk[VEC], xv[VEC], pv[VEC];
+    load_vec<T>(qr + off, xq);
+    load_vec<T>(kr + off, xk);
+    load_vec<T>(kr + offp, pk);
+    load_vec<T>(vr + off, xv);
+    load_vec<T>(vr + offp, pv);
+    const float a = t > 0 ? sigmoid(ka[row]) : 0.0f;
+    const float a1 = 1.0f - sigmoid(ka[row]);
+    const float b = t > 0 ? sigmoid(va[row]) : 0.0f;
+    const float b1 = 1.0f - sigmoid(va[row]);
+    sched_fence();  // keep the loads together, ahead of the arithmetic
     // q = RMSNorm_q(q~)
-    load_vec<T>(qr + off, x);
     float ss = 0.0f;
 #pragma unroll
-    for (int i = 0; i < VEC; ++i) ss += x[i] * x[i];
+    for (int i = 0; i < VEC; ++i) ss += xq[i] * xq[i];
     float r = inv_rms<LPR, D>(ss, eps);
 #pragma unroll
-    for (int i = 0; i < VEC; ++i) x[i] = x[i] * r * wqv[i];
-    store_vec<T>(q + off, x);
+    for (int i = 0; i < VEC; ++i) xq[i] = xq[i] * r * wqv[i];
+    store_vec<T>(q + off, xq);
     // k = RMSNorm_k(a k~_{t-1} + (1 - a) k~_t)
-    load_vec<T>(kr + off, x);
-#pragma unroll
-    for (int i = 0; i < VEC; ++i) p[i] = 0.0f;
-    if (t > 0) load_vec<T>(kr + off - D, p);
-    const float a = sigmoid(ka[row]);
     ss = 0.0f;
 #pragma unroll
     for (int i = 0; i < VEC; ++i) {
-      x[i] = a * p[i] + (1.0f - a) * x[i];
-      ss += x[i] * x[i];
+      xk[i] = a * pk[i] + a1 * xk[i];
+      ss += xk[i] * xk[i];
     }
     r = inv_rms<LPR, D>(ss, eps);
 #pragma unroll
-    for (int i = 0; i < VEC; ++i) x[i] = x[i] * r * wkv[i];
-    store_vec<T>(k + off, x);
+    for (int i = 0; i < VEC; ++i) xk[i] = xk[i] * r * wkv[i];
+    store_vec<T>(k + off, xk);
     // v = b v~_{t-1} + (1 - b) v~_t
-    load_vec<T>(vr + off, x);
 #pragma unroll
-    for (int i = 0; i < VEC; ++i) p[i] = 0.0f;
-    if (t > 0) load_vec<T>(vr + off - D, p);
-    const float b = sigmoid(va[row]);
-#pragma unroll
-    for (int i = 0; i < VEC; ++i) x[i] = b * p[i] + (1.0f - b) * x[i];
-    store_vec<T>(v + off, x);
+    for (int i = 0; i < VEC; ++i) xv[i] = b * pv[i] + b1 * xv[i];
+    store_vec<T>(v + off, xv);
   }
 }
 
@@ -159,7 +173,7 @@ __global__ __launch_bounds__(kProThreads) void pro_prologue_kernel(
 //                dk~_t = (1 - a_t) ds_t + a_{t+1} ds_{t+1},
 //                d(k shift logit)_t = a_t (1 - a_t) ds_t . (k~_{t-1} - k~_t)
 //   value shift: the same with dv in place of ds and no normalisation.
-// ds_{t+1} is recomputed from row t + 1 (it stays in the cache).
+// ds_{t+1} is recomputed from row t + 1 (the neighbour rows come from the cache).
 // ---------------------------------------------------------------------------
 template <typename T, int D>
 __global__ __launch_bounds__(kProThreads) void pro_prologue_bwd_kernel(
@@ -181,105 +195,103 @@ __global__ __launch_bounds__(kProThreads) void pro_prologue_bwd_kernel(
   const size_t base = (size_t)bh * L;
   const int t_end = min(L, (chunk + 1) * kProRows);
 
-  // ds of the key row u (RMSNorm_k backward of dk_u through s_u), with s_u built
-  // from k~_u = cur and k~_{u-1} = prev; also returns n_u for the weight gradient
-  auto key_ds = [&](const float (&prev)[VEC], const float (&cur)[VEC], float a, size_t off_u,
-                    float (&ds)[VEC], float (&n)[VEC], float (&g)[VEC]) {
+  // RMSNorm_k backward of the key row u: s (in: the mixed row, out: n = s r),
+  // g (in: dk_u) -> ds = r (g o w - n mean(g o w o n))
+  auto norm_bwd = [&](float (&sn)[VEC], const float (&g)[VEC], float (&ds)[VEC]) {
     float ss = 0.0f;
 #pragma unroll
-    for (int i = 0; i < VEC; ++i) {
-      n[i] = a * prev[i] + (1.0f - a) * cur[i];
-      ss += n[i] * n[i];
-    }
+    for (int i = 0; i < VEC; ++i) ss += sn[i] * sn[i];
     const float r = inv_rms<LPR, D>(ss, eps);
-    load_vec<T>(dk + off_u, g);
     float m = 0.0f;
 #pragma unroll
     for (int i = 0; i < VEC; ++i) {
-      n[i] *= r;
+      sn[i] *= r;
       ds[i] = g[i] * wkv[i];
-      m += ds[i] * n[i];
+      m += ds[i] * sn[i];
     }
     m = row_sum<LPR>(m) * (1.0f / D);
 #pragma unroll
-    for (int i = 0; i < VEC; ++i) ds[i] = r * (ds[i] - n[i] * m);
+    for (int i = 0; i < VEC; ++i) ds[i] = r * (ds[i] - sn[i] * m);
   };
 
   for (int t = chunk * kProRows + slot; t < t_end; t += RPP) {
     const size_t row = base + t;
     const size_t off = row * D + part * VEC;
-    const bool has_next = t + 1 < L;
+    const bool first = t == 0, last = t + 1 == L;
+    // every load first; the rows t - 1 and t + 1 are clamped to row t at the
+    // sequence ends, where their terms are dropped
+    const size_t offp = first ? off : off - D, offn = last ? off : off + D;
+    float xq[VEC], gq[VEC], kp[VEC], kc[VEC], kn[VEC], gk[VEC], gkn[VEC];
+    float vp[VEC], vc[VEC], gv[VEC], gvn[VEC];
+    load_vec<T>(qr + off, xq);
+    load_vec<T>(dq + off, gq);
+    load_vec<T>(kr + offp, kp);
+    load_vec<T>(kr + off, kc);
+    load_vec<T>(kr + offn, kn);
+    load_vec<T>(dk + off, gk);
+    load_vec<T>(dk + offn, gkn);
+    load_vec<T>(vr + offp, vp);
+    load_vec<T>(vr + off, vc);
+    load_vec<T>(dv + off, gv);
+    load_vec<T>(dv + offn, gvn);
+    const float a = sigmoid(ka[row]), an = sigmoid(ka[last ? row : row + 1]);
+    const float b = sigmoid(va[row]), bn = sigmoid(va[last ? row : row + 1]);
+    sched_fence();  // keep the loads together, ahead of the arithmetic
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) {
+      kp[i] = first ? 0.0f : kp[i];  // k~_0 = v~_0 = 0
+      vp[i] = first ? 0.0f : vp[i];
+    }
     // q
     {
-      float x[VEC], g[VEC];
-      load_vec<T>(qr + off, x);
       float ss = 0.0f;
 #pragma unroll
-      for (int i = 0; i < VEC; ++i) ss += x[i] * x[i];
+      for (int i = 0; i < VEC; ++i) ss += xq[i] * xq[i];
       const float r = inv_rms<LPR, D>(ss, eps);
-      load_vec<T>(dq + off, g);
       float m = 0.0f;
 #pragma unroll
       for (int i = 0; i < VEC; ++i) {
-        x[i] *= r;  // n
-        aq[i] += g[i] * x[i];
-        g[i] *= wqv[i];  // dn
-        m += g[i] * x[i];
+        xq[i] *= r;  // n
+        aq[i] += gq[i] * xq[i];
+        gq[i] *= wqv[i];  // dn
+        m += gq[i] * xq[i];
       }
       m = row_sum<LPR>(m) * (1.0f / D);
 #pragma unroll
-      for (int i = 0; i < VEC; ++i) g[i] = r * (g[i] - x[i] * m);
-      store_vec<T>(dqr + off, g);
+      for (int i = 0; i < VEC; ++i) gq[i] = r * (gq[i] - xq[i] * m);
+      store_vec<T>(dqr + off, gq);
     }
-    // k
+    // k: ds_t through s_t, ds_{t+1} through s_{t+1} = a_{t+1} k~_t + (1 - a_{t+1}) k~_{t+1}
     {
-      float prev[VEC], cur[VEC], nxt[VEC], ds[VEC], dsn[VEC], n[VEC], g[VEC];
+      float sn[VEC], ds[VEC], dsn[VEC];
 #pragma unroll
-      for (int i = 0; i < VEC; ++i) prev[i] = nxt[i] = dsn[i] = 0.0f;
-      if (t > 0) load_vec<T>(kr + off - D, prev);
-      load_vec<T>(kr + off, cur);
-      const float a = sigmoid(ka[row]);
-      key_ds(prev, cur, a, off, ds, n, g);
+      for (int i = 0; i < VEC; ++i) sn[i] = a * kp[i] + (1.0f - a) * kc[i];
+      norm_bwd(sn, gk, ds);
 #pragma unroll
-      for (int i = 0; i < VEC; ++i) ak[i] += g[i] * n[i];
-      float an = 0.0f;
-      if (has_next) {  // uniform over the row's lanes
-        load_vec<T>(kr + off + D, nxt);
-        an = sigmoid(ka[row + 1]);
-        key_ds(cur, nxt, an, off + D, dsn, n, g);
-      }
+      for (int i = 0; i < VEC; ++i) ak[i] += gk[i] * sn[i];
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) sn[i] = an * kc[i] + (1.0f - an) * kn[i];
+      norm_bwd(sn, gkn, dsn);
       float dl = 0.0f;
 #pragma unroll
       for (int i = 0; i < VEC; ++i) {
-        dl += ds[i] * (prev[i] - cur[i]);
-        g[i] = (1.0f - a) * ds[i] + an * dsn[i];
+        dl += ds[i] * (kp[i] - kc[i]);
+        kc[i] = (1.0f - a) * ds[i] + (last ? 0.0f : an * dsn[i]);
       }
       dl = row_sum<LPR>(dl);
-      store_vec<T>(dkr + off, g);
+      store_vec<T>(dkr + off, kc);
       if (part == 0) dka[row] = a * (1.0f - a) * dl;
     }
     // v
     {
-      float prev[VEC], cur[VEC], g[VEC], gn[VEC];
-#pragma unroll
-      for (int i = 0; i < VEC; ++i) prev[i] = gn[i] = 0.0f;
-      if (t > 0) load_vec<T>(vr + off - D, prev);
-      load_vec<T>(vr + off, cur);
-      load_vec<T>(dv + off, g);
-      const float b = sigmoid(va[row]);
-      float bn = 0.0f;
-      if (has_next) {
-        load_vec<T>(dv + off + D, gn);
-        bn = sigmoid(va[row + 1]);
-      }
       float dl = 0.0f;
 #pragma unroll
       for (int i = 0; i < VEC; ++i) {
-        dl += g[i] * (prev[i] - cur[i]);
-        cur[i] = (1.0f - b) * g[i] + bn * gn[i];
+        dl += gv[i] * (vp[i] - vc[i]);
+        vc[i] = (1.0f - b) * gv[i] + (last ? 0.0f : bn * gvn[i]);
       }
       dl = row_sum<LPR>(dl);
-      store_vec<T>(dvr + off, cur);
+      store_vec<T>(dvr + off, vc);
       if (part == 0) dva[row] = b * (1.0f - b) * dl;
     }
   }
@@ -301,11 +313,13 @@ __global__ __launch_bounds__(kProThreads) void out_gate_kernel(
   float w[VEC];
   load_w<VEC>(wo + (size_t)(bh % H) * D + part * VEC, w);
   const int t_end = min(L, (chunk + 1) * kProRows);
+#pragma unroll 2
   for (int t = chunk * kProRows + slot; t < t_end; t += RPP) {
     const size_t off = ((size_t)bh * L + t) * D + part * VEC;
     float o[VEC], g[VEC];
     load_vec<T>(O + off, o);
     load_vec<T>(G + off, g);
+    sched_fence();
     float ss = 0.0f;
 #pragma unroll
     for (int i = 0; i < VEC; ++i) ss += o[i] * o[i];
@@ -337,6 +351,7 @@ __global__ __launch_bounds__(kProThreads) void out_gate_bwd_kernel(
 #pragma unroll
   for (int i = 0; i < VEC; ++i) aw[i] = 0.0f;
   const int t_end = min(L, (chunk + 1) * kProRows);
+#pragma unroll 2
   for (int t = chunk * kProRows + slot; t < t_end; t += RPP) {
     const size_t row = (size_t)bh * L + t;
     const size_t off = row * D + part * VEC;
@@ -344,6 +359,7 @@ __global__ __launch_bounds__(kProThreads) void out_gate_bwd_kernel(
     load_vec<T>(O + off, o);
     load_vec<T>(G + off, g);
     load_vec<T>(dY + off, dy);
+    sched_fence();
     float ss = 0.0f;
 #pragma unroll
     for (int i = 0; i < VEC; ++i) ss += o[i] * o[i];
