@@ -182,29 +182,87 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
     // bias divided by s, so the MFMA chain adds it and one fma per score remains
     const float m_sub = MASK ? 0.0f : m_used;
     float u[32];
+    bf16x8 pb[4];
+    float psum_fast = 0.0f;
+    if constexpr (!MASK) {
+      // unmasked tiles: the scale, exponentials and row sums of keys 0..31 are
+      // scheduled between the MFMAs of keys 32..63 (one wave overlaps the two)
+      bf16x8 ka0[D / 16], ka1[D / 16];
+      f32x16 acc0, acc1;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      bf16x8 ka[D / 16];
-#pragma unroll
-      for (int s = 0; s < D / 16; ++s)
-        ka[s] = *reinterpret_cast<const bf16x8*>(kt_ + kb * 32 * D + koff[s]);
-      f32x16 acc;
+      for (int s = 0; s < D / 16; ++s) ka0[s] = *reinterpret_cast<const bf16x8*>(kt_ + koff[s]);
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const f32x4 ck4 = *reinterpret_cast<const f32x4*>(ct_ + kb * 32 + 8 * g + 4 * h);
+        const f32x4 ck4 = *reinterpret_cast<const f32x4*>(ct_ + 8 * g + 4 * h);
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj) acc[4 * g + jj] = ck4[jj];
+        for (int jj = 0; jj < 4; ++jj) acc0[4 * g + jj] = ck4[jj];
       }
       sched_fence();
 #pragma unroll
-      for (int s = 0; s < D / 16; ++s) acc = mfma32(ka[s], qf[s], acc);
+      for (int s = 0; s < D / 16; ++s) acc0 = mfma32(ka0[s], qf[s], acc0);
+#pragma unroll
+      for (int s = 0; s < D / 16; ++s)
+        ka1[s] = *reinterpret_cast<const bf16x8*>(kt_ + 32 * D + koff[s]);
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
+        const f32x4 ck4 = *reinterpret_cast<const f32x4*>(ct_ + 32 + 8 * g + 4 * h);
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-          float x = acc[4 * g + jj] * scale_log2 - m_sub;
-          if (MASK && key0 + kb * 32 + 8 * g + 4 * h + jj > qi) x = -INFINITY;
-          u[kb * 16 + 4 * g + jj] = x;
+        for (int jj = 0; jj < 4; ++jj) acc1[4 * g + jj] = ck4[jj];
+      }
+      sched_fence();
+#pragma unroll
+      for (int r = 0; r < 16; ++r) u[r] = acc0[r] * scale_log2 - m_sub;
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        float pv[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) pv[i] = exp2_fast(u[8 * c + i]);
+        pb[c] = pack8(pv);
+        psum_fast = sum8_bf16(pb[c], psum_fast);
+      }
+#pragma unroll
+      for (int s = 0; s < D / 16; ++s) acc1 = mfma32(ka1[s], qf[s], acc1);
+#pragma unroll
+      for (int i = 0; i < D / 16; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
+      }
+      sched_fence();
+#pragma unroll
+      for (int r = 0; r < 16; ++r) u[16 + r] = acc1[r] * scale_log2 - m_sub;
+#pragma unroll
+      for (int c = 2; c < 4; ++c) {
+        float pv[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) pv[i] = exp2_fast(u[8 * c + i]);
+        pb[c] = pack8(pv);
+        psum_fast = sum8_bf16(pb[c], psum_fast);
+      }
+    } else {  // the diagonal tile: plain order, then the causal mask
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        bf16x8 ka[D / 16];
+#pragma unroll
+        for (int s = 0; s < D / 16; ++s)
+          ka[s] = *reinterpret_cast<const bf16x8*>(kt_ + kb * 32 * D + koff[s]);
+        f32x16 acc;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x4 ck4 = *reinterpret_cast<const f32x4*>(ct_ + kb * 32 + 8 * g + 4 * h);
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj) acc[4 * g + jj] = ck4[jj];
+        }
+        sched_fence();
+#pragma unroll
+        for (int s = 0; s < D / 16; ++s) acc = mfma32(ka[s], qf[s], acc);
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj) {
+            float x = acc[4 * g + jj] * scale_log2 - m_sub;
+            if (MASK && key0 + kb * 32 + 8 * g + 4 * h + jj > qi) x = -INFINITY;
+            u[kb * 16 + 4 * g + jj] = x;
+          }
         }
       }
     }
@@ -223,7 +281,6 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
       for (int r = 1; r < 32; ++r) mt = fmaxf(mt, u[r]);
       return wave_max_pair(mt);
     };
-    bf16x8 pb[4];
     auto exponentiate = [&]() {
       float psum = 0.0f;
 #pragma unroll
@@ -246,10 +303,10 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
       m_used = mt;
       psum = exponentiate();
     } else {
-      // no maximum: exponentiate against the running one, and only if some score
-      // exceeds it by more than the slack (the lane's sum then exceeds 2^slack)
-      // find the tile maximum, rescale and exponentiate again
-      psum = exponentiate();
+      // no maximum: the scores were exponentiated against the running one above;
+      // only if some score exceeds it by more than the slack (the lane's sum then
+      // exceeds 2^slack) find the tile maximum, rescale and exponentiate again
+      psum = psum_fast;
       if (__any(q_valid && psum > kRescaleSum)) {
         const float shift = fmaxf(tile_max(), 0.0f);
         rescale(shift);
