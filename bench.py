@@ -47,6 +47,10 @@ KERNEL_SOURCES = {
     "bwd_dq_bf16_kernel": ("attn_bwd.hip", "fox_device.h"),
     "fwd_bf16_kernel": ("attn_fwd.hip", "fox_device.h"),
     "decode_split_kernel": ("attn_decode.hip", "fox_device.h"),
+    "pro_prologue_kernel": ("pro_fusions.hip", "fox_device.h"),
+    "pro_prologue_bwd_kernel": ("pro_fusions.hip", "fox_device.h"),
+    "out_gate_kernel": ("pro_fusions.hip", "fox_device.h"),
+    "out_gate_bwd_kernel": ("pro_fusions.hip", "fox_device.h"),
 }
 
 
@@ -320,13 +324,41 @@ def _kernel_family(name):
     return "copy" if "copyBuffer" in name else None
 
 
+def _kernel_key(name):
+    """The kernel family with its template arguments, e.g.
+    bwd_dkdv_bf16_kernel<128,false,false> (dense and skipping instantiations of
+    one family differ in traffic), or "copy"; None for anything else."""
+    fam = _kernel_family(name)
+    if fam in (None, "copy"):
+        return fam
+    m = re.search(r"fox::\w+<([^>]*)>", name)
+    if m:
+        return f"{fam}<{m.group(1).replace(' ', '')}>"
+    # Itanium-mangled: _ZN3fox<n><family>I<args>E...; the argument kinds used here
+    m = re.match(r"_ZN3fox\d+\w+?I((?:DF16b|f|Li\d+E|Lb[01]E)+)E", name)
+    if not m:
+        return fam
+    toks = re.findall(r"DF16b|f|Li\d+E|Lb[01]E", m.group(1))
+    out = []
+    for t in toks:
+        if t == "DF16b":
+            out.append("__bf16")
+        elif t == "f":
+            out.append("float")
+        elif t.startswith("Li"):
+            out.append(t[2:-1])
+        else:
+            out.append("true" if t[2] == "1" else "false")
+    return f"{fam}<{','.join(out)}>"
+
+
 def _per_kernel_kib(rows, counter):
     """Mean counter value (KiB) per dispatch, per kernel family."""
     per = {}
     for r in rows:
         if r["Counter_Name"] != counter:
             continue
-        key = _kernel_family(r["Kernel_Name"])
+        key = _kernel_key(r["Kernel_Name"])
         if key is None:
             continue
         per.setdefault(key, {}).setdefault(r["Dispatch_Id"], 0.0)
@@ -350,26 +382,28 @@ def pmc_summary(fetch_dir, write_dir, copy_mib, command):
              f"# calibration: plain copy of {copy_mib} MiB read {cf:.0f} KiB and wrote {cw:.0f} KiB;",
              f"#   scale factors fetch {f_fac:.4f}, write {w_fac:.4f}",
              "# kernel  dispatches  fetch_KiB  write_KiB  traffic_bytes_per_launch  sources_sha256"]
-    for k in sorted(KERNEL_SOURCES):
-        if k not in fetch or k not in write:
+    for k in sorted(set(fetch) & set(write)):
+        fam = k.split("<")[0]
+        if fam not in KERNEL_SOURCES:
             continue
         fk = sum(fetch[k].values()) / len(fetch[k])
         wk = sum(write[k].values()) / len(write[k])
         tb = (fk * f_fac + wk * w_fac) * 1024.0
-        lines.append(f"{k} {len(fetch[k])} {fk:.1f} {wk:.1f} {tb:.0f} {sources_hash(k)}")
+        lines.append(f"{k} {len(fetch[k])} {fk:.1f} {wk:.1f} {tb:.0f} {sources_hash(fam)}")
     return "\n".join(lines) + "\n"
 
 
 def measured_traffic(kernel: str):
-    """Bytes per launch recorded for `kernel`, or None when there is no record or
-    the kernel's sources changed since the counters were taken."""
+    """Bytes per launch recorded for `kernel` (family<template arguments>), or
+    None when there is no record or the family's sources changed since the
+    counters were taken."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     for line in open(TRAFFIC_FILE):
         f = line.split()
         if line.startswith("#") or len(f) != 6 or f[0] != kernel:
             continue
-        return float(f[4]) if f[5] == sources_hash(kernel) else None
+        return float(f[4]) if f[5] == sources_hash(kernel.split("<")[0]) else None
     return None
 
 
@@ -418,7 +452,7 @@ def main():
     # compulsory HBM bytes of one dK/dV launch: read q, k, v, dO (bf16), c, LSE,
     # delta (fp32); write dK, dV (bf16), dc_k (fp32)
     kv_bytes = B * H * L * (6 * d * 2 + 4 * 4)
-    kv_traffic = measured_traffic("bwd_dkdv_bf16_kernel")
+    kv_traffic = measured_traffic("bwd_dkdv_bf16_kernel<128,false,false>")
     out = {
         "metric": "Forgetting-attn fwd+bwd TFLOP/s bf16 L=16k d=128 (% MFMA peak); decode GB/s",
         "value": round(tflops, 2),
@@ -470,9 +504,13 @@ def main():
         # output gate reads o, g and writes y
         pb = {"prologue": rows * (6 * d * e + 8), "prologue_bwd": rows * (9 * d * e + 16),
               "out_gate": rows * 3 * d * e}
+        kern = {"prologue": "pro_prologue_kernel<__bf16,128>",
+                "prologue_bwd": "pro_prologue_bwd_kernel<__bf16,128>",
+                "out_gate": "out_gate_kernel<__bf16,128>"}
         hbm = {n: {"ms": round(rp[n], 4), "GB/s": round(b / (rp[n] * 1e-3) / 1e9, 1),
                    "frac_of_hbm_peak": round(b / (rp[n] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-                   "compulsory_bytes": b} for n, b in pb.items()}
+                   "compulsory_bytes": b, "kernel": kern[n],
+                   "traffic": measured_traffic(kern[n])} for n, b in pb.items()}
         pro_ms = rp["prologue"] + rp["fwd_pro"] + rp["bwd_pro"] + rp["prologue_bwd"]
         # practical ceiling for kernels that read and write HBM: a plain device copy
         # of about the prologue's traffic (half read, half written)
@@ -509,7 +547,8 @@ def main():
                          "roofline": {"bound": "hbm", "kernel": "fox_attn_decode (split + combine)",
                                       "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
                                       "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
-                                      "traffic": measured_traffic("decode_split_kernel")},
+                                      "traffic": measured_traffic(
+                                          "decode_split_kernel<__bf16,128,false,false>")},
                          "skip": {"what": "fox_attn_decode_skip: exact gate-aware skipping of key "
                                           "splits, outputs bitwise equal to the dense decode",
                                   "ms_per_step": round(rd["skip_ms"], 4),

@@ -86,6 +86,26 @@ __device__ __forceinline__ float sum8_bf16(const bf16x8& v, float acc) {
   return acc;
 }
 
+// x from another lane of the same DPP row (16 lanes), selected by a DPP control
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over aligned groups of LPR lanes (8, 16 or 32), every lane receiving its
+// group's sum: lane ^ 1 and lane ^ 2 (quad permutes), then the mirrored lane
+// within 8 (the other quad) and within 16 (the other half), then lane ^ 16.
+template <int LPR>
+__device__ __forceinline__ float row_sum(float x) {
+  static_assert(LPR == 8 || LPR == 16 || LPR == 32, "rows span 8, 16 or 32 lanes");
+  x += dpp<0xB1>(x);   // quad_perm [1,0,3,2]
+  x += dpp<0x4E>(x);   // quad_perm [2,3,0,1]
+  x += dpp<0x141>(x);  // row_half_mirror
+  if constexpr (LPR >= 16) x += dpp<0x140>(x);  // row_mirror
+  if constexpr (LPR == 32) x += __shfl_xor(x, 16);
+  return x;
+}
+
 // Combine a value with the one held by lane l ^ 32 (v_permlane32_swap on gfx950:
 // the swap of the two half-waves leaves lane l holding both x_l and x_{l^32}).
 __device__ __forceinline__ float wave_max_pair(float x) {

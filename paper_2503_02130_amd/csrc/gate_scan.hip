@@ -7,9 +7,9 @@
 //    carried on through the gate f = sigmoid(x) (Sec. 3) in the same pass:
 //    d x_l = d(log f)_l * sigmoid(-x_l).
 //
-// Each workgroup walks its row in segments of 2048 elements: every thread scans
-// eight consecutive elements sequentially, the 256 thread totals are scanned
-// across the wave with shuffles and across the four waves through LDS, and a
+// Each workgroup walks its row in segments of 8192 elements: every thread scans
+// eight consecutive elements sequentially, the 1024 thread totals are scanned
+// across the wave with shuffles and across the sixteen waves through LDS, and a
 // running carry links the segments.  The per-thread and per-wave steps form a
 // short tree, which keeps the fp32 rounding of long rows small.
 #include "fox_device.h"
@@ -17,7 +17,7 @@
 
 namespace fox {
 
-constexpr int kScanThreads = 256;
+constexpr int kScanThreads = 1024;
 constexpr int kScanPerThread = 8;
 constexpr int kScanSegment = kScanThreads * kScanPerThread;
 

@@ -61,26 +61,6 @@ __device__ __forceinline__ void load_w(const float* p, float (&w)[N]) {
   }
 }
 
-// x from another lane of the same DPP row (16 lanes), selected by a DPP control
-template <int CTRL>
-__device__ __forceinline__ float dpp(float x) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
-}
-
-// Sum over the LPR lanes of a row (aligned groups of LPR lanes), every lane
-// receiving the sum: lane ^ 1 and lane ^ 2 (quad permutes), then the mirrored
-// lane within 8 (the other quad) and within 16 (the other half), then lane ^ 16.
-template <int LPR>
-__device__ __forceinline__ float row_sum(float x) {
-  static_assert(LPR == 8 || LPR == 16 || LPR == 32, "rows span 8, 16 or 32 lanes");
-  x += dpp<0xB1>(x);   // quad_perm [1,0,3,2]
-  x += dpp<0x4E>(x);   // quad_perm [2,3,0,1]
-  x += dpp<0x141>(x);  // row_half_mirror
-  if constexpr (LPR >= 16) x += dpp<0x140>(x);  // row_mirror
-  if constexpr (LPR == 32) x += __shfl_xor(x, 16);
-  return x;
-}
-
 __device__ __forceinline__ float sigmoid(float x) { return 1.0f / (1.0f + expf(-x)); }
 
 // 1 / sqrt(mean of squares + eps) of one row, from each lane's partial sum of squares
@@ -390,18 +370,31 @@ __global__ __launch_bounds__(kProThreads) void out_gate_bwd_kernel(
   store_weight_partial<D, VEC, RPP>(red, aw, slot, part, pwo + (size_t)blockIdx.x * D);
 }
 
-// dw^(h)[e] = sum over batch rows b and chunks of part[(b H + h) n_chunk + chunk][e]
-__global__ __launch_bounds__(128) void weight_grad_reduce_kernel(const float* __restrict__ part,
-                                                                 float* __restrict__ dw, int B,
-                                                                 int H, int n_chunk, int D) {
+// dw^(h)[e] = sum over batch rows b and chunks of part[(b H + h) n_chunk + chunk][e]:
+// workgroup (h, 64 elements e); wave w sums the partials p = w, w + 4, ... in
+// order (loads unrolled for memory-level parallelism), then the four waves' sums
+// are added in order: a fixed order, so the result is deterministic.
+constexpr int kReduceThreads = 256;
+__global__ __launch_bounds__(kReduceThreads) void weight_grad_reduce_kernel(
+    const float* __restrict__ part, float* __restrict__ dw, int B, int H, int n_chunk, int D) {
   const int h = (int)blockIdx.x;
-  for (int e = threadIdx.x; e < D; e += 128) {
-    float s = 0.0f;
-    for (int b = 0; b < B; ++b) {
-      const float* p = part + ((size_t)(b * H + h) * n_chunk) * D + e;
-      for (int c = 0; c < n_chunk; ++c) s += p[(size_t)c * D];
-    }
-    dw[(size_t)h * D + e] = s;
+  const int e = (int)blockIdx.y * 64 + (threadIdx.x & 63);
+  const int w = threadIdx.x >> 6;
+  const int n = B * n_chunk;
+  float s = 0.0f;
+#pragma unroll 8
+  for (int p = w; p < n; p += kReduceThreads / 64) {
+    const int b = p / n_chunk, c = p % n_chunk;
+    s += part[((size_t)(b * H + h) * n_chunk + c) * D + e];
+  }
+  __shared__ float wsum[kReduceThreads / 64][64];
+  wsum[w][threadIdx.x & 63] = s;
+  __syncthreads();
+  if (w == 0) {
+    float t = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kReduceThreads / 64; ++i) t += wsum[i][threadIdx.x];
+    dw[(size_t)h * D + e] = t;
   }
 }
 
@@ -486,9 +479,10 @@ hipError_t launch_pro_prologue_bwd(bool bf16_, const void* qr, const void* kr, c
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int B = BH / H;
-  hipLaunchKernelGGL(weight_grad_reduce_kernel, dim3((unsigned)H), dim3(128), 0, s, pwq, dwq, B,
+  const dim3 rgrid((unsigned)H, (unsigned)(d / 64));
+  hipLaunchKernelGGL(weight_grad_reduce_kernel, rgrid, dim3(kReduceThreads), 0, s, pwq, dwq, B,
                      H, nc, d);
-  hipLaunchKernelGGL(weight_grad_reduce_kernel, dim3((unsigned)H), dim3(128), 0, s, pwk, dwk, B,
+  hipLaunchKernelGGL(weight_grad_reduce_kernel, rgrid, dim3(kReduceThreads), 0, s, pwk, dwk, B,
                      H, nc, d);
   return hipGetLastError();
 }
@@ -547,8 +541,8 @@ hipError_t launch_bwd_pro(bool bf16_, const void* q, const void* k, const void* 
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(weight_grad_reduce_kernel, dim3((unsigned)H), dim3(128), 0, s, pwo, dwo,
-                     BH / H, H, nc, d);
+  hipLaunchKernelGGL(weight_grad_reduce_kernel, dim3((unsigned)H, (unsigned)(d / 64)),
+                     dim3(kReduceThreads), 0, s, pwo, dwo, BH / H, H, nc, d);
   e = hipGetLastError();
   const GateSpec gs = gate_array(c);
   if (e == hipSuccess)

@@ -3,8 +3,9 @@
 // s ||q|| ||k||, and this kernel gives them ||k||'s maximum (or ||q||'s).
 //
 // A workgroup takes a chunk of rows; a group of d / 8 lanes (bf16) or d / 4
-// lanes (fp32) reads one row with 16-byte loads, the groups reduce to the
-// chunk's maximum in LDS, and the chunk maxima meet in an atomic maximum on
+// lanes (fp32) reads one row with 16-byte loads (eight rows' loads are issued
+// before their sums), the row sums are DPP butterflies, the groups reduce to
+// the chunk's maximum in LDS, and the chunk maxima meet in an atomic maximum on
 // the float's bit pattern (non-negative floats order like their bits).  The
 // result is enlarged by 2^-10 relative so that it bounds the exact norm
 // despite the fp32 rounding of the sum of squares.
@@ -14,7 +15,8 @@
 namespace fox {
 
 constexpr int kNormThreads = 256;
-constexpr int kNormChunk = 1024;  // rows per workgroup
+constexpr int kNormChunk = 1024;  // rows per workgroup (one atomic per chunk and head)
+constexpr int kNormAhead = 8;     // rows per lane group whose loads are in flight together
 
 __global__ void zero_kernel(float* __restrict__ out, int n) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
@@ -33,20 +35,24 @@ __global__ __launch_bounds__(kNormThreads) void row_norm_max_kernel(const Tt* __
   const int r0 = chunk * kNormChunk, r1 = min(L, r0 + kNormChunk);
   const Tt* base = x + (size_t)bh * (size_t)L * D + lp * VEC;
   float best = 0.0f;
-  for (int r = r0 + g; r < r1; r += RPI) {
-    float ss = 0.0f;
-    if constexpr (sizeof(Tt) == 2) {
-      const bf16x8 v = *reinterpret_cast<const bf16x8*>(base + (size_t)r * D);
+  for (int rb = r0 + g; rb < r1; rb += kNormAhead * RPI) {
+    float ss[kNormAhead];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) ss += (float)v[e] * (float)v[e];
-    } else {
-      const f32x4 v = *reinterpret_cast<const f32x4*>(base + (size_t)r * D);
+    for (int u = 0; u < kNormAhead; ++u) {
+      const int r = min(rb + u * RPI, r1 - 1);  // rows past the chunk repeat its last row
+      ss[u] = 0.0f;
+      if constexpr (sizeof(Tt) == 2) {
+        const bf16x8 v = *reinterpret_cast<const bf16x8*>(base + (size_t)r * D);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) ss += v[e] * v[e];
+        for (int e = 0; e < 8; ++e) ss[u] += (float)v[e] * (float)v[e];
+      } else {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(base + (size_t)r * D);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) ss[u] += v[e] * v[e];
+      }
     }
 #pragma unroll
-    for (int off = 1; off < LPR; off <<= 1) ss += __shfl_xor(ss, off);
-    best = fmaxf(best, ss);
+    for (int u = 0; u < kNormAhead; ++u) best = fmaxf(best, row_sum<LPR>(ss[u]));
   }
   __shared__ float s_best[kNormThreads / 64];
 #pragma unroll
