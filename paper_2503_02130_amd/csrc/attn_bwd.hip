@@ -330,7 +330,8 @@ struct KvSmem {
   bf16x8 p[3][kKvPairs][BM / 16][64];  // P of each pair: [16-query chunk][lane], bf16 x 8
   float bq[3][BM];  // ((c_i - c_ref) - LSE_i) / s of each query row
   float dl[3][BM];  // Delta_i
-  int skip[3];      // the query tile and every later one contribute exact zeros
+  float raw[2][3][BM];  // c_i, LSE_i, Delta_i of the next tiles as loaded (two tiles ahead)
+  int skip[3];          // the query tile and every later one contribute exact zeros
 };
 
 template <int D, bool FIXED, bool SKIP>
@@ -435,8 +436,35 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
 
   // per query row of a tile: ((c_i - c_ref) - LSE_i) / s and Delta_i
   const float inv_scale = 1.0f / scale;
-  bool skipreg = false;
-  float breg = 0.0f, dreg = 0.0f;
+  // The rows' c, LSE and Delta reach LDS by DMA two tiles ahead (wave 0, one
+  // row per lane; rows past L read as zero), and wave 0 converts them
+  // LDS to LDS one tile ahead: no register holds them across a tile and no
+  // wait for them ever waits for a tile's DMA.
+  const float c_k0 = gr.raw(k0), c_klast = gr.raw(k_last);
+  const __amdgpu_buffer_rsrc_t rsc = make_rsrc(FIXED ? Lh : gate + head, (uint32_t)L * 4);
+  const __amdgpu_buffer_rsrc_t rsl = make_rsrc(Lh, (uint32_t)L * 4);
+  const __amdgpu_buffer_rsrc_t rsd = make_rsrc(Dh, (uint32_t)L * 4);
+  auto issue_stats = [&](int qt, int rb) {
+    if (wave == 0) {
+      const uint32_t off = ((uint32_t)qt * kKvBM + lane) * 4;
+      if constexpr (!FIXED) dma4(rsc, &sm.raw[rb][0][0], off);
+      dma4(rsl, &sm.raw[rb][1][0], off);
+      dma4(rsd, &sm.raw[rb][2][0], off);
+    }
+  };
+  auto convert_stats = [&](int qt, int rb, auto bufc) {
+    constexpr int B = decltype(bufc)::value;
+    if (wave == 0 && lane < kKvBM) {
+      const int qq = qt * kKvBM + lane;
+      const float cr = FIXED ? 0.0f : sm.raw[rb][0][lane];
+      sm.bq[B][lane] = qq < L ? (gr.diff_raw(qq, cr, k0, c_k0) - sm.raw[rb][1][lane]) * inv_scale
+                              : -INFINITY;
+      sm.dl[B][lane] = qq < L ? sm.raw[rb][2][lane] : 0.0f;
+      // the tile's first query against the block's last key
+      if (SKIP && lane == 0)
+        sm.skip[B] = kLog2e * (skip_norm + gr.diff_raw(qq, cr, k_last, c_klast)) < -kSkipMargin;
+    }
+  };
   auto issue_tile = [&](int qt, auto bufc) {
     constexpr int B = decltype(bufc)::value;
     const uint32_t base = (uint32_t)qt * kKvBM * D * 2;
@@ -446,25 +474,6 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
       dma16(rq, &sm.q[B][wslot], base + dma_off[i]);
       dma16(rg, &sm.g[B][wslot], base + dma_off[i]);
     }
-    if (SKIP && wave == 0 && lane == 0)  // the tile's first query against the block's last key
-      skipreg = kLog2e * (skip_norm + gr.diff(qt * kKvBM, k_last)) < -kSkipMargin;
-    if (wave == 0 && lane < kKvBM) {
-      const int qq = qt * kKvBM + lane;
-      breg = -INFINITY;
-      dreg = 0.0f;
-      if (qq < L) {
-        breg = (gr.diff(qq, k0) - Lh[qq]) * inv_scale;
-        dreg = Dh[qq];
-      }
-    }
-  };
-  auto store_rows = [&](auto bufc) {
-    constexpr int B = decltype(bufc)::value;
-    if (wave == 0 && lane < kKvBM) {
-      sm.bq[B][lane] = breg;
-      sm.dl[B][lane] = dreg;
-    }
-    if (SKIP && wave == 0 && lane == 0) sm.skip[B] = skipreg;
   };
 
   // P wave on tile qt held in buffer B
@@ -568,6 +577,7 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
     // tile it and all later ones add exact zeros: the G waves finish tile it - 1
     if (SKIP && it < n_tiles && sm.skip[B]) n_tiles = it;
     if (it + 1 < n_tiles) issue_tile(t_first + it + 1, std::integral_constant<int, BN>());
+    if (it + 2 < n_tiles) issue_stats(t_first + it + 2, it & 1);
     if (pwave) {
       const int qt = t_first + it;
       if (it < n_tiles) {
@@ -578,11 +588,14 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
       const int qt = t_first + it - 1;
       if (it >= 1 && qt >= t_diag) g_tile(std::integral_constant<int, BP>());
     }
-    if (it + 1 < n_tiles) store_rows(std::integral_constant<int, BN>());
+    if (it + 1 < n_tiles) convert_stats(t_first + it + 1, (it + 1) & 1, std::integral_constant<int, BN>());
   };
 
+  issue_stats(t_first, 0);
+  if (1 < n_tiles) issue_stats(t_first + 1, 1);
   issue_tile(t_first, std::integral_constant<int, 0>());
-  store_rows(std::integral_constant<int, 0>());
+  wait_all_memory();  // wave 0's own DMA of the first tile's rows
+  convert_stats(t_first, 0, std::integral_constant<int, 0>());
   for (int it = 0; it <= n_tiles; it += 3) {
     step(it, std::integral_constant<int, 0>());
     if (it + 1 <= n_tiles) step(it + 1, std::integral_constant<int, 1>());

@@ -174,6 +174,12 @@ __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rsrc, void* lds_wav
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t*)lds_wave_base, 16, voffset, 0, 0, 0);
 }
 
+// The same with 4 bytes per lane: lane l's dword lands at lds_wave_base + 4 * l.
+__device__ __forceinline__ void dma4(__amdgpu_buffer_rsrc_t rsrc, void* lds_wave_base,
+                                     uint32_t voffset) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t*)lds_wave_base, 4, voffset, 0, 0, 0);
+}
+
 // Wait until every outstanding memory operation of this wave (including the
 // LDS-bound buffer loads above) has completed.
 __device__ __forceinline__ void wait_all_memory() { __builtin_amdgcn_s_waitcnt(0); }
