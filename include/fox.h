@@ -253,6 +253,33 @@ int fox_attn_decode_fixed_gate(int dtype, const void* q, const void* k_cache,
                                float scale, void* stream);
 
 /*
+ * Fixed gates with exact gate-aware skipping: the entry points above with the
+ * row-norm bounds of fox_attn_fwd_skip / fox_attn_bwd_skip / fox_attn_decode_skip
+ * (q_norm_max, k_norm_max [B,H] fp32 from fox_row_norm_max; the decode needs
+ * only k_norm_max over the cache).  c_i - c_j = (i - j) log sigmoid(b^(h)) makes
+ * the decay of a tile pair a function of its distance alone, so a strongly
+ * forgetting head keeps only a band of tiles near the diagonal.  The results are
+ * bit for bit those of the fixed-gate entry points without skipping.  The forward
+ * and backward skip in bf16 (fp32 runs dense); the decode skips in both dtypes.
+ * Workspaces as the entry points without skipping.
+ */
+int fox_attn_fwd_fixed_gate_skip(int dtype, const void* q, const void* k, const void* v,
+                                 const float* gate_bias, const float* q_norm_max,
+                                 const float* k_norm_max, void* o, float* lse, int B, int H, int L,
+                                 int d, float scale, void* stream);
+int fox_attn_bwd_fixed_gate_skip(int dtype, const void* q, const void* k, const void* v,
+                                 const float* gate_bias, const void* o, const float* lse,
+                                 const void* d_o, const float* q_norm_max,
+                                 const float* k_norm_max, void* dq, void* dk, void* dv,
+                                 float* d_gate_bias, void* workspace, size_t workspace_bytes,
+                                 int B, int H, int L, int d, float scale, void* stream);
+int fox_attn_decode_fixed_gate_skip(int dtype, const void* q, const void* k_cache,
+                                    const void* v_cache, const float* gate_bias,
+                                    const float* k_norm_max, void* o, float* lse, void* workspace,
+                                    size_t workspace_bytes, int B, int H, int T, int d,
+                                    float scale, void* stream);
+
+/*
  * FoX (Pro) prologue and epilogue (Sec. 3 "Architecture design", Eq. shift-linear;
  * appendix "Detailed FoX (Pro) layer computation").  Per head h and time t, from
  * the raw projections q~ = W_q x, k~ = W_k x, v~ = W_v x (already split into

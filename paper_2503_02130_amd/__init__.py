@@ -14,6 +14,7 @@ from ._lib import (  # noqa: F401
     fox_attn_bwd_fixed_gate_workspace_bytes, fox_attn_decode_fixed_gate,
     fox_attn_decode_workspace_bytes, fox_row_norm_max, fox_attn_decode_skip,
     fox_attn_fwd_skip, fox_attn_bwd_skip, LIB_PATH,
+    fox_attn_fwd_fixed_gate_skip, fox_attn_bwd_fixed_gate_skip, fox_attn_decode_fixed_gate_skip,
     fox_pro_prologue, fox_pro_prologue_bwd, fox_pro_prologue_bwd_workspace_bytes,
     fox_pro_output_gate, fox_attn_fwd_pro, fox_attn_bwd_pro, fox_attn_bwd_pro_workspace_bytes,
     EXPORTED,
@@ -28,6 +29,8 @@ __all__ = [
     "fox_attn_decode_fixed_gate",
     "fox_attn_decode", "fox_attn_decode_workspace_bytes", "fox_row_norm_max",
     "fox_attn_decode_skip", "fox_attn_fwd_skip", "fox_attn_bwd_skip",
+    "fox_attn_fwd_fixed_gate_skip", "fox_attn_bwd_fixed_gate_skip",
+    "fox_attn_decode_fixed_gate_skip",
     "fox_pro_prologue", "fox_pro_prologue_bwd", "fox_pro_prologue_bwd_workspace_bytes",
     "fox_pro_output_gate", "fox_attn_fwd_pro", "fox_attn_bwd_pro",
     "fox_attn_bwd_pro_workspace_bytes",

@@ -30,6 +30,8 @@ EXPORTED = (
     "fox_fixed_gate_init", "fox_attn_fwd_fixed_gate", "fox_attn_bwd_fixed_gate_workspace_bytes",
     "fox_attn_bwd_fixed_gate", "fox_attn_decode_fixed_gate",
     "fox_row_norm_max", "fox_attn_decode_skip", "fox_attn_fwd_skip", "fox_attn_bwd_skip",
+    "fox_attn_fwd_fixed_gate_skip", "fox_attn_bwd_fixed_gate_skip",
+    "fox_attn_decode_fixed_gate_skip",
     "fox_pro_prologue", "fox_pro_prologue_bwd_workspace_bytes", "fox_pro_prologue_bwd",
     "fox_pro_output_gate", "fox_attn_fwd_pro", "fox_attn_bwd_pro_workspace_bytes",
     "fox_attn_bwd_pro",
@@ -102,6 +104,13 @@ def load() -> ctypes.CDLL:
                                       F, P]
     lib.fox_attn_decode_skip.restype = I
     lib.fox_attn_decode_skip.argtypes = [I, P, P, P, P, P, P, P, P, P, Z, I, I, I, I, F, P]
+    lib.fox_attn_fwd_fixed_gate_skip.restype = I
+    lib.fox_attn_fwd_fixed_gate_skip.argtypes = [I, P, P, P, P, P, P, P, P, I, I, I, I, F, P]
+    lib.fox_attn_bwd_fixed_gate_skip.restype = I
+    lib.fox_attn_bwd_fixed_gate_skip.argtypes = [I, P, P, P, P, P, P, P, P, P, P, P, P, P, P, Z,
+                                                 I, I, I, I, F, P]
+    lib.fox_attn_decode_fixed_gate_skip.restype = I
+    lib.fox_attn_decode_fixed_gate_skip.argtypes = [I, P, P, P, P, P, P, P, P, Z, I, I, I, I, F, P]
     lib.fox_pro_prologue.restype = I
     lib.fox_pro_prologue.argtypes = [I, P, P, P, P, P, P, P, F, P, P, P, I, I, I, I, P]
     lib.fox_pro_prologue_bwd_workspace_bytes.restype = Z
@@ -575,6 +584,93 @@ def fox_attn_bwd_skip(q, k, v, c, o, lse, d_o, q_norm_max, k_norm_max,
                                   B, H, L, d, s, _stream(q))
     _raise(st, "fox_attn_bwd_skip")
     return dq, dk, dv, d_log_f
+
+
+
+def fox_attn_fwd_fixed_gate_skip(q, k, v, gate_bias, q_norm_max, k_norm_max,
+                                 scale: Optional[float] = None, o=None, lse=None):
+    """fox_attn_fwd_fixed_gate with exact gate-aware skipping (bitwise the same O, LSE)."""
+    B, H, L, d = q.shape
+    dt = q.dtype
+    if dt not in _DT:
+        raise ValueError(f"unsupported dtype {dt}")
+    dev = q.device
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _check(t, name, (B, H, L, d), dt, dev)
+    _check(gate_bias, "gate_bias", (H,), torch.float32, dev)
+    _check(q_norm_max, "q_norm_max", (B, H), torch.float32, dev)
+    _check(k_norm_max, "k_norm_max", (B, H), torch.float32, dev)
+    o = torch.empty_like(q) if o is None else o
+    lse = torch.empty((B, H, L), device=dev, dtype=torch.float32) if lse is None else lse
+    _check(o, "o", (B, H, L, d), dt, dev)
+    _check(lse, "lse", (B, H, L), torch.float32, dev)
+    s = default_scale(d) if scale is None else float(scale)
+    st = load().fox_attn_fwd_fixed_gate_skip(_DT[dt], _ptr(q), _ptr(k), _ptr(v), _ptr(gate_bias),
+                                             _ptr(q_norm_max), _ptr(k_norm_max), _ptr(o),
+                                             _ptr(lse), B, H, L, d, s, _stream(q))
+    _raise(st, "fox_attn_fwd_fixed_gate_skip")
+    return o, lse
+
+
+def fox_attn_bwd_fixed_gate_skip(q, k, v, gate_bias, o, lse, d_o, q_norm_max, k_norm_max,
+                                 scale: Optional[float] = None, want_bias_grad=True,
+                                 workspace=None):
+    """fox_attn_bwd_fixed_gate with exact gate-aware skipping: dq, dk, dv, d gate_bias."""
+    B, H, L, d = q.shape
+    dt = q.dtype
+    if dt not in _DT:
+        raise ValueError(f"unsupported dtype {dt}")
+    dev = q.device
+    for name, t in (("q", q), ("k", k), ("v", v), ("o", o), ("d_o", d_o)):
+        _check(t, name, (B, H, L, d), dt, dev)
+    _check(gate_bias, "gate_bias", (H,), torch.float32, dev)
+    _check(lse, "lse", (B, H, L), torch.float32, dev)
+    _check(q_norm_max, "q_norm_max", (B, H), torch.float32, dev)
+    _check(k_norm_max, "k_norm_max", (B, H), torch.float32, dev)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    db = torch.empty_like(gate_bias) if want_bias_grad else None
+    need = fox_attn_bwd_fixed_gate_workspace_bytes(dt, B, H, L, d)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), device=dev, dtype=torch.uint8)
+    s = default_scale(d) if scale is None else float(scale)
+    st = load().fox_attn_bwd_fixed_gate_skip(_DT[dt], _ptr(q), _ptr(k), _ptr(v), _ptr(gate_bias),
+                                             _ptr(o), _ptr(lse), _ptr(d_o), _ptr(q_norm_max),
+                                             _ptr(k_norm_max), _ptr(dq), _ptr(dk), _ptr(dv),
+                                             _ptr(db), _ptr(workspace),
+                                             workspace.numel() * workspace.element_size(),
+                                             B, H, L, d, s, _stream(q))
+    _raise(st, "fox_attn_bwd_fixed_gate_skip")
+    return dq, dk, dv, db
+
+
+def fox_attn_decode_fixed_gate_skip(q, k_cache, v_cache, gate_bias, k_norm_max,
+                                    scale: Optional[float] = None, o=None, lse=None,
+                                    workspace=None):
+    """fox_attn_decode_fixed_gate with exact skipping of key splits.  Returns o, lse."""
+    B, H, d = q.shape
+    T = k_cache.shape[2]
+    dt = q.dtype
+    if dt not in _DT:
+        raise ValueError(f"unsupported dtype {dt}")
+    dev = q.device
+    _check(q, "q", (B, H, d), dt, dev)
+    _check(k_cache, "k_cache", (B, H, T, d), dt, dev)
+    _check(v_cache, "v_cache", (B, H, T, d), dt, dev)
+    _check(gate_bias, "gate_bias", (H,), torch.float32, dev)
+    _check(k_norm_max, "k_norm_max", (B, H), torch.float32, dev)
+    o = torch.empty_like(q) if o is None else o
+    lse = torch.empty((B, H), device=dev, dtype=torch.float32) if lse is None else lse
+    need = fox_attn_decode_workspace_bytes(dt, B, H, T, d)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), device=dev, dtype=torch.uint8)
+    s = default_scale(d) if scale is None else float(scale)
+    st = load().fox_attn_decode_fixed_gate_skip(_DT[dt], _ptr(q), _ptr(k_cache), _ptr(v_cache),
+                                                _ptr(gate_bias), _ptr(k_norm_max), _ptr(o),
+                                                _ptr(lse), _ptr(workspace),
+                                                workspace.numel() * workspace.element_size(),
+                                                B, H, T, d, s, _stream(q))
+    _raise(st, "fox_attn_decode_fixed_gate_skip")
+    return o, lse
 
 
 # ---------------------------------------------------------------------------

@@ -943,11 +943,12 @@ size_t bwd_fixed_workspace_bytes(int BH, int L) { return 16 * (size_t)BH * (size
 hipError_t launch_bwd_fixed(bool bf16_, const void* q, const void* k, const void* v,
                             const float* bias, int H, const void* o, const float* lse,
                             const void* d_o, void* dq, void* dk, void* dv, float* d_bias, void* ws,
-                            int BH, int L, int d, float scale, hipStream_t s) {
+                            int BH, int L, int d, float scale, hipStream_t s,
+                            const float* q_norm_max, const float* k_norm_max) {
   float* w = static_cast<float*>(ws);
   float* dlf = w + 3 * (size_t)BH * L;
   hipError_t e = launch_bwd_stages(bf16_, q, k, v, gate_fixed(bias, H), o, lse, d_o, dq, dk, dv,
-                                   dlf, w, BH, L, d, scale, s);
+                                   dlf, w, BH, L, d, scale, s, q_norm_max, k_norm_max);
   if (e == hipSuccess && d_bias) {
     hipLaunchKernelGGL(fixed_bias_grad_kernel, dim3(H), dim3(kBiasThreads), 0, s, dlf, bias,
                        d_bias, BH / H, H, L);

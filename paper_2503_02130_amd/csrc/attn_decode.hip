@@ -298,7 +298,11 @@ hipError_t launch_decode_skip(bool bf16_, const void* q, const void* k_cache, co
 
 hipError_t launch_decode_fixed(bool bf16_, const void* q, const void* k_cache, const void* v_cache,
                                const float* bias, int H, void* o, float* lse, void* ws, int BH,
-                               int T, int d, float scale, hipStream_t s) {
+                               int T, int d, float scale, hipStream_t s,
+                               const float* k_norm_max) {
+  if (k_norm_max)
+    return decode_dispatch<true, true>(bf16_, q, k_cache, v_cache, bias, H, nullptr, nullptr,
+                                       k_norm_max, o, lse, ws, BH, T, d, scale, s);
   return decode_dispatch<true, false>(bf16_, q, k_cache, v_cache, bias, H, nullptr, nullptr,
                                       nullptr, o, lse, ws, BH, T, d, scale, s);
 }

@@ -377,6 +377,70 @@ int fox_attn_decode_fixed_gate(int dtype, const void* q, const void* k_cache,
                                                 static_cast<hipStream_t>(stream)));
 }
 
+int fox_attn_fwd_fixed_gate_skip(int dtype, const void* q, const void* k, const void* v,
+                                 const float* gate_bias, const float* q_norm_max,
+                                 const float* k_norm_max, void* o, float* lse, int B, int H, int L,
+                                 int d, float scale, void* stream) {
+  if (!all_set({q, k, v, gate_bias, q_norm_max, k_norm_max, o, lse})) return FOX_ERR_NULL;
+  int st = check_dims(B, H, L, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (!all_aligned16({q, k, v, gate_bias, q_norm_max, k_norm_max, o, lse})) return FOX_ERR_ALIGN;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const fox::GateSpec g = fox::gate_fixed(gate_bias, H);
+  if (dtype == FOX_DTYPE_BF16)
+    return launch_status(
+        fox::launch_fwd_bf16(q, k, v, g, o, lse, B * H, L, d, scale, s, q_norm_max, k_norm_max));
+  return launch_status(fox::launch_fwd_f32((const float*)q, (const float*)k, (const float*)v, g,
+                                           (float*)o, lse, B * H, L, d, scale, s));
+}
+
+int fox_attn_bwd_fixed_gate_skip(int dtype, const void* q, const void* k, const void* v,
+                                 const float* gate_bias, const void* o, const float* lse,
+                                 const void* d_o, const float* q_norm_max,
+                                 const float* k_norm_max, void* dq, void* dk, void* dv,
+                                 float* d_gate_bias, void* workspace, size_t workspace_bytes,
+                                 int B, int H, int L, int d, float scale, void* stream) {
+  if (!all_set({q, k, v, gate_bias, o, lse, d_o, q_norm_max, k_norm_max, dq, dk, dv}))
+    return FOX_ERR_NULL;
+  int st = check_dims(B, H, L, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (!all_aligned16({q, k, v, gate_bias, o, lse, d_o, q_norm_max, k_norm_max, dq, dk, dv}) ||
+      (d_gate_bias && !aligned16(d_gate_bias)))
+    return FOX_ERR_ALIGN;
+  if (!workspace || workspace_bytes < fox::bwd_fixed_workspace_bytes(B * H, L))
+    return FOX_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return FOX_ERR_ALIGN;
+  const bool bf = dtype == FOX_DTYPE_BF16;
+  return launch_status(fox::launch_bwd_fixed(bf, q, k, v, gate_bias, H, o, lse, d_o, dq, dk, dv,
+                                             d_gate_bias, workspace, B * H, L, d, scale,
+                                             static_cast<hipStream_t>(stream),
+                                             bf ? q_norm_max : nullptr, bf ? k_norm_max : nullptr));
+}
+
+int fox_attn_decode_fixed_gate_skip(int dtype, const void* q, const void* k_cache,
+                                    const void* v_cache, const float* gate_bias,
+                                    const float* k_norm_max, void* o, float* lse, void* workspace,
+                                    size_t workspace_bytes, int B, int H, int T, int d,
+                                    float scale, void* stream) {
+  if (!all_set({q, k_cache, v_cache, gate_bias, k_norm_max, o, lse})) return FOX_ERR_NULL;
+  int st = check_dims(B, H, T, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (!all_aligned16({q, k_cache, v_cache, gate_bias, k_norm_max, o, lse})) return FOX_ERR_ALIGN;
+  if (!workspace || workspace_bytes < fox::decode_workspace_bytes(B * H, T, d))
+    return FOX_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return FOX_ERR_ALIGN;
+  return launch_status(fox::launch_decode_fixed(dtype == FOX_DTYPE_BF16, q, k_cache, v_cache,
+                                                gate_bias, H, o, lse, workspace, B * H, T, d,
+                                                scale, static_cast<hipStream_t>(stream),
+                                                k_norm_max));
+}
+
 // ---------------------------------------------------------------------------
 // FoX (Pro) prologue and epilogue
 // ---------------------------------------------------------------------------

@@ -59,7 +59,8 @@ size_t bwd_fixed_workspace_bytes(int BH, int L);
 hipError_t launch_bwd_fixed(bool bf16, const void* q, const void* k, const void* v,
                             const float* bias, int H, const void* o, const float* lse,
                             const void* d_o, void* dq, void* dk, void* dv, float* d_bias, void* ws,
-                            int BH, int L, int d, float scale, hipStream_t s);
+                            int BH, int L, int d, float scale, hipStream_t s,
+                            const float* q_norm_max = nullptr, const float* k_norm_max = nullptr);
 
 // out[bh] = max_t ||x[bh, t, :]||_2, enlarged by 2^-10 relative (an upper bound).
 hipError_t launch_row_norm_max(bool bf16, const void* x, float* out, int BH, int L, int d,
@@ -77,10 +78,11 @@ hipError_t launch_decode_skip(bool bf16, const void* q, const void* k_cache, con
                               float* c_cache, const float* logit_new, const float* k_norm_max,
                               void* o, float* lse, void* ws, int BH, int T, int d, float scale,
                               hipStream_t s);
-// Fixed gates: no prefix cache; bias [H].
+// Fixed gates: no prefix cache; bias [H]; with k_norm_max, exact skipping as above.
 hipError_t launch_decode_fixed(bool bf16, const void* q, const void* k_cache, const void* v_cache,
                                const float* bias, int H, void* o, float* lse, void* ws, int BH,
-                               int T, int d, float scale, hipStream_t s);
+                               int T, int d, float scale, hipStream_t s,
+                               const float* k_norm_max = nullptr);
 
 // FoX (Pro) prologue and epilogue (pro_fusions.hip).  Weights [H, d] fp32; shift
 // logits [BH, L] fp32; everything else [BH, L, d] in the storage type.

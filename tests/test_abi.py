@@ -169,6 +169,27 @@ def test_pro_validation_and_workspace(lib):
                                 None) == 7
 
 
+def test_fixed_gate_skip_validation(lib):
+    c = ctypes.c_void_p
+    f = ctypes.c_float(0.1)
+    B, H, L, d = 1, 2, 8, 64
+    assert lib.fox_attn_fwd_fixed_gate_skip(1, *[c(P16)] * 4, None, c(P16), c(P16), c(P16),
+                                            B, H, L, d, f, None) == 1
+    assert lib.fox_attn_fwd_fixed_gate_skip(1, *[c(P16)] * 5, c(P16 + 4), c(P16), c(P16),
+                                            B, H, L, d, f, None) == 4
+    need = lib.fox_attn_bwd_fixed_gate_workspace_bytes(1, B, H, L, d)
+    args = [c(P16)] * 12
+    assert lib.fox_attn_bwd_fixed_gate_skip(1, *args, None, c(P16), need - 1, B, H, L, d, f,
+                                            None) == 5
+    assert lib.fox_attn_bwd_fixed_gate_skip(1, *args[:7], None, *args[8:], None, c(P16), need,
+                                            B, H, L, d, f, None) == 1
+    dneed = lib.fox_attn_decode_workspace_bytes(1, B, H, 100, d)
+    assert lib.fox_attn_decode_fixed_gate_skip(1, *[c(P16)] * 4, None, c(P16), c(P16), c(P16),
+                                               dneed, B, H, 100, d, f, None) == 1
+    assert lib.fox_attn_decode_fixed_gate_skip(1, *[c(P16)] * 7, c(P16), dneed - 1, B, H, 100, d,
+                                               f, None) == 5
+
+
 def test_bwd_validation_and_workspace(lib):
     c = ctypes.c_void_p
     B, H, L, d = 2, 3, 100, 128

@@ -484,6 +484,34 @@ def test_fwd_bwd_skip_is_bitwise_dense(dtype, d, B, H, L, gate):
         assert torch.equal(a, b), name
 
 
+FIXED_SKIP_CASES = [("bf16", 128, 2, 4, 3000, 2.0, 64.0), ("bf16", 64, 1, 3, 4100, 8.0, 4096.0),
+                    ("bf16", 128, 1, 2, 1, 2.0, 4.0), ("f32", 64, 1, 2, 300, 2.0, 16.0)]
+
+
+@pytest.mark.parametrize("dtype,d,B,H,L,tmin,tmax", FIXED_SKIP_CASES)
+def test_fixed_gate_skip_is_bitwise_dense(dtype, d, B, H, L, tmin, tmax):
+    """Fixed gates with exact skipping: O, LSE, dQ, dK, dV, d b and one decode step
+    (the last row against the whole sequence as cache) equal the fixed-gate entry
+    points without skipping bit for bit."""
+    print(f"fixed skip dtype={dtype} d={d} B={B} H={H} L={L} T=({tmin},{tmax})", flush=True)
+    x = inputs.attn_inputs(B, H, L, d, dtype, ("normal", 0.0, 1.0), 1300 + L, device=DEV)
+    s = fox.default_scale(d)
+    b = fox.fox_fixed_gate_init(H, tmin, tmax).to(DEV)
+    qn, kn = fox.fox_row_norm_max(x["q"]), fox.fox_row_norm_max(x["k"])
+    o1, l1 = fox.fox_attn_fwd_fixed_gate(x["q"], x["k"], x["v"], b, s)
+    o2, l2 = fox.fox_attn_fwd_fixed_gate_skip(x["q"], x["k"], x["v"], b, qn, kn, s)
+    g1 = fox.fox_attn_bwd_fixed_gate(x["q"], x["k"], x["v"], b, o1, l1, x["do"], s)
+    g2 = fox.fox_attn_bwd_fixed_gate_skip(x["q"], x["k"], x["v"], b, o1, l1, x["do"], qn, kn, s)
+    qd = x["q"][:, :, -1].contiguous()
+    d1 = fox.fox_attn_decode_fixed_gate(qd, x["k"], x["v"], b, s)
+    d2 = fox.fox_attn_decode_fixed_gate_skip(qd, x["k"], x["v"], b, kn, s)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+    for name, a, c in zip(("dq", "dk", "dv", "db"), g1, g2):
+        assert torch.equal(a, c), name
+    assert torch.equal(d1[0], d2[0]) and torch.equal(d1[1], d2[1])
+
+
 # ------------------------------------------------------------ FoX (Pro) layer
 PRO_EPS = 1e-6
 PRO_GATE = ("normal", 2.0, 1.0)
