@@ -231,6 +231,49 @@ def bench_pro(w, steps, warmup):
     return {n: t.mean_ms() for n, t in timers.items()}
 
 
+def bench_fixed(w, steps, warmup, t_min=2.0):
+    """Fixed per-head gates (ALiBi form) at the training workload's shape, with
+    the appendix initialisation for (T_min, T_max) = (2, L): time constants
+    log-spaced from 2 to L steps over the heads.  The fwd+bwd step dense and
+    with exact skipping (bound kernels included); outputs must agree bit for bit."""
+    dev = torch.device("cuda:0")
+    x = inputs.workload_inputs(w, device=dev)
+    B, H, L, d = w.B, w.H, w.L, w.d
+    s = fox.default_scale(d)
+    b = fox.fox_fixed_gate_init(H, t_min, float(L)).to(dev)
+    ws = torch.empty(fox.fox_attn_bwd_fixed_gate_workspace_bytes(x["q"].dtype, B, H, L, d),
+                     device=dev, dtype=torch.uint8)
+    out = {}
+
+    def dense():
+        o, lse = fox.fox_attn_fwd_fixed_gate(x["q"], x["k"], x["v"], b, s)
+        g = fox.fox_attn_bwd_fixed_gate(x["q"], x["k"], x["v"], b, o, lse, x["do"], s,
+                                        workspace=ws)
+        out["dense"] = (o, lse) + tuple(g)
+
+    def skip():
+        qn, kn = fox.fox_row_norm_max(x["q"]), fox.fox_row_norm_max(x["k"])
+        o, lse = fox.fox_attn_fwd_fixed_gate_skip(x["q"], x["k"], x["v"], b, qn, kn, s)
+        g = fox.fox_attn_bwd_fixed_gate_skip(x["q"], x["k"], x["v"], b, o, lse, x["do"], qn, kn,
+                                             s, workspace=ws)
+        out["skip"] = (o, lse) + tuple(g)
+
+    res = {}
+    for name, fn in (("dense", dense), ("skip", skip)):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        t = EventTimer()
+        for _ in range(steps):
+            with t:
+                fn()
+        torch.cuda.synchronize()
+        res[name] = t.mean_ms()
+    if not all(torch.equal(a, c) for a, c in zip(out["dense"], out["skip"])):
+        raise RuntimeError("the fixed-gate skipping step differs from the dense step")
+    return res
+
+
 def bench_decode(w, steps, warmup):
     dev = torch.device("cuda:0")
     y = inputs.workload_inputs(w, device=dev)
@@ -416,6 +459,7 @@ def main():
     ap.add_argument("--decode-workload", default="decode_bf16_b64_h16_t32768_d128")
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-pro", action="store_true", help="skip the FoX (Pro) layer timings")
+    ap.add_argument("--no-fixed", action="store_true", help="skip the fixed-gate timings")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="run a plain device copy of this size first (counter calibration)")
@@ -494,6 +538,16 @@ def main():
     }
     log(f"[bench] train step {r['ms']:.3f} ms -> {tflops:.1f} TFLOP/s; with skipping "
         f"{r['skip_ms']:.3f} ms")
+    if not args.no_fixed:
+        rf = bench_fixed(w, args.steps, args.warmup)
+        out["fixed_gate"] = {
+            "what": "fixed per-head gates f = sigmoid(b_h) (ALiBi form), appendix initialisation "
+                    "with (T_min, T_max) = (2, L); fwd+bwd step dense and with exact skipping "
+                    "(bound kernels included), outputs bitwise equal",
+            "dense_ms": round(rf["dense"], 4), "skip_ms": round(rf["skip"], 4),
+            "speedup": round(rf["dense"] / rf["skip"], 3),
+            "dense_TFLOP/s": round((fl_f + fl_b) / (rf["dense"] * 1e-3) / 1e12, 2)}
+        log(f"[bench] fixed gates: step {rf['dense']:.3f} ms, with skipping {rf['skip']:.3f} ms")
     if not args.no_pro:
         rp = bench_pro(w, args.steps, args.warmup)
         rows = B * H * L

@@ -613,3 +613,64 @@ def test_pro_layer_chain_bf16():
              "dwk")
     for name, g, r in zip(names, got, ref):
         check_grad("bf16", name, g, r, "chain")
+
+
+def test_workload_pro_bf16_b2_h16_l16384_d128():
+    """The FoX (Pro) layer at the benchmark's shape and launch configuration.  The
+    prologue and the output norm/gate are row-local, so the oracle checks them on
+    whole heads: the prologue forward and backward on the slices of head 15 (its
+    weight gradients sum over both batch rows), y on sampled query rows (oracle
+    attention rows, then the output norm and gate), the norm/gate backward (dg,
+    dw_o) on every row of head 15 from the stored O; the attention backward that
+    follows it equals fox_attn_bwd fed the oracle's dO."""
+    w = W["fwdbwd_bf16_b2_h16_l16384_d128"]
+    B, H, L, d = w.B, w.H, w.L, w.d
+    x = inputs.pro_inputs(B, H, L, d, w.dtype, w.gate, w.seed + 1, device=DEV)
+    s = fox.default_scale(d)
+    pargs = (x["q_raw"], x["k_raw"], x["v_raw"], x["k_shift"], x["v_shift"], x["wq"], x["wk"])
+    q, k, v = fox.fox_pro_prologue(*pargs, eps=PRO_EPS)
+    c = fox.fox_gate_prefix(x["logit"])
+    y, o, lse = fox.fox_attn_fwd_pro(q, k, v, c, x["g"], x["wo"], s, eps=PRO_EPS)
+    dq, dk, dv, dlf, dg, dwo = fox.fox_attn_bwd_pro(q, k, v, c, o, lse, x["g"], x["wo"], x["dy"],
+                                                    s, eps=PRO_EPS)
+    pg = fox.fox_pro_prologue_bwd(*pargs, dq, dk, dv, eps=PRO_EPS)
+    torch.cuda.synchronize()
+    h = 15
+    print(f"pro workload: oracle on head {h}", flush=True)
+    sl = {n: t[:, h:h + 1].cpu() for n, t in x.items() if t.dim() >= 3}
+    wsl = {n: x[n][h:h + 1].cpu() for n in ("wq", "wk", "wo")}
+    # prologue forward and backward (both batch rows of head h)
+    ref = oracle.pro_prologue(sl["q_raw"], sl["k_raw"], sl["v_raw"], sl["k_shift"],
+                              sl["v_shift"], wsl["wq"], wsl["wk"], PRO_EPS)
+    for name, g_, r in zip("qkv", (q, k, v), ref):
+        check_out("bf16", name, g_[:, h:h + 1], r, "pro workload")
+    gsl = [t[:, h:h + 1].cpu() for t in (dq, dk, dv)]
+    pref = oracle.pro_prologue_backward(sl["q_raw"], sl["k_raw"], sl["v_raw"], sl["k_shift"],
+                                        sl["v_shift"], wsl["wq"], wsl["wk"], PRO_EPS, *gsl)
+    got = [t[:, h:h + 1] for t in pg[:5]] + [pg[5][h:h + 1], pg[6][h:h + 1]]
+    for name, g_, r in zip(("dq_raw", "dk_raw", "dv_raw", "dk_shift", "dv_shift", "dwq", "dwk"),
+                           got, pref):
+        check_grad("bf16", name, g_, r, "pro workload")
+    del ref, pref
+    # y on sampled rows of (b, h) = (1, h): oracle attention rows, then the norm and gate
+    rows = torch.tensor([0, 1, 63, 64, 4095, 8191, 12000, L - 2, L - 1])
+    qs = [t[1, h].cpu() for t in (q, k, v)]
+    O_rows, _ = oracle.forward_head_from_c(*qs, oracle.prefix_c(oracle.log_sigmoid(
+        x["logit"][1, h].cpu())), s, rows=rows)
+    Y_rows = oracle.output_gate(O_rows[None, None], x["g"][1, h, rows].cpu()[None, None],
+                                wsl["wo"], PRO_EPS)[0, 0]
+    check_out("bf16", "y rows", y[1, h, rows], Y_rows, "pro workload")
+    # the norm/gate backward from the stored O (every row of head h)
+    dO_h, dg_h, dwo_h = oracle.output_gate_backward(o[:, h:h + 1].cpu(), sl["g"], wsl["wo"],
+                                                    PRO_EPS, sl["dy"])
+    check_grad("bf16", "dg", dg[:, h:h + 1], dg_h, "pro workload")
+    check_grad("bf16", "dwo", dwo[h:h + 1], dwo_h, "pro workload")
+    del dO_h, dg_h
+    # the attention backward behind it: fox_attn_bwd with the oracle's dO (all heads)
+    dO_ref = oracle.output_gate_backward(o.cpu(), x["g"].cpu(), x["wo"].cpu(), PRO_EPS,
+                                         x["dy"].cpu())[0].to(torch.bfloat16).to(DEV)
+    ref2 = fox.fox_attn_bwd(q, k, v, c, o, lse, dO_ref, s)
+    torch.cuda.synchronize()
+    for name, g_, r in zip(("dq", "dk", "dv", "dlogf"), (dq, dk, dv, dlf), ref2):
+        e = rel_l2(g_, r)
+        assert e <= 1e-2, f"pro workload {name} vs fox_attn_bwd with the oracle's dO: {e:.3e}"
