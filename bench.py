@@ -436,6 +436,56 @@ def pmc_summary(fetch_dir, write_dir, copy_mib, command):
     return "\n".join(lines) + "\n"
 
 
+SQ_PASS_A = ("SQ_INSTS_MFMA", "SQ_INSTS_VALU", "SQ_INSTS_LDS", "SQ_INSTS_SALU",
+             "SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_WAVE_CYCLES", "SQ_INSTS_VALU_TRANS_F32")
+SQ_PASS_B = ("SQ_VALU_MFMA_BUSY_CYCLES", "SQ_VALU_MFMA_COEXEC_CYCLES", "SQ_BUSY_CYCLES",
+             "SQ_LDS_BANK_CONFLICT", "SQ_WAIT_INST_ANY", "SQ_WAIT_ANY", "SQ_ACTIVE_INST_VALU",
+             "SQ_ACTIVE_INST_LDS")
+SQ_KERNELS = ("fwd_bf16_kernel<128,false,false,false>", "bwd_dkdv_bf16_kernel<128,false,false>",
+              "bwd_dq_bf16_kernel<128,false,false>")
+
+
+def sq_summary(dirs, command, ms):
+    """Text summary of rocprofv3 --pmc passes (SQ_PASS_A, SQ_PASS_B) over this
+    benchmark: per dense attention kernel, instruction mix, MFMA work and issue
+    counters.  `ms` maps kernel -> average duration (ms) from a kernel trace of the
+    same command; MFMA utilisation = executed MFMA FLOPs / (duration x peak)."""
+    per = {}
+    for d in dirs:
+        for r in _counter_rows(d):
+            k = _kernel_key(r["Kernel_Name"])
+            if k not in SQ_KERNELS:
+                continue
+            c = per.setdefault(k, {}).setdefault(r["Counter_Name"], {})
+            c[r["Dispatch_Id"]] = c.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+    lines = ["# SQ counters of the dense attention kernels (rocprofv3 --pmc, two passes)",
+             f"# command (one pass per counter set): {command}",
+             "#   pass A: " + " ".join(SQ_PASS_A), "#   pass B: " + " ".join(SQ_PASS_B),
+             "# values: mean per dispatch; MOPS_BF16 counts 512-FLOP MFMA operations"]
+    for k in SQ_KERNELS:
+        if k not in per:
+            continue
+        v = {n: sum(x.values()) / len(x) for n, x in per[k].items()}
+        lines.append(f"\n## {k}")
+        for n in SQ_PASS_A + SQ_PASS_B:
+            if n in v:
+                lines.append(f"{n:32s} {v[n]:.6g}")
+        mf = v.get("SQ_INSTS_MFMA", 0.0)
+        if mf:
+            lines.append(f"{'non-MFMA VALU per MFMA':32s} {(v['SQ_INSTS_VALU'] - mf) / mf:.3f}")
+            lines.append(f"{'LDS instructions per MFMA':32s} {v['SQ_INSTS_LDS'] / mf:.3f}")
+        if v.get("SQ_VALU_MFMA_BUSY_CYCLES"):
+            lines.append(f"{'MFMA/VALU co-issue share':32s} "
+                         f"{v['SQ_VALU_MFMA_COEXEC_CYCLES'] / v['SQ_VALU_MFMA_BUSY_CYCLES']:.3f}")
+        if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in v and k in ms:
+            fl = v["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512.0
+            lines.append(f"{'executed MFMA FLOPs':32s} {fl:.4g}")
+            lines.append(f"{'trace duration ms':32s} {ms[k]:.4f}")
+            lines.append(f"{'MFMA utilisation of 2516.6 TF':32s} "
+                         f"{fl / (ms[k] * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS:.4f}")
+    return "\n".join(lines) + "\n"
+
+
 def measured_traffic(kernel: str):
     """Bytes per launch recorded for `kernel` (family<template arguments>), or
     None when there is no record or the family's sources changed since the
@@ -466,7 +516,21 @@ def main():
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 --pmc passes of this benchmark and exit")
     ap.add_argument("--pmc-command", default="", help="the profiled command, for the summary")
+    ap.add_argument("--sq-summary", nargs="+", metavar="DIR",
+                    help="summarise rocprofv3 --pmc SQ passes of this benchmark and exit; the "
+                         "last argument is a kernel-trace results.db for the durations")
     args = ap.parse_args()
+    if args.sq_summary:
+        import sqlite3
+        *dirs, db = args.sq_summary
+        con = sqlite3.connect(db)
+        ms = {}
+        for name, avg in con.execute("select name, average from top_kernels"):
+            k = _kernel_key(name)
+            if k in SQ_KERNELS:
+                ms[k] = float(avg) / 1e3  # microseconds -> ms
+        print(sq_summary(dirs, args.pmc_command, ms), end="")
+        return
     if args.pmc_summary:
         print(pmc_summary(*args.pmc_summary, args.calibrate_copy_mib or 1024, args.pmc_command),
               end="")
