@@ -20,6 +20,7 @@
 // The forget-gate bias is formed relative to c_ref (the first query of the
 // block for dq, the first key of the block for dkdv), exactly as in the forward:
 //     log2 P_ij = s log2(e) q_i.k_j + log2(e) ((c_i - c_ref) - LSE_i) - log2(e) (c_j - c_ref).
+#include <cstddef>
 #include <type_traits>
 
 #include "fox_device.h"
@@ -115,8 +116,7 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
   const uint32_t head_bytes = (uint32_t)L * D * 2;
   const __amdgpu_buffer_rsrc_t rk = make_rsrc(K + head * D, head_bytes);
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(V + head * D, head_bytes);
-  uint32_t dma_off[NDMA];
-  tile_dma_offsets<D, NDMA>(dma_off, wave, kDqWaves, lane);
+  const uint32_t dma_off = tile_dma_offset<D, kDqWaves>(wave, lane);
   int roff[D / 16];
   tile_row_offsets<D>(roff, col, h);
   int toff[2][D / 32];
@@ -154,49 +154,71 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
 
   const float inv_scale = 1.0f / scale;
   const float skip_norm = SKIP ? 2.0f * scale * qnorm[bh] * knorm[bh] : 0.0f;
-  float creg = 0.0f, crefreg = 0.0f;
-  bool skipreg = false;
+  // Wave 0 loads the next tile's prefix values (one key per lane, and the
+  // tile's reference value) before its share of the tile DMA and turns them
+  // into the LDS row terms only after the current tile's body: memory
+  // operations complete in order, so a wait for them issued right away, or
+  // for loads issued after the DMA, would also wait for the DMA.
+  const float c_q0 = gr.raw(q0);
+  float craw = 0.0f, crefreg = 0.0f;
   auto issue_tile = [&](int kt, auto bufc) {
     constexpr int B = decltype(bufc)::value;
     const uint32_t base = (uint32_t)kt * kDqBN * D * 2;
+    if (wave == 0) {
+      const int key = kt * kDqBN + lane;
+      crefreg = gr.raw(kt * kDqBN / kRefBlock * kRefBlock);
+      craw = key < L ? gr.raw(key) : 0.0f;
+    }
 #pragma unroll
     for (int i = 0; i < NDMA; ++i) {
       const int wslot = (i * kDqWaves + wave) * 512;
-      dma16(rk, &sm.k[B][wslot], base + dma_off[i]);
-      dma16(rv, &sm.v[B][wslot], base + dma_off[i]);
+      const uint32_t voff = dma_off + uniform_u32(base + i * tile_dma_stride<kDqWaves>());
+      dma16(rk, &sm.k[B][wslot], voff);
+      dma16(rv, &sm.v[B][wslot], voff);
     }
+  };
+  auto store_c = [&](int kt, auto bufc) {
+    constexpr int B = decltype(bufc)::value;
     if (wave == 0) {
       const int key = kt * kDqBN + lane;
       const int kref = kt * kDqBN / kRefBlock * kRefBlock;
-      if constexpr (!FIXED) crefreg = gr.c[kref];
-      creg = key < L ? gr.diff(key, kref) * kLog2e : INFINITY;
-      if constexpr (SKIP) {
-        // the tile's last key against the block's first query
-        if (lane == kDqBN - 1)
-          skipreg = key < L && kLog2e * (skip_norm + gr.diff(q0, key)) < -kSkipMargin;
-      }
-    }
-  };
-  auto store_c = [&](auto bufc) {
-    constexpr int B = decltype(bufc)::value;
-    if (wave == 0) {
-      sm.c[B][lane] = creg;
+      sm.c[B][lane] = key < L ? gr.diff_raw(key, craw, kref, crefreg) * kLog2e : INFINITY;
       if (lane == 0) sm.cref[B] = crefreg;
-      if (SKIP && lane == kDqBN - 1) sm.skip[B] = skipreg;
+      // the tile's last key against the block's first query
+      if (SKIP && lane == kDqBN - 1)
+        sm.skip[B] = key < L && kLog2e * (skip_norm + gr.diff_raw(q0, c_q0, key, craw)) < -kSkipMargin;
     }
   };
+
+  // LDS operand addresses: a few opaque per-lane registers plus immediates.
+  // Reads through them (and the transposing reads in assembly) are not taken
+  // for possible readers of the tile that is loading by DMA meanwhile, so the
+  // compiler adds no wait for that DMA before them; they only ever read the
+  // other buffer.  The V tiles sit at a fixed distance from the K tiles.
+  constexpr int kVOff = 2 * 2 * TILE;  // bytes from sm.k[0] to sm.v[0]
+  static_assert(offsetof(DqSmem<D>, v) - offsetof(DqSmem<D>, k) == (size_t)kVOff,
+                "V tiles follow the K tiles");
+  const lds_byte* ka_at[D / 16];
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s) ka_at[s] = lds_opaque(lds_ptr(&sm.k[0][0]) + 2 * roff[s]);
+  uint32_t taddr[2][D / 32];
+#pragma unroll
+  for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+      taddr[k2][db] = (uint32_t)(uintptr_t)lds_opaque(lds_ptr(&sm.k[0][0]) + 2 * toff[k2][db]);
+  const lds_byte* c_at = lds_opaque(lds_ptr(&sm.c[0][4 * h]));
+  const lds_byte* cref_at = lds_opaque(lds_ptr(&sm.cref[0]));
 
   auto tile_body = [&](int j, auto bufc, auto masked) {
     constexpr int B = decltype(bufc)::value;
     constexpr bool MASK = decltype(masked)::value;
-    const bf16* kt_ = sm.k[B];
-    const bf16* vt_ = sm.v[B];
-    const float* ct_ = sm.c[B];
     const int key0 = j * kDqBN;
-    const float dref = FIXED ? gr.diff(qi, key0 / kRefBlock * kRefBlock) : cq - sm.cref[B];
+    const float dref = FIXED ? gr.diff(qi, key0 / kRefBlock * kRefBlock)
+                             : cq - *(const lds_f32_t*)(cref_at + 4 * B);
     const float bq = q_valid ? (dref - lse_q) * inv_scale : -INFINITY;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    static_for<2>([&](auto kbc) {
+      constexpr int kb = decltype(kbc)::value;
       f32x16 sacc, pacc;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
@@ -207,7 +229,7 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
         bf16x8 ka[D / 16];
 #pragma unroll
         for (int s = 0; s < D / 16; ++s)
-          ka[s] = *reinterpret_cast<const bf16x8*>(kt_ + kb * 32 * D + roff[s]);
+          ka[s] = *(const lds_bf16x8_t*)(ka_at[s] + 2 * (B * TILE + kb * 32 * D));
         sched_fence();
 #pragma unroll
         for (int s = 0; s < D / 16; ++s) sacc = mfma32(ka[s], qf[s], sacc);
@@ -216,7 +238,7 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
         bf16x8 va[D / 16];
 #pragma unroll
         for (int s = 0; s < D / 16; ++s)
-          va[s] = *reinterpret_cast<const bf16x8*>(vt_ + kb * 32 * D + roff[s]);
+          va[s] = *(const lds_bf16x8_t*)(ka_at[s] + kVOff + 2 * (B * TILE + kb * 32 * D));
         sched_fence();
 #pragma unroll
         for (int s = 0; s < D / 16; ++s) pacc = mfma32(va[s], dof[s], pacc);
@@ -224,7 +246,7 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
       float pv[16];
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const f32x4 ck4 = *reinterpret_cast<const f32x4*>(ct_ + kb * 32 + 8 * g + 4 * h);
+        const f32x4 ck4 = *(const lds_f32x4_t*)(c_at + 4 * (B * kDqBN + kb * 32 + 8 * g));
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj) {
           float p = exp2_fast(sacc[4 * g + jj] * scale_log2 - ck4[jj]);
@@ -242,17 +264,22 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
         dcq_part += ds;  // dc^q and dc^k sum fp32 dS, the row and column sums of one matrix
         dsv[r] = ds;
       }
-#pragma unroll
-      for (int c = 0; c < 2; ++c) {
+      static_for<2>([&](auto cc) {
+        constexpr int c = decltype(cc)::value;
+        constexpr int OFF = 2 * (B * TILE + (2 * kb + c) * 16 * D);
         const bf16x8 dsb = pack8(&dsv[8 * c]);
-        bf16x8 ta[D / 32];
+        bf16x4 t[2 * (D / 32)];
+        static_for<D / 32>([&](auto dbc) {
+          constexpr int db = decltype(dbc)::value;
+          t[2 * db] = ds_read_tr_asm<OFF>(taddr[0][db]);
+          t[2 * db + 1] = ds_read_tr_asm<OFF>(taddr[1][db]);
+        });
+        lds_wait<0>(t);
 #pragma unroll
-        for (int db = 0; db < D / 32; ++db) ta[db] = tile_tr_operand<D>(kt_, toff, 2 * kb + c, db);
-        sched_fence();
-#pragma unroll
-        for (int db = 0; db < D / 32; ++db) dqacc[db] = mfma32(ta[db], dsb, dqacc[db]);
-      }
-    }
+        for (int db = 0; db < D / 32; ++db)
+          dqacc[db] = mfma32(cat4(t[2 * db], t[2 * db + 1]), dsb, dqacc[db]);
+      });
+    });
   };
 
   // returns true when tile j and all earlier tiles can be skipped
@@ -267,12 +294,12 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
     } else if (j < t_diag) {
       tile_body(j, bufc, std::false_type());
     }
-    if (j > 0) store_c(std::integral_constant<int, 1 - B>());
+    if (j > 0) store_c(j - 1, std::integral_constant<int, 1 - B>());
     return false;
   };
 
   issue_tile(t_last, std::integral_constant<int, 0>());
-  store_c(std::integral_constant<int, 0>());
+  store_c(t_last, std::integral_constant<int, 0>());
   for (int j = t_last; j >= 0; j -= 2) {
     if (step(j, std::integral_constant<int, 0>())) break;
     if (j > 0 && step(j - 1, std::integral_constant<int, 1>())) break;
@@ -366,8 +393,7 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
   const uint32_t head_bytes = (uint32_t)L * D * 2;
   const __amdgpu_buffer_rsrc_t rq = make_rsrc(Q + head * D, head_bytes);
   const __amdgpu_buffer_rsrc_t rg = make_rsrc(dO + head * D, head_bytes);
-  uint32_t dma_off[NDMA];
-  tile_dma_offsets<D, NDMA>(dma_off, wave, kKvWaves, lane);
+  const uint32_t dma_off = tile_dma_offset<D, kKvWaves>(wave, lane);
   int roff[D / 16];
   tile_row_offsets<D>(roff, col, h);
   int toff[2][D / 32];
@@ -471,8 +497,9 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
 #pragma unroll
     for (int i = 0; i < NDMA; ++i) {
       const int wslot = (i * kKvWaves + wave) * 512;
-      dma16(rq, &sm.q[B][wslot], base + dma_off[i]);
-      dma16(rg, &sm.g[B][wslot], base + dma_off[i]);
+      const uint32_t voff = dma_off + uniform_u32(base + i * tile_dma_stride<kKvWaves>());
+      dma16(rq, &sm.q[B][wslot], voff);
+      dma16(rg, &sm.g[B][wslot], voff);
     }
   };
 

@@ -109,8 +109,7 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
   const __amdgpu_buffer_rsrc_t rk = make_rsrc(K + head * D, head_bytes);
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(V + head * D, head_bytes);
 
-  uint32_t dma_off[NDMA];
-  tile_dma_offsets<D, NDMA>(dma_off, wave, kFwdWaves, lane);
+  const uint32_t dma_off = tile_dma_offset<D, kFwdWaves>(wave, lane);
   int koff[D / 16];
   tile_row_offsets<D>(koff, col, h);
   int voff[2][D / 32];
@@ -157,8 +156,9 @@ void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
 #pragma unroll
     for (int i = 0; i < NDMA; ++i) {
       const int wslot = (i * kFwdWaves + wave) * 512;  // bf16 elements of this wave's 1 KB
-      dma16(rk, &sm.k[B][wslot], base + dma_off[i]);
-      dma16(rv, &sm.v[B][wslot], base + dma_off[i]);
+      const uint32_t voff = dma_off + uniform_u32(base + i * tile_dma_stride<kFwdWaves>());
+      dma16(rk, &sm.k[B][wslot], voff);
+      dma16(rv, &sm.v[B][wslot], voff);
     }
     if (wave == 0) {
       ckey = kt * kFwdBN + lane;

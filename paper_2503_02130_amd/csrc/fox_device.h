@@ -152,9 +152,17 @@ struct GateRow<true> {
   float lf;
   __device__ GateRow(const float* gate, int bh, int H, size_t /*row*/)
       : lf(log_sigmoid(gate[bh % H])) {}
-  __device__ float diff(int i, int j) const { return (float)(i - j) * lf; }
+  // The slope passes through an empty asm at each use: otherwise the compiler
+  // hoists products of it out of the tile loops and the kernels run out of
+  // registers.
+  __device__ float slope() const {
+    float x = lf;
+    asm volatile("" : "+v"(x));
+    return x;
+  }
+  __device__ float diff(int i, int j) const { return (float)(i - j) * slope(); }
   __device__ float raw(int) const { return 0.0f; }
-  __device__ float diff_raw(int i, float, int j, float) const { return (float)(i - j) * lf; }
+  __device__ float diff_raw(int i, float, int j, float) const { return (float)(i - j) * slope(); }
 };
 
 // ---------------------------------------------------------------------------
@@ -197,6 +205,7 @@ __device__ __forceinline__ bf16x4 lds_read_tr16(const bf16* p) {
 typedef __attribute__((address_space(3))) char lds_byte;
 typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8_t;
 typedef __attribute__((address_space(3))) f32x4 lds_f32x4_t;
+typedef __attribute__((address_space(3))) float lds_f32_t;
 
 template <typename T>
 __device__ __forceinline__ const lds_byte* lds_ptr(const T* generic) {
@@ -277,19 +286,27 @@ __device__ __forceinline__ int swz_chunk(int r, int c) {
   return c ^ f;
 }
 
-// Global byte offsets (relative to the tile's first row) of the 16-byte chunks a
-// wave moves with its DMA loads: load i of wave w fills LDS slots
-// [(i * nwaves + w) * 64, +64), and slot s holds logical chunk swz(r, s % CPR) of
-// row r = s / CPR.
-template <int D, int NDMA>
-__device__ __forceinline__ void tile_dma_offsets(uint32_t (&off)[NDMA], int wave, int nwaves,
-                                                 int lane) {
-#pragma unroll
-  for (int i = 0; i < NDMA; ++i) {
-    const int slot = (i * nwaves + wave) * 64 + lane;
-    const int r = slot / (D / 8);
-    off[i] = (uint32_t)(r * D * 2 + swz_chunk<D>(r, slot % (D / 8)) * 16);
-  }
+// Global byte offset (relative to the tile's first row) of the 16-byte chunk a
+// wave's first DMA load moves for this lane: load i of wave w fills LDS slots
+// [(i * NWAVES + w) * 64, +64), and slot s holds logical chunk swz(r, s % CPR) of
+// row r = s / CPR.  One load covers NWAVES * 64 / CPR rows, a whole number of the
+// swizzle's 16-row periods, so load i moves the chunks of load 0 shifted by
+// i * tile_dma_stride<NWAVES>() bytes: one register per lane serves every load.
+template <int D, int NWAVES>
+__device__ __forceinline__ uint32_t tile_dma_offset(int wave, int lane) {
+  static_assert((NWAVES * 64 / (D / 8)) % 16 == 0, "a DMA load covers whole 16-row periods");
+  const int slot = wave * 64 + lane;
+  const int r = slot / (D / 8);
+  return (uint32_t)(r * D * 2 + swz_chunk<D>(r, slot % (D / 8)) * 16);
+}
+template <int NWAVES>
+constexpr uint32_t tile_dma_stride() { return NWAVES * 64 * 16; }
+
+// A wave-uniform value the compiler keeps in a scalar register and does not
+// reassociate with per-lane terms (so no per-load sum is hoisted into a vector
+// register).
+__device__ __forceinline__ uint32_t uniform_u32(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_readfirstlane((int)x);
 }
 
 // Element offsets of a lane's plain MFMA-operand reads from a swizzled tile:
