@@ -45,6 +45,7 @@ TRAFFIC_FILE = os.path.join(PROFILES, "hbm_traffic_bench_fwdbwd_l16384_decode_t3
 KERNEL_SOURCES = {
     "bwd_dkdv_bf16_kernel": ("attn_bwd.hip", "fox_device.h"),
     "bwd_dq_bf16_kernel": ("attn_bwd.hip", "fox_device.h"),
+    "bwd_dq_stored_kernel": ("attn_bwd.hip", "fox_device.h"),
     "fwd_bf16_kernel": ("attn_fwd.hip", "fox_device.h"),
     "decode_split_kernel": ("attn_decode.hip", "fox_device.h"),
     "pro_prologue_kernel": ("pro_fusions.hip", "fox_device.h"),
@@ -107,10 +108,11 @@ class EventTimer:
 
 
 def bench_train(w, steps, warmup):
-    """One step = gate prefix -> forward -> backward, the backward through its
-    stage entry points (what fox_attn_bwd runs, its last stage also producing the
-    gate-logit gradient) so that the dominant kernel, dK/dV, can be bracketed by
-    events on the call stream."""
+    """One step = gate prefix -> forward -> backward keeping dS (the stages of
+    fox_attn_bwd_stored, the last one also producing the gate-logit gradient), so
+    that the dominant kernel, dK/dV with the dS store, can be bracketed by events
+    on the call stream.  After it, the same step with the recompute backward (the
+    stages of fox_attn_bwd, O(L) workspace) and with exact skipping."""
     dev = torch.device("cuda:0")
     x = inputs.workload_inputs(w, device=dev)
     s = fox.default_scale(w.d)
@@ -120,6 +122,8 @@ def bench_train(w, steps, warmup):
     lse = torch.empty((B, H, L), device=dev)
     dq, dk, dv = torch.empty_like(x["q"]), torch.empty_like(x["k"]), torch.empty_like(x["v"])
     dlf, dlogit, delta, dcq, dck = (torch.empty((B, H, L), device=dev) for _ in range(5))
+    store = torch.empty(fox.fox_attn_bwd_ds_store_bytes(x["q"].dtype, B, H, L, d), device=dev,
+                        dtype=torch.uint8)
     t_gate, t_fwd, t_dkdv, t_dq, t_bwd = (EventTimer() for _ in range(5))
 
     def step(timed):
@@ -130,11 +134,10 @@ def bench_train(w, steps, warmup):
         with t_bwd.maybe(timed):
             fox.fox_attn_bwd_delta(o, x["do"], delta=delta)
             with t_dkdv.maybe(timed):
-                fox.fox_attn_bwd_dkdv(x["q"], x["k"], x["v"], c, lse, x["do"], delta, s, dk=dk,
-                                      dv=dv, dc_k=dck)
+                fox.fox_attn_bwd_dkdv_store(x["q"], x["k"], x["v"], c, lse, x["do"], delta, store,
+                                            s, dk=dk, dv=dv, dc_k=dck)
             with t_dq.maybe(timed):
-                fox.fox_attn_bwd_dq(x["q"], x["k"], x["v"], c, lse, x["do"], delta, s, dq=dq,
-                                    dc_q=dcq)
+                fox.fox_attn_bwd_dq_stored(x["k"], store, s, dq=dq, dc_q=dcq)
             fox.fox_dlogit_from_dc(dcq, dck, x["logit"], d_logit=dlogit, d_log_f=dlf)
 
     for _ in range(warmup):
@@ -152,9 +155,39 @@ def bench_train(w, steps, warmup):
     ms = start.elapsed_time(end) / steps
     if not (torch.isfinite(o.float()).all() and torch.isfinite(dlf).all()):
         raise RuntimeError("non-finite outputs")
+    stored = [t.clone() for t in (dq, dk, dv, dlf)]
 
-    # The same step with exact gate-aware skipping (row-norm bounds computed
-    # inside the timed step); its outputs must equal the dense step's bit for bit.
+    # The recompute backward: dK/dV bit for bit the same, dQ and d(log f) equal to
+    # rounding (the two dQ passes sum the same bf16 dS in different orders).
+    r_dkdv, r_dq, r_step = EventTimer(), EventTimer(), EventTimer()
+
+    def step_recompute(timed):
+        with r_step.maybe(timed):
+            fox.fox_gate_prefix(x["logit"], c=c)
+            fox.fox_attn_fwd(x["q"], x["k"], x["v"], c, s, o=o, lse=lse)
+            fox.fox_attn_bwd_delta(o, x["do"], delta=delta)
+            with r_dkdv.maybe(timed):
+                fox.fox_attn_bwd_dkdv(x["q"], x["k"], x["v"], c, lse, x["do"], delta, s, dk=dk,
+                                      dv=dv, dc_k=dck)
+            with r_dq.maybe(timed):
+                fox.fox_attn_bwd_dq(x["q"], x["k"], x["v"], c, lse, x["do"], delta, s, dq=dq,
+                                    dc_q=dcq)
+            fox.fox_dlogit_from_dc(dcq, dck, x["logit"], d_logit=dlogit, d_log_f=dlf)
+
+    for _ in range(warmup):
+        step_recompute(False)
+    for _ in range(steps):
+        step_recompute(True)
+    torch.cuda.synchronize()
+    if not (torch.equal(stored[1], dk) and torch.equal(stored[2], dv)):
+        raise RuntimeError("dK/dV of the stored-dS backward differ from the recompute path")
+    for a, b, name in ((stored[0], dq, "dQ"), (stored[3], dlf, "d(log f)")):
+        e = float(torch.linalg.vector_norm((a - b).float()) / torch.linalg.vector_norm(b.float()))
+        if e > 5e-3:
+            raise RuntimeError(f"{name} of the two backward paths differ: rel-L2 {e:.3e}")
+
+    # The recompute step with exact gate-aware skipping (row-norm bounds computed
+    # inside the timed step); its outputs must equal the recompute step's bit for bit.
     ref = [t.clone() for t in (o, lse, dq, dk, dv, dlf)]
     qn = torch.empty((B, H), device=dev)
     kn = torch.empty((B, H), device=dev)
@@ -181,7 +214,8 @@ def bench_train(w, steps, warmup):
         raise RuntimeError("the skipping step differs from the dense step")
     return {"ms": ms, "wall_ms": wall_ms, "gate_ms": t_gate.mean_ms(), "fwd_ms": t_fwd.mean_ms(),
             "bwd_ms": t_bwd.mean_ms(), "dkdv_ms": t_dkdv.mean_ms(), "dq_ms": t_dq.mean_ms(),
-            "skip_ms": t_skip.mean_ms()}
+            "rc_ms": r_step.mean_ms(), "rc_dkdv_ms": r_dkdv.mean_ms(), "rc_dq_ms": r_dq.mean_ms(),
+            "skip_ms": t_skip.mean_ms(), "store_bytes": store.numel()}
 
 
 def bench_pro(w, steps, warmup):
@@ -441,8 +475,10 @@ SQ_PASS_A = ("SQ_INSTS_MFMA", "SQ_INSTS_VALU", "SQ_INSTS_LDS", "SQ_INSTS_SALU",
 SQ_PASS_B = ("SQ_VALU_MFMA_BUSY_CYCLES", "SQ_VALU_MFMA_COEXEC_CYCLES", "SQ_BUSY_CYCLES",
              "SQ_LDS_BANK_CONFLICT", "SQ_WAIT_INST_ANY", "SQ_WAIT_ANY", "SQ_ACTIVE_INST_VALU",
              "SQ_ACTIVE_INST_LDS")
-SQ_KERNELS = ("fwd_bf16_kernel<128,false,false,false>", "bwd_dkdv_bf16_kernel<128,false,false>",
-              "bwd_dq_bf16_kernel<128,false,false>")
+SQ_KERNELS = ("fwd_bf16_kernel<128,false,false,false>",
+              "bwd_dkdv_bf16_kernel<128,false,false,false>",
+              "bwd_dkdv_bf16_kernel<128,false,false,true>", "bwd_dq_bf16_kernel<128,false,false>",
+              "bwd_dq_stored_kernel<128>")
 
 
 def sq_summary(dirs, command, ms):
@@ -558,9 +594,13 @@ def main():
     fl_kv = 8.0 * d * causal_pairs(B, H, L)
     kv_tf = fl_kv / (r["dkdv_ms"] * 1e-3) / 1e12
     # compulsory HBM bytes of one dK/dV launch: read q, k, v, dO (bf16), c, LSE,
-    # delta (fp32); write dK, dV (bf16), dc_k (fp32)
-    kv_bytes = B * H * L * (6 * d * 2 + 4 * 4)
-    kv_traffic = measured_traffic("bwd_dkdv_bf16_kernel<128,false,false>")
+    # delta (fp32); write dK, dV (bf16), dc_k (fp32) and the stored dS
+    kv_bytes = B * H * L * (6 * d * 2 + 4 * 4) + r["store_bytes"]
+    kv_traffic = measured_traffic("bwd_dkdv_bf16_kernel<128,false,false,true>")
+    # dQ from the stored dS: read dS and k, write dQ (bf16) and dc_q (fp32)
+    dq_bytes = r["store_bytes"] + B * H * L * (2 * d * 2 + 4)
+    dq_gbs = dq_bytes / (r["dq_ms"] * 1e-3) / 1e9
+    rc_tf = (fl_f + fl_b) / (r["rc_ms"] * 1e-3) / 1e12
     out = {
         "metric": "Forgetting-attn fwd+bwd TFLOP/s bf16 L=16k d=128 (% MFMA peak); decode GB/s",
         "value": round(tflops, 2),
@@ -578,30 +618,48 @@ def main():
                    "gate_logits": "per-head mean U[0,6], std 1", "causal": True,
                    "flops_per_step": fl_f + fl_b, "parallelism": "none (1 GPU)"},
         "frac_of_peak": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+        "backward": "fox_attn_bwd_stored stages: dK/dV also store bf16 dS (%.2f GB workspace), "
+                    "the dQ pass reads it instead of recomputing S and dP" % (r["store_bytes"] / 1e9),
         "breakdown_ms": {"gate_prefix": round(r["gate_ms"], 4), "fwd": round(r["fwd_ms"], 4),
-                         "bwd": round(r["bwd_ms"], 4), "bwd_dkdv": round(r["dkdv_ms"], 4),
-                         "bwd_dq": round(r["dq_ms"], 4), "wall_per_step": round(r["wall_ms"], 4)},
-        "roofline": {"bound": "mfma", "kernel": "bwd_dkdv_bf16_kernel<128> (fox_attn_bwd_dkdv)",
+                         "bwd": round(r["bwd_ms"], 4), "bwd_dkdv_store": round(r["dkdv_ms"], 4),
+                         "bwd_dq_stored": round(r["dq_ms"], 4),
+                         "wall_per_step": round(r["wall_ms"], 4)},
+        "roofline": {"bound": "mfma",
+                     "kernel": "bwd_dkdv_bf16_kernel<128,false,false,true> (fox_attn_bwd_dkdv_store)",
                      "achieved": round(kv_tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(kv_tf / MFMA_BF16_PEAK_TFLOPS, 4),
                      "traffic": kv_traffic, "algorithmic_flops_per_launch": fl_kv,
                      "compulsory_bytes_per_launch": kv_bytes},
-        "skip": {"what": "the same step through fox_attn_fwd_skip / fox_attn_bwd_skip (exact "
-                         "gate-aware tile skipping, bound kernels included); outputs bitwise "
-                         "equal to the dense step",
+        "roofline_dq_stored": {"bound": "hbm", "kernel": "bwd_dq_stored_kernel<128> "
+                               "(fox_attn_bwd_dq_stored)", "achieved": round(dq_gbs, 1),
+                               "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                               "frac": round(dq_gbs / HBM_PEAK_GBS, 4),
+                               "traffic": measured_traffic("bwd_dq_stored_kernel<128>"),
+                               "compulsory_bytes_per_launch": dq_bytes},
+        "recompute": {"what": "the same step with fox_attn_bwd's stages (the dQ pass recomputes "
+                              "S and dP; O(L) workspace)",
+                      "ms_per_step": round(r["rc_ms"], 4), "TFLOP/s": round(rc_tf, 2),
+                      "frac_of_peak": round(rc_tf / MFMA_BF16_PEAK_TFLOPS, 4),
+                      "bwd_dkdv_ms": round(r["rc_dkdv_ms"], 4),
+                      "bwd_dq_ms": round(r["rc_dq_ms"], 4),
+                      "dkdv_traffic": measured_traffic("bwd_dkdv_bf16_kernel<128,false,false,false>")},
+        "skip": {"what": "the recompute step through fox_attn_fwd_skip / fox_attn_bwd_skip "
+                         "(exact gate-aware tile skipping, bound kernels included); outputs "
+                         "bitwise equal to the recompute step",
                  "ms_per_step": round(r["skip_ms"], 4),
-                 "speedup_vs_dense": round(r["ms"] / r["skip_ms"], 3),
+                 "speedup_vs_dense": round(r["rc_ms"] / r["skip_ms"], 3),
                  "dense_equivalent_TFLOP/s": round((fl_f + fl_b) / (r["skip_ms"] * 1e-3) / 1e12,
                                                    2)},
         "roofline_fwd": {"bound": "mfma", "kernel": "fwd_bf16_kernel<128> (fox_attn_fwd)",
                          "achieved": round(fwd_tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
                          "unit": "TFLOP/s", "frac": round(fwd_tf / MFMA_BF16_PEAK_TFLOPS, 4)},
-        "roofline_bwd": {"bound": "mfma", "kernels": "fox_attn_bwd stages (delta, dkdv, dq, scan)",
+        "roofline_bwd": {"bound": "mfma",
+                         "kernels": "fox_attn_bwd_stored stages (delta, dkdv_store, dq_stored, scan)",
                          "achieved": round(bwd_tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
                          "unit": "TFLOP/s", "frac": round(bwd_tf / MFMA_BF16_PEAK_TFLOPS, 4)},
     }
-    log(f"[bench] train step {r['ms']:.3f} ms -> {tflops:.1f} TFLOP/s; with skipping "
-        f"{r['skip_ms']:.3f} ms")
+    log(f"[bench] train step {r['ms']:.3f} ms -> {tflops:.1f} TFLOP/s; recompute backward "
+        f"{r['rc_ms']:.3f} ms; with skipping {r['skip_ms']:.3f} ms")
     if not args.no_fixed:
         rf = bench_fixed(w, args.steps, args.warmup)
         out["fixed_gate"] = {

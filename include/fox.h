@@ -111,6 +111,53 @@ int fox_attn_bwd(int dtype, const void* q, const void* k, const void* v, const f
                  int B, int H, int L, int d, float scale, void* stream);
 
 /*
+ * The same backward (Alg. 2) trading memory for the recomputation in the dQ
+ * half: the dK/dV pass also writes the bf16 dS it forms, and the dQ pass reads
+ * it instead of recomputing S, P and dP (dQ = s dS K, dc^q = rowsum(dS)).  The
+ * workspace grows with L^2: 16 KB per (128-key block, 64-query tile) pair of the
+ * causal order, per (b, h): about B H L^2 bytes, 8.7 GB at B = 2, H = 16,
+ * L = 16384 (fox_attn_bwd needs 12 B H L bytes).  bf16 only (FOX_ERR_UNSUPPORTED
+ * for fp32).  Arguments, outputs and errors as for fox_attn_bwd; the workspace is
+ * at least fox_attn_bwd_stored_workspace_bytes() (0 for fp32 or invalid
+ * arguments).  Results agree with fox_attn_bwd to rounding (the two dQ halves sum
+ * the same bf16 dS in different orders); dc^q and dc^k remain the row and
+ * column sums of one matrix.
+ */
+size_t fox_attn_bwd_stored_workspace_bytes(int dtype, int B, int H, int L, int d);
+int fox_attn_bwd_stored(int dtype, const void* q, const void* k, const void* v, const float* c,
+                        const void* o, const float* lse, const void* d_o,
+                        void* dq, void* dk, void* dv, float* d_log_f,
+                        void* workspace, size_t workspace_bytes,
+                        int B, int H, int L, int d, float scale, void* stream);
+
+/*
+ * fox_attn_bwd_stored in stages: it is exactly
+ *     fox_attn_bwd_delta -> fox_attn_bwd_dkdv_store -> fox_attn_bwd_dq_stored
+ *     -> fox_dlogf_from_dc
+ * with delta, dc_q, dc_k and the stored dS carved from its workspace.
+ *
+ * fox_attn_bwd_ds_store_bytes: bytes of the stored dS (0 for fp32 or invalid
+ *   arguments).
+ * fox_attn_bwd_dkdv_store: fox_attn_bwd_dkdv (same arguments and outputs, bit for
+ *   bit the same dK, dV, dc_k) that also writes dS, bf16, into ds_store (device,
+ *   at least fox_attn_bwd_ds_store_bytes(), 16-byte aligned; caller-owned, layout
+ *   private to the library, fully rewritten where the dQ stage reads it).
+ * fox_attn_bwd_dq_stored: dQ (overwritten) and dc_q = rowsum(dS) [B,H,L] fp32
+ *   (overwritten) from k [B,H,L,d] and the ds_store written by
+ *   fox_attn_bwd_dkdv_store for the same shape.
+ * bf16 only: FOX_ERR_UNSUPPORTED for fp32.
+ */
+size_t fox_attn_bwd_ds_store_bytes(int dtype, int B, int H, int L, int d);
+int fox_attn_bwd_dkdv_store(int dtype, const void* q, const void* k, const void* v,
+                            const float* c, const float* lse, const void* d_o,
+                            const float* delta, void* dk, void* dv, float* dc_k,
+                            void* ds_store, size_t ds_store_bytes,
+                            int B, int H, int L, int d, float scale, void* stream);
+int fox_attn_bwd_dq_stored(int dtype, const void* k, const void* ds_store, size_t ds_store_bytes,
+                           void* dq, float* dc_q, int B, int H, int L, int d, float scale,
+                           void* stream);
+
+/*
  * The backward pass in stages, for callers that schedule them themselves (for
  * instance dK/dV and dQ on two streams).  fox_attn_bwd is exactly
  *     fox_attn_bwd_delta -> fox_attn_bwd_dkdv -> fox_attn_bwd_dq -> fox_dlogf_from_dc
@@ -125,9 +172,10 @@ int fox_attn_bwd(int dtype, const void* q, const void* k, const void* v, const f
  * fox_dlogf_from_dc: d(log f)_l = sum_{i>=l} (dc_q_i + dc_k_i), the chain rule
  *   through c = cumsum(log f) (Alg. 2 returns dc = dc^q + dc^k); [B,H,L] fp32.
  * Both halves form P and dS from the same expression (bf16 dtype: P rounded to
- * bf16 before dS = P o (dP - delta)), so that dc_q and dc_k are the row and column
- * sums of one matrix and sum(dc) = d(log f)_1 = 0 holds to fp32 rounding.  Inputs
- * as for fox_attn_bwd.
+ * bf16 before dS = P o (dP - delta), and dc summed over dS rounded to bf16, the
+ * values the dQ and dK products take), so that dc_q and dc_k are the row and
+ * column sums of one matrix and sum(dc) = d(log f)_1 = 0 holds to fp32 rounding.
+ * Inputs as for fox_attn_bwd.
  */
 int fox_attn_bwd_delta(int dtype, const void* o, const void* d_o, float* delta,
                        int B, int H, int L, int d, void* stream);

@@ -17,6 +17,8 @@ from ._lib import (  # noqa: F401
     fox_attn_fwd_fixed_gate_skip, fox_attn_bwd_fixed_gate_skip, fox_attn_decode_fixed_gate_skip,
     fox_pro_prologue, fox_pro_prologue_bwd, fox_pro_prologue_bwd_workspace_bytes,
     fox_pro_output_gate, fox_attn_fwd_pro, fox_attn_bwd_pro, fox_attn_bwd_pro_workspace_bytes,
+    fox_attn_bwd_stored, fox_attn_bwd_stored_workspace_bytes, fox_attn_bwd_ds_store_bytes,
+    fox_attn_bwd_dkdv_store, fox_attn_bwd_dq_stored,
     EXPORTED,
 )
 
@@ -33,5 +35,6 @@ __all__ = [
     "fox_attn_decode_fixed_gate_skip",
     "fox_pro_prologue", "fox_pro_prologue_bwd", "fox_pro_prologue_bwd_workspace_bytes",
     "fox_pro_output_gate", "fox_attn_fwd_pro", "fox_attn_bwd_pro",
-    "fox_attn_bwd_pro_workspace_bytes",
+    "fox_attn_bwd_pro_workspace_bytes", "fox_attn_bwd_stored", "fox_attn_bwd_stored_workspace_bytes",
+    "fox_attn_bwd_ds_store_bytes", "fox_attn_bwd_dkdv_store", "fox_attn_bwd_dq_stored",
 ]

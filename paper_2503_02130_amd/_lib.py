@@ -34,7 +34,8 @@ EXPORTED = (
     "fox_attn_decode_fixed_gate_skip",
     "fox_pro_prologue", "fox_pro_prologue_bwd_workspace_bytes", "fox_pro_prologue_bwd",
     "fox_pro_output_gate", "fox_attn_fwd_pro", "fox_attn_bwd_pro_workspace_bytes",
-    "fox_attn_bwd_pro",
+    "fox_attn_bwd_pro", "fox_attn_bwd_stored_workspace_bytes", "fox_attn_bwd_stored",
+    "fox_attn_bwd_ds_store_bytes", "fox_attn_bwd_dkdv_store", "fox_attn_bwd_dq_stored",
 )
 
 
@@ -70,6 +71,17 @@ def load() -> ctypes.CDLL:
     lib.fox_attn_bwd_workspace_bytes.argtypes = [I, I, I, I, I]
     lib.fox_attn_bwd.restype = I
     lib.fox_attn_bwd.argtypes = [I, P, P, P, P, P, P, P, P, P, P, P, P, Z, I, I, I, I, F, P]
+    lib.fox_attn_bwd_stored_workspace_bytes.restype = Z
+    lib.fox_attn_bwd_stored_workspace_bytes.argtypes = [I, I, I, I, I]
+    lib.fox_attn_bwd_stored.restype = I
+    lib.fox_attn_bwd_stored.argtypes = [I, P, P, P, P, P, P, P, P, P, P, P, P, Z, I, I, I, I, F, P]
+    lib.fox_attn_bwd_ds_store_bytes.restype = Z
+    lib.fox_attn_bwd_ds_store_bytes.argtypes = [I, I, I, I, I]
+    lib.fox_attn_bwd_dkdv_store.restype = I
+    lib.fox_attn_bwd_dkdv_store.argtypes = [I, P, P, P, P, P, P, P, P, P, P, P, Z, I, I, I, I, F,
+                                            P]
+    lib.fox_attn_bwd_dq_stored.restype = I
+    lib.fox_attn_bwd_dq_stored.argtypes = [I, P, P, Z, P, P, I, I, I, I, F, P]
     lib.fox_attn_bwd_delta.restype = I
     lib.fox_attn_bwd_delta.argtypes = [I, P, P, P, I, I, I, I, P]
     lib.fox_attn_bwd_dkdv.restype = I
@@ -218,9 +230,28 @@ def fox_attn_bwd_workspace_bytes(dtype: torch.dtype, B: int, H: int, L: int, d: 
     return int(load().fox_attn_bwd_workspace_bytes(_DT[dtype], B, H, L, d))
 
 
+def fox_attn_bwd_stored_workspace_bytes(dtype: torch.dtype, B: int, H: int, L: int,
+                                        d: int) -> int:
+    return int(load().fox_attn_bwd_stored_workspace_bytes(_DT[dtype], B, H, L, d))
+
+
 def fox_attn_bwd(q, k, v, c, o, lse, d_o, scale: Optional[float] = None,
                  dq=None, dk=None, dv=None, d_log_f=None, workspace=None):
     """dq, dk, dv [B,H,L,d] and d(log f) [B,H,L] fp32."""
+    return _attn_bwd_call("fox_attn_bwd", fox_attn_bwd_workspace_bytes, q, k, v, c, o, lse, d_o,
+                          scale, dq, dk, dv, d_log_f, workspace)
+
+
+def fox_attn_bwd_stored(q, k, v, c, o, lse, d_o, scale: Optional[float] = None,
+                        dq=None, dk=None, dv=None, d_log_f=None, workspace=None):
+    """fox_attn_bwd keeping dS in the workspace (about B*H*L^2 bytes) instead of
+    recomputing it for dQ; bf16 only."""
+    return _attn_bwd_call("fox_attn_bwd_stored", fox_attn_bwd_stored_workspace_bytes, q, k, v,
+                          c, o, lse, d_o, scale, dq, dk, dv, d_log_f, workspace)
+
+
+def _attn_bwd_call(entry, ws_bytes, q, k, v, c, o, lse, d_o, scale, dq, dk, dv, d_log_f,
+                   workspace):
     B, H, L, d = q.shape
     dt = q.dtype
     if dt not in _DT:
@@ -237,15 +268,15 @@ def fox_attn_bwd(q, k, v, c, o, lse, d_o, scale: Optional[float] = None,
     for name, t in (("dq", dq), ("dk", dk), ("dv", dv)):
         _check(t, name, (B, H, L, d), dt, dev)
     _check(d_log_f, "d_log_f", (B, H, L), torch.float32, dev)
-    need = fox_attn_bwd_workspace_bytes(dt, B, H, L, d)
+    need = ws_bytes(dt, B, H, L, d)
     if workspace is None:
         workspace = torch.empty(max(need, 16), device=dev, dtype=torch.uint8)
     s = default_scale(d) if scale is None else float(scale)
-    st = load().fox_attn_bwd(_DT[dt], _ptr(q), _ptr(k), _ptr(v), _ptr(c), _ptr(o), _ptr(lse),
-                             _ptr(d_o), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(d_log_f),
-                             _ptr(workspace), workspace.numel() * workspace.element_size(),
-                             B, H, L, d, s, _stream(q))
-    _raise(st, "fox_attn_bwd")
+    st = getattr(load(), entry)(_DT[dt], _ptr(q), _ptr(k), _ptr(v), _ptr(c), _ptr(o), _ptr(lse),
+                                _ptr(d_o), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(d_log_f),
+                                _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                B, H, L, d, s, _stream(q))
+    _raise(st, entry)
     return dq, dk, dv, d_log_f
 
 
@@ -311,6 +342,59 @@ def fox_attn_bwd_dq(q, k, v, c, lse, d_o, delta, scale: Optional[float] = None,
                                 _stream(q))
     _raise(st, "fox_attn_bwd_dq")
     return dq, dc_q
+
+
+def fox_attn_bwd_ds_store_bytes(dtype: torch.dtype, B: int, H: int, L: int, d: int) -> int:
+    return int(load().fox_attn_bwd_ds_store_bytes(_DT[dtype], B, H, L, d))
+
+
+def fox_attn_bwd_dkdv_store(q, k, v, c, lse, d_o, delta, ds_store, scale: Optional[float] = None,
+                            dk=None, dv=None, dc_k=None):
+    """fox_attn_bwd_dkdv that also writes dS (bf16) into ds_store, a uint8
+    device tensor of at least fox_attn_bwd_ds_store_bytes() bytes."""
+    B, H, L, d, dt, dev = _check_bwd_inputs(q, k, v, c, lse, d_o)
+    _check(delta, "delta", (B, H, L), torch.float32, dev)
+    dk = torch.empty_like(k) if dk is None else dk
+    dv = torch.empty_like(v) if dv is None else dv
+    dc_k = torch.empty_like(c) if dc_k is None else dc_k
+    _check(dk, "dk", (B, H, L, d), dt, dev)
+    _check(dv, "dv", (B, H, L, d), dt, dev)
+    _check(dc_k, "dc_k", (B, H, L), torch.float32, dev)
+    _check_store(ds_store, dev)
+    s = default_scale(d) if scale is None else float(scale)
+    st = load().fox_attn_bwd_dkdv_store(_DT[dt], _ptr(q), _ptr(k), _ptr(v), _ptr(c), _ptr(lse),
+                                        _ptr(d_o), _ptr(delta), _ptr(dk), _ptr(dv), _ptr(dc_k),
+                                        _ptr(ds_store), ds_store.numel(), B, H, L, d, s,
+                                        _stream(q))
+    _raise(st, "fox_attn_bwd_dkdv_store")
+    return dk, dv, dc_k
+
+
+def fox_attn_bwd_dq_stored(k, ds_store, scale: Optional[float] = None, dq=None, dc_q=None):
+    """dQ (k's dtype) and dc_q = rowsum(dS) [B,H,L] fp32 from the dS that
+    fox_attn_bwd_dkdv_store wrote."""
+    B, H, L, d = k.shape
+    dt, dev = k.dtype, k.device
+    if dt not in _DT:
+        raise ValueError(f"unsupported dtype {dt}")
+    _check(k, "k", (B, H, L, d), dt, dev)
+    _check_store(ds_store, dev)
+    dq = torch.empty_like(k) if dq is None else dq
+    dc_q = torch.empty((B, H, L), device=dev, dtype=torch.float32) if dc_q is None else dc_q
+    _check(dq, "dq", (B, H, L, d), dt, dev)
+    _check(dc_q, "dc_q", (B, H, L), torch.float32, dev)
+    s = default_scale(d) if scale is None else float(scale)
+    st = load().fox_attn_bwd_dq_stored(_DT[dt], _ptr(k), _ptr(ds_store), ds_store.numel(),
+                                       _ptr(dq), _ptr(dc_q), B, H, L, d, s, _stream(k))
+    _raise(st, "fox_attn_bwd_dq_stored")
+    return dq, dc_q
+
+
+def _check_store(ds_store, dev):
+    if ds_store.dtype != torch.uint8 or ds_store.dim() != 1 or not ds_store.is_contiguous():
+        raise ValueError("ds_store: a contiguous 1-D uint8 tensor")
+    if ds_store.device != dev:
+        raise ValueError(f"ds_store on {ds_store.device}, expected {dev}")
 
 
 def fox_dlogf_from_dc(dc_q, dc_k, d_log_f=None):

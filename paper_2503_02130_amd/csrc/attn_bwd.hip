@@ -77,6 +77,30 @@ constexpr int kRefBlock = 128;
 // bound), and since c falls along the sequence so do all pairs further apart:
 // the tile loops stop there, bit for bit as without skipping.
 constexpr float kSkipMargin = 160.0f;
+
+// ---------------------------------------------------------------------------
+// Stored dS, for the backward that keeps dS instead of recomputing it in the
+// dQ pass.  For each (b, h), one 16 KB slot per pair (128-key block nb, 64-query
+// tile qt) that the causal order reaches (qt >= 2 nb), block-major.  A slot
+// holds the bf16 dS of the block's keys and the tile's queries in the register
+// layout of the dK/dV kernel's G waves: [32-key pair 4][32-query half qb 2]
+// [16-query chunk c 2][lane 64][8 bf16], where lane = 32 h + the key within the
+// pair and element 4 g2 + jj is query 16 c + 8 g2 + 4 h + jj of the half.
+// ---------------------------------------------------------------------------
+constexpr int kDsSlotBytes = 16384;
+constexpr int kNonTemporal = 2;  // cache policy of a buffer instruction: non-temporal
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+__host__ __device__ inline int ds_query_tiles(int L) { return (L + 63) / 64; }
+__host__ __device__ inline int ds_key_blocks(int L) { return (L + 127) / 128; }
+__host__ __device__ inline size_t ds_slots_per_head(int L) {
+  const size_t nq = (size_t)ds_query_tiles(L), nk = (size_t)ds_key_blocks(L);
+  return nk * nq - nk * (nk - 1);
+}
+// slot of (key block nb, query tile qt >= 2 nb) within its head
+__host__ __device__ inline size_t ds_slot(int L, int nb, int qt) {
+  return (size_t)nb * (size_t)ds_query_tiles(L) - (size_t)nb * (size_t)(nb - 1) +
+         (size_t)(qt - 2 * nb);
+}
 static_assert(kRefBlock % kDqBN == 0, "a dq key tile lies in one reference block");
 
 template <int D>
@@ -260,14 +284,14 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
       float dsv[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float ds = pv[r] * (pacc[r] - dlt);
-        dcq_part += ds;  // dc^q and dc^k sum fp32 dS, the row and column sums of one matrix
-        dsv[r] = ds;
+        dsv[r] = pv[r] * (pacc[r] - dlt);
       }
       static_for<2>([&](auto cc) {
         constexpr int c = decltype(cc)::value;
         constexpr int OFF = 2 * (B * TILE + (2 * kb + c) * 16 * D);
         const bf16x8 dsb = pack8(&dsv[8 * c]);
+        // dc^q and dc^k sum the bf16 dS the products use: row and column sums of one matrix
+        dcq_part = sum8_bf16(dsb, dcq_part);
         bf16x4 t[2 * (D / 32)];
         static_for<D / 32>([&](auto dbc) {
           constexpr int db = decltype(dbc)::value;
@@ -361,13 +385,17 @@ struct KvSmem {
   int skip[3];          // the query tile and every later one contribute exact zeros
 };
 
-template <int D, bool FIXED, bool SKIP>
+template <int D, bool FIXED, bool SKIP, bool STORE = false>
 __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
     const float* __restrict__ gate, const float* __restrict__ qnorm,
     const float* __restrict__ knorm, const float* __restrict__ LSE, const bf16* __restrict__ dO,
     const float* __restrict__ delta, bf16* __restrict__ dK, bf16* __restrict__ dV,
-    float* __restrict__ dck, int BH, int H, int L, float scale, float scale_log2) {
+    float* __restrict__ dck, bf16x8* __restrict__ ds_store, int BH, int H, int L, float scale,
+    float scale_log2) {
+  static_assert(!(STORE && SKIP), "the stored-dS backward runs dense");
+  static_assert(!STORE || (kv_bm<D>() == 64 && kKvBN == 128 && kKvPairs == 4),
+                "the stored-dS slot layout");
   constexpr int kKvBM = kv_bm<D>();
   constexpr int NQB = kKvBM / 32;  // 32-query sub-blocks per tile
   constexpr int TILE = kKvBM * D;
@@ -552,8 +580,17 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
       });
     });
   };
+  // STORE: the G waves also write their bf16 dS, as packed for the dK MFMA, to
+  // this block's run of stored slots (16 KB per 64-query tile, from tile t_first
+  // on), for the dQ pass; non-temporal stores, the reader comes after the kernel.
+  const __amdgpu_buffer_rsrc_t rds = make_rsrc(
+      STORE ? ds_store + ((size_t)bh * ds_slots_per_head(L) + ds_slot(L, nblk, t_first)) *
+                             (kDsSlotBytes / 16)
+            : ds_store,
+      STORE ? (uint32_t)(ds_query_tiles(L) - t_first) * kDsSlotBytes : 0u);
+  const int lane16 = lane * 16;
   // G wave on tile qt held in buffer B (its P was stored in the same buffer slot)
-  auto g_tile = [&](auto bufc) {
+  auto g_tile = [&](int qt, auto bufc) {
     constexpr int B = decltype(bufc)::value;
     static_for<NQB>([&](auto qbc) {
       constexpr int qb = decltype(qbc)::value;
@@ -578,12 +615,17 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
           const f32x4 dl4 = *(const lds_f32x4_t*)(row_at + kDlOff + 4 * (B * kKvBM + qb * 32 + 8 * (2 * c + g2)));
 #pragma unroll
           for (int jj = 0; jj < 4; ++jj) {
-            const float ds = to_f32(pb[4 * g2 + jj]) * (pacc[8 * c + 4 * g2 + jj] - dl4[jj]);
-            dck_part += ds;
-            dsv[4 * g2 + jj] = ds;
+            dsv[4 * g2 + jj] = to_f32(pb[4 * g2 + jj]) * (pacc[8 * c + 4 * g2 + jj] - dl4[jj]);
           }
         }
         const bf16x8 dsb = pack8(dsv);
+        dck_part = sum8_bf16(dsb, dck_part);  // the column sums of the bf16 dS (see the dq kernel)
+        if constexpr (STORE)
+          __builtin_amdgcn_raw_buffer_store_b128(
+              __builtin_bit_cast(u32x4, dsb), rds, lane16,
+              (int)uniform_u32((uint32_t)(qt - t_first) * kDsSlotBytes + (uint32_t)pair * 4096u) +
+                  (2 * qb + c) * 1024,
+              kNonTemporal);
         if constexpr (SKIP) read_tr(bufc, std::integral_constant<int, 2 * qb + c>(), tr);
         lds_wait<0>(tr);
 #pragma unroll
@@ -613,7 +655,7 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
       }
     } else {
       const int qt = t_first + it - 1;
-      if (it >= 1 && qt >= t_diag) g_tile(std::integral_constant<int, BP>());
+      if (it >= 1 && qt >= t_diag) g_tile(qt, std::integral_constant<int, BP>());
     }
     if (it + 1 < n_tiles) convert_stats(t_first + it + 1, (it + 1) & 1, std::integral_constant<int, BN>());
   };
@@ -646,6 +688,156 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
   if (!pwave) {
     const float dck_tot = wave_sum_pair(dck_part);
     if (k_valid && h == 0) dck[head + kj] = -dck_tot;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dQ from the stored dS: dQ = s dS K and dc^q = rowsum(dS) over the bf16 dS the
+// dK/dV kernel wrote.  Eight waves own 256 queries (four 64-query tiles, two
+// 32-query halves each); stages of 64 keys (half a stored block) load K and the
+// four tiles' dS by DMA, double-buffered, one barrier per stage.  Each wave
+// accumulates dQ^T = K^T dS^T: the A operand is K transposed out of the LDS
+// tile, the B operand dS^T comes out of the stored layout by transposing reads
+// (lane = query, eight keys in the contraction order of the A operand).  A tile
+// skips the stages wholly above its diagonal; those slots were never written.
+// HBM-bound: every stored dS byte is read once.
+// ---------------------------------------------------------------------------
+constexpr int kDsWaves = 8;
+constexpr int kDsThreads = 64 * kDsWaves;
+constexpr int kDsBM = 32 * kDsWaves;  // queries per workgroup
+constexpr int kDsBN = 64;             // keys per stage
+constexpr int kDsTiles = kDsBM / 64;  // query tiles per workgroup
+constexpr int kDsStageBytes = kDsSlotBytes / 2;  // one tile's dS for one stage
+
+template <int D>
+struct DsSmem {
+  bf16 k[2][kDsBN * D];
+  bf16x8 ds[2][kDsTiles][kDsStageBytes / 16];
+};
+
+template <int D>
+__global__ __launch_bounds__(kDsThreads) void bwd_dq_stored_kernel(
+    const bf16* __restrict__ K, const bf16x8* __restrict__ ds_store, bf16* __restrict__ dQ,
+    float* __restrict__ dcq, int BH, int L, int n_mblk, float scale) {
+  constexpr int TILE = kDsBN * D;
+  constexpr int NDMA = TILE * 2 / 1024 / kDsWaves;
+  static_assert(NDMA >= 1, "every wave issues at least one K DMA load per stage");
+  __shared__ __attribute__((aligned(16))) DsSmem<D> sm;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int h = lane >> 5, col = lane & 31;
+  const int row = (int)(blockIdx.x / BH);
+  const int bh = (int)(blockIdx.x % BH);  // heads fastest
+  const int mblk = n_mblk - 1 - row;      // the longest rows first
+  const int q0 = mblk * kDsBM;
+  const int qt0 = q0 / 64;
+  const int my_t = wave >> 1, qb = wave & 1;  // this wave's tile and half
+  const int qt = qt0 + my_t;
+  const int qi = qt * 64 + qb * 32 + col;
+  const bool q_valid = qi < L;
+  const int n_qt = ds_query_tiles(L);
+  const size_t head = (size_t)bh * (size_t)L;
+  const size_t head_slot = (size_t)bh * ds_slots_per_head(L);
+  const __amdgpu_buffer_rsrc_t rk = make_rsrc(K + head * D, (uint32_t)L * D * 2);
+  const uint32_t dma_off = tile_dma_offset<D, kDsWaves>(wave, lane);
+
+  // A operand: transposing reads of the K tile (tile_tr_offsets); B operand:
+  // in group g16 = lane / 16, lane j16 reads, for the 4 x 16 block of keys
+  // (rows) by the group's 16 queries (columns), key row j16 / 4 and queries
+  // 4 (j16 % 4) .. +3, which sit in one 8-byte half of one stored lane slot.
+  int toff[2][D / 32];
+  tile_tr_offsets<D>(toff, lane);
+  uint32_t taddr[2][D / 32];
+#pragma unroll
+  for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+      taddr[k2][db] = (uint32_t)(uintptr_t)lds_opaque(lds_ptr(&sm.k[0][0]) + 2 * toff[k2][db]);
+  const int g16 = lane >> 4, j16 = lane & 15, cg = j16 & 3;
+  const uint32_t ds_addr = (uint32_t)(uintptr_t)lds_opaque(
+      lds_ptr(&sm.ds[0][my_t][0]) + (2 * qb + (g16 & 1)) * 1024 +
+      ((cg & 1) * 32 + 4 * (g16 >> 1) + (j16 >> 2)) * 16 + (cg >> 1) * 8);
+
+  f32x16 dqacc[D / 32];
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) dqacc[db][r] = 0.0f;
+  float dcq_part = 0.0f;
+
+  const int n_st = (min(L, q0 + kDsBM) + kDsBN - 1) / kDsBN;
+  auto issue = [&](int j, auto bufc) {
+    constexpr int B = decltype(bufc)::value;
+    const uint32_t base = (uint32_t)j * TILE * 2;
+#pragma unroll
+    for (int i = 0; i < NDMA; ++i)
+      dma16(rk, &sm.k[B][(i * kDsWaves + wave) * 512],
+            dma_off + uniform_u32(base + i * tile_dma_stride<kDsWaves>()));
+    // the tiles on or below the diagonal of stage j: slots of key block j / 2
+    const int nb = j >> 1;
+    const int t_lo = max(0, j - qt0), t_hi = min(kDsTiles, n_qt - qt0);
+    if (t_lo < t_hi) {
+      const __amdgpu_buffer_rsrc_t rs = make_rsrc(
+          ds_store + (head_slot + ds_slot(L, nb, qt0 + t_lo)) * (kDsSlotBytes / 16),
+          (uint32_t)(t_hi - t_lo) * kDsSlotBytes);
+      for (int t = t_lo; t < t_hi; ++t)
+        dma16(rs, &sm.ds[B][t][wave * 64],
+              (uint32_t)lane * 16 +
+                  uniform_u32((uint32_t)(t - t_lo) * kDsSlotBytes +
+                              (uint32_t)(j & 1) * kDsStageBytes + (uint32_t)wave * 1024));
+    }
+  };
+  auto body = [&](auto bufc) {
+    constexpr int B = decltype(bufc)::value;
+    static_for<kDsBN / 16>([&](auto sc) {
+      constexpr int S = decltype(sc)::value;  // 16-key step: pair S / 2, keys 16 (S % 2) ..
+      constexpr int DOFF = B * (int)sizeof(sm.ds[0]) + (S / 2) * 4096 + (S % 2) * 256;
+      constexpr int KOFF = 2 * (B * TILE + S * 16 * D);
+      bf16x4 t[2 * (D / 32) + 2];
+      t[0] = ds_read_tr_asm<DOFF>(ds_addr);
+      t[1] = ds_read_tr_asm<DOFF + 128>(ds_addr);
+      static_for<D / 32>([&](auto dbc) {
+        constexpr int db = decltype(dbc)::value;
+        t[2 + 2 * db] = ds_read_tr_asm<KOFF>(taddr[0][db]);
+        t[3 + 2 * db] = ds_read_tr_asm<KOFF>(taddr[1][db]);
+      });
+      lds_wait<0>(t);
+      const bf16x8 dsb = cat4(t[0], t[1]);
+      dcq_part = sum8_bf16(dsb, dcq_part);
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+        dqacc[db] = mfma32(cat4(t[2 + 2 * db], t[3 + 2 * db]), dsb, dqacc[db]);
+    });
+  };
+
+  issue(0, std::integral_constant<int, 0>());
+  for (int j = 0; j < n_st; j += 2) {
+    wait_all_memory();
+    __syncthreads();  // stage j is in LDS; every wave is done with stage j - 1
+    if (j + 1 < n_st) issue(j + 1, std::integral_constant<int, 1>());
+    if (qt >= j && qt < n_qt) body(std::integral_constant<int, 0>());
+    if (j + 1 < n_st) {
+      wait_all_memory();
+      __syncthreads();
+      if (j + 2 < n_st) issue(j + 2, std::integral_constant<int, 0>());
+      if (qt >= j + 1 && qt < n_qt) body(std::integral_constant<int, 1>());
+    }
+  }
+
+  const float dcq_tot = wave_sum_pair(dcq_part);
+  if (q_valid) {
+    bf16* out = dQ + (head + qi) * D;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        bf16x4 w;
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) w[jj] = to_bf16(dqacc[db][4 * g + jj] * scale);
+        *reinterpret_cast<bf16x4*>(out + db * 32 + 8 * g + 4 * h) = w;
+      }
+    }
+    if (h == 0) dcq[head + qi] = dcq_tot;
   }
 }
 
@@ -836,12 +1028,12 @@ static void dkdv_t(bool bf16_, const void* q, const void* k, const void* v, Gate
     if (qn)
       hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, FIXED, true>), grid, dim3(kKvThreads), 0, s,
                          (const bf16*)q, (const bf16*)k, (const bf16*)v, g.ptr, qn, kn, lse,
-                         (const bf16*)d_o, delta, (bf16*)dk, (bf16*)dv, dck, BH, g.H, L, scale,
+                         (const bf16*)d_o, delta, (bf16*)dk, (bf16*)dv, dck, nullptr, BH, g.H, L, scale,
                          sl2);
     else
     hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, FIXED, false>), grid, dim3(kKvThreads), 0, s,
                        (const bf16*)q, (const bf16*)k, (const bf16*)v, g.ptr, qn, kn, lse,
-                       (const bf16*)d_o, delta, (bf16*)dk, (bf16*)dv, dck, BH, g.H, L, scale,
+                       (const bf16*)d_o, delta, (bf16*)dk, (bf16*)dv, dck, nullptr, BH, g.H, L, scale,
                        sl2);
   } else {
     const int rpw = kF32Threads / (D / 32);
@@ -940,6 +1132,64 @@ hipError_t launch_bwd(bool bf16_, const void* q, const void* k, const void* v, c
                       hipStream_t s, const float* q_norm_max, const float* k_norm_max) {
   return launch_bwd_stages(bf16_, q, k, v, gate_array(c), o, lse, d_o, dq, dk, dv, d_log_f,
                            static_cast<float*>(ws), BH, L, d, scale, s, q_norm_max, k_norm_max);
+}
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+size_t ds_store_bytes(int BH, int L) {
+  return (size_t)BH * ds_slots_per_head(L) * (size_t)kDsSlotBytes;
+}
+
+size_t bwd_stored_workspace_bytes(int BH, int L) {
+  return align256(bwd_workspace_bytes(BH, L)) + ds_store_bytes(BH, L);
+}
+
+hipError_t launch_bwd_dkdv_store(const void* q, const void* k, const void* v, const float* c,
+                                 const float* lse, const void* d_o, const float* delta, void* dk,
+                                 void* dv, float* dck, void* ds_store, int BH, int L, int d,
+                                 float scale, hipStream_t s) {
+  const dim3 grid((unsigned)((L + kKvBN - 1) / kKvBN) * (unsigned)BH);
+  if (d == 128)
+    hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<128, false, false, true>), grid, dim3(kKvThreads), 0,
+                       s, (const bf16*)q, (const bf16*)k, (const bf16*)v, c, nullptr, nullptr,
+                       lse, (const bf16*)d_o, delta, (bf16*)dk, (bf16*)dv, dck,
+                       (bf16x8*)ds_store, BH, 1, L, scale, scale * kLog2e);
+  else
+    hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<64, false, false, true>), grid, dim3(kKvThreads), 0,
+                       s, (const bf16*)q, (const bf16*)k, (const bf16*)v, c, nullptr, nullptr,
+                       lse, (const bf16*)d_o, delta, (bf16*)dk, (bf16*)dv, dck,
+                       (bf16x8*)ds_store, BH, 1, L, scale, scale * kLog2e);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_dq_stored(const void* k, const void* ds_store, void* dq, float* dcq,
+                                int BH, int L, int d, float scale, hipStream_t s) {
+  const int n_mblk = (L + kDsBM - 1) / kDsBM;
+  const dim3 grid((unsigned)n_mblk * (unsigned)BH);
+  if (d == 128)
+    hipLaunchKernelGGL((bwd_dq_stored_kernel<128>), grid, dim3(kDsThreads), 0, s,
+                       (const bf16*)k, (const bf16x8*)ds_store, (bf16*)dq, dcq, BH, L, n_mblk,
+                       scale);
+  else
+    hipLaunchKernelGGL((bwd_dq_stored_kernel<64>), grid, dim3(kDsThreads), 0, s, (const bf16*)k,
+                       (const bf16x8*)ds_store, (bf16*)dq, dcq, BH, L, n_mblk, scale);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_stored(const void* q, const void* k, const void* v, const float* c,
+                             const void* o, const float* lse, const void* d_o, void* dq, void* dk,
+                             void* dv, float* d_log_f, void* ws, int BH, int L, int d, float scale,
+                             hipStream_t s) {
+  float* delta = static_cast<float*>(ws);
+  float* dcq = delta + (size_t)BH * L;
+  float* dck = dcq + (size_t)BH * L;
+  void* dss = static_cast<char*>(ws) + align256(bwd_workspace_bytes(BH, L));
+  hipError_t e = launch_bwd_delta(true, o, d_o, delta, BH, L, d, s);
+  if (e == hipSuccess)
+    e = launch_bwd_dkdv_store(q, k, v, c, lse, d_o, delta, dk, dv, dck, dss, BH, L, d, scale, s);
+  if (e == hipSuccess) e = launch_bwd_dq_stored(k, dss, dq, dcq, BH, L, d, scale, s);
+  if (e == hipSuccess) e = launch_reverse_scan_sum(dcq, dck, d_log_f, BH, L, s);
+  return e;
 }
 
 // d b^(h) = sigmoid(-b^(h)) * sum over the rows of head h and all t of d(log f):

@@ -124,6 +124,34 @@ int fox_attn_bwd(int dtype, const void* q, const void* k, const void* v, const f
                                        static_cast<hipStream_t>(stream)));
 }
 
+size_t fox_attn_bwd_stored_workspace_bytes(int dtype, int B, int H, int L, int d) {
+  if (check_dims(B, H, L, d) || check_dtype_d(dtype, d) || dtype != FOX_DTYPE_BF16) return 0;
+  return fox::bwd_stored_workspace_bytes(B * H, L);
+}
+
+int fox_attn_bwd_stored(int dtype, const void* q, const void* k, const void* v, const float* c,
+                        const void* o, const float* lse, const void* d_o, void* dq, void* dk,
+                        void* dv, float* d_log_f, void* workspace, size_t workspace_bytes, int B,
+                        int H, int L, int d, float scale, void* stream) {
+  if (!q || !k || !v || !c || !o || !lse || !d_o || !dq || !dk || !dv || !d_log_f)
+    return FOX_ERR_NULL;
+  int st = check_dims(B, H, L, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (dtype != FOX_DTYPE_BF16) return FOX_ERR_UNSUPPORTED;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(c) || !aligned16(o) ||
+      !aligned16(lse) || !aligned16(d_o) || !aligned16(dq) || !aligned16(dk) || !aligned16(dv) ||
+      !aligned16(d_log_f))
+    return FOX_ERR_ALIGN;
+  if (!workspace || workspace_bytes < fox::bwd_stored_workspace_bytes(B * H, L))
+    return FOX_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return FOX_ERR_ALIGN;
+  return launch_status(fox::launch_bwd_stored(q, k, v, c, o, lse, d_o, dq, dk, dv, d_log_f,
+                                              workspace, B * H, L, d, scale,
+                                              static_cast<hipStream_t>(stream)));
+}
+
 int fox_attn_bwd_delta(int dtype, const void* o, const void* d_o, float* delta, int B, int H,
                        int L, int d, void* stream) {
   if (!o || !d_o || !delta) return FOX_ERR_NULL;
@@ -167,6 +195,49 @@ int fox_attn_bwd_dq(int dtype, const void* q, const void* k, const void* v, cons
   return launch_status(fox::launch_bwd_dq(dtype == FOX_DTYPE_BF16, q, k, v, fox::gate_array(c), lse, d_o, delta,
                                           dq, dc_q, B * H, L, d, scale,
                                           static_cast<hipStream_t>(stream)));
+}
+
+size_t fox_attn_bwd_ds_store_bytes(int dtype, int B, int H, int L, int d) {
+  if (check_dims(B, H, L, d) || check_dtype_d(dtype, d) || dtype != FOX_DTYPE_BF16) return 0;
+  return fox::ds_store_bytes(B * H, L);
+}
+
+int fox_attn_bwd_dkdv_store(int dtype, const void* q, const void* k, const void* v,
+                            const float* c, const float* lse, const void* d_o,
+                            const float* delta, void* dk, void* dv, float* dc_k, void* ds_store,
+                            size_t ds_store_bytes, int B, int H, int L, int d, float scale,
+                            void* stream) {
+  if (!q || !k || !v || !c || !lse || !d_o || !delta || !dk || !dv || !dc_k) return FOX_ERR_NULL;
+  int st = check_dims(B, H, L, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (dtype != FOX_DTYPE_BF16) return FOX_ERR_UNSUPPORTED;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(c) || !aligned16(lse) ||
+      !aligned16(d_o) || !aligned16(delta) || !aligned16(dk) || !aligned16(dv) ||
+      !aligned16(dc_k))
+    return FOX_ERR_ALIGN;
+  if (!ds_store || ds_store_bytes < fox::ds_store_bytes(B * H, L)) return FOX_ERR_WORKSPACE;
+  if (!aligned16(ds_store)) return FOX_ERR_ALIGN;
+  return launch_status(fox::launch_bwd_dkdv_store(q, k, v, c, lse, d_o, delta, dk, dv, dc_k,
+                                                  ds_store, B * H, L, d, scale,
+                                                  static_cast<hipStream_t>(stream)));
+}
+
+int fox_attn_bwd_dq_stored(int dtype, const void* k, const void* ds_store, size_t ds_store_bytes,
+                           void* dq, float* dc_q, int B, int H, int L, int d, float scale,
+                           void* stream) {
+  if (!k || !dq || !dc_q) return FOX_ERR_NULL;
+  int st = check_dims(B, H, L, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (dtype != FOX_DTYPE_BF16) return FOX_ERR_UNSUPPORTED;
+  if (!aligned16(k) || !aligned16(dq) || !aligned16(dc_q)) return FOX_ERR_ALIGN;
+  if (!ds_store || ds_store_bytes < fox::ds_store_bytes(B * H, L)) return FOX_ERR_WORKSPACE;
+  if (!aligned16(ds_store)) return FOX_ERR_ALIGN;
+  return launch_status(fox::launch_bwd_dq_stored(k, ds_store, dq, dc_q, B * H, L, d, scale,
+                                                 static_cast<hipStream_t>(stream)));
 }
 
 int fox_dlogf_from_dc(const float* dc_q, const float* dc_k, float* d_log_f, int B, int H, int L,

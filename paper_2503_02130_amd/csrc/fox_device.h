@@ -262,6 +262,14 @@ __device__ __forceinline__ void lds_wait(bf16x4 (&r)[8]) {
                  "+v"(r[6]), "+v"(r[7])
                : "i"(N));
 }
+// The same for any number of reads: the wait, then each value passes through
+// an empty asm that comes after it (volatile asm statements keep their order).
+template <int N, int M>
+__device__ __forceinline__ void lds_wait(bf16x4 (&r)[M]) {
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"i"(N));
+#pragma unroll
+  for (int i = 0; i < M; ++i) asm volatile("" : "+v"(r[i]));
+}
 __device__ __forceinline__ bf16x8 cat4(const bf16x4& lo, const bf16x4& hi) {
   return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
 }

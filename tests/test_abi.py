@@ -203,6 +203,53 @@ def test_bwd_validation_and_workspace(lib):
                             ctypes.c_float(0.1), None) == 1
 
 
+def test_bwd_stored_validation_and_workspace(lib):
+    """The backward that keeps dS: workspace = the recompute path's, aligned to
+    256 bytes, plus 16 KB per causal (128-key block, 64-query tile) pair and
+    head; bf16 only."""
+    c = ctypes.c_void_p
+    f = ctypes.c_float(0.1)
+    base = lambda x: (x + 255) // 256 * 256
+    for B, H, L in ((2, 3, 100), (1, 1, 1), (1, 2, 64), (1, 2, 128), (2, 1, 129),
+                    (1, 1, 1000), (2, 16, 16384)):
+        nq, nk = -(-L // 64), -(-L // 128)
+        pairs = sum(1 for nb in range(nk) for qt in range(nq) if qt >= 2 * nb)
+        for d in (64, 128):
+            assert lib.fox_attn_bwd_stored_workspace_bytes(1, B, H, L, d) == \
+                base(3 * 4 * B * H * L) + B * H * pairs * 16384, (B, H, L, d)
+    assert lib.fox_attn_bwd_stored_workspace_bytes(1, 2, 16, 16384, 128) == \
+        base(12 * 32 * 16384) + 32 * 16512 * 16384  # 8.66 GB at the long-context shape
+    B, H, L, d = 2, 3, 100, 128
+    assert lib.fox_attn_bwd_stored_workspace_bytes(0, B, H, L, d) == 0  # fp32
+    assert lib.fox_attn_bwd_stored_workspace_bytes(1, B, H, L, 80) == 0
+    need = lib.fox_attn_bwd_stored_workspace_bytes(1, B, H, L, d)
+    args = [c(P16)] * 11
+    assert lib.fox_attn_bwd_stored(0, *args, c(P16), need, B, H, L, d, f, None) == 3
+    assert lib.fox_attn_bwd_stored(1, *args, c(P16), need - 1, B, H, L, d, f, None) == 5
+    assert lib.fox_attn_bwd_stored(1, *args, None, need, B, H, L, d, f, None) == 5
+    assert lib.fox_attn_bwd_stored(1, *args, c(P16 + 4), need, B, H, L, d, f, None) == 4
+    assert lib.fox_attn_bwd_stored(1, *args[:-1], None, c(P16), need, B, H, L, d, f, None) == 1
+    assert lib.fox_attn_bwd_stored(1, *args, c(P16), need, B, H, 0, d, f, None) == 2
+    store = lib.fox_attn_bwd_ds_store_bytes(1, B, H, L, d)
+    assert store == need - (3 * 4 * B * H * L + 255) // 256 * 256
+    assert lib.fox_attn_bwd_ds_store_bytes(0, B, H, L, d) == 0
+    kv = [c(P16)] * 10
+    assert lib.fox_attn_bwd_dkdv_store(1, *kv, c(P16), store - 1, B, H, L, d, f, None) == 5
+    assert lib.fox_attn_bwd_dkdv_store(1, *kv, None, store, B, H, L, d, f, None) == 5
+    assert lib.fox_attn_bwd_dkdv_store(0, *kv, c(P16), store, B, H, L, d, f, None) == 3
+    assert lib.fox_attn_bwd_dkdv_store(1, None, *kv[1:], c(P16), store, B, H, L, d, f, None) == 1
+    assert lib.fox_attn_bwd_dq_stored(1, c(P16), c(P16), store - 1, c(P16), c(P16), B, H, L, d, f,
+                                      None) == 5
+    assert lib.fox_attn_bwd_dq_stored(1, c(P16), None, store, c(P16), c(P16), B, H, L, d, f,
+                                      None) == 5
+    assert lib.fox_attn_bwd_dq_stored(1, c(P16), c(P16 + 2), store, c(P16), c(P16), B, H, L, d,
+                                      f, None) == 4
+    assert lib.fox_attn_bwd_dq_stored(0, c(P16), c(P16), store, c(P16), c(P16), B, H, L, d, f,
+                                      None) == 3
+    assert lib.fox_attn_bwd_dq_stored(1, c(P16), c(P16), store, None, c(P16), B, H, L, d, f,
+                                      None) == 1
+
+
 def test_decode_validation_and_workspace(lib):
     c = ctypes.c_void_p
     need = lib.fox_attn_decode_workspace_bytes(1, 64, 16, 32768, 128)

@@ -191,6 +191,70 @@ def test_backward_is_deterministic():
         assert torch.equal(u, w)
 
 
+# ------------------------------------------------- backward keeping dS
+STORED_CASES = ([(2, 2, 64, L) for L in (1, 2, 63, 64, 65, 127, 128, 129, 255, 256, 257, 700)] +
+                [(2, 2, 128, L) for L in (1, 31, 129, 333, 700, 1000)] +
+                [(1, 3, 128, 513), (3, 1, 64, 1100)])
+
+
+@pytest.mark.parametrize("B,H,d,L", STORED_CASES)
+def test_backward_stored_small(B, H, d, L):
+    """fox_attn_bwd_stored against the oracle; its dK/dV pass is the recompute
+    path's (bit for bit), and no read touches a stored slot the dK/dV pass did
+    not write (the workspace starts as NaN patterns)."""
+    print(f"backward stored B={B} H={H} d={d} L={L}", flush=True)
+    x = inputs.attn_inputs(B, H, L, d, "bf16", ("normal", 2.0, 1.0), 300 + L, device=DEV)
+    s = fox.default_scale(d)
+    c, o, lse = gpu_forward(x, s)
+    need = fox.fox_attn_bwd_stored_workspace_bytes(torch.bfloat16, B, H, L, d)
+    ws = torch.full((need,), 0xFF, dtype=torch.uint8, device=DEV)
+    got = fox.fox_attn_bwd_stored(x["q"], x["k"], x["v"], c, o, lse, x["do"], s, workspace=ws)
+    base = fox.fox_attn_bwd(x["q"], x["k"], x["v"], c, o, lse, x["do"], s)
+    torch.cuda.synchronize()
+    assert torch.equal(got[1], base[1]) and torch.equal(got[2], base[2])
+    for t in got:
+        assert bool(torch.isfinite(t).all())
+    xc = cpu(x)
+    ref = oracle.backward(xc["q"], xc["k"], xc["v"], xc["logit"], xc["do"], s)
+    check_bwd("bf16", got, ref, f"stored L={L}")
+    # sum(dc) = d(log f)_1 = 0: dc^q and dc^k are the row and column sums of one matrix
+    assert float(got[3][..., 0].abs().max()) <= 1e-3 * max(1.0, float(ref[3].abs().max()))
+
+
+def test_backward_stored_stages_equal_fused_entry_point():
+    """fox_attn_bwd_stored == delta -> dkdv_store -> dq_stored -> d(log f), bit
+    for bit; dkdv_store's dK, dV, dc_k equal fox_attn_bwd_dkdv's."""
+    for d in (128, 64):
+        x = inputs.attn_inputs(2, 3, 333, d, "bf16", ("normal", 1.0, 1.0), 78, device=DEV)
+        s = fox.default_scale(d)
+        c, o, lse = gpu_forward(x, s)
+        ref = fox.fox_attn_bwd_stored(x["q"], x["k"], x["v"], c, o, lse, x["do"], s)
+        delta = fox.fox_attn_bwd_delta(o, x["do"])
+        store = torch.empty(fox.fox_attn_bwd_ds_store_bytes(torch.bfloat16, 2, 3, 333, d),
+                            dtype=torch.uint8, device=DEV)
+        dk, dv, dck = fox.fox_attn_bwd_dkdv_store(x["q"], x["k"], x["v"], c, lse, x["do"], delta,
+                                                  store, s)
+        dk2, dv2, dck2 = fox.fox_attn_bwd_dkdv(x["q"], x["k"], x["v"], c, lse, x["do"], delta, s)
+        dq, dcq = fox.fox_attn_bwd_dq_stored(x["k"], store, s)
+        dlf = fox.fox_dlogf_from_dc(dcq, dck)
+        torch.cuda.synchronize()
+        for a, b in zip(ref, (dq, dk, dv, dlf)):
+            assert torch.equal(a, b), d
+        for a, b in zip((dk, dv, dck), (dk2, dv2, dck2)):
+            assert torch.equal(a, b), d
+
+
+def test_backward_stored_is_deterministic():
+    x = inputs.attn_inputs(2, 2, 777, 128, "bf16", ("normal", 1.0, 1.0), 5, device=DEV)
+    s = fox.default_scale(128)
+    c, o, lse = gpu_forward(x, s)
+    a = fox.fox_attn_bwd_stored(x["q"], x["k"], x["v"], c, o, lse, x["do"], s)
+    b = fox.fox_attn_bwd_stored(x["q"], x["k"], x["v"], c, o, lse, x["do"], s)
+    torch.cuda.synchronize()
+    for u, w in zip(a, b):
+        assert torch.equal(u, w)
+
+
 # ------------------------------------------------------------------- decode
 @pytest.mark.parametrize("dtype,d,T", [("bf16", 128, 1), ("bf16", 128, 2), ("bf16", 128, 100),
                                        ("bf16", 64, 1000), ("bf16", 128, 5000),
@@ -284,6 +348,32 @@ def test_workload_fwdbwd_bf16_b2_h16_l16384_d128():
         got = [t[b:b + 1, h:h + 1] for t in (dq, dk, dv, dlf)]
         check_bwd("bf16", got, ref, f"head {(b, h)}")
         del O, LSE, ref
+
+
+def test_workload_fwdbwd_bf16_b2_h16_l16384_d128_stored():
+    """The backward keeping dS at the long-context training shape, in the
+    benchmark's launch configuration: dK/dV equal the recompute path's bit for
+    bit, dQ and d(log f) agree with it to rounding, and sampled heads match the
+    oracle."""
+    w = W["fwdbwd_bf16_b2_h16_l16384_d128"]
+    x = inputs.workload_inputs(w, device=DEV)
+    s = fox.default_scale(w.d)
+    c, o, lse = gpu_forward(x, s)
+    got = fox.fox_attn_bwd_stored(x["q"], x["k"], x["v"], c, o, lse, x["do"], s)
+    torch.cuda.synchronize()
+    base = fox.fox_attn_bwd(x["q"], x["k"], x["v"], c, o, lse, x["do"], s)
+    torch.cuda.synchronize()
+    assert torch.equal(got[1], base[1]) and torch.equal(got[2], base[2])
+    assert rel_l2(got[0], base[0]) <= 5e-3, rel_l2(got[0], base[0])
+    assert rel_l2(got[3], base[3]) <= 5e-3, rel_l2(got[3], base[3])
+    del base
+    heads = _sampled_heads_by_gate(x["logit"], 1)
+    print(f"{w.name} (stored dS): oracle on heads {heads}", flush=True)
+    for (b, h) in heads:
+        sl = {k: v[b:b + 1, h:h + 1].cpu() for k, v in x.items()}
+        ref = oracle.backward(sl["q"], sl["k"], sl["v"], sl["logit"], sl["do"], s)
+        check_bwd("bf16", [t[b:b + 1, h:h + 1] for t in got], ref, f"head {(b, h)}")
+        del ref
 
 
 def test_workload_fwd_bf16_b1_h16_l65536_d128():
