@@ -88,7 +88,6 @@ constexpr float kSkipMargin = 160.0f;
 // pair and element 4 g2 + jj is query 16 c + 8 g2 + 4 h + jj of the half.
 // ---------------------------------------------------------------------------
 constexpr int kDsSlotBytes = 16384;
-constexpr int kNonTemporal = 2;  // cache policy of a buffer instruction: non-temporal
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 __host__ __device__ inline int ds_query_tiles(int L) { return (L + 63) / 64; }
 __host__ __device__ inline int ds_key_blocks(int L) { return (L + 127) / 128; }
@@ -358,7 +357,8 @@ void bwd_dq_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
 // Each wave holds one D x 32 accumulator, so two waves fit on a SIMD, and the
 // two roles never wait for each other inside a tile: Q / dO tiles, their row
 // statistics and P are triple-buffered (tile t + 1 loads by DMA while P works
-// on t and G on t - 1), with one barrier per tile of 64 queries.  Every LDS
+// on t and G on t - 1), with one barrier per tile of 64 queries.  The P waves
+// issue all of the DMA, so the G waves never wait for vector memory.  Every LDS
 // operand address is one of a few opaque per-lane registers plus an immediate:
 // plain reads come from the tile the role multiplies from the left (Q for P,
 // dO for G) and transposing reads from the other one, so both roles share the
@@ -421,7 +421,7 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
   const uint32_t head_bytes = (uint32_t)L * D * 2;
   const __amdgpu_buffer_rsrc_t rq = make_rsrc(Q + head * D, head_bytes);
   const __amdgpu_buffer_rsrc_t rg = make_rsrc(dO + head * D, head_bytes);
-  const uint32_t dma_off = tile_dma_offset<D, kKvWaves>(wave, lane);
+  const uint32_t dma_off = tile_dma_offset<D, kKvPairs>(pair, lane);
   int roff[D / 16];
   tile_row_offsets<D>(roff, col, h);
   int toff[2][D / 32];
@@ -522,12 +522,14 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
   auto issue_tile = [&](int qt, auto bufc) {
     constexpr int B = decltype(bufc)::value;
     const uint32_t base = (uint32_t)qt * kKvBM * D * 2;
+    if (pwave) {
 #pragma unroll
-    for (int i = 0; i < NDMA; ++i) {
-      const int wslot = (i * kKvWaves + wave) * 512;
-      const uint32_t voff = dma_off + uniform_u32(base + i * tile_dma_stride<kKvWaves>());
-      dma16(rq, &sm.q[B][wslot], voff);
-      dma16(rg, &sm.g[B][wslot], voff);
+      for (int i = 0; i < 2 * NDMA; ++i) {
+        const int wslot = (i * kKvPairs + pair) * 512;
+        const uint32_t voff = dma_off + uniform_u32(base + i * tile_dma_stride<kKvPairs>());
+        dma16(rq, &sm.q[B][wslot], voff);
+        dma16(rg, &sm.g[B][wslot], voff);
+      }
     }
   };
 
@@ -641,7 +643,11 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
   auto step = [&](int it, auto bufc) {
     constexpr int B = decltype(bufc)::value;
     constexpr int BN = (B + 1) % 3, BP = (B + 2) % 3;
-    wait_all_memory();
+    // The P waves issue every DMA of the loop and wait for it here; the G waves
+    // wait for their LDS operations only (with the stored-dS backward their
+    // vector memory counter also counts their dS stores, which need no wait).
+    if (pwave) wait_all_memory();
+    else wait_lds();
     __syncthreads();  // tile it and P of tile it - 1 are in LDS
     // tile it and all later ones add exact zeros: the G waves finish tile it - 1
     if (SKIP && it < n_tiles && sm.skip[B]) n_tiles = it;
@@ -700,7 +706,8 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
 // tile, the B operand dS^T comes out of the stored layout by transposing reads
 // (lane = query, eight keys in the contraction order of the A operand).  A tile
 // skips the stages wholly above its diagonal; those slots were never written.
-// HBM-bound: every stored dS byte is read once.
+// HBM-bound: every stored dS byte is read once, by non-temporal DMA, which
+// leaves the caches to the K tiles that neighbouring workgroups re-read.
 // ---------------------------------------------------------------------------
 constexpr int kDsWaves = 8;
 constexpr int kDsThreads = 64 * kDsWaves;
@@ -708,11 +715,18 @@ constexpr int kDsBM = 32 * kDsWaves;  // queries per workgroup
 constexpr int kDsBN = 64;             // keys per stage
 constexpr int kDsTiles = kDsBM / 64;  // query tiles per workgroup
 constexpr int kDsStageBytes = kDsSlotBytes / 2;  // one tile's dS for one stage
+// In LDS each 1 KB stored chunk takes 1152 bytes, so that the two 16-query
+// chunks of a half fall 128 bytes apart modulo the 256-byte bank row, and inside
+// a chunk the slot of lane 32 + k moves to position (32 + k) ^ 4: the 16 slots a
+// transposing read touches then sit in 16 distinct bank groups for any 32 lanes.
+constexpr int kDsChunkLds = 1152;
+constexpr int kDsStageLds = (kDsStageBytes / 1024) * kDsChunkLds;
+__device__ __forceinline__ int ds_lds_pos(int slot) { return slot ^ ((slot >> 5) << 2); }
 
 template <int D>
 struct DsSmem {
   bf16 k[2][kDsBN * D];
-  bf16x8 ds[2][kDsTiles][kDsStageBytes / 16];
+  bf16x8 ds[2][kDsTiles][kDsStageLds / 16];
 };
 
 template <int D>
@@ -755,8 +769,9 @@ __global__ __launch_bounds__(kDsThreads) void bwd_dq_stored_kernel(
       taddr[k2][db] = (uint32_t)(uintptr_t)lds_opaque(lds_ptr(&sm.k[0][0]) + 2 * toff[k2][db]);
   const int g16 = lane >> 4, j16 = lane & 15, cg = j16 & 3;
   const uint32_t ds_addr = (uint32_t)(uintptr_t)lds_opaque(
-      lds_ptr(&sm.ds[0][my_t][0]) + (2 * qb + (g16 & 1)) * 1024 +
-      ((cg & 1) * 32 + 4 * (g16 >> 1) + (j16 >> 2)) * 16 + (cg >> 1) * 8);
+      lds_ptr(&sm.ds[0][my_t][0]) + (2 * qb + (g16 & 1)) * kDsChunkLds +
+      ds_lds_pos((cg & 1) * 32 + 4 * (g16 >> 1) + (j16 >> 2)) * 16 + (cg >> 1) * 8);
+  const uint32_t ds_src = (uint32_t)ds_lds_pos(lane) * 16;  // DMA: stored slot of LDS position lane
 
   f32x16 dqacc[D / 32];
 #pragma unroll
@@ -781,17 +796,16 @@ __global__ __launch_bounds__(kDsThreads) void bwd_dq_stored_kernel(
           ds_store + (head_slot + ds_slot(L, nb, qt0 + t_lo)) * (kDsSlotBytes / 16),
           (uint32_t)(t_hi - t_lo) * kDsSlotBytes);
       for (int t = t_lo; t < t_hi; ++t)
-        dma16(rs, &sm.ds[B][t][wave * 64],
-              (uint32_t)lane * 16 +
-                  uniform_u32((uint32_t)(t - t_lo) * kDsSlotBytes +
-                              (uint32_t)(j & 1) * kDsStageBytes + (uint32_t)wave * 1024));
+        dma16_nt(rs, &sm.ds[B][t][wave * (kDsChunkLds / 16)],
+              ds_src + uniform_u32((uint32_t)(t - t_lo) * kDsSlotBytes +
+                                   (uint32_t)(j & 1) * kDsStageBytes + (uint32_t)wave * 1024));
     }
   };
   auto body = [&](auto bufc) {
     constexpr int B = decltype(bufc)::value;
     static_for<kDsBN / 16>([&](auto sc) {
       constexpr int S = decltype(sc)::value;  // 16-key step: pair S / 2, keys 16 (S % 2) ..
-      constexpr int DOFF = B * (int)sizeof(sm.ds[0]) + (S / 2) * 4096 + (S % 2) * 256;
+      constexpr int DOFF = B * (int)sizeof(sm.ds[0]) + (S / 2) * 4 * kDsChunkLds + (S % 2) * 256;
       constexpr int KOFF = 2 * (B * TILE + S * 16 * D);
       bf16x4 t[2 * (D / 32) + 2];
       t[0] = ds_read_tr_asm<DOFF>(ds_addr);

@@ -177,9 +177,19 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
                                            0x00020000);
 }
 
+constexpr int kNonTemporal = 2;  // cache policy of a buffer instruction: non-temporal
+
 __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rsrc, void* lds_wave_base,
                                       uint32_t voffset) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t*)lds_wave_base, 16, voffset, 0, 0, 0);
+}
+
+// The same for data read once: non-temporal, so that it does not displace what
+// the caches hold for reuse.
+__device__ __forceinline__ void dma16_nt(__amdgpu_buffer_rsrc_t rsrc, void* lds_wave_base,
+                                         uint32_t voffset) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t*)lds_wave_base, 16, voffset, 0, 0,
+                                           kNonTemporal);
 }
 
 // The same with 4 bytes per lane: lane l's dword lands at lds_wave_base + 4 * l.
@@ -191,6 +201,10 @@ __device__ __forceinline__ void dma4(__amdgpu_buffer_rsrc_t rsrc, void* lds_wave
 // Wait until every outstanding memory operation of this wave (including the
 // LDS-bound buffer loads above) has completed.
 __device__ __forceinline__ void wait_all_memory() { __builtin_amdgcn_s_waitcnt(0); }
+// Wait until every LDS operation of this wave has completed (s_waitcnt with
+// lgkmcnt = 0 and the vector-memory and export counts at their maxima, which
+// wait for nothing).
+__device__ __forceinline__ void wait_lds() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 
 // Transposing LDS read (ds_read_b64_tr_b16).  Within each group of 16 lanes,
 // lane j supplies the address of 4 consecutive bf16 in row (j / 4) of a 4 x 16
