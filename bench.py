@@ -221,8 +221,9 @@ def bench_train(w, steps, warmup):
 def bench_pro(w, steps, warmup):
     """The FoX (Pro) layer's hot path at the training workload's shape: prologue
     (QK-norm, KV-shift), attention with the output norm and gate fused into the
-    forward's epilogue, its backward (norm/gate backward fused with Delta), and
-    the prologue's backward.  Each part is timed on its own."""
+    forward's epilogue, its backward (norm/gate backward fused with Delta; the
+    attention backward keeping dS, as in the training step), and the prologue's
+    backward.  Each part is timed on its own."""
     dev = torch.device("cuda:0")
     B, H, L, d = w.B, w.H, w.L, w.d
     x = inputs.pro_inputs(B, H, L, d, w.dtype, w.gate, w.seed + 1, device=dev)
@@ -233,8 +234,8 @@ def bench_pro(w, steps, warmup):
     lse = torch.empty((B, H, L), device=dev)
     pws = torch.empty(fox.fox_pro_prologue_bwd_workspace_bytes(q.dtype, B, H, L, d), device=dev,
                       dtype=torch.uint8)
-    bws = torch.empty(fox.fox_attn_bwd_pro_workspace_bytes(q.dtype, B, H, L, d), device=dev,
-                      dtype=torch.uint8)
+    bws = torch.empty(fox.fox_attn_bwd_pro_stored_workspace_bytes(q.dtype, B, H, L, d),
+                      device=dev, dtype=torch.uint8)
     pargs = (x["q_raw"], x["k_raw"], x["v_raw"], x["k_shift"], x["v_shift"], x["wq"], x["wk"])
     timers = {n: EventTimer() for n in ("prologue", "fwd_pro", "bwd_pro", "prologue_bwd",
                                          "out_gate")}
@@ -246,8 +247,8 @@ def bench_pro(w, steps, warmup):
         with timers["fwd_pro"].maybe(timed):
             fox.fox_attn_fwd_pro(q, k, v, c, x["g"], x["wo"], s, o=o, lse=lse, y=y)
         with timers["bwd_pro"].maybe(timed):
-            grads["attn"] = fox.fox_attn_bwd_pro(q, k, v, c, o, lse, x["g"], x["wo"], x["dy"], s,
-                                                 workspace=bws)
+            grads["attn"] = fox.fox_attn_bwd_pro_stored(q, k, v, c, o, lse, x["g"], x["wo"],
+                                                        x["dy"], s, workspace=bws)
         dq, dk, dv = grads["attn"][:3]
         with timers["prologue_bwd"].maybe(timed):
             grads["pro"] = fox.fox_pro_prologue_bwd(*pargs, dq, dk, dv, workspace=pws)
@@ -702,7 +703,8 @@ def main():
         out["pro"] = {
             "what": "FoX (Pro) layer hot path at the same shape: prologue (QK-norm, KV-shift) -> "
                     "attention with the output RMSNorm and sigmoid gate in the forward epilogue "
-                    "-> its backward (norm/gate backward fused with Delta) -> prologue backward",
+                    "-> its backward (norm/gate backward fused with Delta, attention backward "
+                    "keeping dS: fox_attn_bwd_pro_stored) -> prologue backward",
             "ms_per_step": round(pro_ms, 4),
             "overhead_vs_plain_step": round(pro_ms / (r["fwd_ms"] + r["bwd_ms"]) - 1.0, 4),
             "fwd_pro_ms": round(rp["fwd_pro"], 4), "bwd_pro_ms": round(rp["bwd_pro"], 4),

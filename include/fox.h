@@ -388,6 +388,22 @@ int fox_attn_bwd_pro(int dtype, const void* q, const void* k, const void* v, con
                      void* workspace, size_t workspace_bytes, int B, int H, int L, int d,
                      float scale, void* stream);
 
+/*
+ * fox_attn_bwd_pro with the attention backward keeping dS, as
+ * fox_attn_bwd_stored does: bf16 only (FOX_ERR_UNSUPPORTED for fp32); the
+ * workspace is at least fox_attn_bwd_pro_stored_workspace_bytes() (0 for fp32
+ * or invalid arguments), about B H L^2 bytes.  Arguments, outputs and errors
+ * otherwise as for fox_attn_bwd_pro; dK, dV and the gate and norm-weight
+ * gradients are bit for bit the same, dQ and d(log f) agree to rounding.
+ */
+size_t fox_attn_bwd_pro_stored_workspace_bytes(int dtype, int B, int H, int L, int d);
+int fox_attn_bwd_pro_stored(int dtype, const void* q, const void* k, const void* v,
+                            const float* c, const void* o, const float* lse, const void* g_logit,
+                            const float* o_norm_weight, float eps, const void* dy, void* dq,
+                            void* dk, void* dv, float* d_log_f, void* dg_logit,
+                            float* do_norm_weight, void* workspace, size_t workspace_bytes,
+                            int B, int H, int L, int d, float scale, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

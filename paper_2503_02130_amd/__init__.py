@@ -18,7 +18,8 @@ from ._lib import (  # noqa: F401
     fox_pro_prologue, fox_pro_prologue_bwd, fox_pro_prologue_bwd_workspace_bytes,
     fox_pro_output_gate, fox_attn_fwd_pro, fox_attn_bwd_pro, fox_attn_bwd_pro_workspace_bytes,
     fox_attn_bwd_stored, fox_attn_bwd_stored_workspace_bytes, fox_attn_bwd_ds_store_bytes,
-    fox_attn_bwd_dkdv_store, fox_attn_bwd_dq_stored,
+    fox_attn_bwd_dkdv_store, fox_attn_bwd_dq_stored, fox_attn_bwd_pro_stored,
+    fox_attn_bwd_pro_stored_workspace_bytes,
     EXPORTED,
 )
 
@@ -37,4 +38,5 @@ __all__ = [
     "fox_pro_output_gate", "fox_attn_fwd_pro", "fox_attn_bwd_pro",
     "fox_attn_bwd_pro_workspace_bytes", "fox_attn_bwd_stored", "fox_attn_bwd_stored_workspace_bytes",
     "fox_attn_bwd_ds_store_bytes", "fox_attn_bwd_dkdv_store", "fox_attn_bwd_dq_stored",
+    "fox_attn_bwd_pro_stored", "fox_attn_bwd_pro_stored_workspace_bytes",
 ]

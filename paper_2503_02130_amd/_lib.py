@@ -36,6 +36,7 @@ EXPORTED = (
     "fox_pro_output_gate", "fox_attn_fwd_pro", "fox_attn_bwd_pro_workspace_bytes",
     "fox_attn_bwd_pro", "fox_attn_bwd_stored_workspace_bytes", "fox_attn_bwd_stored",
     "fox_attn_bwd_ds_store_bytes", "fox_attn_bwd_dkdv_store", "fox_attn_bwd_dq_stored",
+    "fox_attn_bwd_pro_stored_workspace_bytes", "fox_attn_bwd_pro_stored",
 )
 
 
@@ -138,6 +139,11 @@ def load() -> ctypes.CDLL:
     lib.fox_attn_bwd_pro_workspace_bytes.argtypes = [I, I, I, I, I]
     lib.fox_attn_bwd_pro.restype = I
     lib.fox_attn_bwd_pro.argtypes = [I, P, P, P, P, P, P, P, P, F, P, P, P, P, P, P, P, P, Z, I, I,
+                                     I, I, F, P]
+    lib.fox_attn_bwd_pro_stored_workspace_bytes.restype = Z
+    lib.fox_attn_bwd_pro_stored_workspace_bytes.argtypes = [I, I, I, I, I]
+    lib.fox_attn_bwd_pro_stored.restype = I
+    lib.fox_attn_bwd_pro_stored.argtypes = [I, P, P, P, P, P, P, P, P, F, P, P, P, P, P, P, P, P, Z, I, I,
                                      I, I, F, P]
     _lib = lib
     return lib
@@ -867,6 +873,25 @@ def fox_attn_bwd_pro_workspace_bytes(dtype: torch.dtype, B: int, H: int, L: int,
 def fox_attn_bwd_pro(q, k, v, c, o, lse, g_logit, o_norm_weight, dy,
                      scale: Optional[float] = None, eps: float = 1e-6, workspace=None):
     """Gradients of sum(y * dy): (dq, dk, dv, d_log_f, dg_logit, do_norm_weight)."""
+    return _attn_bwd_pro_call("fox_attn_bwd_pro", fox_attn_bwd_pro_workspace_bytes, q, k, v, c,
+                              o, lse, g_logit, o_norm_weight, dy, scale, eps, workspace)
+
+
+def fox_attn_bwd_pro_stored_workspace_bytes(dtype: torch.dtype, B: int, H: int, L: int,
+                                            d: int) -> int:
+    return int(load().fox_attn_bwd_pro_stored_workspace_bytes(_DT[dtype], B, H, L, d))
+
+
+def fox_attn_bwd_pro_stored(q, k, v, c, o, lse, g_logit, o_norm_weight, dy,
+                            scale: Optional[float] = None, eps: float = 1e-6, workspace=None):
+    """fox_attn_bwd_pro keeping dS in the workspace (about B*H*L^2 bytes); bf16 only."""
+    return _attn_bwd_pro_call("fox_attn_bwd_pro_stored", fox_attn_bwd_pro_stored_workspace_bytes,
+                              q, k, v, c, o, lse, g_logit, o_norm_weight, dy, scale, eps,
+                              workspace)
+
+
+def _attn_bwd_pro_call(entry, ws_bytes, q, k, v, c, o, lse, g_logit, o_norm_weight, dy, scale,
+                       eps, workspace):
     B, H, L, d, dt, dev = _pro_shapes(q)
     for name, t in (("q", q), ("k", k), ("v", v), ("o", o), ("g_logit", g_logit), ("dy", dy)):
         _check(t, name, (B, H, L, d), dt, dev)
@@ -876,14 +901,14 @@ def fox_attn_bwd_pro(q, k, v, c, o, lse, g_logit, o_norm_weight, dy,
     dq, dk, dv, dg = (torch.empty_like(q) for _ in range(4))
     dlf = torch.empty_like(c)
     dw = torch.empty_like(o_norm_weight)
-    need = fox_attn_bwd_pro_workspace_bytes(dt, B, H, L, d)
+    need = ws_bytes(dt, B, H, L, d)
     if workspace is None:
         workspace = torch.empty(max(need, 16), device=dev, dtype=torch.uint8)
     s = default_scale(d) if scale is None else float(scale)
-    st = load().fox_attn_bwd_pro(_DT[dt], _ptr(q), _ptr(k), _ptr(v), _ptr(c), _ptr(o), _ptr(lse),
-                                 _ptr(g_logit), _ptr(o_norm_weight), float(eps), _ptr(dy),
-                                 _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dlf), _ptr(dg), _ptr(dw),
-                                 _ptr(workspace), workspace.numel() * workspace.element_size(),
-                                 B, H, L, d, s, _stream(q))
-    _raise(st, "fox_attn_bwd_pro")
+    st = getattr(load(), entry)(_DT[dt], _ptr(q), _ptr(k), _ptr(v), _ptr(c), _ptr(o), _ptr(lse),
+                                _ptr(g_logit), _ptr(o_norm_weight), float(eps), _ptr(dy),
+                                _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dlf), _ptr(dg), _ptr(dw),
+                                _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                B, H, L, d, s, _stream(q))
+    _raise(st, entry)
     return dq, dk, dv, dlf, dg, dw

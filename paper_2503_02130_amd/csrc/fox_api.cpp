@@ -613,12 +613,14 @@ size_t fox_attn_bwd_pro_workspace_bytes(int dtype, int B, int H, int L, int d) {
   return fox::bwd_pro_workspace_bytes(dtype == FOX_DTYPE_BF16, B * H, L, d);
 }
 
-int fox_attn_bwd_pro(int dtype, const void* q, const void* k, const void* v, const float* c,
-                     const void* o, const float* lse, const void* g_logit,
-                     const float* o_norm_weight, float eps, const void* dy, void* dq, void* dk,
-                     void* dv, float* d_log_f, void* dg_logit, float* do_norm_weight,
-                     void* workspace, size_t workspace_bytes, int B, int H, int L, int d,
-                     float scale, void* stream) {
+// fox_attn_bwd_pro and fox_attn_bwd_pro_stored: the same checks, the attention
+// backward recomputing or keeping dS.
+static int attn_bwd_pro(bool keep_ds, int dtype, const void* q, const void* k, const void* v,
+                        const float* c, const void* o, const float* lse, const void* g_logit,
+                        const float* o_norm_weight, float eps, const void* dy, void* dq,
+                        void* dk, void* dv, float* d_log_f, void* dg_logit, float* do_norm_weight,
+                        void* workspace, size_t workspace_bytes, int B, int H, int L, int d,
+                        float scale, void* stream) {
   if (!all_set({q, k, v, c, o, lse, g_logit, o_norm_weight, dy, dq, dk, dv, d_log_f, dg_logit,
                 do_norm_weight}))
     return FOX_ERR_NULL;
@@ -631,13 +633,42 @@ int fox_attn_bwd_pro(int dtype, const void* q, const void* k, const void* v, con
                       dg_logit, do_norm_weight}))
     return FOX_ERR_ALIGN;
   const bool bf = dtype == FOX_DTYPE_BF16;
-  if (!workspace || workspace_bytes < fox::bwd_pro_workspace_bytes(bf, B * H, L, d))
-    return FOX_ERR_WORKSPACE;
+  if (keep_ds && !bf) return FOX_ERR_UNSUPPORTED;
+  const size_t need = keep_ds ? fox::bwd_pro_stored_workspace_bytes(B * H, L, d)
+                              : fox::bwd_pro_workspace_bytes(bf, B * H, L, d);
+  if (!workspace || workspace_bytes < need) return FOX_ERR_WORKSPACE;
   if (!aligned16(workspace)) return FOX_ERR_ALIGN;
   return launch_status(fox::launch_bwd_pro(bf, q, k, v, c, o, lse, g_logit, o_norm_weight, eps,
                                            dy, dq, dk, dv, d_log_f, dg_logit, do_norm_weight,
                                            workspace, H, B * H, L, d, scale,
-                                           static_cast<hipStream_t>(stream)));
+                                           static_cast<hipStream_t>(stream), keep_ds));
+}
+
+int fox_attn_bwd_pro(int dtype, const void* q, const void* k, const void* v, const float* c,
+                     const void* o, const float* lse, const void* g_logit,
+                     const float* o_norm_weight, float eps, const void* dy, void* dq, void* dk,
+                     void* dv, float* d_log_f, void* dg_logit, float* do_norm_weight,
+                     void* workspace, size_t workspace_bytes, int B, int H, int L, int d,
+                     float scale, void* stream) {
+  return attn_bwd_pro(false, dtype, q, k, v, c, o, lse, g_logit, o_norm_weight, eps, dy, dq, dk,
+                      dv, d_log_f, dg_logit, do_norm_weight, workspace, workspace_bytes, B, H, L,
+                      d, scale, stream);
+}
+
+size_t fox_attn_bwd_pro_stored_workspace_bytes(int dtype, int B, int H, int L, int d) {
+  if (check_dims(B, H, L, d) || check_dtype_d(dtype, d) || dtype != FOX_DTYPE_BF16) return 0;
+  return fox::bwd_pro_stored_workspace_bytes(B * H, L, d);
+}
+
+int fox_attn_bwd_pro_stored(int dtype, const void* q, const void* k, const void* v,
+                            const float* c, const void* o, const float* lse, const void* g_logit,
+                            const float* o_norm_weight, float eps, const void* dy, void* dq,
+                            void* dk, void* dv, float* d_log_f, void* dg_logit,
+                            float* do_norm_weight, void* workspace, size_t workspace_bytes, int B,
+                            int H, int L, int d, float scale, void* stream) {
+  return attn_bwd_pro(true, dtype, q, k, v, c, o, lse, g_logit, o_norm_weight, eps, dy, dq, dk,
+                      dv, d_log_f, dg_logit, do_norm_weight, workspace, workspace_bytes, B, H, L,
+                      d, scale, stream);
 }
 
 }  // extern "C"

@@ -124,10 +124,13 @@ hipError_t launch_fwd_bf16_out_gate(const void* q, const void* k, const void* v,
                                     hipStream_t s);
 // backward of attention + output norm and gate: the norm/gate backward writes dO
 // and Delta into the workspace, then the attention backward stages run
+// keep_ds (bf16 only): the attention backward keeps dS, in a workspace of
+// bwd_pro_stored_workspace_bytes (the one above, aligned, then the stored dS).
+size_t bwd_pro_stored_workspace_bytes(int BH, int L, int d);
 hipError_t launch_bwd_pro(bool bf16, const void* q, const void* k, const void* v, const float* c,
                           const void* o, const float* lse, const void* g, const float* wo,
                           float eps, const void* dy, void* dq, void* dk, void* dv, float* d_log_f,
                           void* dg, float* dwo, void* ws, int H, int BH, int L, int d, float scale,
-                          hipStream_t s);
+                          hipStream_t s, bool keep_ds = false);
 
 }  // namespace fox

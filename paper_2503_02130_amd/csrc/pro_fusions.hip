@@ -519,11 +519,15 @@ static void out_gate_bwd_t(const void* o, const void* g, const float* wo, float 
                      delta, pwo, H, L, nc);
 }
 
+size_t bwd_pro_stored_workspace_bytes(int BH, int L, int d) {
+  return align256(bwd_pro_workspace_bytes(true, BH, L, d)) + ds_store_bytes(BH, L);
+}
+
 hipError_t launch_bwd_pro(bool bf16_, const void* q, const void* k, const void* v, const float* c,
                           const void* o, const float* lse, const void* g, const float* wo,
                           float eps, const void* dy, void* dq, void* dk, void* dv, float* d_log_f,
                           void* dg, float* dwo, void* ws, int H, int BH, int L, int d, float scale,
-                          hipStream_t s) {
+                          hipStream_t s, bool keep_ds) {
   const int nc = pro_chunks(L);
   const size_t es = bf16_ ? 2 : 4;
   char* w = static_cast<char*>(ws);
@@ -545,10 +549,17 @@ hipError_t launch_bwd_pro(bool bf16_, const void* q, const void* k, const void* 
                      dim3(kReduceThreads), 0, s, pwo, dwo, BH / H, H, nc, d);
   e = hipGetLastError();
   const GateSpec gs = gate_array(c);
-  if (e == hipSuccess)
-    e = launch_bwd_dkdv(bf16_, q, k, v, gs, lse, d_o, delta, dk, dv, dck, BH, L, d, scale, s);
-  if (e == hipSuccess)
-    e = launch_bwd_dq(bf16_, q, k, v, gs, lse, d_o, delta, dq, dcq, BH, L, d, scale, s);
+  if (keep_ds) {
+    void* dss = w + align256(bwd_pro_workspace_bytes(true, BH, L, d));
+    if (e == hipSuccess)
+      e = launch_bwd_dkdv_store(q, k, v, c, lse, d_o, delta, dk, dv, dck, dss, BH, L, d, scale, s);
+    if (e == hipSuccess) e = launch_bwd_dq_stored(k, dss, dq, dcq, BH, L, d, scale, s);
+  } else {
+    if (e == hipSuccess)
+      e = launch_bwd_dkdv(bf16_, q, k, v, gs, lse, d_o, delta, dk, dv, dck, BH, L, d, scale, s);
+    if (e == hipSuccess)
+      e = launch_bwd_dq(bf16_, q, k, v, gs, lse, d_o, delta, dq, dcq, BH, L, d, scale, s);
+  }
   if (e == hipSuccess) e = launch_reverse_scan_sum(dcq, dck, d_log_f, BH, L, s);
   return e;
 }

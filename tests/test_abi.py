@@ -167,6 +167,15 @@ def test_pro_validation_and_workspace(lib):
                                 None) == 5
     assert lib.fox_attn_bwd_pro(1, *args, f(-1.0), *grads, c(P16), bneed, B, H, L, d, f(0.1),
                                 None) == 7
+    sneed = lib.fox_attn_bwd_pro_stored_workspace_bytes(1, B, H, L, d)
+    assert sneed == base(bneed) + lib.fox_attn_bwd_ds_store_bytes(1, B, H, L, d)
+    assert lib.fox_attn_bwd_pro_stored_workspace_bytes(0, B, H, L, d) == 0
+    assert lib.fox_attn_bwd_pro_stored(1, *args, f(1e-6), *grads, c(P16), sneed - 1, B, H, L, d,
+                                       f(0.1), None) == 5
+    assert lib.fox_attn_bwd_pro_stored(0, *args, f(1e-6), *grads, c(P16), sneed, B, H, L, d,
+                                       f(0.1), None) == 3
+    assert lib.fox_attn_bwd_pro_stored(1, *args, f(-1.0), *grads, c(P16), sneed, B, H, L, d,
+                                       f(0.1), None) == 7
 
 
 def test_fixed_gate_skip_validation(lib):

@@ -674,6 +674,18 @@ def test_pro_attention_forward_backward(dtype, d, L):
                               xc["wo"], PRO_EPS, s, xc["dy"])
     for name, g, r in zip(("dQ", "dK", "dV", "dlogf", "dg", "dwo"), grads, ref):
         check_grad(dtype, name, g, r, f"L={L}")
+    if dtype == "bf16":
+        # the same backward keeping dS: dK, dV, dg, dwo bit for bit, dQ and
+        # d(log f) to rounding; the workspace starts as NaN patterns
+        need = fox.fox_attn_bwd_pro_stored_workspace_bytes(torch.bfloat16, 2, 3, L, d)
+        ws = torch.full((need,), 0xFF, dtype=torch.uint8, device=DEV)
+        kept = fox.fox_attn_bwd_pro_stored(q, k, v, c, o, lse, x["g"], x["wo"], x["dy"], s,
+                                           eps=PRO_EPS, workspace=ws)
+        torch.cuda.synchronize()
+        for i in (1, 2, 4, 5):
+            assert torch.equal(kept[i], grads[i]), i
+        for name, g, r in zip(("dQ", "dK", "dV", "dlogf", "dg", "dwo"), kept, ref):
+            check_grad(dtype, name, g, r, f"stored L={L}")
 
 
 def test_pro_layer_chain_bf16():
