@@ -115,8 +115,8 @@ int fox_attn_bwd(int dtype, const void* q, const void* k, const void* v, const f
  * half: the dK/dV pass also writes the bf16 dS it forms, and the dQ pass reads
  * it instead of recomputing S, P and dP (dQ = s dS K, dc^q = rowsum(dS)).  The
  * workspace grows with L^2: 16 KB per (128-key block, 64-query tile) pair of the
- * causal order, per (b, h): about B H L^2 bytes, 8.7 GB at B = 2, H = 16,
- * L = 16384 (fox_attn_bwd needs 12 B H L bytes).  bf16 only (FOX_ERR_UNSUPPORTED
+ * causal order, per (b, h), plus 4 bytes per (b, h, key block): about B H L^2
+ * bytes, 8.7 GB at B = 2, H = 16, L = 16384 (fox_attn_bwd needs 12 B H L bytes).  bf16 only (FOX_ERR_UNSUPPORTED
  * for fp32).  Arguments, outputs and errors as for fox_attn_bwd; the workspace is
  * at least fox_attn_bwd_stored_workspace_bytes() (0 for fp32 or invalid
  * arguments).  Results agree with fox_attn_bwd to rounding (the two dQ halves sum
@@ -261,6 +261,15 @@ int fox_attn_bwd_skip(int dtype, const void* q, const void* k, const void* v, co
                       const float* k_norm_max, void* dq, void* dk, void* dv, float* d_log_f,
                       void* workspace, size_t workspace_bytes, int B, int H, int L, int d,
                       float scale, void* stream);
+/* fox_attn_bwd_skip keeping dS (as fox_attn_bwd_stored; bf16 only): the dK/dV pass
+ * stores the dS of the tiles it computes and the dQ pass reads only those.  Workspace:
+ * at least fox_attn_bwd_stored_workspace_bytes().  Results are bitwise those of
+ * fox_attn_bwd_stored. */
+int fox_attn_bwd_skip_stored(int dtype, const void* q, const void* k, const void* v,
+                             const float* c, const void* o, const float* lse, const void* d_o,
+                             const float* q_norm_max, const float* k_norm_max, void* dq, void* dk,
+                             void* dv, float* d_log_f, void* workspace, size_t workspace_bytes,
+                             int B, int H, int L, int d, float scale, void* stream);
 int fox_attn_decode_skip(int dtype, const void* q, const void* k_cache, const void* v_cache,
                          float* c_cache, const float* gate_logit_new, const float* k_norm_max,
                          void* o, float* lse, void* workspace, size_t workspace_bytes, int B,
@@ -295,6 +304,25 @@ int fox_attn_bwd_fixed_gate(int dtype, const void* q, const void* k, const void*
                             const void* d_o, void* dq, void* dk, void* dv, float* d_gate_bias,
                             void* workspace, size_t workspace_bytes, int B, int H, int L, int d,
                             float scale, void* stream);
+/* fox_attn_bwd_fixed_gate keeping dS (as fox_attn_bwd_stored; bf16 only), and
+ * fox_attn_bwd_fixed_gate_skip keeping dS (bitwise the results of
+ * fox_attn_bwd_fixed_gate_stored).  Workspace: at least
+ * fox_attn_bwd_fixed_gate_stored_workspace_bytes() (0 for fp32 or invalid
+ * arguments), about B H L^2 bytes.  dK and dV are bit for bit those of
+ * fox_attn_bwd_fixed_gate; dQ and the bias gradient agree to rounding. */
+size_t fox_attn_bwd_fixed_gate_stored_workspace_bytes(int dtype, int B, int H, int L, int d);
+int fox_attn_bwd_fixed_gate_stored(int dtype, const void* q, const void* k, const void* v,
+                                   const float* gate_bias, const void* o, const float* lse,
+                                   const void* d_o, void* dq, void* dk, void* dv,
+                                   float* d_gate_bias, void* workspace, size_t workspace_bytes,
+                                   int B, int H, int L, int d, float scale, void* stream);
+int fox_attn_bwd_fixed_gate_skip_stored(int dtype, const void* q, const void* k, const void* v,
+                                        const float* gate_bias, const void* o, const float* lse,
+                                        const void* d_o, const float* q_norm_max,
+                                        const float* k_norm_max, void* dq, void* dk, void* dv,
+                                        float* d_gate_bias, void* workspace,
+                                        size_t workspace_bytes, int B, int H, int L, int d,
+                                        float scale, void* stream);
 int fox_attn_decode_fixed_gate(int dtype, const void* q, const void* k_cache,
                                const void* v_cache, const float* gate_bias, void* o, float* lse,
                                void* workspace, size_t workspace_bytes, int B, int H, int T, int d,

@@ -19,7 +19,9 @@ from ._lib import (  # noqa: F401
     fox_pro_output_gate, fox_attn_fwd_pro, fox_attn_bwd_pro, fox_attn_bwd_pro_workspace_bytes,
     fox_attn_bwd_stored, fox_attn_bwd_stored_workspace_bytes, fox_attn_bwd_ds_store_bytes,
     fox_attn_bwd_dkdv_store, fox_attn_bwd_dq_stored, fox_attn_bwd_pro_stored,
-    fox_attn_bwd_pro_stored_workspace_bytes,
+    fox_attn_bwd_pro_stored_workspace_bytes, fox_attn_bwd_skip_stored,
+    fox_attn_bwd_fixed_gate_stored, fox_attn_bwd_fixed_gate_stored_workspace_bytes,
+    fox_attn_bwd_fixed_gate_skip_stored,
     EXPORTED,
 )
 
@@ -39,4 +41,6 @@ __all__ = [
     "fox_attn_bwd_pro_workspace_bytes", "fox_attn_bwd_stored", "fox_attn_bwd_stored_workspace_bytes",
     "fox_attn_bwd_ds_store_bytes", "fox_attn_bwd_dkdv_store", "fox_attn_bwd_dq_stored",
     "fox_attn_bwd_pro_stored", "fox_attn_bwd_pro_stored_workspace_bytes",
+    "fox_attn_bwd_skip_stored", "fox_attn_bwd_fixed_gate_stored",
+    "fox_attn_bwd_fixed_gate_stored_workspace_bytes", "fox_attn_bwd_fixed_gate_skip_stored",
 ]

@@ -37,6 +37,8 @@ EXPORTED = (
     "fox_attn_bwd_pro", "fox_attn_bwd_stored_workspace_bytes", "fox_attn_bwd_stored",
     "fox_attn_bwd_ds_store_bytes", "fox_attn_bwd_dkdv_store", "fox_attn_bwd_dq_stored",
     "fox_attn_bwd_pro_stored_workspace_bytes", "fox_attn_bwd_pro_stored",
+    "fox_attn_bwd_skip_stored", "fox_attn_bwd_fixed_gate_stored_workspace_bytes",
+    "fox_attn_bwd_fixed_gate_stored", "fox_attn_bwd_fixed_gate_skip_stored",
 )
 
 
@@ -122,6 +124,13 @@ def load() -> ctypes.CDLL:
     lib.fox_attn_bwd_fixed_gate_skip.restype = I
     lib.fox_attn_bwd_fixed_gate_skip.argtypes = [I, P, P, P, P, P, P, P, P, P, P, P, P, P, P, Z,
                                                  I, I, I, I, F, P]
+    for name, twin in (("fox_attn_bwd_skip_stored", "fox_attn_bwd_skip"),
+                       ("fox_attn_bwd_fixed_gate_stored", "fox_attn_bwd_fixed_gate"),
+                       ("fox_attn_bwd_fixed_gate_skip_stored", "fox_attn_bwd_fixed_gate_skip")):
+        getattr(lib, name).restype = I
+        getattr(lib, name).argtypes = getattr(lib, twin).argtypes
+    lib.fox_attn_bwd_fixed_gate_stored_workspace_bytes.restype = Z
+    lib.fox_attn_bwd_fixed_gate_stored_workspace_bytes.argtypes = [I, I, I, I, I]
     lib.fox_attn_decode_fixed_gate_skip.restype = I
     lib.fox_attn_decode_fixed_gate_skip.argtypes = [I, P, P, P, P, P, P, P, P, Z, I, I, I, I, F, P]
     lib.fox_pro_prologue.restype = I
@@ -510,6 +519,27 @@ def fox_attn_bwd_fixed_gate(q, k, v, gate_bias, o, lse, d_o, scale: Optional[flo
                             dq=None, dk=None, dv=None, d_gate_bias=None, want_bias_grad=True,
                             workspace=None):
     """dq, dk, dv and d gate_bias [H] (None when want_bias_grad is False)."""
+    return _bwd_fixed_call("fox_attn_bwd_fixed_gate", fox_attn_bwd_fixed_gate_workspace_bytes, q,
+                           k, v, gate_bias, o, lse, d_o, scale, dq, dk, dv, d_gate_bias,
+                           want_bias_grad, workspace)
+
+
+def fox_attn_bwd_fixed_gate_stored_workspace_bytes(dtype: torch.dtype, B: int, H: int, L: int,
+                                                   d: int) -> int:
+    return int(load().fox_attn_bwd_fixed_gate_stored_workspace_bytes(_DT[dtype], B, H, L, d))
+
+
+def fox_attn_bwd_fixed_gate_stored(q, k, v, gate_bias, o, lse, d_o, scale: Optional[float] = None,
+                                   dq=None, dk=None, dv=None, d_gate_bias=None,
+                                   want_bias_grad=True, workspace=None):
+    """fox_attn_bwd_fixed_gate keeping dS (about B*H*L^2 bytes of workspace); bf16 only."""
+    return _bwd_fixed_call("fox_attn_bwd_fixed_gate_stored",
+                           fox_attn_bwd_fixed_gate_stored_workspace_bytes, q, k, v, gate_bias, o,
+                           lse, d_o, scale, dq, dk, dv, d_gate_bias, want_bias_grad, workspace)
+
+
+def _bwd_fixed_call(entry, ws_bytes, q, k, v, gate_bias, o, lse, d_o, scale, dq, dk, dv,
+                    d_gate_bias, want_bias_grad, workspace):
     B, H, L, d = q.shape
     dt = q.dtype
     if dt not in _DT:
@@ -529,16 +559,16 @@ def fox_attn_bwd_fixed_gate(q, k, v, gate_bias, o, lse, d_o, scale: Optional[flo
         _check(d_gate_bias, "d_gate_bias", (H,), torch.float32, dev)
     else:
         d_gate_bias = None
-    need = fox_attn_bwd_fixed_gate_workspace_bytes(dt, B, H, L, d)
+    need = ws_bytes(dt, B, H, L, d)
     if workspace is None:
         workspace = torch.empty(max(need, 16), device=dev, dtype=torch.uint8)
     s = default_scale(d) if scale is None else float(scale)
-    st = load().fox_attn_bwd_fixed_gate(_DT[dt], _ptr(q), _ptr(k), _ptr(v), _ptr(gate_bias),
-                                        _ptr(o), _ptr(lse), _ptr(d_o), _ptr(dq), _ptr(dk),
-                                        _ptr(dv), _ptr(d_gate_bias), _ptr(workspace),
-                                        workspace.numel() * workspace.element_size(),
-                                        B, H, L, d, s, _stream(q))
-    _raise(st, "fox_attn_bwd_fixed_gate")
+    st = getattr(load(), entry)(_DT[dt], _ptr(q), _ptr(k), _ptr(v), _ptr(gate_bias), _ptr(o),
+                                _ptr(lse), _ptr(d_o), _ptr(dq), _ptr(dk), _ptr(dv),
+                                _ptr(d_gate_bias), _ptr(workspace),
+                                workspace.numel() * workspace.element_size(), B, H, L, d, s,
+                                _stream(q))
+    _raise(st, entry)
     return dq, dk, dv, d_gate_bias
 
 
@@ -645,6 +675,21 @@ def fox_attn_bwd_skip(q, k, v, c, o, lse, d_o, q_norm_max, k_norm_max,
                       scale: Optional[float] = None, dq=None, dk=None, dv=None, d_log_f=None,
                       workspace=None):
     """fox_attn_bwd with exact gate-aware skipping of tile pairs (bitwise equal)."""
+    return _bwd_skip_call("fox_attn_bwd_skip", fox_attn_bwd_workspace_bytes, q, k, v, c, o, lse,
+                          d_o, q_norm_max, k_norm_max, scale, dq, dk, dv, d_log_f, workspace)
+
+
+def fox_attn_bwd_skip_stored(q, k, v, c, o, lse, d_o, q_norm_max, k_norm_max,
+                             scale: Optional[float] = None, dq=None, dk=None, dv=None,
+                             d_log_f=None, workspace=None):
+    """fox_attn_bwd_stored with exact gate-aware skipping (bitwise equal to it)."""
+    return _bwd_skip_call("fox_attn_bwd_skip_stored", fox_attn_bwd_stored_workspace_bytes, q, k,
+                          v, c, o, lse, d_o, q_norm_max, k_norm_max, scale, dq, dk, dv, d_log_f,
+                          workspace)
+
+
+def _bwd_skip_call(entry, ws_bytes, q, k, v, c, o, lse, d_o, q_norm_max, k_norm_max, scale, dq,
+                   dk, dv, d_log_f, workspace):
     B, H, L, d = q.shape
     dt = q.dtype
     if dt not in _DT:
@@ -663,16 +708,16 @@ def fox_attn_bwd_skip(q, k, v, c, o, lse, d_o, q_norm_max, k_norm_max,
     for name, t in (("dq", dq), ("dk", dk), ("dv", dv)):
         _check(t, name, (B, H, L, d), dt, dev)
     _check(d_log_f, "d_log_f", (B, H, L), torch.float32, dev)
-    need = fox_attn_bwd_workspace_bytes(dt, B, H, L, d)
+    need = ws_bytes(dt, B, H, L, d)
     if workspace is None:
         workspace = torch.empty(max(need, 16), device=dev, dtype=torch.uint8)
     s = default_scale(d) if scale is None else float(scale)
-    st = load().fox_attn_bwd_skip(_DT[dt], _ptr(q), _ptr(k), _ptr(v), _ptr(c), _ptr(o), _ptr(lse),
-                                  _ptr(d_o), _ptr(q_norm_max), _ptr(k_norm_max), _ptr(dq),
-                                  _ptr(dk), _ptr(dv), _ptr(d_log_f), _ptr(workspace),
-                                  workspace.numel() * workspace.element_size(),
-                                  B, H, L, d, s, _stream(q))
-    _raise(st, "fox_attn_bwd_skip")
+    st = getattr(load(), entry)(_DT[dt], _ptr(q), _ptr(k), _ptr(v), _ptr(c), _ptr(o), _ptr(lse),
+                                _ptr(d_o), _ptr(q_norm_max), _ptr(k_norm_max), _ptr(dq),
+                                _ptr(dk), _ptr(dv), _ptr(d_log_f), _ptr(workspace),
+                                workspace.numel() * workspace.element_size(),
+                                B, H, L, d, s, _stream(q))
+    _raise(st, entry)
     return dq, dk, dv, d_log_f
 
 
@@ -706,6 +751,24 @@ def fox_attn_bwd_fixed_gate_skip(q, k, v, gate_bias, o, lse, d_o, q_norm_max, k_
                                  scale: Optional[float] = None, want_bias_grad=True,
                                  workspace=None):
     """fox_attn_bwd_fixed_gate with exact gate-aware skipping: dq, dk, dv, d gate_bias."""
+    return _bwd_fixed_skip_call("fox_attn_bwd_fixed_gate_skip",
+                                fox_attn_bwd_fixed_gate_workspace_bytes, q, k, v, gate_bias, o,
+                                lse, d_o, q_norm_max, k_norm_max, scale, want_bias_grad,
+                                workspace)
+
+
+def fox_attn_bwd_fixed_gate_skip_stored(q, k, v, gate_bias, o, lse, d_o, q_norm_max, k_norm_max,
+                                        scale: Optional[float] = None, want_bias_grad=True,
+                                        workspace=None):
+    """fox_attn_bwd_fixed_gate_stored with exact gate-aware skipping (bitwise equal to it)."""
+    return _bwd_fixed_skip_call("fox_attn_bwd_fixed_gate_skip_stored",
+                                fox_attn_bwd_fixed_gate_stored_workspace_bytes, q, k, v,
+                                gate_bias, o, lse, d_o, q_norm_max, k_norm_max, scale,
+                                want_bias_grad, workspace)
+
+
+def _bwd_fixed_skip_call(entry, ws_bytes, q, k, v, gate_bias, o, lse, d_o, q_norm_max,
+                         k_norm_max, scale, want_bias_grad, workspace):
     B, H, L, d = q.shape
     dt = q.dtype
     if dt not in _DT:
@@ -719,17 +782,16 @@ def fox_attn_bwd_fixed_gate_skip(q, k, v, gate_bias, o, lse, d_o, q_norm_max, k_
     _check(k_norm_max, "k_norm_max", (B, H), torch.float32, dev)
     dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
     db = torch.empty_like(gate_bias) if want_bias_grad else None
-    need = fox_attn_bwd_fixed_gate_workspace_bytes(dt, B, H, L, d)
+    need = ws_bytes(dt, B, H, L, d)
     if workspace is None:
         workspace = torch.empty(max(need, 16), device=dev, dtype=torch.uint8)
     s = default_scale(d) if scale is None else float(scale)
-    st = load().fox_attn_bwd_fixed_gate_skip(_DT[dt], _ptr(q), _ptr(k), _ptr(v), _ptr(gate_bias),
-                                             _ptr(o), _ptr(lse), _ptr(d_o), _ptr(q_norm_max),
-                                             _ptr(k_norm_max), _ptr(dq), _ptr(dk), _ptr(dv),
-                                             _ptr(db), _ptr(workspace),
-                                             workspace.numel() * workspace.element_size(),
-                                             B, H, L, d, s, _stream(q))
-    _raise(st, "fox_attn_bwd_fixed_gate_skip")
+    st = getattr(load(), entry)(_DT[dt], _ptr(q), _ptr(k), _ptr(v), _ptr(gate_bias), _ptr(o),
+                                _ptr(lse), _ptr(d_o), _ptr(q_norm_max), _ptr(k_norm_max),
+                                _ptr(dq), _ptr(dk), _ptr(dv), _ptr(db), _ptr(workspace),
+                                workspace.numel() * workspace.element_size(), B, H, L, d, s,
+                                _stream(q))
+    _raise(st, entry)
     return dq, dk, dv, db
 
 

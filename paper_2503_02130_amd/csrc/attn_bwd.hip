@@ -391,9 +391,8 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
     const float* __restrict__ gate, const float* __restrict__ qnorm,
     const float* __restrict__ knorm, const float* __restrict__ LSE, const bf16* __restrict__ dO,
     const float* __restrict__ delta, bf16* __restrict__ dK, bf16* __restrict__ dV,
-    float* __restrict__ dck, bf16x8* __restrict__ ds_store, int BH, int H, int L, float scale,
-    float scale_log2) {
-  static_assert(!(STORE && SKIP), "the stored-dS backward runs dense");
+    float* __restrict__ dck, bf16x8* __restrict__ ds_store, int* __restrict__ ds_tiles, int BH,
+    int H, int L, float scale, float scale_log2) {
   static_assert(!STORE || (kv_bm<D>() == 64 && kKvBN == 128 && kKvPairs == 4),
                 "the stored-dS slot layout");
   constexpr int kKvBM = kv_bm<D>();
@@ -695,6 +694,9 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
     const float dck_tot = wave_sum_pair(dck_part);
     if (k_valid && h == 0) dck[head + kj] = -dck_tot;
   }
+  // the number of query tiles whose dS this block stored (the rest are zeros)
+  if constexpr (STORE && SKIP)
+    if (tid == 0) ds_tiles[(size_t)bh * ds_key_blocks(L) + nblk] = n_tiles;
 }
 
 // ---------------------------------------------------------------------------
@@ -729,10 +731,11 @@ struct DsSmem {
   bf16x8 ds[2][kDsTiles][kDsStageLds / 16];
 };
 
-template <int D>
+template <int D, bool SKIP>
 __global__ __launch_bounds__(kDsThreads) void bwd_dq_stored_kernel(
-    const bf16* __restrict__ K, const bf16x8* __restrict__ ds_store, bf16* __restrict__ dQ,
-    float* __restrict__ dcq, int BH, int L, int n_mblk, float scale) {
+    const bf16* __restrict__ K, const bf16x8* __restrict__ ds_store,
+    const int* __restrict__ ds_tiles, bf16* __restrict__ dQ, float* __restrict__ dcq, int BH,
+    int L, int n_mblk, float scale) {
   constexpr int TILE = kDsBN * D;
   constexpr int NDMA = TILE * 2 / 1024 / kDsWaves;
   static_assert(NDMA >= 1, "every wave issues at least one K DMA load per stage");
@@ -741,8 +744,10 @@ __global__ __launch_bounds__(kDsThreads) void bwd_dq_stored_kernel(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = lane >> 5, col = lane & 31;
   const int row = (int)(blockIdx.x / BH);
-  const int bh = (int)(blockIdx.x % BH);  // heads fastest
-  const int mblk = n_mblk - 1 - row;      // the longest rows first
+  // heads fastest; rotated over the XCDs when skipping, whose work per head
+  // depends on its gates (see the forward kernel)
+  const int bh = SKIP ? (int)((blockIdx.x + row) % BH) : (int)(blockIdx.x % BH);
+  const int mblk = n_mblk - 1 - row;  // the longest rows first
   const int q0 = mblk * kDsBM;
   const int qt0 = q0 / 64;
   const int my_t = wave >> 1, qb = wave & 1;  // this wave's tile and half
@@ -781,6 +786,22 @@ __global__ __launch_bounds__(kDsThreads) void bwd_dq_stored_kernel(
   float dcq_part = 0.0f;
 
   const int n_st = (min(L, q0 + kDsBM) + kDsBN - 1) / kDsBN;
+  // SKIP: key block nb stored the query tiles below cut(nb) = 2 nb + its tile
+  // count, the others being exact zeros; cut never decreases with nb (c never
+  // increases), so the blocks this workgroup needs start at the first nb with
+  // cut(nb) > qt0 (a binary search; block qt0 / 2 holds the diagonal, stored).
+  const int* tiles_row = ds_tiles + (size_t)bh * ds_key_blocks(L);
+  auto cut = [&](int nb) { return SKIP ? 2 * nb + tiles_row[nb] : n_qt; };
+  int j_first = 0;
+  if constexpr (SKIP) {
+    int lo = 0, hi = qt0 / 2;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (cut(mid) > qt0) hi = mid;
+      else lo = mid + 1;
+    }
+    j_first = 2 * lo;
+  }
   auto issue = [&](int j, auto bufc) {
     constexpr int B = decltype(bufc)::value;
     const uint32_t base = (uint32_t)j * TILE * 2;
@@ -790,7 +811,7 @@ __global__ __launch_bounds__(kDsThreads) void bwd_dq_stored_kernel(
             dma_off + uniform_u32(base + i * tile_dma_stride<kDsWaves>()));
     // the tiles on or below the diagonal of stage j: slots of key block j / 2
     const int nb = j >> 1;
-    const int t_lo = max(0, j - qt0), t_hi = min(kDsTiles, n_qt - qt0);
+    const int t_lo = max(0, j - qt0), t_hi = min(min(kDsTiles, n_qt - qt0), cut(nb) - qt0);
     if (t_lo < t_hi) {
       const __amdgpu_buffer_rsrc_t rs = make_rsrc(
           ds_store + (head_slot + ds_slot(L, nb, qt0 + t_lo)) * (kDsSlotBytes / 16),
@@ -824,17 +845,20 @@ __global__ __launch_bounds__(kDsThreads) void bwd_dq_stored_kernel(
     });
   };
 
-  issue(0, std::integral_constant<int, 0>());
-  for (int j = 0; j < n_st; j += 2) {
+  // tile qt takes part in stage j when it lies on or below the diagonal and
+  // (skipping) its dS for the stage's block was stored
+  auto active = [&](int j) { return qt >= j && qt < n_qt && (!SKIP || qt < cut(j >> 1)); };
+  if (j_first < n_st) issue(j_first, std::integral_constant<int, 0>());
+  for (int j = j_first; j < n_st; j += 2) {
     wait_all_memory();
     __syncthreads();  // stage j is in LDS; every wave is done with stage j - 1
     if (j + 1 < n_st) issue(j + 1, std::integral_constant<int, 1>());
-    if (qt >= j && qt < n_qt) body(std::integral_constant<int, 0>());
+    if (active(j)) body(std::integral_constant<int, 0>());
     if (j + 1 < n_st) {
       wait_all_memory();
       __syncthreads();
       if (j + 2 < n_st) issue(j + 2, std::integral_constant<int, 0>());
-      if (qt >= j + 1 && qt < n_qt) body(std::integral_constant<int, 1>());
+      if (active(j + 1)) body(std::integral_constant<int, 1>());
     }
   }
 
@@ -1042,12 +1066,12 @@ static void dkdv_t(bool bf16_, const void* q, const void* k, const void* v, Gate
     if (qn)
       hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, FIXED, true>), grid, dim3(kKvThreads), 0, s,
                          (const bf16*)q, (const bf16*)k, (const bf16*)v, g.ptr, qn, kn, lse,
-                         (const bf16*)d_o, delta, (bf16*)dk, (bf16*)dv, dck, nullptr, BH, g.H, L, scale,
+                         (const bf16*)d_o, delta, (bf16*)dk, (bf16*)dv, dck, nullptr, nullptr, BH, g.H, L, scale,
                          sl2);
     else
     hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, FIXED, false>), grid, dim3(kKvThreads), 0, s,
                        (const bf16*)q, (const bf16*)k, (const bf16*)v, g.ptr, qn, kn, lse,
-                       (const bf16*)d_o, delta, (bf16*)dk, (bf16*)dv, dck, nullptr, BH, g.H, L, scale,
+                       (const bf16*)d_o, delta, (bf16*)dk, (bf16*)dv, dck, nullptr, nullptr, BH, g.H, L, scale,
                        sl2);
   } else {
     const int rpw = kF32Threads / (D / 32);
@@ -1154,56 +1178,116 @@ size_t ds_store_bytes(int BH, int L) {
   return (size_t)BH * ds_slots_per_head(L) * (size_t)kDsSlotBytes;
 }
 
-size_t bwd_stored_workspace_bytes(int BH, int L) {
-  return align256(bwd_workspace_bytes(BH, L)) + ds_store_bytes(BH, L);
+// the stored dS, then (skipping) the stored tile count of each key block
+static size_t stored_tail_bytes(int BH, int L) {
+  return ds_store_bytes(BH, L) + (size_t)BH * ds_key_blocks(L) * sizeof(int);
 }
 
-hipError_t launch_bwd_dkdv_store(const void* q, const void* k, const void* v, const float* c,
-                                 const float* lse, const void* d_o, const float* delta, void* dk,
-                                 void* dv, float* dck, void* ds_store, int BH, int L, int d,
-                                 float scale, hipStream_t s) {
+size_t bwd_stored_workspace_bytes(int BH, int L) {
+  return align256(bwd_workspace_bytes(BH, L)) + stored_tail_bytes(BH, L);
+}
+
+template <int D, bool FIXED, bool SKIP>
+static void dkdv_store_t(const void* q, const void* k, const void* v, GateSpec g,
+                         const float* lse, const void* d_o, const float* delta, void* dk,
+                         void* dv, float* dck, void* ds_store, int* ds_tiles, int BH, int L,
+                         float scale, hipStream_t s, const float* qn, const float* kn) {
   const dim3 grid((unsigned)((L + kKvBN - 1) / kKvBN) * (unsigned)BH);
+  hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, FIXED, SKIP, true>), grid, dim3(kKvThreads), 0, s,
+                     (const bf16*)q, (const bf16*)k, (const bf16*)v, g.ptr, qn, kn, lse,
+                     (const bf16*)d_o, delta, (bf16*)dk, (bf16*)dv, dck, (bf16x8*)ds_store,
+                     ds_tiles, BH, g.H, L, scale, scale * kLog2e);
+}
+
+template <int D>
+static void dkdv_store_d(const void* q, const void* k, const void* v, GateSpec g,
+                         const float* lse, const void* d_o, const float* delta, void* dk,
+                         void* dv, float* dck, void* ds_store, int* ds_tiles, int BH, int L,
+                         float scale, hipStream_t s, const float* qn, const float* kn) {
+  if (g.fixed) {
+    if (qn)
+      dkdv_store_t<D, true, true>(q, k, v, g, lse, d_o, delta, dk, dv, dck, ds_store, ds_tiles,
+                                  BH, L, scale, s, qn, kn);
+    else
+      dkdv_store_t<D, true, false>(q, k, v, g, lse, d_o, delta, dk, dv, dck, ds_store, ds_tiles,
+                                   BH, L, scale, s, qn, kn);
+  } else {
+    if (qn)
+      dkdv_store_t<D, false, true>(q, k, v, g, lse, d_o, delta, dk, dv, dck, ds_store, ds_tiles,
+                                   BH, L, scale, s, qn, kn);
+    else
+      dkdv_store_t<D, false, false>(q, k, v, g, lse, d_o, delta, dk, dv, dck, ds_store, ds_tiles,
+                                    BH, L, scale, s, qn, kn);
+  }
+}
+
+hipError_t launch_bwd_dkdv_store(const void* q, const void* k, const void* v, GateSpec g,
+                                 const float* lse, const void* d_o, const float* delta, void* dk,
+                                 void* dv, float* dck, void* ds_store, int* ds_tiles, int BH,
+                                 int L, int d, float scale, hipStream_t s, const float* qn,
+                                 const float* kn) {
   if (d == 128)
-    hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<128, false, false, true>), grid, dim3(kKvThreads), 0,
-                       s, (const bf16*)q, (const bf16*)k, (const bf16*)v, c, nullptr, nullptr,
-                       lse, (const bf16*)d_o, delta, (bf16*)dk, (bf16*)dv, dck,
-                       (bf16x8*)ds_store, BH, 1, L, scale, scale * kLog2e);
+    dkdv_store_d<128>(q, k, v, g, lse, d_o, delta, dk, dv, dck, ds_store, ds_tiles, BH, L, scale,
+                      s, qn, kn);
   else
-    hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<64, false, false, true>), grid, dim3(kKvThreads), 0,
-                       s, (const bf16*)q, (const bf16*)k, (const bf16*)v, c, nullptr, nullptr,
-                       lse, (const bf16*)d_o, delta, (bf16*)dk, (bf16*)dv, dck,
-                       (bf16x8*)ds_store, BH, 1, L, scale, scale * kLog2e);
+    dkdv_store_d<64>(q, k, v, g, lse, d_o, delta, dk, dv, dck, ds_store, ds_tiles, BH, L, scale,
+                     s, qn, kn);
   return hipGetLastError();
 }
 
-hipError_t launch_bwd_dq_stored(const void* k, const void* ds_store, void* dq, float* dcq,
-                                int BH, int L, int d, float scale, hipStream_t s) {
+template <int D, bool SKIP>
+static void dq_stored_t(const void* k, const void* ds_store, const int* ds_tiles, void* dq,
+                        float* dcq, int BH, int L, float scale, hipStream_t s) {
   const int n_mblk = (L + kDsBM - 1) / kDsBM;
   const dim3 grid((unsigned)n_mblk * (unsigned)BH);
-  if (d == 128)
-    hipLaunchKernelGGL((bwd_dq_stored_kernel<128>), grid, dim3(kDsThreads), 0, s,
-                       (const bf16*)k, (const bf16x8*)ds_store, (bf16*)dq, dcq, BH, L, n_mblk,
-                       scale);
-  else
-    hipLaunchKernelGGL((bwd_dq_stored_kernel<64>), grid, dim3(kDsThreads), 0, s, (const bf16*)k,
-                       (const bf16x8*)ds_store, (bf16*)dq, dcq, BH, L, n_mblk, scale);
+  hipLaunchKernelGGL((bwd_dq_stored_kernel<D, SKIP>), grid, dim3(kDsThreads), 0, s,
+                     (const bf16*)k, (const bf16x8*)ds_store, ds_tiles, (bf16*)dq, dcq, BH, L,
+                     n_mblk, scale);
+}
+
+hipError_t launch_bwd_dq_stored(const void* k, const void* ds_store, const int* ds_tiles,
+                                void* dq, float* dcq, int BH, int L, int d, float scale,
+                                hipStream_t s) {
+  if (d == 128) {
+    if (ds_tiles) dq_stored_t<128, true>(k, ds_store, ds_tiles, dq, dcq, BH, L, scale, s);
+    else dq_stored_t<128, false>(k, ds_store, ds_tiles, dq, dcq, BH, L, scale, s);
+  } else {
+    if (ds_tiles) dq_stored_t<64, true>(k, ds_store, ds_tiles, dq, dcq, BH, L, scale, s);
+    else dq_stored_t<64, false>(k, ds_store, ds_tiles, dq, dcq, BH, L, scale, s);
+  }
   return hipGetLastError();
+}
+
+// delta -> dK/dV storing dS -> dQ from it -> d(log f), with delta, dc_q, dc_k at
+// the start of ws and the stored dS (and tile counts) at `tail`
+static hipError_t launch_bwd_stored_stages(const void* q, const void* k, const void* v,
+                                           GateSpec g, const void* o, const float* lse,
+                                           const void* d_o, void* dq, void* dk, void* dv,
+                                           float* d_log_f, float* ws, char* tail, int BH, int L,
+                                           int d, float scale, hipStream_t s, const float* qn,
+                                           const float* kn) {
+  float* delta = ws;
+  float* dcq = delta + (size_t)BH * L;
+  float* dck = dcq + (size_t)BH * L;
+  void* dss = tail;
+  int* tiles = qn ? reinterpret_cast<int*>(tail + ds_store_bytes(BH, L)) : nullptr;
+  hipError_t e = launch_bwd_delta(true, o, d_o, delta, BH, L, d, s);
+  if (e == hipSuccess)
+    e = launch_bwd_dkdv_store(q, k, v, g, lse, d_o, delta, dk, dv, dck, dss, tiles, BH, L, d,
+                              scale, s, qn, kn);
+  if (e == hipSuccess) e = launch_bwd_dq_stored(k, dss, tiles, dq, dcq, BH, L, d, scale, s);
+  if (e == hipSuccess) e = launch_reverse_scan_sum(dcq, dck, d_log_f, BH, L, s);
+  return e;
 }
 
 hipError_t launch_bwd_stored(const void* q, const void* k, const void* v, const float* c,
                              const void* o, const float* lse, const void* d_o, void* dq, void* dk,
                              void* dv, float* d_log_f, void* ws, int BH, int L, int d, float scale,
-                             hipStream_t s) {
-  float* delta = static_cast<float*>(ws);
-  float* dcq = delta + (size_t)BH * L;
-  float* dck = dcq + (size_t)BH * L;
-  void* dss = static_cast<char*>(ws) + align256(bwd_workspace_bytes(BH, L));
-  hipError_t e = launch_bwd_delta(true, o, d_o, delta, BH, L, d, s);
-  if (e == hipSuccess)
-    e = launch_bwd_dkdv_store(q, k, v, c, lse, d_o, delta, dk, dv, dck, dss, BH, L, d, scale, s);
-  if (e == hipSuccess) e = launch_bwd_dq_stored(k, dss, dq, dcq, BH, L, d, scale, s);
-  if (e == hipSuccess) e = launch_reverse_scan_sum(dcq, dck, d_log_f, BH, L, s);
-  return e;
+                             hipStream_t s, const float* q_norm_max, const float* k_norm_max) {
+  return launch_bwd_stored_stages(q, k, v, gate_array(c), o, lse, d_o, dq, dk, dv, d_log_f,
+                                  static_cast<float*>(ws),
+                                  static_cast<char*>(ws) + align256(bwd_workspace_bytes(BH, L)),
+                                  BH, L, d, scale, s, q_norm_max, k_norm_max);
 }
 
 // d b^(h) = sigmoid(-b^(h)) * sum over the rows of head h and all t of d(log f):
@@ -1240,6 +1324,29 @@ hipError_t launch_bwd_fixed(bool bf16_, const void* q, const void* k, const void
   float* dlf = w + 3 * (size_t)BH * L;
   hipError_t e = launch_bwd_stages(bf16_, q, k, v, gate_fixed(bias, H), o, lse, d_o, dq, dk, dv,
                                    dlf, w, BH, L, d, scale, s, q_norm_max, k_norm_max);
+  if (e == hipSuccess && d_bias) {
+    hipLaunchKernelGGL(fixed_bias_grad_kernel, dim3(H), dim3(kBiasThreads), 0, s, dlf, bias,
+                       d_bias, BH / H, H, L);
+    e = hipGetLastError();
+  }
+  return e;
+}
+
+size_t bwd_fixed_stored_workspace_bytes(int BH, int L) {
+  return align256(bwd_fixed_workspace_bytes(BH, L)) + stored_tail_bytes(BH, L);
+}
+
+hipError_t launch_bwd_fixed_stored(const void* q, const void* k, const void* v,
+                                   const float* bias, int H, const void* o, const float* lse,
+                                   const void* d_o, void* dq, void* dk, void* dv, float* d_bias,
+                                   void* ws, int BH, int L, int d, float scale, hipStream_t s,
+                                   const float* q_norm_max, const float* k_norm_max) {
+  float* w = static_cast<float*>(ws);
+  float* dlf = w + 3 * (size_t)BH * L;
+  hipError_t e = launch_bwd_stored_stages(
+      q, k, v, gate_fixed(bias, H), o, lse, d_o, dq, dk, dv, dlf, w,
+      static_cast<char*>(ws) + align256(bwd_fixed_workspace_bytes(BH, L)), BH, L, d, scale, s,
+      q_norm_max, k_norm_max);
   if (e == hipSuccess && d_bias) {
     hipLaunchKernelGGL(fixed_bias_grad_kernel, dim3(H), dim3(kBiasThreads), 0, s, dlf, bias,
                        d_bias, BH / H, H, L);

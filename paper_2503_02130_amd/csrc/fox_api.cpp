@@ -219,9 +219,9 @@ int fox_attn_bwd_dkdv_store(int dtype, const void* q, const void* k, const void*
     return FOX_ERR_ALIGN;
   if (!ds_store || ds_store_bytes < fox::ds_store_bytes(B * H, L)) return FOX_ERR_WORKSPACE;
   if (!aligned16(ds_store)) return FOX_ERR_ALIGN;
-  return launch_status(fox::launch_bwd_dkdv_store(q, k, v, c, lse, d_o, delta, dk, dv, dc_k,
-                                                  ds_store, B * H, L, d, scale,
-                                                  static_cast<hipStream_t>(stream)));
+  return launch_status(fox::launch_bwd_dkdv_store(q, k, v, fox::gate_array(c), lse, d_o, delta,
+                                                  dk, dv, dc_k, ds_store, nullptr, B * H, L, d,
+                                                  scale, static_cast<hipStream_t>(stream)));
 }
 
 int fox_attn_bwd_dq_stored(int dtype, const void* k, const void* ds_store, size_t ds_store_bytes,
@@ -236,8 +236,8 @@ int fox_attn_bwd_dq_stored(int dtype, const void* k, const void* ds_store, size_
   if (!aligned16(k) || !aligned16(dq) || !aligned16(dc_q)) return FOX_ERR_ALIGN;
   if (!ds_store || ds_store_bytes < fox::ds_store_bytes(B * H, L)) return FOX_ERR_WORKSPACE;
   if (!aligned16(ds_store)) return FOX_ERR_ALIGN;
-  return launch_status(fox::launch_bwd_dq_stored(k, ds_store, dq, dc_q, B * H, L, d, scale,
-                                                 static_cast<hipStream_t>(stream)));
+  return launch_status(fox::launch_bwd_dq_stored(k, ds_store, nullptr, dq, dc_q, B * H, L, d,
+                                                 scale, static_cast<hipStream_t>(stream)));
 }
 
 int fox_dlogf_from_dc(const float* dc_q, const float* dc_k, float* d_log_f, int B, int H, int L,
@@ -346,6 +346,29 @@ int fox_attn_bwd_skip(int dtype, const void* q, const void* k, const void* v, co
                                        bf ? k_norm_max : nullptr));
 }
 
+int fox_attn_bwd_skip_stored(int dtype, const void* q, const void* k, const void* v,
+                             const float* c, const void* o, const float* lse, const void* d_o,
+                             const float* q_norm_max, const float* k_norm_max, void* dq, void* dk,
+                             void* dv, float* d_log_f, void* workspace, size_t workspace_bytes,
+                             int B, int H, int L, int d, float scale, void* stream) {
+  if (!all_set({q, k, v, c, o, lse, d_o, q_norm_max, k_norm_max, dq, dk, dv, d_log_f}))
+    return FOX_ERR_NULL;
+  int st = check_dims(B, H, L, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (dtype != FOX_DTYPE_BF16) return FOX_ERR_UNSUPPORTED;
+  if (!all_aligned16({q, k, v, c, o, lse, d_o, q_norm_max, k_norm_max, dq, dk, dv, d_log_f}))
+    return FOX_ERR_ALIGN;
+  if (!workspace || workspace_bytes < fox::bwd_stored_workspace_bytes(B * H, L))
+    return FOX_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return FOX_ERR_ALIGN;
+  return launch_status(fox::launch_bwd_stored(q, k, v, c, o, lse, d_o, dq, dk, dv, d_log_f,
+                                              workspace, B * H, L, d, scale,
+                                              static_cast<hipStream_t>(stream), q_norm_max,
+                                              k_norm_max));
+}
+
 int fox_attn_decode_skip(int dtype, const void* q, const void* k_cache, const void* v_cache,
                          float* c_cache, const float* gate_logit_new, const float* k_norm_max,
                          void* o, float* lse, void* workspace, size_t workspace_bytes, int B,
@@ -426,6 +449,59 @@ int fox_attn_bwd_fixed_gate(int dtype, const void* q, const void* k, const void*
   return launch_status(fox::launch_bwd_fixed(dtype == FOX_DTYPE_BF16, q, k, v, gate_bias, H, o,
                                              lse, d_o, dq, dk, dv, d_gate_bias, workspace, B * H,
                                              L, d, scale, static_cast<hipStream_t>(stream)));
+}
+
+size_t fox_attn_bwd_fixed_gate_stored_workspace_bytes(int dtype, int B, int H, int L, int d) {
+  if (check_dims(B, H, L, d) || check_dtype_d(dtype, d) || dtype != FOX_DTYPE_BF16) return 0;
+  return fox::bwd_fixed_stored_workspace_bytes(B * H, L);
+}
+
+// fox_attn_bwd_fixed_gate_stored and its skipping twin (norms non-NULL)
+static int bwd_fixed_stored(int dtype, const void* q, const void* k, const void* v,
+                            const float* gate_bias, const void* o, const float* lse,
+                            const void* d_o, const float* q_norm_max, const float* k_norm_max,
+                            void* dq, void* dk, void* dv, float* d_gate_bias, void* workspace,
+                            size_t workspace_bytes, int B, int H, int L, int d, float scale,
+                            void* stream) {
+  int st = check_dims(B, H, L, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (dtype != FOX_DTYPE_BF16) return FOX_ERR_UNSUPPORTED;
+  if (!all_aligned16({q, k, v, gate_bias, o, lse, d_o, dq, dk, dv}) ||
+      (q_norm_max && !all_aligned16({q_norm_max, k_norm_max})) ||
+      (d_gate_bias && !aligned16(d_gate_bias)))
+    return FOX_ERR_ALIGN;
+  if (!workspace || workspace_bytes < fox::bwd_fixed_stored_workspace_bytes(B * H, L))
+    return FOX_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return FOX_ERR_ALIGN;
+  return launch_status(fox::launch_bwd_fixed_stored(q, k, v, gate_bias, H, o, lse, d_o, dq, dk,
+                                                    dv, d_gate_bias, workspace, B * H, L, d,
+                                                    scale, static_cast<hipStream_t>(stream),
+                                                    q_norm_max, k_norm_max));
+}
+
+int fox_attn_bwd_fixed_gate_stored(int dtype, const void* q, const void* k, const void* v,
+                                   const float* gate_bias, const void* o, const float* lse,
+                                   const void* d_o, void* dq, void* dk, void* dv,
+                                   float* d_gate_bias, void* workspace, size_t workspace_bytes,
+                                   int B, int H, int L, int d, float scale, void* stream) {
+  if (!all_set({q, k, v, gate_bias, o, lse, d_o, dq, dk, dv})) return FOX_ERR_NULL;
+  return bwd_fixed_stored(dtype, q, k, v, gate_bias, o, lse, d_o, nullptr, nullptr, dq, dk, dv,
+                          d_gate_bias, workspace, workspace_bytes, B, H, L, d, scale, stream);
+}
+
+int fox_attn_bwd_fixed_gate_skip_stored(int dtype, const void* q, const void* k, const void* v,
+                                        const float* gate_bias, const void* o, const float* lse,
+                                        const void* d_o, const float* q_norm_max,
+                                        const float* k_norm_max, void* dq, void* dk, void* dv,
+                                        float* d_gate_bias, void* workspace,
+                                        size_t workspace_bytes, int B, int H, int L, int d,
+                                        float scale, void* stream) {
+  if (!all_set({q, k, v, gate_bias, o, lse, d_o, q_norm_max, k_norm_max, dq, dk, dv}))
+    return FOX_ERR_NULL;
+  return bwd_fixed_stored(dtype, q, k, v, gate_bias, o, lse, d_o, q_norm_max, k_norm_max, dq, dk,
+                          dv, d_gate_bias, workspace, workspace_bytes, B, H, L, d, scale, stream);
 }
 
 int fox_attn_decode_fixed_gate(int dtype, const void* q, const void* k_cache,

@@ -57,18 +57,33 @@ hipError_t launch_bwd(bool bf16, const void* q, const void* k, const void* v, co
 // bytes, then the stored dS, 16 KB per (128-key block, 64-query tile) pair of
 // the causal order and head.  The dK/dV pass writes it, the dQ pass reads it
 // instead of recomputing S and dP.
+// With skipping (q_norm_max / k_norm_max given) the dK/dV pass also records,
+// after the stored dS, how many query tiles each key block stored, and the dQ
+// pass reads only those.
 size_t bwd_stored_workspace_bytes(int BH, int L);
 size_t ds_store_bytes(int BH, int L);  // the stored dS alone
-hipError_t launch_bwd_dkdv_store(const void* q, const void* k, const void* v, const float* c,
+hipError_t launch_bwd_dkdv_store(const void* q, const void* k, const void* v, GateSpec g,
                                  const float* lse, const void* d_o, const float* delta, void* dk,
-                                 void* dv, float* dck, void* ds_store, int BH, int L, int d,
-                                 float scale, hipStream_t s);
-hipError_t launch_bwd_dq_stored(const void* k, const void* ds_store, void* dq, float* dcq,
-                                int BH, int L, int d, float scale, hipStream_t s);
+                                 void* dv, float* dck, void* ds_store, int* ds_tiles, int BH,
+                                 int L, int d, float scale, hipStream_t s,
+                                 const float* q_norm_max = nullptr,
+                                 const float* k_norm_max = nullptr);
+hipError_t launch_bwd_dq_stored(const void* k, const void* ds_store, const int* ds_tiles,
+                                void* dq, float* dcq, int BH, int L, int d, float scale,
+                                hipStream_t s);
 hipError_t launch_bwd_stored(const void* q, const void* k, const void* v, const float* c,
                              const void* o, const float* lse, const void* d_o, void* dq, void* dk,
                              void* dv, float* d_log_f, void* ws, int BH, int L, int d, float scale,
-                             hipStream_t s);
+                             hipStream_t s, const float* q_norm_max = nullptr,
+                             const float* k_norm_max = nullptr);
+// Fixed gates keeping dS: the fixed-gate workspace, aligned, then the stored tail.
+size_t bwd_fixed_stored_workspace_bytes(int BH, int L);
+hipError_t launch_bwd_fixed_stored(const void* q, const void* k, const void* v,
+                                   const float* bias, int H, const void* o, const float* lse,
+                                   const void* d_o, void* dq, void* dk, void* dv, float* d_bias,
+                                   void* ws, int BH, int L, int d, float scale, hipStream_t s,
+                                   const float* q_norm_max = nullptr,
+                                   const float* k_norm_max = nullptr);
 // Fixed gates: workspace delta, dc_q, dc_k, d(log f), each [BH, L] fp32; the bias
 // gradient d_bias [H] (may be NULL) = sigmoid(-b) * sum over rows and t of d(log f).
 size_t bwd_fixed_workspace_bytes(int BH, int L);

@@ -552,8 +552,9 @@ hipError_t launch_bwd_pro(bool bf16_, const void* q, const void* k, const void* 
   if (keep_ds) {
     void* dss = w + align256(bwd_pro_workspace_bytes(true, BH, L, d));
     if (e == hipSuccess)
-      e = launch_bwd_dkdv_store(q, k, v, c, lse, d_o, delta, dk, dv, dck, dss, BH, L, d, scale, s);
-    if (e == hipSuccess) e = launch_bwd_dq_stored(k, dss, dq, dcq, BH, L, d, scale, s);
+      e = launch_bwd_dkdv_store(q, k, v, gs, lse, d_o, delta, dk, dv, dck, dss, nullptr, BH, L, d,
+                                scale, s);
+    if (e == hipSuccess) e = launch_bwd_dq_stored(k, dss, nullptr, dq, dcq, BH, L, d, scale, s);
   } else {
     if (e == hipSuccess)
       e = launch_bwd_dkdv(bf16_, q, k, v, gs, lse, d_o, delta, dk, dv, dck, BH, L, d, scale, s);

@@ -215,7 +215,7 @@ def test_bwd_validation_and_workspace(lib):
 def test_bwd_stored_validation_and_workspace(lib):
     """The backward that keeps dS: workspace = the recompute path's, aligned to
     256 bytes, plus 16 KB per causal (128-key block, 64-query tile) pair and
-    head; bf16 only."""
+    head, plus a tile count per (head, key block); bf16 only."""
     c = ctypes.c_void_p
     f = ctypes.c_float(0.1)
     base = lambda x: (x + 255) // 256 * 256
@@ -224,10 +224,14 @@ def test_bwd_stored_validation_and_workspace(lib):
         nq, nk = -(-L // 64), -(-L // 128)
         pairs = sum(1 for nb in range(nk) for qt in range(nq) if qt >= 2 * nb)
         for d in (64, 128):
+            tail = B * H * pairs * 16384 + B * H * nk * 4
             assert lib.fox_attn_bwd_stored_workspace_bytes(1, B, H, L, d) == \
-                base(3 * 4 * B * H * L) + B * H * pairs * 16384, (B, H, L, d)
+                base(3 * 4 * B * H * L) + tail, (B, H, L, d)
+            assert lib.fox_attn_bwd_fixed_gate_stored_workspace_bytes(1, B, H, L, d) == \
+                base(4 * 4 * B * H * L) + tail, (B, H, L, d)
+            assert lib.fox_attn_bwd_ds_store_bytes(1, B, H, L, d) == B * H * pairs * 16384
     assert lib.fox_attn_bwd_stored_workspace_bytes(1, 2, 16, 16384, 128) == \
-        base(12 * 32 * 16384) + 32 * 16512 * 16384  # 8.66 GB at the long-context shape
+        base(12 * 32 * 16384) + 32 * 16512 * 16384 + 32 * 128 * 4  # 8.66 GB at 16k
     B, H, L, d = 2, 3, 100, 128
     assert lib.fox_attn_bwd_stored_workspace_bytes(0, B, H, L, d) == 0  # fp32
     assert lib.fox_attn_bwd_stored_workspace_bytes(1, B, H, L, 80) == 0
@@ -240,7 +244,7 @@ def test_bwd_stored_validation_and_workspace(lib):
     assert lib.fox_attn_bwd_stored(1, *args[:-1], None, c(P16), need, B, H, L, d, f, None) == 1
     assert lib.fox_attn_bwd_stored(1, *args, c(P16), need, B, H, 0, d, f, None) == 2
     store = lib.fox_attn_bwd_ds_store_bytes(1, B, H, L, d)
-    assert store == need - (3 * 4 * B * H * L + 255) // 256 * 256
+    assert store == need - base(3 * 4 * B * H * L) - B * H * 1 * 4
     assert lib.fox_attn_bwd_ds_store_bytes(0, B, H, L, d) == 0
     kv = [c(P16)] * 10
     assert lib.fox_attn_bwd_dkdv_store(1, *kv, c(P16), store - 1, B, H, L, d, f, None) == 5
@@ -257,6 +261,27 @@ def test_bwd_stored_validation_and_workspace(lib):
                                       None) == 3
     assert lib.fox_attn_bwd_dq_stored(1, c(P16), c(P16), store, None, c(P16), B, H, L, d, f,
                                       None) == 1
+    # skipping, fixed gates and both: the same checks
+    nm = [c(P16)] * 2
+    a7 = [c(P16)] * 7
+    g4 = [c(P16)] * 4
+    assert lib.fox_attn_bwd_skip_stored(1, *a7, *nm, *g4, c(P16), need - 1, B, H, L, d, f,
+                                        None) == 5
+    assert lib.fox_attn_bwd_skip_stored(0, *a7, *nm, *g4, c(P16), need, B, H, L, d, f, None) == 3
+    assert lib.fox_attn_bwd_skip_stored(1, *a7, None, c(P16), *g4, c(P16), need, B, H, L, d, f,
+                                        None) == 1
+    fneed = lib.fox_attn_bwd_fixed_gate_stored_workspace_bytes(1, B, H, L, d)
+    assert lib.fox_attn_bwd_fixed_gate_stored_workspace_bytes(0, B, H, L, d) == 0
+    assert lib.fox_attn_bwd_fixed_gate_stored(1, *a7, *[c(P16)] * 3, c(P16), c(P16), fneed - 1,
+                                              B, H, L, d, f, None) == 5
+    assert lib.fox_attn_bwd_fixed_gate_stored(0, *a7, *[c(P16)] * 3, c(P16), c(P16), fneed,
+                                              B, H, L, d, f, None) == 3
+    assert lib.fox_attn_bwd_fixed_gate_stored(1, *a7, *[c(P16)] * 3, c(P16 + 4), c(P16), fneed,
+                                              B, H, L, d, f, None) == 4
+    assert lib.fox_attn_bwd_fixed_gate_skip_stored(1, *a7, *nm, *[c(P16)] * 3, c(P16), c(P16),
+                                                   fneed - 1, B, H, L, d, f, None) == 5
+    assert lib.fox_attn_bwd_fixed_gate_skip_stored(1, *a7, c(P16), None, *[c(P16)] * 3, c(P16),
+                                                   c(P16), fneed, B, H, L, d, f, None) == 1
 
 
 def test_decode_validation_and_workspace(lib):

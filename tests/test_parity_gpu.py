@@ -482,6 +482,17 @@ def test_fixed_gate_forward_backward(dtype, d, L, tmin, tmax):
     tol = 1e-4 if dtype == "f32" else 2e-2
     err = max_abs(db, ref[3]) / max(1e-6, float(ref[3].abs().max()))
     assert err <= tol, f"fixed L={L} d_bias rel error {err:.3e}"
+    if dtype == "bf16":
+        # keeping dS: dK, dV bit for bit, the rest against the oracle (NaN-filled workspace)
+        need = fox.fox_attn_bwd_fixed_gate_stored_workspace_bytes(torch.bfloat16, B, H, L, d)
+        ws = torch.full((need,), 0xFF, dtype=torch.uint8, device=DEV)
+        sq, sk, sv, sb = fox.fox_attn_bwd_fixed_gate_stored(x["q"], x["k"], x["v"], b, o, lse,
+                                                            x["do"], s, workspace=ws)
+        torch.cuda.synchronize()
+        assert torch.equal(sk, dk) and torch.equal(sv, dv)
+        check_grad(dtype, "dQ", sq, ref[0], f"fixed stored L={L}")
+        err = max_abs(sb, ref[3]) / max(1e-6, float(ref[3].abs().max()))
+        assert err <= tol, f"fixed stored L={L} d_bias rel error {err:.3e}"
     # the same gates through the data-dependent path (constant logits = b)
     logit = b[None, :, None].expand(B, H, L).contiguous()
     c = fox.fox_gate_prefix(logit)
@@ -575,6 +586,17 @@ def test_fwd_bwd_skip_is_bitwise_dense(dtype, d, B, H, L, gate):
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
     for name, a, b in zip(("dq", "dk", "dv", "dlogf"), g1, g2):
         assert torch.equal(a, b), name
+    if dtype == "bf16":
+        # keeping dS: the skipping dQ pass reads only the slots the skipping dK/dV
+        # pass wrote (the workspace starts as NaN patterns)
+        need = fox.fox_attn_bwd_stored_workspace_bytes(torch.bfloat16, B, H, L, d)
+        ws = torch.full((need,), 0xFF, dtype=torch.uint8, device=DEV)
+        g3 = fox.fox_attn_bwd_stored(x["q"], x["k"], x["v"], c, o1, l1, x["do"], s)
+        g4 = fox.fox_attn_bwd_skip_stored(x["q"], x["k"], x["v"], c, o1, l1, x["do"], qn, kn, s,
+                                          workspace=ws)
+        torch.cuda.synchronize()
+        for name, a, b in zip(("dq", "dk", "dv", "dlogf"), g3, g4):
+            assert torch.equal(a, b), f"stored {name}"
 
 
 FIXED_SKIP_CASES = [("bf16", 128, 2, 4, 3000, 2.0, 64.0), ("bf16", 64, 1, 3, 4100, 8.0, 4096.0),
@@ -595,6 +617,12 @@ def test_fixed_gate_skip_is_bitwise_dense(dtype, d, B, H, L, tmin, tmax):
     o2, l2 = fox.fox_attn_fwd_fixed_gate_skip(x["q"], x["k"], x["v"], b, qn, kn, s)
     g1 = fox.fox_attn_bwd_fixed_gate(x["q"], x["k"], x["v"], b, o1, l1, x["do"], s)
     g2 = fox.fox_attn_bwd_fixed_gate_skip(x["q"], x["k"], x["v"], b, o1, l1, x["do"], qn, kn, s)
+    if dtype == "bf16":
+        need = fox.fox_attn_bwd_fixed_gate_stored_workspace_bytes(torch.bfloat16, B, H, L, d)
+        ws = torch.full((need,), 0xFF, dtype=torch.uint8, device=DEV)
+        g3 = fox.fox_attn_bwd_fixed_gate_stored(x["q"], x["k"], x["v"], b, o1, l1, x["do"], s)
+        g4 = fox.fox_attn_bwd_fixed_gate_skip_stored(x["q"], x["k"], x["v"], b, o1, l1, x["do"],
+                                                     qn, kn, s, workspace=ws)
     qd = x["q"][:, :, -1].contiguous()
     d1 = fox.fox_attn_decode_fixed_gate(qd, x["k"], x["v"], b, s)
     d2 = fox.fox_attn_decode_fixed_gate_skip(qd, x["k"], x["v"], b, kn, s)
@@ -603,6 +631,10 @@ def test_fixed_gate_skip_is_bitwise_dense(dtype, d, B, H, L, tmin, tmax):
     for name, a, c in zip(("dq", "dk", "dv", "db"), g1, g2):
         assert torch.equal(a, c), name
     assert torch.equal(d1[0], d2[0]) and torch.equal(d1[1], d2[1])
+    if dtype == "bf16":
+        for name, a, c in zip(("dq", "dk", "dv", "db"), g3, g4):
+            assert torch.equal(a, c), f"stored {name}"
+        assert torch.equal(g3[1], g1[1]) and torch.equal(g3[2], g1[2])
 
 
 # ------------------------------------------------------------ FoX (Pro) layer
