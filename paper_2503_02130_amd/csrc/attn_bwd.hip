@@ -790,7 +790,7 @@ __global__ __launch_bounds__(kDsThreads) void bwd_dq_stored_kernel(
   // count, the others being exact zeros; cut never decreases with nb (c never
   // increases), so the blocks this workgroup needs start at the first nb with
   // cut(nb) > qt0 (a binary search; block qt0 / 2 holds the diagonal, stored).
-  const int* tiles_row = ds_tiles + (size_t)bh * ds_key_blocks(L);
+  const int* tiles_row = SKIP ? ds_tiles + (size_t)bh * ds_key_blocks(L) : nullptr;
   auto cut = [&](int nb) { return SKIP ? 2 * nb + tiles_row[nb] : n_qt; };
   int j_first = 0;
   if constexpr (SKIP) {
@@ -818,8 +818,8 @@ __global__ __launch_bounds__(kDsThreads) void bwd_dq_stored_kernel(
           (uint32_t)(t_hi - t_lo) * kDsSlotBytes);
       for (int t = t_lo; t < t_hi; ++t)
         dma16_nt(rs, &sm.ds[B][t][wave * (kDsChunkLds / 16)],
-              ds_src + uniform_u32((uint32_t)(t - t_lo) * kDsSlotBytes +
-                                   (uint32_t)(j & 1) * kDsStageBytes + (uint32_t)wave * 1024));
+                 ds_src + uniform_u32((uint32_t)(t - t_lo) * kDsSlotBytes +
+                                      (uint32_t)(j & 1) * kDsStageBytes + (uint32_t)wave * 1024));
     }
   };
   auto body = [&](auto bufc) {
