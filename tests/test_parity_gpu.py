@@ -314,12 +314,15 @@ def test_workload_fwdbwd_bf16_b8_h12_l2048_d64():
     s = fox.default_scale(w.d)
     c, o, lse = gpu_forward(x, s)
     got = fox.fox_attn_bwd(x["q"], x["k"], x["v"], c, o, lse, x["do"], s)
+    kept = fox.fox_attn_bwd_stored(x["q"], x["k"], x["v"], c, o, lse, x["do"], s)
     torch.cuda.synchronize()
     xc = cpu(x)
     O, LSE = oracle.forward(xc["q"], xc["k"], xc["v"], xc["logit"], s)
     check_fwd("bf16", o, lse, O, LSE, w.name)
     ref = oracle.backward(xc["q"], xc["k"], xc["v"], xc["logit"], xc["do"], s)
     check_bwd("bf16", [t.cpu() for t in got], ref, w.name)
+    check_bwd("bf16", [t.cpu() for t in kept], ref, w.name + " (stored dS)")
+    assert torch.equal(kept[1], got[1]) and torch.equal(kept[2], got[2])
 
 
 def _sampled_heads_by_gate(logit, n_each):
