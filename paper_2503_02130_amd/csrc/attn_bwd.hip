@@ -11,11 +11,17 @@
 //   delta kernel   Delta_i from the stored O (bf16 or fp32) and dO.
 //   dq kernel      query-stationary: 32 queries per wave; S^T = K Q^T and
 //                  dP^T = V dO^T on MFMA, dS^T in registers, dQ^T += K^T dS^T with
-//                  K also stored transposed in LDS; dc^q from in-register row sums.
+//                  K^T taken from the row-major LDS tile by transposing reads;
+//                  dc^q from in-register row sums.
 //   dkdv kernel    key-stationary: 32 keys per wave; S = Q K^T and dP = dO V^T,
-//                  then dV^T += dO^T P and dK^T += Q^T dS with Q and dO stored both
-//                  row-major and transposed in LDS; dc^k from in-register sums.
+//                  then dV^T += dO^T P and dK^T += Q^T dS, the transposed
+//                  operands again by transposing reads; dc^k from in-register sums.
 //   reverse scan   (gate_scan.hip) turns dc^q + dc^k into d(log f).
+//
+// The backward that keeps dS replaces the dq kernel: the dkdv kernel's STORE
+// instantiation also writes the bf16 dS it forms, and the stored-dS dq kernel
+// streams it from HBM (dQ^T += K^T dS^T, dc^q = rowsum) instead of recomputing
+// S, P and dP.
 //
 // The forget-gate bias is formed relative to c_ref (the first query of the
 // block for dq, the first key of the block for dkdv), exactly as in the forward:
@@ -399,7 +405,8 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
   constexpr int NQB = kKvBM / 32;  // 32-query sub-blocks per tile
   constexpr int TILE = kKvBM * D;
   constexpr int NDMA = TILE * 2 / 1024 / kKvWaves;
-  static_assert(NDMA >= 1, "every wave issues at least one DMA load per tile");
+  static_assert(NDMA >= 1 && 2 * NDMA * kKvPairs * 1024 == TILE * 2,
+                "the P waves' DMA loads cover a tile exactly");
   __shared__ __attribute__((aligned(16))) KvSmem<D> sm;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
