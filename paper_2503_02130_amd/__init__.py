@@ -25,7 +25,10 @@ from ._lib import (  # noqa: F401
     EXPORTED,
 )
 
+from .autograd import ForgettingAttention, forgetting_attention  # noqa: E402,F401
+
 __all__ = [
+    "ForgettingAttention", "forgetting_attention",
     "FoxError", "default_scale", "load", "status_string",
     "fox_gate_prefix", "fox_attn_fwd", "fox_attn_bwd", "fox_attn_bwd_workspace_bytes",
     "fox_attn_bwd_delta", "fox_attn_bwd_dkdv", "fox_attn_bwd_dq", "fox_dlogf_from_dc",
