@@ -478,10 +478,17 @@ SQ_PASS_A = ("SQ_INSTS_MFMA", "SQ_INSTS_VALU", "SQ_INSTS_LDS", "SQ_INSTS_SALU",
 SQ_PASS_B = ("SQ_VALU_MFMA_BUSY_CYCLES", "SQ_VALU_MFMA_COEXEC_CYCLES", "SQ_BUSY_CYCLES",
              "SQ_LDS_BANK_CONFLICT", "SQ_WAIT_INST_ANY", "SQ_WAIT_ANY", "SQ_ACTIVE_INST_VALU",
              "SQ_ACTIVE_INST_LDS")
+# kernels whose measured traffic the JSON line reports
+KV_STORE_KERNEL = "bwd_dkdv_bf16_kernel<128,false,false,true>"
+KV_KERNEL = "bwd_dkdv_bf16_kernel<128,false,false,false>"
+DQ_STORED_KERNEL = "bwd_dq_stored_kernel<128,false>"
+DECODE_KERNEL = "decode_split_kernel<__bf16,128,false,false>"
+ROOFLINE_KERNELS = (KV_STORE_KERNEL, KV_KERNEL, DQ_STORED_KERNEL, DECODE_KERNEL)
+
 SQ_KERNELS = ("fwd_bf16_kernel<128,false,false,false>",
               "bwd_dkdv_bf16_kernel<128,false,false,false>",
               "bwd_dkdv_bf16_kernel<128,false,false,true>", "bwd_dq_bf16_kernel<128,false,false>",
-              "bwd_dq_stored_kernel<128>")
+              "bwd_dq_stored_kernel<128,false>")
 
 
 def sq_summary(dirs, command, ms):
@@ -599,7 +606,7 @@ def main():
     # compulsory HBM bytes of one dK/dV launch: read q, k, v, dO (bf16), c, LSE,
     # delta (fp32); write dK, dV (bf16), dc_k (fp32) and the stored dS
     kv_bytes = B * H * L * (6 * d * 2 + 4 * 4) + r["store_bytes"]
-    kv_traffic = measured_traffic("bwd_dkdv_bf16_kernel<128,false,false,true>")
+    kv_traffic = measured_traffic(KV_STORE_KERNEL)
     # dQ from the stored dS: read dS and k, write dQ (bf16) and dc_q (fp32)
     dq_bytes = r["store_bytes"] + B * H * L * (2 * d * 2 + 4)
     dq_gbs = dq_bytes / (r["dq_ms"] * 1e-3) / 1e9
@@ -633,11 +640,11 @@ def main():
                      "unit": "TFLOP/s", "frac": round(kv_tf / MFMA_BF16_PEAK_TFLOPS, 4),
                      "traffic": kv_traffic, "algorithmic_flops_per_launch": fl_kv,
                      "compulsory_bytes_per_launch": kv_bytes},
-        "roofline_dq_stored": {"bound": "hbm", "kernel": "bwd_dq_stored_kernel<128> "
+        "roofline_dq_stored": {"bound": "hbm", "kernel": "bwd_dq_stored_kernel<128,false> "
                                "(fox_attn_bwd_dq_stored)", "achieved": round(dq_gbs, 1),
                                "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                "frac": round(dq_gbs / HBM_PEAK_GBS, 4),
-                               "traffic": measured_traffic("bwd_dq_stored_kernel<128>"),
+                               "traffic": measured_traffic(DQ_STORED_KERNEL),
                                "compulsory_bytes_per_launch": dq_bytes},
         "recompute": {"what": "the same step with fox_attn_bwd's stages (the dQ pass recomputes "
                               "S and dP; O(L) workspace)",
@@ -645,7 +652,7 @@ def main():
                       "frac_of_peak": round(rc_tf / MFMA_BF16_PEAK_TFLOPS, 4),
                       "bwd_dkdv_ms": round(r["rc_dkdv_ms"], 4),
                       "bwd_dq_ms": round(r["rc_dq_ms"], 4),
-                      "dkdv_traffic": measured_traffic("bwd_dkdv_bf16_kernel<128,false,false,false>")},
+                      "dkdv_traffic": measured_traffic(KV_KERNEL)},
         "skip": {"what": "the same step through fox_attn_fwd_skip / fox_attn_bwd_skip_stored "
                          "(exact gate-aware tile skipping, bound kernels included); outputs "
                          "bitwise equal to the dense step",
@@ -727,8 +734,7 @@ def main():
                          "roofline": {"bound": "hbm", "kernel": "fox_attn_decode (split + combine)",
                                       "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
                                       "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
-                                      "traffic": measured_traffic(
-                                          "decode_split_kernel<__bf16,128,false,false>")},
+                                      "traffic": measured_traffic(DECODE_KERNEL)},
                          "skip": {"what": "fox_attn_decode_skip: exact gate-aware skipping of key "
                                           "splits, outputs bitwise equal to the dense decode",
                                   "ms_per_step": round(rd["skip_ms"], 4),
