@@ -370,6 +370,13 @@ def test_workload_fwdbwd_bf16_b2_h16_l16384_d128_stored():
     assert rel_l2(got[0], base[0]) <= 5e-3, rel_l2(got[0], base[0])
     assert rel_l2(got[3], base[3]) <= 5e-3, rel_l2(got[3], base[3])
     del base
+    # the same with exact skipping: bit for bit
+    qn, kn = fox.fox_row_norm_max(x["q"]), fox.fox_row_norm_max(x["k"])
+    skipped = fox.fox_attn_bwd_skip_stored(x["q"], x["k"], x["v"], c, o, lse, x["do"], qn, kn, s)
+    torch.cuda.synchronize()
+    for name, a, b in zip(("dq", "dk", "dv", "dlogf"), skipped, got):
+        assert torch.equal(a, b), f"skipping {name}"
+    del skipped
     heads = _sampled_heads_by_gate(x["logit"], 1)
     print(f"{w.name} (stored dS): oracle on heads {heads}", flush=True)
     for (b, h) in heads:
