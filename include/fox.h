@@ -30,6 +30,10 @@
  *     surface at the caller's next synchronisation.
  *   - Causal only (the paper considers causal sequence modelling only, Sec. 2).
  *   - Gate logits must be finite (then log f is finite and c_i - c_j is defined).
+ *   - Backward families: every backward (plain, exact skipping, fixed gates, FoX
+ *     Pro) recomputes P in its dQ half within an O(B H L) workspace; its *_stored
+ *     twin (bf16 only) keeps dS in an O(B H L^2) workspace instead, which is
+ *     faster at long L and gives the same dK, dV bit for bit.
  */
 #ifndef FOX_H_
 #define FOX_H_
