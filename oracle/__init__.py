@@ -8,7 +8,7 @@ from .fox_oracle import (  # noqa: F401
     log_sigmoid, prefix_c, gate_prefix, decay_matrix,
     forward_head_from_c, backward_head_from_c, reverse_cumsum,
     forward_from_logf, forward, backward_from_logf, backward, decode,
-    gate_backward, backward_logit,
+    gate_backward, backward_logit, gate_projection, gate_projection_backward,
     time_constant, fixed_gate_bias_init, fixed_gate_log_f, forward_fixed_gate,
     backward_fixed_gate,
     rms_norm, rms_norm_backward, token_shift, token_shift_backward,

@@ -27,6 +27,9 @@ paper (Forgetting Transformer, arXiv 2503.02130):
                                d(log f)_l = sum_{i >= l} dc_i  (reverse cumsum)
   * d(logit)                   through f = sigmoid(logit): d(logit) =
                                d(log f) * sigmoid(-logit)      (Sec. 3, gate def.)
+  * gate projection            logit_t^(h) = w_f^(h) . x_t + b_f^(h) for the layer
+                               input x_t, one weight vector and bias per head
+                                                              (Sec. 3, gate def.)
   * fixed gates                f_t^(h) = sigmoid(b^(h)) for all t (ALiBi with slope
                                -log sigmoid(b^(h)), Sec. 3); b^(h) initialised so that
                                T(b) = -1/log sigmoid(b) is log-spaced in [T_min, T_max]
@@ -208,6 +211,33 @@ def backward_logit(q, k, v, logit, dO, scale: float, heads=None):
     """dQ, dK, dV and the gradient with respect to the gate logits."""
     dQ, dK, dV, dlf = backward(q, k, v, logit, dO, scale, heads)
     return dQ, dK, dV, gate_backward(logit, dlf)
+
+
+# ---------------------------------------------------------------------------
+# Gate projection (Sec. 3, gate definition): the logits are an affine function
+# of the layer input, one weight vector and one bias per head.
+# ---------------------------------------------------------------------------
+def gate_projection(x, w_f, b_f=None) -> torch.Tensor:
+    """logit[b, h, t] = sum_m x[b, t, m] w_f[h, m] + b_f[h] for x [B, L, M],
+    w_f [H, M], b_f [H] (None: no bias); [B, H, L]."""
+    x64, w64 = _f64(x), _f64(w_f)
+    logit = torch.matmul(x64, w64.T).transpose(1, 2)
+    if b_f is not None:
+        logit = logit + _f64(b_f)[None, :, None]
+    return logit.contiguous()
+
+
+def gate_projection_backward(x, w_f, d_logit):
+    """Gradients of sum(logit * d_logit): dx [B, L, M] = sum_h d_logit[b, h, t]
+    w_f[h]; dw_f [H, M] = sum_{b, t} d_logit[b, h, t] x[b, t]; db_f [H] =
+    sum_{b, t} d_logit[b, h, t]."""
+    x64, w64, g = _f64(x), _f64(w_f), _f64(d_logit)
+    B, L, M = x64.shape
+    H = w64.shape[0]
+    dx = torch.matmul(g.transpose(1, 2), w64)
+    dw = torch.matmul(g.permute(1, 0, 2).reshape(H, B * L), x64.reshape(B * L, M))
+    db = g.sum(dim=(0, 2))
+    return dx, dw, db
 
 
 # ---------------------------------------------------------------------------

@@ -572,6 +572,51 @@ def pin_p19_output_gate_limits(ora, B=1, H=3, L=6, d=5, seed=29):
     _close(do, torch.zeros_like(do), 0.0, "P19 closed gate passes no gradient to o")
 
 
+def pin_p20_gate_projection(ora, B=2, L=3, M=5, H=2, seed=20):
+    """The gate logits against explicit loops over the definition, and the
+    special case w_f^(h) = unit vector m_h: logit^(h)_t = x_t[m_h] + b^(h)."""
+    x, w, b = _rand((B, L, M), seed), _rand((H, M), seed + 1), _rand((H,), seed + 2)
+    got = ora.gate_projection(x, w, b)
+    assert tuple(got.shape) == (B, H, L)
+    for bb in range(B):
+        for h in range(H):
+            for t in range(L):
+                ref = sum(float(x[bb, t, m]) * float(w[h, m]) for m in range(M)) + float(b[h])
+                assert abs(float(got[bb, h, t]) - ref) <= 1e-12 * max(1.0, abs(ref)), (bb, h, t)
+    e = torch.zeros((H, M), dtype=torch.float64)
+    picks = [3, 1]
+    for h, m in enumerate(picks):
+        e[h, m] = 1.0
+    got = ora.gate_projection(x, e, b)
+    for h, m in enumerate(picks):
+        _close(got[:, h, :], x[:, :, m] + b[h], 1e-15, "unit-vector projection")
+    _close(ora.gate_projection(x, w), ora.gate_projection(x, w, b) - b[None, :, None], 1e-14,
+           "bias-free projection")
+
+
+def pin_p21_gate_projection_backward(ora, B=2, L=4, M=6, H=3, seed=21):
+    """dx, dw_f, db_f against explicit loops and against central finite
+    differences of sum(logit * d_logit)."""
+    x, w, b = _rand((B, L, M), seed), _rand((H, M), seed + 1), _rand((H,), seed + 2)
+    g = _rand((B, H, L), seed + 3)
+    dx, dw, db = ora.gate_projection_backward(x, w, g)
+    for bb in range(B):
+        for t in range(L):
+            for m in range(M):
+                ref = sum(float(g[bb, h, t]) * float(w[h, m]) for h in range(H))
+                assert abs(float(dx[bb, t, m]) - ref) <= 1e-12, ("dx", bb, t, m)
+    for h in range(H):
+        for m in range(M):
+            ref = sum(float(g[bb, h, t]) * float(x[bb, t, m]) for bb in range(B) for t in range(L))
+            assert abs(float(dw[h, m]) - ref) <= 1e-12, ("dw", h, m)
+        ref = sum(float(g[bb, h, t]) for bb in range(B) for t in range(L))
+        assert abs(float(db[h]) - ref) <= 1e-12, ("db", h)
+    f = lambda: float((ora.gate_projection(x, w, b) * g).sum())
+    _fd_check(f, x, dx, 1e-4, 1e-7, "dx")
+    _fd_check(f, w, dw, 1e-4, 1e-7, "dw")
+    _fd_check(f, b, db, 1e-4, 1e-7, "db")
+
+
 ALL_PINS = [
     pin_p1_zero_forgetting_is_softmax_attention,
     pin_p2_full_forgetting,
@@ -596,4 +641,6 @@ ALL_PINS = [
     pin_p18_pro_finite_differences,
     pin_p18_pro_autograd,
     pin_p19_output_gate_limits,
+    pin_p20_gate_projection,
+    pin_p21_gate_projection_backward,
 ]

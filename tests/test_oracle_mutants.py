@@ -207,6 +207,40 @@ def _m_head_weight_first_row(m):
     m._head_weight = hw
 
 
+def _m_projection_heads_swapped(m):
+    """The gate projection pairing head h with weight row H-1-h."""
+    orig = m.gate_projection
+    def gp(x, w_f, b_f=None):
+        return orig(x, m._f64(w_f).flip(0), b_f)
+    m.gate_projection = gp
+
+
+def _m_projection_dx_one_head(m):
+    """dx taking only the first head's contribution."""
+    orig = m.gate_projection_backward
+    def gb(x, w_f, d_logit):
+        dx, dw, db = orig(x, w_f, d_logit)
+        g, w = m._f64(d_logit), m._f64(w_f)
+        return g[:, 0, :, None] * w[0][None, None, :], dw, db
+    m.gate_projection_backward = gb
+
+
+def _m_projection_no_bias(m):
+    """The gate projection dropping the bias."""
+    orig = m.gate_projection
+    m.gate_projection = lambda x, w_f, b_f=None: orig(x, w_f, None)
+
+
+def _m_projection_dw_mean(m):
+    """dw_f averaged over tokens instead of summed."""
+    orig = m.gate_projection_backward
+    def gb(x, w_f, d_logit):
+        dx, dw, db = orig(x, w_f, d_logit)
+        n = m._f64(x).shape[0] * m._f64(x).shape[1]
+        return dx, dw / n, db
+    m.gate_projection_backward = gb
+
+
 MUTANTS = {
     "decay_scaled": _m_scale_on_D,
     "exclusive_prefix": _m_exclusive_c,
@@ -232,6 +266,10 @@ MUTANTS = {
     "shift_logit_sign": _m_shift_logit_sign,
     "gate_bwd_no_derivative": _m_gate_bwd_no_derivative,
     "head_weight_first_row": _m_head_weight_first_row,
+    "projection_heads_swapped": _m_projection_heads_swapped,
+    "projection_dx_one_head": _m_projection_dx_one_head,
+    "projection_no_bias": _m_projection_no_bias,
+    "projection_dw_mean": _m_projection_dw_mean,
 }
 
 
