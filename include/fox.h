@@ -436,6 +436,44 @@ int fox_attn_bwd_pro_stored(int dtype, const void* q, const void* k, const void*
                             float* do_norm_weight, void* workspace, size_t workspace_bytes,
                             int B, int H, int L, int d, float scale, void* stream);
 
+/*
+ * The forget-gate projection (Sec. 3, gate definition: f_t = sigmoid(w_f^T x_t
+ * + b_f), one w_f and b_f per head): the logits that fox_gate_prefix and
+ * fox_dlogit_from_dc take, from the layer input.
+ *
+ *   x          [B,L,M] dtype in   layer input, M contiguous; M a multiple of 8
+ *   w_f        [H,M]   fp32  in   one weight row per head (H <= 64)
+ *   b_f        [H]     fp32  in   per-head bias; may be NULL (no bias)
+ *   gate_logit [B,H,L] fp32  out  gate_logit[b,h,t] = w_f[h] . x[b,t] + b_f[h]
+ *
+ * The products run on bf16 MFMA with fp32 accumulation; fp32 operands enter as
+ * a pair of bf16 (hi + lo, within 2^-16 relative), so each product is within
+ * 4 * 2^-16 of exact and the result close to an fp32 dot product (measured
+ * relative L2 error near 2e-6 for either dtype).  Values must be finite and below 3.38e38 in
+ * magnitude (the bf16 range).  H > 64 or M % 8 != 0: FOX_ERR_UNSUPPORTED.
+ */
+int fox_gate_projection(int dtype, const void* x, const float* w_f, const float* b_f,
+                        float* gate_logit, int B, int L, int H, int M, void* stream);
+
+/* Bytes of workspace fox_gate_projection_bwd needs (0 on invalid arguments). */
+size_t fox_gate_projection_bwd_workspace_bytes(int dtype, int B, int L, int H, int M);
+
+/*
+ * Backward of fox_gate_projection: the gradients of sum(gate_logit * d_logit).
+ *
+ *   x, w_f     as for fox_gate_projection                     in
+ *   d_logit    [B,H,L] fp32  in   e.g. from fox_dlogit_from_dc
+ *   dx         [B,L,M] dtype out  sum_h d_logit[b,h,t] w_f[h]; may be NULL (not needed)
+ *   dw_f       [H,M]   fp32  out  sum_{b,t} d_logit[b,h,t] x[b,t] (overwritten, not accumulated)
+ *   db_f       [H]     fp32  out  sum_{b,t} d_logit[b,h,t]; may be NULL
+ *   workspace  device buffer of at least fox_gate_projection_bwd_workspace_bytes()
+ *              (per-chunk partials of dw_f, summed in a fixed order: results are
+ *              deterministic)
+ */
+int fox_gate_projection_bwd(int dtype, const void* x, const float* w_f, const float* d_logit,
+                            void* dx, float* dw_f, float* db_f, void* workspace,
+                            size_t workspace_bytes, int B, int L, int H, int M, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

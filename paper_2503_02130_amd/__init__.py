@@ -22,6 +22,7 @@ from ._lib import (  # noqa: F401
     fox_attn_bwd_pro_stored_workspace_bytes, fox_attn_bwd_skip_stored,
     fox_attn_bwd_fixed_gate_stored, fox_attn_bwd_fixed_gate_stored_workspace_bytes,
     fox_attn_bwd_fixed_gate_skip_stored,
+    fox_gate_projection, fox_gate_projection_bwd, fox_gate_projection_bwd_workspace_bytes,
     EXPORTED,
 )
 
@@ -46,4 +47,5 @@ __all__ = [
     "fox_attn_bwd_pro_stored", "fox_attn_bwd_pro_stored_workspace_bytes",
     "fox_attn_bwd_skip_stored", "fox_attn_bwd_fixed_gate_stored",
     "fox_attn_bwd_fixed_gate_stored_workspace_bytes", "fox_attn_bwd_fixed_gate_skip_stored",
+    "fox_gate_projection", "fox_gate_projection_bwd", "fox_gate_projection_bwd_workspace_bytes",
 ]

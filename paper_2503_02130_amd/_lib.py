@@ -39,6 +39,7 @@ EXPORTED = (
     "fox_attn_bwd_pro_stored_workspace_bytes", "fox_attn_bwd_pro_stored",
     "fox_attn_bwd_skip_stored", "fox_attn_bwd_fixed_gate_stored_workspace_bytes",
     "fox_attn_bwd_fixed_gate_stored", "fox_attn_bwd_fixed_gate_skip_stored",
+    "fox_gate_projection", "fox_gate_projection_bwd_workspace_bytes", "fox_gate_projection_bwd",
 )
 
 
@@ -154,6 +155,12 @@ def load() -> ctypes.CDLL:
     lib.fox_attn_bwd_pro_stored.restype = I
     lib.fox_attn_bwd_pro_stored.argtypes = [I, P, P, P, P, P, P, P, P, F, P, P, P, P, P, P, P, P, Z, I, I,
                                      I, I, F, P]
+    lib.fox_gate_projection.restype = I
+    lib.fox_gate_projection.argtypes = [I, P, P, P, P, I, I, I, I, P]
+    lib.fox_gate_projection_bwd_workspace_bytes.restype = Z
+    lib.fox_gate_projection_bwd_workspace_bytes.argtypes = [I, I, I, I, I]
+    lib.fox_gate_projection_bwd.restype = I
+    lib.fox_gate_projection_bwd.argtypes = [I, P, P, P, P, P, P, P, Z, I, I, I, I, P]
     _lib = lib
     return lib
 
@@ -974,3 +981,52 @@ def _attn_bwd_pro_call(entry, ws_bytes, q, k, v, c, o, lse, g_logit, o_norm_weig
                                 B, H, L, d, s, _stream(q))
     _raise(st, entry)
     return dq, dk, dv, dlf, dg, dw
+
+
+# ---------------------------------------------------------------------------
+def _proj_shapes(x, w_f):
+    if x.dim() != 3 or w_f.dim() != 2:
+        raise ValueError("x must be [B, L, M] and w_f [H, M]")
+    B, L, M = x.shape
+    H = w_f.shape[0]
+    if x.dtype not in _DT:
+        raise ValueError(f"x must be float32 or bfloat16 (got {x.dtype})")
+    _check(x, "x", (B, L, M), None, None)
+    _check(w_f, "w_f", (H, M), torch.float32, x.device)
+    return B, L, H, M
+
+
+def fox_gate_projection(x, w_f, b_f=None, gate_logit=None):
+    """Gate logits [B, H, L] fp32: gate_logit[b, h, t] = w_f[h] . x[b, t] + b_f[h]
+    for x [B, L, M] (bf16 or fp32), w_f [H, M] and b_f [H] (optional) fp32."""
+    B, L, H, M = _proj_shapes(x, w_f)
+    if b_f is not None:
+        _check(b_f, "b_f", (H,), torch.float32, x.device)
+    if gate_logit is None:
+        gate_logit = torch.empty((B, H, L), dtype=torch.float32, device=x.device)
+    _check(gate_logit, "gate_logit", (B, H, L), torch.float32, x.device)
+    st = load().fox_gate_projection(_DT[x.dtype], _ptr(x), _ptr(w_f), _ptr(b_f), _ptr(gate_logit),
+                                    B, L, H, M, _stream(x))
+    _raise(st, "fox_gate_projection")
+    return gate_logit
+
+
+def fox_gate_projection_bwd_workspace_bytes(dtype, B, L, H, M) -> int:
+    return int(load().fox_gate_projection_bwd_workspace_bytes(_DT[dtype], B, L, H, M))
+
+
+def fox_gate_projection_bwd(x, w_f, d_logit, want_dx=True, want_db=True, workspace=None):
+    """Gradients of sum(gate_logit * d_logit): returns (dx or None, dw_f, db_f or None)."""
+    B, L, H, M = _proj_shapes(x, w_f)
+    _check(d_logit, "d_logit", (B, H, L), torch.float32, x.device)
+    dx = torch.empty_like(x) if want_dx else None
+    dw = torch.empty((H, M), dtype=torch.float32, device=x.device)
+    db = torch.empty((H,), dtype=torch.float32, device=x.device) if want_db else None
+    need = fox_gate_projection_bwd_workspace_bytes(x.dtype, B, L, H, M)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=x.device)
+    st = load().fox_gate_projection_bwd(_DT[x.dtype], _ptr(x), _ptr(w_f), _ptr(d_logit), _ptr(dx),
+                                        _ptr(dw), _ptr(db), _ptr(workspace), workspace.numel(),
+                                        B, L, H, M, _stream(x))
+    _raise(st, "fox_gate_projection_bwd")
+    return dx, dw, db

@@ -36,6 +36,16 @@ int check_dtype_d(int dtype, int d) {
 
 int launch_status(hipError_t e) { return e == hipSuccess ? FOX_OK : FOX_ERR_HIP; }
 
+int check_projection(int dtype, int B, int L, int H, int M) {
+  if (B <= 0 || L <= 0 || H <= 0 || M <= 0) return FOX_ERR_SHAPE;
+  const long long n = (long long)B * L;
+  if (n > (1LL << 31) - 1 || (long long)B * H * L > (1LL << 31) - 1) return FOX_ERR_SHAPE;
+  if (n * M > kMaxElems) return FOX_ERR_SHAPE;
+  if (dtype != FOX_DTYPE_F32 && dtype != FOX_DTYPE_BF16) return FOX_ERR_UNSUPPORTED;
+  if (H > 64 || M % 8 != 0) return FOX_ERR_UNSUPPORTED;
+  return FOX_OK;
+}
+
 bool valid_eps(float eps) { return isfinite(eps) && eps >= 0.0f; }
 
 bool all_aligned16(std::initializer_list<const void*> ps) {
@@ -745,6 +755,37 @@ int fox_attn_bwd_pro_stored(int dtype, const void* q, const void* k, const void*
   return attn_bwd_pro(true, dtype, q, k, v, c, o, lse, g_logit, o_norm_weight, eps, dy, dq, dk,
                       dv, d_log_f, dg_logit, do_norm_weight, workspace, workspace_bytes, B, H, L,
                       d, scale, stream);
+}
+
+int fox_gate_projection(int dtype, const void* x, const float* w_f, const float* b_f,
+                        float* gate_logit, int B, int L, int H, int M, void* stream) {
+  if (!all_set({x, w_f, gate_logit})) return FOX_ERR_NULL;
+  int st = check_projection(dtype, B, L, H, M);
+  if (st) return st;
+  if (!all_aligned16({x, w_f, gate_logit})) return FOX_ERR_ALIGN;
+  return launch_status(fox::launch_gate_proj_fwd(dtype == FOX_DTYPE_BF16, x, w_f, b_f, gate_logit,
+                                                 B * L, L, H, M,
+                                                 static_cast<hipStream_t>(stream)));
+}
+
+size_t fox_gate_projection_bwd_workspace_bytes(int dtype, int B, int L, int H, int M) {
+  if (check_projection(dtype, B, L, H, M)) return 0;
+  return fox::gate_proj_bwd_workspace_bytes(B * L, H, M);
+}
+
+int fox_gate_projection_bwd(int dtype, const void* x, const float* w_f, const float* d_logit,
+                            void* dx, float* dw_f, float* db_f, void* workspace,
+                            size_t workspace_bytes, int B, int L, int H, int M, void* stream) {
+  if (!all_set({x, w_f, d_logit, dw_f})) return FOX_ERR_NULL;
+  int st = check_projection(dtype, B, L, H, M);
+  if (st) return st;
+  if (!all_aligned16({x, w_f, d_logit, dw_f}) || (dx && !aligned16(dx))) return FOX_ERR_ALIGN;
+  if (!workspace || workspace_bytes < fox::gate_proj_bwd_workspace_bytes(B * L, H, M))
+    return FOX_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return FOX_ERR_ALIGN;
+  return launch_status(fox::launch_gate_proj_bwd(dtype == FOX_DTYPE_BF16, x, w_f, d_logit, dx,
+                                                 dw_f, db_f, workspace, B, L, H, M,
+                                                 static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

@@ -148,4 +148,15 @@ hipError_t launch_bwd_pro(bool bf16, const void* q, const void* k, const void* v
                           void* dg, float* dwo, void* ws, int H, int BH, int L, int d, float scale,
                           hipStream_t s, bool keep_ds = false);
 
+// Forget-gate projection (gate_proj.hip): x [N = B L, M] (bf16 or fp32, M % 8 == 0),
+// w_f [H, M] fp32 (H <= 64), bias [H] (may be NULL), logits [B, H, L] fp32.
+int gate_proj_chunk_tokens(int N, int H, int M);
+size_t gate_proj_bwd_workspace_bytes(int N, int H, int M);  // the dw_f partials
+hipError_t launch_gate_proj_fwd(bool bf16, const void* x, const float* w, const float* bias,
+                                float* logit, int N, int L, int H, int M, hipStream_t s);
+// dx (may be NULL) in x's type; dw [H, M]; db [H] (may be NULL)
+hipError_t launch_gate_proj_bwd(bool bf16, const void* x, const float* w, const float* d_logit,
+                                void* dx, float* dw, float* db, void* ws, int B, int L, int H,
+                                int M, hipStream_t s);
+
 }  // namespace fox

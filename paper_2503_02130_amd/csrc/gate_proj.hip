@@ -1,0 +1,478 @@
+// The forget-gate projection of Sec. 3 (gate definition): one weight vector and
+// one bias per head map the layer input x_t to the gate logit,
+//     logit[b, h, t] = w_f[h] . x[b, t] + b_f[h],
+// and its backward, the gradients of sum(logit * d_logit):
+//     dx[b, t] = sum_h d_logit[b, h, t] w_f[h]
+//     dw_f[h]  = sum_{b, t} d_logit[b, h, t] x[b, t]
+//     db_f[h]  = sum_{b, t} d_logit[b, h, t].
+//
+// x [B, L, M] is bf16 or fp32 (rows of M contiguous), w_f [H, M] and the
+// logits [B, H, L] are fp32.  Each product streams x (or dx) once, at
+// 2 H FLOPs per element: 16 FLOPs per byte of bf16 x at H = 16, more than the
+// fp32 vector units sustain at HBM rate, so all three run on bf16 MFMA
+// (32x32x16).  fp32 operands enter as a pair of bf16 (hi = RNE(v),
+// lo = RNE(v - hi), |v - hi - lo| <= 2^-16 |v| since bf16 keeps 8 significant
+// bits) and a product keeps the terms hi*hi + hi*lo + lo*hi, within 4 * 2^-16
+// of exact (exact bf16 operands need only the hi terms of the other side);
+// every MFMA product of two bf16 is exact in the fp32 accumulator.
+//
+//   * Logits: a workgroup owns 64 tokens (two 32-token MFMA columns) and its
+//     four waves split the contraction over M in 16-wide steps, four steps'
+//     loads in flight at once; x fragments come straight from HBM (8
+//     contiguous elements per lane), w_f fragments from L2.  The waves' partial
+//     sums meet in LDS.
+//   * Backward: a workgroup owns a 128-column block of M and a chunk of tokens,
+//     32 tokens at a time.  x and d_logit tiles go to LDS (split to bf16
+//     hi/lo); dw_f's product contracts over tokens, so both of its operands
+//     are transposing reads (ds_read_b64_tr_b16) of those tiles.  dx^T = w_f^T
+//     d_logit is one MFMA column per token, written through LDS so that dx rows
+//     leave in 16-byte pieces.  Each chunk writes its dw_f partial; a second
+//     kernel sums the partials in a fixed order and computes db_f (so the
+//     result is deterministic).
+#include <algorithm>
+
+#include "fox_device.h"
+#include "fox_internal.h"
+
+namespace fox {
+
+namespace {
+
+constexpr int kProjThreads = 256;  // four waves
+constexpr int kProjFwdTok = 64;    // tokens per forward workgroup
+constexpr int kProjFwdAhead = 4;   // contraction steps whose loads are in flight together
+constexpr int kProjMBlock = 128;   // columns of M per backward workgroup
+constexpr int kProjTile = 32;      // tokens per backward sub-tile
+constexpr int kProjTargetGroups = 1024;
+
+// v ~ hi[e] + lo[e] with both halves bf16 (round to nearest even); hi and lo
+// are vectors or arrays.
+template <typename V>
+__device__ __forceinline__ void split_at(float v, V& hi, V& lo, int e) {
+  const bf16 h = to_bf16(v);
+  hi[e] = h;
+  lo[e] = to_bf16(v - to_f32(h));
+}
+
+template <typename T>
+__device__ __forceinline__ void load8(const T* p, bool ok, float (&v)[8]);
+template <>
+__device__ __forceinline__ void load8<float>(const float* p, bool ok, float (&v)[8]) {
+  f32x4 a = {0.f, 0.f, 0.f, 0.f}, b = a;
+  if (ok) {
+    a = *reinterpret_cast<const f32x4*>(p);
+    b = *reinterpret_cast<const f32x4*>(p + 4);
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    v[e] = a[e];
+    v[4 + e] = b[e];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Logits.
+// ---------------------------------------------------------------------------
+template <typename T, int HB>
+__global__ __launch_bounds__(kProjThreads) void gate_proj_fwd_kernel(
+    const T* __restrict__ x, const float* __restrict__ w, const float* __restrict__ bias,
+    float* __restrict__ logit, int N, int L, int H, int M) {
+  constexpr bool kBf16 = sizeof(T) == 2;
+  constexpr int TB = kProjFwdTok / 32;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int col = lane & 31, half = lane >> 5;
+  const int n0 = blockIdx.x * kProjFwdTok;
+  const int steps = (M + 15) / 16;
+
+  const T* xrow[TB];
+  bool xok[TB];
+#pragma unroll
+  for (int tb = 0; tb < TB; ++tb) {
+    const int n = n0 + 32 * tb + col;
+    xok[tb] = n < N;
+    xrow[tb] = x + (size_t)min(n, N - 1) * M + 8 * half;
+  }
+  const float* wrow[HB];
+  bool wok[HB];
+#pragma unroll
+  for (int hb = 0; hb < HB; ++hb) {
+    const int h = 32 * hb + col;
+    wok[hb] = h < H;
+    wrow[hb] = w + (size_t)min(h, H - 1) * M + 8 * half;
+  }
+
+  f32x16 acc[TB][HB];
+#pragma unroll
+  for (int tb = 0; tb < TB; ++tb)
+#pragma unroll
+    for (int hb = 0; hb < HB; ++hb) acc[tb][hb] = f32x16{};
+
+  for (int s0 = wave; s0 < steps; s0 += 4 * kProjFwdAhead) {
+    // this wave's steps s0, s0 + 4, ...: all loads first, then the products
+    float wv[kProjFwdAhead][HB][8];
+    bf16x8 xb[kProjFwdAhead][TB];
+    float xv[kBf16 ? 1 : kProjFwdAhead][TB][8];
+#pragma unroll
+    for (int u = 0; u < kProjFwdAhead; ++u) {
+      const int m = 16 * (s0 + 4 * u);
+      const bool mok = s0 + 4 * u < steps && m + 8 * half < M;
+#pragma unroll
+      for (int hb = 0; hb < HB; ++hb) load8<float>(wrow[hb] + m, wok[hb] && mok, wv[u][hb]);
+#pragma unroll
+      for (int tb = 0; tb < TB; ++tb) {
+        if constexpr (kBf16) {
+          xb[u][tb] = bf16x8{};
+          if (xok[tb] && mok) xb[u][tb] = *reinterpret_cast<const bf16x8*>(xrow[tb] + m);
+        } else {
+          load8<float>(reinterpret_cast<const float*>(xrow[tb]) + m, xok[tb] && mok,
+                       xv[u][tb]);
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kProjFwdAhead; ++u) {
+      bf16x8 whi[HB], wlo[HB];
+#pragma unroll
+      for (int hb = 0; hb < HB; ++hb)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) split_at(wv[u][hb][e], whi[hb], wlo[hb], e);
+#pragma unroll
+      for (int tb = 0; tb < TB; ++tb) {
+        bf16x8 xhi, xlo;
+        if constexpr (kBf16) {
+          xhi = xb[u][tb];
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) split_at(xv[u][tb][e], xhi, xlo, e);
+        }
+#pragma unroll
+        for (int hb = 0; hb < HB; ++hb) {
+          acc[tb][hb] = mfma32(whi[hb], xhi, acc[tb][hb]);
+          acc[tb][hb] = mfma32(wlo[hb], xhi, acc[tb][hb]);
+          if constexpr (!kBf16) acc[tb][hb] = mfma32(whi[hb], xlo, acc[tb][hb]);
+        }
+      }
+    }
+  }
+
+  // The four waves' partial sums: entry ((tb * HB + hb) * 16 + r) * 64 + lane.
+  constexpr int kEntries = TB * HB * 16 * 64;
+  __shared__ float red[4][kEntries];
+#pragma unroll
+  for (int tb = 0; tb < TB; ++tb)
+#pragma unroll
+    for (int hb = 0; hb < HB; ++hb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) red[wave][((tb * HB + hb) * 16 + r) * 64 + lane] = acc[tb][hb][r];
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < kEntries / kProjThreads; ++k) {
+    const int e = tid + kProjThreads * k;
+    const int r = (e >> 6) & 15, blk = e >> 10;
+    const int tb = blk / HB, hb = blk % HB;
+    const int head = 32 * hb + mfma_row(r, half);
+    const int n = n0 + 32 * tb + col;
+    if (head < H && n < N) {
+      float v = red[0][e] + red[1][e] + red[2][e] + red[3][e];
+      if (bias) v += bias[head];
+      const int b = n / L, t = n - b * L;
+      logit[((size_t)b * H + head) * L + t] = v;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Backward: dx and the dw_f partial of one (column block, token chunk).
+// ---------------------------------------------------------------------------
+template <typename T, int HB>
+struct ProjBwdSmem {
+  static constexpr int GS = 32 * HB + 8;  // d_logit tile row stride (bf16 elements)
+  static constexpr int OS = sizeof(T) == 2 ? kProjMBlock + 8 : kProjMBlock + 4;  // dx tile row
+  alignas(16) bf16 x_hi[kProjTile * kProjMBlock];  // swizzled rows (swz_chunk<128>)
+  alignas(16) bf16 x_lo[sizeof(T) == 2 ? 8 : kProjTile * kProjMBlock];
+  alignas(16) bf16 g_hi[kProjTile * GS];           // [token][head]
+  alignas(16) bf16 g_lo[kProjTile * GS];
+  alignas(16) T out[kProjTile * OS];               // dx rows of the sub-tile
+};
+
+template <typename T, int HB>
+__global__ __launch_bounds__(kProjThreads) void gate_proj_bwd_kernel(
+    const T* __restrict__ x, const float* __restrict__ w, const float* __restrict__ g,
+    T* __restrict__ dx, float* __restrict__ dw_part, int N, int L, int H, int M, int CT) {
+  constexpr bool kBf16 = sizeof(T) == 2;
+  using S = ProjBwdSmem<T, HB>;
+  constexpr int GS = S::GS, OS = S::OS;
+  constexpr int HPT = 4 * HB;                              // heads staged per thread
+  constexpr int XV = kBf16 ? 2 : 4;                        // 16-byte x pieces per thread
+  __shared__ __attribute__((aligned(16))) S sm;
+
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int col = lane & 31, half = lane >> 5;
+  const int mb0 = blockIdx.x * kProjMBlock;
+  const int n_begin = blockIdx.y * CT, n_end = min(N, n_begin + CT);
+  const int m_lane = mb0 + 32 * wave + col;  // this lane's column of dw_f and of dx^T's rows
+
+  // w_f^T fragments of dx^T = w_f^T d_logit: row m_lane, heads 16 ks + 8 half + e.
+  bf16x8 whi[2 * HB], wlo[2 * HB];
+#pragma unroll
+  for (int ks = 0; ks < 2 * HB; ++ks)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int h = 16 * ks + 8 * half + e;
+      const float v = (h < H && m_lane < M) ? w[(size_t)h * M + m_lane] : 0.0f;
+      split_at(v, whi[ks], wlo[ks], e);
+    }
+
+  // transposing-read offsets: x tile (m rows of the operand), d_logit tile (heads)
+  int xoff[2][kProjMBlock / 32];
+  tile_tr_offsets<kProjMBlock>(xoff, lane);
+  int goff[2];
+  {
+    const int g16 = lane >> 4, j16 = lane & 15;
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2)
+      goff[k2] = (8 * k2 + 4 * (g16 >> 1) + (j16 >> 2)) * GS + 16 * (g16 & 1) + 4 * (j16 & 3);
+  }
+
+  // staging registers for one sub-tile
+  typedef typename std::conditional<kBf16, bf16x8, f32x4>::type XPiece;
+  XPiece xr[XV];
+  float gr[HPT];
+  auto load_tile = [&](int n0) {
+#pragma unroll
+    for (int q = 0; q < XV; ++q) {
+      const int idx = tid + kProjThreads * q;
+      const int row = kBf16 ? idx >> 4 : idx >> 5;
+      const int m = mb0 + (kBf16 ? 8 * (idx & 15) : 4 * (idx & 31));
+      const int n = n0 + row;
+      xr[q] = XPiece{};
+      if (n < n_end && m < M) xr[q] = *reinterpret_cast<const XPiece*>(x + (size_t)n * M + m);
+    }
+    const int n = n0 + (tid & 31);
+    const bool nok = n < n_end;
+    const int b = nok ? n / L : 0, t = nok ? n - b * L : 0;
+    const float* gp = g + (size_t)b * H * L + t;
+#pragma unroll
+    for (int j = 0; j < HPT; ++j) {
+      const int h = HPT * (tid >> 5) + j;
+      gr[j] = (nok && h < H) ? gp[(size_t)h * L] : 0.0f;
+    }
+  };
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int q = 0; q < XV; ++q) {
+      const int idx = tid + kProjThreads * q;
+      if constexpr (kBf16) {
+        const int row = idx >> 4, c = idx & 15;
+        *reinterpret_cast<bf16x8*>(sm.x_hi + row * kProjMBlock + swz_chunk<kProjMBlock>(row, c) * 8) =
+            xr[q];
+      } else {
+        const int row = idx >> 5, c4 = idx & 31;
+        bf16x4 hi, lo;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) split_at(xr[q][e], hi, lo, e);
+        const int at = row * kProjMBlock + swz_chunk<kProjMBlock>(row, c4 >> 1) * 8 + 4 * (c4 & 1);
+        *reinterpret_cast<bf16x4*>(sm.x_hi + at) = hi;
+        *reinterpret_cast<bf16x4*>(sm.x_lo + at) = lo;
+      }
+    }
+    bf16 hi[HPT], lo[HPT];
+#pragma unroll
+    for (int j = 0; j < HPT; ++j) split_at(gr[j], hi, lo, j);
+    const int at = (tid & 31) * GS + HPT * (tid >> 5);
+    if constexpr (HB == 1) {
+      *reinterpret_cast<bf16x4*>(sm.g_hi + at) = bf16x4{hi[0], hi[1], hi[2], hi[3]};
+      *reinterpret_cast<bf16x4*>(sm.g_lo + at) = bf16x4{lo[0], lo[1], lo[2], lo[3]};
+    } else {
+      *reinterpret_cast<bf16x8*>(sm.g_hi + at) =
+          bf16x8{hi[0], hi[1], hi[2], hi[3], hi[4], hi[5], hi[6], hi[7]};
+      *reinterpret_cast<bf16x8*>(sm.g_lo + at) =
+          bf16x8{lo[0], lo[1], lo[2], lo[3], lo[4], lo[5], lo[6], lo[7]};
+    }
+  };
+
+  f32x16 acc_dw[HB];
+#pragma unroll
+  for (int hb = 0; hb < HB; ++hb) acc_dw[hb] = f32x16{};
+
+  if (n_begin < n_end) load_tile(n_begin);
+  for (int n0 = n_begin; n0 < n_end; n0 += kProjTile) {
+    store_tile();
+    __syncthreads();
+    if (n0 + kProjTile < n_end) load_tile(n0 + kProjTile);  // in flight during the products
+
+    // dw_f[heads, m] += d_logit^T-tile (heads x tokens) * x-tile (tokens x m)
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const bf16x8 xh = tile_tr_operand<kProjMBlock>(sm.x_hi, xoff, c, wave);
+      bf16x8 xl;
+      if constexpr (!kBf16) xl = tile_tr_operand<kProjMBlock>(sm.x_lo, xoff, c, wave);
+#pragma unroll
+      for (int hb = 0; hb < HB; ++hb) {
+        const int o = c * 16 * GS + 32 * hb;
+        const bf16x8 gh = cat4(lds_read_tr16(sm.g_hi + o + goff[0]),
+                               lds_read_tr16(sm.g_hi + o + goff[1]));
+        const bf16x8 gl = cat4(lds_read_tr16(sm.g_lo + o + goff[0]),
+                               lds_read_tr16(sm.g_lo + o + goff[1]));
+        acc_dw[hb] = mfma32(gh, xh, acc_dw[hb]);
+        acc_dw[hb] = mfma32(gl, xh, acc_dw[hb]);
+        if constexpr (!kBf16) acc_dw[hb] = mfma32(gh, xl, acc_dw[hb]);
+      }
+    }
+
+    // dx^T[m, tokens] = w_f^T (m x heads) * d_logit-tile^T (heads x tokens)
+    if (dx) {
+      f32x16 acc_dx = {};
+#pragma unroll
+      for (int ks = 0; ks < 2 * HB; ++ks) {
+        const int at = col * GS + 16 * ks + 8 * half;
+        const bf16x8 gh = *reinterpret_cast<const bf16x8*>(sm.g_hi + at);
+        const bf16x8 gl = *reinterpret_cast<const bf16x8*>(sm.g_lo + at);
+        acc_dx = mfma32(whi[ks], gh, acc_dx);
+        acc_dx = mfma32(wlo[ks], gh, acc_dx);
+        acc_dx = mfma32(whi[ks], gl, acc_dx);
+      }
+      // lane: token `col`; registers 4q..4q+3: columns 32 wave + 8 q + 4 half + 0..3
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        T* o = sm.out + col * OS + 32 * wave + 8 * q + 4 * half;
+        if constexpr (kBf16) {
+          *reinterpret_cast<bf16x4*>(o) = bf16x4{to_bf16(acc_dx[4 * q]), to_bf16(acc_dx[4 * q + 1]),
+                                                 to_bf16(acc_dx[4 * q + 2]),
+                                                 to_bf16(acc_dx[4 * q + 3])};
+        } else {
+          *reinterpret_cast<f32x4*>(o) =
+              f32x4{acc_dx[4 * q], acc_dx[4 * q + 1], acc_dx[4 * q + 2], acc_dx[4 * q + 3]};
+        }
+      }
+    }
+    __syncthreads();
+    if (dx) {
+#pragma unroll
+      for (int q = 0; q < XV; ++q) {
+        const int idx = tid + kProjThreads * q;
+        const int row = kBf16 ? idx >> 4 : idx >> 5;
+        const int mo = kBf16 ? 8 * (idx & 15) : 4 * (idx & 31);
+        const int n = n0 + row;
+        if (n < n_end && mb0 + mo < M)
+          *reinterpret_cast<XPiece*>(dx + (size_t)n * M + mb0 + mo) =
+              *reinterpret_cast<const XPiece*>(sm.out + row * OS + mo);
+      }
+    }
+  }
+
+  // this chunk's dw_f partial: lane column m_lane, registers: heads 32 hb + row(r)
+  if (m_lane < M) {
+    float* part = dw_part + (size_t)blockIdx.y * H * M + m_lane;
+#pragma unroll
+    for (int hb = 0; hb < HB; ++hb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int h = 32 * hb + mfma_row(r, half);
+        if (h < H) part[(size_t)h * M] = acc_dw[hb][r];
+      }
+  }
+}
+
+// dw_f = sum of the chunk partials (chunk order); db_f[h] = sum over all tokens
+// of d_logit[., h, .] (per-thread strided sums, then a fixed tree).
+__global__ __launch_bounds__(kProjThreads) void gate_proj_reduce_kernel(
+    const float* __restrict__ dw_part, const float* __restrict__ g, float* __restrict__ dw,
+    float* __restrict__ db, int n_chunks, int B, int L, int H, int M, int dw_groups) {
+  const int tid = threadIdx.x;
+  if ((int)blockIdx.x < dw_groups) {
+    const size_t hm4 = (size_t)H * M / 4;
+    const size_t i = (size_t)blockIdx.x * kProjThreads + tid;
+    if (i >= hm4) return;
+    const f32x4* p = reinterpret_cast<const f32x4*>(dw_part) + i;
+    f32x4 s = p[0];
+    for (int ch = 1; ch < n_chunks; ++ch) s += p[(size_t)ch * hm4];
+    reinterpret_cast<f32x4*>(dw)[i] = s;
+    return;
+  }
+  const int h = blockIdx.x - dw_groups;
+  float s = 0.0f;
+  for (int b = 0; b < B; ++b) {
+    const float* row = g + ((size_t)b * H + h) * L;
+    for (int t = tid; t < L; t += kProjThreads) s += row[t];
+  }
+  __shared__ float red[kProjThreads];
+  red[tid] = s;
+  __syncthreads();
+  for (int k = kProjThreads / 2; k > 0; k >>= 1) {
+    if (tid < k) red[tid] += red[tid + k];
+    __syncthreads();
+  }
+  if (tid == 0) db[h] = red[0];
+}
+
+int proj_head_blocks(int H) { return H <= 32 ? 1 : 2; }
+
+}  // namespace
+
+// Tokens per backward chunk: enough chunks for about kProjTargetGroups
+// workgroups, but each chunk at least 256 tokens per 32 heads (so that the
+// partials stay small next to x) and at most 65535 chunks.
+int gate_proj_chunk_tokens(int N, int H, int M) {
+  const long long mblocks = (M + kProjMBlock - 1) / kProjMBlock;
+  const long long chunks = std::max(1LL, (kProjTargetGroups + mblocks - 1) / mblocks);
+  long long ct = (N + chunks - 1) / chunks;
+  ct = std::max(ct, 256LL * proj_head_blocks(H));
+  ct = std::max(ct, ((long long)N + 65534) / 65535);
+  ct = (ct + kProjTile - 1) / kProjTile * kProjTile;
+  return (int)std::min(ct, (long long)(N + kProjTile - 1) / kProjTile * kProjTile);
+}
+
+size_t gate_proj_bwd_workspace_bytes(int N, int H, int M) {
+  const int ct = gate_proj_chunk_tokens(N, H, M);
+  const size_t chunks = (size_t)((N + ct - 1) / ct);
+  return chunks * (size_t)H * (size_t)M * sizeof(float);
+}
+
+hipError_t launch_gate_proj_fwd(bool bf16in, const void* x, const float* w, const float* bias,
+                                float* logit, int N, int L, int H, int M, hipStream_t s) {
+  const dim3 grid((N + kProjFwdTok - 1) / kProjFwdTok);
+  const int hb = proj_head_blocks(H);
+  if (bf16in) {
+    if (hb == 1)
+      gate_proj_fwd_kernel<bf16, 1><<<grid, kProjThreads, 0, s>>>((const bf16*)x, w, bias, logit, N, L, H, M);
+    else
+      gate_proj_fwd_kernel<bf16, 2><<<grid, kProjThreads, 0, s>>>((const bf16*)x, w, bias, logit, N, L, H, M);
+  } else {
+    if (hb == 1)
+      gate_proj_fwd_kernel<float, 1><<<grid, kProjThreads, 0, s>>>((const float*)x, w, bias, logit, N, L, H, M);
+    else
+      gate_proj_fwd_kernel<float, 2><<<grid, kProjThreads, 0, s>>>((const float*)x, w, bias, logit, N, L, H, M);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_gate_proj_bwd(bool bf16in, const void* x, const float* w, const float* d_logit,
+                                void* dx, float* dw, float* db, void* ws, int B, int L, int H,
+                                int M, hipStream_t s) {
+  const int N = B * L;
+  const int ct = gate_proj_chunk_tokens(N, H, M);
+  const int chunks = (N + ct - 1) / ct;
+  float* part = static_cast<float*>(ws);
+  const dim3 grid((M + kProjMBlock - 1) / kProjMBlock, chunks);
+  const int hb = proj_head_blocks(H);
+  if (bf16in) {
+    if (hb == 1)
+      gate_proj_bwd_kernel<bf16, 1><<<grid, kProjThreads, 0, s>>>((const bf16*)x, w, d_logit, (bf16*)dx, part, N, L, H, M, ct);
+    else
+      gate_proj_bwd_kernel<bf16, 2><<<grid, kProjThreads, 0, s>>>((const bf16*)x, w, d_logit, (bf16*)dx, part, N, L, H, M, ct);
+  } else {
+    if (hb == 1)
+      gate_proj_bwd_kernel<float, 1><<<grid, kProjThreads, 0, s>>>((const float*)x, w, d_logit, (float*)dx, part, N, L, H, M, ct);
+    else
+      gate_proj_bwd_kernel<float, 2><<<grid, kProjThreads, 0, s>>>((const float*)x, w, d_logit, (float*)dx, part, N, L, H, M, ct);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int dw_groups = (int)(((size_t)H * M / 4 + kProjThreads - 1) / kProjThreads);
+  gate_proj_reduce_kernel<<<dw_groups + (db ? H : 0), kProjThreads, 0, s>>>(
+      part, d_logit, dw, db, chunks, B, L, H, M, dw_groups);
+  return hipGetLastError();
+}
+
+}  // namespace fox

@@ -160,6 +160,20 @@ def decode_inputs(B: int, H: int, T: int, d: int, dtype: str, gate: Tuple, seed:
     }
 
 
+def projection_inputs(B: int, L: int, H: int, M: int, dtype: str, seed: int,
+                      device="cpu") -> Dict[str, torch.Tensor]:
+    """The forget-gate projection's operands: the layer input x [B,L,M] ~ N(0, 1)
+    in `dtype`; w_f [H,M] ~ N(0, 0.02) (the paper's weight initialisation) and
+    b_f [H] ~ N(0, 1) in fp32; an upstream d_logit [B,H,L] ~ N(0, 1) in fp32."""
+    g = _gen(seed, device)
+    return {
+        "x": randn((B, L, M), dtype, g, device, True),
+        "w_f": 0.02 * torch.randn((H, M), generator=g, device=device, dtype=torch.float32),
+        "b_f": torch.randn((H,), generator=g, device=device, dtype=torch.float32),
+        "d_logit": torch.randn((B, H, L), generator=g, device=device, dtype=torch.float32),
+    }
+
+
 def workload_inputs(w: Workload, device="cpu", seed: int = None) -> Dict[str, torch.Tensor]:
     s = w.seed if seed is None else seed
     if w.kind == "decode":
