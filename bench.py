@@ -52,6 +52,9 @@ KERNEL_SOURCES = {
     "pro_prologue_bwd_kernel": ("pro_fusions.hip", "fox_device.h"),
     "out_gate_kernel": ("pro_fusions.hip", "fox_device.h"),
     "out_gate_bwd_kernel": ("pro_fusions.hip", "fox_device.h"),
+    "gate_proj_fwd_kernel": ("gate_proj.hip", "fox_device.h"),
+    "gate_proj_bwd_kernel": ("gate_proj.hip", "fox_device.h"),
+    "gate_proj_reduce_kernel": ("gate_proj.hip", "fox_device.h"),
 }
 
 
@@ -311,6 +314,41 @@ def bench_fixed(w, steps, warmup, t_min=2.0):
     return res
 
 
+def projection_bytes(B, L, H, M):
+    """Algorithmic HBM bytes of the gate projection with bf16 x: the logits read
+    x and w_f, write the logits; the backward reads x, w_f and d_logit and writes
+    dx, dw_f and db_f (the per-chunk partials are not counted)."""
+    fwd = B * L * M * 2 + H * M * 4 + H * 4 + B * H * L * 4
+    bwd = 2 * B * L * M * 2 + B * H * L * 4 + 2 * H * M * 4 + H * 4
+    return fwd, bwd
+
+
+def bench_projection(w, steps, warmup):
+    """The forget-gate projection at the workload's model width M = H d: logits
+    from x [B, L, M] bf16, then dx, dw_f and db_f."""
+    dev = torch.device("cuda:0")
+    B, H, L, M = w.B, w.H, w.L, w.H * w.d
+    p = inputs.projection_inputs(B, L, H, M, "bf16", 11, device=dev)
+    logit = torch.empty((B, H, L), device=dev)
+    ws = torch.empty(fox.fox_gate_projection_bwd_workspace_bytes(torch.bfloat16, B, L, H, M),
+                     device=dev, dtype=torch.uint8)
+    tf, tb = EventTimer(), EventTimer()
+
+    def once(timed):
+        with tf.maybe(timed):
+            fox.fox_gate_projection(p["x"], p["w_f"], p["b_f"], logit)
+        with tb.maybe(timed):
+            fox.fox_gate_projection_bwd(p["x"], p["w_f"], p["d_logit"], workspace=ws)
+
+    for _ in range(warmup):
+        once(False)
+    torch.cuda.synchronize()
+    for _ in range(steps):
+        once(True)
+    torch.cuda.synchronize()
+    return {"B": B, "L": L, "H": H, "M": M, "fwd_ms": tf.mean_ms(), "bwd_ms": tb.mean_ms()}
+
+
 def bench_decode(w, steps, warmup):
     dev = torch.device("cuda:0")
     y = inputs.workload_inputs(w, device=dev)
@@ -483,7 +521,10 @@ KV_STORE_KERNEL = "bwd_dkdv_bf16_kernel<128,false,false,true>"
 KV_KERNEL = "bwd_dkdv_bf16_kernel<128,false,false,false>"
 DQ_STORED_KERNEL = "bwd_dq_stored_kernel<128,false>"
 DECODE_KERNEL = "decode_split_kernel<__bf16,128,false,false>"
-ROOFLINE_KERNELS = (KV_STORE_KERNEL, KV_KERNEL, DQ_STORED_KERNEL, DECODE_KERNEL)
+PROJ_FWD_KERNEL = "gate_proj_fwd_kernel<true,1>"
+PROJ_BWD_KERNEL = "gate_proj_bwd_kernel<true,1>"
+ROOFLINE_KERNELS = (KV_STORE_KERNEL, KV_KERNEL, DQ_STORED_KERNEL, DECODE_KERNEL, PROJ_FWD_KERNEL,
+                    PROJ_BWD_KERNEL)
 
 SQ_KERNELS = ("fwd_bf16_kernel<128,false,false,false>",
               "bwd_dkdv_bf16_kernel<128,false,false,false>",
@@ -556,6 +597,8 @@ def main():
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-pro", action="store_true", help="skip the FoX (Pro) layer timings")
     ap.add_argument("--no-fixed", action="store_true", help="skip the fixed-gate timings")
+    ap.add_argument("--no-projection", action="store_true",
+                    help="skip the forget-gate projection timings")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="run a plain device copy of this size first (counter calibration)")
@@ -743,6 +786,26 @@ def main():
                                                                  / 1e9, 1)}}
         log(f"[bench] decode {rd['ms']:.3f} ms -> {gbs:.0f} GB/s; with skipping "
             f"{rd['skip_ms']:.3f} ms")
+    if not args.no_projection:
+        rj = bench_projection(w, max(args.steps, 20), args.warmup)
+        fb, bb = projection_bytes(rj["B"], rj["L"], rj["H"], rj["M"])
+        legs = {}
+        for leg, ms, byt, kern, what in (
+                ("fwd", rj["fwd_ms"], fb, PROJ_FWD_KERNEL, "gate_proj_fwd_kernel"),
+                ("bwd", rj["bwd_ms"], bb, PROJ_BWD_KERNEL,
+                 "gate_proj_bwd_kernel + gate_proj_reduce_kernel")):
+            gbs = byt / (ms * 1e-3) / 1e9
+            legs[leg] = {"ms": round(ms, 5), "bytes": byt,
+                         "roofline": {"bound": "hbm", "kernel": what, "achieved": round(gbs, 1),
+                                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                      "frac": round(gbs / HBM_PEAK_GBS, 4),
+                                      "traffic": measured_traffic(kern)}}
+        out["gate_projection"] = {
+            "what": "forget-gate logits w_f^T x_t + b_f per head and their backward (dx, dw_f, "
+                    "db_f), x bf16 [B, L, H*d]",
+            "config": {"B": rj["B"], "L": rj["L"], "H": rj["H"], "M": rj["M"]}, **legs}
+        log(f"[bench] gate projection fwd {rj['fwd_ms'] * 1e3:.1f} us, bwd "
+            f"{rj['bwd_ms'] * 1e3:.1f} us")
     if not args.no_cpu_baseline:
         log("[bench] timing the fp64 oracle on the host")
         out["cpu_baseline"] = cpu_baseline(w)

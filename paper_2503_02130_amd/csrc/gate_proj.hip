@@ -17,18 +17,20 @@
 // every MFMA product of two bf16 is exact in the fp32 accumulator.
 //
 //   * Logits: a workgroup owns 64 tokens (two 32-token MFMA columns) and its
-//     four waves split the contraction over M in 16-wide steps, four steps'
-//     loads in flight at once; x fragments come straight from HBM (8
-//     contiguous elements per lane), w_f fragments from L2.  The waves' partial
+//     eight waves split the contraction over M in 16-wide steps, four steps'
+//     loads in flight per wave; x fragments come straight from HBM (8
+//     contiguous elements per lane; four waves' steps cover a 128-byte line of
+//     each row), w_f fragments from L2.  The waves' partial
 //     sums meet in LDS.
 //   * Backward: a workgroup owns a 128-column block of M and a chunk of tokens,
-//     32 tokens at a time.  x and d_logit tiles go to LDS (split to bf16
+//     32 tokens at a time, the loads of the next two sub-tiles in flight (two
+//     register slots).  x and d_logit tiles go to LDS (split to bf16
 //     hi/lo); dw_f's product contracts over tokens, so both of its operands
 //     are transposing reads (ds_read_b64_tr_b16) of those tiles.  dx^T = w_f^T
 //     d_logit is one MFMA column per token, written through LDS so that dx rows
-//     leave in 16-byte pieces.  Each chunk writes its dw_f partial; a second
-//     kernel sums the partials in a fixed order and computes db_f (so the
-//     result is deterministic).
+//     leave in 16-byte pieces.  Each chunk writes its dw_f and db_f partials
+//     (the column-block-0 workgroups sum d_logit over their tokens); a second
+//     kernel sums the partials in a fixed order, so results are deterministic.
 #include <algorithm>
 
 #include "fox_device.h"
@@ -36,10 +38,9 @@
 
 namespace fox {
 
-namespace {
-
 constexpr int kProjThreads = 256;  // four waves
 constexpr int kProjFwdTok = 64;    // tokens per forward workgroup
+constexpr int kProjFwdWaves = 8;   // waves per forward workgroup (each takes every 8th step)
 constexpr int kProjFwdAhead = 4;   // contraction steps whose loads are in flight together
 constexpr int kProjMBlock = 128;   // columns of M per backward workgroup
 constexpr int kProjTile = 32;      // tokens per backward sub-tile
@@ -70,14 +71,20 @@ __device__ __forceinline__ void load8<float>(const float* p, bool ok, float (&v)
   }
 }
 
+// Storage type of x and dx: bf16 or fp32 (a bool template argument, so that
+// profiler names read gate_proj_*_kernel<true, 1>).
+template <bool BF16>
+using proj_t = typename std::conditional<BF16, bf16, float>::type;
+
 // ---------------------------------------------------------------------------
 // Logits.
 // ---------------------------------------------------------------------------
-template <typename T, int HB>
-__global__ __launch_bounds__(kProjThreads) void gate_proj_fwd_kernel(
-    const T* __restrict__ x, const float* __restrict__ w, const float* __restrict__ bias,
+template <bool BF16, int HB>
+__global__ __launch_bounds__(kProjFwdWaves * 64) void gate_proj_fwd_kernel(
+    const proj_t<BF16>* __restrict__ x, const float* __restrict__ w, const float* __restrict__ bias,
     float* __restrict__ logit, int N, int L, int H, int M) {
-  constexpr bool kBf16 = sizeof(T) == 2;
+  using T = proj_t<BF16>;
+  constexpr bool kBf16 = BF16;
   constexpr int TB = kProjFwdTok / 32;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int col = lane & 31, half = lane >> 5;
@@ -107,15 +114,15 @@ __global__ __launch_bounds__(kProjThreads) void gate_proj_fwd_kernel(
 #pragma unroll
     for (int hb = 0; hb < HB; ++hb) acc[tb][hb] = f32x16{};
 
-  for (int s0 = wave; s0 < steps; s0 += 4 * kProjFwdAhead) {
-    // this wave's steps s0, s0 + 4, ...: all loads first, then the products
+  for (int s0 = wave; s0 < steps; s0 += kProjFwdWaves * kProjFwdAhead) {
+    // this wave's steps s0, s0 + kProjFwdWaves, ...: all loads first, then the products
     float wv[kProjFwdAhead][HB][8];
     bf16x8 xb[kProjFwdAhead][TB];
     float xv[kBf16 ? 1 : kProjFwdAhead][TB][8];
 #pragma unroll
     for (int u = 0; u < kProjFwdAhead; ++u) {
-      const int m = 16 * (s0 + 4 * u);
-      const bool mok = s0 + 4 * u < steps && m + 8 * half < M;
+      const int m = 16 * (s0 + kProjFwdWaves * u);
+      const bool mok = s0 + kProjFwdWaves * u < steps && m + 8 * half < M;
 #pragma unroll
       for (int hb = 0; hb < HB; ++hb) load8<float>(wrow[hb] + m, wok[hb] && mok, wv[u][hb]);
 #pragma unroll
@@ -155,9 +162,9 @@ __global__ __launch_bounds__(kProjThreads) void gate_proj_fwd_kernel(
     }
   }
 
-  // The four waves' partial sums: entry ((tb * HB + hb) * 16 + r) * 64 + lane.
+  // The waves' partial sums: entry ((tb * HB + hb) * 16 + r) * 64 + lane.
   constexpr int kEntries = TB * HB * 16 * 64;
-  __shared__ float red[4][kEntries];
+  __shared__ float red[kProjFwdWaves][kEntries];
 #pragma unroll
   for (int tb = 0; tb < TB; ++tb)
 #pragma unroll
@@ -166,14 +173,16 @@ __global__ __launch_bounds__(kProjThreads) void gate_proj_fwd_kernel(
       for (int r = 0; r < 16; ++r) red[wave][((tb * HB + hb) * 16 + r) * 64 + lane] = acc[tb][hb][r];
   __syncthreads();
 #pragma unroll
-  for (int k = 0; k < kEntries / kProjThreads; ++k) {
-    const int e = tid + kProjThreads * k;
+  for (int k = 0; k < kEntries / (kProjFwdWaves * 64); ++k) {
+    const int e = tid + kProjFwdWaves * 64 * k;
     const int r = (e >> 6) & 15, blk = e >> 10;
     const int tb = blk / HB, hb = blk % HB;
     const int head = 32 * hb + mfma_row(r, half);
     const int n = n0 + 32 * tb + col;
     if (head < H && n < N) {
-      float v = red[0][e] + red[1][e] + red[2][e] + red[3][e];
+      float v = 0.0f;
+#pragma unroll
+      for (int wv = 0; wv < kProjFwdWaves; ++wv) v += red[wv][e];
       if (bias) v += bias[head];
       const int b = n / L, t = n - b * L;
       logit[((size_t)b * H + head) * L + t] = v;
@@ -195,11 +204,13 @@ struct ProjBwdSmem {
   alignas(16) T out[kProjTile * OS];               // dx rows of the sub-tile
 };
 
-template <typename T, int HB>
+template <bool BF16, int HB>
 __global__ __launch_bounds__(kProjThreads) void gate_proj_bwd_kernel(
-    const T* __restrict__ x, const float* __restrict__ w, const float* __restrict__ g,
-    T* __restrict__ dx, float* __restrict__ dw_part, int N, int L, int H, int M, int CT) {
-  constexpr bool kBf16 = sizeof(T) == 2;
+    const proj_t<BF16>* __restrict__ x, const float* __restrict__ w, const float* __restrict__ g,
+    proj_t<BF16>* __restrict__ dx, float* __restrict__ dw_part, float* __restrict__ db_part, int N, int L,
+    int H, int M, int CT) {
+  using T = proj_t<BF16>;
+  constexpr bool kBf16 = BF16;
   using S = ProjBwdSmem<T, HB>;
   constexpr int GS = S::GS, OS = S::OS;
   constexpr int HPT = 4 * HB;                              // heads staged per thread
@@ -234,19 +245,23 @@ __global__ __launch_bounds__(kProjThreads) void gate_proj_bwd_kernel(
       goff[k2] = (8 * k2 + 4 * (g16 >> 1) + (j16 >> 2)) * GS + 16 * (g16 & 1) + 4 * (j16 & 3);
   }
 
-  // staging registers for one sub-tile
+  float db_acc[HPT];  // this thread's tokens' sum of d_logit for heads HPT (tid / 32) + j
+#pragma unroll
+  for (int j = 0; j < HPT; ++j) db_acc[j] = 0.0f;
+
+  // staging registers: two slots, one sub-tile each
   typedef typename std::conditional<kBf16, bf16x8, f32x4>::type XPiece;
-  XPiece xr[XV];
-  float gr[HPT];
-  auto load_tile = [&](int n0) {
+  XPiece xr[2][XV];
+  float gr[2][HPT];
+  auto load_tile = [&](auto slot, int n0) {
 #pragma unroll
     for (int q = 0; q < XV; ++q) {
       const int idx = tid + kProjThreads * q;
       const int row = kBf16 ? idx >> 4 : idx >> 5;
       const int m = mb0 + (kBf16 ? 8 * (idx & 15) : 4 * (idx & 31));
       const int n = n0 + row;
-      xr[q] = XPiece{};
-      if (n < n_end && m < M) xr[q] = *reinterpret_cast<const XPiece*>(x + (size_t)n * M + m);
+      xr[slot][q] = XPiece{};
+      if (n < n_end && m < M) xr[slot][q] = *reinterpret_cast<const XPiece*>(x + (size_t)n * M + m);
     }
     const int n = n0 + (tid & 31);
     const bool nok = n < n_end;
@@ -255,22 +270,22 @@ __global__ __launch_bounds__(kProjThreads) void gate_proj_bwd_kernel(
 #pragma unroll
     for (int j = 0; j < HPT; ++j) {
       const int h = HPT * (tid >> 5) + j;
-      gr[j] = (nok && h < H) ? gp[(size_t)h * L] : 0.0f;
+      gr[slot][j] = (nok && h < H) ? gp[(size_t)h * L] : 0.0f;
     }
   };
-  auto store_tile = [&]() {
+  auto store_tile = [&](auto slot) {
 #pragma unroll
     for (int q = 0; q < XV; ++q) {
       const int idx = tid + kProjThreads * q;
       if constexpr (kBf16) {
         const int row = idx >> 4, c = idx & 15;
         *reinterpret_cast<bf16x8*>(sm.x_hi + row * kProjMBlock + swz_chunk<kProjMBlock>(row, c) * 8) =
-            xr[q];
+            xr[slot][q];
       } else {
         const int row = idx >> 5, c4 = idx & 31;
         bf16x4 hi, lo;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) split_at(xr[q][e], hi, lo, e);
+        for (int e = 0; e < 4; ++e) split_at(xr[slot][q][e], hi, lo, e);
         const int at = row * kProjMBlock + swz_chunk<kProjMBlock>(row, c4 >> 1) * 8 + 4 * (c4 & 1);
         *reinterpret_cast<bf16x4*>(sm.x_hi + at) = hi;
         *reinterpret_cast<bf16x4*>(sm.x_lo + at) = lo;
@@ -278,7 +293,10 @@ __global__ __launch_bounds__(kProjThreads) void gate_proj_bwd_kernel(
     }
     bf16 hi[HPT], lo[HPT];
 #pragma unroll
-    for (int j = 0; j < HPT; ++j) split_at(gr[j], hi, lo, j);
+    for (int j = 0; j < HPT; ++j) {
+      split_at(gr[slot][j], hi, lo, j);
+      db_acc[j] += gr[slot][j];
+    }
     const int at = (tid & 31) * GS + HPT * (tid >> 5);
     if constexpr (HB == 1) {
       *reinterpret_cast<bf16x4*>(sm.g_hi + at) = bf16x4{hi[0], hi[1], hi[2], hi[3]};
@@ -295,11 +313,11 @@ __global__ __launch_bounds__(kProjThreads) void gate_proj_bwd_kernel(
 #pragma unroll
   for (int hb = 0; hb < HB; ++hb) acc_dw[hb] = f32x16{};
 
-  if (n_begin < n_end) load_tile(n_begin);
-  for (int n0 = n_begin; n0 < n_end; n0 += kProjTile) {
-    store_tile();
+  auto sub_tile = [&](auto slot, int n0) {
+    store_tile(slot);
     __syncthreads();
-    if (n0 + kProjTile < n_end) load_tile(n0 + kProjTile);  // in flight during the products
+    // the sub-tile after next reuses this slot; in flight during two sub-tiles' products
+    if (n0 + 2 * kProjTile < n_end) load_tile(slot, n0 + 2 * kProjTile);
 
     // dw_f[heads, m] += d_logit^T-tile (heads x tokens) * x-tile (tokens x m)
 #pragma unroll
@@ -325,6 +343,7 @@ __global__ __launch_bounds__(kProjThreads) void gate_proj_bwd_kernel(
       f32x16 acc_dx = {};
 #pragma unroll
       for (int ks = 0; ks < 2 * HB; ++ks) {
+        if (16 * ks >= H) break;  // all-zero head slice
         const int at = col * GS + 16 * ks + 8 * half;
         const bf16x8 gh = *reinterpret_cast<const bf16x8*>(sm.g_hi + at);
         const bf16x8 gl = *reinterpret_cast<const bf16x8*>(sm.g_lo + at);
@@ -359,6 +378,24 @@ __global__ __launch_bounds__(kProjThreads) void gate_proj_bwd_kernel(
               *reinterpret_cast<const XPiece*>(sm.out + row * OS + mo);
       }
     }
+  };
+  constexpr std::integral_constant<int, 0> kSlot0{};
+  constexpr std::integral_constant<int, 1> kSlot1{};
+  if (n_begin < n_end) load_tile(kSlot0, n_begin);
+  if (n_begin + kProjTile < n_end) load_tile(kSlot1, n_begin + kProjTile);
+  for (int n0 = n_begin; n0 < n_end; n0 += 2 * kProjTile) {
+    sub_tile(kSlot0, n0);
+    if (n0 + kProjTile < n_end) sub_tile(kSlot1, n0 + kProjTile);
+  }
+
+  // this chunk's db_f partial: the 32 lanes of a half-wave share their heads
+  if (blockIdx.x == 0) {
+#pragma unroll
+    for (int j = 0; j < HPT; ++j) {
+      const float v = row_sum<32>(db_acc[j]);
+      const int h = HPT * (tid >> 5) + j;
+      if ((tid & 31) == 0 && h < H) db_part[(size_t)blockIdx.y * H + h] = v;
+    }
   }
 
   // this chunk's dw_f partial: lane column m_lane, registers: heads 32 hb + row(r)
@@ -374,41 +411,27 @@ __global__ __launch_bounds__(kProjThreads) void gate_proj_bwd_kernel(
   }
 }
 
-// dw_f = sum of the chunk partials (chunk order); db_f[h] = sum over all tokens
-// of d_logit[., h, .] (per-thread strided sums, then a fixed tree).
+// dw_f and db_f: the sums of the chunk partials, in chunk order (one thread per
+// element; the unrolled loop issues its loads ahead of the ordered adds).
 __global__ __launch_bounds__(kProjThreads) void gate_proj_reduce_kernel(
-    const float* __restrict__ dw_part, const float* __restrict__ g, float* __restrict__ dw,
-    float* __restrict__ db, int n_chunks, int B, int L, int H, int M, int dw_groups) {
-  const int tid = threadIdx.x;
-  if ((int)blockIdx.x < dw_groups) {
-    const size_t hm4 = (size_t)H * M / 4;
-    const size_t i = (size_t)blockIdx.x * kProjThreads + tid;
-    if (i >= hm4) return;
-    const f32x4* p = reinterpret_cast<const f32x4*>(dw_part) + i;
-    f32x4 s = p[0];
-    for (int ch = 1; ch < n_chunks; ++ch) s += p[(size_t)ch * hm4];
-    reinterpret_cast<f32x4*>(dw)[i] = s;
-    return;
+    const float* __restrict__ dw_part, const float* __restrict__ db_part, float* __restrict__ dw,
+    float* __restrict__ db, int n_chunks, int H, int M) {
+  const size_t hm = (size_t)H * M;
+  const size_t i = (size_t)blockIdx.x * kProjThreads + threadIdx.x;
+  if (i < hm) {
+    float s = 0.0f;
+#pragma unroll 16
+    for (int ch = 0; ch < n_chunks; ++ch) s += dw_part[(size_t)ch * hm + i];
+    dw[i] = s;
+  } else if (db && i < hm + H) {
+    const int h = (int)(i - hm);
+    float s = 0.0f;
+    for (int ch = 0; ch < n_chunks; ++ch) s += db_part[(size_t)ch * H + h];
+    db[h] = s;
   }
-  const int h = blockIdx.x - dw_groups;
-  float s = 0.0f;
-  for (int b = 0; b < B; ++b) {
-    const float* row = g + ((size_t)b * H + h) * L;
-    for (int t = tid; t < L; t += kProjThreads) s += row[t];
-  }
-  __shared__ float red[kProjThreads];
-  red[tid] = s;
-  __syncthreads();
-  for (int k = kProjThreads / 2; k > 0; k >>= 1) {
-    if (tid < k) red[tid] += red[tid + k];
-    __syncthreads();
-  }
-  if (tid == 0) db[h] = red[0];
 }
 
 int proj_head_blocks(int H) { return H <= 32 ? 1 : 2; }
-
-}  // namespace
 
 // Tokens per backward chunk: enough chunks for about kProjTargetGroups
 // workgroups, but each chunk at least 256 tokens per 32 heads (so that the
@@ -423,10 +446,11 @@ int gate_proj_chunk_tokens(int N, int H, int M) {
   return (int)std::min(ct, (long long)(N + kProjTile - 1) / kProjTile * kProjTile);
 }
 
+// dw_f partials [chunks, H, M], then db_f partials [chunks, H].
 size_t gate_proj_bwd_workspace_bytes(int N, int H, int M) {
   const int ct = gate_proj_chunk_tokens(N, H, M);
   const size_t chunks = (size_t)((N + ct - 1) / ct);
-  return chunks * (size_t)H * (size_t)M * sizeof(float);
+  return chunks * (size_t)H * ((size_t)M + 1) * sizeof(float);
 }
 
 hipError_t launch_gate_proj_fwd(bool bf16in, const void* x, const float* w, const float* bias,
@@ -435,14 +459,14 @@ hipError_t launch_gate_proj_fwd(bool bf16in, const void* x, const float* w, cons
   const int hb = proj_head_blocks(H);
   if (bf16in) {
     if (hb == 1)
-      gate_proj_fwd_kernel<bf16, 1><<<grid, kProjThreads, 0, s>>>((const bf16*)x, w, bias, logit, N, L, H, M);
+      gate_proj_fwd_kernel<true, 1><<<grid, kProjFwdWaves * 64, 0, s>>>((const bf16*)x, w, bias, logit, N, L, H, M);
     else
-      gate_proj_fwd_kernel<bf16, 2><<<grid, kProjThreads, 0, s>>>((const bf16*)x, w, bias, logit, N, L, H, M);
+      gate_proj_fwd_kernel<true, 2><<<grid, kProjFwdWaves * 64, 0, s>>>((const bf16*)x, w, bias, logit, N, L, H, M);
   } else {
     if (hb == 1)
-      gate_proj_fwd_kernel<float, 1><<<grid, kProjThreads, 0, s>>>((const float*)x, w, bias, logit, N, L, H, M);
+      gate_proj_fwd_kernel<false, 1><<<grid, kProjFwdWaves * 64, 0, s>>>((const float*)x, w, bias, logit, N, L, H, M);
     else
-      gate_proj_fwd_kernel<float, 2><<<grid, kProjThreads, 0, s>>>((const float*)x, w, bias, logit, N, L, H, M);
+      gate_proj_fwd_kernel<false, 2><<<grid, kProjFwdWaves * 64, 0, s>>>((const float*)x, w, bias, logit, N, L, H, M);
   }
   return hipGetLastError();
 }
@@ -454,24 +478,25 @@ hipError_t launch_gate_proj_bwd(bool bf16in, const void* x, const float* w, cons
   const int ct = gate_proj_chunk_tokens(N, H, M);
   const int chunks = (N + ct - 1) / ct;
   float* part = static_cast<float*>(ws);
+  float* dbp = part + (size_t)chunks * H * M;
   const dim3 grid((M + kProjMBlock - 1) / kProjMBlock, chunks);
   const int hb = proj_head_blocks(H);
   if (bf16in) {
     if (hb == 1)
-      gate_proj_bwd_kernel<bf16, 1><<<grid, kProjThreads, 0, s>>>((const bf16*)x, w, d_logit, (bf16*)dx, part, N, L, H, M, ct);
+      gate_proj_bwd_kernel<true, 1><<<grid, kProjThreads, 0, s>>>((const bf16*)x, w, d_logit, (bf16*)dx, part, dbp, N, L, H, M, ct);
     else
-      gate_proj_bwd_kernel<bf16, 2><<<grid, kProjThreads, 0, s>>>((const bf16*)x, w, d_logit, (bf16*)dx, part, N, L, H, M, ct);
+      gate_proj_bwd_kernel<true, 2><<<grid, kProjThreads, 0, s>>>((const bf16*)x, w, d_logit, (bf16*)dx, part, dbp, N, L, H, M, ct);
   } else {
     if (hb == 1)
-      gate_proj_bwd_kernel<float, 1><<<grid, kProjThreads, 0, s>>>((const float*)x, w, d_logit, (float*)dx, part, N, L, H, M, ct);
+      gate_proj_bwd_kernel<false, 1><<<grid, kProjThreads, 0, s>>>((const float*)x, w, d_logit, (float*)dx, part, dbp, N, L, H, M, ct);
     else
-      gate_proj_bwd_kernel<float, 2><<<grid, kProjThreads, 0, s>>>((const float*)x, w, d_logit, (float*)dx, part, N, L, H, M, ct);
+      gate_proj_bwd_kernel<false, 2><<<grid, kProjThreads, 0, s>>>((const float*)x, w, d_logit, (float*)dx, part, dbp, N, L, H, M, ct);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int dw_groups = (int)(((size_t)H * M / 4 + kProjThreads - 1) / kProjThreads);
-  gate_proj_reduce_kernel<<<dw_groups + (db ? H : 0), kProjThreads, 0, s>>>(
-      part, d_logit, dw, db, chunks, B, L, H, M, dw_groups);
+  const size_t n_out = (size_t)H * M + (db ? H : 0);
+  gate_proj_reduce_kernel<<<(unsigned)((n_out + kProjThreads - 1) / kProjThreads), kProjThreads, 0,
+                            s>>>(part, dbp, dw, db, chunks, H, M);
   return hipGetLastError();
 }
 

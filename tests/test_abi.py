@@ -82,16 +82,16 @@ def test_gate_projection_validation(lib):
     assert fwd(1, c(P16 + 4), c(P16), None, c(P16), 1, 4, 2, 64, None) == 4
     ws = lib.fox_gate_projection_bwd_workspace_bytes
     assert ws(1, 1, 4, 65, 64) == 0 and ws(1, 1, 4, 2, 60) == 0
-    # one chunk of 256-token granularity: chunks * H * M * 4 bytes
-    assert ws(1, 1, 4, 2, 64) == 1 * 2 * 64 * 4
-    assert ws(1, 2, 16384, 16, 2048) == 64 * 16 * 2048 * 4
-    assert ws(0, 8, 2048, 12, 768) == 64 * 12 * 768 * 4
+    # per chunk of tokens (at least 256 per 32 heads): dw_f and db_f partials, chunks * H * (M + 1) * 4
+    assert ws(1, 1, 4, 2, 64) == 1 * 2 * 65 * 4
+    assert ws(1, 2, 16384, 16, 2048) == 64 * 16 * 2049 * 4
+    assert ws(0, 8, 2048, 12, 768) == 64 * 12 * 769 * 4
     bwd = lib.fox_gate_projection_bwd
     args = lambda wsp, wsb, dw=c(P16): (1, c(P16), c(P16), c(P16), None, dw, None, wsp, wsb,
                                         1, 4, 2, 64, None)
     assert bwd(*args(c(P16), 1 << 20, dw=None)) == 1
     assert bwd(*args(None, 1 << 20)) == 5
-    assert bwd(*args(c(P16), 2 * 64 * 4 - 1)) == 5
+    assert bwd(*args(c(P16), 2 * 65 * 4 - 1)) == 5
     assert bwd(*args(c(P16 + 8), 1 << 20)) == 4
 
 
