@@ -26,10 +26,12 @@ from ._lib import (  # noqa: F401
     EXPORTED,
 )
 
-from .autograd import ForgettingAttention, forgetting_attention  # noqa: E402,F401
+from .autograd import (  # noqa: E402,F401
+    ForgettingAttention, GateProjection, forget_gate_logits, forgetting_attention,
+)
 
 __all__ = [
-    "ForgettingAttention", "forgetting_attention",
+    "ForgettingAttention", "forgetting_attention", "GateProjection", "forget_gate_logits",
     "FoxError", "default_scale", "load", "status_string",
     "fox_gate_prefix", "fox_attn_fwd", "fox_attn_bwd", "fox_attn_bwd_workspace_bytes",
     "fox_attn_bwd_delta", "fox_attn_bwd_dkdv", "fox_attn_bwd_dq", "fox_dlogf_from_dc",

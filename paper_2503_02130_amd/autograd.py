@@ -3,8 +3,10 @@
 Glue only: the forward runs fox_gate_prefix and fox_attn_fwd, the backward the
 staged backward (recomputing, or keeping dS when asked and the dtype is bf16)
 and fox_dlogit_from_dc, which returns the gradient of the gate logits through
-log f = logsigmoid(logit) and c = cumsum(log f) (Sec. 3).  Every step runs in
-the library's kernels.
+log f = logsigmoid(logit) and c = cumsum(log f) (Sec. 3).  GateProjection
+gives the logits themselves from the layer input, w_f^T x_t + b_f per head,
+with fox_gate_projection and fox_gate_projection_bwd.  Every step runs in the
+library's kernels.
 """
 from __future__ import annotations
 
@@ -60,3 +62,32 @@ def forgetting_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
     """
     s = fox.default_scale(q.shape[-1]) if scale is None else float(scale)
     return ForgettingAttention.apply(q, k, v, gate_logit, s, keep_ds)
+
+
+class GateProjection(torch.autograd.Function):
+    """gate_logit[b, h, t] = w_f[h] . x[b, t] + b_f[h] (Sec. 3, gate definition)."""
+
+    @staticmethod
+    def forward(ctx, x, w_f, b_f):
+        x, w_f = x.contiguous(), w_f.contiguous()
+        b = None if b_f is None else b_f.contiguous()
+        logit = fox.fox_gate_projection(x, w_f, b)
+        ctx.save_for_backward(x, w_f)
+        ctx.has_bias = b_f is not None
+        return logit
+
+    @staticmethod
+    def backward(ctx, d_logit):
+        x, w_f = ctx.saved_tensors
+        dx, dw, db = fox.fox_gate_projection_bwd(x, w_f, d_logit.contiguous(),
+                                                 want_dx=ctx.needs_input_grad[0],
+                                                 want_db=ctx.has_bias)
+        return dx, dw, db
+
+
+def forget_gate_logits(x: torch.Tensor, w_f: torch.Tensor,
+                       b_f: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """The forget-gate logits [B, H, L] fp32 from the layer input x [B, L, M]
+    (bf16 or fp32, M % 8 == 0), w_f [H, M] and b_f [H] fp32 (H <= 64), with
+    autograd support; feed them to forgetting_attention."""
+    return GateProjection.apply(x, w_f, b_f)

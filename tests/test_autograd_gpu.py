@@ -44,3 +44,36 @@ def test_forgetting_attention_autograd(dtype, d, L, keep):
     for name, g, r in zip(("dq", "dk", "dv", "dlogit"), (q.grad, k.grad, v.grad, logit.grad), ref):
         e = _rel_l2(g, r)
         assert e <= lim, f"{name} rel-L2 {e:.3e}"
+
+
+def test_gate_projection_autograd_chain():
+    """Layer input -> gate logits -> Forgetting Attention, all through autograd:
+    the projection's gradients equal the entry point's on the same d_logit bit
+    for bit, and the chain matches the oracle's."""
+    B, H, L, d, M = 2, 3, 200, 64, 96
+    print(f"autograd gate projection chain B={B} H={H} L={L} d={d} M={M}", flush=True)
+    a = inputs.attn_inputs(B, H, L, d, "bf16", ("normal", 2.0, 1.0), 71, device=DEV)
+    p = inputs.projection_inputs(B, L, H, M, "bf16", 72, device=DEV)
+    xin = p["x"].clone().requires_grad_()
+    w = p["w_f"].clone().requires_grad_()
+    b = (p["b_f"] + 2.0).requires_grad_()
+    logit = fox.forget_gate_logits(xin, w, b)
+    logit.retain_grad()
+    o = fox.forgetting_attention(a["q"], a["k"], a["v"], logit)
+    o.backward(a["do"])
+    torch.cuda.synchronize()
+    assert torch.equal(logit.detach(), fox.fox_gate_projection(p["x"], p["w_f"], b.detach()))
+    dx, dw, db = fox.fox_gate_projection_bwd(p["x"], p["w_f"], logit.grad)
+    torch.cuda.synchronize()
+    for name, u, v in (("dx", xin.grad, dx), ("dw", w.grad, dw), ("db", b.grad, db)):
+        assert torch.equal(u, v), name
+    # the oracle's chain: logits, then the logit gradient of the attention, then the projection
+    cpu = lambda t: t.detach().cpu()
+    ref_logit = oracle.gate_projection(cpu(p["x"]), cpu(w), cpu(b))
+    s = fox.default_scale(d)
+    _, _, _, dlogit_ref = oracle.backward_logit(cpu(a["q"]), cpu(a["k"]), cpu(a["v"]), ref_logit,
+                                                cpu(a["do"]), s)
+    rdx, rdw, rdb = oracle.gate_projection_backward(cpu(p["x"]), cpu(w), dlogit_ref)
+    assert _rel_l2(logit, ref_logit) <= 1e-5
+    for name, u, r in (("dx", xin.grad, rdx), ("dw", w.grad, rdw), ("db", b.grad, rdb)):
+        assert _rel_l2(u, r) <= 2e-2, name
