@@ -53,7 +53,8 @@ KERNEL_SOURCES = {
     "out_gate_kernel": ("pro_fusions.hip", "fox_device.h"),
     "out_gate_bwd_kernel": ("pro_fusions.hip", "fox_device.h"),
     "gate_proj_fwd_kernel": ("gate_proj.hip", "fox_device.h"),
-    "gate_proj_bwd_kernel": ("gate_proj.hip", "fox_device.h"),
+    "gate_proj_dw_kernel": ("gate_proj.hip", "fox_device.h"),
+    "gate_proj_dx_kernel": ("gate_proj.hip", "fox_device.h"),
     "gate_proj_reduce_kernel": ("gate_proj.hip", "fox_device.h"),
 }
 
@@ -522,9 +523,10 @@ KV_KERNEL = "bwd_dkdv_bf16_kernel<128,false,false,false>"
 DQ_STORED_KERNEL = "bwd_dq_stored_kernel<128,false>"
 DECODE_KERNEL = "decode_split_kernel<__bf16,128,false,false>"
 PROJ_FWD_KERNEL = "gate_proj_fwd_kernel<true,1>"
-PROJ_BWD_KERNEL = "gate_proj_bwd_kernel<true,1>"
+PROJ_DW_KERNEL = "gate_proj_dw_kernel<true,1>"
+PROJ_DX_KERNEL = "gate_proj_dx_kernel<true,1>"
 ROOFLINE_KERNELS = (KV_STORE_KERNEL, KV_KERNEL, DQ_STORED_KERNEL, DECODE_KERNEL, PROJ_FWD_KERNEL,
-                    PROJ_BWD_KERNEL)
+                    PROJ_DW_KERNEL, PROJ_DX_KERNEL)
 
 SQ_KERNELS = ("fwd_bf16_kernel<128,false,false,false>",
               "bwd_dkdv_bf16_kernel<128,false,false,false>",
@@ -790,16 +792,17 @@ def main():
         rj = bench_projection(w, max(args.steps, 20), args.warmup)
         fb, bb = projection_bytes(rj["B"], rj["L"], rj["H"], rj["M"])
         legs = {}
-        for leg, ms, byt, kern, what in (
-                ("fwd", rj["fwd_ms"], fb, PROJ_FWD_KERNEL, "gate_proj_fwd_kernel"),
-                ("bwd", rj["bwd_ms"], bb, PROJ_BWD_KERNEL,
-                 "gate_proj_bwd_kernel + gate_proj_reduce_kernel")):
+        tdw, tdx = measured_traffic(PROJ_DW_KERNEL), measured_traffic(PROJ_DX_KERNEL)
+        for leg, ms, byt, traffic, what in (
+                ("fwd", rj["fwd_ms"], fb, measured_traffic(PROJ_FWD_KERNEL), "gate_proj_fwd_kernel"),
+                ("bwd", rj["bwd_ms"], bb, None if tdw is None or tdx is None else tdw + tdx,
+                 "gate_proj_dx_kernel + gate_proj_dw_kernel + gate_proj_reduce_kernel")):
             gbs = byt / (ms * 1e-3) / 1e9
             legs[leg] = {"ms": round(ms, 5), "bytes": byt,
                          "roofline": {"bound": "hbm", "kernel": what, "achieved": round(gbs, 1),
                                       "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                       "frac": round(gbs / HBM_PEAK_GBS, 4),
-                                      "traffic": measured_traffic(kern)}}
+                                      "traffic": traffic}}
         out["gate_projection"] = {
             "what": "forget-gate logits w_f^T x_t + b_f per head and their backward (dx, dw_f, "
                     "db_f), x bf16 [B, L, H*d]",

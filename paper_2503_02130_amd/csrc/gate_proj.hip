@@ -16,19 +16,22 @@
 // of exact (exact bf16 operands need only the hi terms of the other side);
 // every MFMA product of two bf16 is exact in the fp32 accumulator.
 //
-//   * Logits: a workgroup owns 64 tokens (two 32-token MFMA columns) and its
-//     eight waves split the contraction over M in 16-wide steps, four steps'
-//     loads in flight per wave; x fragments come straight from HBM (8
-//     contiguous elements per lane; four waves' steps cover a 128-byte line of
-//     each row), w_f fragments from L2.  The waves' partial
-//     sums meet in LDS.
-//   * Backward: a workgroup owns a 128-column block of M and a chunk of tokens,
-//     32 tokens at a time, the loads of the next two sub-tiles in flight (two
-//     register slots).  x and d_logit tiles go to LDS (split to bf16
-//     hi/lo); dw_f's product contracts over tokens, so both of its operands
-//     are transposing reads (ds_read_b64_tr_b16) of those tiles.  dx^T = w_f^T
-//     d_logit is one MFMA column per token, written through LDS so that dx rows
-//     leave in 16-byte pieces.  Each chunk writes its dw_f and db_f partials
+//   * Logits: a workgroup owns 64 tokens (two 32-token MFMA columns) and walks
+//     M in 128-column chunks: x goes to LDS in whole row pieces (16 lanes read
+//     256 contiguous bytes of a row), each wave takes two 16-wide steps of a
+//     chunk with its w_f fragments from L2; both x and w_f are loaded two
+//     chunks ahead into registers.  The four waves' partial sums meet in LDS.
+//   * Backward, two kernels (dx needs no x, and a loop that mixes stores with
+//     its prefetch loads waits for all of them each time on gfx9, whose one
+//     vector-memory counter serves both):
+//     - dw_f: a workgroup owns a 128-column block of M and a chunk of tokens,
+//       32 tokens at a time, the loads of the next two sub-tiles in flight (two
+//       register slots).  x and d_logit tiles go to LDS (split to bf16
+//       hi/lo); the product contracts over tokens, so both of its operands are
+//       transposing reads (ds_read_b64_tr_b16) of those tiles.
+//     - dx^T = w_f^T d_logit: a workgroup stages 128 tokens of d_logit once,
+//       then per 32 tokens one MFMA column per token, written through LDS so
+//       that dx rows leave in 16-byte pieces.  Each chunk writes its dw_f and db_f partials
 //     (the column-block-0 workgroups sum d_logit over their tokens); a second
 //     kernel sums the partials in a fixed order, so results are deterministic.
 #include <algorithm>
@@ -40,8 +43,6 @@ namespace fox {
 
 constexpr int kProjThreads = 256;  // four waves
 constexpr int kProjFwdTok = 64;    // tokens per forward workgroup
-constexpr int kProjFwdWaves = 8;   // waves per forward workgroup (each takes every 8th step)
-constexpr int kProjFwdAhead = 4;   // contraction steps whose loads are in flight together
 constexpr int kProjMBlock = 128;   // columns of M per backward workgroup
 constexpr int kProjTile = 32;      // tokens per backward sub-tile
 constexpr int kProjTargetGroups = 1024;
@@ -80,25 +81,28 @@ using proj_t = typename std::conditional<BF16, bf16, float>::type;
 // Logits.
 // ---------------------------------------------------------------------------
 template <bool BF16, int HB>
-__global__ __launch_bounds__(kProjFwdWaves * 64) void gate_proj_fwd_kernel(
+struct ProjFwdSmem {
+  static constexpr int kTok = kProjFwdTok;
+  alignas(16) bf16 x_hi[2][kTok * kProjMBlock];  // swizzled rows (swz_chunk<128>), two buffers
+  alignas(16) bf16 x_lo[BF16 ? 1 : 2][BF16 ? 8 : kTok * kProjMBlock];
+  alignas(16) float red[4][(kTok / 32) * HB * 16 * 64];
+};
+
+template <bool BF16, int HB>
+__global__ __launch_bounds__(kProjThreads) void gate_proj_fwd_kernel(
     const proj_t<BF16>* __restrict__ x, const float* __restrict__ w, const float* __restrict__ bias,
     float* __restrict__ logit, int N, int L, int H, int M) {
   using T = proj_t<BF16>;
   constexpr bool kBf16 = BF16;
   constexpr int TB = kProjFwdTok / 32;
+  constexpr int XV = kProjFwdTok * kProjMBlock * (int)sizeof(T) / 16 / kProjThreads;  // pieces/thread
+  typedef typename std::conditional<kBf16, bf16x8, f32x4>::type XPiece;
+  __shared__ ProjFwdSmem<BF16, HB> sm;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int col = lane & 31, half = lane >> 5;
   const int n0 = blockIdx.x * kProjFwdTok;
-  const int steps = (M + 15) / 16;
+  const int chunks = (M + kProjMBlock - 1) / kProjMBlock;
 
-  const T* xrow[TB];
-  bool xok[TB];
-#pragma unroll
-  for (int tb = 0; tb < TB; ++tb) {
-    const int n = n0 + 32 * tb + col;
-    xok[tb] = n < N;
-    xrow[tb] = x + (size_t)min(n, N - 1) * M + 8 * half;
-  }
   const float* wrow[HB];
   bool wok[HB];
 #pragma unroll
@@ -108,81 +112,121 @@ __global__ __launch_bounds__(kProjFwdWaves * 64) void gate_proj_fwd_kernel(
     wrow[hb] = w + (size_t)min(h, H - 1) * M + 8 * half;
   }
 
+  // x staging: 16 threads (bf16) or 32 (fp32) read one row's 256 or 512 bytes of
+  // a 128-column chunk; two register slots keep the next two chunks in flight.
+  XPiece xr[2][XV];
+  auto load_chunk = [&](auto slot, int mc) {
+#pragma unroll
+    for (int q = 0; q < XV; ++q) {
+      const int idx = tid + kProjThreads * q;
+      const int row = kBf16 ? idx >> 4 : idx >> 5;
+      const int m = mc + (kBf16 ? 8 * (idx & 15) : 4 * (idx & 31));
+      const int n = n0 + row;
+      xr[slot][q] = XPiece{};
+      if (n < N && m < M) xr[slot][q] = *reinterpret_cast<const XPiece*>(x + (size_t)n * M + m);
+    }
+  };
+  auto store_chunk = [&](auto slot, int buf) {
+#pragma unroll
+    for (int q = 0; q < XV; ++q) {
+      const int idx = tid + kProjThreads * q;
+      if constexpr (kBf16) {
+        const int row = idx >> 4, c = idx & 15;
+        *reinterpret_cast<bf16x8*>(sm.x_hi[buf] + row * kProjMBlock +
+                                   swz_chunk<kProjMBlock>(row, c) * 8) = xr[slot][q];
+      } else {
+        const int row = idx >> 5, c4 = idx & 31;
+        bf16x4 hi, lo;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) split_at(xr[slot][q][e], hi, lo, e);
+        const int at = row * kProjMBlock + swz_chunk<kProjMBlock>(row, c4 >> 1) * 8 + 4 * (c4 & 1);
+        *reinterpret_cast<bf16x4*>(sm.x_hi[buf] + at) = hi;
+        *reinterpret_cast<bf16x4*>(sm.x_lo[buf] + at) = lo;
+      }
+    }
+  };
+
   f32x16 acc[TB][HB];
 #pragma unroll
   for (int tb = 0; tb < TB; ++tb)
 #pragma unroll
     for (int hb = 0; hb < HB; ++hb) acc[tb][hb] = f32x16{};
 
-  for (int s0 = wave; s0 < steps; s0 += kProjFwdWaves * kProjFwdAhead) {
-    // this wave's steps s0, s0 + kProjFwdWaves, ...: all loads first, then the products
-    float wv[kProjFwdAhead][HB][8];
-    bf16x8 xb[kProjFwdAhead][TB];
-    float xv[kBf16 ? 1 : kProjFwdAhead][TB][8];
+  // w_f fragments of a chunk's two steps for this wave (columns 32 wave + 16 i
+  // + 8 half .. +7), loaded two chunks ahead like x
+  float wv[2][2][HB][8];
+  auto load_w = [&](auto slot, int mc) {
 #pragma unroll
-    for (int u = 0; u < kProjFwdAhead; ++u) {
-      const int m = 16 * (s0 + kProjFwdWaves * u);
-      const bool mok = s0 + kProjFwdWaves * u < steps && m + 8 * half < M;
+    for (int i = 0; i < 2; ++i) {
+      const int m = mc + 32 * wave + 16 * i;
 #pragma unroll
-      for (int hb = 0; hb < HB; ++hb) load8<float>(wrow[hb] + m, wok[hb] && mok, wv[u][hb]);
-#pragma unroll
-      for (int tb = 0; tb < TB; ++tb) {
-        if constexpr (kBf16) {
-          xb[u][tb] = bf16x8{};
-          if (xok[tb] && mok) xb[u][tb] = *reinterpret_cast<const bf16x8*>(xrow[tb] + m);
-        } else {
-          load8<float>(reinterpret_cast<const float*>(xrow[tb]) + m, xok[tb] && mok,
-                       xv[u][tb]);
-        }
-      }
+      for (int hb = 0; hb < HB; ++hb)
+        load8<float>(wrow[hb] + m, wok[hb] && m + 8 * half < M, wv[slot][i][hb]);
     }
+  };
+  auto chunk = [&](auto slot, int ci) {
+    const int mc = ci * kProjMBlock;
+    const int buf = ci & 1;
+    store_chunk(slot, buf);
+    __syncthreads();  // chunk ci is in LDS; every wave is done with chunk ci - 2's buffer
+    if (ci + 2 < chunks) load_chunk(slot, mc + 2 * kProjMBlock);
 #pragma unroll
-    for (int u = 0; u < kProjFwdAhead; ++u) {
+    for (int i = 0; i < 2; ++i) {
       bf16x8 whi[HB], wlo[HB];
 #pragma unroll
       for (int hb = 0; hb < HB; ++hb)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) split_at(wv[u][hb][e], whi[hb], wlo[hb], e);
+        for (int e = 0; e < 8; ++e) split_at(wv[slot][i][hb][e], whi[hb], wlo[hb], e);
+      const int c8 = 4 * wave + 2 * i + half;  // this lane's 8-column piece of the chunk
 #pragma unroll
       for (int tb = 0; tb < TB; ++tb) {
-        bf16x8 xhi, xlo;
-        if constexpr (kBf16) {
-          xhi = xb[u][tb];
-        } else {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) split_at(xv[u][tb][e], xhi, xlo, e);
-        }
+        const int row = 32 * tb + col;
+        const int at = row * kProjMBlock + swz_chunk<kProjMBlock>(row, c8) * 8;
+        const bf16x8 xh = *reinterpret_cast<const bf16x8*>(sm.x_hi[buf] + at);
+        bf16x8 xl;
+        if constexpr (!kBf16) xl = *reinterpret_cast<const bf16x8*>(sm.x_lo[buf] + at);
 #pragma unroll
         for (int hb = 0; hb < HB; ++hb) {
-          acc[tb][hb] = mfma32(whi[hb], xhi, acc[tb][hb]);
-          acc[tb][hb] = mfma32(wlo[hb], xhi, acc[tb][hb]);
-          if constexpr (!kBf16) acc[tb][hb] = mfma32(whi[hb], xlo, acc[tb][hb]);
+          acc[tb][hb] = mfma32(whi[hb], xh, acc[tb][hb]);
+          acc[tb][hb] = mfma32(wlo[hb], xh, acc[tb][hb]);
+          if constexpr (!kBf16) acc[tb][hb] = mfma32(whi[hb], xl, acc[tb][hb]);
         }
       }
     }
+    if (ci + 2 < chunks) load_w(slot, mc + 2 * kProjMBlock);
+  };
+  constexpr std::integral_constant<int, 0> kSlot0{};
+  constexpr std::integral_constant<int, 1> kSlot1{};
+  load_chunk(kSlot0, 0);
+  load_w(kSlot0, 0);
+  if (1 < chunks) {
+    load_chunk(kSlot1, kProjMBlock);
+    load_w(kSlot1, kProjMBlock);
+  }
+  for (int ci = 0; ci < chunks; ci += 2) {
+    chunk(kSlot0, ci);
+    if (ci + 1 < chunks) chunk(kSlot1, ci + 1);
   }
 
-  // The waves' partial sums: entry ((tb * HB + hb) * 16 + r) * 64 + lane.
+  // The four waves' partial sums: entry ((tb * HB + hb) * 16 + r) * 64 + lane.
   constexpr int kEntries = TB * HB * 16 * 64;
-  __shared__ float red[kProjFwdWaves][kEntries];
 #pragma unroll
   for (int tb = 0; tb < TB; ++tb)
 #pragma unroll
     for (int hb = 0; hb < HB; ++hb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) red[wave][((tb * HB + hb) * 16 + r) * 64 + lane] = acc[tb][hb][r];
+      for (int r = 0; r < 16; ++r)
+        sm.red[wave][((tb * HB + hb) * 16 + r) * 64 + lane] = acc[tb][hb][r];
   __syncthreads();
 #pragma unroll
-  for (int k = 0; k < kEntries / (kProjFwdWaves * 64); ++k) {
-    const int e = tid + kProjFwdWaves * 64 * k;
+  for (int k = 0; k < kEntries / kProjThreads; ++k) {
+    const int e = tid + kProjThreads * k;
     const int r = (e >> 6) & 15, blk = e >> 10;
     const int tb = blk / HB, hb = blk % HB;
     const int head = 32 * hb + mfma_row(r, half);
     const int n = n0 + 32 * tb + col;
     if (head < H && n < N) {
-      float v = 0.0f;
-#pragma unroll
-      for (int wv = 0; wv < kProjFwdWaves; ++wv) v += red[wv][e];
+      float v = sm.red[0][e] + sm.red[1][e] + sm.red[2][e] + sm.red[3][e];
       if (bias) v += bias[head];
       const int b = n / L, t = n - b * L;
       logit[((size_t)b * H + head) * L + t] = v;
@@ -191,48 +235,35 @@ __global__ __launch_bounds__(kProjFwdWaves * 64) void gate_proj_fwd_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Backward: dx and the dw_f partial of one (column block, token chunk).
+// Backward, dw_f: the dw_f and db_f partials of one (column block, token chunk).
 // ---------------------------------------------------------------------------
 template <typename T, int HB>
 struct ProjBwdSmem {
   static constexpr int GS = 32 * HB + 8;  // d_logit tile row stride (bf16 elements)
-  static constexpr int OS = sizeof(T) == 2 ? kProjMBlock + 8 : kProjMBlock + 4;  // dx tile row
-  alignas(16) bf16 x_hi[kProjTile * kProjMBlock];  // swizzled rows (swz_chunk<128>)
-  alignas(16) bf16 x_lo[sizeof(T) == 2 ? 8 : kProjTile * kProjMBlock];
-  alignas(16) bf16 g_hi[kProjTile * GS];           // [token][head]
-  alignas(16) bf16 g_lo[kProjTile * GS];
-  alignas(16) T out[kProjTile * OS];               // dx rows of the sub-tile
+  // two buffers, alternating between sub-tiles
+  alignas(16) bf16 x_hi[2][kProjTile * kProjMBlock];  // swizzled rows (swz_chunk<128>)
+  alignas(16) bf16 x_lo[2][sizeof(T) == 2 ? 8 : kProjTile * kProjMBlock];
+  alignas(16) bf16 g_hi[2][kProjTile * GS];           // [token][head]
+  alignas(16) bf16 g_lo[2][kProjTile * GS];
 };
 
 template <bool BF16, int HB>
-__global__ __launch_bounds__(kProjThreads) void gate_proj_bwd_kernel(
-    const proj_t<BF16>* __restrict__ x, const float* __restrict__ w, const float* __restrict__ g,
-    proj_t<BF16>* __restrict__ dx, float* __restrict__ dw_part, float* __restrict__ db_part, int N, int L,
-    int H, int M, int CT) {
+__device__ __forceinline__ void proj_dw_body(
+    ProjBwdSmem<proj_t<BF16>, HB>& sm, int mblk, int chunk, const proj_t<BF16>* __restrict__ x,
+    const float* __restrict__ g, float* __restrict__ dw_part, float* __restrict__ db_part, int N,
+    int L, int H, int M, int CT) {
   using T = proj_t<BF16>;
   constexpr bool kBf16 = BF16;
   using S = ProjBwdSmem<T, HB>;
-  constexpr int GS = S::GS, OS = S::OS;
+  constexpr int GS = S::GS;
   constexpr int HPT = 4 * HB;                              // heads staged per thread
   constexpr int XV = kBf16 ? 2 : 4;                        // 16-byte x pieces per thread
-  __shared__ __attribute__((aligned(16))) S sm;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int col = lane & 31, half = lane >> 5;
-  const int mb0 = blockIdx.x * kProjMBlock;
-  const int n_begin = blockIdx.y * CT, n_end = min(N, n_begin + CT);
-  const int m_lane = mb0 + 32 * wave + col;  // this lane's column of dw_f and of dx^T's rows
-
-  // w_f^T fragments of dx^T = w_f^T d_logit: row m_lane, heads 16 ks + 8 half + e.
-  bf16x8 whi[2 * HB], wlo[2 * HB];
-#pragma unroll
-  for (int ks = 0; ks < 2 * HB; ++ks)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int h = 16 * ks + 8 * half + e;
-      const float v = (h < H && m_lane < M) ? w[(size_t)h * M + m_lane] : 0.0f;
-      split_at(v, whi[ks], wlo[ks], e);
-    }
+  const int mb0 = mblk * kProjMBlock;
+  const int n_begin = chunk * CT, n_end = min(N, n_begin + CT);
+  const int m_lane = mb0 + 32 * wave + col;  // this lane's column of dw_f
 
   // transposing-read offsets: x tile (m rows of the operand), d_logit tile (heads)
   int xoff[2][kProjMBlock / 32];
@@ -273,13 +304,13 @@ __global__ __launch_bounds__(kProjThreads) void gate_proj_bwd_kernel(
       gr[slot][j] = (nok && h < H) ? gp[(size_t)h * L] : 0.0f;
     }
   };
-  auto store_tile = [&](auto slot) {
+  auto store_tile = [&](auto slot, int buf) {
 #pragma unroll
     for (int q = 0; q < XV; ++q) {
       const int idx = tid + kProjThreads * q;
       if constexpr (kBf16) {
         const int row = idx >> 4, c = idx & 15;
-        *reinterpret_cast<bf16x8*>(sm.x_hi + row * kProjMBlock + swz_chunk<kProjMBlock>(row, c) * 8) =
+        *reinterpret_cast<bf16x8*>(sm.x_hi[buf] + row * kProjMBlock + swz_chunk<kProjMBlock>(row, c) * 8) =
             xr[slot][q];
       } else {
         const int row = idx >> 5, c4 = idx & 31;
@@ -287,8 +318,8 @@ __global__ __launch_bounds__(kProjThreads) void gate_proj_bwd_kernel(
 #pragma unroll
         for (int e = 0; e < 4; ++e) split_at(xr[slot][q][e], hi, lo, e);
         const int at = row * kProjMBlock + swz_chunk<kProjMBlock>(row, c4 >> 1) * 8 + 4 * (c4 & 1);
-        *reinterpret_cast<bf16x4*>(sm.x_hi + at) = hi;
-        *reinterpret_cast<bf16x4*>(sm.x_lo + at) = lo;
+        *reinterpret_cast<bf16x4*>(sm.x_hi[buf] + at) = hi;
+        *reinterpret_cast<bf16x4*>(sm.x_lo[buf] + at) = lo;
       }
     }
     bf16 hi[HPT], lo[HPT];
@@ -299,12 +330,12 @@ __global__ __launch_bounds__(kProjThreads) void gate_proj_bwd_kernel(
     }
     const int at = (tid & 31) * GS + HPT * (tid >> 5);
     if constexpr (HB == 1) {
-      *reinterpret_cast<bf16x4*>(sm.g_hi + at) = bf16x4{hi[0], hi[1], hi[2], hi[3]};
-      *reinterpret_cast<bf16x4*>(sm.g_lo + at) = bf16x4{lo[0], lo[1], lo[2], lo[3]};
+      *reinterpret_cast<bf16x4*>(sm.g_hi[buf] + at) = bf16x4{hi[0], hi[1], hi[2], hi[3]};
+      *reinterpret_cast<bf16x4*>(sm.g_lo[buf] + at) = bf16x4{lo[0], lo[1], lo[2], lo[3]};
     } else {
-      *reinterpret_cast<bf16x8*>(sm.g_hi + at) =
+      *reinterpret_cast<bf16x8*>(sm.g_hi[buf] + at) =
           bf16x8{hi[0], hi[1], hi[2], hi[3], hi[4], hi[5], hi[6], hi[7]};
-      *reinterpret_cast<bf16x8*>(sm.g_lo + at) =
+      *reinterpret_cast<bf16x8*>(sm.g_lo[buf] + at) =
           bf16x8{lo[0], lo[1], lo[2], lo[3], lo[4], lo[5], lo[6], lo[7]};
     }
   };
@@ -313,8 +344,11 @@ __global__ __launch_bounds__(kProjThreads) void gate_proj_bwd_kernel(
 #pragma unroll
   for (int hb = 0; hb < HB; ++hb) acc_dw[hb] = f32x16{};
 
+  // one barrier per sub-tile: sub-tile j fills buffer j % 2, whose readers
+  // (sub-tile j - 2) have all passed the barrier of sub-tile j - 1
   auto sub_tile = [&](auto slot, int n0) {
-    store_tile(slot);
+    const int buf = ((n0 - n_begin) / kProjTile) & 1;
+    store_tile(slot, buf);
     __syncthreads();
     // the sub-tile after next reuses this slot; in flight during two sub-tiles' products
     if (n0 + 2 * kProjTile < n_end) load_tile(slot, n0 + 2 * kProjTile);
@@ -322,60 +356,19 @@ __global__ __launch_bounds__(kProjThreads) void gate_proj_bwd_kernel(
     // dw_f[heads, m] += d_logit^T-tile (heads x tokens) * x-tile (tokens x m)
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
-      const bf16x8 xh = tile_tr_operand<kProjMBlock>(sm.x_hi, xoff, c, wave);
+      const bf16x8 xh = tile_tr_operand<kProjMBlock>(sm.x_hi[buf], xoff, c, wave);
       bf16x8 xl;
-      if constexpr (!kBf16) xl = tile_tr_operand<kProjMBlock>(sm.x_lo, xoff, c, wave);
+      if constexpr (!kBf16) xl = tile_tr_operand<kProjMBlock>(sm.x_lo[buf], xoff, c, wave);
 #pragma unroll
       for (int hb = 0; hb < HB; ++hb) {
         const int o = c * 16 * GS + 32 * hb;
-        const bf16x8 gh = cat4(lds_read_tr16(sm.g_hi + o + goff[0]),
-                               lds_read_tr16(sm.g_hi + o + goff[1]));
-        const bf16x8 gl = cat4(lds_read_tr16(sm.g_lo + o + goff[0]),
-                               lds_read_tr16(sm.g_lo + o + goff[1]));
+        const bf16x8 gh = cat4(lds_read_tr16(sm.g_hi[buf] + o + goff[0]),
+                               lds_read_tr16(sm.g_hi[buf] + o + goff[1]));
+        const bf16x8 gl = cat4(lds_read_tr16(sm.g_lo[buf] + o + goff[0]),
+                               lds_read_tr16(sm.g_lo[buf] + o + goff[1]));
         acc_dw[hb] = mfma32(gh, xh, acc_dw[hb]);
         acc_dw[hb] = mfma32(gl, xh, acc_dw[hb]);
         if constexpr (!kBf16) acc_dw[hb] = mfma32(gh, xl, acc_dw[hb]);
-      }
-    }
-
-    // dx^T[m, tokens] = w_f^T (m x heads) * d_logit-tile^T (heads x tokens)
-    if (dx) {
-      f32x16 acc_dx = {};
-#pragma unroll
-      for (int ks = 0; ks < 2 * HB; ++ks) {
-        if (16 * ks >= H) break;  // all-zero head slice
-        const int at = col * GS + 16 * ks + 8 * half;
-        const bf16x8 gh = *reinterpret_cast<const bf16x8*>(sm.g_hi + at);
-        const bf16x8 gl = *reinterpret_cast<const bf16x8*>(sm.g_lo + at);
-        acc_dx = mfma32(whi[ks], gh, acc_dx);
-        acc_dx = mfma32(wlo[ks], gh, acc_dx);
-        acc_dx = mfma32(whi[ks], gl, acc_dx);
-      }
-      // lane: token `col`; registers 4q..4q+3: columns 32 wave + 8 q + 4 half + 0..3
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        T* o = sm.out + col * OS + 32 * wave + 8 * q + 4 * half;
-        if constexpr (kBf16) {
-          *reinterpret_cast<bf16x4*>(o) = bf16x4{to_bf16(acc_dx[4 * q]), to_bf16(acc_dx[4 * q + 1]),
-                                                 to_bf16(acc_dx[4 * q + 2]),
-                                                 to_bf16(acc_dx[4 * q + 3])};
-        } else {
-          *reinterpret_cast<f32x4*>(o) =
-              f32x4{acc_dx[4 * q], acc_dx[4 * q + 1], acc_dx[4 * q + 2], acc_dx[4 * q + 3]};
-        }
-      }
-    }
-    __syncthreads();
-    if (dx) {
-#pragma unroll
-      for (int q = 0; q < XV; ++q) {
-        const int idx = tid + kProjThreads * q;
-        const int row = kBf16 ? idx >> 4 : idx >> 5;
-        const int mo = kBf16 ? 8 * (idx & 15) : 4 * (idx & 31);
-        const int n = n0 + row;
-        if (n < n_end && mb0 + mo < M)
-          *reinterpret_cast<XPiece*>(dx + (size_t)n * M + mb0 + mo) =
-              *reinterpret_cast<const XPiece*>(sm.out + row * OS + mo);
       }
     }
   };
@@ -389,18 +382,18 @@ __global__ __launch_bounds__(kProjThreads) void gate_proj_bwd_kernel(
   }
 
   // this chunk's db_f partial: the 32 lanes of a half-wave share their heads
-  if (blockIdx.x == 0) {
+  if (mblk == 0) {
 #pragma unroll
     for (int j = 0; j < HPT; ++j) {
       const float v = row_sum<32>(db_acc[j]);
       const int h = HPT * (tid >> 5) + j;
-      if ((tid & 31) == 0 && h < H) db_part[(size_t)blockIdx.y * H + h] = v;
+      if ((tid & 31) == 0 && h < H) db_part[(size_t)chunk * H + h] = v;
     }
   }
 
   // this chunk's dw_f partial: lane column m_lane, registers: heads 32 hb + row(r)
   if (m_lane < M) {
-    float* part = dw_part + (size_t)blockIdx.y * H * M + m_lane;
+    float* part = dw_part + (size_t)chunk * H * M + m_lane;
 #pragma unroll
     for (int hb = 0; hb < HB; ++hb)
 #pragma unroll
@@ -411,23 +404,158 @@ __global__ __launch_bounds__(kProjThreads) void gate_proj_bwd_kernel(
   }
 }
 
-// dw_f and db_f: the sums of the chunk partials, in chunk order (one thread per
-// element; the unrolled loop issues its loads ahead of the ordered adds).
+// Backward, dx: dx^T = w_f^T d_logit^T for one (column block, 128 tokens).  The
+// d_logit tile is staged once, then each 32-token sub-tile is one MFMA column
+// per token whose rows leave through LDS (two buffers, one barrier each).
+constexpr int kProjDxTok = 128;
+
+template <bool BF16, int HB>
+struct ProjDxSmem {
+  using T = proj_t<BF16>;
+  static constexpr int GS = 32 * HB + 8;
+  static constexpr int OS = BF16 ? kProjMBlock + 8 : kProjMBlock + 4;
+  alignas(16) bf16 g_hi[kProjDxTok * GS];  // [token][head]
+  alignas(16) bf16 g_lo[kProjDxTok * GS];
+  alignas(16) T out[2][kProjTile * OS];
+};
+
+template <bool BF16, int HB>
+__device__ __forceinline__ void proj_dx_body(ProjDxSmem<BF16, HB>& sm, int mblk, int tblk,
+                                             const float* __restrict__ w,
+                                             const float* __restrict__ g,
+                                             proj_t<BF16>* __restrict__ dx, int N, int L, int H,
+                                             int M) {
+  using T = proj_t<BF16>;
+  using S = ProjDxSmem<BF16, HB>;
+  constexpr int GS = S::GS, OS = S::OS;
+  constexpr int HPT = 16 * HB;  // heads staged per thread
+  constexpr int XV = kProjTile * kProjMBlock * (int)sizeof(T) / 16 / kProjThreads;
+  typedef typename std::conditional<BF16, bf16x8, f32x4>::type XPiece;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int col = lane & 31, half = lane >> 5;
+  const int mb0 = mblk * kProjMBlock;
+  const int n_begin = tblk * kProjDxTok, n_end = min(N, n_begin + kProjDxTok);
+  const int m_lane = mb0 + 32 * wave + col;
+
+  // d_logit of the 128 tokens: thread -> token tid % 128, heads HPT (tid / 128) + j
+  {
+    const int n = n_begin + (tid & 127);
+    const bool nok = n < n_end;
+    const int b = nok ? n / L : 0, t = nok ? n - b * L : 0;
+    const float* gp = g + (size_t)b * H * L + t;
+    float gv[HPT];
+#pragma unroll
+    for (int j = 0; j < HPT; ++j) {
+      const int h = HPT * (tid >> 7) + j;
+      gv[j] = (nok && h < H) ? gp[(size_t)h * L] : 0.0f;
+    }
+    bf16x8 hi[HPT / 8], lo[HPT / 8];
+#pragma unroll
+    for (int j = 0; j < HPT; ++j) split_at(gv[j], hi[j / 8], lo[j / 8], j % 8);
+    const int at = (tid & 127) * GS + HPT * (tid >> 7);
+#pragma unroll
+    for (int v = 0; v < HPT / 8; ++v) {
+      *reinterpret_cast<bf16x8*>(sm.g_hi + at + 8 * v) = hi[v];
+      *reinterpret_cast<bf16x8*>(sm.g_lo + at + 8 * v) = lo[v];
+    }
+  }
+  // w_f^T fragments: row m_lane, heads 16 ks + 8 half + e
+  bf16x8 whi[2 * HB], wlo[2 * HB];
+#pragma unroll
+  for (int ks = 0; ks < 2 * HB; ++ks)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int h = 16 * ks + 8 * half + e;
+      const float v = (h < H && m_lane < M) ? w[(size_t)h * M + m_lane] : 0.0f;
+      split_at(v, whi[ks], wlo[ks], e);
+    }
+  __syncthreads();
+
+  for (int st = 0; st * kProjTile < n_end - n_begin; ++st) {
+    const int buf = st & 1;
+    f32x16 acc = {};
+#pragma unroll
+    for (int ks = 0; ks < 2 * HB; ++ks) {
+      if (16 * ks >= H) break;  // all-zero head slice
+      const int at = (kProjTile * st + col) * GS + 16 * ks + 8 * half;
+      const bf16x8 gh = *reinterpret_cast<const bf16x8*>(sm.g_hi + at);
+      const bf16x8 gl = *reinterpret_cast<const bf16x8*>(sm.g_lo + at);
+      acc = mfma32(whi[ks], gh, acc);
+      acc = mfma32(wlo[ks], gh, acc);
+      acc = mfma32(whi[ks], gl, acc);
+    }
+    // lane: token `col` of the sub-tile; registers 4q..4q+3: columns 32 wave + 8 q + 4 half + 0..3
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      T* o = sm.out[buf] + col * OS + 32 * wave + 8 * q + 4 * half;
+      if constexpr (BF16) {
+        *reinterpret_cast<bf16x4*>(o) = bf16x4{to_bf16(acc[4 * q]), to_bf16(acc[4 * q + 1]),
+                                               to_bf16(acc[4 * q + 2]), to_bf16(acc[4 * q + 3])};
+      } else {
+        *reinterpret_cast<f32x4*>(o) = f32x4{acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]};
+      }
+    }
+    __syncthreads();  // this buffer is complete; the other one's readers are done
+    const int n0 = n_begin + kProjTile * st;
+#pragma unroll
+    for (int q = 0; q < XV; ++q) {
+      const int idx = tid + kProjThreads * q;
+      const int row = BF16 ? idx >> 4 : idx >> 5;
+      const int mo = BF16 ? 8 * (idx & 15) : 4 * (idx & 31);
+      const int n = n0 + row;
+      if (n < n_end && mb0 + mo < M)
+        *reinterpret_cast<XPiece*>(dx + (size_t)n * M + mb0 + mo) =
+            *reinterpret_cast<const XPiece*>(sm.out[buf] + row * OS + mo);
+    }
+  }
+}
+
+// The backward's two kernels: dw_f partials over (column block, token chunk)
+// and dx over (column block, 128 tokens).  (One launch interleaving both kinds
+// of workgroup was slower: the larger LDS and register footprint of the two
+// lowers the occupancy of each.)
+template <bool BF16, int HB>
+__global__ __launch_bounds__(kProjThreads) void gate_proj_dw_kernel(
+    const proj_t<BF16>* __restrict__ x, const float* __restrict__ g, float* __restrict__ dw_part,
+    float* __restrict__ db_part, int N, int L, int H, int M, int CT) {
+  __shared__ ProjBwdSmem<proj_t<BF16>, HB> sm;
+  proj_dw_body<BF16, HB>(sm, blockIdx.x, blockIdx.y, x, g, dw_part, db_part, N, L, H, M, CT);
+}
+
+template <bool BF16, int HB>
+__global__ __launch_bounds__(kProjThreads) void gate_proj_dx_kernel(
+    const float* __restrict__ w, const float* __restrict__ g, proj_t<BF16>* __restrict__ dx,
+    int N, int L, int H, int M) {
+  __shared__ ProjDxSmem<BF16, HB> sm;
+  proj_dx_body<BF16, HB>(sm, blockIdx.x, blockIdx.y, w, g, dx, N, L, H, M);
+}
+
+// dw_f and db_f: the sums of the chunk partials.  Eight lanes serve one
+// element: lane p sums chunks p, p + 8, ... in order, then the eight sums meet
+// in a fixed butterfly, so results are deterministic.
+constexpr int kProjReduceLanes = 8;
+
 __global__ __launch_bounds__(kProjThreads) void gate_proj_reduce_kernel(
     const float* __restrict__ dw_part, const float* __restrict__ db_part, float* __restrict__ dw,
     float* __restrict__ db, int n_chunks, int H, int M) {
   const size_t hm = (size_t)H * M;
-  const size_t i = (size_t)blockIdx.x * kProjThreads + threadIdx.x;
+  const size_t t = (size_t)blockIdx.x * kProjThreads + threadIdx.x;
+  const size_t i = t / kProjReduceLanes;  // the element (uniform over the 8 lanes)
+  const int p = (int)(t % kProjReduceLanes);
+  float s = 0.0f;
   if (i < hm) {
-    float s = 0.0f;
-#pragma unroll 16
-    for (int ch = 0; ch < n_chunks; ++ch) s += dw_part[(size_t)ch * hm + i];
-    dw[i] = s;
+#pragma unroll 8
+    for (int ch = p; ch < n_chunks; ch += kProjReduceLanes) s += dw_part[(size_t)ch * hm + i];
   } else if (db && i < hm + H) {
     const int h = (int)(i - hm);
-    float s = 0.0f;
-    for (int ch = 0; ch < n_chunks; ++ch) s += db_part[(size_t)ch * H + h];
-    db[h] = s;
+    for (int ch = p; ch < n_chunks; ch += kProjReduceLanes) s += db_part[(size_t)ch * H + h];
+  }
+  s += __shfl_xor(s, 1);
+  s += __shfl_xor(s, 2);
+  s += __shfl_xor(s, 4);
+  if (p == 0) {
+    if (i < hm) dw[i] = s;
+    else if (db && i < hm + H) db[i - hm] = s;
   }
 }
 
@@ -459,14 +587,14 @@ hipError_t launch_gate_proj_fwd(bool bf16in, const void* x, const float* w, cons
   const int hb = proj_head_blocks(H);
   if (bf16in) {
     if (hb == 1)
-      gate_proj_fwd_kernel<true, 1><<<grid, kProjFwdWaves * 64, 0, s>>>((const bf16*)x, w, bias, logit, N, L, H, M);
+      gate_proj_fwd_kernel<true, 1><<<grid, kProjThreads, 0, s>>>((const bf16*)x, w, bias, logit, N, L, H, M);
     else
-      gate_proj_fwd_kernel<true, 2><<<grid, kProjFwdWaves * 64, 0, s>>>((const bf16*)x, w, bias, logit, N, L, H, M);
+      gate_proj_fwd_kernel<true, 2><<<grid, kProjThreads, 0, s>>>((const bf16*)x, w, bias, logit, N, L, H, M);
   } else {
     if (hb == 1)
-      gate_proj_fwd_kernel<false, 1><<<grid, kProjFwdWaves * 64, 0, s>>>((const float*)x, w, bias, logit, N, L, H, M);
+      gate_proj_fwd_kernel<false, 1><<<grid, kProjThreads, 0, s>>>((const float*)x, w, bias, logit, N, L, H, M);
     else
-      gate_proj_fwd_kernel<false, 2><<<grid, kProjFwdWaves * 64, 0, s>>>((const float*)x, w, bias, logit, N, L, H, M);
+      gate_proj_fwd_kernel<false, 2><<<grid, kProjThreads, 0, s>>>((const float*)x, w, bias, logit, N, L, H, M);
   }
   return hipGetLastError();
 }
@@ -479,22 +607,36 @@ hipError_t launch_gate_proj_bwd(bool bf16in, const void* x, const float* w, cons
   const int chunks = (N + ct - 1) / ct;
   float* part = static_cast<float*>(ws);
   float* dbp = part + (size_t)chunks * H * M;
-  const dim3 grid((M + kProjMBlock - 1) / kProjMBlock, chunks);
+  const unsigned mblocks = (M + kProjMBlock - 1) / kProjMBlock;
   const int hb = proj_head_blocks(H);
-  if (bf16in) {
-    if (hb == 1)
-      gate_proj_bwd_kernel<true, 1><<<grid, kProjThreads, 0, s>>>((const bf16*)x, w, d_logit, (bf16*)dx, part, dbp, N, L, H, M, ct);
-    else
-      gate_proj_bwd_kernel<true, 2><<<grid, kProjThreads, 0, s>>>((const bf16*)x, w, d_logit, (bf16*)dx, part, dbp, N, L, H, M, ct);
-  } else {
-    if (hb == 1)
-      gate_proj_bwd_kernel<false, 1><<<grid, kProjThreads, 0, s>>>((const float*)x, w, d_logit, (float*)dx, part, dbp, N, L, H, M, ct);
-    else
-      gate_proj_bwd_kernel<false, 2><<<grid, kProjThreads, 0, s>>>((const float*)x, w, d_logit, (float*)dx, part, dbp, N, L, H, M, ct);
+#define FOX_PROJ_DX(B16, HBV, TT)                                                              \
+  gate_proj_dx_kernel<B16, HBV><<<gdx, kProjThreads, 0, s>>>(w, d_logit, (TT*)dx, N, L, H, M)
+#define FOX_PROJ_DW(B16, HBV, TT)                                                              \
+  gate_proj_dw_kernel<B16, HBV><<<gdw, kProjThreads, 0, s>>>((const TT*)x, d_logit, part, dbp,  \
+                                                            N, L, H, M, ct)
+  if (dx) {
+    const dim3 gdx(mblocks, (N + kProjDxTok - 1) / kProjDxTok);
+    if (bf16in) {
+      if (hb == 1) FOX_PROJ_DX(true, 1, bf16);
+      else FOX_PROJ_DX(true, 2, bf16);
+    } else {
+      if (hb == 1) FOX_PROJ_DX(false, 1, float);
+      else FOX_PROJ_DX(false, 2, float);
+    }
   }
+  const dim3 gdw(mblocks, chunks);
+  if (bf16in) {
+    if (hb == 1) FOX_PROJ_DW(true, 1, bf16);
+    else FOX_PROJ_DW(true, 2, bf16);
+  } else {
+    if (hb == 1) FOX_PROJ_DW(false, 1, float);
+    else FOX_PROJ_DW(false, 2, float);
+  }
+#undef FOX_PROJ_DX
+#undef FOX_PROJ_DW
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const size_t n_out = (size_t)H * M + (db ? H : 0);
+  const size_t n_out = ((size_t)H * M + (db ? H : 0)) * kProjReduceLanes;
   gate_proj_reduce_kernel<<<(unsigned)((n_out + kProjThreads - 1) / kProjThreads), kProjThreads, 0,
                             s>>>(part, dbp, dw, db, chunks, H, M);
   return hipGetLastError();
