@@ -1015,13 +1015,23 @@ def fox_gate_projection_bwd_workspace_bytes(dtype, B, L, H, M) -> int:
     return int(load().fox_gate_projection_bwd_workspace_bytes(_DT[dtype], B, L, H, M))
 
 
-def fox_gate_projection_bwd(x, w_f, d_logit, want_dx=True, want_db=True, workspace=None):
-    """Gradients of sum(gate_logit * d_logit): returns (dx or None, dw_f, db_f or None)."""
+def fox_gate_projection_bwd(x, w_f, d_logit, want_dx=True, want_db=True, workspace=None,
+                            dx=None, dw=None, db=None):
+    """Gradients of sum(gate_logit * d_logit): returns (dx or None, dw_f, db_f or None).
+    dx, dw, db: optional preallocated outputs (giving one implies wanting it)."""
     B, L, H, M = _proj_shapes(x, w_f)
     _check(d_logit, "d_logit", (B, H, L), torch.float32, x.device)
-    dx = torch.empty_like(x) if want_dx else None
-    dw = torch.empty((H, M), dtype=torch.float32, device=x.device)
-    db = torch.empty((H,), dtype=torch.float32, device=x.device) if want_db else None
+    if dx is None and want_dx:
+        dx = torch.empty_like(x)
+    if dx is not None:
+        _check(dx, "dx", (B, L, M), x.dtype, x.device)
+    if dw is None:
+        dw = torch.empty((H, M), dtype=torch.float32, device=x.device)
+    _check(dw, "dw", (H, M), torch.float32, x.device)
+    if db is None and want_db:
+        db = torch.empty((H,), dtype=torch.float32, device=x.device)
+    if db is not None:
+        _check(db, "db", (H,), torch.float32, x.device)
     need = fox_gate_projection_bwd_workspace_bytes(x.dtype, B, L, H, M)
     if workspace is None:
         workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=x.device)

@@ -2,8 +2,9 @@
 
 Every entry point only enqueues kernels on the caller's stream (no allocation,
 no memset, no synchronisation), so a whole step can be captured once and
-replayed.  The graph here holds the gate prefix, the forward and the four
-stages of the backward keeping dS; it is replayed several times with eager work
+replayed.  The graph here holds the gate projection from the layer input, the
+gate prefix, the forward, the four stages of the backward keeping dS and the
+projection's backward; it is replayed several times with eager work
 and synchronisations between the replays, and every replay must reproduce the
 eager step bit for bit.
 """
@@ -28,16 +29,25 @@ def test_training_step_replays_in_a_hip_graph():
     delta, dcq, dck, dlf, dlogit = (torch.empty((B, H, L), device=DEV) for _ in range(5))
     store = torch.empty(fox.fox_attn_bwd_ds_store_bytes(torch.bfloat16, B, H, L, d),
                         dtype=torch.uint8, device=DEV)
-    outs = (c, o, lse, dq, dk, dv, dlf, dlogit)
+    M = 96
+    pj = inputs.projection_inputs(B, L, H, M, "bf16", 32, device=DEV)
+    logit = torch.empty((B, H, L), device=DEV)
+    pdx, pdw, pdb = torch.empty_like(pj["x"]), torch.empty((H, M), device=DEV), torch.empty(H, device=DEV)
+    pws = torch.empty(fox.fox_gate_projection_bwd_workspace_bytes(torch.bfloat16, B, L, H, M),
+                      dtype=torch.uint8, device=DEV)
+    outs = (logit, c, o, lse, dq, dk, dv, dlf, dlogit, pdx, pdw, pdb)
 
     def step():
-        fox.fox_gate_prefix(x["logit"], c=c)
+        fox.fox_gate_projection(pj["x"], pj["w_f"], pj["b_f"], gate_logit=logit)
+        fox.fox_gate_prefix(logit, c=c)
         fox.fox_attn_fwd(x["q"], x["k"], x["v"], c, s, o=o, lse=lse)
         fox.fox_attn_bwd_delta(o, x["do"], delta=delta)
         fox.fox_attn_bwd_dkdv_store(x["q"], x["k"], x["v"], c, lse, x["do"], delta, store, s,
                                     dk=dk, dv=dv, dc_k=dck)
         fox.fox_attn_bwd_dq_stored(x["k"], store, s, dq=dq, dc_q=dcq)
-        fox.fox_dlogit_from_dc(dcq, dck, x["logit"], d_logit=dlogit, d_log_f=dlf)
+        fox.fox_dlogit_from_dc(dcq, dck, logit, d_logit=dlogit, d_log_f=dlf)
+        fox.fox_gate_projection_bwd(pj["x"], pj["w_f"], dlogit, workspace=pws, dx=pdx, dw=pdw,
+                                    db=pdb)
 
     step()
     torch.cuda.synchronize()
