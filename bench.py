@@ -110,6 +110,9 @@ class EventTimer:
     def mean_ms(self):
         return sum(a.elapsed_time(b) for a, b in self.pairs) / max(1, len(self.pairs))
 
+    def times_ms(self):
+        return sorted(a.elapsed_time(b) for a, b in self.pairs)
+
 
 def bench_train(w, steps, warmup):
     """One step = gate prefix -> forward -> backward keeping dS (the stages of
@@ -150,12 +153,15 @@ def bench_train(w, steps, warmup):
     log(f"[bench] {w.name}: warmup done")
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
+    t_step = EventTimer()  # each step on its own as well, for the median and minimum
     start.record()
     for _ in range(steps):
-        step(True)
+        with t_step:
+            step(True)
     end.record()
     torch.cuda.synchronize()
     wall_ms = (time.perf_counter() - t0) * 1e3 / steps
+    per_step = t_step.times_ms()
     ms = start.elapsed_time(end) / steps
     if not (torch.isfinite(o.float()).all() and torch.isfinite(dlf).all()):
         raise RuntimeError("non-finite outputs")
@@ -217,7 +223,8 @@ def bench_train(w, steps, warmup):
     torch.cuda.synchronize()
     if not all(torch.equal(a, b) for a, b in zip(ref, (o, lse, dq, dk, dv, dlf))):
         raise RuntimeError("the skipping step differs from the dense step")
-    return {"ms": ms, "wall_ms": wall_ms, "gate_ms": t_gate.mean_ms(), "fwd_ms": t_fwd.mean_ms(),
+    return {"ms": ms, "wall_ms": wall_ms, "step_median_ms": per_step[len(per_step) // 2],
+            "step_min_ms": per_step[0], "gate_ms": t_gate.mean_ms(), "fwd_ms": t_fwd.mean_ms(),
             "bwd_ms": t_bwd.mean_ms(), "dkdv_ms": t_dkdv.mean_ms(), "dq_ms": t_dq.mean_ms(),
             "rc_ms": r_step.mean_ms(), "rc_dkdv_ms": r_dkdv.mean_ms(), "rc_dq_ms": r_dq.mean_ms(),
             "skip_ms": t_skip.mean_ms(), "store_bytes": store_bytes}
@@ -402,8 +409,15 @@ def cpu_baseline(w, n_heads=4):
     oracle.backward(x["q"], x["k"], x["v"], x["logit"], x["do"], s)
     dt = time.perf_counter() - t0
     flops = fwd_flops(1, n_heads, w.L, w.d) + bwd_flops(1, n_heads, w.L, w.d)
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            model = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")),
+                         model)
+    except OSError:
+        pass
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": torch.get_num_threads(),
-            "kind": "oracle",
+            "cpu_model": model, "kind": "oracle",
             "sample": f"fp64 forward+backward of {n_heads} of {w.B * w.H} (batch, head) slices "
                       f"at L={w.L}, d={w.d}: {dt:.1f} s; value = those slices' causal FLOPs / time"}
 
@@ -592,7 +606,7 @@ def measured_traffic(kernel: str):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="fwdbwd_bf16_b2_h16_l16384_d128")
     ap.add_argument("--decode-workload", default="decode_bf16_b64_h16_t32768_d128")
@@ -664,6 +678,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(r["ms"], 4),
+        "step_ms_median": round(r["step_median_ms"], 4),
+        "step_ms_min": round(r["step_min_ms"], 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -671,7 +687,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "B": B, "H": H, "L": L, "d": d,
                    "gate_logits": "per-head mean U[0,6], std 1", "causal": True,
-                   "flops_per_step": fl_f + fl_b, "parallelism": "none (1 GPU)"},
+                   "flops_per_step": fl_f + fl_b, "parallelism": "none (1 GPU)",
+                   "seed": w.seed},
         "frac_of_peak": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
         "backward": "fox_attn_bwd_stored stages: dK/dV also store bf16 dS (%.2f GB workspace), "
                     "the dQ pass reads it instead of recomputing S and dP" % (r["store_bytes"] / 1e9),
