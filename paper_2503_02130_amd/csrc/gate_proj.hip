@@ -21,19 +21,20 @@
 //     256 contiguous bytes of a row), each wave takes two 16-wide steps of a
 //     chunk with its w_f fragments from L2; both x and w_f are loaded two
 //     chunks ahead into registers.  The four waves' partial sums meet in LDS.
-//   * Backward, two kernels (dx needs no x, and a loop that mixes stores with
-//     its prefetch loads waits for all of them each time on gfx9, whose one
-//     vector-memory counter serves both):
+//   * Backward, three kernels (dx needs no x, and a loop that mixes stores
+//     with its prefetch loads waits for all of them each time on gfx9, whose
+//     one vector-memory counter serves both):
 //     - dw_f: a workgroup owns a 128-column block of M and a chunk of tokens,
 //       32 tokens at a time, the loads of the next two sub-tiles in flight (two
 //       register slots).  x and d_logit tiles go to LDS (split to bf16
 //       hi/lo); the product contracts over tokens, so both of its operands are
-//       transposing reads (ds_read_b64_tr_b16) of those tiles.
+//       transposing reads (ds_read_b64_tr_b16) of those tiles.  Each chunk
+//       writes its dw_f partial, and the column-block-0 workgroups its db_f
+//       partial.
 //     - dx^T = w_f^T d_logit: a workgroup stages 128 tokens of d_logit once,
 //       then per 32 tokens one MFMA column per token, written through LDS so
-//       that dx rows leave in 16-byte pieces.  Each chunk writes its dw_f and db_f partials
-//     (the column-block-0 workgroups sum d_logit over their tokens); a second
-//     kernel sums the partials in a fixed order, so results are deterministic.
+//       that dx rows leave in 16-byte pieces.
+//     - the partials are summed in a fixed order, so results are deterministic.
 #include <algorithm>
 
 #include "fox_device.h"
@@ -43,7 +44,7 @@ namespace fox {
 
 constexpr int kProjThreads = 256;  // four waves
 constexpr int kProjFwdTok = 64;    // tokens per forward workgroup
-constexpr int kProjMBlock = 128;   // columns of M per backward workgroup
+constexpr int kProjMBlock = 128;   // columns of M per logits chunk and per backward workgroup
 constexpr int kProjTile = 32;      // tokens per backward sub-tile
 constexpr int kProjTargetGroups = 1024;
 
@@ -56,10 +57,8 @@ __device__ __forceinline__ void split_at(float v, V& hi, V& lo, int e) {
   lo[e] = to_bf16(v - to_f32(h));
 }
 
-template <typename T>
-__device__ __forceinline__ void load8(const T* p, bool ok, float (&v)[8]);
-template <>
-__device__ __forceinline__ void load8<float>(const float* p, bool ok, float (&v)[8]) {
+// Eight consecutive floats (two 16-byte loads), or zeros when !ok.
+__device__ __forceinline__ void load8(const float* p, bool ok, float (&v)[8]) {
   f32x4 a = {0.f, 0.f, 0.f, 0.f}, b = a;
   if (ok) {
     a = *reinterpret_cast<const f32x4*>(p);
@@ -161,7 +160,7 @@ __global__ __launch_bounds__(kProjThreads) void gate_proj_fwd_kernel(
       const int m = mc + 32 * wave + 16 * i;
 #pragma unroll
       for (int hb = 0; hb < HB; ++hb)
-        load8<float>(wrow[hb] + m, wok[hb] && m + 8 * half < M, wv[slot][i][hb]);
+        load8(wrow[hb] + m, wok[hb] && m + 8 * half < M, wv[slot][i][hb]);
     }
   };
   auto chunk = [&](auto slot, int ci) {
