@@ -436,9 +436,12 @@ __device__ __forceinline__ void proj_dx_body(ProjDxSmem<BF16, HB>& sm, int mblk,
   const int n_begin = tblk * kProjDxTok, n_end = min(N, n_begin + kProjDxTok);
   const int m_lane = mb0 + 32 * wave + col;
 
-  // d_logit of the 128 tokens: thread -> token tid % 128, heads HPT (tid / 128) + j
-  {
-    const int n = n_begin + (tid & 127);
+  // d_logit of the workgroup's tokens: thread -> token 128 tt + tid % 128, heads
+  // HPT (tid / 128) + j
+#pragma unroll
+  for (int tt = 0; tt < kProjDxTok / 128; ++tt) {
+    const int tok = 128 * tt + (tid & 127);
+    const int n = n_begin + tok;
     const bool nok = n < n_end;
     const int b = nok ? n / L : 0, t = nok ? n - b * L : 0;
     const float* gp = g + (size_t)b * H * L + t;
@@ -451,7 +454,7 @@ __device__ __forceinline__ void proj_dx_body(ProjDxSmem<BF16, HB>& sm, int mblk,
     bf16x8 hi[HPT / 8], lo[HPT / 8];
 #pragma unroll
     for (int j = 0; j < HPT; ++j) split_at(gv[j], hi[j / 8], lo[j / 8], j % 8);
-    const int at = (tid & 127) * GS + HPT * (tid >> 7);
+    const int at = tok * GS + HPT * (tid >> 7);
 #pragma unroll
     for (int v = 0; v < HPT / 8; ++v) {
       *reinterpret_cast<bf16x8*>(sm.g_hi + at + 8 * v) = hi[v];

@@ -85,7 +85,10 @@ CASES = [("f32", 1, 1, 1, 8), ("bf16", 1, 1, 1, 8),
          ("f32", 2, 37, 3, 40), ("bf16", 2, 37, 3, 40),
          ("f32", 1, 256, 2, 128), ("bf16", 3, 300, 12, 768),
          ("bf16", 2, 129, 40, 136), ("f32", 1, 65, 64, 264),
-         ("bf16", 1, 1000, 16, 2048), ("f32", 3, 33, 32, 16)]
+         ("bf16", 1, 1000, 16, 2048), ("f32", 3, 33, 32, 16),
+         # every 32-token tile crosses batches; the smallest two-head-block case;
+         # a long ragged token count with the largest head count and M = 8
+         ("bf16", 5, 1, 2, 16), ("f32", 3, 7, 33, 24), ("bf16", 2, 4097, 64, 8)]
 
 
 @pytest.mark.parametrize("dtype,B,L,H,M", CASES)
