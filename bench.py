@@ -322,6 +322,9 @@ def bench_fixed(w, steps, warmup, t_min=2.0):
     return res
 
 
+PROJ_SEED = 11  # seed of the gate projection's synthetic inputs
+
+
 def projection_bytes(B, L, H, M):
     """Algorithmic HBM bytes of the gate projection with bf16 x: the logits read
     x and w_f, write the logits; the backward reads x, w_f and d_logit and writes
@@ -336,7 +339,7 @@ def bench_projection(w, steps, warmup):
     from x [B, L, M] bf16, then dx, dw_f and db_f."""
     dev = torch.device("cuda:0")
     B, H, L, M = w.B, w.H, w.L, w.H * w.d
-    p = inputs.projection_inputs(B, L, H, M, "bf16", 11, device=dev)
+    p = inputs.projection_inputs(B, L, H, M, "bf16", PROJ_SEED, device=dev)
     logit = torch.empty((B, H, L), device=dev)
     ws = torch.empty(fox.fox_gate_projection_bwd_workspace_bytes(torch.bfloat16, B, L, H, M),
                      device=dev, dtype=torch.uint8)
@@ -792,7 +795,7 @@ def main():
         out["decode"] = {"metric": "decode HBM GB/s", "value": round(gbs, 1), "unit": "GB/s",
                          "ms_per_step": round(rd["ms"], 4),
                          "config": {"workload": wd.name, "B": wd.B, "H": wd.H, "T": wd.L,
-                                    "d": wd.d, "bytes_per_step": byt},
+                                    "d": wd.d, "bytes_per_step": byt, "seed": wd.seed},
                          "roofline": {"bound": "hbm", "kernel": "fox_attn_decode (split + combine)",
                                       "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
                                       "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
@@ -823,7 +826,8 @@ def main():
         out["gate_projection"] = {
             "what": "forget-gate logits w_f^T x_t + b_f per head and their backward (dx, dw_f, "
                     "db_f), x bf16 [B, L, H*d]",
-            "config": {"B": rj["B"], "L": rj["L"], "H": rj["H"], "M": rj["M"]}, **legs}
+            "config": {"B": rj["B"], "L": rj["L"], "H": rj["H"], "M": rj["M"], "seed": PROJ_SEED},
+            **legs}
         log(f"[bench] gate projection fwd {rj['fwd_ms'] * 1e3:.1f} us, bwd "
             f"{rj['bwd_ms'] * 1e3:.1f} us")
     if not args.no_cpu_baseline:
