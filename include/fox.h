@@ -40,13 +40,19 @@
 
 #include <stddef.h>
 
+/* hipStream_t (the stream every entry point enqueues on) */
+#include <hip/hip_runtime_api.h>
+
 #ifdef __cplusplus
 extern "C" {
 #endif
 
 typedef enum {
   FOX_DTYPE_F32 = 0,
-  FOX_DTYPE_BF16 = 1
+  FOX_DTYPE_BF16 = 1,
+  /* not a dtype: makes the enum as wide as an int, so that any int a caller
+     passes is a representable value and is rejected by the range check */
+  FOX_DTYPE_MAX_ENUM = 0x7FFFFFFF
 } fox_dtype_t;
 
 typedef enum {
@@ -57,11 +63,12 @@ typedef enum {
   FOX_ERR_ALIGN = 4,        /* a pointer is not 16-byte aligned                    */
   FOX_ERR_WORKSPACE = 5,    /* workspace missing or smaller than required          */
   FOX_ERR_HIP = 6,          /* the HIP runtime reported an error at launch         */
-  FOX_ERR_VALUE = 7         /* a scalar argument out of range (eps: finite, >= 0)  */
+  FOX_ERR_VALUE = 7,        /* a scalar argument out of range (eps: finite, >= 0)  */
+  FOX_STATUS_MAX_ENUM = 0x7FFFFFFF  /* not a status: keeps the enum int-sized        */
 } fox_status_t;
 
 /* Human-readable name of a status code.  Never returns NULL. */
-const char* fox_status_string(int status);
+const char* fox_status_string(fox_status_t status);
 
 /* Library version as major*10000 + minor*100 + patch. */
 int fox_version(void);
@@ -74,8 +81,8 @@ int fox_version(void);
  *   log_f      [B,H,L] fp32 out  log f_t = log sigmoid(x_t); may be NULL
  *   c          [B,H,L] fp32 out  inclusive prefix sum of log f along t
  */
-int fox_gate_prefix(const float* gate_logit, float* log_f, float* c,
-                    int B, int H, int L, void* stream);
+fox_status_t fox_gate_prefix(const float* gate_logit, float* log_f, float* c,
+                    int B, int H, int L, hipStream_t stream);
 
 /*
  * Forward pass (Alg. 1 of the appendix "Hardware-aware implementation of
@@ -88,11 +95,11 @@ int fox_gate_prefix(const float* gate_logit, float* log_f, float* c,
  *   lse     [B,H,L]   fp32  out  natural-log logsumexp of row i of s Q K^T + D
  *   scale   the factor s on q.k (1/sqrt(d) in the paper)
  */
-int fox_attn_fwd(int dtype, const void* q, const void* k, const void* v, const float* c,
-                 void* o, float* lse, int B, int H, int L, int d, float scale, void* stream);
+fox_status_t fox_attn_fwd(fox_dtype_t dtype, const void* q, const void* k, const void* v, const float* c,
+                 void* o, float* lse, int B, int H, int L, int d, float scale, hipStream_t stream);
 
 /* Bytes of workspace fox_attn_bwd needs for this shape (0 on invalid arguments). */
-size_t fox_attn_bwd_workspace_bytes(int dtype, int B, int H, int L, int d);
+size_t fox_attn_bwd_workspace_bytes(fox_dtype_t dtype, int B, int H, int L, int d);
 
 /*
  * Backward pass (Alg. 2 of the same appendix): the gradients of
@@ -108,11 +115,11 @@ size_t fox_attn_bwd_workspace_bytes(int dtype, int B, int H, int L, int d);
  *   d_log_f          [B,H,L]   fp32  out (fully overwritten)
  *   workspace        device buffer of at least fox_attn_bwd_workspace_bytes()
  */
-int fox_attn_bwd(int dtype, const void* q, const void* k, const void* v, const float* c,
+fox_status_t fox_attn_bwd(fox_dtype_t dtype, const void* q, const void* k, const void* v, const float* c,
                  const void* o, const float* lse, const void* d_o,
                  void* dq, void* dk, void* dv, float* d_log_f,
                  void* workspace, size_t workspace_bytes,
-                 int B, int H, int L, int d, float scale, void* stream);
+                 int B, int H, int L, int d, float scale, hipStream_t stream);
 
 /*
  * The same backward (Alg. 2) trading memory for the recomputation in the dQ
@@ -127,12 +134,12 @@ int fox_attn_bwd(int dtype, const void* q, const void* k, const void* v, const f
  * the same bf16 dS in different orders); dc^q and dc^k remain the row and
  * column sums of one matrix.
  */
-size_t fox_attn_bwd_stored_workspace_bytes(int dtype, int B, int H, int L, int d);
-int fox_attn_bwd_stored(int dtype, const void* q, const void* k, const void* v, const float* c,
+size_t fox_attn_bwd_stored_workspace_bytes(fox_dtype_t dtype, int B, int H, int L, int d);
+fox_status_t fox_attn_bwd_stored(fox_dtype_t dtype, const void* q, const void* k, const void* v, const float* c,
                         const void* o, const float* lse, const void* d_o,
                         void* dq, void* dk, void* dv, float* d_log_f,
                         void* workspace, size_t workspace_bytes,
-                        int B, int H, int L, int d, float scale, void* stream);
+                        int B, int H, int L, int d, float scale, hipStream_t stream);
 
 /*
  * fox_attn_bwd_stored in stages: it is exactly
@@ -151,15 +158,15 @@ int fox_attn_bwd_stored(int dtype, const void* q, const void* k, const void* v, 
  *   fox_attn_bwd_dkdv_store for the same shape.
  * bf16 only: FOX_ERR_UNSUPPORTED for fp32.
  */
-size_t fox_attn_bwd_ds_store_bytes(int dtype, int B, int H, int L, int d);
-int fox_attn_bwd_dkdv_store(int dtype, const void* q, const void* k, const void* v,
+size_t fox_attn_bwd_ds_store_bytes(fox_dtype_t dtype, int B, int H, int L, int d);
+fox_status_t fox_attn_bwd_dkdv_store(fox_dtype_t dtype, const void* q, const void* k, const void* v,
                             const float* c, const float* lse, const void* d_o,
                             const float* delta, void* dk, void* dv, float* dc_k,
                             void* ds_store, size_t ds_store_bytes,
-                            int B, int H, int L, int d, float scale, void* stream);
-int fox_attn_bwd_dq_stored(int dtype, const void* k, const void* ds_store, size_t ds_store_bytes,
+                            int B, int H, int L, int d, float scale, hipStream_t stream);
+fox_status_t fox_attn_bwd_dq_stored(fox_dtype_t dtype, const void* k, const void* ds_store, size_t ds_store_bytes,
                            void* dq, float* dc_q, int B, int H, int L, int d, float scale,
-                           void* stream);
+                           hipStream_t stream);
 
 /*
  * The backward pass in stages, for callers that schedule them themselves (for
@@ -181,18 +188,18 @@ int fox_attn_bwd_dq_stored(int dtype, const void* k, const void* ds_store, size_
  * column sums of one matrix and sum(dc) = d(log f)_1 = 0 holds to fp32 rounding.
  * Inputs as for fox_attn_bwd.
  */
-int fox_attn_bwd_delta(int dtype, const void* o, const void* d_o, float* delta,
-                       int B, int H, int L, int d, void* stream);
-int fox_attn_bwd_dkdv(int dtype, const void* q, const void* k, const void* v, const float* c,
+fox_status_t fox_attn_bwd_delta(fox_dtype_t dtype, const void* o, const void* d_o, float* delta,
+                       int B, int H, int L, int d, hipStream_t stream);
+fox_status_t fox_attn_bwd_dkdv(fox_dtype_t dtype, const void* q, const void* k, const void* v, const float* c,
                       const float* lse, const void* d_o, const float* delta,
                       void* dk, void* dv, float* dc_k,
-                      int B, int H, int L, int d, float scale, void* stream);
-int fox_attn_bwd_dq(int dtype, const void* q, const void* k, const void* v, const float* c,
+                      int B, int H, int L, int d, float scale, hipStream_t stream);
+fox_status_t fox_attn_bwd_dq(fox_dtype_t dtype, const void* q, const void* k, const void* v, const float* c,
                     const float* lse, const void* d_o, const float* delta,
                     void* dq, float* dc_q,
-                    int B, int H, int L, int d, float scale, void* stream);
-int fox_dlogf_from_dc(const float* dc_q, const float* dc_k, float* d_log_f,
-                      int B, int H, int L, void* stream);
+                    int B, int H, int L, int d, float scale, hipStream_t stream);
+fox_status_t fox_dlogf_from_dc(const float* dc_q, const float* dc_k, float* d_log_f,
+                      int B, int H, int L, hipStream_t stream);
 
 /*
  * Gate backward (Sec. 3: f_t = sigmoid(x_t), so d log f_t / d x_t = 1 - f_t =
@@ -204,11 +211,11 @@ int fox_dlogf_from_dc(const float* dc_q, const float* dc_k, float* d_log_f,
  *   d_log_f     [B,H,L] fp32 out  may be NULL
  *   d_logit     [B,H,L] fp32 out  the gradient with respect to the gate logits
  */
-int fox_dlogit_from_dc(const float* dc_q, const float* dc_k, const float* gate_logit,
-                       float* d_log_f, float* d_logit, int B, int H, int L, void* stream);
+fox_status_t fox_dlogit_from_dc(const float* dc_q, const float* dc_k, const float* gate_logit,
+                       float* d_log_f, float* d_logit, int B, int H, int L, hipStream_t stream);
 
 /* Bytes of workspace fox_attn_decode needs for this shape (0 on invalid arguments). */
-size_t fox_attn_decode_workspace_bytes(int dtype, int B, int H, int T, int d);
+size_t fox_attn_decode_workspace_bytes(fox_dtype_t dtype, int B, int H, int T, int d);
 
 /*
  * One decode step: Eq. fot-weight evaluated for the last position i = T of a
@@ -227,10 +234,10 @@ size_t fox_attn_decode_workspace_bytes(int dtype, int B, int H, int T, int d);
  *   lse            [B,H]     fp32 out  natural-log logsumexp of the new row
  *   workspace      device buffer of at least fox_attn_decode_workspace_bytes()
  */
-int fox_attn_decode(int dtype, const void* q, const void* k_cache, const void* v_cache,
+fox_status_t fox_attn_decode(fox_dtype_t dtype, const void* q, const void* k_cache, const void* v_cache,
                     float* c_cache, const float* gate_logit_new, void* o, float* lse,
                     void* workspace, size_t workspace_bytes,
-                    int B, int H, int T, int d, float scale, void* stream);
+                    int B, int H, int T, int d, float scale, hipStream_t stream);
 
 /*
  * Gate-aware exact skipping (the paper's outlook, Sec. 6: forget gates could
@@ -255,29 +262,29 @@ int fox_attn_decode(int dtype, const void* q, const void* k_cache, const void* v
  *   closest query/key pair puts this below 2^-160 is skipped.  bf16 only; the
  *   fp32 path runs dense.  Workspace as fox_attn_bwd.
  */
-int fox_row_norm_max(int dtype, const void* x, float* out, int B, int H, int L, int d,
-                     void* stream);
-int fox_attn_fwd_skip(int dtype, const void* q, const void* k, const void* v, const float* c,
+fox_status_t fox_row_norm_max(fox_dtype_t dtype, const void* x, float* out, int B, int H, int L, int d,
+                     hipStream_t stream);
+fox_status_t fox_attn_fwd_skip(fox_dtype_t dtype, const void* q, const void* k, const void* v, const float* c,
                       const float* q_norm_max, const float* k_norm_max, void* o, float* lse,
-                      int B, int H, int L, int d, float scale, void* stream);
-int fox_attn_bwd_skip(int dtype, const void* q, const void* k, const void* v, const float* c,
+                      int B, int H, int L, int d, float scale, hipStream_t stream);
+fox_status_t fox_attn_bwd_skip(fox_dtype_t dtype, const void* q, const void* k, const void* v, const float* c,
                       const void* o, const float* lse, const void* d_o, const float* q_norm_max,
                       const float* k_norm_max, void* dq, void* dk, void* dv, float* d_log_f,
                       void* workspace, size_t workspace_bytes, int B, int H, int L, int d,
-                      float scale, void* stream);
+                      float scale, hipStream_t stream);
 /* fox_attn_bwd_skip keeping dS (as fox_attn_bwd_stored; bf16 only): the dK/dV pass
  * stores the dS of the tiles it computes and the dQ pass reads only those.  Workspace:
  * at least fox_attn_bwd_stored_workspace_bytes().  Results are bitwise those of
  * fox_attn_bwd_stored. */
-int fox_attn_bwd_skip_stored(int dtype, const void* q, const void* k, const void* v,
+fox_status_t fox_attn_bwd_skip_stored(fox_dtype_t dtype, const void* q, const void* k, const void* v,
                              const float* c, const void* o, const float* lse, const void* d_o,
                              const float* q_norm_max, const float* k_norm_max, void* dq, void* dk,
                              void* dv, float* d_log_f, void* workspace, size_t workspace_bytes,
-                             int B, int H, int L, int d, float scale, void* stream);
-int fox_attn_decode_skip(int dtype, const void* q, const void* k_cache, const void* v_cache,
+                             int B, int H, int L, int d, float scale, hipStream_t stream);
+fox_status_t fox_attn_decode_skip(fox_dtype_t dtype, const void* q, const void* k_cache, const void* v_cache,
                          float* c_cache, const float* gate_logit_new, const float* k_norm_max,
                          void* o, float* lse, void* workspace, size_t workspace_bytes, int B,
-                         int H, int T, int d, float scale, void* stream);
+                         int H, int T, int d, float scale, hipStream_t stream);
 
 /*
  * Fixed (data-independent) forget gates: f_t^(h) = sigmoid(b^(h)) for every t
@@ -298,39 +305,39 @@ int fox_attn_decode_skip(int dtype, const void* q, const void* k_cache, const vo
  * fox_attn_decode_fixed_gate: one decode step as fox_attn_decode, without a
  *   prefix cache; workspace: fox_attn_decode_workspace_bytes().
  */
-int fox_fixed_gate_init(float* gate_bias, int H, float t_min, float t_max);
-int fox_attn_fwd_fixed_gate(int dtype, const void* q, const void* k, const void* v,
+fox_status_t fox_fixed_gate_init(float* gate_bias, int H, float t_min, float t_max);
+fox_status_t fox_attn_fwd_fixed_gate(fox_dtype_t dtype, const void* q, const void* k, const void* v,
                             const float* gate_bias, void* o, float* lse, int B, int H, int L, int d,
-                            float scale, void* stream);
-size_t fox_attn_bwd_fixed_gate_workspace_bytes(int dtype, int B, int H, int L, int d);
-int fox_attn_bwd_fixed_gate(int dtype, const void* q, const void* k, const void* v,
+                            float scale, hipStream_t stream);
+size_t fox_attn_bwd_fixed_gate_workspace_bytes(fox_dtype_t dtype, int B, int H, int L, int d);
+fox_status_t fox_attn_bwd_fixed_gate(fox_dtype_t dtype, const void* q, const void* k, const void* v,
                             const float* gate_bias, const void* o, const float* lse,
                             const void* d_o, void* dq, void* dk, void* dv, float* d_gate_bias,
                             void* workspace, size_t workspace_bytes, int B, int H, int L, int d,
-                            float scale, void* stream);
+                            float scale, hipStream_t stream);
 /* fox_attn_bwd_fixed_gate keeping dS (as fox_attn_bwd_stored; bf16 only), and
  * fox_attn_bwd_fixed_gate_skip keeping dS (bitwise the results of
  * fox_attn_bwd_fixed_gate_stored).  Workspace: at least
  * fox_attn_bwd_fixed_gate_stored_workspace_bytes() (0 for fp32 or invalid
  * arguments), about B H L^2 bytes.  dK and dV are bit for bit those of
  * fox_attn_bwd_fixed_gate; dQ and the bias gradient agree to rounding. */
-size_t fox_attn_bwd_fixed_gate_stored_workspace_bytes(int dtype, int B, int H, int L, int d);
-int fox_attn_bwd_fixed_gate_stored(int dtype, const void* q, const void* k, const void* v,
+size_t fox_attn_bwd_fixed_gate_stored_workspace_bytes(fox_dtype_t dtype, int B, int H, int L, int d);
+fox_status_t fox_attn_bwd_fixed_gate_stored(fox_dtype_t dtype, const void* q, const void* k, const void* v,
                                    const float* gate_bias, const void* o, const float* lse,
                                    const void* d_o, void* dq, void* dk, void* dv,
                                    float* d_gate_bias, void* workspace, size_t workspace_bytes,
-                                   int B, int H, int L, int d, float scale, void* stream);
-int fox_attn_bwd_fixed_gate_skip_stored(int dtype, const void* q, const void* k, const void* v,
+                                   int B, int H, int L, int d, float scale, hipStream_t stream);
+fox_status_t fox_attn_bwd_fixed_gate_skip_stored(fox_dtype_t dtype, const void* q, const void* k, const void* v,
                                         const float* gate_bias, const void* o, const float* lse,
                                         const void* d_o, const float* q_norm_max,
                                         const float* k_norm_max, void* dq, void* dk, void* dv,
                                         float* d_gate_bias, void* workspace,
                                         size_t workspace_bytes, int B, int H, int L, int d,
-                                        float scale, void* stream);
-int fox_attn_decode_fixed_gate(int dtype, const void* q, const void* k_cache,
+                                        float scale, hipStream_t stream);
+fox_status_t fox_attn_decode_fixed_gate(fox_dtype_t dtype, const void* q, const void* k_cache,
                                const void* v_cache, const float* gate_bias, void* o, float* lse,
                                void* workspace, size_t workspace_bytes, int B, int H, int T, int d,
-                               float scale, void* stream);
+                               float scale, hipStream_t stream);
 
 /*
  * Fixed gates with exact gate-aware skipping: the entry points above with the
@@ -343,21 +350,21 @@ int fox_attn_decode_fixed_gate(int dtype, const void* q, const void* k_cache,
  * and backward skip in bf16 (fp32 runs dense); the decode skips in both dtypes.
  * Workspaces as the entry points without skipping.
  */
-int fox_attn_fwd_fixed_gate_skip(int dtype, const void* q, const void* k, const void* v,
+fox_status_t fox_attn_fwd_fixed_gate_skip(fox_dtype_t dtype, const void* q, const void* k, const void* v,
                                  const float* gate_bias, const float* q_norm_max,
                                  const float* k_norm_max, void* o, float* lse, int B, int H, int L,
-                                 int d, float scale, void* stream);
-int fox_attn_bwd_fixed_gate_skip(int dtype, const void* q, const void* k, const void* v,
+                                 int d, float scale, hipStream_t stream);
+fox_status_t fox_attn_bwd_fixed_gate_skip(fox_dtype_t dtype, const void* q, const void* k, const void* v,
                                  const float* gate_bias, const void* o, const float* lse,
                                  const void* d_o, const float* q_norm_max,
                                  const float* k_norm_max, void* dq, void* dk, void* dv,
                                  float* d_gate_bias, void* workspace, size_t workspace_bytes,
-                                 int B, int H, int L, int d, float scale, void* stream);
-int fox_attn_decode_fixed_gate_skip(int dtype, const void* q, const void* k_cache,
+                                 int B, int H, int L, int d, float scale, hipStream_t stream);
+fox_status_t fox_attn_decode_fixed_gate_skip(fox_dtype_t dtype, const void* q, const void* k_cache,
                                     const void* v_cache, const float* gate_bias,
                                     const float* k_norm_max, void* o, float* lse, void* workspace,
                                     size_t workspace_bytes, int B, int H, int T, int d,
-                                    float scale, void* stream);
+                                    float scale, hipStream_t stream);
 
 /*
  * FoX (Pro) prologue and epilogue (Sec. 3 "Architecture design", Eq. shift-linear;
@@ -393,32 +400,32 @@ int fox_attn_decode_fixed_gate_skip(int dtype, const void* q, const void* k_cach
  *   the attention backward, in the workspace: at least
  *   fox_attn_bwd_pro_workspace_bytes().
  */
-int fox_pro_prologue(int dtype, const void* q_raw, const void* k_raw, const void* v_raw,
+fox_status_t fox_pro_prologue(fox_dtype_t dtype, const void* q_raw, const void* k_raw, const void* v_raw,
                      const float* k_shift_logit, const float* v_shift_logit,
                      const float* q_norm_weight, const float* k_norm_weight, float eps, void* q,
-                     void* k, void* v, int B, int H, int L, int d, void* stream);
-size_t fox_pro_prologue_bwd_workspace_bytes(int dtype, int B, int H, int L, int d);
-int fox_pro_prologue_bwd(int dtype, const void* q_raw, const void* k_raw, const void* v_raw,
+                     void* k, void* v, int B, int H, int L, int d, hipStream_t stream);
+size_t fox_pro_prologue_bwd_workspace_bytes(fox_dtype_t dtype, int B, int H, int L, int d);
+fox_status_t fox_pro_prologue_bwd(fox_dtype_t dtype, const void* q_raw, const void* k_raw, const void* v_raw,
                          const float* k_shift_logit, const float* v_shift_logit,
                          const float* q_norm_weight, const float* k_norm_weight, float eps,
                          const void* dq, const void* dk, const void* dv, void* dq_raw,
                          void* dk_raw, void* dv_raw, float* dk_shift_logit,
                          float* dv_shift_logit, float* dq_norm_weight, float* dk_norm_weight,
                          void* workspace, size_t workspace_bytes, int B, int H, int L, int d,
-                         void* stream);
-int fox_pro_output_gate(int dtype, const void* o, const void* g_logit,
+                         hipStream_t stream);
+fox_status_t fox_pro_output_gate(fox_dtype_t dtype, const void* o, const void* g_logit,
                         const float* o_norm_weight, float eps, void* y, int B, int H, int L,
-                        int d, void* stream);
-int fox_attn_fwd_pro(int dtype, const void* q, const void* k, const void* v, const float* c,
+                        int d, hipStream_t stream);
+fox_status_t fox_attn_fwd_pro(fox_dtype_t dtype, const void* q, const void* k, const void* v, const float* c,
                      const void* g_logit, const float* o_norm_weight, float eps, void* o,
-                     float* lse, void* y, int B, int H, int L, int d, float scale, void* stream);
-size_t fox_attn_bwd_pro_workspace_bytes(int dtype, int B, int H, int L, int d);
-int fox_attn_bwd_pro(int dtype, const void* q, const void* k, const void* v, const float* c,
+                     float* lse, void* y, int B, int H, int L, int d, float scale, hipStream_t stream);
+size_t fox_attn_bwd_pro_workspace_bytes(fox_dtype_t dtype, int B, int H, int L, int d);
+fox_status_t fox_attn_bwd_pro(fox_dtype_t dtype, const void* q, const void* k, const void* v, const float* c,
                      const void* o, const float* lse, const void* g_logit,
                      const float* o_norm_weight, float eps, const void* dy, void* dq, void* dk,
                      void* dv, float* d_log_f, void* dg_logit, float* do_norm_weight,
                      void* workspace, size_t workspace_bytes, int B, int H, int L, int d,
-                     float scale, void* stream);
+                     float scale, hipStream_t stream);
 
 /*
  * fox_attn_bwd_pro with the attention backward keeping dS, as
@@ -428,13 +435,13 @@ int fox_attn_bwd_pro(int dtype, const void* q, const void* k, const void* v, con
  * otherwise as for fox_attn_bwd_pro; dK, dV and the gate and norm-weight
  * gradients are bit for bit the same, dQ and d(log f) agree to rounding.
  */
-size_t fox_attn_bwd_pro_stored_workspace_bytes(int dtype, int B, int H, int L, int d);
-int fox_attn_bwd_pro_stored(int dtype, const void* q, const void* k, const void* v,
+size_t fox_attn_bwd_pro_stored_workspace_bytes(fox_dtype_t dtype, int B, int H, int L, int d);
+fox_status_t fox_attn_bwd_pro_stored(fox_dtype_t dtype, const void* q, const void* k, const void* v,
                             const float* c, const void* o, const float* lse, const void* g_logit,
                             const float* o_norm_weight, float eps, const void* dy, void* dq,
                             void* dk, void* dv, float* d_log_f, void* dg_logit,
                             float* do_norm_weight, void* workspace, size_t workspace_bytes,
-                            int B, int H, int L, int d, float scale, void* stream);
+                            int B, int H, int L, int d, float scale, hipStream_t stream);
 
 /*
  * The forget-gate projection (Sec. 3, gate definition: f_t = sigmoid(w_f^T x_t
@@ -452,11 +459,11 @@ int fox_attn_bwd_pro_stored(int dtype, const void* q, const void* k, const void*
  * relative L2 error near 2e-6 for either dtype).  Values must be finite and below 3.38e38 in
  * magnitude (the bf16 range).  H > 64 or M % 8 != 0: FOX_ERR_UNSUPPORTED.
  */
-int fox_gate_projection(int dtype, const void* x, const float* w_f, const float* b_f,
-                        float* gate_logit, int B, int L, int H, int M, void* stream);
+fox_status_t fox_gate_projection(fox_dtype_t dtype, const void* x, const float* w_f, const float* b_f,
+                        float* gate_logit, int B, int L, int H, int M, hipStream_t stream);
 
 /* Bytes of workspace fox_gate_projection_bwd needs (0 on invalid arguments). */
-size_t fox_gate_projection_bwd_workspace_bytes(int dtype, int B, int L, int H, int M);
+size_t fox_gate_projection_bwd_workspace_bytes(fox_dtype_t dtype, int B, int L, int H, int M);
 
 /*
  * Backward of fox_gate_projection: the gradients of sum(gate_logit * d_logit).
@@ -470,9 +477,9 @@ size_t fox_gate_projection_bwd_workspace_bytes(int dtype, int B, int L, int H, i
  *              (per-chunk partials of dw_f, summed in a fixed order: results are
  *              deterministic)
  */
-int fox_gate_projection_bwd(int dtype, const void* x, const float* w_f, const float* d_logit,
+fox_status_t fox_gate_projection_bwd(fox_dtype_t dtype, const void* x, const float* w_f, const float* d_logit,
                             void* dx, float* dw_f, float* db_f, void* workspace,
-                            size_t workspace_bytes, int B, int L, int H, int M, void* stream);
+                            size_t workspace_bytes, int B, int L, int H, int M, hipStream_t stream);
 
 #ifdef __cplusplus
 }

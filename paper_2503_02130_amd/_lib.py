@@ -62,6 +62,8 @@ def load() -> ctypes.CDLL:
             f"{LIB_PATH} is missing: build it with `python -m paper_2503_02130_amd.build` "
             "(the HIP library is required; there is no fallback)")
     lib = ctypes.CDLL(LIB_PATH)
+    # fox_status_t and fox_dtype_t are int-sized enums (their MAX_ENUM members) and
+    # hipStream_t is a pointer, so c_int and c_void_p are their exact C types
     P, I, F, Z = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
     lib.fox_status_string.restype = ctypes.c_char_p
     lib.fox_status_string.argtypes = [I]

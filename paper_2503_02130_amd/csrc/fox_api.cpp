@@ -17,7 +17,7 @@ constexpr long long kMaxWorkgroups = 1LL << 22;   // 256-thread workgroups per l
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-int check_dims(int B, int H, int L, int d) {
+fox_status_t check_dims(int B, int H, int L, int d) {
   if (B <= 0 || H <= 0 || L <= 0 || d <= 0) return FOX_ERR_SHAPE;
   const long long bh = (long long)B * H;
   if (bh > (1LL << 30)) return FOX_ERR_SHAPE;
@@ -28,15 +28,15 @@ int check_dims(int B, int H, int L, int d) {
   return FOX_OK;
 }
 
-int check_dtype_d(int dtype, int d) {
+fox_status_t check_dtype_d(int dtype, int d) {
   if (dtype != FOX_DTYPE_F32 && dtype != FOX_DTYPE_BF16) return FOX_ERR_UNSUPPORTED;
   if (d != 64 && d != 128) return FOX_ERR_UNSUPPORTED;
   return FOX_OK;
 }
 
-int launch_status(hipError_t e) { return e == hipSuccess ? FOX_OK : FOX_ERR_HIP; }
+fox_status_t launch_status(hipError_t e) { return e == hipSuccess ? FOX_OK : FOX_ERR_HIP; }
 
-int check_projection(int dtype, int B, int L, int H, int M) {
+fox_status_t check_projection(int dtype, int B, int L, int H, int M) {
   if (B <= 0 || L <= 0 || H <= 0 || M <= 0) return FOX_ERR_SHAPE;
   const long long n = (long long)B * L;
   if (n > (1LL << 31) - 1 || (long long)B * H * L > (1LL << 31) - 1) return FOX_ERR_SHAPE;
@@ -64,7 +64,7 @@ bool all_set(std::initializer_list<const void*> ps) {
 
 extern "C" {
 
-const char* fox_status_string(int status) {
+const char* fox_status_string(fox_status_t status) {
   switch (status) {
     case FOX_OK: return "FOX_OK";
     case FOX_ERR_NULL: return "FOX_ERR_NULL: a required pointer is NULL";
@@ -80,20 +80,20 @@ const char* fox_status_string(int status) {
 
 int fox_version(void) { return 100; }
 
-int fox_gate_prefix(const float* gate_logit, float* log_f, float* c, int B, int H, int L,
-                    void* stream) {
+fox_status_t fox_gate_prefix(const float* gate_logit, float* log_f, float* c, int B, int H, int L,
+                    hipStream_t stream) {
   if (!gate_logit || !c) return FOX_ERR_NULL;
-  int st = check_dims(B, H, L, 1);
+  fox_status_t st = check_dims(B, H, L, 1);
   if (st) return st;
   if (!aligned16(gate_logit) || !aligned16(c) || (log_f && !aligned16(log_f))) return FOX_ERR_ALIGN;
   return launch_status(fox::launch_gate_prefix(gate_logit, log_f, c, B * H, L,
                                                static_cast<hipStream_t>(stream)));
 }
 
-int fox_attn_fwd(int dtype, const void* q, const void* k, const void* v, const float* c, void* o,
-                 float* lse, int B, int H, int L, int d, float scale, void* stream) {
+fox_status_t fox_attn_fwd(fox_dtype_t dtype, const void* q, const void* k, const void* v, const float* c, void* o,
+                 float* lse, int B, int H, int L, int d, float scale, hipStream_t stream) {
   if (!q || !k || !v || !c || !o || !lse) return FOX_ERR_NULL;
-  int st = check_dims(B, H, L, d);
+  fox_status_t st = check_dims(B, H, L, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -108,18 +108,18 @@ int fox_attn_fwd(int dtype, const void* q, const void* k, const void* v, const f
                                            s));
 }
 
-size_t fox_attn_bwd_workspace_bytes(int dtype, int B, int H, int L, int d) {
+size_t fox_attn_bwd_workspace_bytes(fox_dtype_t dtype, int B, int H, int L, int d) {
   if (check_dims(B, H, L, d) || check_dtype_d(dtype, d)) return 0;
   return fox::bwd_workspace_bytes(B * H, L);
 }
 
-int fox_attn_bwd(int dtype, const void* q, const void* k, const void* v, const float* c,
+fox_status_t fox_attn_bwd(fox_dtype_t dtype, const void* q, const void* k, const void* v, const float* c,
                  const void* o, const float* lse, const void* d_o, void* dq, void* dk, void* dv,
                  float* d_log_f, void* workspace, size_t workspace_bytes, int B, int H, int L,
-                 int d, float scale, void* stream) {
+                 int d, float scale, hipStream_t stream) {
   if (!q || !k || !v || !c || !o || !lse || !d_o || !dq || !dk || !dv || !d_log_f)
     return FOX_ERR_NULL;
-  int st = check_dims(B, H, L, d);
+  fox_status_t st = check_dims(B, H, L, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -134,18 +134,18 @@ int fox_attn_bwd(int dtype, const void* q, const void* k, const void* v, const f
                                        static_cast<hipStream_t>(stream)));
 }
 
-size_t fox_attn_bwd_stored_workspace_bytes(int dtype, int B, int H, int L, int d) {
+size_t fox_attn_bwd_stored_workspace_bytes(fox_dtype_t dtype, int B, int H, int L, int d) {
   if (check_dims(B, H, L, d) || check_dtype_d(dtype, d) || dtype != FOX_DTYPE_BF16) return 0;
   return fox::bwd_stored_workspace_bytes(B * H, L);
 }
 
-int fox_attn_bwd_stored(int dtype, const void* q, const void* k, const void* v, const float* c,
+fox_status_t fox_attn_bwd_stored(fox_dtype_t dtype, const void* q, const void* k, const void* v, const float* c,
                         const void* o, const float* lse, const void* d_o, void* dq, void* dk,
                         void* dv, float* d_log_f, void* workspace, size_t workspace_bytes, int B,
-                        int H, int L, int d, float scale, void* stream) {
+                        int H, int L, int d, float scale, hipStream_t stream) {
   if (!q || !k || !v || !c || !o || !lse || !d_o || !dq || !dk || !dv || !d_log_f)
     return FOX_ERR_NULL;
-  int st = check_dims(B, H, L, d);
+  fox_status_t st = check_dims(B, H, L, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -162,10 +162,10 @@ int fox_attn_bwd_stored(int dtype, const void* q, const void* k, const void* v, 
                                               static_cast<hipStream_t>(stream)));
 }
 
-int fox_attn_bwd_delta(int dtype, const void* o, const void* d_o, float* delta, int B, int H,
-                       int L, int d, void* stream) {
+fox_status_t fox_attn_bwd_delta(fox_dtype_t dtype, const void* o, const void* d_o, float* delta, int B, int H,
+                       int L, int d, hipStream_t stream) {
   if (!o || !d_o || !delta) return FOX_ERR_NULL;
-  int st = check_dims(B, H, L, d);
+  fox_status_t st = check_dims(B, H, L, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -174,11 +174,11 @@ int fox_attn_bwd_delta(int dtype, const void* o, const void* d_o, float* delta, 
                                              static_cast<hipStream_t>(stream)));
 }
 
-int fox_attn_bwd_dkdv(int dtype, const void* q, const void* k, const void* v, const float* c,
+fox_status_t fox_attn_bwd_dkdv(fox_dtype_t dtype, const void* q, const void* k, const void* v, const float* c,
                       const float* lse, const void* d_o, const float* delta, void* dk, void* dv,
-                      float* dc_k, int B, int H, int L, int d, float scale, void* stream) {
+                      float* dc_k, int B, int H, int L, int d, float scale, hipStream_t stream) {
   if (!q || !k || !v || !c || !lse || !d_o || !delta || !dk || !dv || !dc_k) return FOX_ERR_NULL;
-  int st = check_dims(B, H, L, d);
+  fox_status_t st = check_dims(B, H, L, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -191,11 +191,11 @@ int fox_attn_bwd_dkdv(int dtype, const void* q, const void* k, const void* v, co
                                             static_cast<hipStream_t>(stream)));
 }
 
-int fox_attn_bwd_dq(int dtype, const void* q, const void* k, const void* v, const float* c,
+fox_status_t fox_attn_bwd_dq(fox_dtype_t dtype, const void* q, const void* k, const void* v, const float* c,
                     const float* lse, const void* d_o, const float* delta, void* dq, float* dc_q,
-                    int B, int H, int L, int d, float scale, void* stream) {
+                    int B, int H, int L, int d, float scale, hipStream_t stream) {
   if (!q || !k || !v || !c || !lse || !d_o || !delta || !dq || !dc_q) return FOX_ERR_NULL;
-  int st = check_dims(B, H, L, d);
+  fox_status_t st = check_dims(B, H, L, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -207,18 +207,18 @@ int fox_attn_bwd_dq(int dtype, const void* q, const void* k, const void* v, cons
                                           static_cast<hipStream_t>(stream)));
 }
 
-size_t fox_attn_bwd_ds_store_bytes(int dtype, int B, int H, int L, int d) {
+size_t fox_attn_bwd_ds_store_bytes(fox_dtype_t dtype, int B, int H, int L, int d) {
   if (check_dims(B, H, L, d) || check_dtype_d(dtype, d) || dtype != FOX_DTYPE_BF16) return 0;
   return fox::ds_store_bytes(B * H, L);
 }
 
-int fox_attn_bwd_dkdv_store(int dtype, const void* q, const void* k, const void* v,
+fox_status_t fox_attn_bwd_dkdv_store(fox_dtype_t dtype, const void* q, const void* k, const void* v,
                             const float* c, const float* lse, const void* d_o,
                             const float* delta, void* dk, void* dv, float* dc_k, void* ds_store,
                             size_t ds_store_bytes, int B, int H, int L, int d, float scale,
-                            void* stream) {
+                            hipStream_t stream) {
   if (!q || !k || !v || !c || !lse || !d_o || !delta || !dk || !dv || !dc_k) return FOX_ERR_NULL;
-  int st = check_dims(B, H, L, d);
+  fox_status_t st = check_dims(B, H, L, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -234,11 +234,11 @@ int fox_attn_bwd_dkdv_store(int dtype, const void* q, const void* k, const void*
                                                   scale, static_cast<hipStream_t>(stream)));
 }
 
-int fox_attn_bwd_dq_stored(int dtype, const void* k, const void* ds_store, size_t ds_store_bytes,
+fox_status_t fox_attn_bwd_dq_stored(fox_dtype_t dtype, const void* k, const void* ds_store, size_t ds_store_bytes,
                            void* dq, float* dc_q, int B, int H, int L, int d, float scale,
-                           void* stream) {
+                           hipStream_t stream) {
   if (!k || !dq || !dc_q) return FOX_ERR_NULL;
-  int st = check_dims(B, H, L, d);
+  fox_status_t st = check_dims(B, H, L, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -250,20 +250,20 @@ int fox_attn_bwd_dq_stored(int dtype, const void* k, const void* ds_store, size_
                                                  scale, static_cast<hipStream_t>(stream)));
 }
 
-int fox_dlogf_from_dc(const float* dc_q, const float* dc_k, float* d_log_f, int B, int H, int L,
-                      void* stream) {
+fox_status_t fox_dlogf_from_dc(const float* dc_q, const float* dc_k, float* d_log_f, int B, int H, int L,
+                      hipStream_t stream) {
   if (!dc_q || !dc_k || !d_log_f) return FOX_ERR_NULL;
-  int st = check_dims(B, H, L, 1);
+  fox_status_t st = check_dims(B, H, L, 1);
   if (st) return st;
   if (!aligned16(dc_q) || !aligned16(dc_k) || !aligned16(d_log_f)) return FOX_ERR_ALIGN;
   return launch_status(fox::launch_reverse_scan_sum(dc_q, dc_k, d_log_f, B * H, L,
                                                     static_cast<hipStream_t>(stream)));
 }
 
-int fox_dlogit_from_dc(const float* dc_q, const float* dc_k, const float* gate_logit,
-                       float* d_log_f, float* d_logit, int B, int H, int L, void* stream) {
+fox_status_t fox_dlogit_from_dc(const float* dc_q, const float* dc_k, const float* gate_logit,
+                       float* d_log_f, float* d_logit, int B, int H, int L, hipStream_t stream) {
   if (!dc_q || !dc_k || !gate_logit || !d_logit) return FOX_ERR_NULL;
-  int st = check_dims(B, H, L, 1);
+  fox_status_t st = check_dims(B, H, L, 1);
   if (st) return st;
   if (!aligned16(dc_q) || !aligned16(dc_k) || !aligned16(gate_logit) || !aligned16(d_logit) ||
       (d_log_f && !aligned16(d_log_f)))
@@ -272,18 +272,18 @@ int fox_dlogit_from_dc(const float* dc_q, const float* dc_k, const float* gate_l
                                                      B * H, L, static_cast<hipStream_t>(stream)));
 }
 
-size_t fox_attn_decode_workspace_bytes(int dtype, int B, int H, int T, int d) {
+size_t fox_attn_decode_workspace_bytes(fox_dtype_t dtype, int B, int H, int T, int d) {
   if (check_dims(B, H, T, d) || check_dtype_d(dtype, d)) return 0;
   return fox::decode_workspace_bytes(B * H, T, d);
 }
 
-int fox_attn_decode(int dtype, const void* q, const void* k_cache, const void* v_cache,
+fox_status_t fox_attn_decode(fox_dtype_t dtype, const void* q, const void* k_cache, const void* v_cache,
                     float* c_cache, const float* gate_logit_new, void* o, float* lse,
                     void* workspace, size_t workspace_bytes, int B, int H, int T, int d,
-                    float scale, void* stream) {
+                    float scale, hipStream_t stream) {
   if (!q || !k_cache || !v_cache || !c_cache || !gate_logit_new || !o || !lse)
     return FOX_ERR_NULL;
-  int st = check_dims(B, H, T, d);
+  fox_status_t st = check_dims(B, H, T, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -299,10 +299,10 @@ int fox_attn_decode(int dtype, const void* q, const void* k_cache, const void* v
 }
 
 // ------------------------------------------------------- gate-aware skipping
-int fox_row_norm_max(int dtype, const void* x, float* out, int B, int H, int L, int d,
-                     void* stream) {
+fox_status_t fox_row_norm_max(fox_dtype_t dtype, const void* x, float* out, int B, int H, int L, int d,
+                     hipStream_t stream) {
   if (!x || !out) return FOX_ERR_NULL;
-  int st = check_dims(B, H, L, d);
+  fox_status_t st = check_dims(B, H, L, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -311,11 +311,11 @@ int fox_row_norm_max(int dtype, const void* x, float* out, int B, int H, int L, 
                                                 static_cast<hipStream_t>(stream)));
 }
 
-int fox_attn_fwd_skip(int dtype, const void* q, const void* k, const void* v, const float* c,
+fox_status_t fox_attn_fwd_skip(fox_dtype_t dtype, const void* q, const void* k, const void* v, const float* c,
                       const float* q_norm_max, const float* k_norm_max, void* o, float* lse,
-                      int B, int H, int L, int d, float scale, void* stream) {
+                      int B, int H, int L, int d, float scale, hipStream_t stream) {
   if (!q || !k || !v || !c || !q_norm_max || !k_norm_max || !o || !lse) return FOX_ERR_NULL;
-  int st = check_dims(B, H, L, d);
+  fox_status_t st = check_dims(B, H, L, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -331,15 +331,15 @@ int fox_attn_fwd_skip(int dtype, const void* q, const void* k, const void* v, co
                                            s));
 }
 
-int fox_attn_bwd_skip(int dtype, const void* q, const void* k, const void* v, const float* c,
+fox_status_t fox_attn_bwd_skip(fox_dtype_t dtype, const void* q, const void* k, const void* v, const float* c,
                       const void* o, const float* lse, const void* d_o, const float* q_norm_max,
                       const float* k_norm_max, void* dq, void* dk, void* dv, float* d_log_f,
                       void* workspace, size_t workspace_bytes, int B, int H, int L, int d,
-                      float scale, void* stream) {
+                      float scale, hipStream_t stream) {
   if (!q || !k || !v || !c || !o || !lse || !d_o || !q_norm_max || !k_norm_max || !dq || !dk ||
       !dv || !d_log_f)
     return FOX_ERR_NULL;
-  int st = check_dims(B, H, L, d);
+  fox_status_t st = check_dims(B, H, L, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -356,14 +356,14 @@ int fox_attn_bwd_skip(int dtype, const void* q, const void* k, const void* v, co
                                        bf ? k_norm_max : nullptr));
 }
 
-int fox_attn_bwd_skip_stored(int dtype, const void* q, const void* k, const void* v,
+fox_status_t fox_attn_bwd_skip_stored(fox_dtype_t dtype, const void* q, const void* k, const void* v,
                              const float* c, const void* o, const float* lse, const void* d_o,
                              const float* q_norm_max, const float* k_norm_max, void* dq, void* dk,
                              void* dv, float* d_log_f, void* workspace, size_t workspace_bytes,
-                             int B, int H, int L, int d, float scale, void* stream) {
+                             int B, int H, int L, int d, float scale, hipStream_t stream) {
   if (!all_set({q, k, v, c, o, lse, d_o, q_norm_max, k_norm_max, dq, dk, dv, d_log_f}))
     return FOX_ERR_NULL;
-  int st = check_dims(B, H, L, d);
+  fox_status_t st = check_dims(B, H, L, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -379,13 +379,13 @@ int fox_attn_bwd_skip_stored(int dtype, const void* q, const void* k, const void
                                               k_norm_max));
 }
 
-int fox_attn_decode_skip(int dtype, const void* q, const void* k_cache, const void* v_cache,
+fox_status_t fox_attn_decode_skip(fox_dtype_t dtype, const void* q, const void* k_cache, const void* v_cache,
                          float* c_cache, const float* gate_logit_new, const float* k_norm_max,
                          void* o, float* lse, void* workspace, size_t workspace_bytes, int B,
-                         int H, int T, int d, float scale, void* stream) {
+                         int H, int T, int d, float scale, hipStream_t stream) {
   if (!q || !k_cache || !v_cache || !c_cache || !gate_logit_new || !k_norm_max || !o || !lse)
     return FOX_ERR_NULL;
-  int st = check_dims(B, H, T, d);
+  fox_status_t st = check_dims(B, H, T, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -402,7 +402,7 @@ int fox_attn_decode_skip(int dtype, const void* q, const void* k_cache, const vo
 }
 
 // ---------------------------------------------------------------- fixed gates
-int fox_fixed_gate_init(float* gate_bias, int H, float t_min, float t_max) {
+fox_status_t fox_fixed_gate_init(float* gate_bias, int H, float t_min, float t_max) {
   if (!gate_bias) return FOX_ERR_NULL;
   if (H <= 0 || !(t_min > 0.0f) || !(t_max >= t_min) || !isfinite(t_max)) return FOX_ERR_SHAPE;
   for (int h = 0; h < H; ++h) {
@@ -414,11 +414,11 @@ int fox_fixed_gate_init(float* gate_bias, int H, float t_min, float t_max) {
   return FOX_OK;
 }
 
-int fox_attn_fwd_fixed_gate(int dtype, const void* q, const void* k, const void* v,
+fox_status_t fox_attn_fwd_fixed_gate(fox_dtype_t dtype, const void* q, const void* k, const void* v,
                             const float* gate_bias, void* o, float* lse, int B, int H, int L, int d,
-                            float scale, void* stream) {
+                            float scale, hipStream_t stream) {
   if (!q || !k || !v || !gate_bias || !o || !lse) return FOX_ERR_NULL;
-  int st = check_dims(B, H, L, d);
+  fox_status_t st = check_dims(B, H, L, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -433,19 +433,19 @@ int fox_attn_fwd_fixed_gate(int dtype, const void* q, const void* k, const void*
                                            (float*)o, lse, B * H, L, d, scale, s));
 }
 
-size_t fox_attn_bwd_fixed_gate_workspace_bytes(int dtype, int B, int H, int L, int d) {
+size_t fox_attn_bwd_fixed_gate_workspace_bytes(fox_dtype_t dtype, int B, int H, int L, int d) {
   if (check_dims(B, H, L, d) || check_dtype_d(dtype, d)) return 0;
   return fox::bwd_fixed_workspace_bytes(B * H, L);
 }
 
-int fox_attn_bwd_fixed_gate(int dtype, const void* q, const void* k, const void* v,
+fox_status_t fox_attn_bwd_fixed_gate(fox_dtype_t dtype, const void* q, const void* k, const void* v,
                             const float* gate_bias, const void* o, const float* lse,
                             const void* d_o, void* dq, void* dk, void* dv, float* d_gate_bias,
                             void* workspace, size_t workspace_bytes, int B, int H, int L, int d,
-                            float scale, void* stream) {
+                            float scale, hipStream_t stream) {
   if (!q || !k || !v || !gate_bias || !o || !lse || !d_o || !dq || !dk || !dv)
     return FOX_ERR_NULL;
-  int st = check_dims(B, H, L, d);
+  fox_status_t st = check_dims(B, H, L, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -461,19 +461,19 @@ int fox_attn_bwd_fixed_gate(int dtype, const void* q, const void* k, const void*
                                              L, d, scale, static_cast<hipStream_t>(stream)));
 }
 
-size_t fox_attn_bwd_fixed_gate_stored_workspace_bytes(int dtype, int B, int H, int L, int d) {
+size_t fox_attn_bwd_fixed_gate_stored_workspace_bytes(fox_dtype_t dtype, int B, int H, int L, int d) {
   if (check_dims(B, H, L, d) || check_dtype_d(dtype, d) || dtype != FOX_DTYPE_BF16) return 0;
   return fox::bwd_fixed_stored_workspace_bytes(B * H, L);
 }
 
 // fox_attn_bwd_fixed_gate_stored and its skipping twin (norms non-NULL)
-static int bwd_fixed_stored(int dtype, const void* q, const void* k, const void* v,
+static fox_status_t bwd_fixed_stored(fox_dtype_t dtype, const void* q, const void* k, const void* v,
                             const float* gate_bias, const void* o, const float* lse,
                             const void* d_o, const float* q_norm_max, const float* k_norm_max,
                             void* dq, void* dk, void* dv, float* d_gate_bias, void* workspace,
                             size_t workspace_bytes, int B, int H, int L, int d, float scale,
-                            void* stream) {
-  int st = check_dims(B, H, L, d);
+                            hipStream_t stream) {
+  fox_status_t st = check_dims(B, H, L, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -491,35 +491,35 @@ static int bwd_fixed_stored(int dtype, const void* q, const void* k, const void*
                                                     q_norm_max, k_norm_max));
 }
 
-int fox_attn_bwd_fixed_gate_stored(int dtype, const void* q, const void* k, const void* v,
+fox_status_t fox_attn_bwd_fixed_gate_stored(fox_dtype_t dtype, const void* q, const void* k, const void* v,
                                    const float* gate_bias, const void* o, const float* lse,
                                    const void* d_o, void* dq, void* dk, void* dv,
                                    float* d_gate_bias, void* workspace, size_t workspace_bytes,
-                                   int B, int H, int L, int d, float scale, void* stream) {
+                                   int B, int H, int L, int d, float scale, hipStream_t stream) {
   if (!all_set({q, k, v, gate_bias, o, lse, d_o, dq, dk, dv})) return FOX_ERR_NULL;
   return bwd_fixed_stored(dtype, q, k, v, gate_bias, o, lse, d_o, nullptr, nullptr, dq, dk, dv,
                           d_gate_bias, workspace, workspace_bytes, B, H, L, d, scale, stream);
 }
 
-int fox_attn_bwd_fixed_gate_skip_stored(int dtype, const void* q, const void* k, const void* v,
+fox_status_t fox_attn_bwd_fixed_gate_skip_stored(fox_dtype_t dtype, const void* q, const void* k, const void* v,
                                         const float* gate_bias, const void* o, const float* lse,
                                         const void* d_o, const float* q_norm_max,
                                         const float* k_norm_max, void* dq, void* dk, void* dv,
                                         float* d_gate_bias, void* workspace,
                                         size_t workspace_bytes, int B, int H, int L, int d,
-                                        float scale, void* stream) {
+                                        float scale, hipStream_t stream) {
   if (!all_set({q, k, v, gate_bias, o, lse, d_o, q_norm_max, k_norm_max, dq, dk, dv}))
     return FOX_ERR_NULL;
   return bwd_fixed_stored(dtype, q, k, v, gate_bias, o, lse, d_o, q_norm_max, k_norm_max, dq, dk,
                           dv, d_gate_bias, workspace, workspace_bytes, B, H, L, d, scale, stream);
 }
 
-int fox_attn_decode_fixed_gate(int dtype, const void* q, const void* k_cache,
+fox_status_t fox_attn_decode_fixed_gate(fox_dtype_t dtype, const void* q, const void* k_cache,
                                const void* v_cache, const float* gate_bias, void* o, float* lse,
                                void* workspace, size_t workspace_bytes, int B, int H, int T, int d,
-                               float scale, void* stream) {
+                               float scale, hipStream_t stream) {
   if (!q || !k_cache || !v_cache || !gate_bias || !o || !lse) return FOX_ERR_NULL;
-  int st = check_dims(B, H, T, d);
+  fox_status_t st = check_dims(B, H, T, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -534,12 +534,12 @@ int fox_attn_decode_fixed_gate(int dtype, const void* q, const void* k_cache,
                                                 static_cast<hipStream_t>(stream)));
 }
 
-int fox_attn_fwd_fixed_gate_skip(int dtype, const void* q, const void* k, const void* v,
+fox_status_t fox_attn_fwd_fixed_gate_skip(fox_dtype_t dtype, const void* q, const void* k, const void* v,
                                  const float* gate_bias, const float* q_norm_max,
                                  const float* k_norm_max, void* o, float* lse, int B, int H, int L,
-                                 int d, float scale, void* stream) {
+                                 int d, float scale, hipStream_t stream) {
   if (!all_set({q, k, v, gate_bias, q_norm_max, k_norm_max, o, lse})) return FOX_ERR_NULL;
-  int st = check_dims(B, H, L, d);
+  fox_status_t st = check_dims(B, H, L, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -553,15 +553,15 @@ int fox_attn_fwd_fixed_gate_skip(int dtype, const void* q, const void* k, const 
                                            (float*)o, lse, B * H, L, d, scale, s));
 }
 
-int fox_attn_bwd_fixed_gate_skip(int dtype, const void* q, const void* k, const void* v,
+fox_status_t fox_attn_bwd_fixed_gate_skip(fox_dtype_t dtype, const void* q, const void* k, const void* v,
                                  const float* gate_bias, const void* o, const float* lse,
                                  const void* d_o, const float* q_norm_max,
                                  const float* k_norm_max, void* dq, void* dk, void* dv,
                                  float* d_gate_bias, void* workspace, size_t workspace_bytes,
-                                 int B, int H, int L, int d, float scale, void* stream) {
+                                 int B, int H, int L, int d, float scale, hipStream_t stream) {
   if (!all_set({q, k, v, gate_bias, o, lse, d_o, q_norm_max, k_norm_max, dq, dk, dv}))
     return FOX_ERR_NULL;
-  int st = check_dims(B, H, L, d);
+  fox_status_t st = check_dims(B, H, L, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -578,13 +578,13 @@ int fox_attn_bwd_fixed_gate_skip(int dtype, const void* q, const void* k, const 
                                              bf ? q_norm_max : nullptr, bf ? k_norm_max : nullptr));
 }
 
-int fox_attn_decode_fixed_gate_skip(int dtype, const void* q, const void* k_cache,
+fox_status_t fox_attn_decode_fixed_gate_skip(fox_dtype_t dtype, const void* q, const void* k_cache,
                                     const void* v_cache, const float* gate_bias,
                                     const float* k_norm_max, void* o, float* lse, void* workspace,
                                     size_t workspace_bytes, int B, int H, int T, int d,
-                                    float scale, void* stream) {
+                                    float scale, hipStream_t stream) {
   if (!all_set({q, k_cache, v_cache, gate_bias, k_norm_max, o, lse})) return FOX_ERR_NULL;
-  int st = check_dims(B, H, T, d);
+  fox_status_t st = check_dims(B, H, T, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -601,14 +601,14 @@ int fox_attn_decode_fixed_gate_skip(int dtype, const void* q, const void* k_cach
 // ---------------------------------------------------------------------------
 // FoX (Pro) prologue and epilogue
 // ---------------------------------------------------------------------------
-int fox_pro_prologue(int dtype, const void* q_raw, const void* k_raw, const void* v_raw,
+fox_status_t fox_pro_prologue(fox_dtype_t dtype, const void* q_raw, const void* k_raw, const void* v_raw,
                      const float* k_shift_logit, const float* v_shift_logit,
                      const float* q_norm_weight, const float* k_norm_weight, float eps, void* q,
-                     void* k, void* v, int B, int H, int L, int d, void* stream) {
+                     void* k, void* v, int B, int H, int L, int d, hipStream_t stream) {
   if (!all_set({q_raw, k_raw, v_raw, k_shift_logit, v_shift_logit, q_norm_weight, k_norm_weight,
                 q, k, v}))
     return FOX_ERR_NULL;
-  int st = check_dims(B, H, L, d);
+  fox_status_t st = check_dims(B, H, L, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -621,24 +621,24 @@ int fox_pro_prologue(int dtype, const void* q_raw, const void* k_raw, const void
       k_norm_weight, eps, q, k, v, H, B * H, L, d, static_cast<hipStream_t>(stream)));
 }
 
-size_t fox_pro_prologue_bwd_workspace_bytes(int dtype, int B, int H, int L, int d) {
+size_t fox_pro_prologue_bwd_workspace_bytes(fox_dtype_t dtype, int B, int H, int L, int d) {
   if (check_dims(B, H, L, d) || check_dtype_d(dtype, d)) return 0;
   return fox::pro_prologue_bwd_workspace_bytes(B * H, L, d);
 }
 
-int fox_pro_prologue_bwd(int dtype, const void* q_raw, const void* k_raw, const void* v_raw,
+fox_status_t fox_pro_prologue_bwd(fox_dtype_t dtype, const void* q_raw, const void* k_raw, const void* v_raw,
                          const float* k_shift_logit, const float* v_shift_logit,
                          const float* q_norm_weight, const float* k_norm_weight, float eps,
                          const void* dq, const void* dk, const void* dv, void* dq_raw,
                          void* dk_raw, void* dv_raw, float* dk_shift_logit,
                          float* dv_shift_logit, float* dq_norm_weight, float* dk_norm_weight,
                          void* workspace, size_t workspace_bytes, int B, int H, int L, int d,
-                         void* stream) {
+                         hipStream_t stream) {
   if (!all_set({q_raw, k_raw, v_raw, k_shift_logit, v_shift_logit, q_norm_weight, k_norm_weight,
                 dq, dk, dv, dq_raw, dk_raw, dv_raw, dk_shift_logit, dv_shift_logit,
                 dq_norm_weight, dk_norm_weight}))
     return FOX_ERR_NULL;
-  int st = check_dims(B, H, L, d);
+  fox_status_t st = check_dims(B, H, L, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -657,11 +657,11 @@ int fox_pro_prologue_bwd(int dtype, const void* q_raw, const void* k_raw, const 
       static_cast<hipStream_t>(stream)));
 }
 
-int fox_pro_output_gate(int dtype, const void* o, const void* g_logit,
+fox_status_t fox_pro_output_gate(fox_dtype_t dtype, const void* o, const void* g_logit,
                         const float* o_norm_weight, float eps, void* y, int B, int H, int L,
-                        int d, void* stream) {
+                        int d, hipStream_t stream) {
   if (!all_set({o, g_logit, o_norm_weight, y})) return FOX_ERR_NULL;
-  int st = check_dims(B, H, L, d);
+  fox_status_t st = check_dims(B, H, L, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -672,11 +672,11 @@ int fox_pro_output_gate(int dtype, const void* o, const void* g_logit,
                                             static_cast<hipStream_t>(stream)));
 }
 
-int fox_attn_fwd_pro(int dtype, const void* q, const void* k, const void* v, const float* c,
+fox_status_t fox_attn_fwd_pro(fox_dtype_t dtype, const void* q, const void* k, const void* v, const float* c,
                      const void* g_logit, const float* o_norm_weight, float eps, void* o,
-                     float* lse, void* y, int B, int H, int L, int d, float scale, void* stream) {
+                     float* lse, void* y, int B, int H, int L, int d, float scale, hipStream_t stream) {
   if (!all_set({q, k, v, c, g_logit, o_norm_weight, o, lse, y})) return FOX_ERR_NULL;
-  int st = check_dims(B, H, L, d);
+  fox_status_t st = check_dims(B, H, L, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -694,23 +694,23 @@ int fox_attn_fwd_pro(int dtype, const void* q, const void* k, const void* v, con
   return launch_status(e);
 }
 
-size_t fox_attn_bwd_pro_workspace_bytes(int dtype, int B, int H, int L, int d) {
+size_t fox_attn_bwd_pro_workspace_bytes(fox_dtype_t dtype, int B, int H, int L, int d) {
   if (check_dims(B, H, L, d) || check_dtype_d(dtype, d)) return 0;
   return fox::bwd_pro_workspace_bytes(dtype == FOX_DTYPE_BF16, B * H, L, d);
 }
 
 // fox_attn_bwd_pro and fox_attn_bwd_pro_stored: the same checks, the attention
 // backward recomputing or keeping dS.
-static int attn_bwd_pro(bool keep_ds, int dtype, const void* q, const void* k, const void* v,
+static fox_status_t attn_bwd_pro(bool keep_ds, fox_dtype_t dtype, const void* q, const void* k, const void* v,
                         const float* c, const void* o, const float* lse, const void* g_logit,
                         const float* o_norm_weight, float eps, const void* dy, void* dq,
                         void* dk, void* dv, float* d_log_f, void* dg_logit, float* do_norm_weight,
                         void* workspace, size_t workspace_bytes, int B, int H, int L, int d,
-                        float scale, void* stream) {
+                        float scale, hipStream_t stream) {
   if (!all_set({q, k, v, c, o, lse, g_logit, o_norm_weight, dy, dq, dk, dv, d_log_f, dg_logit,
                 do_norm_weight}))
     return FOX_ERR_NULL;
-  int st = check_dims(B, H, L, d);
+  fox_status_t st = check_dims(B, H, L, d);
   if (st) return st;
   st = check_dtype_d(dtype, d);
   if (st) return st;
@@ -730,37 +730,37 @@ static int attn_bwd_pro(bool keep_ds, int dtype, const void* q, const void* k, c
                                            static_cast<hipStream_t>(stream), keep_ds));
 }
 
-int fox_attn_bwd_pro(int dtype, const void* q, const void* k, const void* v, const float* c,
+fox_status_t fox_attn_bwd_pro(fox_dtype_t dtype, const void* q, const void* k, const void* v, const float* c,
                      const void* o, const float* lse, const void* g_logit,
                      const float* o_norm_weight, float eps, const void* dy, void* dq, void* dk,
                      void* dv, float* d_log_f, void* dg_logit, float* do_norm_weight,
                      void* workspace, size_t workspace_bytes, int B, int H, int L, int d,
-                     float scale, void* stream) {
+                     float scale, hipStream_t stream) {
   return attn_bwd_pro(false, dtype, q, k, v, c, o, lse, g_logit, o_norm_weight, eps, dy, dq, dk,
                       dv, d_log_f, dg_logit, do_norm_weight, workspace, workspace_bytes, B, H, L,
                       d, scale, stream);
 }
 
-size_t fox_attn_bwd_pro_stored_workspace_bytes(int dtype, int B, int H, int L, int d) {
+size_t fox_attn_bwd_pro_stored_workspace_bytes(fox_dtype_t dtype, int B, int H, int L, int d) {
   if (check_dims(B, H, L, d) || check_dtype_d(dtype, d) || dtype != FOX_DTYPE_BF16) return 0;
   return fox::bwd_pro_stored_workspace_bytes(B * H, L, d);
 }
 
-int fox_attn_bwd_pro_stored(int dtype, const void* q, const void* k, const void* v,
+fox_status_t fox_attn_bwd_pro_stored(fox_dtype_t dtype, const void* q, const void* k, const void* v,
                             const float* c, const void* o, const float* lse, const void* g_logit,
                             const float* o_norm_weight, float eps, const void* dy, void* dq,
                             void* dk, void* dv, float* d_log_f, void* dg_logit,
                             float* do_norm_weight, void* workspace, size_t workspace_bytes, int B,
-                            int H, int L, int d, float scale, void* stream) {
+                            int H, int L, int d, float scale, hipStream_t stream) {
   return attn_bwd_pro(true, dtype, q, k, v, c, o, lse, g_logit, o_norm_weight, eps, dy, dq, dk,
                       dv, d_log_f, dg_logit, do_norm_weight, workspace, workspace_bytes, B, H, L,
                       d, scale, stream);
 }
 
-int fox_gate_projection(int dtype, const void* x, const float* w_f, const float* b_f,
-                        float* gate_logit, int B, int L, int H, int M, void* stream) {
+fox_status_t fox_gate_projection(fox_dtype_t dtype, const void* x, const float* w_f, const float* b_f,
+                        float* gate_logit, int B, int L, int H, int M, hipStream_t stream) {
   if (!all_set({x, w_f, gate_logit})) return FOX_ERR_NULL;
-  int st = check_projection(dtype, B, L, H, M);
+  fox_status_t st = check_projection(dtype, B, L, H, M);
   if (st) return st;
   if (!all_aligned16({x, w_f, gate_logit})) return FOX_ERR_ALIGN;
   return launch_status(fox::launch_gate_proj_fwd(dtype == FOX_DTYPE_BF16, x, w_f, b_f, gate_logit,
@@ -768,16 +768,16 @@ int fox_gate_projection(int dtype, const void* x, const float* w_f, const float*
                                                  static_cast<hipStream_t>(stream)));
 }
 
-size_t fox_gate_projection_bwd_workspace_bytes(int dtype, int B, int L, int H, int M) {
+size_t fox_gate_projection_bwd_workspace_bytes(fox_dtype_t dtype, int B, int L, int H, int M) {
   if (check_projection(dtype, B, L, H, M)) return 0;
   return fox::gate_proj_bwd_workspace_bytes(B * L, H, M);
 }
 
-int fox_gate_projection_bwd(int dtype, const void* x, const float* w_f, const float* d_logit,
+fox_status_t fox_gate_projection_bwd(fox_dtype_t dtype, const void* x, const float* w_f, const float* d_logit,
                             void* dx, float* dw_f, float* db_f, void* workspace,
-                            size_t workspace_bytes, int B, int L, int H, int M, void* stream) {
+                            size_t workspace_bytes, int B, int L, int H, int M, hipStream_t stream) {
   if (!all_set({x, w_f, d_logit, dw_f})) return FOX_ERR_NULL;
-  int st = check_projection(dtype, B, L, H, M);
+  fox_status_t st = check_projection(dtype, B, L, H, M);
   if (st) return st;
   if (!all_aligned16({x, w_f, d_logit, dw_f}) || (dx && !aligned16(dx))) return FOX_ERR_ALIGN;
   if (!workspace || workspace_bytes < fox::gate_proj_bwd_workspace_bytes(B * L, H, M))

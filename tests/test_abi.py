@@ -35,6 +35,36 @@ def test_header_declares_the_boundary():
         assert n in names
 
 
+def test_header_compiles_as_c_and_cpp(tmp_path):
+    """fox.h is self-contained for C (C99) and C++ consumers, its enums are
+    int-sized, and the prototypes use the boundary's own types: fox_status_t
+    results, fox_dtype_t dtypes and hipStream_t streams."""
+    import shutil
+    import subprocess
+    src = tmp_path / "use_fox.c"
+    src.write_text(
+        '#include "fox.h"\n'
+        "typedef char status_is_int[sizeof(fox_status_t) == sizeof(int) ? 1 : -1];\n"
+        "typedef char dtype_is_int[sizeof(fox_dtype_t) == sizeof(int) ? 1 : -1];\n"
+        "static fox_status_t (*fwd)(fox_dtype_t, const void*, const void*, const void*,\n"
+        "    const float*, void*, float*, int, int, int, int, float, hipStream_t) = fox_attn_fwd;\n"
+        "static fox_status_t (*bwd)(fox_dtype_t, const void*, const void*, const void*,\n"
+        "    const float*, const void*, const float*, const void*, void*, void*, void*, float*,\n"
+        "    void*, size_t, int, int, int, int, float, hipStream_t) = fox_attn_bwd;\n"
+        "int main(void) { return (fwd && bwd) ? (int)FOX_OK : 1; }\n")
+    inc = ["-I", os.path.join(ROOT, "include"), "-I", "/opt/rocm/include",
+           "-D__HIP_PLATFORM_AMD__"]
+    for cc, std, lang in (("gcc", "-std=c99", "c"), ("g++", "-std=c++17", "c++")):
+        if shutil.which(cc) is None:
+            pytest.skip(f"{cc} not available")
+        r = subprocess.run([cc, std, "-x", lang, "-Wall", "-Werror", "-fsyntax-only", *inc,
+                            str(src)], capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr
+    text = open(HEADER).read()
+    assert "void* stream" not in text and "int dtype" not in text
+    assert re.search(r"fox_status_t fox_attn_bwd\(fox_dtype_t dtype", text)
+
+
 def test_every_declared_symbol_is_exported(lib):
     for n in declared_symbols():
         assert hasattr(lib, n), f"{n} is declared in fox.h but not exported"
