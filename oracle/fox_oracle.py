@@ -50,7 +50,8 @@ Readings of the paper this oracle takes (where it is silent or garbled):
     multiplication by exp(m_old - m_new) (the FlashAttention-2 rescale); the
     oracle needs no online softmax, so it simply uses the plain softmax;
   * Alg. 2's rowsum(dO o O) "in R^d" is one value per row (R^N);
-  * Delta uses the exact O here (the oracle has no rounded O);
+  * Delta uses the exact O by default; with o_dtype, the O that Alg. 2 reads
+    back from HBM, i.e. O rounded to the dtype it was stored in;
   * decode: the query at position T attends to keys 1..T including itself.
   * Pro layer: RMSNorm(x) = x / sqrt(mean(x^2) + eps) * w with per-head
     weights and eps an argument; the token shift of t = 1 mixes with zero.
@@ -129,15 +130,20 @@ def forward_head_from_c(q, k, v, c, scale: float, rows=None, return_A: bool = Fa
     return O, LSE
 
 
-def backward_head_from_c(q, k, v, c, dO, scale: float, return_dS: bool = False):
+def backward_head_from_c(q, k, v, c, dO, scale: float, return_dS: bool = False,
+                         o_dtype=None):
     """Gradients of sum(O * dO) for one head, by Alg. 2's formulas on full matrices.
 
-    Returns dQ, dK, dV [L, d] and dc [L] (= dc^q + dc^k, Alg. 2's last steps)."""
+    Returns dQ, dK, dV [L, d] and dc [L] (= dc^q + dc^k, Alg. 2's last steps).
+    Alg. 2 reads O back from HBM for Delta; o_dtype (e.g. torch.bfloat16) is the
+    dtype O was stored in there, and Delta then uses O rounded to it (round to
+    nearest even); None uses the exact O."""
     q, k, v, c, dO = _f64(q), _f64(k), _f64(v), _f64(c), _f64(dO)
     O, _, A = forward_head_from_c(q, k, v, c, scale, return_A=True)
     dV = A.T @ dO
     dA = dO @ v.T
-    delta = (dO * O).sum(dim=1, keepdim=True)          # rowsum(dO o O), one per row
+    O_read = O if o_dtype is None else O.to(o_dtype).to(F64)
+    delta = (dO * O_read).sum(dim=1, keepdim=True)     # rowsum(dO o O), one per row
     dS = A * (dA - delta)                               # masked entries: A = 0 there
     dQ = scale * (dS @ k)
     dK = scale * (dS.T @ q)
@@ -182,23 +188,26 @@ def forward(q, k, v, logit, scale: float, heads=None, rows=None):
     return forward_from_logf(q, k, v, log_sigmoid(logit), scale, heads, rows)
 
 
-def backward_from_logf(q, k, v, log_f, dO, scale: float, heads=None):
-    """dQ, dK, dV [B,H,L,d] and d(log f) [B,H,L], fp64 (NaN outside `heads`)."""
+def backward_from_logf(q, k, v, log_f, dO, scale: float, heads=None, o_dtype=None):
+    """dQ, dK, dV [B,H,L,d] and d(log f) [B,H,L], fp64 (NaN outside `heads`);
+    o_dtype as for backward_head_from_c."""
     B, H, L, d = q.shape
     c = prefix_c(log_f)
     dQ = torch.full((B, H, L, d), math.nan, dtype=F64)
     dK = dQ.clone()
     dV = dQ.clone()
     dlogf = torch.full((B, H, L), math.nan, dtype=F64)
+    kw = {} if o_dtype is None else {"o_dtype": o_dtype}
     for b, h in _heads(B, H, heads):
-        gq, gk, gv, dc = backward_head_from_c(q[b, h], k[b, h], v[b, h], c[b, h], dO[b, h], scale)
+        gq, gk, gv, dc = backward_head_from_c(q[b, h], k[b, h], v[b, h], c[b, h], dO[b, h], scale,
+                                              **kw)
         dQ[b, h], dK[b, h], dV[b, h] = gq, gk, gv
         dlogf[b, h] = reverse_cumsum(dc)
     return dQ, dK, dV, dlogf
 
 
-def backward(q, k, v, logit, dO, scale: float, heads=None):
-    return backward_from_logf(q, k, v, log_sigmoid(logit), dO, scale, heads)
+def backward(q, k, v, logit, dO, scale: float, heads=None, o_dtype=None):
+    return backward_from_logf(q, k, v, log_sigmoid(logit), dO, scale, heads, o_dtype)
 
 
 def gate_backward(logit, d_log_f) -> torch.Tensor:

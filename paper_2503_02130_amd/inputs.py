@@ -174,6 +174,40 @@ def projection_inputs(B: int, L: int, H: int, M: int, dtype: str, seed: int,
     }
 
 
+def rescale_inputs(B: int, H: int, L: int, d: int, dtype: str, gate: Tuple, seed: int,
+                   device="cpu") -> Dict[str, torch.Tensor]:
+    """Inputs whose softmax rows are dominated by a few early keys: the shape of
+    attention-sink rows.  Per (b, h) a random unit direction u; every query is
+    sqrt(d) u plus N(0, 0.3^2) noise, so that s q.k_j is about u.k_j for the
+    N(0, 1) keys; a key in each of up to five early 64-key tiles (0, 3, .., 12) is
+    a multiple of u whose score is 12 nats for the latest and 7 nats more for each
+    earlier one;
+    the key at every 64-key tile start is -3 sqrt(d) u + noise, so the first query
+    of a tile sees its own key at a very low score.  With the 1/sqrt(d) scale
+    these give scores far above each query's nearby ones.  dO ~ N(0, 1)."""
+    g = _gen(seed, device)
+    f32 = dict(generator=g, device=device, dtype=torch.float32)
+    u = torch.randn((B, H, 1, d), **f32)
+    u = u / torch.linalg.vector_norm(u, dim=-1, keepdim=True)
+    sd = math.sqrt(d)
+    q = sd * u + 0.3 * torch.randn((B, H, L, d), **f32)
+    k = torch.randn((B, H, L, d), **f32)
+    n_tiles = (L + 63) // 64
+    planted = [t for t in range(0, min(n_tiles - 1, 15), 3)]  # tiles 0, 3, .., 12
+    for rank, t in enumerate(reversed(planted)):             # later tile, lower score
+        k[:, :, 64 * t + 17] = (12.0 + 7.0 * rank) * u[:, :, 0]
+    for t in range(1, n_tiles):
+        k[:, :, 64 * t] = -3.0 * sd * u[:, :, 0] + 0.3 * torch.randn((B, H, d), **f32)
+    dt = DTYPES[dtype]
+    return {
+        "q": q.to(dt),
+        "k": k.to(dt),
+        "v": randn((B, H, L, d), dtype, g, device),
+        "logit": gate_logits(gate, B, H, L, g, device),
+        "do": randn((B, H, L, d), dtype, g, device),
+    }
+
+
 def workload_inputs(w: Workload, device="cpu", seed: int = None) -> Dict[str, torch.Tensor]:
     s = w.seed if seed is None else seed
     if w.kind == "decode":

@@ -617,7 +617,39 @@ def pin_p21_gate_projection_backward(ora, B=2, L=4, M=6, H=3, seed=21):
     _fd_check(f, b, db, 1e-4, 1e-7, "db")
 
 
+# --------------------------------------------------------------------------- P22
+def pin_p22_delta_from_stored_o(ora):
+    """Alg. 2 reads O back from HBM for Delta = rowsum(dO o O).  With O stored in
+    bf16, L = 2 written out by hand: q = 0 and log f = 0 give A_21 = A_22 = 1/2;
+    v = (1, 2^-8) makes o_2 = 1/2 + 2^-9, a tie that bf16 (round to nearest even)
+    sends to 1/2; dO = (1, g) with g = 1 + 2^-9 (not a bf16 value, so a rounded
+    dO would show).  Then Delta_2 = g/2, dS_21 = g/4, dS_22 = g (2^-9 - 1/4),
+    dS_1 = 0, dQ_2 = s g (k_1/4 + k_2 (2^-9 - 1/4)), dc = (-g/4, g/4) and
+    d(log f) = (0, g/4); dV = A^T dO = (1 + g/2, g/2).  With the exact O every
+    2^-9 term changes (Delta_2 = g (1/2 + 2^-9))."""
+    g = 1.0 + 2.0 ** -9
+    q = torch.zeros(1, 1, 2, 1, dtype=F64)
+    k = torch.tensor([[[[1.0], [3.0]]]], dtype=F64)
+    v = torch.tensor([[[[1.0], [2.0 ** -8]]]], dtype=F64)
+    dO = torch.tensor([[[[1.0], [g]]]], dtype=F64)
+    lf = torch.zeros(1, 1, 2, dtype=F64)
+    s = 0.75
+    dQ, dK, dV, dlf = ora.backward_from_logf(q, k, v, lf, dO, s, o_dtype=torch.bfloat16)
+    _close(dQ[0, 0, 1, 0], s * g * (1.0 / 4 + 3.0 * (2.0 ** -9 - 1.0 / 4)), 1e-15, "P22 dQ_2")
+    _close(dQ[0, 0, 0, 0], 0.0, 1e-15, "P22 dQ_1")
+    _close(dK[0, 0], torch.zeros(2, 1, dtype=F64), 1e-15, "P22 dK (q = 0)")
+    _close(dV[0, 0, :, 0], torch.tensor([1.0 + g / 2, g / 2], dtype=F64), 1e-15, "P22 dV")
+    _close(dlf[0, 0], torch.tensor([0.0, g / 4], dtype=F64), 1e-15, "P22 d(log f)")
+    # the exact O: Delta_2 = g (1/2 + 2^-9), dS_21 = g (1/4 - 2^-10), dS_22 = g (2^-10 - 1/4)
+    dQ, _, _, dlf = ora.backward_from_logf(q, k, v, lf, dO, s)
+    _close(dQ[0, 0, 1, 0], s * g * ((1.0 / 4 - 2.0 ** -10) + 3.0 * (2.0 ** -10 - 1.0 / 4)), 1e-15,
+           "P22 dQ_2 (exact O)")
+    _close(dlf[0, 0], torch.tensor([0.0, g * (1.0 / 4 - 2.0 ** -10)], dtype=F64), 1e-15,
+           "P22 d(log f) (exact O)")
+
+
 ALL_PINS = [
+    pin_p22_delta_from_stored_o,
     pin_p1_zero_forgetting_is_softmax_attention,
     pin_p2_full_forgetting,
     pin_p3_constant_gate_is_alibi,

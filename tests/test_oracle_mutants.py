@@ -50,11 +50,16 @@ def _m_logsigmoid_max(m):
 
 
 def _patch_backward(m, variant):
-    def bwd(q, k, v, c, dO, scale, return_dS=False):
+    def bwd(q, k, v, c, dO, scale, return_dS=False, o_dtype=None):
         q, k, v, c, dO = (m._f64(t) for t in (q, k, v, c, dO))
         O, _, A = m.forward_head_from_c(q, k, v, c, scale, return_A=True)
         dV = A @ dO if variant == "dV_untransposed" else A.T @ dO
         dA = dO @ v.T
+        if o_dtype is not None:
+            if variant == "delta_rounds_dO":
+                dO = dO.to(o_dtype).to(torch.float64)
+            else:
+                O = O.to(o_dtype).to(torch.float64)
         delta = (dO * O).sum(1, keepdim=True)
         if variant == "delta_from_dA":
             delta = dA.sum(1, keepdim=True)
@@ -252,6 +257,7 @@ MUTANTS = {
     "dK_no_scale": lambda m: _patch_backward(m, "dK_no_scale"),
     "delta_from_dA": lambda m: _patch_backward(m, "delta_from_dA"),
     "dc_sign": lambda m: _patch_backward(m, "dc_sign"),
+    "delta_rounds_dO": lambda m: _patch_backward(m, "delta_rounds_dO"),
     "forward_cumsum_for_dlogf": _m_forward_cumsum,
     "lse_without_max": _m_lse_no_max,
     "decode_bias_sign": _m_decode_sign,
