@@ -230,6 +230,160 @@ def bench_train(w, steps, warmup):
             "skip_ms": t_skip.mean_ms(), "store_bytes": store_bytes}
 
 
+def _capture(fn):
+    """fn's launches captured in a HIP graph (after one warm-up run on a side
+    stream, as graph capture requires)."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        fn()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        fn()
+    torch.cuda.synchronize()
+    return g
+
+
+def _graph_ms(g, reps, warmup):
+    """Mean time of one replay: `reps` back-to-back replays bracketed by HIP events
+    on the current stream (the stream replays run on), after `warmup` replays."""
+    for _ in range(warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        g.replay()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / reps
+
+
+def bench_train_graph(w, steps, warmup):
+    """The training step of a short-sequence workload (about 0.5 ms per step, so
+    launches from Python would show between the kernels): the step keeping dS
+    and the step recomputing P, each captured once in a HIP graph and replayed
+    back to back; each stage is also captured alone for its own time.  Replays
+    must reproduce the eager step bit for bit."""
+    dev = torch.device("cuda:0")
+    x = inputs.workload_inputs(w, device=dev)
+    s = fox.default_scale(w.d)
+    B, H, L, d = w.B, w.H, w.L, w.d
+    c = torch.empty((B, H, L), device=dev)
+    o = torch.empty_like(x["q"])
+    lse = torch.empty((B, H, L), device=dev)
+    dq, dk, dv = torch.empty_like(x["q"]), torch.empty_like(x["k"]), torch.empty_like(x["v"])
+    dlf, dlogit, delta, dcq, dck = (torch.empty((B, H, L), device=dev) for _ in range(5))
+    store = torch.empty(fox.fox_attn_bwd_ds_store_bytes(x["q"].dtype, B, H, L, d), device=dev,
+                        dtype=torch.uint8)
+    stage = {
+        "gate_prefix": lambda: fox.fox_gate_prefix(x["logit"], c=c),
+        "fwd": lambda: fox.fox_attn_fwd(x["q"], x["k"], x["v"], c, s, o=o, lse=lse),
+        "delta": lambda: fox.fox_attn_bwd_delta(o, x["do"], delta=delta),
+        "dkdv_store": lambda: fox.fox_attn_bwd_dkdv_store(x["q"], x["k"], x["v"], c, lse,
+                                                          x["do"], delta, store, s, dk=dk, dv=dv,
+                                                          dc_k=dck),
+        "dq_stored": lambda: fox.fox_attn_bwd_dq_stored(x["k"], store, s, dq=dq, dc_q=dcq),
+        "dkdv": lambda: fox.fox_attn_bwd_dkdv(x["q"], x["k"], x["v"], c, lse, x["do"], delta, s,
+                                              dk=dk, dv=dv, dc_k=dck),
+        "dq": lambda: fox.fox_attn_bwd_dq(x["q"], x["k"], x["v"], c, lse, x["do"], delta, s,
+                                          dq=dq, dc_q=dcq),
+        "scan": lambda: fox.fox_dlogit_from_dc(dcq, dck, x["logit"], d_logit=dlogit,
+                                               d_log_f=dlf),
+    }
+    kept = ("gate_prefix", "fwd", "delta", "dkdv_store", "dq_stored", "scan")
+    recomputed = ("gate_prefix", "fwd", "delta", "dkdv", "dq", "scan")
+    outs = (c, o, lse, dq, dk, dv, dlf, dlogit)
+    res = {}
+    for name, order in (("stored", kept), ("recompute", recomputed)):
+        def step(order=order):
+            for n in order:
+                stage[n]()
+        step()
+        torch.cuda.synchronize()
+        ref = [t.clone() for t in outs]
+        g = _capture(step)
+        res[name + "_ms"] = _graph_ms(g, steps, warmup)
+        if not all(torch.equal(a, b) for a, b in zip(outs, ref)):
+            raise RuntimeError(f"{w.name}: graph replay of the {name} step differs from eager")
+        if not (torch.isfinite(o.float()).all() and torch.isfinite(dlf).all()):
+            raise RuntimeError("non-finite outputs")
+        del g
+    reps = max(steps, 20)
+    for n, fn in stage.items():
+        g = _capture(fn)
+        res[n] = _graph_ms(g, reps, warmup)
+        del g
+    res["store_bytes"] = store.numel()
+    return res
+
+
+def train_graph_summary(w, r):
+    """JSON object of a graph-timed training leg: both backwards, per-stage times
+    and the MFMA roofline of the dominant kernel (dK/dV with the dS store)."""
+    B, H, L, d = w.B, w.H, w.L, w.d
+    fl_f, fl_b = fwd_flops(B, H, L, d), bwd_flops(B, H, L, d)
+    fl_kv = 8.0 * d * causal_pairs(B, H, L)
+    tf = (fl_f + fl_b) / (r["stored_ms"] * 1e-3) / 1e12
+    tf_rc = (fl_f + fl_b) / (r["recompute_ms"] * 1e-3) / 1e12
+    kv = fl_kv / (r["dkdv_store"] * 1e-3) / 1e12
+    kv_rc = fl_kv / (r["dkdv"] * 1e-3) / 1e12
+    fw = fl_f / (r["fwd"] * 1e-3) / 1e12
+    return {
+        "what": "training step (gate prefix -> forward -> backward -> d(logit)) at the 125M-model "
+                "head shape; each step captured in a HIP graph and replayed back to back, each "
+                "stage also captured and replayed alone",
+        "config": {"B": B, "H": H, "L": L, "d": d, "seed": w.seed, "flops_per_step": fl_f + fl_b},
+        "ms_per_step": round(r["stored_ms"], 4), "TFLOP/s": round(tf, 2),
+        "frac_of_peak": round(tf / MFMA_BF16_PEAK_TFLOPS, 4),
+        "backward": "keeping dS (fox_attn_bwd_stored stages, %.2f GB workspace)"
+                    % (r["store_bytes"] / 1e9),
+        "recompute": {"ms_per_step": round(r["recompute_ms"], 4), "TFLOP/s": round(tf_rc, 2),
+                      "frac_of_peak": round(tf_rc / MFMA_BF16_PEAK_TFLOPS, 4),
+                      "dkdv_TFLOP/s": round(kv_rc, 2)},
+        "breakdown_ms": {n: round(r[n], 5) for n in ("gate_prefix", "fwd", "delta", "dkdv_store",
+                                                     "dq_stored", "dkdv", "dq", "scan")},
+        "roofline": {"bound": "mfma", "kernel": "bwd_dkdv_bf16_kernel<64,false,false,true> "
+                     "(fox_attn_bwd_dkdv_store)", "achieved": round(kv, 2),
+                     "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(kv / MFMA_BF16_PEAK_TFLOPS, 4),
+                     "algorithmic_flops_per_launch": fl_kv},
+        "roofline_fwd": {"bound": "mfma", "kernel": "fwd_bf16_kernel<64> (fox_attn_fwd)",
+                         "achieved": round(fw, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
+                         "unit": "TFLOP/s", "frac": round(fw / MFMA_BF16_PEAK_TFLOPS, 4)},
+    }
+
+
+def bench_prefill(w, steps, warmup):
+    """Forward-only workload (the length-extrapolation prefill): gate prefix ->
+    forward, timed per step with events on the call stream."""
+    dev = torch.device("cuda:0")
+    x = inputs.workload_inputs(w, device=dev)
+    s = fox.default_scale(w.d)
+    c = torch.empty((w.B, w.H, w.L), device=dev)
+    o = torch.empty_like(x["q"])
+    lse = torch.empty((w.B, w.H, w.L), device=dev)
+    t_step, t_fwd = EventTimer(), EventTimer()
+
+    def step(timed):
+        with t_step.maybe(timed):
+            fox.fox_gate_prefix(x["logit"], c=c)
+            with t_fwd.maybe(timed):
+                fox.fox_attn_fwd(x["q"], x["k"], x["v"], c, s, o=o, lse=lse)
+
+    for _ in range(warmup):
+        step(False)
+    torch.cuda.synchronize()
+    for _ in range(steps):
+        step(True)
+    torch.cuda.synchronize()
+    if not (torch.isfinite(o.float()).all() and torch.isfinite(lse).all()):
+        raise RuntimeError("non-finite prefill outputs")
+    return {"ms": t_step.mean_ms(), "fwd_ms": t_fwd.mean_ms()}
+
+
 def bench_pro(w, steps, warmup):
     """The FoX (Pro) layer's hot path at the training workload's shape: prologue
     (QK-norm, KV-shift), attention with the output norm and gate fused into the
@@ -360,7 +514,7 @@ def bench_projection(w, steps, warmup):
     return {"B": B, "L": L, "H": H, "M": M, "fwd_ms": tf.mean_ms(), "bwd_ms": tb.mean_ms()}
 
 
-def bench_decode(w, steps, warmup):
+def bench_decode(w, steps, warmup, cpu=False):
     dev = torch.device("cuda:0")
     y = inputs.workload_inputs(w, device=dev)
     T = w.L
@@ -396,15 +550,33 @@ def bench_decode(w, steps, warmup):
     torch.cuda.synchronize()
     if not (torch.equal(o, o2) and torch.equal(lse, lse2)):
         raise RuntimeError("skipping decode differs from the dense decode")
-    return {"ms": t.mean_ms(), "skip_ms": t2.mean_ms()}
+    res = {"ms": t.mean_ms(), "skip_ms": t2.mean_ms()}
+    if cpu:
+        log("[bench] timing the fp64 oracle decode on the host")
+        res["decode_cpu_baseline"] = cpu_baseline_decode(w, y)
+    return res
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            return next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")),
+                        "unknown")
+    except OSError:
+        return "unknown"
+
+
+def _oracle_threads():
+    threads = len(os.sched_getaffinity(0))
+    torch.set_num_threads(threads)
+    return torch.get_num_threads()
 
 
 def cpu_baseline(w, n_heads=4):
     """The fp64 oracle, untouched, on a bounded sample: forward + backward of
     n_heads (batch, head) slices of the workload (n_heads / (B*H) of the step)."""
     import oracle
-    threads = len(os.sched_getaffinity(0))
-    torch.set_num_threads(threads)
+    cores = _oracle_threads()
     x = inputs.attn_inputs(1, n_heads, w.L, w.d, w.dtype, w.gate, w.seed, device="cpu")
     s = fox.default_scale(w.d)
     t0 = time.perf_counter()
@@ -412,17 +584,81 @@ def cpu_baseline(w, n_heads=4):
     oracle.backward(x["q"], x["k"], x["v"], x["logit"], x["do"], s)
     dt = time.perf_counter() - t0
     flops = fwd_flops(1, n_heads, w.L, w.d) + bwd_flops(1, n_heads, w.L, w.d)
-    model = "unknown"
-    try:
-        with open("/proc/cpuinfo") as fh:
-            model = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")),
-                         model)
-    except OSError:
-        pass
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": torch.get_num_threads(),
-            "cpu_model": model, "kind": "oracle",
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": cores,
+            "cpu_model": _cpu_model(), "kind": "oracle", "seconds": round(dt, 2),
             "sample": f"fp64 forward+backward of {n_heads} of {w.B * w.H} (batch, head) slices "
                       f"at L={w.L}, d={w.d}: {dt:.1f} s; value = those slices' causal FLOPs / time"}
+
+
+def cpu_baseline_full(w):
+    """The fp64 oracle on the whole workload (inputs drawn on the host with the
+    workload's shapes, seed and distributions): forward, and backward for the
+    training workloads, over every (batch, head) slice."""
+    import oracle
+    cores = _oracle_threads()
+    x = inputs.workload_inputs(w, device="cpu")
+    s = fox.default_scale(w.d)
+    t0 = time.perf_counter()
+    oracle.forward(x["q"], x["k"], x["v"], x["logit"], s)
+    if w.kind == "fwdbwd":
+        oracle.backward(x["q"], x["k"], x["v"], x["logit"], x["do"], s)
+    dt = time.perf_counter() - t0
+    flops = fwd_flops(w.B, w.H, w.L, w.d) + (bwd_flops(w.B, w.H, w.L, w.d)
+                                             if w.kind == "fwdbwd" else 0.0)
+    what = "forward+backward" if w.kind == "fwdbwd" else "forward"
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+            "seconds": round(dt, 3),
+            "sample": f"full: fp64 {what} of all {w.B * w.H} (batch, head) slices at L={w.L}, "
+                      f"d={w.d}: {dt:.2f} s"}
+
+
+def cpu_baseline_rows(w, n_rows=512):
+    """The fp64 oracle forward on n_rows query rows of one head of each gate group
+    (the oracle computes a row block against all keys, masked, so the whole
+    problem in blocks of n_rows costs L / n_rows blocks per head): the time is
+    extrapolated to every row of every head, and labelled so."""
+    import oracle
+    cores = _oracle_threads()
+    x = inputs.workload_inputs(w, device="cpu")
+    s = fox.default_scale(w.d)
+    heads = (0, w.H - 1)
+    r0 = w.L // 2
+    rows = list(range(r0, r0 + n_rows))
+    t0 = time.perf_counter()
+    for h in heads:
+        sl = {k: v[:1, h:h + 1] for k, v in x.items()}
+        oracle.forward(sl["q"], sl["k"], sl["v"], sl["logit"], s, rows=rows)
+    dt = time.perf_counter() - t0
+    full = dt / len(heads) * (w.L / n_rows) * w.B * w.H
+    return {"value": fwd_flops(w.B, w.H, w.L, w.d) / full / 1e12, "unit": "TFLOP/s",
+            "cores": cores, "kind": "oracle", "seconds": round(full, 1),
+            "sample": f"extrapolated: fp64 forward of {n_rows} query rows of heads {heads} "
+                      f"(one per gate group) at L={w.L} took {dt:.2f} s; scaled by "
+                      f"(L / {n_rows}) row blocks x {w.B * w.H} heads to {full:.0f} s for the "
+                      "whole forward"}
+
+
+def cpu_baseline_decode(w, y):
+    """The fp64 oracle decode over every (batch, head) slice of the decode
+    workload's cache `y` (on the GPU): each batch row is copied to the host
+    outside the timed region, then the oracle's step is timed."""
+    import oracle
+    cores = _oracle_threads()
+    s = fox.default_scale(w.d)
+    dt = 0.0
+    for b in range(w.B):
+        sl = {k: v[b:b + 1].cpu() for k, v in y.items()}
+        t0 = time.perf_counter()
+        oracle.decode(sl["q"], sl["k_cache"], sl["v_cache"], sl["cached_logit"], sl["logit_new"],
+                      s)
+        dt += time.perf_counter() - t0
+        del sl
+    byt = decode_bytes(w.B, w.H, w.L, w.d)
+    return {"value": byt / dt / 1e9, "unit": "GB/s", "cores": cores, "kind": "oracle",
+            "seconds": round(dt, 2),
+            "sample": f"full: fp64 decode of all {w.B * w.H} (batch, head) slices at T={w.L}, "
+                      f"d={w.d}: {dt:.1f} s (host copies of the cache not timed); value = the "
+                      "step's algorithmic cache bytes / time"}
 
 
 def calibration_copy(mib: int):
@@ -619,6 +855,8 @@ def main():
     ap.add_argument("--no-projection", action="store_true",
                     help="skip the forget-gate projection timings")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-other-workloads", action="store_true",
+                    help="skip the d = 64 training shape and the 65536-length prefill legs")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="run a plain device copy of this size first (counter calibration)")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -789,7 +1027,7 @@ def main():
             f"{rp['prologue_bwd']:.3f}, out_gate {rp['out_gate']:.3f})")
     if not args.no_decode:
         wd = inputs.WORKLOADS[args.decode_workload]
-        rd = bench_decode(wd, max(args.steps, 10), args.warmup)
+        rd = bench_decode(wd, max(args.steps, 10), args.warmup, cpu=not args.no_cpu_baseline)
         byt = decode_bytes(wd.B, wd.H, wd.L, wd.d)
         gbs = byt / (rd["ms"] * 1e-3) / 1e9
         out["decode"] = {"metric": "decode HBM GB/s", "value": round(gbs, 1), "unit": "GB/s",
@@ -830,9 +1068,43 @@ def main():
             **legs}
         log(f"[bench] gate projection fwd {rj['fwd_ms'] * 1e3:.1f} us, bwd "
             f"{rj['bwd_ms'] * 1e3:.1f} us")
+    if not args.no_other_workloads:
+        out["workloads"] = {}
+        w2 = inputs.WORKLOADS["fwdbwd_bf16_b8_h12_l2048_d64"]
+        r2 = bench_train_graph(w2, args.steps, args.warmup)
+        out["workloads"][w2.name] = train_graph_summary(w2, r2)
+        log(f"[bench] {w2.name}: step {r2['stored_ms']:.4f} ms (keeping dS), "
+            f"{r2['recompute_ms']:.4f} ms (recomputing)")
+        w4 = inputs.WORKLOADS["fwd_bf16_b1_h16_l65536_d128"]
+        r4 = bench_prefill(w4, max(3, args.steps // 4), 1)
+        fl4 = fwd_flops(w4.B, w4.H, w4.L, w4.d)
+        tf4 = fl4 / (r4["fwd_ms"] * 1e-3) / 1e12
+        out["workloads"][w4.name] = {
+            "what": "length-extrapolation prefill: gate prefix -> forward (O, LSE); heads 0-7 "
+                    "logits N(6, 1), heads 8-15 N(0, variance 2)",
+            "config": {"B": w4.B, "H": w4.H, "L": w4.L, "d": w4.d, "seed": w4.seed,
+                       "flops_per_step": fl4},
+            "ms_per_step": round(r4["ms"], 4),
+            "TFLOP/s": round(fl4 / (r4["ms"] * 1e-3) / 1e12, 2),
+            "frac_of_peak": round(fl4 / (r4["ms"] * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+            "roofline": {"bound": "mfma", "kernel": "fwd_bf16_kernel<128> (fox_attn_fwd)",
+                         "achieved": round(tf4, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
+                         "unit": "TFLOP/s", "frac": round(tf4 / MFMA_BF16_PEAK_TFLOPS, 4),
+                         "algorithmic_flops_per_launch": fl4}}
+        log(f"[bench] {w4.name}: forward {r4['fwd_ms']:.3f} ms -> {tf4:.1f} TFLOP/s")
     if not args.no_cpu_baseline:
         log("[bench] timing the fp64 oracle on the host")
         out["cpu_baseline"] = cpu_baseline(w)
+        if not args.no_other_workloads:
+            w1 = inputs.WORKLOADS["fwd_f32_b1_h2_l256_d64"]
+            out["workloads"][w1.name] = {"what": "fp32 forward (parity workload; oracle time "
+                                                 "only)",
+                                         "cpu_baseline": cpu_baseline_full(w1)}
+            out["workloads"][w2.name]["cpu_baseline"] = cpu_baseline_full(w2)
+            out["workloads"][w4.name]["cpu_baseline"] = cpu_baseline_rows(w4)
+            log("[bench] oracle times of the other workloads done")
+        if not args.no_decode and "decode_cpu_baseline" in rd:
+            out["decode"]["cpu_baseline"] = rd["decode_cpu_baseline"]
     print(json.dumps(out), flush=True)
 
 
