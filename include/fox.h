@@ -64,6 +64,8 @@ typedef enum {
   FOX_ERR_WORKSPACE = 5,    /* workspace missing or smaller than required          */
   FOX_ERR_HIP = 6,          /* the HIP runtime reported an error at launch         */
   FOX_ERR_VALUE = 7,        /* a scalar argument out of range (eps: finite, >= 0)  */
+  FOX_ERR_TOO_LARGE = 8,    /* the shape needs more scratch than the allocation-free
+                               entry point holds                                   */
   FOX_STATUS_MAX_ENUM = 0x7FFFFFFF  /* not a status: keeps the enum int-sized        */
 } fox_status_t;
 
@@ -238,6 +240,28 @@ fox_status_t fox_attn_decode(fox_dtype_t dtype, const void* q, const void* k_cac
                     float* c_cache, const float* gate_logit_new, void* o, float* lse,
                     void* workspace, size_t workspace_bytes,
                     int B, int H, int T, int d, float scale, hipStream_t stream);
+
+/*
+ * fox_attn_decode for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation.  It takes
+ * no workspace; the split partials live in a file-scope device array of 64 MiB
+ * that the library holds on every device it runs on until the process ends.  No
+ * call allocates or frees anything (the array's device address is looked up once
+ * per device, on the first call with that device current).
+ *
+ *   Arguments, outputs and results as for fox_attn_decode (bit for bit: the same
+ *   kernels, the same split plan).
+ *   Limit: shapes whose partials exceed the array, i.e. whenever
+ *   fox_attn_decode_workspace_bytes() > 64 MiB (for example B*H = 1024 heads at
+ *   d = 128 with T above 129024), return FOX_ERR_TOO_LARGE and launch nothing.
+ *   Calls that overlap on one device (different streams, or host threads) share
+ *   the array and race: serialise them.  Each call overwrites every partial it
+ *   reads, so nothing carries over from an earlier call.
+ */
+fox_status_t fox_attn_decode_noalloc(fox_dtype_t dtype, const void* q, const void* k_cache,
+                                     const void* v_cache, float* c_cache,
+                                     const float* gate_logit_new, void* o, float* lse,
+                                     int B, int H, int T, int d, float scale, hipStream_t stream);
 
 /*
  * Gate-aware exact skipping (the paper's outlook, Sec. 6: forget gates could

@@ -9,7 +9,7 @@ from ._lib import (  # noqa: F401
     FoxError, default_scale, load, status_string,
     fox_gate_prefix, fox_attn_fwd, fox_attn_bwd, fox_attn_bwd_workspace_bytes,
     fox_attn_bwd_delta, fox_attn_bwd_dkdv, fox_attn_bwd_dq, fox_dlogf_from_dc,
-    fox_dlogit_from_dc, fox_attn_decode,
+    fox_dlogit_from_dc, fox_attn_decode, fox_attn_decode_noalloc,
     fox_fixed_gate_init, fox_attn_fwd_fixed_gate, fox_attn_bwd_fixed_gate,
     fox_attn_bwd_fixed_gate_workspace_bytes, fox_attn_decode_fixed_gate,
     fox_attn_decode_workspace_bytes, fox_row_norm_max, fox_attn_decode_skip,
@@ -38,7 +38,8 @@ __all__ = [
     "fox_dlogit_from_dc", "fox_fixed_gate_init", "fox_attn_fwd_fixed_gate",
     "fox_attn_bwd_fixed_gate", "fox_attn_bwd_fixed_gate_workspace_bytes",
     "fox_attn_decode_fixed_gate",
-    "fox_attn_decode", "fox_attn_decode_workspace_bytes", "fox_row_norm_max",
+    "fox_attn_decode", "fox_attn_decode_noalloc", "fox_attn_decode_workspace_bytes",
+    "fox_row_norm_max",
     "fox_attn_decode_skip", "fox_attn_fwd_skip", "fox_attn_bwd_skip",
     "fox_attn_fwd_fixed_gate_skip", "fox_attn_bwd_fixed_gate_skip",
     "fox_attn_decode_fixed_gate_skip",

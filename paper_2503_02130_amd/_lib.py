@@ -26,7 +26,7 @@ EXPORTED = (
     "fox_status_string", "fox_version", "fox_gate_prefix", "fox_attn_fwd",
     "fox_attn_bwd_workspace_bytes", "fox_attn_bwd", "fox_attn_bwd_delta", "fox_attn_bwd_dkdv",
     "fox_attn_bwd_dq", "fox_dlogf_from_dc", "fox_dlogit_from_dc",
-    "fox_attn_decode_workspace_bytes", "fox_attn_decode",
+    "fox_attn_decode_workspace_bytes", "fox_attn_decode", "fox_attn_decode_noalloc",
     "fox_fixed_gate_init", "fox_attn_fwd_fixed_gate", "fox_attn_bwd_fixed_gate_workspace_bytes",
     "fox_attn_bwd_fixed_gate", "fox_attn_decode_fixed_gate",
     "fox_row_norm_max", "fox_attn_decode_skip", "fox_attn_fwd_skip", "fox_attn_bwd_skip",
@@ -102,6 +102,8 @@ def load() -> ctypes.CDLL:
     lib.fox_attn_decode_workspace_bytes.argtypes = [I, I, I, I, I]
     lib.fox_attn_decode.restype = I
     lib.fox_attn_decode.argtypes = [I, P, P, P, P, P, P, P, P, Z, I, I, I, I, F, P]
+    lib.fox_attn_decode_noalloc.restype = I
+    lib.fox_attn_decode_noalloc.argtypes = [I, P, P, P, P, P, P, P, I, I, I, I, F, P]
     lib.fox_fixed_gate_init.restype = I
     lib.fox_fixed_gate_init.argtypes = [P, I, F, F]
     lib.fox_attn_fwd_fixed_gate.restype = I
@@ -485,6 +487,34 @@ def fox_attn_decode(q, k_cache, v_cache, c_cache, gate_logit_new, scale: Optiona
                                 workspace.numel() * workspace.element_size(), B, H, T, d, s,
                                 _stream(q))
     _raise(st, "fox_attn_decode")
+    return o, lse
+
+
+def fox_attn_decode_noalloc(q, k_cache, v_cache, c_cache, gate_logit_new,
+                            scale: Optional[float] = None, o=None, lse=None):
+    """fox_attn_decode without a workspace (the library's per-device scratch
+    array holds the split partials; shapes needing more than it holds raise).
+    Pass o and lse to allocate nothing at all."""
+    B, H, d = q.shape
+    T = k_cache.shape[2]
+    dt = q.dtype
+    if dt not in _DT:
+        raise ValueError(f"unsupported dtype {dt}")
+    dev = q.device
+    _check(q, "q", (B, H, d), dt, dev)
+    _check(k_cache, "k_cache", (B, H, T, d), dt, dev)
+    _check(v_cache, "v_cache", (B, H, T, d), dt, dev)
+    _check(c_cache, "c_cache", (B, H, T), torch.float32, dev)
+    _check(gate_logit_new, "gate_logit_new", (B, H), torch.float32, dev)
+    o = torch.empty_like(q) if o is None else o
+    lse = torch.empty((B, H), device=dev, dtype=torch.float32) if lse is None else lse
+    _check(o, "o", (B, H, d), dt, dev)
+    _check(lse, "lse", (B, H), torch.float32, dev)
+    s = default_scale(d) if scale is None else float(scale)
+    st = load().fox_attn_decode_noalloc(_DT[dt], _ptr(q), _ptr(k_cache), _ptr(v_cache),
+                                        _ptr(c_cache), _ptr(gate_logit_new), _ptr(o), _ptr(lse),
+                                        B, H, T, d, s, _stream(q))
+    _raise(st, "fox_attn_decode_noalloc")
     return o, lse
 
 

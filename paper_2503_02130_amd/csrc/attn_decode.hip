@@ -17,6 +17,8 @@
 // a small second kernel merges the splits (log-sum-exp merge) and appends c_T
 // to the prefix cache.  Entry T-1 of that cache is never read: every workgroup
 // derives c_T itself, so the write cannot race with the readers.
+#include <mutex>
+
 #include "fox_device.h"
 #include "fox_internal.h"
 
@@ -284,6 +286,54 @@ static hipError_t decode_dispatch(bool bf16_, const void* q, const void* k_cache
 hipError_t launch_decode(bool bf16_, const void* q, const void* k_cache, const void* v_cache,
                          float* c_cache, const float* logit_new, void* o, float* lse, void* ws,
                          int BH, int T, int d, float scale, hipStream_t s) {
+  return decode_dispatch<false, false>(bf16_, q, k_cache, v_cache, c_cache, 1, c_cache, logit_new,
+                                       nullptr, o, lse, ws, BH, T, d, scale, s);
+}
+
+// ---------------------------------------------------------------------------
+// The decode step without a caller workspace: the split partials live in a
+// file-scope device array, `scratch`, of kDecodeScratchBytes (every device the
+// library runs on holds its own copy, loaded with the code object, until the
+// process ends).  In host code the name `scratch` is only a host-side stand-in;
+// the device address comes from hipGetSymbolAddress, taken once per device with
+// that device current and kept in scratch_ptr[].  The partials are fully
+// written by the split kernel before the combine kernel reads them (skipped
+// splits write empty partials), so nothing needs clearing between calls; calls
+// that overlap on one device share the array and race.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) float scratch[kDecodeScratchBytes / sizeof(float)];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void* scratch_ptr[kMaxDevices] = {};
+
+hipError_t device_scratch(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (!scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    scratch_ptr[dev] = p;
+  }
+  *out = scratch_ptr[dev];
+  return hipSuccess;
+}
+}  // namespace
+
+hipError_t launch_decode_noalloc(bool bf16_, const void* q, const void* k_cache,
+                                 const void* v_cache, float* c_cache, const float* logit_new,
+                                 void* o, float* lse, int BH, int T, int d, float scale,
+                                 hipStream_t s) {
+  if (decode_workspace_bytes(BH, T, d) > kDecodeScratchBytes) return hipErrorInvalidValue;
+  void* ws = nullptr;
+  hipError_t e = device_scratch(&ws);
+  if (e != hipSuccess) return e;
   return decode_dispatch<false, false>(bf16_, q, k_cache, v_cache, c_cache, 1, c_cache, logit_new,
                                        nullptr, o, lse, ws, BH, T, d, scale, s);
 }

@@ -74,6 +74,9 @@ const char* fox_status_string(fox_status_t status) {
     case FOX_ERR_WORKSPACE: return "FOX_ERR_WORKSPACE: workspace missing or too small";
     case FOX_ERR_HIP: return "FOX_ERR_HIP: the HIP runtime reported a launch error";
     case FOX_ERR_VALUE: return "FOX_ERR_VALUE: a scalar argument is out of range (eps: finite, >= 0)";
+    case FOX_ERR_TOO_LARGE:
+      return "FOX_ERR_TOO_LARGE: the shape needs more scratch than fox_attn_decode_noalloc holds "
+             "(64 MiB of split partials); use fox_attn_decode with a workspace";
     default: return "unknown fox status";
   }
 }
@@ -296,6 +299,26 @@ fox_status_t fox_attn_decode(fox_dtype_t dtype, const void* q, const void* k_cac
   return launch_status(fox::launch_decode(dtype == FOX_DTYPE_BF16, q, k_cache, v_cache, c_cache,
                                           gate_logit_new, o, lse, workspace, B * H, T, d, scale,
                                           static_cast<hipStream_t>(stream)));
+}
+
+fox_status_t fox_attn_decode_noalloc(fox_dtype_t dtype, const void* q, const void* k_cache,
+                                     const void* v_cache, float* c_cache,
+                                     const float* gate_logit_new, void* o, float* lse, int B,
+                                     int H, int T, int d, float scale, hipStream_t stream) {
+  if (!q || !k_cache || !v_cache || !c_cache || !gate_logit_new || !o || !lse)
+    return FOX_ERR_NULL;
+  fox_status_t st = check_dims(B, H, T, d);
+  if (st) return st;
+  st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(c_cache) ||
+      !aligned16(gate_logit_new) || !aligned16(o) || !aligned16(lse))
+    return FOX_ERR_ALIGN;
+  if (fox::decode_workspace_bytes(B * H, T, d) > fox::kDecodeScratchBytes)
+    return FOX_ERR_TOO_LARGE;
+  return launch_status(fox::launch_decode_noalloc(dtype == FOX_DTYPE_BF16, q, k_cache, v_cache,
+                                                  c_cache, gate_logit_new, o, lse, B * H, T, d,
+                                                  scale, stream));
 }
 
 // ------------------------------------------------------- gate-aware skipping

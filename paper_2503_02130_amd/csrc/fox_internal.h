@@ -99,6 +99,13 @@ hipError_t launch_row_norm_max(bool bf16, const void* x, float* out, int BH, int
 
 int decode_num_splits(int BH, int T);
 size_t decode_workspace_bytes(int BH, int T, int d);
+// the allocation-free decode: its split partials in a file-scope device array of
+// this many bytes (per device); shapes needing more are rejected
+constexpr size_t kDecodeScratchBytes = size_t(64) << 20;
+hipError_t launch_decode_noalloc(bool bf16, const void* q, const void* k_cache,
+                                 const void* v_cache, float* c_cache, const float* logit_new,
+                                 void* o, float* lse, int BH, int T, int d, float scale,
+                                 hipStream_t s);
 hipError_t launch_decode(bool bf16, const void* q, const void* k_cache, const void* v_cache,
                          float* c_cache, const float* logit_new, void* o, float* lse, void* ws,
                          int BH, int T, int d, float scale, hipStream_t s);

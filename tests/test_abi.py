@@ -72,7 +72,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_status_strings(lib):
-    for code in range(8):
+    for code in range(9):
         assert lib.fox_status_string(code) and b"unknown" not in lib.fox_status_string(code)
     assert b"unknown" in lib.fox_status_string(99)
     assert lib.fox_version() >= 100
@@ -348,6 +348,25 @@ def test_decode_validation_and_workspace(lib):
                                ctypes.c_float(0.1), None) == 5
     assert lib.fox_attn_decode(1, *args, c(P16), need, 64, 16, 0, 128,
                                ctypes.c_float(0.1), None) == 2
+
+
+def test_decode_noalloc_validation(lib):
+    """The allocation-free decode checks its arguments like fox_attn_decode and
+    refuses, before touching the GPU, shapes whose split partials exceed its
+    64 MiB scratch (B*H = 1024, d = 128: T up to 129024 fits)."""
+    def call(ptrs=(P16,) * 7, B=1, H=1, T=8, d=64, dtype=1):
+        return lib.fox_attn_decode_noalloc(dtype, *[ctypes.c_void_p(p) if p else None
+                                                    for p in ptrs],
+                                           B, H, T, d, ctypes.c_float(0.125), None)
+    assert call(ptrs=(0,) + (P16,) * 6) == 1
+    assert call(B=0) == 2
+    assert call(d=96) == 3
+    assert call(ptrs=(P16 + 4,) + (P16,) * 6) == 4
+    assert call(B=64, H=16, T=129025, d=128) == 8
+    assert call(B=16, H=16, T=600000, d=128) == 8
+    assert lib.fox_attn_decode_workspace_bytes(1, 64, 16, 129024, 128) <= 64 << 20
+    assert lib.fox_attn_decode_workspace_bytes(1, 64, 16, 129025, 128) > 64 << 20
+    assert b"TOO_LARGE" in lib.fox_status_string(8)
 
 
 def test_binding_refuses_host_tensors(lib):
