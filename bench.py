@@ -311,10 +311,15 @@ def bench_train_graph(w, steps, warmup):
         if not (torch.isfinite(o.float()).all() and torch.isfinite(dlf).all()):
             raise RuntimeError("non-finite outputs")
         del g
-    reps = max(steps, 20)
+    # each stage alone: ten launches per graph, so that the host's cost of one graph
+    # launch does not show in the short kernels' times
+    per_graph = 10
     for n, fn in stage.items():
-        g = _capture(fn)
-        res[n] = _graph_ms(g, reps, warmup)
+        def many(fn=fn):
+            for _ in range(per_graph):
+                fn()
+        g = _capture(many)
+        res[n] = _graph_ms(g, max(2, steps // 2), warmup) / per_graph
         del g
     res["store_bytes"] = store.numel()
     return res
@@ -333,8 +338,8 @@ def train_graph_summary(w, r):
     fw = fl_f / (r["fwd"] * 1e-3) / 1e12
     return {
         "what": "training step (gate prefix -> forward -> backward -> d(logit)) at the 125M-model "
-                "head shape; each step captured in a HIP graph and replayed back to back, each "
-                "stage also captured and replayed alone",
+                "head shape; each step captured in a HIP graph and replayed back to back; each "
+                "stage also captured alone, ten launches per graph, for its own time",
         "config": {"B": B, "H": H, "L": L, "d": d, "seed": w.seed, "flops_per_step": fl_f + fl_b},
         "ms_per_step": round(r["stored_ms"], 4), "TFLOP/s": round(tf, 2),
         "frac_of_peak": round(tf / MFMA_BF16_PEAK_TFLOPS, 4),

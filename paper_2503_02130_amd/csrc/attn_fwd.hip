@@ -80,8 +80,12 @@ struct FwdSmem {
 // layer computation): y = RMSNorm(o) o sigmoid(g) per query row, from the row
 // as rounded to bf16 for O (the backward normalises the stored O the same way).
 // A lane holds half of its row; the other half is in lane l ^ 32.
+//
+// Occupancy: two waves per SIMD at D = 128 (about 240 VGPRs); at D = 64 the
+// kernel fits 128 VGPRs and runs four (the LDS would allow four workgroups per
+// CU; measured 3 % faster than three).
 template <int D, bool FIXED, bool SKIP, bool OUTG = false>
-__global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(D == 64 ? 4 : 2)))
 void fwd_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ K,
                      const bf16* __restrict__ V, const float* __restrict__ gate,
                      const float* __restrict__ qnorm, const float* __restrict__ knorm,

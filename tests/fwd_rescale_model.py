@@ -71,7 +71,7 @@ def rescale_events(q, k, c, scale):
             act = t_d > j
             if not bool(act.any()):
                 continue
-            ut = u[act][:, :, j * TILE:(j + 1) * TILE]     # [w, 32, 64]
+            ut = u[:, :, j * TILE:(j + 1) * TILE][act]     # [w, 32, 64]
             ma = m[act]
             p = torch.exp2(ut - ma[:, :, None]).to(torch.bfloat16).float()
             s0 = p[:, :, half == 0].sum(-1)
