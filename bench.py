@@ -39,7 +39,7 @@ HBM_PEAK_GBS = 8000.0            # MI355X HBM3E
 
 CSRC = os.path.join(ROOT, "paper_2503_02130_amd", "csrc")
 PROFILES = os.path.join(ROOT, "profiles")
-TRAFFIC_FILE = os.path.join(PROFILES, "hbm_traffic_bench_fwdbwd_l16384_decode_t32768.txt")
+TRAFFIC_FILE = os.path.join(PROFILES, "hbm_traffic_bench_workloads.txt")
 # kernel -> the sources its machine code is built from (the traffic measured for
 # a kernel is reported only while these are unchanged)
 KERNEL_SOURCES = {
@@ -77,6 +77,11 @@ def fwd_flops(B, H, L, d) -> float:
 
 def bwd_flops(B, H, L, d) -> float:
     return 10.0 * d * causal_pairs(B, H, L)
+
+
+def fwd_grid_threads(B, H, L) -> int:
+    """Threads the bf16 forward launches: one 256-thread workgroup per 128 queries."""
+    return B * H * ((L + 127) // 128) * 256
 
 
 def decode_bytes(B, H, T, d, elem=2) -> float:
@@ -354,6 +359,7 @@ def train_graph_summary(w, r):
                      "(fox_attn_bwd_dkdv_store)", "achieved": round(kv, 2),
                      "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(kv / MFMA_BF16_PEAK_TFLOPS, 4),
+                     "traffic": measured_traffic(f"bwd_dkdv_bf16_kernel<{d},false,false,true>"),
                      "algorithmic_flops_per_launch": fl_kv},
         "roofline_fwd": {"bound": "mfma", "kernel": "fwd_bf16_kernel<64> (fox_attn_fwd)",
                          "achieved": round(fw, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
@@ -730,7 +736,8 @@ def _kernel_key(name):
 
 
 def _per_kernel_kib(rows, counter):
-    """Mean counter value (KiB) per dispatch, per kernel family."""
+    """Counter value (KiB) per dispatch, per (kernel, launch grid in threads); the
+    copy kernels are keyed ("copy", 0)."""
     per = {}
     for r in rows:
         if r["Counter_Name"] != counter:
@@ -738,8 +745,9 @@ def _per_kernel_kib(rows, counter):
         key = _kernel_key(r["Kernel_Name"])
         if key is None:
             continue
-        per.setdefault(key, {}).setdefault(r["Dispatch_Id"], 0.0)
-        per[key][r["Dispatch_Id"]] += float(r["Counter_Value"])
+        k = (key, 0 if key == "copy" else int(r["Grid_Size"]))
+        per.setdefault(k, {}).setdefault(r["Dispatch_Id"], 0.0)
+        per[k][r["Dispatch_Id"]] += float(r["Counter_Value"])
     return per
 
 
@@ -750,23 +758,25 @@ def pmc_summary(fetch_dir, write_dir, copy_mib, command):
     fetch = _per_kernel_kib(_counter_rows(fetch_dir), "FETCH_SIZE")
     write = _per_kernel_kib(_counter_rows(write_dir), "WRITE_SIZE")
     # the calibration copy is by far the largest device-to-device copy of the run
-    cf = max(fetch["copy"].values())
-    cw = max(write["copy"].values())
+    cf = max(fetch[("copy", 0)].values())
+    cw = max(write[("copy", 0)].values())
     f_fac = copy_mib * 1024.0 / cf
     w_fac = copy_mib * 1024.0 / cw
     lines = ["# HBM traffic per launch from rocprofv3 FETCH_SIZE / WRITE_SIZE",
              f"# command (one pass per counter): {command}",
              f"# calibration: plain copy of {copy_mib} MiB read {cf:.0f} KiB and wrote {cw:.0f} KiB;",
              f"#   scale factors fetch {f_fac:.4f}, write {w_fac:.4f}",
-             "# kernel  dispatches  fetch_KiB  write_KiB  traffic_bytes_per_launch  sources_sha256"]
-    for k in sorted(set(fetch) & set(write)):
+             "# kernel  grid_threads  dispatches  fetch_KiB  write_KiB  traffic_bytes_per_launch  "
+             "sources_sha256"]
+    for k, grid in sorted(set(fetch) & set(write)):
         fam = k.split("<")[0]
         if fam not in KERNEL_SOURCES:
             continue
-        fk = sum(fetch[k].values()) / len(fetch[k])
-        wk = sum(write[k].values()) / len(write[k])
+        f_, w_ = fetch[(k, grid)], write[(k, grid)]
+        fk = sum(f_.values()) / len(f_)
+        wk = sum(w_.values()) / len(w_)
         tb = (fk * f_fac + wk * w_fac) * 1024.0
-        lines.append(f"{k} {len(fetch[k])} {fk:.1f} {wk:.1f} {tb:.0f} {sources_hash(fam)}")
+        lines.append(f"{k} {grid} {len(f_)} {fk:.1f} {wk:.1f} {tb:.0f} {sources_hash(fam)}")
     return "\n".join(lines) + "\n"
 
 
@@ -786,65 +796,100 @@ PROJ_DX_KERNEL = "gate_proj_dx_kernel<true,1>"
 ROOFLINE_KERNELS = (KV_STORE_KERNEL, KV_KERNEL, DQ_STORED_KERNEL, DECODE_KERNEL, PROJ_FWD_KERNEL,
                     PROJ_DW_KERNEL, PROJ_DX_KERNEL)
 
-SQ_KERNELS = ("fwd_bf16_kernel<128,false,false,false>",
-              "bwd_dkdv_bf16_kernel<128,false,false,false>",
-              "bwd_dkdv_bf16_kernel<128,false,false,true>", "bwd_dq_bf16_kernel<128,false,false>",
-              "bwd_dq_stored_kernel<128,false>")
+SQ_KERNELS = tuple(k for dd in (128, 64) for k in (
+    f"fwd_bf16_kernel<{dd},false,false,false>", f"bwd_dkdv_bf16_kernel<{dd},false,false,false>",
+    f"bwd_dkdv_bf16_kernel<{dd},false,false,true>", f"bwd_dq_bf16_kernel<{dd},false,false>",
+    f"bwd_dq_stored_kernel<{dd},false>"))
 
 
 def sq_summary(dirs, command, ms):
     """Text summary of rocprofv3 --pmc passes (SQ_PASS_A, SQ_PASS_B) over this
-    benchmark: per dense attention kernel, instruction mix, MFMA work and issue
-    counters.  `ms` maps kernel -> average duration (ms) from a kernel trace of the
-    same command; MFMA utilisation = executed MFMA FLOPs / (duration x peak)."""
+    benchmark: per dense attention kernel and launch grid (the workloads launch
+    different grids), instruction mix, MFMA work and issue counters.  `ms` maps
+    (kernel, grid) -> median duration (ms) from a kernel trace of the same
+    command; MFMA utilisation = executed MFMA FLOPs / (duration x peak)."""
     per = {}
     for d in dirs:
         for r in _counter_rows(d):
             k = _kernel_key(r["Kernel_Name"])
             if k not in SQ_KERNELS:
                 continue
-            c = per.setdefault(k, {}).setdefault(r["Counter_Name"], {})
+            c = per.setdefault((k, int(r["Grid_Size"])), {}).setdefault(r["Counter_Name"], {})
             c[r["Dispatch_Id"]] = c.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
     lines = ["# SQ counters of the dense attention kernels (rocprofv3 --pmc, two passes)",
              f"# command (one pass per counter set): {command}",
              "#   pass A: " + " ".join(SQ_PASS_A), "#   pass B: " + " ".join(SQ_PASS_B),
-             "# values: mean per dispatch; MOPS_BF16 counts 512-FLOP MFMA operations"]
+             "# values: mean per dispatch; MOPS_BF16 counts 512-FLOP MFMA operations; one section",
+             "# per kernel and launch grid (threads), i.e. per workload"]
     for k in SQ_KERNELS:
-        if k not in per:
-            continue
-        v = {n: sum(x.values()) / len(x) for n, x in per[k].items()}
-        lines.append(f"\n## {k}")
-        for n in SQ_PASS_A + SQ_PASS_B:
-            if n in v:
-                lines.append(f"{n:32s} {v[n]:.6g}")
-        mf = v.get("SQ_INSTS_MFMA", 0.0)
-        if mf:
-            lines.append(f"{'non-MFMA VALU per MFMA':32s} {(v['SQ_INSTS_VALU'] - mf) / mf:.3f}")
-            lines.append(f"{'LDS instructions per MFMA':32s} {v['SQ_INSTS_LDS'] / mf:.3f}")
-        if v.get("SQ_VALU_MFMA_BUSY_CYCLES"):
-            lines.append(f"{'MFMA/VALU co-issue share':32s} "
-                         f"{v['SQ_VALU_MFMA_COEXEC_CYCLES'] / v['SQ_VALU_MFMA_BUSY_CYCLES']:.3f}")
-        if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in v and k in ms:
-            fl = v["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512.0
-            lines.append(f"{'executed MFMA FLOPs':32s} {fl:.4g}")
-            lines.append(f"{'trace duration ms':32s} {ms[k]:.4f}")
-            lines.append(f"{'MFMA utilisation of 2516.6 TF':32s} "
-                         f"{fl / (ms[k] * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS:.4f}")
+        for (kk, grid) in sorted(g for g in per if g[0] == k):
+            v = {n: sum(x.values()) / len(x) for n, x in per[(kk, grid)].items()}
+            lines.append(f"\n## {k}, grid {grid} threads")
+            for n in SQ_PASS_A + SQ_PASS_B:
+                if n in v:
+                    lines.append(f"{n:32s} {v[n]:.6g}")
+            mf = v.get("SQ_INSTS_MFMA", 0.0)
+            if mf:
+                lines.append(f"{'non-MFMA VALU per MFMA':32s} {(v['SQ_INSTS_VALU'] - mf) / mf:.3f}")
+                lines.append(f"{'LDS instructions per MFMA':32s} {v['SQ_INSTS_LDS'] / mf:.3f}")
+            if v.get("SQ_VALU_MFMA_BUSY_CYCLES"):
+                lines.append(f"{'MFMA/VALU co-issue share':32s} "
+                             f"{v['SQ_VALU_MFMA_COEXEC_CYCLES'] / v['SQ_VALU_MFMA_BUSY_CYCLES']:.3f}")
+            if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in v and (k, grid) in ms:
+                fl = v["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512.0
+                t = ms[(k, grid)]
+                lines.append(f"{'executed MFMA FLOPs':32s} {fl:.4g}")
+                lines.append(f"{'trace duration ms (median)':32s} {t:.4f}")
+                lines.append(f"{'MFMA utilisation of 2516.6 TF':32s} "
+                             f"{fl / (t * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS:.4f}")
     return "\n".join(lines) + "\n"
 
 
-def measured_traffic(kernel: str):
-    """Bytes per launch recorded for `kernel` (family<template arguments>), or
-    None when there is no record or the family's sources changed since the
-    counters were taken."""
+def trace_summary(db, command):
+    """Markdown summary of a rocprofv3 --kernel-trace results database of this
+    benchmark: per library kernel and launch grid (each workload launches its own
+    grid), calls, mean / min / max duration and LDS bytes."""
+    import sqlite3
+    con = sqlite3.connect(db)
+    rows = con.execute("select name, grid_x, workgroup_x, duration, lds_size from kernels")
+    groups = {}
+    for name, gx, wx, dur, lds in rows:
+        key = _kernel_key(name)
+        if key in (None, "copy"):
+            continue
+        g = groups.setdefault((key, gx // max(wx, 1), wx), {"d": [], "lds": lds})
+        g["d"].append(dur / 1e3)
+    lines = ["# Kernel trace of bench.py: every library kernel, per launch grid",
+             "", f"Command: `{command}`", "",
+             "Durations in microseconds from the trace (one line per kernel and grid; the "
+             "workloads differ in grid size).", "",
+             "| kernel | workgroups | threads | calls | mean us | min us | max us | LDS bytes |",
+             "|---|---:|---:|---:|---:|---:|---:|---:|"]
+    for (key, wgs, wx), g in sorted(groups.items(), key=lambda kv: -sum(kv[1]["d"])):
+        d = g["d"]
+        lines.append(f"| {key} | {wgs} | {wx} | {len(d)} | {sum(d) / len(d):.1f} | {min(d):.1f} | "
+                     f"{max(d):.1f} | {g['lds']} |")
+    return "\n".join(lines) + "\n"
+
+
+def measured_traffic(kernel: str, grid: int = None):
+    """Bytes per launch recorded for `kernel` (family<template arguments>) at
+    launch grid `grid` (threads; may be omitted when the kernel ran with one grid
+    only), or None when there is no record, the grid is ambiguous, or the family's
+    sources changed since the counters were taken."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
+    found = []
     for line in open(TRAFFIC_FILE):
         f = line.split()
-        if line.startswith("#") or len(f) != 6 or f[0] != kernel:
+        if line.startswith("#") or len(f) != 7 or f[0] != kernel:
             continue
-        return float(f[4]) if f[5] == sources_hash(kernel.split("<")[0]) else None
-    return None
+        if grid is None or int(f[1]) == grid:
+            found.append(f)
+    if len(found) != 1:
+        return None
+    f = found[0]
+    return float(f[5]) if f[6] == sources_hash(kernel.split("<")[0]) else None
 
 
 def main():
@@ -867,19 +912,25 @@ def main():
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 --pmc passes of this benchmark and exit")
     ap.add_argument("--pmc-command", default="", help="the profiled command, for the summary")
+    ap.add_argument("--trace-summary", metavar="RESULTS_DB",
+                    help="summarise a rocprofv3 --kernel-trace results.db of this benchmark and exit")
     ap.add_argument("--sq-summary", nargs="+", metavar="DIR",
                     help="summarise rocprofv3 --pmc SQ passes of this benchmark and exit; the "
                          "last argument is a kernel-trace results.db for the durations")
     args = ap.parse_args()
+    if args.trace_summary:
+        print(trace_summary(args.trace_summary, args.pmc_command), end="")
+        return
     if args.sq_summary:
         import sqlite3
         *dirs, db = args.sq_summary
         con = sqlite3.connect(db)
-        ms = {}
-        for name, avg in con.execute("select name, average from top_kernels"):
+        durs = {}
+        for name, gx, dur in con.execute("select name, grid_x, duration from kernels"):
             k = _kernel_key(name)
             if k in SQ_KERNELS:
-                ms[k] = float(avg) / 1e3  # microseconds -> ms
+                durs.setdefault((k, int(gx)), []).append(float(dur) / 1e6)  # ns -> ms
+        ms = {key: sorted(v)[len(v) // 2] for key, v in durs.items()}
         print(sq_summary(dirs, args.pmc_command, ms), end="")
         return
     if args.pmc_summary:
@@ -970,7 +1021,9 @@ def main():
                                                    2)},
         "roofline_fwd": {"bound": "mfma", "kernel": "fwd_bf16_kernel<128> (fox_attn_fwd)",
                          "achieved": round(fwd_tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
-                         "unit": "TFLOP/s", "frac": round(fwd_tf / MFMA_BF16_PEAK_TFLOPS, 4)},
+                         "unit": "TFLOP/s", "frac": round(fwd_tf / MFMA_BF16_PEAK_TFLOPS, 4),
+                         "traffic": measured_traffic(f"fwd_bf16_kernel<{d},false,false,false>",
+                                                     fwd_grid_threads(B, H, L))},
         "roofline_bwd": {"bound": "mfma",
                          "kernels": "fox_attn_bwd_stored stages (delta, dkdv_store, dq_stored, scan)",
                          "achieved": round(bwd_tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
@@ -1095,6 +1148,8 @@ def main():
             "roofline": {"bound": "mfma", "kernel": "fwd_bf16_kernel<128> (fox_attn_fwd)",
                          "achieved": round(tf4, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
                          "unit": "TFLOP/s", "frac": round(tf4 / MFMA_BF16_PEAK_TFLOPS, 4),
+                         "traffic": measured_traffic(f"fwd_bf16_kernel<{w4.d},false,false,false>",
+                                                     fwd_grid_threads(w4.B, w4.H, w4.L)),
                          "algorithmic_flops_per_launch": fl4}}
         log(f"[bench] {w4.name}: forward {r4['fwd_ms']:.3f} ms -> {tf4:.1f} TFLOP/s")
     if not args.no_cpu_baseline:
