@@ -715,7 +715,8 @@ __global__ __launch_bounds__(kKvThreads) void bwd_dkdv_bf16_kernel(
 // dQ from the stored dS: dQ = s dS K and dc^q = rowsum(dS) over the bf16 dS the
 // dK/dV kernel wrote.  Eight waves own 256 queries (four 64-query tiles, two
 // 32-query halves each); stages of 64 keys (half a stored block) load K and the
-// four tiles' dS by DMA, double-buffered, one barrier per stage.  Each wave
+// four tiles' dS by DMA, triple-buffered (two stages in flight, 156 KB of LDS),
+// one barrier per stage.  Each wave
 // accumulates dQ^T = K^T dS^T: the A operand is K transposed out of the LDS
 // tile, the B operand dS^T comes out of the stored layout by transposing reads
 // (lane = query, eight keys in the contraction order of the A operand).  A tile
@@ -739,8 +740,8 @@ __device__ __forceinline__ int ds_lds_pos(int slot) { return slot ^ ((slot >> 5)
 
 template <int D>
 struct DsSmem {
-  bf16 k[2][kDsBN * D];
-  bf16x8 ds[2][kDsTiles][kDsStageLds / 16];
+  bf16 k[3][kDsBN * D];
+  bf16x8 ds[3][kDsTiles][kDsStageLds / 16];
 };
 
 template <int D, bool SKIP>
@@ -788,6 +789,9 @@ __global__ __launch_bounds__(kDsThreads) void bwd_dq_stored_kernel(
   const uint32_t ds_addr = (uint32_t)(uintptr_t)lds_opaque(
       lds_ptr(&sm.ds[0][my_t][0]) + (2 * qb + (g16 & 1)) * kDsChunkLds +
       ds_lds_pos((cg & 1) * 32 + 4 * (g16 >> 1) + (j16 >> 2)) * 16 + (cg >> 1) * 8);
+  // buffer 2 lies beyond the 16-bit reach of an LDS immediate offset: own base
+  const uint32_t ds_addr2 = (uint32_t)(uintptr_t)lds_opaque(
+      (const lds_byte*)(uintptr_t)(ds_addr + 2 * (uint32_t)sizeof(sm.ds[0])));
   const uint32_t ds_src = (uint32_t)ds_lds_pos(lane) * 16;  // DMA: stored slot of LDS position lane
 
   f32x16 dqacc[D / 32];
@@ -814,7 +818,8 @@ __global__ __launch_bounds__(kDsThreads) void bwd_dq_stored_kernel(
     }
     j_first = 2 * lo;
   }
-  auto issue = [&](int j, auto bufc) {
+  // stage j's DMA into buffer B; returns the number of loads this wave issued
+  auto issue = [&](int j, auto bufc) -> int {
     constexpr int B = decltype(bufc)::value;
     const uint32_t base = (uint32_t)j * TILE * 2;
 #pragma unroll
@@ -832,17 +837,21 @@ __global__ __launch_bounds__(kDsThreads) void bwd_dq_stored_kernel(
         dma16_nt(rs, &sm.ds[B][t][wave * (kDsChunkLds / 16)],
                  ds_src + uniform_u32((uint32_t)(t - t_lo) * kDsSlotBytes +
                                       (uint32_t)(j & 1) * kDsStageBytes + (uint32_t)wave * 1024));
+      return NDMA + (t_hi - t_lo);
     }
+    return NDMA;
   };
   auto body = [&](auto bufc) {
     constexpr int B = decltype(bufc)::value;
     static_for<kDsBN / 16>([&](auto sc) {
       constexpr int S = decltype(sc)::value;  // 16-key step: pair S / 2, keys 16 (S % 2) ..
-      constexpr int DOFF = B * (int)sizeof(sm.ds[0]) + (S / 2) * 4 * kDsChunkLds + (S % 2) * 256;
+      constexpr int DOFF = (B == 2 ? 0 : B * (int)sizeof(sm.ds[0])) + (S / 2) * 4 * kDsChunkLds +
+                           (S % 2) * 256;
+      const uint32_t dbase = B == 2 ? ds_addr2 : ds_addr;
       constexpr int KOFF = 2 * (B * TILE + S * 16 * D);
       bf16x4 t[2 * (D / 32) + 2];
-      t[0] = ds_read_tr_asm<DOFF>(ds_addr);
-      t[1] = ds_read_tr_asm<DOFF + 128>(ds_addr);
+      t[0] = ds_read_tr_asm<DOFF>(dbase);
+      t[1] = ds_read_tr_asm<DOFF + 128>(dbase);
       static_for<D / 32>([&](auto dbc) {
         constexpr int db = decltype(dbc)::value;
         t[2 + 2 * db] = ds_read_tr_asm<KOFF>(taddr[0][db]);
@@ -860,18 +869,52 @@ __global__ __launch_bounds__(kDsThreads) void bwd_dq_stored_kernel(
   // tile qt takes part in stage j when it lies on or below the diagonal and
   // (skipping) its dS for the stage's block was stored
   auto active = [&](int j) { return qt >= j && qt < n_qt && (!SKIP || qt < cut(j >> 1)); };
-  if (j_first < n_st) issue(j_first, std::integral_constant<int, 0>());
-  for (int j = j_first; j < n_st; j += 2) {
-    wait_all_memory();
-    __syncthreads();  // stage j is in LDS; every wave is done with stage j - 1
-    if (j + 1 < n_st) issue(j + 1, std::integral_constant<int, 1>());
-    if (active(j)) body(std::integral_constant<int, 0>());
-    if (j + 1 < n_st) {
+  // Three buffers: stages j + 1 and j + 2 load while stage j is used.  Before
+  // stage j is read, the wave waits until only its loads of stage j + 1 (the
+  // newest issued) are outstanding; the barrier then shows every wave's part of
+  // stage j and that every wave is done reading stage j - 1, whose buffer stage
+  // j + 2 fills.  The body's LDS reads are complete when it returns.
+  static_assert(NDMA + kDsTiles < 16, "loads per stage fit the vmcnt immediate");
+  int newest = -1, pending = 0;  // the newest issued stage, this wave's loads for it
+  auto wait_stage = [&](int j) {
+    if (newest <= j) {
       wait_all_memory();
-      __syncthreads();
-      if (j + 2 < n_st) issue(j + 2, std::integral_constant<int, 0>());
-      if (active(j + 1)) body(std::integral_constant<int, 1>());
+      return;
     }
+    switch (pending) {
+      case 0: wait_vmem<0>(); break;
+      case 1: wait_vmem<1>(); break;
+      case 2: wait_vmem<2>(); break;
+      case 3: wait_vmem<3>(); break;
+      case 4: wait_vmem<4>(); break;
+      case 5: wait_vmem<5>(); break;
+      default: wait_vmem<NDMA + kDsTiles>(); break;
+    }
+  };
+  // every step runs (a step past the last stage only meets the barrier) so that
+  // no copies of the accumulators appear at the unrolled loop's back edge
+  auto step = [&](int j, auto bufc) {
+    constexpr int B = decltype(bufc)::value;
+    wait_stage(j);
+    barrier_no_fence();
+    if (j + 2 < n_st) {
+      pending = issue(j + 2, std::integral_constant<int, (B + 2) % 3>());
+      newest = j + 2;
+    }
+    if (j < n_st && active(j)) body(bufc);
+  };
+  if (j_first < n_st) {
+    pending = issue(j_first, std::integral_constant<int, 0>());
+    newest = j_first;
+  }
+  if (j_first + 1 < n_st) {
+    pending = issue(j_first + 1, std::integral_constant<int, 1>());
+    newest = j_first + 1;
+  }
+  for (int j = j_first; j < n_st; j += 3) {
+    step(j, std::integral_constant<int, 0>());
+    step(j + 1, std::integral_constant<int, 1>());
+    step(j + 2, std::integral_constant<int, 2>());
   }
 
   const float dcq_tot = wave_sum_pair(dcq_part);

@@ -198,6 +198,21 @@ __device__ __forceinline__ void dma4(__amdgpu_buffer_rsrc_t rsrc, void* lds_wave
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t*)lds_wave_base, 4, voffset, 0, 0, 0);
 }
 
+// Workgroup barrier without the memory fence of __syncthreads() (which waits for
+// every outstanding memory operation of the wave).  The caller must first wait
+// for whatever other waves read after the barrier: its LDS writes (lgkmcnt) and
+// its DMA into LDS (vmcnt).
+__device__ __forceinline__ void barrier_no_fence() { asm volatile("s_barrier" ::: "memory"); }
+
+// Wait until at most N vector-memory operations of this wave are outstanding
+// (loads complete in order, so all but the last N issued are done); the LDS
+// and export counts are left at their maxima (no wait).
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+  static_assert(N >= 0 && N < 16, "vmcnt immediate");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+}
+
 // Wait until every outstanding memory operation of this wave (including the
 // LDS-bound buffer loads above) has completed.
 __device__ __forceinline__ void wait_all_memory() { __builtin_amdgcn_s_waitcnt(0); }

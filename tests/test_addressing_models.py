@@ -55,8 +55,10 @@ def test_model_matches_the_kernel_source():
     assert "return slot ^ ((slot >> 5) << 2);" in BWD
     assert "(r2 | (r1 << 1) | (r0 << 2) | ((r3 ^ r1 ^ r0) << 3))" in DEV
     assert "(r2 | ((r0 ^ r3) << 1) | (r1 << 2))" in DEV
-    assert re.search(r"DOFF = B \* \(int\)sizeof\(sm\.ds\[0\]\) \+ \(S / 2\) \* 4 \* kDsChunkLds "
-                     r"\+ \(S % 2\) \* 256;", BWD)
+    assert re.search(r"DOFF = \(B == 2 \? 0 : B \* \(int\)sizeof\(sm\.ds\[0\]\)\) \+ "
+                     r"\(S / 2\) \* 4 \* kDsChunkLds \+\s*\(S % 2\) \* 256;", BWD)
+    assert "bf16x8 ds[3][kDsTiles][kDsStageLds / 16];" in BWD
+    assert "ds_addr + 2 * (uint32_t)sizeof(sm.ds[0])" in BWD
 
 
 # ----------------------------------------------------------- swizzled tiles
@@ -322,6 +324,25 @@ def test_stored_ds_reads_are_conflict_free(group):
         return w
     assert worst(CHUNK_LDS, True) == 1
     assert worst(1024, False) >= 2
+
+
+def test_stored_ds_buffers_fit_the_immediate_offsets():
+    """The dQ pass keeps three stored-dS buffers of kDsTiles x kDsStageLds bytes;
+    buffers 0 and 1 are reached from one base register plus an immediate, buffer 2
+    (beyond the 16-bit reach of an LDS immediate) from a second base: every
+    immediate stays below 2^16 and every buffer's address is the same either way."""
+    buf = 4 * (SLOT_BYTES // 2 // 1024) * CHUNK_LDS         # sizeof(sm.ds[0])
+    for B in range(3):
+        base = 2 * buf if B == 2 else 0
+        for S in range(4):
+            for k2 in range(2):
+                imm = (0 if B == 2 else B * buf) + (S // 2) * 4 * CHUNK_LDS + (S % 2) * 256 + 128 * k2
+                assert imm < 1 << 16, (B, S, k2)
+                assert base + imm == B * buf + (S // 2) * 4 * CHUNK_LDS + (S % 2) * 256 + 128 * k2
+    # the K tiles of the three stages (64 keys x D bf16 each) stay within reach too
+    for D in (64, 128):
+        for B in range(3):
+            assert 2 * (B * 64 * D + 3 * 16 * D) < 1 << 16
 
 
 def test_stored_ds_permutation_and_immediates():
