@@ -501,28 +501,36 @@ def projection_bytes(B, L, H, M):
 
 def bench_projection(w, steps, warmup):
     """The forget-gate projection at the workload's model width M = H d: logits
-    from x [B, L, M] bf16, then dx, dw_f and db_f."""
+    from x [B, L, M] bf16, then dx, dw_f and db_f; each direction captured in a HIP
+    graph (ten launches) and replayed, for the kernels' own time."""
     dev = torch.device("cuda:0")
     B, H, L, M = w.B, w.H, w.L, w.H * w.d
     p = inputs.projection_inputs(B, L, H, M, "bf16", PROJ_SEED, device=dev)
     logit = torch.empty((B, H, L), device=dev)
     ws = torch.empty(fox.fox_gate_projection_bwd_workspace_bytes(torch.bfloat16, B, L, H, M),
                      device=dev, dtype=torch.uint8)
-    tf, tb = EventTimer(), EventTimer()
+    dx = torch.empty_like(p["x"])
+    dw, db = torch.empty((H, M), device=dev), torch.empty((H,), device=dev)
+    # each direction lasts some tens of microseconds, so that launches from Python
+    # would show in an event bracket: ten launches per HIP graph, replayed
+    per_graph = 10
 
-    def once(timed):
-        with tf.maybe(timed):
+    def fwd():
+        for _ in range(per_graph):
             fox.fox_gate_projection(p["x"], p["w_f"], p["b_f"], logit)
-        with tb.maybe(timed):
-            fox.fox_gate_projection_bwd(p["x"], p["w_f"], p["d_logit"], workspace=ws)
 
-    for _ in range(warmup):
-        once(False)
-    torch.cuda.synchronize()
-    for _ in range(steps):
-        once(True)
-    torch.cuda.synchronize()
-    return {"B": B, "L": L, "H": H, "M": M, "fwd_ms": tf.mean_ms(), "bwd_ms": tb.mean_ms()}
+    def bwd():
+        for _ in range(per_graph):
+            fox.fox_gate_projection_bwd(p["x"], p["w_f"], p["d_logit"], workspace=ws, dx=dx,
+                                        dw=dw, db=db)
+
+    reps = max(2, steps // 2)
+    gf, gb = _capture(fwd), _capture(bwd)
+    res = {"B": B, "L": L, "H": H, "M": M, "fwd_ms": _graph_ms(gf, reps, warmup) / per_graph,
+           "bwd_ms": _graph_ms(gb, reps, warmup) / per_graph}
+    if not (torch.isfinite(logit).all() and torch.isfinite(dw).all()):
+        raise RuntimeError("non-finite gate projection outputs")
+    return res
 
 
 def bench_decode(w, steps, warmup, cpu=False):
