@@ -331,37 +331,47 @@ def bench_train_graph(w, steps, warmup):
 
 
 def train_graph_summary(w, r):
-    """JSON object of a graph-timed training leg: both backwards, per-stage times
-    and the MFMA roofline of the dominant kernel (dK/dV with the dS store)."""
+    """JSON object of a graph-timed training leg.  Both backwards are timed; the
+    leg's step is the faster of the two (named in "backward"; at this short
+    length the dS store saves less than it costs), the other one is reported
+    beside it, with per-stage times and the MFMA roofline of the step's dK/dV
+    kernel."""
     B, H, L, d = w.B, w.H, w.L, w.d
     fl_f, fl_b = fwd_flops(B, H, L, d), bwd_flops(B, H, L, d)
     fl_kv = 8.0 * d * causal_pairs(B, H, L)
-    tf = (fl_f + fl_b) / (r["stored_ms"] * 1e-3) / 1e12
-    tf_rc = (fl_f + fl_b) / (r["recompute_ms"] * 1e-3) / 1e12
-    kv = fl_kv / (r["dkdv_store"] * 1e-3) / 1e12
-    kv_rc = fl_kv / (r["dkdv"] * 1e-3) / 1e12
+    tf = {k: (fl_f + fl_b) / (r[k + "_ms"] * 1e-3) / 1e12 for k in ("stored", "recompute")}
+    kv = {"stored": fl_kv / (r["dkdv_store"] * 1e-3) / 1e12,
+          "recompute": fl_kv / (r["dkdv"] * 1e-3) / 1e12}
     fw = fl_f / (r["fwd"] * 1e-3) / 1e12
+    main = "stored" if r["stored_ms"] <= r["recompute_ms"] else "recompute"
+    other = "recompute" if main == "stored" else "stored"
+    what = {"stored": "keeping dS (fox_attn_bwd_stored stages, %.2f GB workspace)"
+                      % (r["store_bytes"] / 1e9),
+            "recompute": "recomputing S and dP in the dQ pass (fox_attn_bwd stages, O(L) "
+                         "workspace)"}
+    kernel = {"stored": (f"bwd_dkdv_bf16_kernel<{d},false,false,true>", "fox_attn_bwd_dkdv_store"),
+              "recompute": (f"bwd_dkdv_bf16_kernel<{d},false,false,false>", "fox_attn_bwd_dkdv")}
     return {
         "what": "training step (gate prefix -> forward -> backward -> d(logit)) at the 125M-model "
                 "head shape; each step captured in a HIP graph and replayed back to back; each "
                 "stage also captured alone, ten launches per graph, for its own time",
         "config": {"B": B, "H": H, "L": L, "d": d, "seed": w.seed, "flops_per_step": fl_f + fl_b},
-        "ms_per_step": round(r["stored_ms"], 4), "TFLOP/s": round(tf, 2),
-        "frac_of_peak": round(tf / MFMA_BF16_PEAK_TFLOPS, 4),
-        "backward": "keeping dS (fox_attn_bwd_stored stages, %.2f GB workspace)"
-                    % (r["store_bytes"] / 1e9),
-        "recompute": {"ms_per_step": round(r["recompute_ms"], 4), "TFLOP/s": round(tf_rc, 2),
-                      "frac_of_peak": round(tf_rc / MFMA_BF16_PEAK_TFLOPS, 4),
-                      "dkdv_TFLOP/s": round(kv_rc, 2)},
+        "ms_per_step": round(r[main + "_ms"], 4), "TFLOP/s": round(tf[main], 2),
+        "frac_of_peak": round(tf[main] / MFMA_BF16_PEAK_TFLOPS, 4),
+        "backward": what[main] + "; the faster of the two backwards at this shape",
+        other: {"backward": what[other], "ms_per_step": round(r[other + "_ms"], 4),
+                "TFLOP/s": round(tf[other], 2),
+                "frac_of_peak": round(tf[other] / MFMA_BF16_PEAK_TFLOPS, 4),
+                "dkdv_TFLOP/s": round(kv[other], 2)},
         "breakdown_ms": {n: round(r[n], 5) for n in ("gate_prefix", "fwd", "delta", "dkdv_store",
                                                      "dq_stored", "dkdv", "dq", "scan")},
-        "roofline": {"bound": "mfma", "kernel": "bwd_dkdv_bf16_kernel<64,false,false,true> "
-                     "(fox_attn_bwd_dkdv_store)", "achieved": round(kv, 2),
+        "roofline": {"bound": "mfma", "kernel": "%s (%s)" % kernel[main],
+                     "achieved": round(kv[main], 2),
                      "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(kv / MFMA_BF16_PEAK_TFLOPS, 4),
-                     "traffic": measured_traffic(f"bwd_dkdv_bf16_kernel<{d},false,false,true>"),
+                     "frac": round(kv[main] / MFMA_BF16_PEAK_TFLOPS, 4),
+                     "traffic": measured_traffic(kernel[main][0]),
                      "algorithmic_flops_per_launch": fl_kv},
-        "roofline_fwd": {"bound": "mfma", "kernel": "fwd_bf16_kernel<64> (fox_attn_fwd)",
+        "roofline_fwd": {"bound": "mfma", "kernel": f"fwd_bf16_kernel<{d}> (fox_attn_fwd)",
                          "achieved": round(fw, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
                          "unit": "TFLOP/s", "frac": round(fw / MFMA_BF16_PEAK_TFLOPS, 4)},
     }
