@@ -869,13 +869,16 @@ def trace_summary(db, command):
     grid), calls, mean / min / max duration and LDS bytes."""
     import sqlite3
     con = sqlite3.connect(db)
-    rows = con.execute("select name, grid_x, workgroup_x, duration, lds_size from kernels")
+    rows = con.execute("select name, grid_x, grid_y, grid_z, workgroup_x, workgroup_y, "
+                       "workgroup_z, duration, lds_size from kernels")
     groups = {}
-    for name, gx, wx, dur, lds in rows:
+    for name, gx, gy, gz, wx, wy, wz, dur, lds in rows:
         key = _kernel_key(name)
         if key in (None, "copy"):
             continue
-        g = groups.setdefault((key, gx // max(wx, 1), wx), {"d": [], "lds": lds})
+        # the grid is given in work-items per dimension
+        wgs = (gx // max(wx, 1)) * (gy // max(wy, 1)) * (gz // max(wz, 1))
+        g = groups.setdefault((key, wgs, wx * wy * wz), {"d": [], "lds": lds})
         g["d"].append(dur / 1e3)
     lines = ["# Kernel trace of bench.py: every library kernel, per launch grid",
              "", f"Command: `{command}`", "",
