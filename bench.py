@@ -715,7 +715,7 @@ def _counter_rows(d):
 def _kernel_family(name):
     """fox::<family><...> (demangled or Itanium-mangled), or "copy" for the
     runtime's device-to-device copy kernel; None for anything else."""
-    m = re.search(r"fox::(\w+)<", name)
+    m = re.search(r"fox::(\w+)[<(]", name)
     if m:
         return m.group(1)
     m = re.match(r"_ZN3fox(\d+)", name)

@@ -95,14 +95,18 @@ def _free_memory():
 
 
 # --------------------------------------------------------------------- prelude
-@pytest.mark.parametrize("L", [1, 2, 3, 17, 2047, 2048, 2049, 65536])
+# aligned rows of one segment (2048), of several (16384, 65536: log sigmoid
+# over all rows first, then the scan in place), and unaligned rows (odd L, 16387)
+@pytest.mark.parametrize("L", [1, 2, 3, 17, 2047, 2048, 2049, 16384, 16387, 65536])
 def test_gate_prefix(L):
     print(f"gate_prefix L={L}", flush=True)
     g = torch.Generator(device=DEV).manual_seed(L)
     x = torch.randn(3, 2, L, generator=g, device=DEV) * 2.0 + torch.tensor(
         [-2.0, 1.0, 6.0], device=DEV)[:, None, None]
     c, lf = fox.fox_gate_prefix(x, want_log_f=True)
+    c_only = fox.fox_gate_prefix(x)  # without the log f output: the same c
     torch.cuda.synchronize()
+    assert torch.equal(c, c_only)
     lf_ref, c_ref = oracle.gate_prefix(x.cpu())
     assert max_abs(lf, lf_ref) <= 2e-6
     tol = 4 * 2.0 ** -23 * float(c_ref.abs().max()) * max(1.0, math.log2(L)) + 1e-5
