@@ -37,26 +37,43 @@ namespace fox {
 size_t bwd_workspace_bytes(int BH, int L) { return (size_t)3 * BH * (size_t)L * sizeof(float); }
 
 // ---------------------------------------------------------------------------
-// Delta_i = sum_d dO_id * O_id
+// Delta_i = sum_d dO_id * O_id.  LPR lanes share a row, one 16-byte piece of O
+// and of dO each; a lane group takes kDeltaRows rows (one workgroup pass apart)
+// and issues all of their loads before it reduces any (rows past the end load
+// the last row and store nothing).  Each row's sum has the same order for any
+// kDeltaRows.
 // ---------------------------------------------------------------------------
+constexpr int kDeltaRows = 4;
 template <typename T, int D>
 __global__ __launch_bounds__(256) void bwd_delta_kernel(const T* __restrict__ O,
                                                         const T* __restrict__ dO,
                                                         float* __restrict__ delta, size_t rows) {
   constexpr int VEC = 16 / sizeof(T);
-  constexpr int LPR = D / VEC;  // lanes per row
-  const size_t row = ((size_t)blockIdx.x * 256 + threadIdx.x) / LPR;
+  constexpr int LPR = D / VEC;     // lanes per row
+  constexpr int RPP = 256 / LPR;   // rows per workgroup pass
+  typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
   const int part = threadIdx.x % LPR;
-  float acc = 0.0f;
-  if (row < rows) {
-    const T* o = O + row * D + part * VEC;
-    const T* g = dO + row * D + part * VEC;
+  const size_t row0 = (size_t)blockIdx.x * (RPP * kDeltaRows) + threadIdx.x / LPR;
+  u32x4_t ov[kDeltaRows], gv[kDeltaRows];
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) acc += (float)o[e] * (float)g[e];
+  for (int r = 0; r < kDeltaRows; ++r) {
+    const size_t row = min(row0 + (size_t)r * RPP, rows - 1);
+    ov[r] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(O + row * D + part * VEC));
+    gv[r] = *reinterpret_cast<const u32x4_t*>(dO + row * D + part * VEC);
   }
 #pragma unroll
-  for (int off = 1; off < LPR; off <<= 1) acc += __shfl_xor(acc, off);
-  if (row < rows && part == 0) delta[row] = acc;
+  for (int r = 0; r < kDeltaRows; ++r) {
+    const size_t row = row0 + (size_t)r * RPP;
+    T o[VEC], g[VEC];
+    __builtin_memcpy(o, &ov[r], 16);
+    __builtin_memcpy(g, &gv[r], 16);
+    float acc = 0.0f;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) acc += (float)o[e] * (float)g[e];
+#pragma unroll
+    for (int off = 1; off < LPR; off <<= 1) acc += __shfl_xor(acc, off);
+    if (row < rows && part == 0) delta[row] = acc;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1094,8 +1111,8 @@ static hipError_t launch_delta(const T* o, const T* g, float* delta, int BH, int
                                hipStream_t s) {
   const size_t rows = (size_t)BH * (size_t)L;
   const int lpr = d / (16 / (int)sizeof(T));
-  const size_t threads = rows * (size_t)lpr;
-  const dim3 grid((unsigned)((threads + 255) / 256));
+  const size_t per_block = (size_t)(256 / lpr) * kDeltaRows;
+  const dim3 grid((unsigned)((rows + per_block - 1) / per_block));
   if (d == 128) {
     hipLaunchKernelGGL((bwd_delta_kernel<T, 128>), grid, dim3(256), 0, s, o, g, delta, rows);
   } else {
