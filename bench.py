@@ -53,8 +53,7 @@ KERNEL_SOURCES = {
     "out_gate_kernel": ("pro_fusions.hip", "fox_device.h"),
     "out_gate_bwd_kernel": ("pro_fusions.hip", "fox_device.h"),
     "gate_proj_fwd_kernel": ("gate_proj.hip", "fox_device.h"),
-    "gate_proj_dw_kernel": ("gate_proj.hip", "fox_device.h"),
-    "gate_proj_dx_kernel": ("gate_proj.hip", "fox_device.h"),
+    "gate_proj_bwd_kernel": ("gate_proj.hip", "fox_device.h"),
     "gate_proj_reduce_kernel": ("gate_proj.hip", "fox_device.h"),
 }
 
@@ -809,10 +808,10 @@ KV_KERNEL = "bwd_dkdv_bf16_kernel<128,false,false,false>"
 DQ_STORED_KERNEL = "bwd_dq_stored_kernel<128,false>"
 DECODE_KERNEL = "decode_split_kernel<__bf16,128,false,false>"
 PROJ_FWD_KERNEL = "gate_proj_fwd_kernel<true,1>"
-PROJ_DW_KERNEL = "gate_proj_dw_kernel<true,1>"
-PROJ_DX_KERNEL = "gate_proj_dx_kernel<true,1>"
+PROJ_BWD_KERNEL = "gate_proj_bwd_kernel<true,1>"
+PROJ_REDUCE_KERNEL = "gate_proj_reduce_kernel"
 ROOFLINE_KERNELS = (KV_STORE_KERNEL, KV_KERNEL, DQ_STORED_KERNEL, DECODE_KERNEL, PROJ_FWD_KERNEL,
-                    PROJ_DW_KERNEL, PROJ_DX_KERNEL)
+                    PROJ_BWD_KERNEL, PROJ_REDUCE_KERNEL)
 
 SQ_KERNELS = tuple(k for dd in (128, 64) for k in (
     f"fwd_bf16_kernel<{dd},false,false,false>", f"bwd_dkdv_bf16_kernel<{dd},false,false,false>",
@@ -1129,11 +1128,11 @@ def main():
         rj = bench_projection(w, max(args.steps, 20), args.warmup)
         fb, bb = projection_bytes(rj["B"], rj["L"], rj["H"], rj["M"])
         legs = {}
-        tdw, tdx = measured_traffic(PROJ_DW_KERNEL), measured_traffic(PROJ_DX_KERNEL)
+        tb, tr = measured_traffic(PROJ_BWD_KERNEL), measured_traffic(PROJ_REDUCE_KERNEL)
         for leg, ms, byt, traffic, what in (
                 ("fwd", rj["fwd_ms"], fb, measured_traffic(PROJ_FWD_KERNEL), "gate_proj_fwd_kernel"),
-                ("bwd", rj["bwd_ms"], bb, None if tdw is None or tdx is None else tdw + tdx,
-                 "gate_proj_dx_kernel + gate_proj_dw_kernel + gate_proj_reduce_kernel")):
+                ("bwd", rj["bwd_ms"], bb, None if tb is None or tr is None else tb + tr,
+                 "gate_proj_bwd_kernel + gate_proj_reduce_kernel")):
             gbs = byt / (ms * 1e-3) / 1e9
             legs[leg] = {"ms": round(ms, 5), "bytes": byt,
                          "roofline": {"bound": "hbm", "kernel": what, "achieved": round(gbs, 1),

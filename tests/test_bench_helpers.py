@@ -49,9 +49,9 @@ def test_trace_summary_counts_every_grid_dimension(tmp_path):
     con = sqlite3.connect(db)
     con.execute("create table kernels (name text, grid_x int, grid_y int, grid_z int, "
                 "workgroup_x int, workgroup_y int, workgroup_z int, duration int, lds_size int)")
-    rows = [("void fox::gate_proj_dx_kernel<true, 1>(float const*)", 4096, 256, 1, 256, 1, 1,
+    rows = [("void fox::gate_proj_bwd_kernel<true, 1>(float const*)", 4096, 256, 1, 256, 1, 1,
              27000, 37888),
-            ("void fox::gate_proj_dx_kernel<true, 1>(float const*)", 4096, 256, 1, 256, 1, 1,
+            ("void fox::gate_proj_bwd_kernel<true, 1>(float const*)", 4096, 256, 1, 256, 1, 1,
              29000, 37888),
             ("fox::gate_proj_reduce_kernel(float const*)", 262400, 1, 1, 256, 1, 1, 3000, 0),
             ("__amd_rocclr_copyBuffer", 1024, 1, 1, 256, 1, 1, 5000, 0)]
@@ -59,7 +59,7 @@ def test_trace_summary_counts_every_grid_dimension(tmp_path):
     con.commit()
     con.close()
     text = bench.trace_summary(str(db), "cmd")
-    assert "| gate_proj_dx_kernel<true,1> | 4096 | 256 | 2 | 28.0 | 27.0 | 29.0 | 37888 |" in text
+    assert "| gate_proj_bwd_kernel<true,1> | 4096 | 256 | 2 | 28.0 | 27.0 | 29.0 | 37888 |" in text
     assert "| gate_proj_reduce_kernel | 1025 | 256 | 1 | 3.0 | 3.0 | 3.0 | 0 |" in text
     assert "copy" not in text.split("|---|")[-1]
 
