@@ -5,7 +5,8 @@ that their swizzled LDS tiles are read without bank conflicts, that each DMA
 load fills every tile position exactly once, and, for the backward keeping dS
 (the dQ half of Alg. 2 reading the dS its dK/dV half stored), that every store
 lands inside its slot run once and every read names a chunk that was written,
-also when gate-aware skipping cuts the stored tiles of each key block.
+also when gate-aware skipping cuts the stored tiles of each key block.  The
+scans' 16-byte accesses and the Delta kernel's row mapping are modelled too.
 
 Each model restates the kernel's formula in Python.  The constants are read
 from the kernel sources, and the formulas the models restate are matched
@@ -358,3 +359,74 @@ def test_stored_ds_permutation_and_immediates():
                 for k2 in range(2):
                     imm = (S // 2) * 4 * CHUNK_LDS + (S % 2) * 256 + k2 * 128
                     assert _ds_read_addr(lane, qb, S, k2, CHUNK_LDS, True) == base + imm
+
+
+# ------------------------------------------------------------------ scans, Delta
+SCAN = _src("gate_scan.hip")
+
+
+def test_scan_model_matches_the_kernel_source():
+    assert _const(SCAN, "kScanThreads") == "1024" and _const(SCAN, "kScanPerThread") == "8"
+    assert "constexpr bool FWD = MODE == 0 || MODE == 3;" in SCAN
+    assert "auto pos = [&](int p) { return (size_t)(FWD ? p : L - 1 - p); };" in SCAN
+    assert "const int p0 = seg + threadIdx.x * kScanPerThread;" in SCAN
+    assert "const bool whole = VEC && p0 + kScanPerThread <= L;" in SCAN
+    assert ("const size_t i0 = base + (FWD ? (size_t)p0 : (size_t)(L - kScanPerThread - p0));"
+            in SCAN)
+    assert "auto at = [&](int e) { return FWD ? e : kScanPerThread - 1 - e; };" in SCAN
+    assert "if (aligned && L > kScanSegment) {" in SCAN
+    assert "if (L % 4) return false;" in SCAN
+
+
+@pytest.mark.parametrize("fwd", [True, False])
+@pytest.mark.parametrize("L", [4, 8, 12, 2044, 2048, 8188, 8192, 8196, 16384, 24580])
+def test_scan_vector_accesses_cover_each_row_once(fwd, L):
+    """Rows with L % 4 == 0: every thread whose eight elements lie inside the
+    row moves them as two aligned 16-byte accesses at i0 and i0 + 4, element e
+    (scan order) sitting at i0 + at(e), the same position the scalar path uses;
+    the rest use the scalar path.  Together they touch every position of the
+    row exactly once, and nothing outside it."""
+    threads, per = 1024, 8
+    seen = [0] * L
+    for seg in range(0, L, threads * per):
+        for t in range(threads):
+            p0 = seg + t * per
+            whole = p0 + per <= L
+            i0 = p0 if fwd else L - per - p0
+            for e in range(per):
+                p = p0 + e
+                pos = p if fwd else L - 1 - p
+                if whole:
+                    at = e if fwd else per - 1 - e
+                    assert i0 % 4 == 0 and 0 <= i0 and i0 + per <= L
+                    assert i0 + at == pos
+                    seen[i0 + at] += 1
+                elif p < L:
+                    seen[pos] += 1
+    assert all(n == 1 for n in seen)
+
+
+def test_delta_rows_model():
+    """Delta kernel: LPR lanes share a row and a lane group takes kDeltaRows rows
+    one workgroup pass apart; every row of every grid is reduced by exactly one
+    lane group, and the clamped loads stay inside the tensor."""
+    assert _const(BWD, "kDeltaRows") == "4"
+    assert ("const size_t row0 = (size_t)blockIdx.x * (RPP * kDeltaRows) + threadIdx.x / LPR;"
+            in BWD)
+    assert "const size_t row = min(row0 + (size_t)r * RPP, rows - 1);" in BWD
+    assert "const size_t per_block = (size_t)(256 / lpr) * kDeltaRows;" in BWD
+    for lpr in (8, 16, 32):          # bf16 d = 64, 128; fp32 d = 128
+        rpp = 256 // lpr
+        for rows in (1, 5, rpp * 4 - 1, rpp * 4, rpp * 4 + 1, 1000, 4099):
+            per_block = rpp * 4
+            blocks = (rows + per_block - 1) // per_block
+            done = [0] * rows
+            for b in range(blocks):
+                for sub in range(rpp):
+                    row0 = b * per_block + sub
+                    for r in range(4):
+                        row = row0 + r * rpp
+                        assert min(row, rows - 1) < rows
+                        if row < rows:
+                            done[row] += 1
+            assert all(n == 1 for n in done)
