@@ -430,3 +430,29 @@ def test_delta_rows_model():
                         if row < rows:
                             done[row] += 1
             assert all(n == 1 for n in done)
+
+
+def test_projection_backward_block_mapping():
+    """gate_proj_bwd_kernel: the first n_dw workgroups are the dw_f blocks, the
+    rest the dx blocks; each kind's block k covers (column block k % mblocks,
+    token block k / mblocks) once."""
+    proj = _src("gate_proj.hip")
+    assert "const bool is_dx = i >= n_dw;  // the dw_f blocks first" in proj
+    assert "const int k = is_dx ? i - n_dw : i;" in proj
+    assert ("if (is_dx) proj_dx_body<BF16, HB>(sm.dx, k % mblocks, k / mblocks, w, g, dx, N, L, H, M);"
+            in proj)
+    assert "const dim3 grid((unsigned)(n_dx + n_dw));" in proj
+    for mblocks, n_tok_dx, chunks, with_dx in ((16, 256, 64, True), (6, 128, 171, True),
+                                               (1, 1, 1, True), (16, 256, 64, False)):
+        n_dx = mblocks * n_tok_dx if with_dx else 0
+        n_dw = mblocks * chunks
+        seen = {True: set(), False: set()}
+        for i in range(n_dx + n_dw):
+            is_dx = i >= n_dw
+            k = i - n_dw if is_dx else i
+            cell = (k % mblocks, k // mblocks)
+            assert cell not in seen[is_dx]
+            seen[is_dx].add(cell)
+        assert seen[True] == {(m, t) for m in range(mblocks) for t in range(n_tok_dx)} if with_dx \
+            else not seen[True]
+        assert seen[False] == {(m, c) for m in range(mblocks) for c in range(chunks)}
